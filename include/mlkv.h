@@ -1,0 +1,120 @@
+/*
+ * mlkv.h - batched embedding-table get / put_grad on one AMD MI355X (gfx950).
+ *
+ * The calls follow the key-value interface of MLKV (He et al., "MLKV:
+ * Efficiently Scaling up Large Embedding Model Training with Disk-based
+ * Key-Value Storage", arXiv 2504.01506):
+ *   Open(model_id, dim, staleness_bound)  Sec. III-A (Interfaces Summary)
+ *   Get(keys) -> values                   Sec. III-A; workflow step 2, Sec. III-B
+ *   Rmw at workflow step 8                Sec. III-B (Workflows); here the
+ *                                         modify function is "sum the gradients
+ *                                         of duplicate keys, then one row-wise
+ *                                         Adagrad step"
+ * Tables live entirely in HBM. Staleness bound is 0 (bulk-synchronous, Sec.
+ * III-C1): calls on one table must be ordered on one HIP stream.
+ *
+ * Conventions for every call below
+ *   - Pointers named d_* are DEVICE pointers (HBM), owned by the caller, that
+ *     must stay valid until the stream work of the call has finished. The
+ *     library never keeps them after the call's kernels complete.
+ *   - `hip_stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *   - Return codes cover host-side validation and launch failures only; calls
+ *     are asynchronous. Conditions found on the device (capacity exceeded,
+ *     a reserved key in the input) make the whole call a no-op on the table
+ *     and are reported by the next mlkv_sync().
+ *   - A failed call leaves the table unchanged; outputs are then unspecified.
+ *   - mlkv_last_error() returns a thread-local message for the last failure.
+ */
+#ifndef MLKV_H
+#define MLKV_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct mlkv_table mlkv_table;
+
+enum {
+  MLKV_OK = 0,
+  MLKV_EINVAL = -1,  /* bad argument, or a reserved key (all ones) in the input */
+  MLKV_EFULL = -2,   /* the call would grow the table beyond its capacity */
+  MLKV_ENOMEM = -3,  /* device allocation failed */
+  MLKV_EDEVICE = -4  /* HIP runtime or launch error */
+};
+
+#define MLKV_DEFAULT_SEED 0x4D4C4B56ull /* seed of the initial rows for mlkv_open */
+#define MLKV_RESERVED_KEY 0xFFFFFFFFFFFFFFFFull
+
+/* Creates a table of `dim`-wide fp32 rows with room for `capacity` keys
+ * (Open, Sec. III-A; model_id and staleness_bound are not needed: one table,
+ * bound 0). Limits: 1 <= dim <= 1024, 1 <= capacity <= 2^32 - 2. The table
+ * owns all of its device memory (hash index, rows, optimizer state,
+ * scratch), allocated on the current HIP device. Returns NULL on failure
+ * (see mlkv_last_error). Uses seed MLKV_DEFAULT_SEED and max load 0.75. */
+mlkv_table *mlkv_open(int32_t dim, int64_t capacity);
+
+/* As mlkv_open with an explicit initial-row seed and the largest fraction of
+ * hash-index slots that may hold keys (0 < max_load <= 0.9). */
+mlkv_table *mlkv_open_ex(int32_t dim, int64_t capacity, uint64_t seed, float max_load);
+
+/* Get (Sec. III-A): d_out[i*dim + c] = row(d_keys[i])[c] for i < n, where a key
+ * that is not yet in the table is first inserted. Within one call, the
+ * distinct new keys take the rows size, size+1, ... in ascending key order,
+ * and element c of a new key's row is
+ *     t = (int32)(h >> 40) - 2^23,  h = mix64(mix64(key ^ seed) + c * 0x9E3779B97F4A7C15)
+ *     value = (float)t * (0.01f * 2^-23)          (uniform on [-0.01, 0.01))
+ * with mix64 the SplitMix64 output function. d_out may be NULL (insert only).
+ * n may be 0. d_keys: n uint64 keys. d_out: n*dim floats, row-major. */
+int mlkv_get(mlkv_table *t, const uint64_t *d_keys, int64_t n, float *d_out, void *hip_stream);
+
+/* Rmw (Sec. III-B, step 8) with row-wise Adagrad as the modify function:
+ * missing keys are inserted as in mlkv_get; then for every distinct key k of
+ * the batch, with positions i_1 < i_2 < ... holding k,
+ *     g[c]  = fp32( sum_j fp64(d_grads[i_j*dim + c]) )
+ *     m     = fp32( sum_c fp64(g[c])^2 / dim )
+ *     G'    = G + m;   den = sqrtf(G') + eps
+ *     w[c] -= lr * (g[c] / den)     (separate fp32 operations)
+ *     G     = G'
+ * G starts at 0 for every row. d_grads: n*dim floats, row-major.
+ * lr and eps must be finite, eps >= 0. */
+int mlkv_put_grad(mlkv_table *t, const uint64_t *d_keys, const float *d_grads, int64_t n,
+                  float lr, float eps, void *hip_stream);
+
+/* Waits for all work on `hip_stream`, then returns and clears the first error
+ * latched on the device since the previous mlkv_sync (MLKV_EFULL or
+ * MLKV_EINVAL), or MLKV_OK. */
+int mlkv_sync(mlkv_table *t, void *hip_stream);
+
+/* Number of rows in use (synchronizes the device). -1 on error. */
+int64_t mlkv_size(mlkv_table *t);
+
+/* Number of hash-index slots (8 per bucket). */
+int64_t mlkv_num_slots(mlkv_table *t);
+
+/* Releases the table and all of its device memory (synchronizes the device). */
+void mlkv_close(mlkv_table *t);
+
+/* Thread-local text of the last error reported by this library. */
+const char *mlkv_last_error(void);
+
+/* ---- inspection (tests and debugging; asynchronous on hip_stream) ---- */
+
+/* d_rows_out[i] = row of d_keys[i] or -1 if absent; never inserts. */
+int mlkv_lookup_rows(mlkv_table *t, const uint64_t *d_keys, int64_t n, int64_t *d_rows_out,
+                     void *hip_stream);
+
+/* Copies table contents into caller buffers (any may be NULL):
+ * d_rows_out [nrows*dim] rows 0..nrows-1, d_state_out [nrows] their Adagrad
+ * accumulators, d_slot_keys_out [num_slots] / d_slot_rows_out [num_slots] the
+ * raw index slots (empty slots hold MLKV_RESERVED_KEY / 0xFFFFFFFF).
+ * nrows must be <= the current size. */
+int mlkv_export(mlkv_table *t, int64_t nrows, float *d_rows_out, float *d_state_out,
+                uint64_t *d_slot_keys_out, uint32_t *d_slot_rows_out, void *hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MLKV_H */

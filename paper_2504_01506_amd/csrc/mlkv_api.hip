@@ -1,0 +1,333 @@
+// C ABI of libmlkv: table manager (device allocation, index sizing, per-call
+// scratch, error latch) and the launch sequence of each call.
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+
+#include "mlkv.h"
+#include "mlkv_kernels.h"
+
+using namespace mlkv;
+
+struct mlkv_table {
+  int device = 0;
+  int32_t dim = 0;
+  int64_t capacity = 0;
+  uint64_t seed = 0;
+  float max_load = 0.75f;
+  uint32_t nb_log2 = 0;
+  uint64_t nb = 0;
+  Bucket* idx = nullptr;
+  float* rows = nullptr;
+  float* state = nullptr;
+  Ctrl* ctrl = nullptr;
+  // sequence number of calls that may change the table; starts at 1 because
+  // the control block's epoch markers start at 0 ("no call")
+  uint64_t epoch = 1;
+
+  // per-call scratch, grown on demand
+  int64_t ws_n = 0;
+  NewKey* newlist = nullptr;
+  uint32_t* tile_cnt = nullptr;
+  uint64_t* items = nullptr;
+  uint32_t* meta = nullptr;
+  uint64_t* spill = nullptr;
+  uint64_t spill_words = 0;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  g_err = std::string(what) + ": " + hipGetErrorString(e);
+  return e == hipErrorOutOfMemory ? MLKV_ENOMEM : MLKV_EDEVICE;
+}
+
+template <class T>
+hipError_t dev_alloc(T** p, size_t bytes) {
+  *p = nullptr;
+  if (bytes == 0) bytes = 256;
+  return hipMalloc(reinterpret_cast<void**>(p), bytes);
+}
+
+void free_workspace(mlkv_table* t) {
+  (void)hipFree(t->newlist);
+  (void)hipFree(t->tile_cnt);
+  (void)hipFree(t->items);
+  (void)hipFree(t->meta);
+  (void)hipFree(t->spill);
+  t->newlist = nullptr;
+  t->tile_cnt = nullptr;
+  t->items = nullptr;
+  t->meta = nullptr;
+  t->spill = nullptr;
+  t->ws_n = 0;
+  t->spill_words = 0;
+}
+
+// Scratch for calls of up to n keys: new-key lists, per-tile counts, the
+// partitioned (slot, pos) pairs, partition metadata and the spill area.
+int ensure_workspace(mlkv_table* t, int64_t n) {
+  if (n <= t->ws_n) return MLKV_OK;
+  int64_t want = std::max<int64_t>(n, std::max<int64_t>(65536, 2 * t->ws_n));
+  want = (want + kPutTile - 1) / kPutTile * kPutTile;
+  hipError_t e = hipDeviceSynchronize();  // old scratch may still be in use
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+  free_workspace(t);
+  const int64_t get_tiles = (want + kGetTile - 1) / kGetTile;
+  const int64_t put_tiles = want / kPutTile;
+  const uint64_t spill_words = 4ull * (uint64_t)want + 4096;
+  if ((e = dev_alloc(&t->newlist, sizeof(NewKey) * (size_t)want)) != hipSuccess ||
+      (e = dev_alloc(&t->tile_cnt, sizeof(uint32_t) * (size_t)get_tiles)) != hipSuccess ||
+      (e = dev_alloc(&t->items, sizeof(uint64_t) * (size_t)want)) != hipSuccess ||
+      (e = dev_alloc(&t->meta, sizeof(uint32_t) * (size_t)kMaxParts * (size_t)put_tiles)) != hipSuccess ||
+      (e = dev_alloc(&t->spill, sizeof(uint64_t) * (size_t)spill_words)) != hipSuccess) {
+    free_workspace(t);
+    return hip_fail(e, "scratch allocation");
+  }
+  t->ws_n = want;
+  t->spill_words = spill_words;
+  return MLKV_OK;
+}
+
+int check_table(mlkv_table* t) {
+  if (t == nullptr) return fail(MLKV_EINVAL, "table is NULL");
+  hipError_t e = hipSetDevice(t->device);
+  if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
+  return MLKV_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char* mlkv_last_error(void) { return g_err.c_str(); }
+
+mlkv_table* mlkv_open_ex(int32_t dim, int64_t capacity, uint64_t seed, float max_load) {
+  if (dim < 1 || dim > 1024) {
+    fail(MLKV_EINVAL, "dim must be in [1, 1024]");
+    return nullptr;
+  }
+  if (capacity < 1 || capacity > 0xFFFFFFFEll) {
+    fail(MLKV_EINVAL, "capacity must be in [1, 2^32 - 2]");
+    return nullptr;
+  }
+  if (!(max_load > 0.0f) || !(max_load <= 0.9f)) {
+    fail(MLKV_EINVAL, "max_load must be in (0, 0.9]");
+    return nullptr;
+  }
+  // buckets: a power of two with 8 * nb * max_load >= capacity
+  const double need = std::ceil((double)capacity / (8.0 * (double)max_load));
+  uint32_t lg = 0;
+  while ((double)(1ull << lg) < need) ++lg;
+  if (lg > 28) {
+    fail(MLKV_EINVAL, "hash index would exceed 2^31 slots; raise max_load or lower capacity");
+    return nullptr;
+  }
+  mlkv_table* t = new mlkv_table();
+  t->dim = dim;
+  t->capacity = capacity;
+  t->seed = seed;
+  t->max_load = max_load;
+  t->nb_log2 = lg;
+  t->nb = 1ull << lg;
+  hipError_t e = hipGetDevice(&t->device);
+  if (e != hipSuccess) {
+    hip_fail(e, "hipGetDevice");
+    delete t;
+    return nullptr;
+  }
+  if ((e = dev_alloc(&t->idx, sizeof(Bucket) * t->nb)) != hipSuccess ||
+      (e = dev_alloc(&t->rows, sizeof(float) * (size_t)capacity * (size_t)dim)) != hipSuccess ||
+      (e = dev_alloc(&t->state, sizeof(float) * (size_t)capacity)) != hipSuccess ||
+      (e = dev_alloc(&t->ctrl, sizeof(Ctrl))) != hipSuccess) {
+    hip_fail(e, "table allocation");
+    mlkv_close(t);
+    return nullptr;
+  }
+  // empty index: all key tags EMPTY (all ones) and all row ids pending (all ones)
+  Ctrl c;
+  std::memset(&c, 0, sizeof(c));
+  if ((e = hipMemset(t->idx, 0xFF, sizeof(Bucket) * t->nb)) != hipSuccess ||
+      (e = hipMemcpy(t->ctrl, &c, sizeof(Ctrl), hipMemcpyHostToDevice)) != hipSuccess ||
+      (e = hipDeviceSynchronize()) != hipSuccess) {
+    hip_fail(e, "table initialisation");
+    mlkv_close(t);
+    return nullptr;
+  }
+  return t;
+}
+
+mlkv_table* mlkv_open(int32_t dim, int64_t capacity) {
+  return mlkv_open_ex(dim, capacity, MLKV_DEFAULT_SEED, 0.75f);
+}
+
+void mlkv_close(mlkv_table* t) {
+  if (t == nullptr) return;
+  (void)hipSetDevice(t->device);
+  (void)hipDeviceSynchronize();
+  free_workspace(t);
+  (void)hipFree(t->idx);
+  (void)hipFree(t->rows);
+  (void)hipFree(t->state);
+  (void)hipFree(t->ctrl);
+  delete t;
+}
+
+int mlkv_get(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, void* hip_stream) {
+  int rc = check_table(t);
+  if (rc) return rc;
+  if (n < 0 || n > 0x7FFFFFFFll) return fail(MLKV_EINVAL, "n must be in [0, 2^31 - 1]");
+  if (n == 0) return MLKV_OK;
+  if (d_keys == nullptr) return fail(MLKV_EINVAL, "keys is NULL");
+  if ((rc = ensure_workspace(t, n)) != MLKV_OK) return rc;
+  GetArgs a;
+  a.idx = t->idx;
+  a.nb_log2 = t->nb_log2;
+  a.keys = d_keys;
+  a.n = n;
+  a.out = d_out;
+  a.rows = t->rows;
+  a.state = t->state;
+  a.D = t->dim;
+  a.seed = t->seed;
+  a.capacity = t->capacity;
+  a.newlist = t->newlist;
+  a.tile_cnt = t->tile_cnt;
+  a.ctrl = t->ctrl;
+  a.epoch = t->epoch;
+  const bool vec4 = (t->dim % 4 == 0) && (d_out == nullptr || aligned16(d_out));
+  hipError_t e = launch_get(a, vec4, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail(e, "mlkv_get launch");
+  t->epoch++;
+  return MLKV_OK;
+}
+
+int mlkv_put_grad(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, int64_t n, float lr,
+                  float eps, void* hip_stream) {
+  int rc = check_table(t);
+  if (rc) return rc;
+  if (n < 0 || n > 0x7FFFFFFFll) return fail(MLKV_EINVAL, "n must be in [0, 2^31 - 1]");
+  if (!std::isfinite(lr)) return fail(MLKV_EINVAL, "lr must be finite");
+  if (!std::isfinite(eps) || eps < 0.0f) return fail(MLKV_EINVAL, "eps must be finite and >= 0");
+  if (n == 0) return MLKV_OK;
+  if (d_keys == nullptr || d_grads == nullptr) return fail(MLKV_EINVAL, "keys or grads is NULL");
+  if ((rc = ensure_workspace(t, n)) != MLKV_OK) return rc;
+  // partitions: about 256 entries each, a power of two, at most kMaxParts
+  const uint32_t slot_bits = t->nb_log2 + 3;
+  uint32_t pb = 0;
+  while (pb < 12 && ((int64_t)256 << (pb + 1)) <= n + (n >> 1)) ++pb;
+  if (pb > slot_bits) pb = slot_bits;
+  PutArgs a;
+  a.idx = t->idx;
+  a.nb_log2 = t->nb_log2;
+  a.keys = d_keys;
+  a.grads = d_grads;
+  a.n = n;
+  a.rows = t->rows;
+  a.state = t->state;
+  a.D = t->dim;
+  a.seed = t->seed;
+  a.capacity = t->capacity;
+  a.lr = lr;
+  a.eps = eps;
+  a.shift = (int)(slot_bits - pb);
+  a.NP = 1 << pb;
+  a.items = t->items;
+  a.meta = t->meta;
+  a.newlist = t->newlist;
+  a.tile_cnt = t->tile_cnt;
+  a.spill = t->spill;
+  a.spill_words = t->spill_words;
+  a.ctrl = t->ctrl;
+  a.epoch = t->epoch;
+  const bool vec4 = (t->dim % 4 == 0) && aligned16(d_grads);
+  hipError_t e = launch_put(a, vec4, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail(e, "mlkv_put_grad launch");
+  t->epoch++;
+  return MLKV_OK;
+}
+
+int mlkv_sync(mlkv_table* t, void* hip_stream) {
+  int rc = check_table(t);
+  if (rc) return rc;
+  hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  int latched = 0;
+  e = hipMemcpy(&latched, &t->ctrl->latched, sizeof(int), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "read error latch");
+  if (latched != 0) {
+    const int zero = 0;
+    e = hipMemcpy(&t->ctrl->latched, &zero, sizeof(int), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "clear error latch");
+    return fail(latched, latched == MLKV_EFULL ? "a call exceeded the table capacity"
+                                               : "a call contained the reserved key");
+  }
+  return MLKV_OK;
+}
+
+int64_t mlkv_size(mlkv_table* t) {
+  if (check_table(t)) return -1;
+  hipError_t e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    hip_fail(e, "hipDeviceSynchronize");
+    return -1;
+  }
+  unsigned long long s = 0;
+  e = hipMemcpy(&s, &t->ctrl->size[t->epoch & 1], sizeof(s), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) {
+    hip_fail(e, "read size");
+    return -1;
+  }
+  return (int64_t)s;
+}
+
+int64_t mlkv_num_slots(mlkv_table* t) {
+  if (t == nullptr) return -1;
+  return (int64_t)(t->nb * kSlots);
+}
+
+int mlkv_lookup_rows(mlkv_table* t, const uint64_t* d_keys, int64_t n, int64_t* d_rows_out,
+                     void* hip_stream) {
+  int rc = check_table(t);
+  if (rc) return rc;
+  if (n < 0 || n > 0x7FFFFFFFll) return fail(MLKV_EINVAL, "n must be in [0, 2^31 - 1]");
+  if (n == 0) return MLKV_OK;
+  if (d_keys == nullptr || d_rows_out == nullptr) return fail(MLKV_EINVAL, "NULL pointer");
+  hipError_t e = launch_lookup(t->idx, t->nb_log2, d_keys, n, d_rows_out,
+                               static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail(e, "mlkv_lookup_rows launch");
+  return MLKV_OK;
+}
+
+int mlkv_export(mlkv_table* t, int64_t nrows, float* d_rows_out, float* d_state_out,
+                uint64_t* d_slot_keys_out, uint32_t* d_slot_rows_out, void* hip_stream) {
+  int rc = check_table(t);
+  if (rc) return rc;
+  const int64_t size = mlkv_size(t);
+  if (size < 0) return MLKV_EDEVICE;
+  if (nrows < 0 || nrows > size) return fail(MLKV_EINVAL, "nrows must be in [0, size]");
+  hipStream_t st = static_cast<hipStream_t>(hip_stream);
+  hipError_t e = hipSuccess;
+  if (d_rows_out && nrows > 0)
+    e = hipMemcpyAsync(d_rows_out, t->rows, sizeof(float) * (size_t)nrows * (size_t)t->dim,
+                       hipMemcpyDeviceToDevice, st);
+  if (e == hipSuccess && d_state_out && nrows > 0)
+    e = hipMemcpyAsync(d_state_out, t->state, sizeof(float) * (size_t)nrows, hipMemcpyDeviceToDevice, st);
+  if (e == hipSuccess && (d_slot_keys_out || d_slot_rows_out))
+    e = launch_export_slots(t->idx, t->nb * kSlots, d_slot_keys_out, d_slot_rows_out, st);
+  if (e != hipSuccess) return hip_fail(e, "mlkv_export");
+  return MLKV_OK;
+}
+
+}  // extern "C"

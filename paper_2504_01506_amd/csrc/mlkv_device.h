@@ -1,0 +1,238 @@
+// Device-side building blocks shared by the kernels of libmlkv (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mlkv {
+
+constexpr uint64_t kEmptyKey = ~0ull;
+constexpr uint32_t kPendingRow = 0xFFFFFFFFu;
+constexpr int kSlots = 8;          // slots per bucket
+constexpr int kMaxProbe = 4096;    // buckets visited before a call reports overflow
+
+// One bucket = one 128-byte line: 8 key tags, the 8 row ids, 8 spare words.
+struct __align__(128) Bucket {
+  uint64_t key[kSlots];
+  uint32_t row[kSlots];
+  uint32_t aux[kSlots];
+};
+static_assert(sizeof(Bucket) == 128, "bucket must be one 128-byte line");
+
+// A key first inserted by the current call, owned by the lane that won its slot.
+struct NewKey {
+  uint64_t key;
+  uint32_t slot;
+  uint32_t pad;
+};
+
+// Per-table control block in device memory.
+struct Ctrl {
+  unsigned long long size[2];         // rows in use, ping-pong on the call epoch
+  unsigned long long bad_epoch;       // epoch of a call that met the reserved key
+  unsigned long long overflow_epoch;  // epoch of a call whose inserts overran the probe bound
+  unsigned long long spill_next;      // bump allocator for partitions larger than LDS
+  int latched;                        // first device-side error since mlkv_sync
+  unsigned int pad[9];
+};
+
+// ---------------------------------------------------------------------------
+// Hashing
+// ---------------------------------------------------------------------------
+// Bucket choice: a 64-bit finaliser (MurmurHash3 fmix64) then the top bits.
+__device__ __forceinline__ uint64_t index_hash(uint64_t k) {
+  k ^= k >> 33;
+  k *= 0xff51afd7ed558ccdull;
+  k ^= k >> 33;
+  k *= 0xc4ceb9fe1a85ec53ull;
+  k ^= k >> 33;
+  return k;
+}
+
+// SplitMix64 output function (Steele, Lea & Flood 2014).
+__device__ __forceinline__ uint64_t splitmix_mix(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// Initial value of column c of a new key, given s0 = mix64(key ^ seed): the
+// top 24 bits of mix64(s0 + c * golden gamma), centred and scaled by
+// 0.01f * 2^-23, i.e. uniform on [-0.01, 0.01).
+__device__ __forceinline__ float init_elem(uint64_t s0, int c) {
+  const uint64_t h = splitmix_mix(s0 + (uint64_t)(uint32_t)c * 0x9E3779B97F4A7C15ull);
+  const int t = (int)(uint32_t)(h >> 40) - (1 << 23);
+  constexpr float kScale = 0.01f * 0x1p-23f;
+  return __fmul_rn((float)t, kScale);
+}
+
+// ---------------------------------------------------------------------------
+// Probe / insert, one key per lane.
+// ---------------------------------------------------------------------------
+enum ProbeStatus : int {
+  P_HIT = 0,        // key present from an earlier call; row valid
+  P_NEW_MINE = 1,   // this lane inserted the key (row pending)
+  P_NEW_OTHER = 2,  // another lane of this call inserted it (row pending)
+  P_ABSENT = 3,     // not present (lookup only)
+  P_OVERFLOW = 4,   // probe bound reached while inserting
+  P_BAD = 5,        // reserved key
+  P_NONE = 6        // lane has no key
+};
+
+struct Probe {
+  uint32_t slot;
+  uint32_t row;
+  int status;
+};
+
+// Linear probing over buckets. A bucket holding an EMPTY tag ends the chain.
+// Inserts claim the first EMPTY tag in chain order with a CAS; a failed CAS
+// returns the tag that is really there, so a stale view of the line never
+// produces a duplicate key (tags only ever go from EMPTY to a key in a call).
+__device__ __forceinline__ Probe probe_key(Bucket* __restrict__ idx, uint32_t nb_log2,
+                                           uint64_t key, bool insert) {
+  const uint64_t mask = (nb_log2 >= 64) ? ~0ull : ((1ull << nb_log2) - 1);
+  uint64_t b = nb_log2 ? (index_hash(key) >> (64 - nb_log2)) : 0;
+  const uint64_t limit = mask < (uint64_t)kMaxProbe ? mask + 1 : (uint64_t)kMaxProbe;
+  for (uint64_t p = 0; p < limit; ++p) {
+    Bucket* B = idx + b;
+    const ulonglong2* kp = reinterpret_cast<const ulonglong2*>(B->key);
+    uint64_t k[kSlots];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const ulonglong2 v = kp[q];
+      k[2 * q] = v.x;
+      k[2 * q + 1] = v.y;
+    }
+    int hit = -1;
+    bool has_empty = false;
+#pragma unroll
+    for (int j = kSlots - 1; j >= 0; --j) {
+      if (k[j] == key) hit = j;
+      has_empty |= (k[j] == kEmptyKey);
+    }
+    if (hit >= 0) {
+      const uint32_t r = B->row[hit];
+      return {(uint32_t)(b * kSlots + hit), r, r == kPendingRow ? P_NEW_OTHER : P_HIT};
+    }
+    if (has_empty) {
+      if (!insert) return {0, kPendingRow, P_ABSENT};
+      for (int j = 0; j < kSlots; ++j) {
+        if (k[j] != kEmptyKey) continue;
+        const uint64_t old = atomicCAS(reinterpret_cast<unsigned long long*>(&B->key[j]),
+                                       (unsigned long long)kEmptyKey, (unsigned long long)key);
+        if (old == kEmptyKey) return {(uint32_t)(b * kSlots + j), kPendingRow, P_NEW_MINE};
+        if (old == key) return {(uint32_t)(b * kSlots + j), kPendingRow, P_NEW_OTHER};
+      }
+      // every EMPTY tag seen was taken by other keys meanwhile: the chain goes on
+    }
+    b = (b + 1) & mask;
+  }
+  return {0, kPendingRow, insert ? P_OVERFLOW : P_ABSENT};
+}
+
+// ---------------------------------------------------------------------------
+// Block-wide helpers
+// ---------------------------------------------------------------------------
+// Exclusive scan over the block; NT threads, s_w needs NT/64 words.
+template <int NT>
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s_w, uint32_t* total) {
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) s_w[w] = x;
+  __syncthreads();
+  if (w == 0) {
+    uint32_t s = lane < NT / 64 ? s_w[lane] : 0u;
+#pragma unroll
+    for (int o = 1; o < NT / 64; o <<= 1) {
+      const uint32_t y = __shfl_up(s, o, 64);
+      if (lane >= o) s += y;
+    }
+    if (lane < NT / 64) s_w[lane] = s;
+  }
+  __syncthreads();
+  const uint32_t pre = (w > 0 ? s_w[w - 1] : 0u) + x - v;
+  *total = s_w[NT / 64 - 1];
+  __syncthreads();
+  return pre;
+}
+
+template <int NT>
+__device__ __forceinline__ uint64_t block_sum_u64(uint64_t v, unsigned long long* s_w) {
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor((unsigned long long)v, o, 64);
+  if (lane == 0) s_w[w] = v;
+  __syncthreads();
+  uint64_t t = 0;
+#pragma unroll
+  for (int j = 0; j < NT / 64; ++j) t += s_w[j];
+  __syncthreads();
+  return t;
+}
+
+// Bitonic sort of N (power of two) 64-bit words, ascending, by the whole block.
+template <int NT, class P>
+__device__ void block_bitonic_sort(P a, uint32_t N) {
+  for (uint32_t k = 2; k <= N; k <<= 1) {
+    for (uint32_t j = k >> 1; j > 0; j >>= 1) {
+      for (uint32_t i = threadIdx.x; i < N; i += NT) {
+        const uint32_t ixj = i ^ j;
+        if (ixj > i) {
+          const uint64_t x = a[i];
+          const uint64_t y = a[ixj];
+          const bool up = (i & k) == 0;
+          if ((x > y) == up) {
+            a[i] = y;
+            a[ixj] = x;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Lane <-> row-element mapping. A wave is split into RPW = 64/LPR lane groups;
+// a group of LPR lanes covers one row, VEC consecutive floats per lane per
+// chunk, K chunks: column of (chunk k, element v) = (k*LPR + q)*VEC + v.
+// ---------------------------------------------------------------------------
+template <int VEC_, int LPR_, int K_>
+struct RowMap {
+  static constexpr int VEC = VEC_;
+  static constexpr int LPR = LPR_;
+  static constexpr int K = K_;
+  static constexpr int RPW = 64 / LPR_;
+};
+
+template <int VEC>
+struct VecT;
+template <>
+struct VecT<1> {
+  using T = float;
+  static __device__ __forceinline__ float get(const T& x, int) { return x; }
+  static __device__ __forceinline__ void set(T& x, int, float v) { x = v; }
+};
+template <>
+struct VecT<4> {
+  using T = float4;
+  static __device__ __forceinline__ float get(const T& x, int v) {
+    return v == 0 ? x.x : v == 1 ? x.y : v == 2 ? x.z : x.w;
+  }
+  static __device__ __forceinline__ void set(T& x, int v, float f) {
+    if (v == 0) x.x = f;
+    else if (v == 1) x.y = f;
+    else if (v == 2) x.z = f;
+    else x.w = f;
+  }
+};
+
+}  // namespace mlkv

@@ -1,0 +1,68 @@
+// Launch interface between the host table manager and the HIP kernels.
+#pragma once
+
+#include <algorithm>
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "mlkv_device.h"
+
+namespace mlkv {
+
+constexpr int kGetTile = 256;    // keys per probe_gather block (one per lane)
+constexpr int kPutTile = 1024;   // keys per put_probe block (one per lane)
+constexpr int kMaxParts = 4096;  // partitions (MSD digits) per put call
+constexpr int kRedThreads = 512; // threads of a reduce_update block
+constexpr int kRedCap = 2048;    // partition entries held in LDS
+constexpr int kLongSeg = 32;     // segments longer than this are split over the block
+
+struct GetArgs {
+  Bucket* idx;
+  uint32_t nb_log2;
+  const uint64_t* keys;
+  int64_t n;
+  float* out;
+  float* rows;
+  float* state;
+  int D;
+  uint64_t seed;
+  int64_t capacity;
+  NewKey* newlist;
+  uint32_t* tile_cnt;
+  Ctrl* ctrl;
+  uint64_t epoch;
+};
+
+struct PutArgs {
+  Bucket* idx;
+  uint32_t nb_log2;
+  const uint64_t* keys;
+  const float* grads;
+  int64_t n;
+  float* rows;
+  float* state;
+  int D;
+  uint64_t seed;
+  int64_t capacity;
+  float lr;
+  float eps;
+  int shift;  // slot >> shift = partition
+  int NP;     // number of partitions
+  uint64_t* items;
+  uint32_t* meta;
+  NewKey* newlist;
+  uint32_t* tile_cnt;
+  uint64_t* spill;
+  uint64_t spill_words;
+  Ctrl* ctrl;
+  uint64_t epoch;
+};
+
+hipError_t launch_get(const GetArgs& a, bool vec4, hipStream_t st);
+hipError_t launch_put(const PutArgs& a, bool vec4, hipStream_t st);
+hipError_t launch_lookup(Bucket* idx, uint32_t nb_log2, const uint64_t* keys, int64_t n,
+                         int64_t* rows_out, hipStream_t st);
+hipError_t launch_export_slots(const Bucket* idx, uint64_t nslots, uint64_t* keys_out,
+                               uint32_t* rows_out, hipStream_t st);
+
+}  // namespace mlkv

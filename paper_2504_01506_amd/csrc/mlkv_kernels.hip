@@ -1,0 +1,802 @@
+// HIP kernels of libmlkv for gfx950 (MI355X): hash-index probe, row gather,
+// in-batch dedup by MSD radix partition + LDS sort + run-length encoding, and
+// the fp64 segment-reduce fused with the row-wise Adagrad scatter-update.
+#include "mlkv_kernels.h"
+
+namespace mlkv {
+
+// ===========================================================================
+// Get: probe + gather (+ insert-on-miss), one key per lane.
+// ===========================================================================
+template <int VEC>
+__device__ __forceinline__ typename VecT<VEC>::T load_vec(const float* p) {
+  if constexpr (VEC == 4) {
+    return *reinterpret_cast<const float4*>(p);
+  } else {
+    return *p;
+  }
+}
+
+template <int VEC>
+__device__ __forceinline__ void store_vec(float* p, const typename VecT<VEC>::T& v) {
+  if constexpr (VEC == 4) {
+    *reinterpret_cast<float4*>(p) = v;
+  } else {
+    *p = v;
+  }
+}
+
+template <int VEC>
+__device__ __forceinline__ typename VecT<VEC>::T init_vec(uint64_t s0, int col) {
+  typename VecT<VEC>::T v;
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) VecT<VEC>::set(v, e, init_elem(s0, col + e));
+  return v;
+}
+
+// The wave copies the rows of its 64 positions into `out`: rows of keys that
+// were present are read from the table, rows of keys new in this call are
+// generated from their seed (they equal what the table will hold).
+template <class M>
+__device__ __forceinline__ void wave_emit_rows(float* __restrict__ out, const float* __restrict__ rows,
+                                               int D, int64_t wave_base, int64_t n, bool hit,
+                                               uint32_t row, uint64_t s0, int lane) {
+  constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
+  constexpr int ITERS = 64 / RPW;
+  constexpr int UNITS = ITERS * K;
+  constexpr int CH = UNITS < 16 ? UNITS : 16;
+  const int g = lane / LPR;
+  const int q = lane % LPR;
+  const int ihit = hit ? 1 : 0;
+#pragma unroll 1
+  for (int u0 = 0; u0 < UNITS; u0 += CH) {
+    typename VecT<VEC>::T v[CH];
+#pragma unroll
+    for (int u = 0; u < CH; ++u) {
+      const int uu = u0 + u;
+      const int it = uu / K;
+      const int k = uu % K;
+      const int r = it * RPW + g;
+      const uint32_t rr = __shfl(row, r, 64);
+      const int hh = __shfl(ihit, r, 64);
+      const uint64_t ss = __shfl((unsigned long long)s0, r, 64);
+      const int col = (k * LPR + q) * VEC;
+      const int64_t p = wave_base + r;
+      if (uu < UNITS && p < n && col < D) {
+        if (hh) v[u] = load_vec<VEC>(rows + (size_t)rr * (size_t)D + col);
+        else v[u] = init_vec<VEC>(ss, col);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < CH; ++u) {
+      const int uu = u0 + u;
+      const int it = uu / K;
+      const int k = uu % K;
+      const int r = it * RPW + g;
+      const int col = (k * LPR + q) * VEC;
+      const int64_t p = wave_base + r;
+      if (uu < UNITS && p < n && col < D) store_vec<VEC>(out + (size_t)p * (size_t)D + col, v[u]);
+    }
+  }
+}
+
+template <class M>
+__global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
+    Bucket* __restrict__ idx, uint32_t nb_log2, const uint64_t* __restrict__ keys, int64_t n,
+    float* __restrict__ out, const float* __restrict__ rows, int D, uint64_t seed,
+    NewKey* __restrict__ newlist, uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch) {
+  __shared__ uint32_t s_cnt;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int64_t base = (int64_t)blockIdx.x * kGetTile;
+  const int64_t i = base + tid;
+  if (tid == 0) s_cnt = 0;
+  __syncthreads();
+  uint64_t key = 0;
+  Probe pr = {0, kPendingRow, P_NONE};
+  if (i < n) {
+    key = keys[i];
+    if (key == kEmptyKey) {
+      pr.status = P_BAD;
+      ctrl->bad_epoch = epoch;
+    } else {
+      pr = probe_key(idx, nb_log2, key, true);
+      if (pr.status == P_OVERFLOW) ctrl->overflow_epoch = epoch;
+    }
+  }
+  if (pr.status == P_NEW_MINE) {
+    const uint32_t j = atomicAdd(&s_cnt, 1u);
+    newlist[base + j] = NewKey{key, pr.slot, 0u};
+  }
+  if (out != nullptr) {
+    const uint64_t s0 = splitmix_mix(key ^ seed);
+    wave_emit_rows<M>(out, rows, D, base + wave * 64, n, pr.status == P_HIT, pr.row, s0, lane);
+  }
+  __syncthreads();
+  if (tid == 0) tile_cnt[blockIdx.x] = s_cnt;
+}
+
+// ===========================================================================
+// Streaming every new key of the call through LDS (used to rank new keys).
+// ===========================================================================
+constexpr int kChunk = 2048;
+
+// Calls body(s_chunk, cnt) for consecutive chunks of this call's new keys;
+// the block's NT threads must all call it. s_pref: NT+1 words.
+template <int NT, class Body>
+__device__ void for_each_new_key_chunk(const NewKey* __restrict__ newlist,
+                                       const uint32_t* __restrict__ tile_cnt, int ntiles,
+                                       int tile_size, uint32_t* s_pref, uint32_t* s_w,
+                                       uint64_t* s_chunk, Body body) {
+  constexpr int PER = kChunk / NT;
+  for (int t0 = 0; t0 < ntiles; t0 += NT) {
+    const int nt = min(NT, ntiles - t0);
+    const uint32_t c = (int)threadIdx.x < nt ? tile_cnt[t0 + threadIdx.x] : 0u;
+    uint32_t total;
+    const uint32_t pre = block_exclusive_scan<NT>(c, s_w, &total);
+    s_pref[threadIdx.x] = pre;
+    __syncthreads();
+    for (uint32_t k0 = 0; k0 < total; k0 += kChunk) {
+      const uint32_t cnt = min((uint32_t)kChunk, total - k0);
+      uint64_t v[PER];
+#pragma unroll
+      for (int e = 0; e < PER; ++e) {
+        const uint32_t k = threadIdx.x + e * NT;
+        v[e] = 0;
+        if (k < cnt) {
+          const uint32_t gk = k0 + k;
+          int lo = 0, hi = nt - 1;
+          while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (s_pref[mid] <= gk) lo = mid;
+            else hi = mid - 1;
+          }
+          v[e] = newlist[(size_t)(t0 + lo) * tile_size + (gk - s_pref[lo])].key;
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < PER; ++e) {
+        const uint32_t k = threadIdx.x + e * NT;
+        if (k < cnt) s_chunk[k] = v[e];
+      }
+      __syncthreads();
+      body(s_chunk, cnt);
+      __syncthreads();
+    }
+    __syncthreads();
+  }
+}
+
+// Sum of the per-tile new-key counts, i.e. the number M of distinct keys the
+// call inserts.
+template <int NT>
+__device__ __forceinline__ uint64_t count_new_keys(const uint32_t* __restrict__ tile_cnt, int ntiles,
+                                                   unsigned long long* s_w64) {
+  uint64_t m = 0;
+  for (int t = threadIdx.x; t < ntiles; t += NT) m += tile_cnt[t];
+  return block_sum_u64<NT>(m, s_w64);
+}
+
+// Decides whether the call fails, and publishes the size for the next call.
+__device__ __forceinline__ int call_verdict(Ctrl* ctrl, uint64_t epoch, uint64_t size0, uint64_t M,
+                                            int64_t capacity) {
+  int err = 0;
+  if (ctrl->bad_epoch == epoch) err = -1;                          // MLKV_EINVAL
+  else if (ctrl->overflow_epoch == epoch || size0 + M > (uint64_t)capacity) err = -2;  // MLKV_EFULL
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    ctrl->size[(epoch + 1) & 1] = err ? size0 : size0 + M;
+    if (err) atomicCAS(&ctrl->latched, 0, err);
+  }
+  return err;
+}
+
+// ===========================================================================
+// Get, second kernel: assign rows to the call's new keys (ascending key order),
+// write their initial rows and zero accumulators; or roll the call back.
+// ===========================================================================
+constexpr int kAssignThreads = 256;
+constexpr int kAssignBatch = 8;
+constexpr int kAssignMine = kAssignBatch * kAssignThreads;
+
+__global__ __launch_bounds__(kAssignThreads) void k_assign_new(
+    Bucket* __restrict__ idx, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
+    int ntiles, int tile_size, float* __restrict__ rows, float* __restrict__ state, int D,
+    uint64_t seed, int64_t capacity, Ctrl* ctrl, uint64_t epoch) {
+  constexpr int NT = kAssignThreads;
+  __shared__ unsigned long long s_w64[NT / 64];
+  __shared__ uint32_t s_w[NT / 64];
+  __shared__ uint32_t s_pref[NT + 1];
+  __shared__ uint64_t s_chunk[kChunk];
+  __shared__ uint64_t s_key[kAssignMine];
+  __shared__ uint32_t s_slot[kAssignMine];
+  __shared__ uint32_t s_rank[kAssignMine];
+
+  const uint64_t M = count_new_keys<NT>(tile_cnt, ntiles, s_w64);
+  const uint64_t size0 = ctrl->size[epoch & 1];
+  const int err = call_verdict(ctrl, epoch, size0, M, capacity);
+  if (M == 0) return;
+
+  if (err) {  // undo this call's insertions: the index returns to its state before the call
+    for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+      const uint32_t c = tile_cnt[t];
+      for (uint32_t j = threadIdx.x; j < c; j += NT) {
+        const uint32_t slot = newlist[(size_t)t * tile_size + j].slot;
+        idx[slot / kSlots].key[slot % kSlots] = kEmptyKey;
+      }
+    }
+    return;
+  }
+
+  // This block owns the tiles t = blockIdx.x (mod gridDim.x); it takes them
+  // kAssignBatch at a time (thread j holds entry j of each tile) and ranks
+  // their keys against all M new keys of the call.
+  static_assert(kGetTile == NT, "one thread per entry of a probe tile");
+  for (int tb = blockIdx.x; tb < ntiles; tb += gridDim.x * kAssignBatch) {
+    uint32_t have = 0;
+#pragma unroll
+    for (int b = 0; b < kAssignBatch; ++b) {
+      const int t = tb + b * (int)gridDim.x;
+      const uint32_t c = t < ntiles ? tile_cnt[t] : 0u;
+      const uint32_t j = threadIdx.x;
+      const int m = b * NT + (int)j;
+      if (j < c) {
+        const NewKey nk = newlist[(size_t)t * tile_size + j];
+        s_key[m] = nk.key;
+        s_slot[m] = nk.slot;
+        have = 1;
+      } else {
+        s_slot[m] = kPendingRow;  // marks an unused entry
+      }
+      s_rank[m] = 0;
+    }
+    if (block_sum_u64<NT>(have, s_w64) == 0) continue;
+    for_each_new_key_chunk<NT>(newlist, tile_cnt, ntiles, tile_size, s_pref, s_w, s_chunk,
+                               [&](const uint64_t* ck, uint32_t cnt) {
+#pragma unroll
+                                 for (int b = 0; b < kAssignBatch; ++b) {
+                                   const int m = b * NT + (int)threadIdx.x;
+                                   if (s_slot[m] == kPendingRow) continue;
+                                   const uint64_t mk = s_key[m];
+                                   uint32_t r = 0;
+                                   for (uint32_t e = 0; e < cnt; ++e) r += ck[e] < mk ? 1u : 0u;
+                                   s_rank[m] += r;
+                                 }
+                               });
+#pragma unroll
+    for (int b = 0; b < kAssignBatch; ++b) {
+      const int m = b * NT + (int)threadIdx.x;
+      const uint32_t slot = s_slot[m];
+      if (slot == kPendingRow) continue;
+      const uint32_t row = (uint32_t)(size0 + s_rank[m]);
+      idx[slot / kSlots].row[slot % kSlots] = row;
+      state[row] = 0.0f;
+    }
+    // initial rows, written cooperatively (coalesced along each row)
+    for (int b = 0; b < kAssignBatch; ++b) {
+      const int t = tb + b * (int)gridDim.x;
+      const uint32_t c = t < ntiles ? tile_cnt[t] : 0u;
+      const uint64_t total = (uint64_t)c * (uint64_t)D;
+      for (uint64_t e = threadIdx.x; e < total; e += NT) {
+        const uint32_t j = (uint32_t)(e / (uint64_t)D);
+        const int col = (int)(e - (uint64_t)j * D);
+        const int m = b * NT + (int)j;
+        const uint64_t row = size0 + s_rank[m];
+        rows[row * (uint64_t)D + col] = init_elem(splitmix_mix(s_key[m] ^ seed), col);
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ===========================================================================
+// Put, first kernel: probe (+ insert) and partition the tile's (slot, pos)
+// pairs by the top bits of the slot (one MSD radix digit), in LDS.
+// ===========================================================================
+__global__ __launch_bounds__(kPutTile) void k_put_probe(
+    Bucket* __restrict__ idx, uint32_t nb_log2, const uint64_t* __restrict__ keys, int64_t n,
+    int shift, int NP, uint64_t* __restrict__ items, uint32_t* __restrict__ meta,
+    NewKey* __restrict__ newlist, uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch) {
+  constexpr int NT = kPutTile;
+  __shared__ uint32_t s_hist[kMaxParts];
+  __shared__ uint32_t s_w[NT / 64];
+  __shared__ uint32_t s_cnt;
+  const int tid = threadIdx.x;
+  const int tile = blockIdx.x;
+  const int64_t i = (int64_t)tile * NT + tid;
+  if (tile == 0 && tid == 0) ctrl->spill_next = 0;
+  for (int d = tid; d < NP; d += NT) s_hist[d] = 0;
+  if (tid == 0) s_cnt = 0;
+  __syncthreads();
+
+  uint64_t key = 0;
+  Probe pr = {0, kPendingRow, P_NONE};
+  if (i < n) {
+    key = keys[i];
+    if (key == kEmptyKey) {
+      pr.status = P_BAD;
+      ctrl->bad_epoch = epoch;
+    } else {
+      pr = probe_key(idx, nb_log2, key, true);
+      if (pr.status == P_OVERFLOW) ctrl->overflow_epoch = epoch;
+    }
+  }
+  const bool item = pr.status == P_HIT || pr.status == P_NEW_MINE || pr.status == P_NEW_OTHER;
+  uint32_t d = 0, r = 0;
+  if (item) {
+    d = pr.slot >> shift;
+    r = atomicAdd(&s_hist[d], 1u);
+  }
+  if (pr.status == P_NEW_MINE) {
+    const uint32_t j = atomicAdd(&s_cnt, 1u);
+    newlist[(size_t)tile * NT + j] = NewKey{key, pr.slot, 0u};
+  }
+  __syncthreads();
+
+  constexpr int PER = kMaxParts / NT;
+  uint32_t c[PER];
+  uint32_t sum = 0;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int dd = tid * PER + j;
+    c[j] = dd < NP ? s_hist[dd] : 0u;
+    sum += c[j];
+  }
+  uint32_t tot;
+  uint32_t off = block_exclusive_scan<NT>(sum, s_w, &tot);
+  uint32_t offs[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int dd = tid * PER + j;
+    offs[j] = off;
+    if (dd < NP) meta[(size_t)tile * NP + dd] = off | (c[j] << 16);
+    off += c[j];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int dd = tid * PER + j;
+    if (dd < NP) s_hist[dd] = offs[j];
+  }
+  __syncthreads();
+  if (item) items[(size_t)tile * NT + s_hist[d] + r] = ((uint64_t)pr.slot << 32) | (uint32_t)i;
+  if (tid == 0) tile_cnt[tile] = s_cnt;
+}
+
+// ===========================================================================
+// Put, second kernel: one block per partition. Gathers the partition's
+// (slot, pos) pairs, sorts them, run-length encodes them into segments (one
+// per distinct key, positions ascending), sums each segment's gradient rows in
+// fp64 and applies one row-wise Adagrad step to the key's row.
+// ===========================================================================
+template <class M>
+struct SegmentOps {
+  static constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
+  using V = typename VecT<VEC>::T;
+  static constexpr int UNR = (K * VEC >= 8) ? 4 : 8;
+
+  // acc += grads rows of sorted entries [b, e) (positions in the low 32 bits)
+  static __device__ __forceinline__ void accumulate(double (&acc)[K][VEC], const uint64_t* it,
+                                                    uint32_t b, uint32_t e,
+                                                    const float* __restrict__ grads, int D, int q) {
+    for (uint32_t j = b; j < e; j += UNR) {
+      V v[UNR][K];
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        if (j + u < e) {
+          const uint32_t pos = (uint32_t)it[j + u];
+          const float* g = grads + (size_t)pos * (size_t)D;
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            const int col = (k * LPR + q) * VEC;
+            if (col < D) v[u][k] = load_vec<VEC>(g + col);
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        if (j + u < e) {
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            const int col = (k * LPR + q) * VEC;
+            if (col < D) {
+#pragma unroll
+              for (int x = 0; x < VEC; ++x) acc[k][x] += (double)VecT<VEC>::get(v[u][k], x);
+            }
+          }
+        }
+      }
+    }
+  }
+
+  // Current row values (or the initial row of a key new in this call).
+  static __device__ __forceinline__ void load_w(V (&w)[K], const float* __restrict__ rows, uint32_t row,
+                                                bool isnew, uint64_t s0, int D, int q) {
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int col = (k * LPR + q) * VEC;
+      if (col < D) {
+        if (isnew) w[k] = init_vec<VEC>(s0, col);
+        else w[k] = load_vec<VEC>(rows + (size_t)row * (size_t)D + col);
+      }
+    }
+  }
+
+  // g = fp32(acc); m = fp32(sum g^2 / D) over the group's lanes; G' = G + m;
+  // den = sqrt(G') + eps; w -= lr * (g / den); writes w and G'.
+  static __device__ __forceinline__ void adagrad(const double (&acc)[K][VEC], V (&w)[K], float G0,
+                                                 float* __restrict__ rows, float* __restrict__ state,
+                                                 uint32_t row, int D, int q, int leader, float lr,
+                                                 float eps) {
+    float gf[K][VEC];
+    double sq = 0.0;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int col = (k * LPR + q) * VEC;
+#pragma unroll
+      for (int x = 0; x < VEC; ++x) {
+        gf[k][x] = (float)acc[k][x];
+        if (col + x < D) sq += (double)gf[k][x] * (double)gf[k][x];
+      }
+    }
+#pragma unroll
+    for (int o = LPR / 2; o > 0; o >>= 1) sq += __shfl_xor(sq, o, 64);
+    const float m = (float)(sq / (double)D);
+    const float G = __shfl(G0, leader, 64);
+    const float Gn = __fadd_rn(G, m);
+    const float den = __fadd_rn(__builtin_sqrtf(Gn), eps);  // correctly rounded sqrt
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int col = (k * LPR + q) * VEC;
+      if (col < D) {
+#pragma unroll
+        for (int x = 0; x < VEC; ++x) {
+          const float qv = __fdiv_rn(gf[k][x], den);
+          const float p = __fmul_rn(lr, qv);
+          VecT<VEC>::set(w[k], x, __fsub_rn(VecT<VEC>::get(w[k], x), p));
+        }
+        store_vec<VEC>(rows + (size_t)row * (size_t)D + col, w[k]);
+      }
+    }
+    if (q == 0) state[row] = Gn;
+  }
+};
+
+template <class M>
+__global__ __launch_bounds__(kRedThreads) void k_reduce_update(
+    Bucket* __restrict__ idx, const uint64_t* __restrict__ items, const uint32_t* __restrict__ meta,
+    int ntiles, int NP, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
+    const float* __restrict__ grads, float* __restrict__ rows, float* __restrict__ state, int D,
+    uint64_t seed, float lr, float eps, int64_t capacity, Ctrl* ctrl, uint64_t epoch,
+    uint64_t* __restrict__ spill, uint64_t spill_words) {
+  constexpr int NT = kRedThreads;
+  constexpr int NW = NT / 64;
+  using Ops = SegmentOps<M>;
+  constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
+  constexpr int NG = NW * RPW;  // lane groups per block
+  using V = typename VecT<VEC>::T;
+
+  extern __shared__ double s_dyn[];  // partial sums [NG][D] or a key chunk [kChunk]
+  __shared__ uint64_t s_items[kRedCap];
+  __shared__ uint32_t s_seg[kRedCap + 1];
+  __shared__ uint32_t s_row[kRedCap];
+  __shared__ uint32_t s_pref[NT + 1];
+  __shared__ uint32_t s_w[NW];
+  __shared__ unsigned long long s_w64[NW];
+  __shared__ uint64_t s_spill_base;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int g = lane / LPR;
+  const int q = lane % LPR;
+  const int gid = wave * RPW + g;
+  const int leader = g * LPR;
+  const uint32_t p = blockIdx.x;
+
+  const uint64_t Mnew = count_new_keys<NT>(tile_cnt, ntiles, s_w64);
+  const uint64_t size0 = ctrl->size[epoch & 1];
+  const int err = call_verdict(ctrl, epoch, size0, Mnew, capacity);
+
+  // size of this partition
+  uint64_t mp64 = 0;
+  for (int t = tid; t < ntiles; t += NT) mp64 += meta[(size_t)t * NP + p] >> 16;
+  const uint32_t mp = (uint32_t)block_sum_u64<NT>(mp64, s_w64);
+  if (mp == 0) return;
+
+  if (err) {
+    if (Mnew == 0) return;
+    // roll back keys this call inserted whose slots fall in this partition
+    for (int t = tid; t < ntiles; t += NT) {
+      const uint32_t mt = meta[(size_t)t * NP + p];
+      const uint32_t off = mt & 0xFFFFu, cnt = mt >> 16;
+      for (uint32_t j = 0; j < cnt; ++j) {
+        const uint32_t slot = (uint32_t)(items[(size_t)t * kPutTile + off + j] >> 32);
+        Bucket* B = idx + slot / kSlots;
+        if (B->row[slot % kSlots] == kPendingRow) B->key[slot % kSlots] = kEmptyKey;
+      }
+    }
+    return;
+  }
+
+  // ---- gather into LDS (or a global spill area when it does not fit) ----
+  uint32_t P2 = 1;
+  while (P2 < mp) P2 <<= 1;
+  const bool spilled = mp > (uint32_t)kRedCap;
+  uint64_t* it;
+  uint32_t* seg;
+  uint32_t* rowv;
+  if (spilled) {
+    if (tid == 0) {
+      const uint64_t need = 2ull * P2 + 2;
+      const uint64_t b = atomicAdd(&ctrl->spill_next, (unsigned long long)need);
+      s_spill_base = (b + need <= spill_words) ? b : ~0ull;
+    }
+    __syncthreads();
+    if (s_spill_base == ~0ull) {  // cannot happen when the spill area is sized 4n
+      if (tid == 0) atomicCAS(&ctrl->latched, 0, -4);
+      return;
+    }
+    it = spill + s_spill_base;
+    seg = reinterpret_cast<uint32_t*>(spill + s_spill_base + P2);
+    rowv = seg + P2 + 1;
+  } else {
+    it = s_items;
+    seg = s_seg;
+    rowv = s_row;
+  }
+  {
+    uint32_t base = 0;
+    for (int t0 = 0; t0 < ntiles; t0 += NT) {
+      const int t = t0 + tid;
+      const uint32_t mt = t < ntiles ? meta[(size_t)t * NP + p] : 0u;
+      const uint32_t off = mt & 0xFFFFu, cnt = mt >> 16;
+      uint32_t tot;
+      const uint32_t pre = block_exclusive_scan<NT>(cnt, s_w, &tot);
+      for (uint32_t j = 0; j < cnt; ++j) it[base + pre + j] = items[(size_t)t * kPutTile + off + j];
+      base += tot;
+    }
+    for (uint32_t j = mp + tid; j < P2; j += NT) it[j] = ~0ull;
+    __syncthreads();
+  }
+  block_bitonic_sort<NT>(it, P2);
+
+  // ---- run-length encode: segment starts ----
+  uint32_t S = 0;
+  for (uint32_t b0 = 0; b0 < mp; b0 += NT) {
+    const uint32_t j = b0 + tid;
+    const uint32_t head = (j < mp) && (j == 0 || (it[j] >> 32) != (it[j - 1] >> 32)) ? 1u : 0u;
+    uint32_t tot;
+    const uint32_t pre = block_exclusive_scan<NT>(head, s_w, &tot);
+    if (head) seg[S + pre] = j;
+    S += tot;
+  }
+  if (tid == 0) seg[S] = mp;
+  __syncthreads();
+
+  // ---- row of every segment; new keys of this call get their rows here ----
+  uint64_t* s_chunk = reinterpret_cast<uint64_t*>(s_dyn);
+  for (uint32_t s0 = 0; s0 < S; s0 += NT) {
+    const uint32_t s = s0 + tid;
+    uint32_t slot = 0, row = 0;
+    uint64_t key = 0;
+    if (s < S) {
+      slot = (uint32_t)(it[seg[s]] >> 32);
+      row = idx[slot / kSlots].row[slot % kSlots];
+    }
+    const uint32_t pend = (s < S && row == kPendingRow) ? 1u : 0u;
+    const uint64_t npend = block_sum_u64<NT>(pend, s_w64);
+    if (npend > 0) {
+      if (pend) key = idx[slot / kSlots].key[slot % kSlots];
+      uint32_t rank = 0;
+      for_each_new_key_chunk<NT>(newlist, tile_cnt, ntiles, kPutTile, s_pref, s_w, s_chunk,
+                                 [&](const uint64_t* ck, uint32_t cnt) {
+                                   if (pend)
+                                     for (uint32_t e = 0; e < cnt; ++e) rank += ck[e] < key ? 1u : 0u;
+                                 });
+      if (pend) {
+        row = (uint32_t)(size0 + rank);
+        idx[slot / kSlots].row[slot % kSlots] = row;
+      }
+    }
+    if (s < S) rowv[s] = row;
+  }
+  __syncthreads();
+
+  double* s_part = s_dyn;
+
+  // ---- long segments: every lane group of the block takes a slice ----
+  for (uint32_t s = 0; s < S; ++s) {
+    const uint32_t b = seg[s], e = seg[s + 1];
+    if (e - b <= (uint32_t)kLongSeg) continue;
+    const uint32_t len = e - b;
+    const uint32_t per = (len + NG - 1) / NG;
+    const uint32_t lb = min(e, b + gid * per), le = min(e, lb + per);
+    double acc[K][VEC];
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+#pragma unroll
+      for (int x = 0; x < VEC; ++x) acc[k][x] = 0.0;
+    Ops::accumulate(acc, it, lb, le, grads, D, q);
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int col = (k * LPR + q) * VEC;
+#pragma unroll
+      for (int x = 0; x < VEC; ++x)
+        if (col + x < D) s_part[(size_t)gid * D + col + x] = acc[k][x];
+    }
+    __syncthreads();
+    if (gid == 0) {
+      const uint32_t row = rowv[s];
+      const bool isnew = row >= size0;
+      uint64_t s0 = 0;
+      if (isnew) {
+        const uint32_t slot = (uint32_t)(it[b] >> 32);
+        s0 = splitmix_mix(idx[slot / kSlots].key[slot % kSlots] ^ seed);
+      }
+      V w[K];
+      Ops::load_w(w, rows, row, isnew, s0, D, q);
+      const float G0 = (q == 0 && !isnew) ? state[row] : 0.0f;
+      double tot[K][VEC];
+#pragma unroll
+      for (int k = 0; k < K; ++k)
+#pragma unroll
+        for (int x = 0; x < VEC; ++x) tot[k][x] = 0.0;
+      for (int h = 0; h < NG; ++h) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const int col = (k * LPR + q) * VEC;
+#pragma unroll
+          for (int x = 0; x < VEC; ++x)
+            if (col + x < D) tot[k][x] += s_part[(size_t)h * D + col + x];
+        }
+      }
+      Ops::adagrad(tot, w, G0, rows, state, row, D, q, leader, lr, eps);
+    }
+    __syncthreads();
+  }
+
+  // ---- short segments: one lane group each ----
+  for (uint32_t s = gid; s < S; s += NG) {
+    const uint32_t b = seg[s], e = seg[s + 1];
+    if (e - b > (uint32_t)kLongSeg) continue;
+    const uint32_t row = rowv[s];
+    const bool isnew = row >= size0;
+    uint64_t s0 = 0;
+    if (isnew) {
+      const uint32_t slot = (uint32_t)(it[b] >> 32);
+      s0 = splitmix_mix(idx[slot / kSlots].key[slot % kSlots] ^ seed);
+    }
+    V w[K];
+    Ops::load_w(w, rows, row, isnew, s0, D, q);
+    const float G0 = (q == 0 && !isnew) ? state[row] : 0.0f;
+    double acc[K][VEC];
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+#pragma unroll
+      for (int x = 0; x < VEC; ++x) acc[k][x] = 0.0;
+    Ops::accumulate(acc, it, b, e, grads, D, q);
+    Ops::adagrad(acc, w, G0, rows, state, row, D, q, leader, lr, eps);
+  }
+}
+
+// ===========================================================================
+// Inspection kernels
+// ===========================================================================
+__global__ __launch_bounds__(256) void k_lookup(Bucket* __restrict__ idx, uint32_t nb_log2,
+                                                const uint64_t* __restrict__ keys, int64_t n,
+                                                int64_t* __restrict__ rows_out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  const uint64_t key = keys[i];
+  int64_t r = -1;
+  if (key != kEmptyKey) {
+    const Probe pr = probe_key(idx, nb_log2, key, false);
+    if (pr.status == P_HIT) r = pr.row;
+  }
+  rows_out[i] = r;
+}
+
+__global__ __launch_bounds__(256) void k_export_slots(const Bucket* __restrict__ idx, uint64_t nslots,
+                                                      uint64_t* __restrict__ keys_out,
+                                                      uint32_t* __restrict__ rows_out) {
+  const uint64_t s = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+  if (s >= nslots) return;
+  const Bucket* B = idx + s / kSlots;
+  if (keys_out) keys_out[s] = B->key[s % kSlots];
+  if (rows_out) rows_out[s] = B->row[s % kSlots];
+}
+
+// ===========================================================================
+// Launchers
+// ===========================================================================
+template <class M>
+static hipError_t launch_get_t(const GetArgs& a, hipStream_t st) {
+  const int64_t ntiles = (a.n + kGetTile - 1) / kGetTile;
+  hipLaunchKernelGGL(k_get_probe_gather<M>, dim3((unsigned)ntiles), dim3(kGetTile), 0, st, a.idx,
+                     a.nb_log2, a.keys, a.n, a.out, a.rows, a.D, a.seed, a.newlist, a.tile_cnt, a.ctrl,
+                     a.epoch);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int grid = (int)std::min<int64_t>(ntiles, 256);
+  hipLaunchKernelGGL(k_assign_new, dim3(grid), dim3(kAssignThreads), 0, st, a.idx, a.newlist,
+                     a.tile_cnt, (int)ntiles, kGetTile, a.rows, a.state, a.D, a.seed, a.capacity,
+                     a.ctrl, a.epoch);
+  return hipGetLastError();
+}
+
+template <class M>
+static size_t reduce_dyn_bytes(int D) {
+  const size_t part = (size_t)(kRedThreads / 64) * M::RPW * (size_t)D * sizeof(double);
+  const size_t chunk = (size_t)kChunk * sizeof(uint64_t);
+  return part > chunk ? part : chunk;
+}
+
+template <class M>
+static hipError_t launch_put_t(const PutArgs& a, hipStream_t st) {
+  const int64_t ntiles = (a.n + kPutTile - 1) / kPutTile;
+  hipLaunchKernelGGL(k_put_probe, dim3((unsigned)ntiles), dim3(kPutTile), 0, st, a.idx, a.nb_log2,
+                     a.keys, a.n, a.shift, a.NP, a.items, a.meta, a.newlist, a.tile_cnt, a.ctrl,
+                     a.epoch);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const size_t dyn = reduce_dyn_bytes<M>(a.D);
+  static bool attr_set = false;
+  if (!attr_set) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_reduce_update<M>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, 96 * 1024);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(k_reduce_update<M>, dim3((unsigned)a.NP), dim3(kRedThreads), dyn, st, a.idx,
+                     a.items, a.meta, (int)ntiles, a.NP, a.newlist, a.tile_cnt, a.grads, a.rows,
+                     a.state, a.D, a.seed, a.lr, a.eps, a.capacity, a.ctrl, a.epoch, a.spill,
+                     a.spill_words);
+  return hipGetLastError();
+}
+
+// Row maps: float4 lanes when rows are 16-byte aligned multiples of 4 floats.
+using MapD16 = RowMap<4, 4, 1>;     // dim <= 16
+using MapD32 = RowMap<4, 8, 1>;     // dim <= 32
+using MapD64 = RowMap<4, 16, 1>;    // dim <= 64
+using MapD128 = RowMap<4, 32, 1>;   // dim <= 128
+using MapD256 = RowMap<4, 64, 1>;   // dim <= 256
+using MapD512 = RowMap<4, 64, 2>;   // dim <= 512
+using MapD1024 = RowMap<4, 64, 4>;  // dim <= 1024
+using MapAny = RowMap<1, 64, 16>;   // any dim <= 1024, one float per lane
+
+template <class F>
+static hipError_t dispatch_map(int D, bool vec4, F f) {
+  if (!vec4) return f(MapAny{});
+  if (D <= 16) return f(MapD16{});
+  if (D <= 32) return f(MapD32{});
+  if (D <= 64) return f(MapD64{});
+  if (D <= 128) return f(MapD128{});
+  if (D <= 256) return f(MapD256{});
+  if (D <= 512) return f(MapD512{});
+  return f(MapD1024{});
+}
+
+hipError_t launch_get(const GetArgs& a, bool vec4, hipStream_t st) {
+  return dispatch_map(a.D, vec4, [&](auto m) { return launch_get_t<decltype(m)>(a, st); });
+}
+
+hipError_t launch_put(const PutArgs& a, bool vec4, hipStream_t st) {
+  return dispatch_map(a.D, vec4, [&](auto m) { return launch_put_t<decltype(m)>(a, st); });
+}
+
+hipError_t launch_lookup(Bucket* idx, uint32_t nb_log2, const uint64_t* keys, int64_t n, int64_t* rows_out,
+                         hipStream_t st) {
+  const int64_t grid = (n + 255) / 256;
+  hipLaunchKernelGGL(k_lookup, dim3((unsigned)grid), dim3(256), 0, st, idx, nb_log2, keys, n, rows_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_export_slots(const Bucket* idx, uint64_t nslots, uint64_t* keys_out, uint32_t* rows_out,
+                               hipStream_t st) {
+  const uint64_t grid = (nslots + 255) / 256;
+  hipLaunchKernelGGL(k_export_slots, dim3((unsigned)grid), dim3(256), 0, st, idx, nslots, keys_out, rows_out);
+  return hipGetLastError();
+}
+
+}  // namespace mlkv

@@ -1,0 +1,208 @@
+"""ctypes binding of libmlkv.so (see include/mlkv.h for the contract).
+
+Functions carry the C names and only marshal arguments: torch tensors are
+passed as device pointers and torch streams as hipStream_t. Every step of the
+get / put_grad path runs in the library's HIP kernels; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch  # loads the HIP runtime that libmlkv binds to (same soname)
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmlkv.so")
+
+MLKV_OK, MLKV_EINVAL, MLKV_EFULL, MLKV_ENOMEM, MLKV_EDEVICE = 0, -1, -2, -3, -4
+MLKV_DEFAULT_SEED = 0x4D4C4B56
+MLKV_RESERVED_KEY = 0xFFFFFFFFFFFFFFFF
+
+EXPORTS = ("mlkv_open", "mlkv_open_ex", "mlkv_get", "mlkv_put_grad", "mlkv_sync", "mlkv_size",
+           "mlkv_num_slots", "mlkv_close", "mlkv_last_error", "mlkv_lookup_rows", "mlkv_export")
+
+_lib = None
+
+
+class MlkvError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{msg} (code {code})")
+        self.code = code
+
+
+def load() -> ctypes.CDLL:
+    """Loads libmlkv.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                          "(or python paper_2504_01506_amd/build.py)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, U64, F32, INT = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64,
+                                  ctypes.c_float, ctypes.c_int)
+    sig = {
+        "mlkv_open": (P, [I32, I64]),
+        "mlkv_open_ex": (P, [I32, I64, U64, F32]),
+        "mlkv_get": (INT, [P, P, I64, P, P]),
+        "mlkv_put_grad": (INT, [P, P, P, I64, F32, F32, P]),
+        "mlkv_sync": (INT, [P, P]),
+        "mlkv_size": (I64, [P]),
+        "mlkv_num_slots": (I64, [P]),
+        "mlkv_close": (None, [P]),
+        "mlkv_last_error": (ctypes.c_char_p, []),
+        "mlkv_lookup_rows": (INT, [P, P, I64, P, P]),
+        "mlkv_export": (INT, [P, I64, P, P, P, P, P]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = lib
+    return lib
+
+
+def hip_runtimes_loaded() -> list[str]:
+    """Paths of every libamdhip64 mapped into this process (must be exactly one)."""
+    paths = set()
+    with open("/proc/self/maps") as f:
+        for line in f:
+            if "libamdhip64" in line:
+                paths.add(line.split()[-1])
+    return sorted(paths)
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(s):
+    if s is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def last_error() -> str:
+    return load().mlkv_last_error().decode()
+
+
+def _check(rc: int):
+    if rc != MLKV_OK:
+        raise MlkvError(rc, last_error())
+
+
+# ---- the C calls, same names ------------------------------------------------
+def mlkv_open(dim: int, capacity: int) -> int:
+    h = load().mlkv_open(dim, capacity)
+    if not h:
+        raise MlkvError(MLKV_EINVAL, last_error())
+    return h
+
+
+def mlkv_open_ex(dim: int, capacity: int, seed: int, max_load: float) -> int:
+    h = load().mlkv_open_ex(dim, capacity, seed, max_load)
+    if not h:
+        raise MlkvError(MLKV_EINVAL, last_error())
+    return h
+
+
+def mlkv_get(t: int, keys, n: int, out, stream=None) -> int:
+    return load().mlkv_get(t, _ptr(keys), n, _ptr(out), _stream(stream))
+
+
+def mlkv_put_grad(t: int, keys, grads, n: int, lr: float, eps: float, stream=None) -> int:
+    return load().mlkv_put_grad(t, _ptr(keys), _ptr(grads), n, lr, eps, _stream(stream))
+
+
+def mlkv_sync(t: int, stream=None) -> int:
+    return load().mlkv_sync(t, _stream(stream))
+
+
+def mlkv_size(t: int) -> int:
+    return load().mlkv_size(t)
+
+
+def mlkv_num_slots(t: int) -> int:
+    return load().mlkv_num_slots(t)
+
+
+def mlkv_close(t: int) -> None:
+    load().mlkv_close(t)
+
+
+def mlkv_last_error() -> str:
+    return last_error()
+
+
+def mlkv_lookup_rows(t: int, keys, n: int, rows_out, stream=None) -> int:
+    return load().mlkv_lookup_rows(t, _ptr(keys), n, _ptr(rows_out), _stream(stream))
+
+
+def mlkv_export(t: int, nrows: int, rows_out=None, state_out=None, slot_keys_out=None,
+                slot_rows_out=None, stream=None) -> int:
+    return load().mlkv_export(t, nrows, _ptr(rows_out), _ptr(state_out), _ptr(slot_keys_out),
+                              _ptr(slot_rows_out), _stream(stream))
+
+
+# ---- a small object wrapper over the same calls -----------------------------
+class Table:
+    """One embedding table on the current GPU. Keys are uint64 (stored in an
+    int64 tensor), rows fp32. Methods raise MlkvError on a non-zero code."""
+
+    def __init__(self, dim: int, capacity: int, seed: int = MLKV_DEFAULT_SEED, max_load: float = 0.75):
+        self.dim = int(dim)
+        self.capacity = int(capacity)
+        self.h = mlkv_open_ex(self.dim, self.capacity, seed, max_load)
+
+    def close(self):
+        if self.h:
+            mlkv_close(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def get(self, keys: torch.Tensor, out: torch.Tensor | None = None, stream=None):
+        _check(mlkv_get(self.h, keys, keys.numel(), out, stream))
+        return out
+
+    def put_grad(self, keys: torch.Tensor, grads: torch.Tensor, lr: float, eps: float, stream=None):
+        _check(mlkv_put_grad(self.h, keys, grads, keys.numel(), lr, eps, stream))
+
+    def sync(self, stream=None) -> int:
+        return mlkv_sync(self.h, stream)
+
+    @property
+    def size(self) -> int:
+        return mlkv_size(self.h)
+
+    @property
+    def num_slots(self) -> int:
+        return mlkv_num_slots(self.h)
+
+    def lookup_rows(self, keys: torch.Tensor, stream=None) -> torch.Tensor:
+        out = torch.empty(keys.numel(), dtype=torch.int64, device=keys.device)
+        _check(mlkv_lookup_rows(self.h, keys, keys.numel(), out, stream))
+        return out
+
+    def export(self, nrows: int | None = None, stream=None):
+        """(rows[nrows, dim], state[nrows], slot_keys[num_slots] int64, slot_rows[num_slots] int32)."""
+        if nrows is None:
+            nrows = self.size
+        dev = torch.device("cuda", torch.cuda.current_device())
+        rows = torch.empty((nrows, self.dim), dtype=torch.float32, device=dev)
+        st = torch.empty(nrows, dtype=torch.float32, device=dev)
+        ns = self.num_slots
+        sk = torch.empty(ns, dtype=torch.int64, device=dev)
+        sr = torch.empty(ns, dtype=torch.int32, device=dev)
+        _check(mlkv_export(self.h, nrows, rows, st, sk, sr, stream))
+        return rows, st, sk, sr

@@ -1,0 +1,142 @@
+"""Runs the GPU library and the CPU oracle side by side on identical inputs."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+from oracle import oracle as O
+from paper_2504_01506_amd import mlkv
+
+RTOL = 1e-5  # relative bound on updated rows and accumulators
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def dev_keys(k: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(k, dtype=np.uint64).view(np.int64)).cuda()
+
+
+def dev(a: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def row_scaled_err(a: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """|a - b| / max(|b|, max |b| over the row): the error measure for rows."""
+    scale = np.maximum(np.abs(b), np.max(np.abs(b), axis=-1, keepdims=True))
+    scale = np.where(scale == 0, 1.0, scale)
+    return np.abs(a.astype(np.float64) - b.astype(np.float64)) / scale
+
+
+def ulp_diff(a: np.ndarray, b: np.ndarray) -> int:
+    ia = a.astype(np.float32).view(np.int32).astype(np.int64)
+    ib = b.astype(np.float32).view(np.int32).astype(np.int64)
+    ia = np.where(ia < 0, -(ia & 0x7FFFFFFF), ia)
+    ib = np.where(ib < 0, -(ib & 0x7FFFFFFF), ib)
+    return int(np.max(np.abs(ia - ib))) if ia.size else 0
+
+
+class Pair:
+    """A GPU table and an oracle table that receive exactly the same calls."""
+
+    def __init__(self, dim, capacity, seed=mlkv.MLKV_DEFAULT_SEED, max_load=0.75, lazy_oracle=False):
+        self.dim = dim
+        self.gpu = mlkv.Table(dim, capacity, seed=seed, max_load=max_load)
+        self.ora = O.OracleTable(dim, capacity, seed=seed)
+        self.updated = set()      # rows written by put_grad at least once (oracle row ids)
+        self.stats = {"max_err": 0.0, "max_ulp": 0, "exact_mismatch": 0}
+
+    def close(self):
+        self.gpu.close()
+        self.ora.close()
+
+    def prefill(self, keys_sorted: np.ndarray, chunk: int = 1 << 16):
+        """Inserts ascending keys through get(out=NULL) in chunks on the GPU, and
+        as one sorted prefill in the oracle (identical rows: row = rank)."""
+        for s in range(0, keys_sorted.size, chunk):
+            k = dev_keys(keys_sorted[s:s + chunk])
+            self.gpu.get(k, None)
+        assert self.gpu.sync() == mlkv.MLKV_OK
+        assert self.ora.prefill_sorted(keys_sorted) == O.OK
+        assert self.gpu.size == self.ora.size == keys_sorted.size
+
+    def get(self, keys: np.ndarray, check: bool = True):
+        k = dev_keys(keys)
+        out = torch.empty((keys.size, self.dim), dtype=torch.float32, device="cuda")
+        self.gpu.get(k, out)
+        rc, want = self.ora.get(keys)
+        assert rc == O.OK
+        assert self.gpu.sync() == mlkv.MLKV_OK
+        got = out.cpu().numpy()
+        if check:
+            self.compare_get(keys, got, want)
+        return got, want
+
+    def compare_get(self, keys, got, want):
+        rows = self.ora.lookup_rows(keys)
+        fresh = np.array([r not in self.updated for r in rows.tolist()], dtype=bool)
+        # rows never updated: bit-exact
+        if fresh.any():
+            bad = ~np.all(got[fresh].view(np.uint32) == want[fresh].view(np.uint32), axis=1)
+            assert not bad.any(), f"{int(bad.sum())} never-updated rows differ"
+        if (~fresh).any():
+            err = row_scaled_err(got[~fresh], want[~fresh])
+            self.stats["max_err"] = max(self.stats["max_err"], float(err.max()))
+            self.stats["max_ulp"] = max(self.stats["max_ulp"], ulp_diff(got[~fresh], want[~fresh]))
+            self.stats["exact_mismatch"] += int(np.sum(got[~fresh].view(np.uint32) != want[~fresh].view(np.uint32)))
+            assert err.max() <= RTOL, f"updated rows differ: max row-scaled error {err.max():.3e}"
+
+    def put(self, keys: np.ndarray, grads: np.ndarray, lr: float, eps: float):
+        self.gpu.put_grad(dev_keys(keys), dev(grads), lr, eps)
+        assert self.ora.put_grad(keys, grads, lr, eps) == O.OK
+        assert self.gpu.sync() == mlkv.MLKV_OK
+        self.updated.update(self.ora.lookup_rows(keys).tolist())
+
+    def compare_rows(self, rows: np.ndarray | None = None):
+        """Key->row bit-exact for the keys of `rows`; row values and accumulators
+        within RTOL (bit-exact for never-updated rows)."""
+        size = self.ora.size
+        assert self.gpu.size == size
+        if rows is None:
+            rows = np.arange(size, dtype=np.int64)
+        keys = self.ora.row_keys(rows)
+        got_rows = self.gpu.lookup_rows(dev_keys(keys)).cpu().numpy()
+        assert np.array_equal(got_rows, rows), "key -> row differs"
+        w_all, st_all, _, _ = self.gpu.export(size)
+        w = w_all[torch.from_numpy(rows).cuda()].cpu().numpy()
+        st = st_all[torch.from_numpy(rows).cuda()].cpu().numpy()
+        want_w, want_st = self.ora.read_rows(rows)
+        fresh = np.array([r not in self.updated for r in rows.tolist()], dtype=bool)
+        if fresh.any():
+            assert np.array_equal(w[fresh].view(np.uint32), want_w[fresh].view(np.uint32))
+            assert np.all(st[fresh] == 0) and np.all(want_st[fresh] == 0)
+        if (~fresh).any():
+            err = row_scaled_err(w[~fresh], want_w[~fresh])
+            assert err.max() <= RTOL, f"rows differ: {err.max():.3e}"
+            st_err = np.abs(st[~fresh].astype(np.float64) - want_st[~fresh]) / np.maximum(np.abs(want_st[~fresh]), 1e-30)
+            assert st_err.max() <= RTOL, f"accumulators differ: {st_err.max():.3e}"
+            self.stats["max_err"] = max(self.stats["max_err"], float(err.max()))
+            self.stats["max_ulp"] = max(self.stats["max_ulp"], ulp_diff(w[~fresh], want_w[~fresh]))
+
+    def check_index(self):
+        """Index invariants: each key in exactly one slot, rows a permutation of
+        [0, size), no pending rows, every stored key found by lookup."""
+        size = self.gpu.size
+        _, _, sk, sr = self.gpu.export(0)
+        sk = sk.cpu().numpy().view(np.uint64)
+        sr = sr.cpu().numpy().view(np.uint32)
+        used = sk != np.uint64(mlkv.MLKV_RESERVED_KEY)
+        keys = sk[used]
+        rows = sr[used].astype(np.int64)
+        assert keys.size == size
+        assert np.unique(keys).size == keys.size, "a key occupies two slots"
+        assert np.array_equal(np.sort(rows), np.arange(size)), "rows are not a permutation of [0, size)"
+        assert np.all(sr[~used] == 0xFFFFFFFF)
+        found = self.gpu.lookup_rows(dev_keys(keys)).cpu().numpy()
+        assert np.array_equal(found, rows), "a stored key is not reachable on its probe path"
+        want = self.ora.lookup_rows(keys)
+        assert np.array_equal(want, rows), "key -> row differs from the oracle"
