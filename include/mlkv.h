@@ -113,6 +113,20 @@ int mlkv_lookup_rows(mlkv_table *t, const uint64_t *d_keys, int64_t n, int64_t *
 int mlkv_export(mlkv_table *t, int64_t nrows, float *d_rows_out, float *d_state_out,
                 uint64_t *d_slot_keys_out, uint32_t *d_slot_rows_out, void *hip_stream);
 
+/* ---- per-kernel timing (benchmarks) ----
+ * The library runs MLKV_NUM_KERNELS kernels: 0 get_probe_gather and
+ * 1 assign_new for mlkv_get, 2 put_probe and 3 reduce_update for
+ * mlkv_put_grad. While enabled, HIP events are recorded on the call's stream
+ * before and after every launch. mlkv_profile_read waits for the recorded
+ * launches, writes per-kernel sums of their durations (ms) and launch counts
+ * into the host arrays total_ms[MLKV_NUM_KERNELS] and
+ * launches[MLKV_NUM_KERNELS], and forgets them. */
+#define MLKV_NUM_KERNELS 4
+int mlkv_profile_enable(mlkv_table *t, int enable);
+int mlkv_profile_read(mlkv_table *t, double *total_ms, int64_t *launches);
+/* Name of kernel `kernel` (0 <= kernel < MLKV_NUM_KERNELS), else NULL. */
+const char *mlkv_kernel_name(int kernel);
+
 #ifdef __cplusplus
 }
 #endif

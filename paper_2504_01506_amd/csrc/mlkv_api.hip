@@ -5,6 +5,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <string>
+#include <vector>
 
 #include "mlkv.h"
 #include "mlkv_kernels.h"
@@ -35,6 +36,16 @@ struct mlkv_table {
   uint32_t* meta = nullptr;
   uint64_t* spill = nullptr;
   uint64_t spill_words = 0;
+
+  // optional per-launch timing: HIP events recorded around each kernel
+  struct ProfRec {
+    int kernel;
+    hipEvent_t start, stop;
+  };
+  bool prof_on = false;
+  std::vector<ProfRec> prof_recs;
+  std::vector<hipEvent_t> prof_pool;
+  hipEvent_t prof_open[K_COUNT] = {};
 };
 
 namespace {
@@ -107,6 +118,51 @@ int check_table(mlkv_table* t) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+hipEvent_t prof_event(mlkv_table* t) {
+  if (!t->prof_pool.empty()) {
+    hipEvent_t e = t->prof_pool.back();
+    t->prof_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+void prof_hook(void* ctx, int kernel, int phase, hipStream_t st) {
+  mlkv_table* t = static_cast<mlkv_table*>(ctx);
+  hipEvent_t e = prof_event(t);
+  if (e == nullptr) return;
+  (void)hipEventRecord(e, st);
+  if (phase == 0) {
+    t->prof_open[kernel] = e;
+  } else if (t->prof_open[kernel] != nullptr) {
+    t->prof_recs.push_back({kernel, t->prof_open[kernel], e});
+    t->prof_open[kernel] = nullptr;
+  } else {
+    t->prof_pool.push_back(e);
+  }
+}
+
+LaunchHook hook_of(mlkv_table* t) {
+  LaunchHook h;
+  if (t->prof_on) {
+    h.fn = prof_hook;
+    h.ctx = t;
+  }
+  return h;
+}
+
+void prof_release(mlkv_table* t) {
+  for (auto& r : t->prof_recs) {
+    (void)hipEventDestroy(r.start);
+    (void)hipEventDestroy(r.stop);
+  }
+  for (auto e : t->prof_pool) (void)hipEventDestroy(e);
+  t->prof_recs.clear();
+  t->prof_pool.clear();
+}
+
 }  // namespace
 
 extern "C" {
@@ -177,6 +233,7 @@ void mlkv_close(mlkv_table* t) {
   (void)hipSetDevice(t->device);
   (void)hipDeviceSynchronize();
   free_workspace(t);
+  prof_release(t);
   (void)hipFree(t->idx);
   (void)hipFree(t->rows);
   (void)hipFree(t->state);
@@ -207,7 +264,7 @@ int mlkv_get(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, voi
   a.ctrl = t->ctrl;
   a.epoch = t->epoch;
   const bool vec4 = (t->dim % 4 == 0) && (d_out == nullptr || aligned16(d_out));
-  hipError_t e = launch_get(a, vec4, static_cast<hipStream_t>(hip_stream));
+  hipError_t e = launch_get(a, vec4, static_cast<hipStream_t>(hip_stream), hook_of(t));
   if (e != hipSuccess) return hip_fail(e, "mlkv_get launch");
   t->epoch++;
   return MLKV_OK;
@@ -223,10 +280,10 @@ int mlkv_put_grad(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, i
   if (n == 0) return MLKV_OK;
   if (d_keys == nullptr || d_grads == nullptr) return fail(MLKV_EINVAL, "keys or grads is NULL");
   if ((rc = ensure_workspace(t, n)) != MLKV_OK) return rc;
-  // partitions: about 256 entries each, a power of two, at most kMaxParts
+  // partitions: about 512 entries each, a power of two, at most kMaxParts
   const uint32_t slot_bits = t->nb_log2 + 3;
   uint32_t pb = 0;
-  while (pb < 12 && ((int64_t)256 << (pb + 1)) <= n + (n >> 1)) ++pb;
+  while (pb < 12 && ((int64_t)512 << (pb + 1)) <= n + (n >> 1)) ++pb;
   if (pb > slot_bits) pb = slot_bits;
   PutArgs a;
   a.idx = t->idx;
@@ -252,7 +309,7 @@ int mlkv_put_grad(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, i
   a.ctrl = t->ctrl;
   a.epoch = t->epoch;
   const bool vec4 = (t->dim % 4 == 0) && aligned16(d_grads);
-  hipError_t e = launch_put(a, vec4, static_cast<hipStream_t>(hip_stream));
+  hipError_t e = launch_put(a, vec4, static_cast<hipStream_t>(hip_stream), hook_of(t));
   if (e != hipSuccess) return hip_fail(e, "mlkv_put_grad launch");
   t->epoch++;
   return MLKV_OK;
@@ -328,6 +385,40 @@ int mlkv_export(mlkv_table* t, int64_t nrows, float* d_rows_out, float* d_state_
     e = launch_export_slots(t->idx, t->nb * kSlots, d_slot_keys_out, d_slot_rows_out, st);
   if (e != hipSuccess) return hip_fail(e, "mlkv_export");
   return MLKV_OK;
+}
+
+int mlkv_profile_enable(mlkv_table* t, int enable) {
+  if (t == nullptr) return fail(MLKV_EINVAL, "table is NULL");
+  t->prof_on = enable != 0;
+  return MLKV_OK;
+}
+
+int mlkv_profile_read(mlkv_table* t, double* total_ms, int64_t* launches) {
+  int rc = check_table(t);
+  if (rc) return rc;
+  if (total_ms == nullptr || launches == nullptr) return fail(MLKV_EINVAL, "NULL output");
+  for (int k = 0; k < K_COUNT; ++k) {
+    total_ms[k] = 0.0;
+    launches[k] = 0;
+  }
+  for (auto& r : t->prof_recs) {
+    hipError_t e = hipEventSynchronize(r.stop);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    float ms = 0.0f;
+    e = hipEventElapsedTime(&ms, r.start, r.stop);
+    if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+    total_ms[r.kernel] += ms;
+    launches[r.kernel] += 1;
+    t->prof_pool.push_back(r.start);
+    t->prof_pool.push_back(r.stop);
+  }
+  t->prof_recs.clear();
+  return MLKV_OK;
+}
+
+const char* mlkv_kernel_name(int kernel) {
+  static const char* names[K_COUNT] = {"get_probe_gather", "assign_new", "put_probe", "reduce_update"};
+  return (kernel >= 0 && kernel < K_COUNT) ? names[kernel] : nullptr;
 }
 
 }  // extern "C"

@@ -32,8 +32,9 @@ struct Ctrl {
   unsigned long long bad_epoch;       // epoch of a call that met the reserved key
   unsigned long long overflow_epoch;  // epoch of a call whose inserts overran the probe bound
   unsigned long long spill_next;      // bump allocator for partitions larger than LDS
+  unsigned long long new_epoch;       // epoch of a call that inserted at least one key
   int latched;                        // first device-side error since mlkv_sync
-  unsigned int pad[9];
+  unsigned int pad[7];
 };
 
 // ---------------------------------------------------------------------------

@@ -13,8 +13,19 @@ constexpr int kGetTile = 256;    // keys per probe_gather block (one per lane)
 constexpr int kPutTile = 1024;   // keys per put_probe block (one per lane)
 constexpr int kMaxParts = 4096;  // partitions (MSD digits) per put call
 constexpr int kRedThreads = 512; // threads of a reduce_update block
-constexpr int kRedCap = 2048;    // partition entries held in LDS
-constexpr int kLongSeg = 32;     // segments longer than this are split over the block
+constexpr int kRedCap = 4096;    // partition entries held in LDS
+
+// Kernels of the library, for per-launch timing.
+enum KernelId : int { K_GET_PROBE_GATHER = 0, K_ASSIGN_NEW = 1, K_PUT_PROBE = 2, K_REDUCE_UPDATE = 3, K_COUNT = 4 };
+
+// Optional callback around each launch (phase 0 before, 1 after), on the launch stream.
+struct LaunchHook {
+  void (*fn)(void* ctx, int kernel, int phase, hipStream_t st) = nullptr;
+  void* ctx = nullptr;
+  void operator()(int kernel, int phase, hipStream_t st) const {
+    if (fn) fn(ctx, kernel, phase, st);
+  }
+};
 
 struct GetArgs {
   Bucket* idx;
@@ -58,8 +69,8 @@ struct PutArgs {
   uint64_t epoch;
 };
 
-hipError_t launch_get(const GetArgs& a, bool vec4, hipStream_t st);
-hipError_t launch_put(const PutArgs& a, bool vec4, hipStream_t st);
+hipError_t launch_get(const GetArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook);
+hipError_t launch_put(const PutArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook);
 hipError_t launch_lookup(Bucket* idx, uint32_t nb_log2, const uint64_t* keys, int64_t n,
                          int64_t* rows_out, hipStream_t st);
 hipError_t launch_export_slots(const Bucket* idx, uint64_t nslots, uint64_t* keys_out,

@@ -108,6 +108,7 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
   if (pr.status == P_NEW_MINE) {
     const uint32_t j = atomicAdd(&s_cnt, 1u);
     newlist[base + j] = NewKey{key, pr.slot, 0u};
+    ctrl->new_epoch = epoch;
   }
   if (out != nullptr) {
     const uint64_t s0 = splitmix_mix(key ^ seed);
@@ -212,8 +213,9 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
   __shared__ uint32_t s_slot[kAssignMine];
   __shared__ uint32_t s_rank[kAssignMine];
 
-  const uint64_t M = count_new_keys<NT>(tile_cnt, ntiles, s_w64);
   const uint64_t size0 = ctrl->size[epoch & 1];
+  const bool any_new = ctrl->new_epoch == epoch;
+  const uint64_t M = any_new ? count_new_keys<NT>(tile_cnt, ntiles, s_w64) : 0ull;
   const int err = call_verdict(ctrl, epoch, size0, M, capacity);
   if (M == 0) return;
 
@@ -290,12 +292,28 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
 }
 
 // ===========================================================================
-// Put, first kernel: probe (+ insert) and partition the tile's (slot, pos)
-// pairs by the top bits of the slot (one MSD radix digit), in LDS.
+// Put. The (key position) pairs of a call flow through "items":
+//   bit 63     1 if the key is inserted by this call (row not yet known)
+//   bits 31-62 the key's row, or its index slot when bit 63 is set
+//   bits 0-30  the position of the key in the batch
+// Sorting items therefore groups the positions of each key, in ascending
+// order, and puts the keys new in this call last.
 // ===========================================================================
+__device__ __forceinline__ uint64_t make_item(bool fresh, uint32_t tag, uint32_t pos) {
+  return ((uint64_t)(fresh ? 1u : 0u) << 63) | ((uint64_t)tag << 31) | (uint64_t)pos;
+}
+__device__ __forceinline__ uint32_t item_pos(uint64_t it) { return (uint32_t)(it & 0x7FFFFFFFull); }
+__device__ __forceinline__ uint32_t item_tag(uint64_t it) { return (uint32_t)(it >> 31); }
+__device__ __forceinline__ bool item_fresh(uint64_t it) { return (it >> 63) != 0; }
+__device__ __forceinline__ uint64_t item_group(uint64_t it) { return it >> 31; }
+
+// ---------------------------------------------------------------------------
+// Put, first kernel: probe (+ insert) each key and partition the tile's items
+// by the top bits of the key's slot (one MSD radix digit), in LDS.
+// ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kPutTile) void k_put_probe(
     Bucket* __restrict__ idx, uint32_t nb_log2, const uint64_t* __restrict__ keys, int64_t n,
-    int shift, int NP, uint64_t* __restrict__ items, uint32_t* __restrict__ meta,
+    int shift, int NP, int ntiles, uint64_t* __restrict__ items, uint32_t* __restrict__ meta,
     NewKey* __restrict__ newlist, uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch) {
   constexpr int NT = kPutTile;
   __shared__ uint32_t s_hist[kMaxParts];
@@ -330,6 +348,7 @@ __global__ __launch_bounds__(kPutTile) void k_put_probe(
   if (pr.status == P_NEW_MINE) {
     const uint32_t j = atomicAdd(&s_cnt, 1u);
     newlist[(size_t)tile * NT + j] = NewKey{key, pr.slot, 0u};
+    ctrl->new_epoch = epoch;
   }
   __syncthreads();
 
@@ -349,7 +368,7 @@ __global__ __launch_bounds__(kPutTile) void k_put_probe(
   for (int j = 0; j < PER; ++j) {
     const int dd = tid * PER + j;
     offs[j] = off;
-    if (dd < NP) meta[(size_t)tile * NP + dd] = off | (c[j] << 16);
+    if (dd < NP) meta[(size_t)dd * ntiles + tile] = off | (c[j] << 16);
     off += c[j];
   }
   __syncthreads();
@@ -359,33 +378,35 @@ __global__ __launch_bounds__(kPutTile) void k_put_probe(
     if (dd < NP) s_hist[dd] = offs[j];
   }
   __syncthreads();
-  if (item) items[(size_t)tile * NT + s_hist[d] + r] = ((uint64_t)pr.slot << 32) | (uint32_t)i;
+  if (item) {
+    const bool fresh = pr.status != P_HIT;
+    items[(size_t)tile * NT + s_hist[d] + r] = make_item(fresh, fresh ? pr.slot : pr.row, (uint32_t)i);
+  }
   if (tid == 0) tile_cnt[tile] = s_cnt;
 }
 
-// ===========================================================================
-// Put, second kernel: one block per partition. Gathers the partition's
-// (slot, pos) pairs, sorts them, run-length encodes them into segments (one
-// per distinct key, positions ascending), sums each segment's gradient rows in
-// fp64 and applies one row-wise Adagrad step to the key's row.
-// ===========================================================================
+// ---------------------------------------------------------------------------
+// Put, second kernel: one block per partition. Gathers the partition's items,
+// sorts them, run-length encodes them into segments (one per distinct key,
+// positions ascending), sums each segment's gradient rows in fp64 and applies
+// one row-wise Adagrad step to the key's row.
+// ---------------------------------------------------------------------------
 template <class M>
 struct SegmentOps {
   static constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
   using V = typename VecT<VEC>::T;
   static constexpr int UNR = (K * VEC >= 8) ? 4 : 8;
 
-  // acc += grads rows of sorted entries [b, e) (positions in the low 32 bits)
-  static __device__ __forceinline__ void accumulate(double (&acc)[K][VEC], const uint64_t* it,
-                                                    uint32_t b, uint32_t e,
+  // acc += gradient rows of the sorted items [b, e)
+  template <class IP>
+  static __device__ __forceinline__ void accumulate(double (&acc)[K][VEC], IP it, uint32_t b, uint32_t e,
                                                     const float* __restrict__ grads, int D, int q) {
     for (uint32_t j = b; j < e; j += UNR) {
       V v[UNR][K];
 #pragma unroll
       for (int u = 0; u < UNR; ++u) {
         if (j + u < e) {
-          const uint32_t pos = (uint32_t)it[j + u];
-          const float* g = grads + (size_t)pos * (size_t)D;
+          const float* g = grads + (size_t)item_pos(it[j + u]) * (size_t)D;
 #pragma unroll
           for (int k = 0; k < K; ++k) {
             const int col = (k * LPR + q) * VEC;
@@ -460,224 +481,360 @@ struct SegmentOps {
     }
     if (q == 0) state[row] = Gn;
   }
-};
 
-template <class M>
-__global__ __launch_bounds__(kRedThreads) void k_reduce_update(
-    Bucket* __restrict__ idx, const uint64_t* __restrict__ items, const uint32_t* __restrict__ meta,
-    int ntiles, int NP, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
-    const float* __restrict__ grads, float* __restrict__ rows, float* __restrict__ state, int D,
-    uint64_t seed, float lr, float eps, int64_t capacity, Ctrl* ctrl, uint64_t epoch,
-    uint64_t* __restrict__ spill, uint64_t spill_words) {
-  constexpr int NT = kRedThreads;
-  constexpr int NW = NT / 64;
-  using Ops = SegmentOps<M>;
-  constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
-  constexpr int NG = NW * RPW;  // lane groups per block
-  using V = typename VecT<VEC>::T;
-
-  extern __shared__ double s_dyn[];  // partial sums [NG][D] or a key chunk [kChunk]
-  __shared__ uint64_t s_items[kRedCap];
-  __shared__ uint32_t s_seg[kRedCap + 1];
-  __shared__ uint32_t s_row[kRedCap];
-  __shared__ uint32_t s_pref[NT + 1];
-  __shared__ uint32_t s_w[NW];
-  __shared__ unsigned long long s_w64[NW];
-  __shared__ uint64_t s_spill_base;
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int g = lane / LPR;
-  const int q = lane % LPR;
-  const int gid = wave * RPW + g;
-  const int leader = g * LPR;
-  const uint32_t p = blockIdx.x;
-
-  const uint64_t Mnew = count_new_keys<NT>(tile_cnt, ntiles, s_w64);
-  const uint64_t size0 = ctrl->size[epoch & 1];
-  const int err = call_verdict(ctrl, epoch, size0, Mnew, capacity);
-
-  // size of this partition
-  uint64_t mp64 = 0;
-  for (int t = tid; t < ntiles; t += NT) mp64 += meta[(size_t)t * NP + p] >> 16;
-  const uint32_t mp = (uint32_t)block_sum_u64<NT>(mp64, s_w64);
-  if (mp == 0) return;
-
-  if (err) {
-    if (Mnew == 0) return;
-    // roll back keys this call inserted whose slots fall in this partition
-    for (int t = tid; t < ntiles; t += NT) {
-      const uint32_t mt = meta[(size_t)t * NP + p];
-      const uint32_t off = mt & 0xFFFFu, cnt = mt >> 16;
-      for (uint32_t j = 0; j < cnt; ++j) {
-        const uint32_t slot = (uint32_t)(items[(size_t)t * kPutTile + off + j] >> 32);
-        Bucket* B = idx + slot / kSlots;
-        if (B->row[slot % kSlots] == kPendingRow) B->key[slot % kSlots] = kEmptyKey;
-      }
-    }
-    return;
-  }
-
-  // ---- gather into LDS (or a global spill area when it does not fit) ----
-  uint32_t P2 = 1;
-  while (P2 < mp) P2 <<= 1;
-  const bool spilled = mp > (uint32_t)kRedCap;
-  uint64_t* it;
-  uint32_t* seg;
-  uint32_t* rowv;
-  if (spilled) {
-    if (tid == 0) {
-      const uint64_t need = 2ull * P2 + 2;
-      const uint64_t b = atomicAdd(&ctrl->spill_next, (unsigned long long)need);
-      s_spill_base = (b + need <= spill_words) ? b : ~0ull;
-    }
-    __syncthreads();
-    if (s_spill_base == ~0ull) {  // cannot happen when the spill area is sized 4n
-      if (tid == 0) atomicCAS(&ctrl->latched, 0, -4);
-      return;
-    }
-    it = spill + s_spill_base;
-    seg = reinterpret_cast<uint32_t*>(spill + s_spill_base + P2);
-    rowv = seg + P2 + 1;
-  } else {
-    it = s_items;
-    seg = s_seg;
-    rowv = s_row;
-  }
-  {
-    uint32_t base = 0;
-    for (int t0 = 0; t0 < ntiles; t0 += NT) {
-      const int t = t0 + tid;
-      const uint32_t mt = t < ntiles ? meta[(size_t)t * NP + p] : 0u;
-      const uint32_t off = mt & 0xFFFFu, cnt = mt >> 16;
-      uint32_t tot;
-      const uint32_t pre = block_exclusive_scan<NT>(cnt, s_w, &tot);
-      for (uint32_t j = 0; j < cnt; ++j) it[base + pre + j] = items[(size_t)t * kPutTile + off + j];
-      base += tot;
-    }
-    for (uint32_t j = mp + tid; j < P2; j += NT) it[j] = ~0ull;
-    __syncthreads();
-  }
-  block_bitonic_sort<NT>(it, P2);
-
-  // ---- run-length encode: segment starts ----
-  uint32_t S = 0;
-  for (uint32_t b0 = 0; b0 < mp; b0 += NT) {
-    const uint32_t j = b0 + tid;
-    const uint32_t head = (j < mp) && (j == 0 || (it[j] >> 32) != (it[j - 1] >> 32)) ? 1u : 0u;
-    uint32_t tot;
-    const uint32_t pre = block_exclusive_scan<NT>(head, s_w, &tot);
-    if (head) seg[S + pre] = j;
-    S += tot;
-  }
-  if (tid == 0) seg[S] = mp;
-  __syncthreads();
-
-  // ---- row of every segment; new keys of this call get their rows here ----
-  uint64_t* s_chunk = reinterpret_cast<uint64_t*>(s_dyn);
-  for (uint32_t s0 = 0; s0 < S; s0 += NT) {
-    const uint32_t s = s0 + tid;
-    uint32_t slot = 0, row = 0;
-    uint64_t key = 0;
-    if (s < S) {
-      slot = (uint32_t)(it[seg[s]] >> 32);
-      row = idx[slot / kSlots].row[slot % kSlots];
-    }
-    const uint32_t pend = (s < S && row == kPendingRow) ? 1u : 0u;
-    const uint64_t npend = block_sum_u64<NT>(pend, s_w64);
-    if (npend > 0) {
-      if (pend) key = idx[slot / kSlots].key[slot % kSlots];
-      uint32_t rank = 0;
-      for_each_new_key_chunk<NT>(newlist, tile_cnt, ntiles, kPutTile, s_pref, s_w, s_chunk,
-                                 [&](const uint64_t* ck, uint32_t cnt) {
-                                   if (pend)
-                                     for (uint32_t e = 0; e < cnt; ++e) rank += ck[e] < key ? 1u : 0u;
-                                 });
-      if (pend) {
-        row = (uint32_t)(size0 + rank);
-        idx[slot / kSlots].row[slot % kSlots] = row;
-      }
-    }
-    if (s < S) rowv[s] = row;
-  }
-  __syncthreads();
-
-  double* s_part = s_dyn;
-
-  // ---- long segments: every lane group of the block takes a slice ----
-  for (uint32_t s = 0; s < S; ++s) {
-    const uint32_t b = seg[s], e = seg[s + 1];
-    if (e - b <= (uint32_t)kLongSeg) continue;
-    const uint32_t len = e - b;
-    const uint32_t per = (len + NG - 1) / NG;
-    const uint32_t lb = min(e, b + gid * per), le = min(e, lb + per);
-    double acc[K][VEC];
+  static __device__ __forceinline__ void zero(double (&acc)[K][VEC]) {
 #pragma unroll
     for (int k = 0; k < K; ++k)
 #pragma unroll
       for (int x = 0; x < VEC; ++x) acc[k][x] = 0.0;
-    Ops::accumulate(acc, it, lb, le, grads, D, q);
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-      const int col = (k * LPR + q) * VEC;
-#pragma unroll
-      for (int x = 0; x < VEC; ++x)
-        if (col + x < D) s_part[(size_t)gid * D + col + x] = acc[k][x];
+  }
+};
+
+struct RedCtx {
+  Bucket* idx;
+  const float* grads;
+  float* rows;
+  float* state;
+  int D;
+  uint64_t seed;
+  float lr;
+  float eps;
+  uint64_t size0;
+};
+
+// Run-length encodes the sorted items: seg[s] = first item of segment s,
+// seg[S] = mp, sid[j] = segment of item j. Returns S (block-uniform).
+template <int NT, class IP, class SP, class DP>
+__device__ __forceinline__ uint32_t encode_segments(IP it, uint32_t mp, SP seg, DP sid, uint32_t* s_w) {
+  uint32_t S = 0;
+  for (uint32_t b0 = 0; b0 < mp; b0 += NT) {
+    const uint32_t j = b0 + threadIdx.x;
+    const uint32_t head = (j < mp) && (j == 0 || item_group(it[j]) != item_group(it[j - 1])) ? 1u : 0u;
+    uint32_t tot;
+    const uint32_t pre = block_exclusive_scan<NT>(head, s_w, &tot);
+    if (head) seg[S + pre] = j;
+    if (j < mp) sid[j] = S + pre + head - 1;
+    S += tot;
+  }
+  if (threadIdx.x == 0) seg[S] = mp;
+  __syncthreads();
+  return S;
+}
+
+// Keys first inserted by this call (their items sort last) get rows
+// size0 + rank among all new keys of the call; the row replaces the slot in
+// the segment's first item, whose "fresh" bit stays set.
+template <int NT, class IP, class SP>
+__device__ __forceinline__ void resolve_new_rows(IP it, SP seg, uint32_t S, uint32_t mp, const RedCtx& c,
+                                                 const NewKey* __restrict__ newlist,
+                                                 const uint32_t* __restrict__ tile_cnt, int ntiles,
+                                                 uint32_t* s_pref, uint32_t* s_w,
+                                                 unsigned long long* s_w64, uint64_t* s_chunk) {
+  if (!item_fresh(it[mp - 1])) return;  // block-uniform: no key of this partition is new
+  for (uint32_t s0 = 0; s0 < S; s0 += NT) {
+    const uint32_t s = s0 + threadIdx.x;
+    bool pend = false;
+    uint32_t slot = 0;
+    uint64_t x = 0;
+    if (s < S) {
+      x = it[seg[s]];
+      pend = item_fresh(x);
+      slot = item_tag(x);
     }
-    __syncthreads();
-    if (gid == 0) {
-      const uint32_t row = rowv[s];
-      const bool isnew = row >= size0;
-      uint64_t s0 = 0;
-      if (isnew) {
-        const uint32_t slot = (uint32_t)(it[b] >> 32);
-        s0 = splitmix_mix(idx[slot / kSlots].key[slot % kSlots] ^ seed);
+    const uint64_t npend = block_sum_u64<NT>(pend ? 1u : 0u, s_w64);
+    if (npend == 0) continue;
+    const uint64_t key = pend ? c.idx[slot / kSlots].key[slot % kSlots] : 0ull;
+    uint32_t rank = 0;
+    for_each_new_key_chunk<NT>(newlist, tile_cnt, ntiles, kPutTile, s_pref, s_w, s_chunk,
+                               [&](const uint64_t* ck, uint32_t cnt) {
+                                 if (pend)
+                                   for (uint32_t e = 0; e < cnt; ++e) rank += ck[e] < key ? 1u : 0u;
+                               });
+    if (pend) {
+      const uint32_t row = (uint32_t)(c.size0 + rank);
+      c.idx[slot / kSlots].row[slot % kSlots] = row;
+      it[seg[s]] = make_item(true, row, item_pos(x));
+      // the new row starts from its initial value and a zero accumulator
+      const uint64_t s0 = splitmix_mix(key ^ c.seed);
+      float* w = c.rows + (size_t)row * (size_t)c.D;
+      for (int col = 0; col < c.D; ++col) w[col] = init_elem(s0, col);
+      c.state[row] = 0.0f;
+    }
+  }
+  __syncthreads();
+}
+
+// Applies every segment. Each lane group takes an equal contiguous slice of
+// the sorted items and walks it in batches: the gradient rows of a batch and
+// the row / accumulator of every segment that ends in the batch are loaded
+// together, then segments are summed (fp64) and the ones that start in the
+// slice are updated. The piece of a segment that began before the slice goes
+// to s_part[group]; after a barrier, the group where a cut segment began adds
+// the pieces of the following groups in slice order and updates it.
+template <class M, int NT, class IP, class SP, class DP>
+__device__ __forceinline__ void apply_segments(IP it, SP seg, DP sid, uint32_t mp, const RedCtx& c,
+                                               double* s_part) {
+  using Ops = SegmentOps<M>;
+  constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
+  constexpr int NG = (NT / 64) * RPW;
+  constexpr int B = (K * VEC >= 8) ? 4 : 8;
+  using V = typename VecT<VEC>::T;
+  const int lane = threadIdx.x & 63;
+  const int g = lane / LPR;
+  const int q = lane % LPR;
+  const int gid = (threadIdx.x >> 6) * RPW + g;
+  const int leader = g * LPR;
+  const int D = c.D;
+
+  const uint32_t L = (mp + NG - 1) / NG;
+  const uint32_t lo = min(mp, (uint32_t)gid * L);
+  const uint32_t hi = min(mp, lo + L);
+
+  double acc[K][VEC];
+  Ops::zero(acc);
+  for (uint32_t j0 = lo; j0 < hi; j0 += B) {
+    V gv[B][K];
+    V wv[B][K];
+    float G0[B];
+    uint32_t sj[B];
+    bool ends[B], owned[B];
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const uint32_t j = j0 + u;
+      ends[u] = false;
+      owned[u] = false;
+      G0[u] = 0.0f;
+      if (j < hi) {
+        const uint64_t x = it[j];
+        sj[u] = sid[j];
+        const float* gr = c.grads + (size_t)item_pos(x) * (size_t)D;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const int col = (k * LPR + q) * VEC;
+          if (col < D) gv[u][k] = load_vec<VEC>(gr + col);
+        }
+        ends[u] = seg[sj[u] + 1] == j + 1;
+        owned[u] = seg[sj[u]] >= lo;
+        if (ends[u] && owned[u]) {
+          const uint32_t row = item_tag(it[seg[sj[u]]]);
+          Ops::load_w(wv[u], c.rows, row, false, 0, D, q);
+          G0[u] = c.state[row];
+        }
       }
-      V w[K];
-      Ops::load_w(w, rows, row, isnew, s0, D, q);
-      const float G0 = (q == 0 && !isnew) ? state[row] : 0.0f;
-      double tot[K][VEC];
+    }
 #pragma unroll
-      for (int k = 0; k < K; ++k)
+    for (int u = 0; u < B; ++u) {
+      const uint32_t j = j0 + u;
+      if (j < hi) {
 #pragma unroll
-        for (int x = 0; x < VEC; ++x) tot[k][x] = 0.0;
-      for (int h = 0; h < NG; ++h) {
+        for (int k = 0; k < K; ++k) {
+          const int col = (k * LPR + q) * VEC;
+          if (col < D) {
+#pragma unroll
+            for (int x = 0; x < VEC; ++x) acc[k][x] += (double)VecT<VEC>::get(gv[u][k], x);
+          }
+        }
+        if (ends[u]) {
+          if (owned[u]) {
+            Ops::adagrad(acc, wv[u], G0[u], c.rows, c.state, item_tag(it[seg[sj[u]]]), D, q, leader, c.lr,
+                         c.eps);
+          } else {
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              const int col = (k * LPR + q) * VEC;
+#pragma unroll
+              for (int x = 0; x < VEC; ++x)
+                if (col + x < D) s_part[(size_t)gid * D + col + x] = acc[k][x];
+            }
+          }
+          Ops::zero(acc);
+        }
+      }
+    }
+  }
+  // the slice ends inside a segment
+  uint32_t tail = 0xFFFFFFFFu;
+  if (lo < hi) {
+    const uint32_t sl = sid[hi - 1];
+    if (seg[sl + 1] > hi) {
+      if (seg[sl] >= lo) {
+        tail = sl;
+      } else {
 #pragma unroll
         for (int k = 0; k < K; ++k) {
           const int col = (k * LPR + q) * VEC;
 #pragma unroll
           for (int x = 0; x < VEC; ++x)
-            if (col + x < D) tot[k][x] += s_part[(size_t)h * D + col + x];
+            if (col + x < D) s_part[(size_t)gid * D + col + x] = acc[k][x];
         }
       }
-      Ops::adagrad(tot, w, G0, rows, state, row, D, q, leader, lr, eps);
+    }
+  }
+  __syncthreads();
+  if (tail != 0xFFFFFFFFu) {
+    const uint32_t end = seg[tail + 1];
+    for (uint32_t h = gid + 1; h < (uint32_t)NG && h * L < end; ++h) {
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const int col = (k * LPR + q) * VEC;
+#pragma unroll
+        for (int x = 0; x < VEC; ++x)
+          if (col + x < D) acc[k][x] += s_part[(size_t)h * D + col + x];
+      }
+    }
+    const uint32_t row = item_tag(it[seg[tail]]);
+    V w[K];
+    Ops::load_w(w, c.rows, row, false, 0, D, q);
+    const float G = c.state[row];
+    Ops::adagrad(acc, w, G, c.rows, c.state, row, D, q, leader, c.lr, c.eps);
+  }
+}
+
+// Partition larger than the block's LDS share: the same steps on a global
+// scratch area (bitonic sort in place).
+template <class M, int NT>
+__device__ __forceinline__ void reduce_partition_global(uint32_t p, uint32_t mp, const uint64_t* __restrict__ items,
+                                                     const uint32_t* __restrict__ meta, int ntiles,
+                                                     const RedCtx& c, const NewKey* __restrict__ newlist,
+                                                     const uint32_t* __restrict__ tile_cnt, Ctrl* ctrl,
+                                                     uint64_t* __restrict__ spill, uint64_t spill_words,
+                                                     double* s_part, uint32_t* s_pref, uint32_t* s_w,
+                                                     unsigned long long* s_w64, uint64_t* s_base) {
+  uint32_t P2 = 1;
+  while (P2 < mp) P2 <<= 1;
+  if (threadIdx.x == 0) {
+    const uint64_t need = 2ull * P2 + 2;
+    const uint64_t b = atomicAdd(&ctrl->spill_next, (unsigned long long)need);
+    *s_base = (b + need <= spill_words) ? b : ~0ull;
+  }
+  __syncthreads();
+  const uint64_t base = *s_base;
+  if (base == ~0ull) {  // cannot happen when the spill area holds 4n words
+    if (threadIdx.x == 0) atomicCAS(&ctrl->latched, 0, -4);
+    return;
+  }
+  uint64_t* it = spill + base;
+  uint32_t* seg = reinterpret_cast<uint32_t*>(spill + base + P2);
+  uint32_t* sid = seg + P2 + 1;
+  uint32_t dst = 0;
+  for (int t0 = 0; t0 < ntiles; t0 += NT) {
+    const int t = t0 + (int)threadIdx.x;
+    const uint32_t mt = t < ntiles ? meta[(size_t)p * ntiles + t] : 0u;
+    const uint32_t off = mt & 0xFFFFu, cnt = mt >> 16;
+    uint32_t tot;
+    const uint32_t pre = block_exclusive_scan<NT>(cnt, s_w, &tot);
+    for (uint32_t j = 0; j < cnt; ++j) it[dst + pre + j] = items[(size_t)t * kPutTile + off + j];
+    dst += tot;
+  }
+  for (uint32_t j = mp + threadIdx.x; j < P2; j += NT) it[j] = ~0ull;
+  __syncthreads();
+  block_bitonic_sort<NT>(it, P2);
+  const uint32_t S = encode_segments<NT>(it, mp, seg, sid, s_w);
+  resolve_new_rows<NT>(it, seg, S, mp, c, newlist, tile_cnt, ntiles, s_pref, s_w, s_w64,
+                       reinterpret_cast<uint64_t*>(s_part));
+  apply_segments<M, NT>(it, seg, sid, mp, c, s_part);
+}
+
+template <class M>
+__global__ __launch_bounds__(kRedThreads, (M::K * M::VEC >= 16) ? 2 : 4) void k_reduce_update(
+    Bucket* __restrict__ idx, const uint64_t* __restrict__ items, const uint32_t* __restrict__ meta,
+    int ntiles, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
+    const float* __restrict__ grads, float* __restrict__ rows, float* __restrict__ state, int D,
+    uint64_t seed, float lr, float eps, int64_t capacity, Ctrl* ctrl, uint64_t epoch,
+    uint64_t* __restrict__ spill, uint64_t spill_words) {
+  constexpr int NT = kRedThreads;
+  constexpr int NW = NT / 64;
+
+  extern __shared__ double s_dyn[];  // pieces of cut segments [lane groups][D], or a chunk of new keys
+  __shared__ uint64_t s_items[kRedCap];
+  __shared__ uint16_t s_sid[kRedCap];
+  __shared__ uint16_t s_seg[kRedCap + 1];
+  __shared__ uint32_t s_pref[NT + 1];
+  __shared__ uint32_t s_w[NW];
+  __shared__ unsigned long long s_w64[NW];
+  __shared__ uint64_t s_base;
+
+  const uint32_t p = blockIdx.x;
+  const int tid = threadIdx.x;
+  const uint64_t size0 = ctrl->size[epoch & 1];
+  const bool any_new = ctrl->new_epoch == epoch;
+  const uint32_t* pm = meta + (size_t)p * ntiles;
+
+  // entries of this partition in every tile
+  uint64_t mp64 = 0;
+  for (int t = tid; t < ntiles; t += NT) mp64 += pm[t] >> 16;
+  const uint32_t mp = (uint32_t)block_sum_u64<NT>(mp64, s_w64);
+
+  const uint64_t Mnew = any_new ? count_new_keys<NT>(tile_cnt, ntiles, s_w64) : 0ull;
+  const int err = call_verdict(ctrl, epoch, size0, Mnew, capacity);
+  if (mp == 0) return;
+  if (err) {
+    if (Mnew == 0) return;
+    // undo the insertions of this call whose slots fall in this partition
+    for (int t = tid; t < ntiles; t += NT) {
+      const uint32_t mt = pm[t];
+      const uint32_t off = mt & 0xFFFFu, cnt = mt >> 16;
+      for (uint32_t j = 0; j < cnt; ++j) {
+        const uint64_t x = items[(size_t)t * kPutTile + off + j];
+        if (item_fresh(x)) {
+          const uint32_t slot = item_tag(x);
+          idx[slot / kSlots].key[slot % kSlots] = kEmptyKey;
+        }
+      }
+    }
+    return;
+  }
+
+  const RedCtx c{idx, grads, rows, state, D, seed, lr, eps, size0};
+  if (mp > (uint32_t)kRedCap) {
+    reduce_partition_global<M, NT>(p, mp, items, meta, ntiles, c, newlist, tile_cnt, ctrl, spill, spill_words,
+                                   s_dyn, s_pref, s_w, s_w64, &s_base);
+    return;
+  }
+
+  // ---- gather the partition's items into LDS ----
+  {
+    uint32_t dst = 0;
+    for (int t0 = 0; t0 < ntiles; t0 += NT) {
+      const int t = t0 + tid;
+      const uint32_t mt = t < ntiles ? pm[t] : 0u;
+      const uint32_t off = mt & 0xFFFFu, cnt = mt >> 16;
+      uint32_t tot;
+      const uint32_t pre = block_exclusive_scan<NT>(cnt, s_w, &tot);
+      for (uint32_t j = 0; j < cnt; ++j) s_items[dst + pre + j] = items[(size_t)t * kPutTile + off + j];
+      dst += tot;
     }
     __syncthreads();
   }
 
-  // ---- short segments: one lane group each ----
-  for (uint32_t s = gid; s < S; s += NG) {
-    const uint32_t b = seg[s], e = seg[s + 1];
-    if (e - b > (uint32_t)kLongSeg) continue;
-    const uint32_t row = rowv[s];
-    const bool isnew = row >= size0;
-    uint64_t s0 = 0;
-    if (isnew) {
-      const uint32_t slot = (uint32_t)(it[b] >> 32);
-      s0 = splitmix_mix(idx[slot / kSlots].key[slot % kSlots] ^ seed);
+  // ---- sort (all items are distinct: positions are) ----
+  if (mp <= (uint32_t)NT) {
+    // rank = number of smaller items
+    const uint64_t v = tid < (int)mp ? s_items[tid] : ~0ull;
+    uint32_t rk = 0;
+    if (tid < (int)mp) {
+      uint32_t e = 0;
+      for (; e + 4 <= mp; e += 4) {
+        const uint64_t a0 = s_items[e], a1 = s_items[e + 1], a2 = s_items[e + 2], a3 = s_items[e + 3];
+        rk += (a0 < v ? 1u : 0u) + (a1 < v ? 1u : 0u) + (a2 < v ? 1u : 0u) + (a3 < v ? 1u : 0u);
+      }
+      for (; e < mp; ++e) rk += s_items[e] < v ? 1u : 0u;
     }
-    V w[K];
-    Ops::load_w(w, rows, row, isnew, s0, D, q);
-    const float G0 = (q == 0 && !isnew) ? state[row] : 0.0f;
-    double acc[K][VEC];
-#pragma unroll
-    for (int k = 0; k < K; ++k)
-#pragma unroll
-      for (int x = 0; x < VEC; ++x) acc[k][x] = 0.0;
-    Ops::accumulate(acc, it, b, e, grads, D, q);
-    Ops::adagrad(acc, w, G0, rows, state, row, D, q, leader, lr, eps);
+    __syncthreads();
+    if (tid < (int)mp) s_items[rk] = v;
+    __syncthreads();
+  } else {
+    uint32_t P2 = 1;
+    while (P2 < mp) P2 <<= 1;
+    for (uint32_t j = mp + tid; j < P2; j += NT) s_items[j] = ~0ull;
+    __syncthreads();
+    block_bitonic_sort<NT>(s_items, P2);
   }
+
+  const uint32_t S = encode_segments<NT>(s_items, mp, s_seg, s_sid, s_w);
+  resolve_new_rows<NT>(s_items, s_seg, S, mp, c, newlist, tile_cnt, ntiles, s_pref, s_w, s_w64,
+                       reinterpret_cast<uint64_t*>(s_dyn));
+  apply_segments<M, NT>(s_items, s_seg, s_sid, mp, c, s_dyn);
 }
 
 // ===========================================================================
@@ -711,17 +868,21 @@ __global__ __launch_bounds__(256) void k_export_slots(const Bucket* __restrict__
 // Launchers
 // ===========================================================================
 template <class M>
-static hipError_t launch_get_t(const GetArgs& a, hipStream_t st) {
+static hipError_t launch_get_t(const GetArgs& a, hipStream_t st, const LaunchHook& hook) {
   const int64_t ntiles = (a.n + kGetTile - 1) / kGetTile;
+  hook(K_GET_PROBE_GATHER, 0, st);
   hipLaunchKernelGGL(k_get_probe_gather<M>, dim3((unsigned)ntiles), dim3(kGetTile), 0, st, a.idx,
                      a.nb_log2, a.keys, a.n, a.out, a.rows, a.D, a.seed, a.newlist, a.tile_cnt, a.ctrl,
                      a.epoch);
+  hook(K_GET_PROBE_GATHER, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int grid = (int)std::min<int64_t>(ntiles, 256);
+  hook(K_ASSIGN_NEW, 0, st);
   hipLaunchKernelGGL(k_assign_new, dim3(grid), dim3(kAssignThreads), 0, st, a.idx, a.newlist,
                      a.tile_cnt, (int)ntiles, kGetTile, a.rows, a.state, a.D, a.seed, a.capacity,
                      a.ctrl, a.epoch);
+  hook(K_ASSIGN_NEW, 1, st);
   return hipGetLastError();
 }
 
@@ -733,11 +894,13 @@ static size_t reduce_dyn_bytes(int D) {
 }
 
 template <class M>
-static hipError_t launch_put_t(const PutArgs& a, hipStream_t st) {
+static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHook& hook) {
   const int64_t ntiles = (a.n + kPutTile - 1) / kPutTile;
+  hook(K_PUT_PROBE, 0, st);
   hipLaunchKernelGGL(k_put_probe, dim3((unsigned)ntiles), dim3(kPutTile), 0, st, a.idx, a.nb_log2,
-                     a.keys, a.n, a.shift, a.NP, a.items, a.meta, a.newlist, a.tile_cnt, a.ctrl,
-                     a.epoch);
+                     a.keys, a.n, a.shift, a.NP, (int)ntiles, a.items, a.meta, a.newlist, a.tile_cnt,
+                     a.ctrl, a.epoch);
+  hook(K_PUT_PROBE, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t dyn = reduce_dyn_bytes<M>(a.D);
@@ -748,10 +911,12 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st) {
     if (e != hipSuccess) return e;
     attr_set = true;
   }
+  hook(K_REDUCE_UPDATE, 0, st);
   hipLaunchKernelGGL(k_reduce_update<M>, dim3((unsigned)a.NP), dim3(kRedThreads), dyn, st, a.idx,
-                     a.items, a.meta, (int)ntiles, a.NP, a.newlist, a.tile_cnt, a.grads, a.rows,
+                     a.items, a.meta, (int)ntiles, a.newlist, a.tile_cnt, a.grads, a.rows,
                      a.state, a.D, a.seed, a.lr, a.eps, a.capacity, a.ctrl, a.epoch, a.spill,
                      a.spill_words);
+  hook(K_REDUCE_UPDATE, 1, st);
   return hipGetLastError();
 }
 
@@ -777,12 +942,12 @@ static hipError_t dispatch_map(int D, bool vec4, F f) {
   return f(MapD1024{});
 }
 
-hipError_t launch_get(const GetArgs& a, bool vec4, hipStream_t st) {
-  return dispatch_map(a.D, vec4, [&](auto m) { return launch_get_t<decltype(m)>(a, st); });
+hipError_t launch_get(const GetArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook) {
+  return dispatch_map(a.D, vec4, [&](auto m) { return launch_get_t<decltype(m)>(a, st, hook); });
 }
 
-hipError_t launch_put(const PutArgs& a, bool vec4, hipStream_t st) {
-  return dispatch_map(a.D, vec4, [&](auto m) { return launch_put_t<decltype(m)>(a, st); });
+hipError_t launch_put(const PutArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook) {
+  return dispatch_map(a.D, vec4, [&](auto m) { return launch_put_t<decltype(m)>(a, st, hook); });
 }
 
 hipError_t launch_lookup(Bucket* idx, uint32_t nb_log2, const uint64_t* keys, int64_t n, int64_t* rows_out,

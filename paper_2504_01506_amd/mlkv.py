@@ -18,8 +18,7 @@ MLKV_OK, MLKV_EINVAL, MLKV_EFULL, MLKV_ENOMEM, MLKV_EDEVICE = 0, -1, -2, -3, -4
 MLKV_DEFAULT_SEED = 0x4D4C4B56
 MLKV_RESERVED_KEY = 0xFFFFFFFFFFFFFFFF
 
-EXPORTS = ("mlkv_open", "mlkv_open_ex", "mlkv_get", "mlkv_put_grad", "mlkv_sync", "mlkv_size",
-           "mlkv_num_slots", "mlkv_close", "mlkv_last_error", "mlkv_lookup_rows", "mlkv_export")
+MLKV_NUM_KERNELS = 4
 
 _lib = None
 
@@ -53,6 +52,9 @@ def load() -> ctypes.CDLL:
         "mlkv_last_error": (ctypes.c_char_p, []),
         "mlkv_lookup_rows": (INT, [P, P, I64, P, P]),
         "mlkv_export": (INT, [P, I64, P, P, P, P, P]),
+        "mlkv_profile_enable": (INT, [P, INT]),
+        "mlkv_profile_read": (INT, [P, P, P]),
+        "mlkv_kernel_name": (ctypes.c_char_p, [INT]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -148,6 +150,23 @@ def mlkv_export(t: int, nrows: int, rows_out=None, state_out=None, slot_keys_out
                 slot_rows_out=None, stream=None) -> int:
     return load().mlkv_export(t, nrows, _ptr(rows_out), _ptr(state_out), _ptr(slot_keys_out),
                               _ptr(slot_rows_out), _stream(stream))
+
+
+def mlkv_profile_enable(t: int, enable: bool) -> int:
+    return load().mlkv_profile_enable(t, 1 if enable else 0)
+
+
+def mlkv_profile_read(t: int):
+    """{kernel name: (total ms, launches)} of the launches since the last read."""
+    ms = (ctypes.c_double * MLKV_NUM_KERNELS)()
+    cnt = (ctypes.c_int64 * MLKV_NUM_KERNELS)()
+    _check(load().mlkv_profile_read(t, ms, cnt))
+    return {mlkv_kernel_name(k): (ms[k], cnt[k]) for k in range(MLKV_NUM_KERNELS)}
+
+
+def mlkv_kernel_name(kernel: int) -> str:
+    r = load().mlkv_kernel_name(kernel)
+    return r.decode() if r else None
 
 
 # ---- a small object wrapper over the same calls -----------------------------
