@@ -66,7 +66,7 @@ mlkv_table *mlkv_open_ex(int32_t dim, int64_t capacity, uint64_t seed, float max
  *     t = (int32)(h >> 40) - 2^23,  h = mix64(mix64(key ^ seed) + c * 0x9E3779B97F4A7C15)
  *     value = (float)t * (0.01f * 2^-23)          (uniform on [-0.01, 0.01))
  * with mix64 the SplitMix64 output function. d_out may be NULL (insert only).
- * n may be 0. d_keys: n uint64 keys. d_out: n*dim floats, row-major. */
+ * 0 <= n <= 2^31 - 1. d_keys: n uint64 keys. d_out: n*dim floats, row-major. */
 int mlkv_get(mlkv_table *t, const uint64_t *d_keys, int64_t n, float *d_out, void *hip_stream);
 
 /* Rmw (Sec. III-B, step 8) with row-wise Adagrad as the modify function:
@@ -78,7 +78,7 @@ int mlkv_get(mlkv_table *t, const uint64_t *d_keys, int64_t n, float *d_out, voi
  *     w[c] -= lr * (g[c] / den)     (separate fp32 operations)
  *     G     = G'
  * G starts at 0 for every row. d_grads: n*dim floats, row-major.
- * lr and eps must be finite, eps >= 0. */
+ * 0 <= n <= 2^30 - 1; lr and eps must be finite, eps >= 0. */
 int mlkv_put_grad(mlkv_table *t, const uint64_t *d_keys, const float *d_grads, int64_t n,
                   float lr, float eps, void *hip_stream);
 
@@ -101,7 +101,8 @@ const char *mlkv_last_error(void);
 
 /* ---- inspection (tests and debugging; asynchronous on hip_stream) ---- */
 
-/* d_rows_out[i] = row of d_keys[i] or -1 if absent; never inserts. */
+/* d_rows_out[i] = row of d_keys[i] or -1 if absent; never inserts.
+ * 0 <= n <= 2^31 - 1. */
 int mlkv_lookup_rows(mlkv_table *t, const uint64_t *d_keys, int64_t n, int64_t *d_rows_out,
                      void *hip_stream);
 

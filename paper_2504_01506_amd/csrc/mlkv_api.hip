@@ -36,6 +36,7 @@ struct mlkv_table {
   uint32_t* meta = nullptr;
   uint64_t* spill = nullptr;
   uint64_t spill_words = 0;
+  double* partials = nullptr;
 
   // optional per-launch timing: HIP events recorded around each kernel
   struct ProfRec {
@@ -75,6 +76,8 @@ void free_workspace(mlkv_table* t) {
   (void)hipFree(t->items);
   (void)hipFree(t->meta);
   (void)hipFree(t->spill);
+  (void)hipFree(t->partials);
+  t->partials = nullptr;
   t->newlist = nullptr;
   t->tile_cnt = nullptr;
   t->items = nullptr;
@@ -100,7 +103,8 @@ int ensure_workspace(mlkv_table* t, int64_t n) {
       (e = dev_alloc(&t->tile_cnt, sizeof(uint32_t) * (size_t)get_tiles)) != hipSuccess ||
       (e = dev_alloc(&t->items, sizeof(uint64_t) * (size_t)want)) != hipSuccess ||
       (e = dev_alloc(&t->meta, sizeof(uint32_t) * (size_t)kMaxParts * (size_t)put_tiles)) != hipSuccess ||
-      (e = dev_alloc(&t->spill, sizeof(uint64_t) * (size_t)spill_words)) != hipSuccess) {
+      (e = dev_alloc(&t->spill, sizeof(uint64_t) * (size_t)spill_words)) != hipSuccess ||
+      (e = dev_alloc(&t->partials, sizeof(double) * (size_t)want * (size_t)t->dim)) != hipSuccess) {
     free_workspace(t);
     return hip_fail(e, "scratch allocation");
   }
@@ -274,17 +278,16 @@ int mlkv_put_grad(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, i
                   float eps, void* hip_stream) {
   int rc = check_table(t);
   if (rc) return rc;
-  if (n < 0 || n > 0x7FFFFFFFll) return fail(MLKV_EINVAL, "n must be in [0, 2^31 - 1]");
+  if (n < 0 || n > 0x3FFFFFFFll) return fail(MLKV_EINVAL, "n must be in [0, 2^30 - 1]");
   if (!std::isfinite(lr)) return fail(MLKV_EINVAL, "lr must be finite");
   if (!std::isfinite(eps) || eps < 0.0f) return fail(MLKV_EINVAL, "eps must be finite and >= 0");
   if (n == 0) return MLKV_OK;
   if (d_keys == nullptr || d_grads == nullptr) return fail(MLKV_EINVAL, "keys or grads is NULL");
   if ((rc = ensure_workspace(t, n)) != MLKV_OK) return rc;
-  // partitions: about 512 entries each, a power of two, at most kMaxParts
-  const uint32_t slot_bits = t->nb_log2 + 3;
+  // partitions: about 128 keys each before in-tile merging, a power of two,
+  // at most kMaxParts
   uint32_t pb = 0;
-  while (pb < 12 && ((int64_t)512 << (pb + 1)) <= n + (n >> 1)) ++pb;
-  if (pb > slot_bits) pb = slot_bits;
+  while ((1 << (pb + 1)) <= kMaxParts && ((int64_t)128 << (pb + 1)) <= n + (n >> 1)) ++pb;
   PutArgs a;
   a.idx = t->idx;
   a.nb_log2 = t->nb_log2;
@@ -298,9 +301,9 @@ int mlkv_put_grad(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, i
   a.capacity = t->capacity;
   a.lr = lr;
   a.eps = eps;
-  a.shift = (int)(slot_bits - pb);
-  a.NP = 1 << pb;
+  a.pb = (int)pb;
   a.items = t->items;
+  a.partials = t->partials;
   a.meta = t->meta;
   a.newlist = t->newlist;
   a.tile_cnt = t->tile_cnt;

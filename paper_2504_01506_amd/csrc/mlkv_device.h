@@ -86,40 +86,63 @@ struct Probe {
   int status;
 };
 
+// First bucket of a key's probe chain (the bucket index), used to issue the
+// loads of several keys before examining any of them.
+__device__ __forceinline__ uint64_t home_bucket(uint64_t key, uint32_t nb_log2) {
+  return nb_log2 ? (index_hash(key) >> (64 - nb_log2)) : 0;
+}
+
+struct BucketView {
+  uint64_t k[8];
+  uint32_t r[8];
+};
+
+__device__ __forceinline__ BucketView load_bucket(const Bucket* B) {
+  BucketView v;
+  const ulonglong2* kp = reinterpret_cast<const ulonglong2*>(B->key);
+  const uint4* rp = reinterpret_cast<const uint4*>(B->row);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const ulonglong2 x = kp[q];
+    v.k[2 * q] = x.x;
+    v.k[2 * q + 1] = x.y;
+  }
+  const uint4 r0 = rp[0], r1 = rp[1];
+  v.r[0] = r0.x; v.r[1] = r0.y; v.r[2] = r0.z; v.r[3] = r0.w;
+  v.r[4] = r1.x; v.r[5] = r1.y; v.r[6] = r1.z; v.r[7] = r1.w;
+  return v;
+}
+
 // Linear probing over buckets. A bucket holding an EMPTY tag ends the chain.
 // Inserts claim the first EMPTY tag in chain order with a CAS; a failed CAS
 // returns the tag that is really there, so a stale view of the line never
 // produces a duplicate key (tags only ever go from EMPTY to a key in a call).
-__device__ __forceinline__ Probe probe_key(Bucket* __restrict__ idx, uint32_t nb_log2,
-                                           uint64_t key, bool insert) {
+// `v` is the already loaded view of bucket `b`, the key's home bucket.
+__device__ __forceinline__ Probe probe_with(Bucket* __restrict__ idx, uint32_t nb_log2, uint64_t key,
+                                            bool insert, uint64_t b, BucketView v) {
   const uint64_t mask = (nb_log2 >= 64) ? ~0ull : ((1ull << nb_log2) - 1);
-  uint64_t b = nb_log2 ? (index_hash(key) >> (64 - nb_log2)) : 0;
   const uint64_t limit = mask < (uint64_t)kMaxProbe ? mask + 1 : (uint64_t)kMaxProbe;
   for (uint64_t p = 0; p < limit; ++p) {
-    Bucket* B = idx + b;
-    const ulonglong2* kp = reinterpret_cast<const ulonglong2*>(B->key);
-    uint64_t k[kSlots];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const ulonglong2 v = kp[q];
-      k[2 * q] = v.x;
-      k[2 * q + 1] = v.y;
-    }
+    if (p > 0) v = load_bucket(idx + b);
     int hit = -1;
     bool has_empty = false;
 #pragma unroll
     for (int j = kSlots - 1; j >= 0; --j) {
-      if (k[j] == key) hit = j;
-      has_empty |= (k[j] == kEmptyKey);
+      if (v.k[j] == key) hit = j;
+      has_empty |= (v.k[j] == kEmptyKey);
     }
     if (hit >= 0) {
-      const uint32_t r = B->row[hit];
+      uint32_t r = v.r[0];
+#pragma unroll
+      for (int j = 1; j < kSlots; ++j)
+        if (hit == j) r = v.r[j];
       return {(uint32_t)(b * kSlots + hit), r, r == kPendingRow ? P_NEW_OTHER : P_HIT};
     }
     if (has_empty) {
       if (!insert) return {0, kPendingRow, P_ABSENT};
+      Bucket* B = idx + b;
       for (int j = 0; j < kSlots; ++j) {
-        if (k[j] != kEmptyKey) continue;
+        if (v.k[j] != kEmptyKey) continue;
         const uint64_t old = atomicCAS(reinterpret_cast<unsigned long long*>(&B->key[j]),
                                        (unsigned long long)kEmptyKey, (unsigned long long)key);
         if (old == kEmptyKey) return {(uint32_t)(b * kSlots + j), kPendingRow, P_NEW_MINE};
@@ -130,6 +153,12 @@ __device__ __forceinline__ Probe probe_key(Bucket* __restrict__ idx, uint32_t nb
     b = (b + 1) & mask;
   }
   return {0, kPendingRow, insert ? P_OVERFLOW : P_ABSENT};
+}
+
+__device__ __forceinline__ Probe probe_key(Bucket* __restrict__ idx, uint32_t nb_log2, uint64_t key,
+                                           bool insert) {
+  const uint64_t b = home_bucket(key, nb_log2);
+  return probe_with(idx, nb_log2, key, insert, b, load_bucket(idx + b));
 }
 
 // ---------------------------------------------------------------------------
@@ -181,7 +210,7 @@ __device__ __forceinline__ uint64_t block_sum_u64(uint64_t v, unsigned long long
 
 // Bitonic sort of N (power of two) 64-bit words, ascending, by the whole block.
 template <int NT, class P>
-__device__ void block_bitonic_sort(P a, uint32_t N) {
+__device__ __forceinline__ void block_bitonic_sort(P a, uint32_t N) {
   for (uint32_t k = 2; k <= N; k <<= 1) {
     for (uint32_t j = k >> 1; j > 0; j >>= 1) {
       for (uint32_t i = threadIdx.x; i < N; i += NT) {

@@ -10,10 +10,11 @@
 namespace mlkv {
 
 constexpr int kGetTile = 256;    // keys per probe_gather block (one per lane)
-constexpr int kPutTile = 1024;   // keys per put_probe block (one per lane)
+constexpr int kPutTile = 1024;   // keys per put_probe block
+constexpr int kPutThreads = 1024; // threads of a put_probe block
 constexpr int kMaxParts = 4096;  // partitions (MSD digits) per put call
-constexpr int kRedThreads = 512; // threads of a reduce_update block
-constexpr int kRedCap = 4096;    // partition entries held in LDS
+constexpr int kRedThreads = 256; // threads of a reduce_update block
+constexpr int kRedCap = 1024;    // partition entries held in LDS
 
 // Kernels of the library, for per-launch timing.
 enum KernelId : int { K_GET_PROBE_GATHER = 0, K_ASSIGN_NEW = 1, K_PUT_PROBE = 2, K_REDUCE_UPDATE = 3, K_COUNT = 4 };
@@ -57,9 +58,9 @@ struct PutArgs {
   int64_t capacity;
   float lr;
   float eps;
-  int shift;  // slot >> shift = partition
-  int NP;     // number of partitions
+  int pb;     // 2^pb partitions
   uint64_t* items;
+  double* partials;  // [n][D] fp64 sums of keys repeated within a tile
   uint32_t* meta;
   NewKey* newlist;
   uint32_t* tile_cnt;

@@ -26,6 +26,27 @@ __device__ __forceinline__ void store_vec(float* p, const typename VecT<VEC>::T&
   }
 }
 
+// Loads W consecutive 32-bit words (W = 1, 2, 4 or 8; 16-byte aligned when W >= 4).
+template <int W>
+__device__ __forceinline__ void load_words(uint32_t* dst, const uint32_t* src) {
+  if constexpr (W >= 4) {
+#pragma unroll
+    for (int h = 0; h < W / 4; ++h) {
+      const uint4 v = reinterpret_cast<const uint4*>(src)[h];
+      dst[4 * h] = v.x;
+      dst[4 * h + 1] = v.y;
+      dst[4 * h + 2] = v.z;
+      dst[4 * h + 3] = v.w;
+    }
+  } else if constexpr (W == 2) {
+    const uint2 v = *reinterpret_cast<const uint2*>(src);
+    dst[0] = v.x;
+    dst[1] = v.y;
+  } else {
+    dst[0] = *src;
+  }
+}
+
 template <int VEC>
 __device__ __forceinline__ typename VecT<VEC>::T init_vec(uint64_t s0, int col) {
   typename VecT<VEC>::T v;
@@ -126,7 +147,7 @@ constexpr int kChunk = 2048;
 // Calls body(s_chunk, cnt) for consecutive chunks of this call's new keys;
 // the block's NT threads must all call it. s_pref: NT+1 words.
 template <int NT, class Body>
-__device__ void for_each_new_key_chunk(const NewKey* __restrict__ newlist,
+__device__ __forceinline__ void for_each_new_key_chunk(const NewKey* __restrict__ newlist,
                                        const uint32_t* __restrict__ tile_cnt, int ntiles,
                                        int tile_size, uint32_t* s_pref, uint32_t* s_w,
                                        uint64_t* s_chunk, Body body) {
@@ -292,66 +313,259 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
 }
 
 // ===========================================================================
-// Put. The (key position) pairs of a call flow through "items":
+// Put. The (key, position) pairs of a call flow through "items":
 //   bit 63     1 if the key is inserted by this call (row not yet known)
 //   bits 31-62 the key's row, or its index slot when bit 63 is set
-//   bits 0-30  the position of the key in the batch
-// Sorting items therefore groups the positions of each key, in ascending
-// order, and puts the keys new in this call last.
+//   bit 30     1 if the item stands for several positions of one tile whose
+//              gradient rows were already summed (fp64) into partials[pos]
+//   bits 0-29  the position of the key in the batch (the first one for a
+//              summed item)
+// Sorting items groups the positions of each key (single positions first,
+// then summed tiles, each in ascending order) and puts new keys last.
 // ===========================================================================
-__device__ __forceinline__ uint64_t make_item(bool fresh, uint32_t tag, uint32_t pos) {
-  return ((uint64_t)(fresh ? 1u : 0u) << 63) | ((uint64_t)tag << 31) | (uint64_t)pos;
+constexpr uint64_t kItemSummed = 1ull << 30;
+
+__device__ __forceinline__ uint64_t make_item(bool fresh, uint32_t tag, uint32_t low31) {
+  return ((uint64_t)(fresh ? 1u : 0u) << 63) | ((uint64_t)tag << 31) | (uint64_t)(low31 & 0x7FFFFFFFu);
 }
-__device__ __forceinline__ uint32_t item_pos(uint64_t it) { return (uint32_t)(it & 0x7FFFFFFFull); }
+__device__ __forceinline__ uint32_t item_pos(uint64_t it) { return (uint32_t)(it & 0x3FFFFFFFull); }
+__device__ __forceinline__ uint32_t item_low31(uint64_t it) { return (uint32_t)(it & 0x7FFFFFFFull); }
+__device__ __forceinline__ bool item_summed(uint64_t it) { return (it & kItemSummed) != 0; }
 __device__ __forceinline__ uint32_t item_tag(uint64_t it) { return (uint32_t)(it >> 31); }
 __device__ __forceinline__ bool item_fresh(uint64_t it) { return (it >> 63) != 0; }
 __device__ __forceinline__ uint64_t item_group(uint64_t it) { return it >> 31; }
 
+// Partition of a key's group: top bits of a hash of (fresh, row or slot).
+__device__ __forceinline__ uint32_t group_partition(uint64_t group, int pb) {
+  return pb ? (uint32_t)(index_hash(group) >> (64 - pb)) : 0u;
+}
+
 // ---------------------------------------------------------------------------
-// Put, first kernel: probe (+ insert) each key and partition the tile's items
-// by the top bits of the key's slot (one MSD radix digit), in LDS.
+// Put, first kernel (one block per tile of kPutTile keys, kPutThreads
+// threads): probe (+ insert) each key; find the keys that occur more than once
+// in the tile with an LDS hash table and sum each one's gradient rows
+// (positions ascending, fp64) into one partial; partition the resulting items
+// by a hash of the key (one MSD radix digit).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kPutTile) void k_put_probe(
-    Bucket* __restrict__ idx, uint32_t nb_log2, const uint64_t* __restrict__ keys, int64_t n,
-    int shift, int NP, int ntiles, uint64_t* __restrict__ items, uint32_t* __restrict__ meta,
-    NewKey* __restrict__ newlist, uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch) {
-  constexpr int NT = kPutTile;
+constexpr int kTileHash = 2 * kPutTile;  // LDS hash slots per tile
+
+template <class M>
+__global__ __launch_bounds__(kPutThreads) void k_put_probe(
+    Bucket* __restrict__ idx, uint32_t nb_log2, const uint64_t* __restrict__ keys,
+    const float* __restrict__ grads, int64_t n, int D, int pb, int ntiles, uint64_t* __restrict__ items,
+    uint32_t* __restrict__ meta, double* __restrict__ partials, NewKey* __restrict__ newlist,
+    uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch) {
+  constexpr int NT = kPutThreads;
+  constexpr int KPT = kPutTile / kPutThreads;  // keys per thread
+  constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
+  constexpr int NG = (NT / 64) * RPW;
+  using V = typename VecT<VEC>::T;
   __shared__ uint32_t s_hist[kMaxParts];
+  __shared__ unsigned long long s_hkey[kTileHash];  // group of each hash slot
+  __shared__ uint32_t s_hcnt[kTileHash];            // occurrences of the group in the tile
+  __shared__ uint32_t s_hfirst[kTileHash];          // first entry holding the group
+  __shared__ uint32_t s_hcur[kTileHash];            // fill cursor of the group's entry list
+  __shared__ uint16_t s_hdup[kTileHash];            // index of a repeated group
+  __shared__ uint16_t s_lanes[kPutTile];            // entries of repeated groups, grouped
+  __shared__ uint16_t s_doff[kPutTile / 2 + 1];     // start of each repeated group's entries
   __shared__ uint32_t s_w[NT / 64];
   __shared__ uint32_t s_cnt;
+  const int NP = 1 << pb;
   const int tid = threadIdx.x;
   const int tile = blockIdx.x;
-  const int64_t i = (int64_t)tile * NT + tid;
+  const int64_t base = (int64_t)tile * kPutTile;
   if (tile == 0 && tid == 0) ctrl->spill_next = 0;
   for (int d = tid; d < NP; d += NT) s_hist[d] = 0;
+  for (int h = tid; h < kTileHash; h += NT) {
+    s_hkey[h] = ~0ull;
+    s_hcnt[h] = 0;
+    s_hfirst[h] = 0xFFFFFFFFu;
+    s_hcur[h] = 0;
+  }
   if (tid == 0) s_cnt = 0;
-  __syncthreads();
 
-  uint64_t key = 0;
-  Probe pr = {0, kPendingRow, P_NONE};
-  if (i < n) {
-    key = keys[i];
-    if (key == kEmptyKey) {
-      pr.status = P_BAD;
-      ctrl->bad_epoch = epoch;
-    } else {
-      pr = probe_key(idx, nb_log2, key, true);
-      if (pr.status == P_OVERFLOW) ctrl->overflow_epoch = epoch;
+  // entry e = kk * NT + tid of the tile is batch position base + e
+  uint64_t key[KPT];
+  Probe pr[KPT];
+  {
+    uint64_t hb[KPT];
+    BucketView bv[KPT];
+#pragma unroll
+    for (int kk = 0; kk < KPT; ++kk) {
+      const int64_t i = base + kk * NT + tid;
+      key[kk] = i < n ? keys[i] : kEmptyKey;
+      pr[kk] = {0, kPendingRow, i < n ? P_BAD : P_NONE};
+    }
+#pragma unroll
+    for (int kk = 0; kk < KPT; ++kk) {
+      if (key[kk] != kEmptyKey) {
+        hb[kk] = home_bucket(key[kk], nb_log2);
+        bv[kk] = load_bucket(idx + hb[kk]);
+      }
+    }
+#pragma unroll
+    for (int kk = 0; kk < KPT; ++kk) {
+      if (key[kk] != kEmptyKey) {
+        pr[kk] = probe_with(idx, nb_log2, key[kk], true, hb[kk], bv[kk]);
+        if (pr[kk].status == P_OVERFLOW) ctrl->overflow_epoch = epoch;
+      } else if (pr[kk].status == P_BAD) {
+        ctrl->bad_epoch = epoch;
+      }
     }
   }
-  const bool item = pr.status == P_HIT || pr.status == P_NEW_MINE || pr.status == P_NEW_OTHER;
-  uint32_t d = 0, r = 0;
-  if (item) {
-    d = pr.slot >> shift;
-    r = atomicAdd(&s_hist[d], 1u);
-  }
-  if (pr.status == P_NEW_MINE) {
-    const uint32_t j = atomicAdd(&s_cnt, 1u);
-    newlist[(size_t)tile * NT + j] = NewKey{key, pr.slot, 0u};
-    ctrl->new_epoch = epoch;
-  }
   __syncthreads();
 
+  uint64_t x[KPT];
+  uint32_t hs[KPT];
+  bool valid[KPT];
+#pragma unroll
+  for (int kk = 0; kk < KPT; ++kk) {
+    const int e = kk * NT + tid;
+    valid[kk] = pr[kk].status == P_HIT || pr[kk].status == P_NEW_MINE || pr[kk].status == P_NEW_OTHER;
+    if (pr[kk].status == P_NEW_MINE) {
+      const uint32_t j = atomicAdd(&s_cnt, 1u);
+      newlist[(size_t)base + j] = NewKey{key[kk], pr[kk].slot, 0u};
+      ctrl->new_epoch = epoch;
+    }
+    const bool fresh = pr[kk].status != P_HIT;
+    x[kk] = valid[kk] ? make_item(fresh, fresh ? pr[kk].slot : pr[kk].row, (uint32_t)(base + e)) : ~0ull;
+    // count the tile's occurrences of every group
+    hs[kk] = 0;
+    if (valid[kk]) {
+      const uint64_t grp = item_group(x[kk]);
+      uint32_t h = (uint32_t)index_hash(grp) & (kTileHash - 1);
+      while (true) {
+        const unsigned long long old = atomicCAS(&s_hkey[h], ~0ull, (unsigned long long)grp);
+        if (old == ~0ull || old == grp) break;
+        h = (h + 1) & (kTileHash - 1);
+      }
+      hs[kk] = h;
+      atomicAdd(&s_hcnt[h], 1u);
+      atomicMin(&s_hfirst[h], (uint32_t)e);
+    }
+  }
+  __syncthreads();
+  uint32_t cnt[KPT];
+  bool dup[KPT], owner[KPT];
+  uint32_t n_own = 0, l_own = 0;
+#pragma unroll
+  for (int kk = 0; kk < KPT; ++kk) {
+    const int e = kk * NT + tid;
+    cnt[kk] = valid[kk] ? s_hcnt[hs[kk]] : 0u;
+    dup[kk] = cnt[kk] >= 2;
+    owner[kk] = dup[kk] && s_hfirst[hs[kk]] == (uint32_t)e;
+    n_own += owner[kk] ? 1u : 0u;
+    l_own += owner[kk] ? cnt[kk] : 0u;
+  }
+
+  // repeated groups: index them, then list their entries contiguously
+  uint32_t ndup, nlanes;
+  uint32_t dpre = block_exclusive_scan<NT>(n_own, s_w, &ndup);
+  uint32_t lpre = block_exclusive_scan<NT>(l_own, s_w, &nlanes);
+#pragma unroll
+  for (int kk = 0; kk < KPT; ++kk) {
+    if (owner[kk]) {
+      s_hdup[hs[kk]] = (uint16_t)dpre;
+      s_doff[dpre] = (uint16_t)lpre;
+      ++dpre;
+      lpre += cnt[kk];
+    }
+  }
+  if (tid == 0) s_doff[ndup] = (uint16_t)nlanes;
+  __syncthreads();
+  uint32_t my_off[KPT];
+#pragma unroll
+  for (int kk = 0; kk < KPT; ++kk) {
+    my_off[kk] = 0;
+    if (dup[kk]) {
+      my_off[kk] = s_doff[s_hdup[hs[kk]]];
+      s_lanes[my_off[kk] + atomicAdd(&s_hcur[hs[kk]], 1u)] = (uint16_t)(kk * NT + tid);
+    }
+  }
+  __syncthreads();
+  // sort each repeated group's entry list: an entry's rank is the number of
+  // smaller entries in its group's list
+  uint32_t rank[KPT];
+#pragma unroll
+  for (int kk = 0; kk < KPT; ++kk) {
+    rank[kk] = 0;
+    if (dup[kk]) {
+      const uint32_t e = kk * NT + tid;
+      for (uint32_t m = 0; m < cnt[kk]; ++m) rank[kk] += s_lanes[my_off[kk] + m] < e ? 1u : 0u;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int kk = 0; kk < KPT; ++kk)
+    if (dup[kk]) s_lanes[my_off[kk] + rank[kk]] = (uint16_t)(kk * NT + tid);
+  __syncthreads();
+
+  // each lane group sums the rows of repeated groups, positions ascending
+  {
+    constexpr int UNR = (K * VEC >= 8) ? 4 : 8;
+    const int lane = tid & 63;
+    const int g = lane / LPR;
+    const int q = lane % LPR;
+    const int gid = (tid >> 6) * RPW + g;
+    for (uint32_t dg = gid; dg < ndup; dg += NG) {
+      const uint32_t b = s_doff[dg], e = s_doff[dg + 1];
+      double acc[K][VEC];
+#pragma unroll
+      for (int k = 0; k < K; ++k)
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) acc[k][v] = 0.0;
+      for (uint32_t j = b; j < e; j += UNR) {
+        V gv[UNR][K];
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+          if (j + u < e) {
+            const float* gr = grads + (size_t)(base + s_lanes[j + u]) * (size_t)D;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              const int col = (k * LPR + q) * VEC;
+              if (col < D) gv[u][k] = load_vec<VEC>(gr + col);
+            }
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+          if (j + u < e) {
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              const int col = (k * LPR + q) * VEC;
+              if (col < D) {
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) acc[k][v] += (double)VecT<VEC>::get(gv[u][k], v);
+              }
+            }
+          }
+        }
+      }
+      double* dst = partials + (size_t)(base + s_lanes[b]) * (size_t)D;
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const int col = (k * LPR + q) * VEC;
+#pragma unroll
+        for (int v = 0; v < VEC; ++v)
+          if (col + v < D) dst[col + v] = acc[k][v];
+      }
+    }
+  }
+
+  // emit single positions, and one summed item per repeated key
+  bool emit[KPT];
+  uint32_t d[KPT], r[KPT];
+#pragma unroll
+  for (int kk = 0; kk < KPT; ++kk) {
+    emit[kk] = valid[kk] && (!dup[kk] || owner[kk]);
+    d[kk] = 0;
+    r[kk] = 0;
+    if (emit[kk]) {
+      d[kk] = group_partition(item_group(x[kk]), pb);
+      r[kk] = atomicAdd(&s_hist[d[kk]], 1u);
+    }
+  }
+  __syncthreads();
   constexpr int PER = kMaxParts / NT;
   uint32_t c[PER];
   uint32_t sum = 0;
@@ -378,10 +592,9 @@ __global__ __launch_bounds__(kPutTile) void k_put_probe(
     if (dd < NP) s_hist[dd] = offs[j];
   }
   __syncthreads();
-  if (item) {
-    const bool fresh = pr.status != P_HIT;
-    items[(size_t)tile * NT + s_hist[d] + r] = make_item(fresh, fresh ? pr.slot : pr.row, (uint32_t)i);
-  }
+#pragma unroll
+  for (int kk = 0; kk < KPT; ++kk)
+    if (emit[kk]) items[(size_t)base + s_hist[d[kk]] + r[kk]] = dup[kk] ? (x[kk] | kItemSummed) : x[kk];
   if (tid == 0) tile_cnt[tile] = s_cnt;
 }
 
@@ -493,6 +706,7 @@ struct SegmentOps {
 struct RedCtx {
   Bucket* idx;
   const float* grads;
+  const double* partials;
   float* rows;
   float* state;
   int D;
@@ -553,7 +767,7 @@ __device__ __forceinline__ void resolve_new_rows(IP it, SP seg, uint32_t S, uint
     if (pend) {
       const uint32_t row = (uint32_t)(c.size0 + rank);
       c.idx[slot / kSlots].row[slot % kSlots] = row;
-      it[seg[s]] = make_item(true, row, item_pos(x));
+      it[seg[s]] = make_item(true, row, item_low31(x));
       // the new row starts from its initial value and a zero accumulator
       const uint64_t s0 = splitmix_mix(key ^ c.seed);
       float* w = c.rows + (size_t)row * (size_t)c.D;
@@ -577,7 +791,7 @@ __device__ __forceinline__ void apply_segments(IP it, SP seg, DP sid, uint32_t m
   using Ops = SegmentOps<M>;
   constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
   constexpr int NG = (NT / 64) * RPW;
-  constexpr int B = (K * VEC >= 8) ? 4 : 8;
+  constexpr int B = (K * VEC >= 8) ? 2 : 4;
   using V = typename VecT<VEC>::T;
   const int lane = threadIdx.x & 63;
   const int g = lane / LPR;
@@ -594,24 +808,38 @@ __device__ __forceinline__ void apply_segments(IP it, SP seg, DP sid, uint32_t m
   Ops::zero(acc);
   for (uint32_t j0 = lo; j0 < hi; j0 += B) {
     V gv[B][K];
+    double pv[B][K][VEC];
     V wv[B][K];
     float G0[B];
     uint32_t sj[B];
-    bool ends[B], owned[B];
+    bool ends[B], owned[B], summ[B];
 #pragma unroll
     for (int u = 0; u < B; ++u) {
       const uint32_t j = j0 + u;
       ends[u] = false;
       owned[u] = false;
+      summ[u] = false;
       G0[u] = 0.0f;
       if (j < hi) {
         const uint64_t x = it[j];
         sj[u] = sid[j];
-        const float* gr = c.grads + (size_t)item_pos(x) * (size_t)D;
+        summ[u] = item_summed(x);
+        if (summ[u]) {
+          const double* pr = c.partials + (size_t)item_pos(x) * (size_t)D;
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
-          const int col = (k * LPR + q) * VEC;
-          if (col < D) gv[u][k] = load_vec<VEC>(gr + col);
+          for (int k = 0; k < K; ++k) {
+            const int col = (k * LPR + q) * VEC;
+#pragma unroll
+            for (int v = 0; v < VEC; ++v)
+              if (col + v < D) pv[u][k][v] = pr[col + v];
+          }
+        } else {
+          const float* gr = c.grads + (size_t)item_pos(x) * (size_t)D;
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            const int col = (k * LPR + q) * VEC;
+            if (col < D) gv[u][k] = load_vec<VEC>(gr + col);
+          }
         }
         ends[u] = seg[sj[u] + 1] == j + 1;
         owned[u] = seg[sj[u]] >= lo;
@@ -631,7 +859,8 @@ __device__ __forceinline__ void apply_segments(IP it, SP seg, DP sid, uint32_t m
           const int col = (k * LPR + q) * VEC;
           if (col < D) {
 #pragma unroll
-            for (int x = 0; x < VEC; ++x) acc[k][x] += (double)VecT<VEC>::get(gv[u][k], x);
+            for (int x = 0; x < VEC; ++x)
+              acc[k][x] += summ[u] ? pv[u][k][x] : (double)VecT<VEC>::get(gv[u][k], x);
           }
         }
         if (ends[u]) {
@@ -739,7 +968,7 @@ template <class M>
 __global__ __launch_bounds__(kRedThreads, (M::K * M::VEC >= 16) ? 2 : 4) void k_reduce_update(
     Bucket* __restrict__ idx, const uint64_t* __restrict__ items, const uint32_t* __restrict__ meta,
     int ntiles, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
-    const float* __restrict__ grads, float* __restrict__ rows, float* __restrict__ state, int D,
+    const float* __restrict__ grads, const double* __restrict__ partials, float* __restrict__ rows, float* __restrict__ state, int D,
     uint64_t seed, float lr, float eps, int64_t capacity, Ctrl* ctrl, uint64_t epoch,
     uint64_t* __restrict__ spill, uint64_t spill_words) {
   constexpr int NT = kRedThreads;
@@ -785,7 +1014,7 @@ __global__ __launch_bounds__(kRedThreads, (M::K * M::VEC >= 16) ? 2 : 4) void k_
     return;
   }
 
-  const RedCtx c{idx, grads, rows, state, D, seed, lr, eps, size0};
+  const RedCtx c{idx, grads, partials, rows, state, D, seed, lr, eps, size0};
   if (mp > (uint32_t)kRedCap) {
     reduce_partition_global<M, NT>(p, mp, items, meta, ntiles, c, newlist, tile_cnt, ctrl, spill, spill_words,
                                    s_dyn, s_pref, s_w, s_w64, &s_base);
@@ -807,28 +1036,32 @@ __global__ __launch_bounds__(kRedThreads, (M::K * M::VEC >= 16) ? 2 : 4) void k_
     __syncthreads();
   }
 
-  // ---- sort (all items are distinct: positions are) ----
-  if (mp <= (uint32_t)NT) {
-    // rank = number of smaller items
-    const uint64_t v = tid < (int)mp ? s_items[tid] : ~0ull;
-    uint32_t rk = 0;
-    if (tid < (int)mp) {
-      uint32_t e = 0;
-      for (; e + 4 <= mp; e += 4) {
-        const uint64_t a0 = s_items[e], a1 = s_items[e + 1], a2 = s_items[e + 2], a3 = s_items[e + 3];
-        rk += (a0 < v ? 1u : 0u) + (a1 < v ? 1u : 0u) + (a2 < v ? 1u : 0u) + (a3 < v ? 1u : 0u);
+  // ---- sort: an item's rank is the number of smaller items (all items are
+  // distinct, since positions are) ----
+  {
+    constexpr int IPT = kRedCap / NT;
+    uint64_t v[IPT];
+    uint32_t rk[IPT];
+    int mine = 0;
+#pragma unroll
+    for (int j = 0; j < IPT; ++j) {
+      const uint32_t k = tid + j * NT;
+      v[j] = k < mp ? s_items[k] : ~0ull;
+      rk[j] = 0;
+      mine += k < mp ? 1 : 0;
+    }
+    if (mine > 0) {
+      for (uint32_t e = 0; e < mp; ++e) {
+        const uint64_t a = s_items[e];
+#pragma unroll
+        for (int j = 0; j < IPT; ++j) rk[j] += a < v[j] ? 1u : 0u;
       }
-      for (; e < mp; ++e) rk += s_items[e] < v ? 1u : 0u;
     }
     __syncthreads();
-    if (tid < (int)mp) s_items[rk] = v;
+#pragma unroll
+    for (int j = 0; j < IPT; ++j)
+      if (tid + j * NT < mp) s_items[rk[j]] = v[j];
     __syncthreads();
-  } else {
-    uint32_t P2 = 1;
-    while (P2 < mp) P2 <<= 1;
-    for (uint32_t j = mp + tid; j < P2; j += NT) s_items[j] = ~0ull;
-    __syncthreads();
-    block_bitonic_sort<NT>(s_items, P2);
   }
 
   const uint32_t S = encode_segments<NT>(s_items, mp, s_seg, s_sid, s_w);
@@ -897,9 +1130,9 @@ template <class M>
 static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHook& hook) {
   const int64_t ntiles = (a.n + kPutTile - 1) / kPutTile;
   hook(K_PUT_PROBE, 0, st);
-  hipLaunchKernelGGL(k_put_probe, dim3((unsigned)ntiles), dim3(kPutTile), 0, st, a.idx, a.nb_log2,
-                     a.keys, a.n, a.shift, a.NP, (int)ntiles, a.items, a.meta, a.newlist, a.tile_cnt,
-                     a.ctrl, a.epoch);
+  hipLaunchKernelGGL(k_put_probe<M>, dim3((unsigned)ntiles), dim3(kPutThreads), 0, st, a.idx, a.nb_log2,
+                     a.keys, a.grads, a.n, a.D, a.pb, (int)ntiles, a.items, a.meta, a.partials,
+                     a.newlist, a.tile_cnt, a.ctrl, a.epoch);
   hook(K_PUT_PROBE, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -912,10 +1145,9 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
     attr_set = true;
   }
   hook(K_REDUCE_UPDATE, 0, st);
-  hipLaunchKernelGGL(k_reduce_update<M>, dim3((unsigned)a.NP), dim3(kRedThreads), dyn, st, a.idx,
-                     a.items, a.meta, (int)ntiles, a.newlist, a.tile_cnt, a.grads, a.rows,
-                     a.state, a.D, a.seed, a.lr, a.eps, a.capacity, a.ctrl, a.epoch, a.spill,
-                     a.spill_words);
+  hipLaunchKernelGGL(k_reduce_update<M>, dim3(1u << a.pb), dim3(kRedThreads), dyn, st, a.idx, a.items,
+                     a.meta, (int)ntiles, a.newlist, a.tile_cnt, a.grads, a.partials, a.rows, a.state,
+                     a.D, a.seed, a.lr, a.eps, a.capacity, a.ctrl, a.epoch, a.spill, a.spill_words);
   hook(K_REDUCE_UPDATE, 1, st);
   return hipGetLastError();
 }
