@@ -114,6 +114,13 @@ int mlkv_lookup_rows(mlkv_table *t, const uint64_t *d_keys, int64_t n, int64_t *
 int mlkv_export(mlkv_table *t, int64_t nrows, float *d_rows_out, float *d_state_out,
                 uint64_t *d_slot_keys_out, uint32_t *d_slot_rows_out, void *hip_stream);
 
+/* d_rows_out[i*dim + c] = element c of row d_rows[i], d_state_out[i] = its
+ * Adagrad accumulator (either output may be NULL), for 0 <= n <= 2^31 - 1 row
+ * ids. A row id outside [0, size) gives a NaN row and accumulator and makes
+ * the next mlkv_sync return MLKV_EINVAL. */
+int mlkv_read_rows(mlkv_table *t, const int64_t *d_rows, int64_t n, float *d_rows_out,
+                   float *d_state_out, void *hip_stream);
+
 /* ---- per-kernel timing (benchmarks) ----
  * The library runs MLKV_NUM_KERNELS kernels: 0 get_probe_gather and
  * 1 assign_new for mlkv_get, 2 put_probe and 3 reduce_update for

@@ -390,6 +390,19 @@ int mlkv_export(mlkv_table* t, int64_t nrows, float* d_rows_out, float* d_state_
   return MLKV_OK;
 }
 
+int mlkv_read_rows(mlkv_table* t, const int64_t* d_rows, int64_t n, float* d_rows_out, float* d_state_out,
+                   void* hip_stream) {
+  int rc = check_table(t);
+  if (rc) return rc;
+  if (n < 0 || n > 0x7FFFFFFFll) return fail(MLKV_EINVAL, "n must be in [0, 2^31 - 1]");
+  if (n == 0) return MLKV_OK;
+  if (d_rows == nullptr) return fail(MLKV_EINVAL, "rows is NULL");
+  hipError_t e = launch_read_rows(t->rows, t->state, t->dim, &t->ctrl->size[t->epoch & 1], d_rows, n,
+                                  d_rows_out, d_state_out, t->ctrl, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail(e, "mlkv_read_rows launch");
+  return MLKV_OK;
+}
+
 int mlkv_profile_enable(mlkv_table* t, int enable) {
   if (t == nullptr) return fail(MLKV_EINVAL, "table is NULL");
   t->prof_on = enable != 0;

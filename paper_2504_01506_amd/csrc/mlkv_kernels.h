@@ -76,5 +76,8 @@ hipError_t launch_lookup(Bucket* idx, uint32_t nb_log2, const uint64_t* keys, in
                          int64_t* rows_out, hipStream_t st);
 hipError_t launch_export_slots(const Bucket* idx, uint64_t nslots, uint64_t* keys_out,
                                uint32_t* rows_out, hipStream_t st);
+hipError_t launch_read_rows(const float* rows, const float* state, int D, const unsigned long long* size_now,
+                            const int64_t* ids, int64_t n, float* w_out, float* st_out, Ctrl* ctrl,
+                            hipStream_t st);
 
 }  // namespace mlkv

@@ -1097,6 +1097,26 @@ __global__ __launch_bounds__(256) void k_export_slots(const Bucket* __restrict__
   if (rows_out) rows_out[s] = B->row[s % kSlots];
 }
 
+// Copies rows and accumulators by row id; ids outside [0, size) give NaN
+// rows and latch MLKV_EINVAL (-1).
+__global__ __launch_bounds__(256) void k_read_rows(const float* __restrict__ rows, const float* __restrict__ state,
+                                                   int D, const unsigned long long* size_now,
+                                                   const int64_t* __restrict__ ids, int64_t n,
+                                                   float* __restrict__ w_out, float* __restrict__ st_out,
+                                                   Ctrl* ctrl) {
+  const uint64_t size = *size_now;
+  const uint64_t total = (uint64_t)n * (uint64_t)D;
+  for (uint64_t e = (uint64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (uint64_t)gridDim.x * 256) {
+    const uint64_t i = e / (uint64_t)D;
+    const int c = (int)(e % (uint64_t)D);
+    const int64_t r = ids[i];
+    const bool ok = r >= 0 && (uint64_t)r < size;
+    if (!ok && c == 0) atomicCAS(&ctrl->latched, 0, -1);
+    if (w_out) w_out[e] = ok ? rows[(uint64_t)r * (uint64_t)D + c] : __builtin_nanf("");
+    if (st_out && c == 0) st_out[i] = ok ? state[r] : __builtin_nanf("");
+  }
+}
+
 // ===========================================================================
 // Launchers
 // ===========================================================================
@@ -1193,6 +1213,16 @@ hipError_t launch_export_slots(const Bucket* idx, uint64_t nslots, uint64_t* key
                                hipStream_t st) {
   const uint64_t grid = (nslots + 255) / 256;
   hipLaunchKernelGGL(k_export_slots, dim3((unsigned)grid), dim3(256), 0, st, idx, nslots, keys_out, rows_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_read_rows(const float* rows, const float* state, int D, const unsigned long long* size_now,
+                            const int64_t* ids, int64_t n, float* w_out, float* st_out, Ctrl* ctrl,
+                            hipStream_t st) {
+  const uint64_t total = (uint64_t)n * (uint64_t)D;
+  const uint64_t grid = std::min<uint64_t>((total + 255) / 256, 65536);
+  hipLaunchKernelGGL(k_read_rows, dim3((unsigned)grid), dim3(256), 0, st, rows, state, D, size_now, ids, n,
+                     w_out, st_out, ctrl);
   return hipGetLastError();
 }
 

@@ -52,6 +52,7 @@ def load() -> ctypes.CDLL:
         "mlkv_last_error": (ctypes.c_char_p, []),
         "mlkv_lookup_rows": (INT, [P, P, I64, P, P]),
         "mlkv_export": (INT, [P, I64, P, P, P, P, P]),
+        "mlkv_read_rows": (INT, [P, P, I64, P, P, P]),
         "mlkv_profile_enable": (INT, [P, INT]),
         "mlkv_profile_read": (INT, [P, P, P]),
         "mlkv_kernel_name": (ctypes.c_char_p, [INT]),
@@ -152,6 +153,10 @@ def mlkv_export(t: int, nrows: int, rows_out=None, state_out=None, slot_keys_out
                               _ptr(slot_rows_out), _stream(stream))
 
 
+def mlkv_read_rows(t: int, rows, n: int, rows_out=None, state_out=None, stream=None) -> int:
+    return load().mlkv_read_rows(t, _ptr(rows), n, _ptr(rows_out), _ptr(state_out), _stream(stream))
+
+
 def mlkv_profile_enable(t: int, enable: bool) -> int:
     return load().mlkv_profile_enable(t, 1 if enable else 0)
 
@@ -212,6 +217,13 @@ class Table:
         out = torch.empty(keys.numel(), dtype=torch.int64, device=keys.device)
         _check(mlkv_lookup_rows(self.h, keys, keys.numel(), out, stream))
         return out
+
+    def read_rows(self, rows: torch.Tensor, stream=None):
+        """(values[len(rows), dim], accumulators[len(rows)]) of the given row ids (int64)."""
+        w = torch.empty((rows.numel(), self.dim), dtype=torch.float32, device=rows.device)
+        st = torch.empty(rows.numel(), dtype=torch.float32, device=rows.device)
+        _check(mlkv_read_rows(self.h, rows, rows.numel(), w, st, stream))
+        return w, st
 
     def export(self, nrows: int | None = None, stream=None):
         """(rows[nrows, dim], state[nrows], slot_keys[num_slots] int64, slot_rows[num_slots] int32)."""

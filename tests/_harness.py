@@ -47,7 +47,7 @@ class Pair:
         self.dim = dim
         self.gpu = mlkv.Table(dim, capacity, seed=seed, max_load=max_load)
         self.ora = O.OracleTable(dim, capacity, seed=seed)
-        self.updated = set()      # rows written by put_grad at least once (oracle row ids)
+        self.updated = np.zeros(capacity, dtype=bool)  # rows written by put_grad at least once
         self.stats = {"max_err": 0.0, "max_ulp": 0, "exact_mismatch": 0}
 
     def close(self):
@@ -78,7 +78,7 @@ class Pair:
 
     def compare_get(self, keys, got, want):
         rows = self.ora.lookup_rows(keys)
-        fresh = np.array([r not in self.updated for r in rows.tolist()], dtype=bool)
+        fresh = ~self.updated[rows]
         # rows never updated: bit-exact
         if fresh.any():
             bad = ~np.all(got[fresh].view(np.uint32) == want[fresh].view(np.uint32), axis=1)
@@ -94,7 +94,7 @@ class Pair:
         self.gpu.put_grad(dev_keys(keys), dev(grads), lr, eps)
         assert self.ora.put_grad(keys, grads, lr, eps) == O.OK
         assert self.gpu.sync() == mlkv.MLKV_OK
-        self.updated.update(self.ora.lookup_rows(keys).tolist())
+        self.updated[self.ora.lookup_rows(keys)] = True
 
     def compare_rows(self, rows: np.ndarray | None = None):
         """Key->row bit-exact for the keys of `rows`; row values and accumulators
@@ -106,11 +106,11 @@ class Pair:
         keys = self.ora.row_keys(rows)
         got_rows = self.gpu.lookup_rows(dev_keys(keys)).cpu().numpy()
         assert np.array_equal(got_rows, rows), "key -> row differs"
-        w_all, st_all, _, _ = self.gpu.export(size)
-        w = w_all[torch.from_numpy(rows).cuda()].cpu().numpy()
-        st = st_all[torch.from_numpy(rows).cuda()].cpu().numpy()
+        w_d, st_d = self.gpu.read_rows(torch.from_numpy(rows).cuda())
+        w, st = w_d.cpu().numpy(), st_d.cpu().numpy()
+        assert self.gpu.sync() == mlkv.MLKV_OK
         want_w, want_st = self.ora.read_rows(rows)
-        fresh = np.array([r not in self.updated for r in rows.tolist()], dtype=bool)
+        fresh = ~self.updated[rows]
         if fresh.any():
             assert np.array_equal(w[fresh].view(np.uint32), want_w[fresh].view(np.uint32))
             assert np.all(st[fresh] == 0) and np.all(want_st[fresh] == 0)

@@ -1,0 +1,85 @@
+"""GPU against the oracle at the workloads' full sizes, in the same calls the
+benchmark times (a table opened with the default load factor, get(keys, out)
+then put_grad(keys, grads) on one stream).
+
+Compared every step: the whole get output (bit-exact for rows never updated,
+1e-5 row-scaled otherwise), key -> row of every key of the batch (bit-exact),
+every row the step updated and its accumulator (1e-5), and a seeded sample of
+other rows (bit-exact, initial values); table size after every call.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2504_01506_amd import mlkv, workloads as W
+from _harness import Pair, dev, dev_keys, log
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+STEPS = {"dlrm": 3, "kg": 2, "gnn": 2, "large": 2}
+
+
+def check_step(pr, keys, rng, n_sample=20000):
+    # key -> row of the batch
+    want_rows = pr.ora.lookup_rows(keys)
+    got_rows = pr.gpu.lookup_rows(dev_keys(keys)).cpu().numpy()
+    assert np.array_equal(got_rows, want_rows), "key -> row differs"
+    # rows updated by the step, and a sample of the rest
+    touched = np.unique(want_rows)
+    size = pr.ora.size
+    assert pr.gpu.size == size
+    other = rng.integers(0, size, size=n_sample).astype(np.int64)
+    pr.compare_rows(touched)
+    pr.compare_rows(np.unique(other))
+
+
+@pytest.mark.parametrize("name", ["dlrm", "kg", "gnn", "large"])
+def test_full_size_config(name):
+    wl = W.make(name, scale=1.0)
+    steps = STEPS[name]
+    log(f"[full] {name}: cap={wl.capacity} dim={wl.dim} n={wl.n} steps={steps}")
+    pr = Pair(wl.dim, wl.capacity)
+    pre = wl.prefill_keys()
+    if pre.size:
+        pr.prefill(pre)
+    log(f"[full] {name}: prefilled {pre.size} keys, size={pr.gpu.size}")
+    del pre
+    rng = np.random.default_rng(99)
+    for s in range(steps):
+        keys = wl.keys(s)
+        pr.get(keys)
+        log(f"[full] {name} step {s}: get ok, size={pr.ora.size}")
+        pr.put(keys, wl.grads(s), wl.lr, wl.eps)
+        check_step(pr, keys, rng)
+        log(f"[full] {name} step {s}: put ok, stats={pr.stats}")
+    pr.close()
+
+
+def test_full_size_ragged_batch_and_repeat():
+    """DLRM-sized table, a batch whose length is not a multiple of any tile,
+    then the same keys again (all present)."""
+    wl = W.make("dlrm", scale=1.0)
+    pr = Pair(wl.dim, wl.capacity)
+    pr.prefill(wl.prefill_keys())
+    rng = np.random.default_rng(7)
+    keys = wl.keys(0)[: 212992 - 333]
+    for _ in range(2):
+        pr.get(keys)
+        pr.put(keys, rng.normal(0, 0.01, size=(keys.size, wl.dim)).astype(np.float32), wl.lr, wl.eps)
+        check_step(pr, keys, rng, n_sample=5000)
+    log(f"[full] ragged ok, stats={pr.stats}")
+    pr.close()
+
+
+def test_full_size_max_batch_of_one_hot_key():
+    """The largest batch the benchmark issues, every position one key: the
+    longest possible segment (212,992 gradient rows into one row)."""
+    dim, n = 64, 212992
+    pr = Pair(dim, 1000)
+    keys = np.full(n, 12345, dtype=np.uint64)
+    rng = np.random.default_rng(8)
+    pr.get(keys)
+    pr.put(keys, rng.normal(0, 0.01, size=(n, dim)).astype(np.float32), 0.01, 1e-8)
+    pr.compare_rows()
+    log(f"[full] one-hot ok, stats={pr.stats}")
+    pr.close()

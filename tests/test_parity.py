@@ -74,7 +74,7 @@ def test_misaligned_output_and_grads_use_the_scalar_path():
     pr.gpu.put_grad(k, gbuf[1:], 0.01, 1e-8)
     pr.ora.put_grad(keys, g, 0.01, 1e-8)
     assert pr.gpu.sync() == 0
-    pr.updated.update(pr.ora.lookup_rows(keys).tolist())
+    pr.updated[pr.ora.lookup_rows(keys)] = True
     pr.compare_rows()
     pr.close()
 
