@@ -37,6 +37,12 @@ struct mlkv_table {
   uint64_t* spill = nullptr;
   uint64_t spill_words = 0;
   double* partials = nullptr;
+  uint64_t* gitems = nullptr;
+  uint32_t* gdesc = nullptr;
+  SegDesc* gsd = nullptr;
+  PartMeta* pmeta = nullptr;
+  double* gpiece = nullptr;
+  int flat_blocks = 256;  // blocks of the flat put kernels: one per CU
 
   // optional per-launch timing: HIP events recorded around each kernel
   struct ProfRec {
@@ -77,7 +83,17 @@ void free_workspace(mlkv_table* t) {
   (void)hipFree(t->meta);
   (void)hipFree(t->spill);
   (void)hipFree(t->partials);
+  (void)hipFree(t->gitems);
+  (void)hipFree(t->gdesc);
+  (void)hipFree(t->gsd);
+  (void)hipFree(t->pmeta);
+  (void)hipFree(t->gpiece);
   t->partials = nullptr;
+  t->gitems = nullptr;
+  t->gdesc = nullptr;
+  t->gsd = nullptr;
+  t->pmeta = nullptr;
+  t->gpiece = nullptr;
   t->newlist = nullptr;
   t->tile_cnt = nullptr;
   t->items = nullptr;
@@ -87,8 +103,17 @@ void free_workspace(mlkv_table* t) {
   t->spill_words = 0;
 }
 
+// Partitions of a put call of n keys: a power of two, at most kMaxParts,
+// with at most kPartTarget keys each on average before in-tile merging.
+uint32_t part_bits(int64_t n) {
+  uint32_t pb = 0;
+  while ((1 << pb) < kMaxParts && ((int64_t)kPartTarget << pb) < n) ++pb;
+  return pb;
+}
+
 // Scratch for calls of up to n keys: new-key lists, per-tile counts, the
-// partitioned (slot, pos) pairs, partition metadata and the spill area.
+// partitioned items, partition metadata, the spill area, in-tile sums and the
+// grouped partitions handed to the flat put kernels.
 int ensure_workspace(mlkv_table* t, int64_t n) {
   if (n <= t->ws_n) return MLKV_OK;
   int64_t want = std::max<int64_t>(n, std::max<int64_t>(65536, 2 * t->ws_n));
@@ -99,7 +124,14 @@ int ensure_workspace(mlkv_table* t, int64_t n) {
   const int64_t get_tiles = (want + kGetTile - 1) / kGetTile;
   const int64_t put_tiles = want / kPutTile;
   const uint64_t spill_words = 4ull * (uint64_t)want + 4096;
+  const size_t np = (size_t)1 << part_bits(want);
+  const size_t ng = (size_t)std::max(flat_groups_per_block(t->dim, true), flat_groups_per_block(t->dim, false));
   if ((e = dev_alloc(&t->newlist, sizeof(NewKey) * (size_t)want)) != hipSuccess ||
+      (e = dev_alloc(&t->gitems, sizeof(uint64_t) * np * kRedCap)) != hipSuccess ||
+      (e = dev_alloc(&t->gdesc, sizeof(uint32_t) * np * kRedCap)) != hipSuccess ||
+      (e = dev_alloc(&t->gsd, sizeof(SegDesc) * np * kRedCap)) != hipSuccess ||
+      (e = dev_alloc(&t->pmeta, sizeof(PartMeta) * np)) != hipSuccess ||
+      (e = dev_alloc(&t->gpiece, sizeof(double) * 2 * (size_t)t->flat_blocks * ng * (size_t)t->dim)) != hipSuccess ||
       (e = dev_alloc(&t->tile_cnt, sizeof(uint32_t) * (size_t)get_tiles)) != hipSuccess ||
       (e = dev_alloc(&t->items, sizeof(uint64_t) * (size_t)want)) != hipSuccess ||
       (e = dev_alloc(&t->meta, sizeof(uint32_t) * (size_t)kMaxParts * (size_t)put_tiles)) != hipSuccess ||
@@ -202,11 +234,13 @@ mlkv_table* mlkv_open_ex(int32_t dim, int64_t capacity, uint64_t seed, float max
   t->nb_log2 = lg;
   t->nb = 1ull << lg;
   hipError_t e = hipGetDevice(&t->device);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&t->flat_blocks, hipDeviceAttributeMultiprocessorCount, t->device);
   if (e != hipSuccess) {
     hip_fail(e, "hipGetDevice");
     delete t;
     return nullptr;
   }
+  t->flat_blocks = std::max(1, t->flat_blocks);
   if ((e = dev_alloc(&t->idx, sizeof(Bucket) * t->nb)) != hipSuccess ||
       (e = dev_alloc(&t->rows, sizeof(float) * (size_t)capacity * (size_t)dim)) != hipSuccess ||
       (e = dev_alloc(&t->state, sizeof(float) * (size_t)capacity)) != hipSuccess ||
@@ -284,10 +318,7 @@ int mlkv_put_grad(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, i
   if (n == 0) return MLKV_OK;
   if (d_keys == nullptr || d_grads == nullptr) return fail(MLKV_EINVAL, "keys or grads is NULL");
   if ((rc = ensure_workspace(t, n)) != MLKV_OK) return rc;
-  // partitions: about 128 keys each before in-tile merging, a power of two,
-  // at most kMaxParts
-  uint32_t pb = 0;
-  while ((1 << (pb + 1)) <= kMaxParts && ((int64_t)128 << (pb + 1)) <= n + (n >> 1)) ++pb;
+  const uint32_t pb = part_bits(n);
   PutArgs a;
   a.idx = t->idx;
   a.nb_log2 = t->nb_log2;
@@ -309,6 +340,12 @@ int mlkv_put_grad(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, i
   a.tile_cnt = t->tile_cnt;
   a.spill = t->spill;
   a.spill_words = t->spill_words;
+  a.gitems = t->gitems;
+  a.gdesc = t->gdesc;
+  a.gsd = t->gsd;
+  a.pmeta = t->pmeta;
+  a.gpiece = t->gpiece;
+  a.flat_blocks = t->flat_blocks;
   a.ctrl = t->ctrl;
   a.epoch = t->epoch;
   const bool vec4 = (t->dim % 4 == 0) && aligned16(d_grads);
@@ -433,7 +470,8 @@ int mlkv_profile_read(mlkv_table* t, double* total_ms, int64_t* launches) {
 }
 
 const char* mlkv_kernel_name(int kernel) {
-  static const char* names[K_COUNT] = {"get_probe_gather", "assign_new", "put_probe", "reduce_update"};
+  static const char* names[K_COUNT] = {"get_probe_gather", "assign_new", "put_probe",
+                                       "put_group",        "put_sum",    "put_update"};
   return (kernel >= 0 && kernel < K_COUNT) ? names[kernel] : nullptr;
 }
 

@@ -13,11 +13,36 @@ constexpr int kGetTile = 256;    // keys per probe_gather block (one per lane)
 constexpr int kPutTile = 1024;   // keys per put_probe block
 constexpr int kPutThreads = 1024; // threads of a put_probe block
 constexpr int kMaxParts = 4096;  // partitions (MSD digits) per put call
-constexpr int kRedThreads = 256; // threads of a reduce_update block
-constexpr int kRedCap = 1024;    // partition entries held in LDS
+constexpr int kRedCap = 3072;    // partition entries grouped in LDS by a reduce_update block
+constexpr int kRedHash = 4096;   // LDS hash slots for that grouping (load <= 0.75)
+constexpr int kPartTarget = 1024; // put keys per partition the partition count aims for
 
 // Kernels of the library, for per-launch timing.
-enum KernelId : int { K_GET_PROBE_GATHER = 0, K_ASSIGN_NEW = 1, K_PUT_PROBE = 2, K_REDUCE_UPDATE = 3, K_COUNT = 4 };
+enum KernelId : int {
+  K_GET_PROBE_GATHER = 0,
+  K_ASSIGN_NEW = 1,
+  K_PUT_PROBE = 2,
+  K_PUT_GROUP = 3,
+  K_PUT_SUM = 4,
+  K_PUT_UPDATE = 5,
+  K_COUNT = 6
+};
+
+// Per-partition results of put_group, read by put_sum and put_update.
+struct PartMeta {
+  uint32_t mA;    // items of the segments that need a sum (stored first)
+  uint32_t S;     // segments (distinct keys) of the partition
+  uint32_t nsum;  // segments that need a sum
+  uint32_t pad;
+};
+
+// One segment (distinct key) of a partition, for put_update.
+struct SegDesc {
+  uint32_t row;    // row of the key
+  uint32_t first;  // position of its first item | in-tile-sum bit 30 | needs-sum bit 31
+  uint32_t last;   // position of its last item (where put_sum leaves g)
+  uint32_t range;  // index of its first item | index of its end << 16, within the partition
+};
 
 // Optional callback around each launch (phase 0 before, 1 after), on the launch stream.
 struct LaunchHook {
@@ -66,9 +91,18 @@ struct PutArgs {
   uint32_t* tile_cnt;
   uint64_t* spill;
   uint64_t spill_words;
+  uint64_t* gitems;   // [partitions][kRedCap] grouped items
+  uint32_t* gdesc;    // [partitions][kRedCap] segment range of each item
+  SegDesc* gsd;       // [partitions][kRedCap] segments
+  PartMeta* pmeta;    // [partitions]
+  double* gpiece;     // [2 * flat groups][D] pieces of segments cut between put_sum slices
+  int flat_blocks;    // blocks of put_sum and put_update
   Ctrl* ctrl;
   uint64_t epoch;
 };
+
+// Lane groups of a put_sum / put_update block for dim D (vec4: 16-byte rows).
+int flat_groups_per_block(int D, bool vec4);
 
 hipError_t launch_get(const GetArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook);
 hipError_t launch_put(const PutArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook);

@@ -3,6 +3,8 @@
 // the fp64 segment-reduce fused with the row-wise Adagrad scatter-update.
 #include "mlkv_kernels.h"
 
+#include <type_traits>
+
 namespace mlkv {
 
 // ===========================================================================
@@ -202,10 +204,10 @@ __device__ __forceinline__ uint64_t count_new_keys(const uint32_t* __restrict__ 
 
 // Decides whether the call fails, and publishes the size for the next call.
 __device__ __forceinline__ int call_verdict(Ctrl* ctrl, uint64_t epoch, uint64_t size0, uint64_t M,
-                                            int64_t capacity) {
+                                            int64_t capacity, uint64_t bad_epoch, uint64_t overflow_epoch) {
   int err = 0;
-  if (ctrl->bad_epoch == epoch) err = -1;                          // MLKV_EINVAL
-  else if (ctrl->overflow_epoch == epoch || size0 + M > (uint64_t)capacity) err = -2;  // MLKV_EFULL
+  if (bad_epoch == epoch) err = -1;                                           // MLKV_EINVAL
+  else if (overflow_epoch == epoch || size0 + M > (uint64_t)capacity) err = -2;  // MLKV_EFULL
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     ctrl->size[(epoch + 1) & 1] = err ? size0 : size0 + M;
     if (err) atomicCAS(&ctrl->latched, 0, err);
@@ -237,7 +239,7 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
   const uint64_t size0 = ctrl->size[epoch & 1];
   const bool any_new = ctrl->new_epoch == epoch;
   const uint64_t M = any_new ? count_new_keys<NT>(tile_cnt, ntiles, s_w64) : 0ull;
-  const int err = call_verdict(ctrl, epoch, size0, M, capacity);
+  const int err = call_verdict(ctrl, epoch, size0, M, capacity, ctrl->bad_epoch, ctrl->overflow_epoch);
   if (M == 0) return;
 
   if (err) {  // undo this call's insertions: the index returns to its state before the call
@@ -600,83 +602,59 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
 
 // ---------------------------------------------------------------------------
 // Put, second kernel: one block per partition. Gathers the partition's items,
-// sorts them, run-length encodes them into segments (one per distinct key,
-// positions ascending), sums each segment's gradient rows in fp64 and applies
-// one row-wise Adagrad step to the key's row.
+// groups them into segments (one per distinct key, positions ascending), sums
+// each segment's gradient rows in fp64 and applies one row-wise Adagrad step
+// to the key's row.
 // ---------------------------------------------------------------------------
+
+// Sum over the LPR lanes of a lane group (LPR a power of two, groups aligned);
+// every lane of the group receives the same value. Steps within 16 lanes use
+// DPP moves, wider steps lane shuffles.
+template <int LPR>
+__device__ __forceinline__ double group_sum(double x) {
+  auto dpp = [](double v, auto ctrl_tag) {
+    constexpr int ctrl = decltype(ctrl_tag)::value;
+    const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), ctrl, 0xF, 0xF, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), ctrl, 0xF, 0xF, false);
+    return __hiloint2double(hi, lo);
+  };
+  using Xor1 = std::integral_constant<int, 0xB1>;       // quad_perm [1,0,3,2]
+  using Xor2 = std::integral_constant<int, 0x4E>;       // quad_perm [2,3,0,1]
+  using HalfMirror = std::integral_constant<int, 0x141>;  // row_half_mirror
+  using Mirror = std::integral_constant<int, 0x140>;      // row_mirror
+  if constexpr (LPR >= 2) x += dpp(x, Xor1{});
+  if constexpr (LPR >= 4) x += dpp(x, Xor2{});
+  if constexpr (LPR >= 8) x += dpp(x, HalfMirror{});
+  if constexpr (LPR >= 16) x += dpp(x, Mirror{});
+  if constexpr (LPR >= 32) x += __shfl_xor(x, 16, 64);
+  if constexpr (LPR >= 64) x += __shfl_xor(x, 32, 64);
+  return x;
+}
+
 template <class M>
 struct SegmentOps {
   static constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
   using V = typename VecT<VEC>::T;
-  static constexpr int UNR = (K * VEC >= 8) ? 4 : 8;
 
-  // acc += gradient rows of the sorted items [b, e)
-  template <class IP>
-  static __device__ __forceinline__ void accumulate(double (&acc)[K][VEC], IP it, uint32_t b, uint32_t e,
-                                                    const float* __restrict__ grads, int D, int q) {
-    for (uint32_t j = b; j < e; j += UNR) {
-      V v[UNR][K];
-#pragma unroll
-      for (int u = 0; u < UNR; ++u) {
-        if (j + u < e) {
-          const float* g = grads + (size_t)item_pos(it[j + u]) * (size_t)D;
-#pragma unroll
-          for (int k = 0; k < K; ++k) {
-            const int col = (k * LPR + q) * VEC;
-            if (col < D) v[u][k] = load_vec<VEC>(g + col);
-          }
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < UNR; ++u) {
-        if (j + u < e) {
-#pragma unroll
-          for (int k = 0; k < K; ++k) {
-            const int col = (k * LPR + q) * VEC;
-            if (col < D) {
-#pragma unroll
-              for (int x = 0; x < VEC; ++x) acc[k][x] += (double)VecT<VEC>::get(v[u][k], x);
-            }
-          }
-        }
-      }
-    }
-  }
-
-  // Current row values (or the initial row of a key new in this call).
-  static __device__ __forceinline__ void load_w(V (&w)[K], const float* __restrict__ rows, uint32_t row,
-                                                bool isnew, uint64_t s0, int D, int q) {
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-      const int col = (k * LPR + q) * VEC;
-      if (col < D) {
-        if (isnew) w[k] = init_vec<VEC>(s0, col);
-        else w[k] = load_vec<VEC>(rows + (size_t)row * (size_t)D + col);
-      }
-    }
-  }
-
-  // g = fp32(acc); m = fp32(sum g^2 / D) over the group's lanes; G' = G + m;
+  // Row-wise Adagrad step of one row, given its summed gradient g (fp32):
+  // m = fp32(sum g^2 / D) over the group's lanes; G' = G + m;
   // den = sqrt(G') + eps; w -= lr * (g / den); writes w and G'.
-  static __device__ __forceinline__ void adagrad(const double (&acc)[K][VEC], V (&w)[K], float G0,
-                                                 float* __restrict__ rows, float* __restrict__ state,
-                                                 uint32_t row, int D, int q, int leader, float lr,
-                                                 float eps) {
-    float gf[K][VEC];
+  static __device__ __forceinline__ void adagrad(const V (&g)[K], V (&w)[K], float G, float* __restrict__ rows,
+                                                 float* __restrict__ state, uint32_t row, int D, int q,
+                                                 bool d_pow2, double inv_d, float lr, float eps) {
     double sq = 0.0;
 #pragma unroll
     for (int k = 0; k < K; ++k) {
       const int col = (k * LPR + q) * VEC;
 #pragma unroll
       for (int x = 0; x < VEC; ++x) {
-        gf[k][x] = (float)acc[k][x];
-        if (col + x < D) sq += (double)gf[k][x] * (double)gf[k][x];
+        const double gx = (double)VecT<VEC>::get(g[k], x);
+        if (col + x < D) sq += gx * gx;
       }
     }
-#pragma unroll
-    for (int o = LPR / 2; o > 0; o >>= 1) sq += __shfl_xor(sq, o, 64);
-    const float m = (float)(sq / (double)D);
-    const float G = __shfl(G0, leader, 64);
+    sq = group_sum<LPR>(sq);
+    // D a power of two: multiplying by 1/D is exact, hence equal to sq / D
+    const float m = (float)(d_pow2 ? sq * inv_d : sq / (double)D);
     const float Gn = __fadd_rn(G, m);
     const float den = __fadd_rn(__builtin_sqrtf(Gn), eps);  // correctly rounded sqrt
 #pragma unroll
@@ -685,7 +663,7 @@ struct SegmentOps {
       if (col < D) {
 #pragma unroll
         for (int x = 0; x < VEC; ++x) {
-          const float qv = __fdiv_rn(gf[k][x], den);
+          const float qv = __fdiv_rn(VecT<VEC>::get(g[k], x), den);
           const float p = __fmul_rn(lr, qv);
           VecT<VEC>::set(w[k], x, __fsub_rn(VecT<VEC>::get(w[k], x), p));
         }
@@ -700,6 +678,23 @@ struct SegmentOps {
     for (int k = 0; k < K; ++k)
 #pragma unroll
       for (int x = 0; x < VEC; ++x) acc[k][x] = 0.0;
+  }
+
+  // g = fp32(acc) over the fp64 partials row at position pos (that row is no
+  // longer read once its segment is summed).
+  static __device__ __forceinline__ void store_g(const double (&acc)[K][VEC], const double* partials,
+                                                 uint32_t pos, int D, int q) {
+    float* gp = reinterpret_cast<float*>(const_cast<double*>(partials) + (size_t)pos * (size_t)D);
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int col = (k * LPR + q) * VEC;
+      if (col < D) {
+        V v;
+#pragma unroll
+        for (int x = 0; x < VEC; ++x) VecT<VEC>::set(v, x, (float)acc[k][x]);
+        store_vec<VEC>(gp + col, v);
+      }
+    }
   }
 };
 
@@ -716,7 +711,7 @@ struct RedCtx {
   uint64_t size0;
 };
 
-// Run-length encodes the sorted items: seg[s] = first item of segment s,
+// Run-length encodes items sorted by value: seg[s] = first item of segment s,
 // seg[S] = mp, sid[j] = segment of item j. Returns S (block-uniform).
 template <int NT, class IP, class SP, class DP>
 __device__ __forceinline__ uint32_t encode_segments(IP it, uint32_t mp, SP seg, DP sid, uint32_t* s_w) {
@@ -735,16 +730,16 @@ __device__ __forceinline__ uint32_t encode_segments(IP it, uint32_t mp, SP seg, 
   return S;
 }
 
-// Keys first inserted by this call (their items sort last) get rows
-// size0 + rank among all new keys of the call; the row replaces the slot in
-// the segment's first item, whose "fresh" bit stays set.
+// Keys first inserted by this call get rows size0 + rank among all new keys
+// of the call; the row replaces the slot in the segment's first item, whose
+// "fresh" bit stays set. The new row starts from its initial value and a zero
+// accumulator.
 template <int NT, class IP, class SP>
-__device__ __forceinline__ void resolve_new_rows(IP it, SP seg, uint32_t S, uint32_t mp, const RedCtx& c,
+__device__ __forceinline__ void resolve_new_rows(IP it, SP seg, uint32_t S, const RedCtx& c,
                                                  const NewKey* __restrict__ newlist,
                                                  const uint32_t* __restrict__ tile_cnt, int ntiles,
                                                  uint32_t* s_pref, uint32_t* s_w,
                                                  unsigned long long* s_w64, uint64_t* s_chunk) {
-  if (!item_fresh(it[mp - 1])) return;  // block-uniform: no key of this partition is new
   for (uint32_t s0 = 0; s0 < S; s0 += NT) {
     const uint32_t s = s0 + threadIdx.x;
     bool pend = false;
@@ -768,26 +763,26 @@ __device__ __forceinline__ void resolve_new_rows(IP it, SP seg, uint32_t S, uint
       const uint32_t row = (uint32_t)(c.size0 + rank);
       c.idx[slot / kSlots].row[slot % kSlots] = row;
       it[seg[s]] = make_item(true, row, item_low31(x));
-      // the new row starts from its initial value and a zero accumulator
-      const uint64_t s0 = splitmix_mix(key ^ c.seed);
+      const uint64_t s0k = splitmix_mix(key ^ c.seed);
       float* w = c.rows + (size_t)row * (size_t)c.D;
-      for (int col = 0; col < c.D; ++col) w[col] = init_elem(s0, col);
+      for (int col = 0; col < c.D; ++col) w[col] = init_elem(s0k, col);
       c.state[row] = 0.0f;
     }
   }
   __syncthreads();
 }
 
-// Applies every segment. Each lane group takes an equal contiguous slice of
-// the sorted items and walks it in batches: the gradient rows of a batch and
-// the row / accumulator of every segment that ends in the batch are loaded
-// together, then segments are summed (fp64) and the ones that start in the
-// slice are updated. The piece of a segment that began before the slice goes
-// to s_part[group]; after a barrier, the group where a cut segment began adds
-// the pieces of the following groups in slice order and updates it.
+// Update, phase A: the fp64 sum of every segment that needs one (more than
+// one item, or an in-tile sum as its only item) over items [0, mA), written
+// as fp32 g over the partials row of the segment's first item. Each lane
+// group takes an equal contiguous slice of the items and walks it in batches
+// (all gradient rows of a batch are loaded together). The piece of a segment
+// that began before the slice goes to s_part[group]; after a barrier, the
+// group where a cut segment began adds the pieces of the following groups in
+// slice order.
 template <class M, int NT, class IP, class SP, class DP>
-__device__ __forceinline__ void apply_segments(IP it, SP seg, DP sid, uint32_t mp, const RedCtx& c,
-                                               double* s_part) {
+__device__ __forceinline__ void sum_segments(IP it, SP seg, DP sid, uint32_t mA, const RedCtx& c,
+                                             double* s_part) {
   using Ops = SegmentOps<M>;
   constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
   constexpr int NG = (NT / 64) * RPW;
@@ -797,87 +792,82 @@ __device__ __forceinline__ void apply_segments(IP it, SP seg, DP sid, uint32_t m
   const int g = lane / LPR;
   const int q = lane % LPR;
   const int gid = (threadIdx.x >> 6) * RPW + g;
-  const int leader = g * LPR;
   const int D = c.D;
 
-  const uint32_t L = (mp + NG - 1) / NG;
-  const uint32_t lo = min(mp, (uint32_t)gid * L);
-  const uint32_t hi = min(mp, lo + L);
+  const uint32_t L = (mA + NG - 1) / NG;
+  const uint32_t lo = min(mA, (uint32_t)gid * L);
+  const uint32_t hi = min(mA, lo + L);
 
   double acc[K][VEC];
   Ops::zero(acc);
   for (uint32_t j0 = lo; j0 < hi; j0 += B) {
     V gv[B][K];
     double pv[B][K][VEC];
-    V wv[B][K];
-    float G0[B];
-    uint32_t sj[B];
-    bool ends[B], owned[B], summ[B];
+    uint32_t first[B];
+    bool use[B], ends[B], owned[B], summ[B];
 #pragma unroll
     for (int u = 0; u < B; ++u) {
       const uint32_t j = j0 + u;
+      use[u] = false;
       ends[u] = false;
       owned[u] = false;
       summ[u] = false;
-      G0[u] = 0.0f;
+      first[u] = 0;
       if (j < hi) {
         const uint64_t x = it[j];
-        sj[u] = sid[j];
+        const uint32_t sj = sid[j];
+        const uint32_t b = seg[sj], e = seg[sj + 1];
         summ[u] = item_summed(x);
-        if (summ[u]) {
-          const double* pr = c.partials + (size_t)item_pos(x) * (size_t)D;
+        use[u] = (e - b > 1) || summ[u];
+        ends[u] = e == j + 1;
+        owned[u] = b >= lo;
+        first[u] = b;
+        if (use[u]) {
+          if (summ[u]) {
+            const double* pr = c.partials + (size_t)item_pos(x) * (size_t)D;
 #pragma unroll
-          for (int k = 0; k < K; ++k) {
-            const int col = (k * LPR + q) * VEC;
+            for (int k = 0; k < K; ++k) {
+              const int col = (k * LPR + q) * VEC;
 #pragma unroll
-            for (int v = 0; v < VEC; ++v)
-              if (col + v < D) pv[u][k][v] = pr[col + v];
+              for (int v = 0; v < VEC; ++v)
+                if (col + v < D) pv[u][k][v] = pr[col + v];
+            }
+          } else {
+            const float* gr = c.grads + (size_t)item_pos(x) * (size_t)D;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              const int col = (k * LPR + q) * VEC;
+              if (col < D) gv[u][k] = load_vec<VEC>(gr + col);
+            }
           }
-        } else {
-          const float* gr = c.grads + (size_t)item_pos(x) * (size_t)D;
-#pragma unroll
-          for (int k = 0; k < K; ++k) {
-            const int col = (k * LPR + q) * VEC;
-            if (col < D) gv[u][k] = load_vec<VEC>(gr + col);
-          }
-        }
-        ends[u] = seg[sj[u] + 1] == j + 1;
-        owned[u] = seg[sj[u]] >= lo;
-        if (ends[u] && owned[u]) {
-          const uint32_t row = item_tag(it[seg[sj[u]]]);
-          Ops::load_w(wv[u], c.rows, row, false, 0, D, q);
-          G0[u] = c.state[row];
         }
       }
     }
 #pragma unroll
     for (int u = 0; u < B; ++u) {
-      const uint32_t j = j0 + u;
-      if (j < hi) {
+      if (!use[u]) continue;
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
-          const int col = (k * LPR + q) * VEC;
-          if (col < D) {
+      for (int k = 0; k < K; ++k) {
+        const int col = (k * LPR + q) * VEC;
+        if (col < D) {
+#pragma unroll
+          for (int x = 0; x < VEC; ++x)
+            acc[k][x] += summ[u] ? pv[u][k][x] : (double)VecT<VEC>::get(gv[u][k], x);
+        }
+      }
+      if (ends[u]) {
+        if (owned[u]) {
+          Ops::store_g(acc, c.partials, item_pos(it[first[u]]), D, q);
+        } else {
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            const int col = (k * LPR + q) * VEC;
 #pragma unroll
             for (int x = 0; x < VEC; ++x)
-              acc[k][x] += summ[u] ? pv[u][k][x] : (double)VecT<VEC>::get(gv[u][k], x);
+              if (col + x < D) s_part[(size_t)gid * D + col + x] = acc[k][x];
           }
         }
-        if (ends[u]) {
-          if (owned[u]) {
-            Ops::adagrad(acc, wv[u], G0[u], c.rows, c.state, item_tag(it[seg[sj[u]]]), D, q, leader, c.lr,
-                         c.eps);
-          } else {
-#pragma unroll
-            for (int k = 0; k < K; ++k) {
-              const int col = (k * LPR + q) * VEC;
-#pragma unroll
-              for (int x = 0; x < VEC; ++x)
-                if (col + x < D) s_part[(size_t)gid * D + col + x] = acc[k][x];
-            }
-          }
-          Ops::zero(acc);
-        }
+        Ops::zero(acc);
       }
     }
   }
@@ -911,12 +901,266 @@ __device__ __forceinline__ void apply_segments(IP it, SP seg, DP sid, uint32_t m
           if (col + x < D) acc[k][x] += s_part[(size_t)h * D + col + x];
       }
     }
-    const uint32_t row = item_tag(it[seg[tail]]);
-    V w[K];
-    Ops::load_w(w, c.rows, row, false, 0, D, q);
-    const float G = c.state[row];
-    Ops::adagrad(acc, w, G, c.rows, c.state, row, D, q, leader, c.lr, c.eps);
+    Ops::store_g(acc, c.partials, item_pos(it[seg[tail]]), D, q);
   }
+  __syncthreads();
+}
+
+// Update, phase B: one Adagrad step per segment. Segments are dealt to lane
+// groups in turn (group gid takes gid, gid + NG, ...), so the groups of a
+// wave update rows together. g is read from the partials row phase A wrote,
+// or from the segment's only gradient row.
+template <class M, int NT, class IP, class SP>
+__device__ __forceinline__ void update_segments(IP it, SP seg, uint32_t S, const RedCtx& c) {
+  using Ops = SegmentOps<M>;
+  constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
+  constexpr int NG = (NT / 64) * RPW;
+  constexpr int BB = (K * VEC >= 8) ? 2 : 4;
+  using V = typename VecT<VEC>::T;
+  const int lane = threadIdx.x & 63;
+  const int g = lane / LPR;
+  const int q = lane % LPR;
+  const int gid = (threadIdx.x >> 6) * RPW + g;
+  const int D = c.D;
+  const bool d_pow2 = (D & (D - 1)) == 0;
+  const double inv_d = 1.0 / (double)D;
+
+  for (uint32_t s0 = gid; s0 < S; s0 += (uint32_t)NG * BB) {
+    V gf[BB][K], w[BB][K];
+    float G[BB];
+    uint32_t row[BB];
+#pragma unroll
+    for (int u = 0; u < BB; ++u) {
+      const uint32_t s = s0 + u * NG;
+      G[u] = 0.0f;
+      row[u] = 0;
+      if (s < S) {
+        const uint32_t b = seg[s];
+        const uint64_t x = it[b];
+        row[u] = item_tag(x);
+        const bool from_a = (seg[s + 1] - b > 1) || item_summed(x);
+        const float* src = from_a ? reinterpret_cast<const float*>(c.partials + (size_t)item_pos(x) * (size_t)D)
+                                  : c.grads + (size_t)item_pos(x) * (size_t)D;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const int col = (k * LPR + q) * VEC;
+          if (col < D) {
+            gf[u][k] = load_vec<VEC>(src + col);
+            w[u][k] = load_vec<VEC>(c.rows + (size_t)row[u] * (size_t)D + col);
+          }
+        }
+        G[u] = c.state[row[u]];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < BB; ++u) {
+      if (s0 + u * NG < S)
+        Ops::adagrad(gf[u], w[u], G[u], c.rows, c.state, row[u], D, q, d_pow2, inv_d, c.lr, c.eps);
+    }
+  }
+}
+
+// Dynamic LDS of a reduce_update block, in bytes. The first region holds the
+// gathered items and the grouping tables; once items are grouped it is reused
+// for a chunk of new keys and then for the pieces of cut segments.
+template <int NT>
+struct RedLds {
+  static constexpr size_t it = 0;                                  // u64[kRedCap] gather order
+  static constexpr size_t hash = it + 8 * (size_t)kRedCap;          // u32[2 * kRedHash]
+  static constexpr size_t inv = hash + 8 * (size_t)kRedHash;        // u16[kRedHash]
+  static constexpr size_t pl = inv + 2 * (size_t)kRedHash;          // u16[kRedCap]
+  static constexpr size_t reuse = pl + 2 * (size_t)kRedCap;         // end of the reused region
+  static constexpr size_t sorted = reuse;                           // u64[kRedCap] grouped items
+  static constexpr size_t sid = sorted + 8 * (size_t)kRedCap;       // u16[kRedCap]
+  static constexpr size_t seg = sid + 2 * (size_t)kRedCap;          // u32[kRedCap + 1]
+  static constexpr size_t pref = (seg + 4 * ((size_t)kRedCap + 1) + 15) & ~(size_t)15;  // u32[NT + 1]
+  static constexpr size_t w = (pref + 4 * ((size_t)NT + 1) + 15) & ~(size_t)15;          // u32[NT / 64]
+  static constexpr size_t w64 = (w + 4 * (size_t)(NT / 64) + 15) & ~(size_t)15;          // u64[NT / 64]
+  static constexpr size_t base = w64 + 8 * (size_t)(NT / 64);                            // u64
+  static constexpr size_t total = base + 16;
+};
+
+// Threads of a reduce_update block: 1024 (one block per CU) unless the
+// pieces of cut segments (one fp64 row per lane group) would not fit the
+// reused LDS region.
+template <class M>
+struct RedCfg {
+  static constexpr int DMAX = M::LPR * M::K * M::VEC;
+  static constexpr int NT = DMAX <= 512 ? 1024 : 512;
+  static constexpr int NG = (NT / 64) * M::RPW;
+};
+
+// Number of entries of pl[b, e) (u16, LDS) below j.
+__device__ __forceinline__ uint32_t count_below(const uint16_t* pl, uint32_t b, uint32_t e, uint32_t j) {
+  uint32_t r = 0;
+  uint32_t i = b;
+  for (; i < e && (i & 7u); ++i) r += pl[i] < j ? 1u : 0u;
+  const uint4* p8 = reinterpret_cast<const uint4*>(pl);
+  for (; i + 16 <= e; i += 16) {
+    const uint4 a = p8[i >> 3], c = p8[(i >> 3) + 1];
+    const uint32_t wv[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
+#pragma unroll
+    for (int t = 0; t < 8; ++t) r += ((wv[t] & 0xFFFFu) < j ? 1u : 0u) + ((wv[t] >> 16) < j ? 1u : 0u);
+  }
+  for (; i < e; ++i) r += pl[i] < j ? 1u : 0u;
+  return r;
+}
+
+// Groups a partition's items by key in LDS.
+// In:  it[0, mp) in gather order (tiles ascending; a tile holds at most one
+//      item per key, so a key's items are in position order).
+// Out: sorted[] = the items grouped into segments, one per distinct key; the
+//      segments that need a sum (more than one item, or an in-tile sum) come
+//      first; items of a segment in gather order; seg[s] = first item of
+//      segment s, seg[S] = mp; sid[i] = segment of sorted item i.
+//      Returns S; *n_sum = segments of the first kind; *any_fresh = whether
+//      a segment holds a key new in the call.
+// Segment order: keys go to an LDS hash table with linear probing. The set of
+// occupied slots does not depend on the order of insertion, only which key
+// sits where inside a run of occupied slots does; keys are therefore given
+// the slots of their run in ascending order, and segments follow these
+// positions. So every order above depends only on the set of items, and sums
+// over segments are reproducible.
+template <int NT>
+__device__ __forceinline__ uint32_t group_items(const uint64_t* it, uint32_t mp, uint64_t* sorted,
+                                               uint16_t* sid, uint32_t* seg, uint32_t* hidx,
+                                               uint32_t* hcnt, uint16_t* inv, uint16_t* pl, uint32_t* s_w,
+                                               uint32_t* n_sum, bool* any_fresh) {
+  constexpr int IPT = (kRedCap + NT - 1) / NT;
+  constexpr int HPT = kRedHash / NT;
+  constexpr uint32_t kNone = 0xFFFFFFFFu;
+  constexpr uint32_t kMask = kRedHash - 1;
+  const int tid = threadIdx.x;
+  for (int h = tid; h < kRedHash; h += NT) {
+    hidx[h] = kNone;
+    hcnt[h] = 0u;
+  }
+  __syncthreads();
+
+  // 1. one hash slot per distinct group; count its items
+  uint32_t hs[IPT];
+#pragma unroll
+  for (int k = 0; k < IPT; ++k) {
+    const uint32_t j = tid + k * NT;
+    hs[k] = 0;
+    if (j < mp) {
+      const uint64_t gr = item_group(it[j]);
+      uint32_t h = (uint32_t)index_hash(gr) & kMask;
+      while (true) {
+        const uint32_t old = atomicCAS(&hidx[h], kNone, j);
+        if (old == kNone || item_group(it[old]) == gr) break;
+        h = (h + 1) & kMask;
+      }
+      hs[k] = h;
+      atomicAdd(&hcnt[h], 1u);
+    }
+  }
+  __syncthreads();
+
+  // 2. position of each key within its run of occupied slots
+#pragma unroll
+  for (int q = 0; q < HPT; ++q) {
+    const uint32_t h = tid * HPT + q;
+    const uint32_t j = hidx[h];
+    if (j != kNone) {
+      const uint64_t key = item_group(it[j]);
+      uint32_t cs = h;
+      while (hidx[(cs - 1) & kMask] != kNone) cs = (cs - 1) & kMask;
+      uint32_t r = 0;
+      for (uint32_t c = cs; hidx[c] != kNone; c = (c + 1) & kMask) r += item_group(it[hidx[c]]) < key ? 1u : 0u;
+      inv[(cs + r) & kMask] = (uint16_t)h;
+    }
+  }
+  __syncthreads();
+
+  // 3. number segments in position order, those needing a sum first;
+  // seg[u] = item count of segment u, hcnt[slot] = u
+  uint32_t cnt[HPT], hh[HPT];
+  bool need[HPT], occ[HPT];
+  uint32_t n_need = 0, n_one = 0;
+  bool fresh = false;
+#pragma unroll
+  for (int q = 0; q < HPT; ++q) {
+    const uint32_t pos = tid * HPT + q;
+    occ[q] = hidx[pos] != kNone;
+    need[q] = false;
+    cnt[q] = 0;
+    hh[q] = 0;
+    if (occ[q]) {
+      hh[q] = inv[pos];
+      const uint64_t x = it[hidx[hh[q]]];
+      cnt[q] = hcnt[hh[q]];
+      need[q] = cnt[q] > 1 || item_summed(x);
+      fresh |= item_fresh(x);
+      n_need += need[q] ? 1u : 0u;
+      n_one += need[q] ? 0u : 1u;
+    }
+  }
+  uint32_t tot;
+  const uint32_t pre = block_exclusive_scan<NT>(n_need | (n_one << 16), s_w, &tot);
+  const uint32_t NS = tot & 0xFFFFu, S = NS + (tot >> 16);
+  uint32_t u_need = pre & 0xFFFFu, u_one = NS + (pre >> 16);
+#pragma unroll
+  for (int q = 0; q < HPT; ++q) {
+    if (occ[q]) {
+      const uint32_t u = need[q] ? u_need++ : u_one++;
+      seg[u] = cnt[q];
+      hcnt[hh[q]] = u;
+    }
+  }
+  *n_sum = NS;
+  *any_fresh = __syncthreads_or(fresh ? 1 : 0) != 0;
+
+  // 4. segment offsets (exclusive scan of counts); hidx becomes the fill
+  // cursor of each segment
+  {
+    uint32_t c[IPT];
+    uint32_t sum = 0;
+#pragma unroll
+    for (int k = 0; k < IPT; ++k) {
+      const uint32_t x = tid * IPT + k;
+      c[k] = x < S ? seg[x] : 0u;
+      sum += c[k];
+    }
+    uint32_t t2;
+    uint32_t off = block_exclusive_scan<NT>(sum, s_w, &t2);
+#pragma unroll
+    for (int k = 0; k < IPT; ++k) {
+      const uint32_t x = tid * IPT + k;
+      if (x < S) seg[x] = off;
+      off += c[k];
+    }
+    if (tid == 0) seg[S] = mp;
+    for (uint32_t x = tid; x < S; x += NT) hidx[x] = 0u;
+  }
+  __syncthreads();
+
+  // 5. drop each item into its segment (any order within it)
+  uint32_t rs[IPT];
+#pragma unroll
+  for (int k = 0; k < IPT; ++k) {
+    const uint32_t j = tid + k * NT;
+    rs[k] = 0;
+    if (j < mp) {
+      rs[k] = hcnt[hs[k]];
+      pl[seg[rs[k]] + atomicAdd(&hidx[rs[k]], 1u)] = (uint16_t)j;
+    }
+  }
+  __syncthreads();
+
+  // 6. order a segment's items by gather index
+#pragma unroll
+  for (int k = 0; k < IPT; ++k) {
+    const uint32_t j = tid + k * NT;
+    if (j < mp) {
+      const uint32_t b = seg[rs[k]], e = seg[rs[k] + 1];
+      const uint32_t rank = e - b > 1 ? count_below(pl, b, e, j) : 0u;
+      sorted[b + rank] = it[j];
+      sid[b + rank] = (uint16_t)rs[k];
+    }
+  }
+  __syncthreads();
+  return S;
 }
 
 // Partition larger than the block's LDS share: the same steps on a global
@@ -959,43 +1203,66 @@ __device__ __forceinline__ void reduce_partition_global(uint32_t p, uint32_t mp,
   __syncthreads();
   block_bitonic_sort<NT>(it, P2);
   const uint32_t S = encode_segments<NT>(it, mp, seg, sid, s_w);
-  resolve_new_rows<NT>(it, seg, S, mp, c, newlist, tile_cnt, ntiles, s_pref, s_w, s_w64,
+  resolve_new_rows<NT>(it, seg, S, c, newlist, tile_cnt, ntiles, s_pref, s_w, s_w64,
                        reinterpret_cast<uint64_t*>(s_part));
-  apply_segments<M, NT>(it, seg, sid, mp, c, s_part);
+  sum_segments<M, NT>(it, seg, sid, mp, c, s_part);
+  update_segments<M, NT>(it, seg, S, c);
 }
 
-template <class M>
-__global__ __launch_bounds__(kRedThreads, (M::K * M::VEC >= 16) ? 2 : 4) void k_reduce_update(
+// ---------------------------------------------------------------------------
+// Put, second kernel (one block per partition): gathers the partition's
+// items, groups them into segments, gives keys new in the call their rows,
+// and writes the grouped items, per-item segment ranges and per-segment
+// descriptors for the two flat kernels that follow. A partition too large
+// for LDS is summed and updated here, in a global scratch area.
+// ---------------------------------------------------------------------------
+template <class M, int NT>
+__global__ __launch_bounds__(NT) void k_put_group(
     Bucket* __restrict__ idx, const uint64_t* __restrict__ items, const uint32_t* __restrict__ meta,
     int ntiles, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
-    const float* __restrict__ grads, const double* __restrict__ partials, float* __restrict__ rows, float* __restrict__ state, int D,
-    uint64_t seed, float lr, float eps, int64_t capacity, Ctrl* ctrl, uint64_t epoch,
-    uint64_t* __restrict__ spill, uint64_t spill_words) {
-  constexpr int NT = kRedThreads;
-  constexpr int NW = NT / 64;
-
-  extern __shared__ double s_dyn[];  // pieces of cut segments [lane groups][D], or a chunk of new keys
-  __shared__ uint64_t s_items[kRedCap];
-  __shared__ uint16_t s_sid[kRedCap];
-  __shared__ uint16_t s_seg[kRedCap + 1];
-  __shared__ uint32_t s_pref[NT + 1];
-  __shared__ uint32_t s_w[NW];
-  __shared__ unsigned long long s_w64[NW];
-  __shared__ uint64_t s_base;
+    const float* __restrict__ grads, const double* __restrict__ partials, float* __restrict__ rows,
+    float* __restrict__ state, int D, uint64_t seed, float lr, float eps, int64_t capacity, Ctrl* ctrl,
+    uint64_t epoch, uint64_t* __restrict__ spill, uint64_t spill_words, uint64_t* __restrict__ gitems,
+    uint32_t* __restrict__ gdesc, SegDesc* __restrict__ gsd, PartMeta* __restrict__ pmeta) {
+  using L = RedLds<NT>;
+  constexpr int IPT = (kRedCap + NT - 1) / NT;
+  extern __shared__ __align__(16) unsigned char s_raw[];
+  uint64_t* s_it = reinterpret_cast<uint64_t*>(s_raw + L::it);
+  uint32_t* s_hidx = reinterpret_cast<uint32_t*>(s_raw + L::hash);
+  uint32_t* s_hcnt = s_hidx + kRedHash;
+  uint16_t* s_inv = reinterpret_cast<uint16_t*>(s_raw + L::inv);
+  uint16_t* s_pl = reinterpret_cast<uint16_t*>(s_raw + L::pl);
+  double* s_part = reinterpret_cast<double*>(s_raw);              // reused region
+  uint64_t* s_chunk = reinterpret_cast<uint64_t*>(s_raw);         // reused region
+  uint64_t* s_sorted = reinterpret_cast<uint64_t*>(s_raw + L::sorted);
+  uint16_t* s_sid = reinterpret_cast<uint16_t*>(s_raw + L::sid);
+  uint32_t* s_seg = reinterpret_cast<uint32_t*>(s_raw + L::seg);
+  uint32_t* s_pref = reinterpret_cast<uint32_t*>(s_raw + L::pref);
+  uint32_t* s_w = reinterpret_cast<uint32_t*>(s_raw + L::w);
+  unsigned long long* s_w64 = reinterpret_cast<unsigned long long*>(s_raw + L::w64);
+  uint64_t* s_base = reinterpret_cast<uint64_t*>(s_raw + L::base);
 
   const uint32_t p = blockIdx.x;
   const int tid = threadIdx.x;
   const uint64_t size0 = ctrl->size[epoch & 1];
-  const bool any_new = ctrl->new_epoch == epoch;
+  const uint64_t new_e = ctrl->new_epoch, bad_e = ctrl->bad_epoch, ovf_e = ctrl->overflow_epoch;
   const uint32_t* pm = meta + (size_t)p * ntiles;
+  const bool one_chunk = ntiles <= NT;  // common case: one thread per tile
+  const uint32_t mt0 = one_chunk && tid < ntiles ? pm[tid] : 0u;
+  if (tid == 0) pmeta[p] = PartMeta{0u, 0u, 0u, 0u};  // nothing for the flat kernels unless set below
 
   // entries of this partition in every tile
-  uint64_t mp64 = 0;
-  for (int t = tid; t < ntiles; t += NT) mp64 += pm[t] >> 16;
-  const uint32_t mp = (uint32_t)block_sum_u64<NT>(mp64, s_w64);
+  uint32_t mp, pre0 = 0;
+  if (one_chunk) {
+    pre0 = block_exclusive_scan<NT>(mt0 >> 16, s_w, &mp);
+  } else {
+    uint64_t mp64 = 0;
+    for (int t = tid; t < ntiles; t += NT) mp64 += pm[t] >> 16;
+    mp = (uint32_t)block_sum_u64<NT>(mp64, s_w64);
+  }
 
-  const uint64_t Mnew = any_new ? count_new_keys<NT>(tile_cnt, ntiles, s_w64) : 0ull;
-  const int err = call_verdict(ctrl, epoch, size0, Mnew, capacity);
+  const uint64_t Mnew = new_e == epoch ? count_new_keys<NT>(tile_cnt, ntiles, s_w64) : 0ull;
+  const int err = call_verdict(ctrl, epoch, size0, Mnew, capacity, bad_e, ovf_e);
   if (mp == 0) return;
   if (err) {
     if (Mnew == 0) return;
@@ -1017,57 +1284,402 @@ __global__ __launch_bounds__(kRedThreads, (M::K * M::VEC >= 16) ? 2 : 4) void k_
   const RedCtx c{idx, grads, partials, rows, state, D, seed, lr, eps, size0};
   if (mp > (uint32_t)kRedCap) {
     reduce_partition_global<M, NT>(p, mp, items, meta, ntiles, c, newlist, tile_cnt, ctrl, spill, spill_words,
-                                   s_dyn, s_pref, s_w, s_w64, &s_base);
+                                   s_part, s_pref, s_w, s_w64, s_base);
     return;
   }
 
-  // ---- gather the partition's items into LDS ----
+  // ---- gather the partition's items into LDS, tile order ----
   {
     uint32_t dst = 0;
     for (int t0 = 0; t0 < ntiles; t0 += NT) {
-      const int t = t0 + tid;
-      const uint32_t mt = t < ntiles ? pm[t] : 0u;
-      const uint32_t off = mt & 0xFFFFu, cnt = mt >> 16;
-      uint32_t tot;
-      const uint32_t pre = block_exclusive_scan<NT>(cnt, s_w, &tot);
-      for (uint32_t j = 0; j < cnt; ++j) s_items[dst + pre + j] = items[(size_t)t * kPutTile + off + j];
+      const int nt = min(NT, ntiles - t0);
+      uint32_t mt = mt0, pre = pre0, tot = mp;
+      if (!one_chunk) {
+        mt = tid < nt ? pm[t0 + tid] : 0u;
+        pre = block_exclusive_scan<NT>(mt >> 16, s_w, &tot);
+      }
+      s_pref[tid] = pre | (mt << 16);  // items before this tile | offset in the tile
+      __syncthreads();
+      uint64_t v[IPT];
+#pragma unroll
+      for (int e = 0; e < IPT; ++e) {
+        const uint32_t k = tid + e * NT;
+        v[e] = 0;
+        if (k < tot) {
+          int lo = 0, hi = nt - 1;
+          while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if ((s_pref[mid] & 0xFFFFu) <= k) lo = mid;
+            else hi = mid - 1;
+          }
+          const uint32_t pe = s_pref[lo];
+          v[e] = items[(size_t)(t0 + lo) * kPutTile + (pe >> 16) + (k - (pe & 0xFFFFu))];
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < IPT; ++e) {
+        const uint32_t k = tid + e * NT;
+        if (k < tot) s_it[dst + k] = v[e];
+      }
       dst += tot;
+      __syncthreads();
     }
-    __syncthreads();
   }
 
-  // ---- sort: an item's rank is the number of smaller items (all items are
-  // distinct, since positions are) ----
-  {
-    constexpr int IPT = kRedCap / NT;
-    uint64_t v[IPT];
-    uint32_t rk[IPT];
-    int mine = 0;
-#pragma unroll
-    for (int j = 0; j < IPT; ++j) {
-      const uint32_t k = tid + j * NT;
-      v[j] = k < mp ? s_items[k] : ~0ull;
-      rk[j] = 0;
-      mine += k < mp ? 1 : 0;
+  uint32_t n_sum;
+  bool any_fresh;
+  const uint32_t S =
+      group_items<NT>(s_it, mp, s_sorted, s_sid, s_seg, s_hidx, s_hcnt, s_inv, s_pl, s_w, &n_sum, &any_fresh);
+  if (any_fresh)
+    resolve_new_rows<NT>(s_sorted, s_seg, S, c, newlist, tile_cnt, ntiles, s_pref, s_w, s_w64, s_chunk);
+
+  // ---- hand the grouped partition to the flat kernels ----
+  uint64_t* gi = gitems + (size_t)p * kRedCap;
+  uint32_t* gd = gdesc + (size_t)p * kRedCap;
+  SegDesc* sd = gsd + (size_t)p * kRedCap;
+  for (uint32_t i = tid; i < mp; i += NT) {
+    gi[i] = s_sorted[i];
+    const uint32_t s = s_sid[i];
+    gd[i] = s_seg[s] | (s_seg[s + 1] << 16);
+  }
+  for (uint32_t s = tid; s < S; s += NT) {
+    const uint32_t b = s_seg[s], e = s_seg[s + 1];
+    const uint64_t x = s_sorted[b];
+    const uint64_t xl = s_sorted[e - 1];
+    SegDesc d;
+    d.row = item_tag(x);
+    d.first = item_pos(x) | (item_summed(x) ? (1u << 30) : 0u) | (s < n_sum ? (1u << 31) : 0u);
+    d.last = item_pos(xl);
+    d.range = b | (e << 16);
+    sd[s] = d;
+  }
+  if (tid == 0) pmeta[p] = PartMeta{s_seg[n_sum], S, n_sum, 0u};
+}
+
+// Exclusive prefix over partitions of f(pmeta[p]) into out[0, np]; the block's
+// NT threads each take consecutive partitions. Returns the total.
+template <int NT, class F>
+__device__ __forceinline__ uint32_t partition_prefix(const PartMeta* __restrict__ pmeta, int np, uint32_t* out,
+                                                     uint32_t* s_w, F f) {
+  const int per = (np + NT - 1) / NT;
+  const int b = threadIdx.x * per;
+  uint32_t sum = 0;
+  for (int k = 0; k < per; ++k)
+    if (b + k < np) sum += f(pmeta[b + k]);
+  uint32_t tot;
+  uint32_t off = block_exclusive_scan<NT>(sum, s_w, &tot);
+  for (int k = 0; k < per; ++k) {
+    if (b + k < np) {
+      out[b + k] = off;
+      off += f(pmeta[b + k]);
     }
-    if (mine > 0) {
-      for (uint32_t e = 0; e < mp; ++e) {
-        const uint64_t a = s_items[e];
+  }
+  if (threadIdx.x == 0) out[np] = tot;
+  __syncthreads();
+  return tot;
+}
+
+// Largest partition p with pre[p] <= j (pre: np + 1 ascending prefix values).
+__device__ __forceinline__ int partition_of(const uint32_t* pre, int np, uint32_t j) {
+  int lo = 0, hi = np - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (pre[mid] <= j) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+// ---------------------------------------------------------------------------
+// Put, third kernel (flat): the fp64 sum of every segment that needs one. All
+// such items of all partitions form one sequence; each lane group of the
+// grid takes an equal contiguous slice (a block: NG consecutive slices) and
+// walks it in batches. A segment cut by slice boundaries inside a block is
+// completed in LDS by the group where it starts, adding the pieces of the
+// following groups in order. A segment that ends inside the block where it
+// starts gets g = fp32(sum) written over the partials row of its last item;
+// one that crosses a block boundary leaves one fp64 piece per block (the
+// tail piece of the block where it starts at [2 * block + 1], the head piece
+// of each later block at [2 * block]) for put_update to add.
+// ---------------------------------------------------------------------------
+template <class M, int NT>
+__global__ __launch_bounds__(NT) void k_put_sum(const uint64_t* __restrict__ gitems,
+                                                const uint32_t* __restrict__ gdesc,
+                                                const PartMeta* __restrict__ pmeta, int np,
+                                                const float* __restrict__ grads, double* __restrict__ partials,
+                                                double* __restrict__ gpiece, int D) {
+  using Ops = SegmentOps<M>;
+  constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
+  constexpr int NG = (NT / 64) * RPW;
+  constexpr int B = (K * VEC >= 8) ? 2 : 4;
+  using V = typename VecT<VEC>::T;
+  extern __shared__ __align__(16) unsigned char s_dyn[];  // pieces [NG][D] fp64, then prefix [np + 1]
+  double* s_part = reinterpret_cast<double*>(s_dyn);
+  uint32_t* s_pa = reinterpret_cast<uint32_t*>(s_dyn + sizeof(double) * (size_t)NG * D);
+  __shared__ uint32_t s_w[NT / 64];
+  const uint32_t NA = partition_prefix<NT>(pmeta, np, s_pa, s_w, [](const PartMeta& m) { return m.mA; });
+  if (NA == 0) return;
+  const int lane = threadIdx.x & 63;
+  const int g = lane / LPR;
+  const int q = lane % LPR;
+  const int gid = (threadIdx.x >> 6) * RPW + g;
+  const uint32_t G = gridDim.x * NG;
+  const uint32_t L = (NA + G - 1) / G;
+  const uint32_t blo = min(NA, blockIdx.x * (uint32_t)NG * L);  // the block's items
+  const uint32_t bhi = min(NA, blo + (uint32_t)NG * L);
+  if (blo >= bhi) return;  // block-uniform
+  const uint32_t lo = min(bhi, blo + (uint32_t)gid * L);
+  const uint32_t hi = min(bhi, lo + L);
+
+  auto put_row = [&](double* dst, const double (&a)[K][VEC]) {
 #pragma unroll
-        for (int j = 0; j < IPT; ++j) rk[j] += a < v[j] ? 1u : 0u;
+    for (int k = 0; k < K; ++k) {
+      const int col = (k * LPR + q) * VEC;
+#pragma unroll
+      for (int xx = 0; xx < VEC; ++xx)
+        if (col + xx < D) dst[col + xx] = a[k][xx];
+    }
+  };
+  auto add_row = [&](double (&a)[K][VEC], const double* src) {
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int col = (k * LPR + q) * VEC;
+#pragma unroll
+      for (int xx = 0; xx < VEC; ++xx)
+        if (col + xx < D) a[k][xx] += src[col + xx];
+    }
+  };
+
+  int p = partition_of(s_pa, np, lo < hi ? lo : blo);
+  double acc[K][VEC];
+  Ops::zero(acc);
+  // the batch's items are loaded one batch ahead of their gradient rows
+  uint64_t xn[B] = {};
+  uint32_t dn[B] = {}, bn[B] = {};
+  auto load_items = [&](uint32_t j0) {
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const uint32_t j = j0 + u;
+      xn[u] = 0;
+      dn[u] = 0;
+      bn[u] = 0;
+      if (j < hi) {
+        while (s_pa[p + 1] <= j) ++p;
+        const size_t at = (size_t)p * kRedCap + (j - s_pa[p]);
+        xn[u] = gitems[at];
+        dn[u] = gdesc[at];
+        bn[u] = s_pa[p];
       }
     }
-    __syncthreads();
+  };
+  if (lo < hi) load_items(lo);
+  // the first item's segment (for the block's head piece) and the last one's
+  const uint32_t first_fst = bn[0] + (dn[0] & 0xFFFFu), first_end = bn[0] + (dn[0] >> 16);
+  bool last_ends = true, last_owned = true;
+  uint32_t last_end = 0, last_base = 0;
+  int last_p = p;
+  for (uint32_t j0 = lo; j0 < hi; j0 += B) {
+    uint64_t x[B];
+    uint32_t fst[B], end[B], bs[B];
 #pragma unroll
-    for (int j = 0; j < IPT; ++j)
-      if (tid + j * NT < mp) s_items[rk[j]] = v[j];
-    __syncthreads();
+    for (int u = 0; u < B; ++u) {
+      x[u] = xn[u];
+      bs[u] = bn[u];
+      fst[u] = bn[u] + (dn[u] & 0xFFFFu);
+      end[u] = bn[u] + (dn[u] >> 16);
+    }
+    const int pcur = p;
+    V gv[B][K];
+    double pv[B][K][VEC];
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      if (j0 + u < hi) {
+        if (item_summed(x[u])) {
+          const double* pr = partials + (size_t)item_pos(x[u]) * (size_t)D;
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            const int col = (k * LPR + q) * VEC;
+#pragma unroll
+            for (int v = 0; v < VEC; ++v)
+              if (col + v < D) pv[u][k][v] = pr[col + v];
+          }
+        } else {
+          const float* gr = grads + (size_t)item_pos(x[u]) * (size_t)D;
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            const int col = (k * LPR + q) * VEC;
+            if (col < D) gv[u][k] = load_vec<VEC>(gr + col);
+          }
+        }
+      }
+    }
+    if (j0 + B < hi) load_items(j0 + B);
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const uint32_t j = j0 + u;
+      if (j >= hi) continue;
+      const bool summ = item_summed(x[u]);
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const int col = (k * LPR + q) * VEC;
+        if (col < D) {
+#pragma unroll
+          for (int xx = 0; xx < VEC; ++xx)
+            acc[k][xx] += summ ? pv[u][k][xx] : (double)VecT<VEC>::get(gv[u][k], xx);
+        }
+      }
+      last_ends = end[u] == j + 1;
+      last_owned = fst[u] >= lo;
+      last_end = end[u];
+      last_base = bs[u];
+      if (last_ends) {
+        if (last_owned) Ops::store_g(acc, partials, item_pos(x[u]), D, q);
+        else put_row(s_part + (size_t)gid * D, acc);  // the group's head piece
+        Ops::zero(acc);
+      }
+    }
+    // partition of the batch's last item (items of one segment share it)
+    last_p = pcur;
+    while (s_pa[last_p + 1] <= min(hi, j0 + B) - 1) ++last_p;
   }
+  // the slice ends inside a segment: the piece of one that began before the
+  // slice goes to LDS; one that began in the slice stays here as the tail
+  const bool tail = lo < hi && !last_ends && last_owned;
+  if (lo < hi && !last_ends && !last_owned) put_row(s_part + (size_t)gid * D, acc);
+  __syncthreads();
+  if (tail) {
+    for (uint32_t h = gid + 1; h < (uint32_t)NG && blo + h * L < last_end; ++h) add_row(acc, s_part + (size_t)h * D);
+    if (last_end <= bhi) {
+      // ends in this block: g over the partials row of its last item
+      const uint64_t xl = gitems[(size_t)last_p * kRedCap + (last_end - 1 - last_base)];
+      Ops::store_g(acc, partials, item_pos(xl), D, q);
+    } else {
+      put_row(gpiece + (size_t)(2 * blockIdx.x + 1) * D, acc);
+    }
+  }
+  // the block's first segment began in an earlier block: the sum of its
+  // pieces in this block is the block's head piece
+  if (gid == 0 && first_fst < blo) {
+    double hacc[K][VEC];
+    Ops::zero(hacc);
+    for (uint32_t h = 0; h < (uint32_t)NG && blo + h * L < first_end; ++h) add_row(hacc, s_part + (size_t)h * D);
+    put_row(gpiece + (size_t)(2 * blockIdx.x) * D, hacc);
+  }
+}
 
-  const uint32_t S = encode_segments<NT>(s_items, mp, s_seg, s_sid, s_w);
-  resolve_new_rows<NT>(s_items, s_seg, S, mp, c, newlist, tile_cnt, ntiles, s_pref, s_w, s_w64,
-                       reinterpret_cast<uint64_t*>(s_dyn));
-  apply_segments<M, NT>(s_items, s_seg, s_sid, mp, c, s_dyn);
+// ---------------------------------------------------------------------------
+// Put, fourth kernel (flat): one row-wise Adagrad step per segment. All
+// segments of all partitions form one sequence; each lane group takes an
+// equal contiguous share. g comes from put_sum (the partials row of the last
+// item, or the pieces of a segment that crosses put_sum blocks, added in
+// block order) or, for a single plain position, from its gradient row.
+// ---------------------------------------------------------------------------
+template <class M, int NT>
+__global__ __launch_bounds__(NT) void k_put_update(const SegDesc* __restrict__ gsd,
+                                                   const PartMeta* __restrict__ pmeta, int np,
+                                                   const float* __restrict__ grads,
+                                                   const double* __restrict__ partials,
+                                                   const double* __restrict__ gpiece, uint32_t sum_groups,
+                                                   uint32_t sum_group_block,
+                                                   float* __restrict__ rows, float* __restrict__ state, int D,
+                                                   float lr, float eps) {
+  using Ops = SegmentOps<M>;
+  constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
+  constexpr int NG = (NT / 64) * RPW;
+  constexpr int BB = (K * VEC >= 8) ? 2 : 4;
+  using V = typename VecT<VEC>::T;
+  extern __shared__ __align__(16) uint32_t s_pre[];  // [np + 1] items needing a sum, [np + 1] segments
+  __shared__ uint32_t s_w[NT / 64];
+  uint32_t* s_pa = s_pre;
+  uint32_t* s_ps = s_pre + np + 1;
+  const uint32_t NA = partition_prefix<NT>(pmeta, np, s_pa, s_w, [](const PartMeta& m) { return m.mA; });
+  const uint32_t ST = partition_prefix<NT>(pmeta, np, s_ps, s_w, [](const PartMeta& m) { return m.S; });
+  if (ST == 0) return;
+  const int lane = threadIdx.x & 63;
+  const int g = lane / LPR;
+  const int q = lane % LPR;
+  const uint32_t gidx = blockIdx.x * NG + (threadIdx.x >> 6) * RPW + g;
+  const uint32_t G = gridDim.x * NG;
+  const uint32_t per = (ST + G - 1) / G;
+  const uint32_t lo = min(ST, gidx * per);
+  const uint32_t hi = min(ST, lo + per);
+  // items of one put_sum block
+  const uint32_t LB = (NA + sum_groups - 1) / max(sum_groups, 1u) * sum_group_block;
+  const int D_ = D;
+  const bool d_pow2 = (D_ & (D_ - 1)) == 0;
+  const double inv_d = 1.0 / (double)D_;
+  int p = partition_of(s_ps, np, lo);
+
+  for (uint32_t s0 = lo; s0 < hi; s0 += BB) {
+    uint4 sd[BB];
+    uint32_t pa[BB];
+#pragma unroll
+    for (int u = 0; u < BB; ++u) {
+      const uint32_t s = s0 + u;
+      sd[u] = make_uint4(0, 0, 0, 0);
+      pa[u] = 0;
+      if (s < hi) {
+        while (s_ps[p + 1] <= s) ++p;
+        sd[u] = reinterpret_cast<const uint4*>(gsd)[(size_t)p * kRedCap + (s - s_ps[p])];
+        pa[u] = s_pa[p];
+      }
+    }
+    V gf[BB][K], w[BB][K];
+    float Gs[BB];
+    bool cut[BB];
+    uint32_t g1[BB], g2[BB];
+#pragma unroll
+    for (int u = 0; u < BB; ++u) {
+      Gs[u] = 0.0f;
+      cut[u] = false;
+      g1[u] = g2[u] = 0;
+      if (s0 + u < hi) {
+        const uint32_t row = sd[u].x;
+        const bool needs = (sd[u].y >> 31) != 0;
+        const float* src = grads + (size_t)(sd[u].y & 0x3FFFFFFFu) * (size_t)D_;
+        if (needs) {
+          const uint32_t A = pa[u] + (sd[u].w & 0xFFFFu), E = pa[u] + (sd[u].w >> 16);
+          g1[u] = A / LB;
+          g2[u] = (E - 1) / LB;
+          cut[u] = g1[u] != g2[u];
+          src = reinterpret_cast<const float*>(partials + (size_t)sd[u].z * (size_t)D_);
+        }
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const int col = (k * LPR + q) * VEC;
+          if (col < D_) {
+            if (!cut[u]) gf[u][k] = load_vec<VEC>(src + col);
+            w[u][k] = load_vec<VEC>(rows + (size_t)row * (size_t)D_ + col);
+          }
+        }
+        Gs[u] = state[row];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < BB; ++u) {
+      if (s0 + u >= hi) continue;
+      if (cut[u]) {
+        // tail piece of the first block, then the head pieces of the later ones
+        double acc[K][VEC];
+        Ops::zero(acc);
+        for (uint32_t h = g1[u]; h <= g2[u]; ++h) {
+          const double* pc = gpiece + (size_t)(2 * h + (h == g1[u] ? 1 : 0)) * D_;
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            const int col = (k * LPR + q) * VEC;
+#pragma unroll
+            for (int xx = 0; xx < VEC; ++xx)
+              if (col + xx < D_) acc[k][xx] += pc[col + xx];
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < K; ++k)
+#pragma unroll
+          for (int xx = 0; xx < VEC; ++xx) VecT<VEC>::set(gf[u][k], xx, (float)acc[k][xx]);
+      }
+      Ops::adagrad(gf[u], w[u], Gs[u], rows, state, sd[u].x, D_, q, d_pow2, inv_d, lr, eps);
+    }
+  }
 }
 
 // ===========================================================================
@@ -1140,15 +1752,16 @@ static hipError_t launch_get_t(const GetArgs& a, hipStream_t st, const LaunchHoo
 }
 
 template <class M>
-static size_t reduce_dyn_bytes(int D) {
-  const size_t part = (size_t)(kRedThreads / 64) * M::RPW * (size_t)D * sizeof(double);
-  const size_t chunk = (size_t)kChunk * sizeof(uint64_t);
-  return part > chunk ? part : chunk;
-}
-
-template <class M>
 static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHook& hook) {
+  constexpr int NT = RedCfg<M>::NT;
+  constexpr int NG = RedCfg<M>::NG;
+  using L = RedLds<NT>;
+  static_assert((size_t)NG * RedCfg<M>::DMAX * sizeof(double) <= L::reuse,
+                "cut-segment pieces must fit the reused LDS region");
+  static_assert((size_t)kChunk * sizeof(uint64_t) <= L::reuse, "new-key chunk must fit the reused LDS region");
+  static_assert(L::total <= 160 * 1024, "LDS budget of a gfx950 workgroup");
   const int64_t ntiles = (a.n + kPutTile - 1) / kPutTile;
+  const int np = 1 << a.pb;
   hook(K_PUT_PROBE, 0, st);
   hipLaunchKernelGGL(k_put_probe<M>, dim3((unsigned)ntiles), dim3(kPutThreads), 0, st, a.idx, a.nb_log2,
                      a.keys, a.grads, a.n, a.D, a.pb, (int)ntiles, a.items, a.meta, a.partials,
@@ -1156,19 +1769,36 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   hook(K_PUT_PROBE, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const size_t dyn = reduce_dyn_bytes<M>(a.D);
+  constexpr size_t sum_lds_max = sizeof(double) * NG * RedCfg<M>::DMAX + sizeof(uint32_t) * (kMaxParts + 1);
+  static_assert(sum_lds_max <= 160 * 1024, "LDS budget of a gfx950 workgroup");
   static bool attr_set = false;
   if (!attr_set) {
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_reduce_update<M>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, 96 * 1024);
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_put_group<M, NT>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)L::total);
+    if (e == hipSuccess)
+      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_put_sum<M, NT>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)sum_lds_max);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hook(K_REDUCE_UPDATE, 0, st);
-  hipLaunchKernelGGL(k_reduce_update<M>, dim3(1u << a.pb), dim3(kRedThreads), dyn, st, a.idx, a.items,
+  hook(K_PUT_GROUP, 0, st);
+  hipLaunchKernelGGL((k_put_group<M, NT>), dim3((unsigned)np), dim3(NT), L::total, st, a.idx, a.items,
                      a.meta, (int)ntiles, a.newlist, a.tile_cnt, a.grads, a.partials, a.rows, a.state,
-                     a.D, a.seed, a.lr, a.eps, a.capacity, a.ctrl, a.epoch, a.spill, a.spill_words);
-  hook(K_REDUCE_UPDATE, 1, st);
+                     a.D, a.seed, a.lr, a.eps, a.capacity, a.ctrl, a.epoch, a.spill, a.spill_words, a.gitems,
+                     a.gdesc, a.gsd, a.pmeta);
+  hook(K_PUT_GROUP, 1, st);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hook(K_PUT_SUM, 0, st);
+  hipLaunchKernelGGL((k_put_sum<M, NT>), dim3((unsigned)a.flat_blocks), dim3(NT),
+                     sizeof(double) * NG * (size_t)a.D + sizeof(uint32_t) * (np + 1), st, a.gitems, a.gdesc,
+                     a.pmeta, np, a.grads, a.partials, a.gpiece, a.D);
+  hook(K_PUT_SUM, 1, st);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hook(K_PUT_UPDATE, 0, st);
+  hipLaunchKernelGGL((k_put_update<M, NT>), dim3((unsigned)a.flat_blocks), dim3(NT),
+                     2 * sizeof(uint32_t) * (np + 1), st, a.gsd, a.pmeta, np, a.grads, a.partials, a.gpiece,
+                     (uint32_t)(a.flat_blocks * NG), (uint32_t)NG, a.rows, a.state, a.D, a.lr, a.eps);
+  hook(K_PUT_UPDATE, 1, st);
   return hipGetLastError();
 }
 
@@ -1192,6 +1822,15 @@ static hipError_t dispatch_map(int D, bool vec4, F f) {
   if (D <= 256) return f(MapD256{});
   if (D <= 512) return f(MapD512{});
   return f(MapD1024{});
+}
+
+int flat_groups_per_block(int D, bool vec4) {
+  int ng = 0;
+  (void)dispatch_map(D, vec4, [&](auto m) {
+    ng = RedCfg<decltype(m)>::NG;
+    return hipSuccess;
+  });
+  return ng;
 }
 
 hipError_t launch_get(const GetArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook) {
