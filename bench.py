@@ -28,13 +28,12 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0
 METRIC = "embedding get+put keys/sec and achieved HBM GB/s (% of peak), 1 MI355X"
-KERNELS = ("get_probe_gather", "assign_new", "put_probe", "put_group", "put_sum", "put_update")
+KERNELS = ("get_probe_gather", "assign_new", "put_probe", "put_group", "put_apply")
 
 
-def kernel_bytes(n, U, M, D, n_rep):
+def kernel_bytes(n, U, M, D):
     """Algorithmic bytes each kernel must move for one batch: n lookups, U
-    distinct keys of which M are new, rows of D fp32, n_rep positions whose
-    key occurs more than once in the batch."""
+    distinct keys of which M are new, rows of D fp32."""
     return {
         # keys in, one index entry (8 B tag + 4 B row) per distinct key,
         # distinct existing rows read, output rows written
@@ -45,11 +44,9 @@ def kernel_bytes(n, U, M, D, n_rep):
         "put_probe": 8 * n + 12 * U,
         # grouping works on scratch only
         "put_group": 0,
-        # gradient rows of repeated keys in
-        "put_sum": 4 * D * n_rep,
-        # gradient rows of keys seen once in, distinct rows read and written,
-        # accumulators read and written
-        "put_update": 4 * D * (n - n_rep) + 8 * D * U + 8 * U,
+        # gradient rows in, distinct rows read and written, accumulators read
+        # and written
+        "put_apply": 4 * D * n + 8 * D * U + 8 * U,
     }
 
 
@@ -133,8 +130,7 @@ def main():
     keys_h, grads_d, keys_d, UM = [], [], [], []
     for s in range(total_steps):
         k = wl.keys(s)
-        u, cnt = np.unique(k, return_counts=True)
-        n_rep = int(cnt[cnt > 1].sum())
+        u = np.unique(k)
         if known.size:
             pos = np.minimum(np.searchsorted(known, u), known.size - 1)
             new = u[known[pos] != u]
@@ -142,7 +138,7 @@ def main():
             new = u
         if new.size:
             known = np.union1d(known, new)
-        UM.append((u.size, new.size, n_rep))
+        UM.append((u.size, new.size))
         keys_d.append(torch.from_numpy(k.view(np.int64)).cuda())
         grads_d.append(torch.from_numpy(wl.grads(s)).cuda())
     out = torch.empty((n, D), dtype=torch.float32, device="cuda")
@@ -180,7 +176,7 @@ def main():
     assert t.sync() == mlkv.MLKV_OK
     ms_step = ms / args.steps
     keys_per_s = n * args.steps / (ms * 1e-3)
-    bytes_steps = [kernel_bytes(n, U, M, D, r) for (U, M, r) in UM]
+    bytes_steps = [kernel_bytes(n, U, M, D) for (U, M) in UM]
     alg_bytes = sum(sum(b.values()) for b in bytes_steps[first:first + args.steps])
     gbps = alg_bytes / (ms * 1e-3) / 1e9
     log(f"timed {args.steps} steps: {ms_step * 1e3:.2f} us/step (wall {wall * 1e3 / args.steps:.2f}), "
@@ -236,7 +232,7 @@ def main():
         cpu = cpu_baseline(wl, args.cpu_seconds)
         log(f"cpu baseline: {cpu['value'] / 1e6:.3f} M keys/s")
 
-    U_avg = float(np.mean([u for u, _, _ in UM[first:first + args.steps]]))
+    U_avg = float(np.mean([u for u, _ in UM[first:first + args.steps]]))
     res = {
         "metric": METRIC,
         "value": keys_per_s,

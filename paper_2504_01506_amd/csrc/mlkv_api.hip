@@ -39,10 +39,8 @@ struct mlkv_table {
   double* partials = nullptr;
   uint64_t* gitems = nullptr;
   uint32_t* gdesc = nullptr;
-  SegDesc* gsd = nullptr;
   PartMeta* pmeta = nullptr;
-  double* gpiece = nullptr;
-  int flat_blocks = 256;  // blocks of the flat put kernels: one per CU
+  int flat_blocks = 256;  // least number of put_apply blocks: one per CU
 
   // optional per-launch timing: HIP events recorded around each kernel
   struct ProfRec {
@@ -85,15 +83,11 @@ void free_workspace(mlkv_table* t) {
   (void)hipFree(t->partials);
   (void)hipFree(t->gitems);
   (void)hipFree(t->gdesc);
-  (void)hipFree(t->gsd);
   (void)hipFree(t->pmeta);
-  (void)hipFree(t->gpiece);
   t->partials = nullptr;
   t->gitems = nullptr;
   t->gdesc = nullptr;
-  t->gsd = nullptr;
   t->pmeta = nullptr;
-  t->gpiece = nullptr;
   t->newlist = nullptr;
   t->tile_cnt = nullptr;
   t->items = nullptr;
@@ -121,19 +115,18 @@ int ensure_workspace(mlkv_table* t, int64_t n) {
   hipError_t e = hipDeviceSynchronize();  // old scratch may still be in use
   if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
   free_workspace(t);
-  const int64_t get_tiles = (want + kGetTile - 1) / kGetTile;
-  const int64_t put_tiles = want / kPutTile;
+  const int64_t get_tiles = std::max<int64_t>((want + kGetTile - 1) / kGetTile, t->flat_blocks + 1);
+  // put tiles are kPutTile keys, or fewer so that every CU gets one
+  const int64_t put_tiles = std::max<int64_t>(want / kPutTile, t->flat_blocks + 1);
+  const int64_t slots = std::max<int64_t>(want, put_tiles * kPutTile);
   const uint64_t spill_words = 4ull * (uint64_t)want + 4096;
   const size_t np = (size_t)1 << part_bits(want);
-  const size_t ng = (size_t)std::max(flat_groups_per_block(t->dim, true), flat_groups_per_block(t->dim, false));
-  if ((e = dev_alloc(&t->newlist, sizeof(NewKey) * (size_t)want)) != hipSuccess ||
+  if ((e = dev_alloc(&t->newlist, sizeof(NewKey) * (size_t)slots)) != hipSuccess ||
       (e = dev_alloc(&t->gitems, sizeof(uint64_t) * np * kRedCap)) != hipSuccess ||
       (e = dev_alloc(&t->gdesc, sizeof(uint32_t) * np * kRedCap)) != hipSuccess ||
-      (e = dev_alloc(&t->gsd, sizeof(SegDesc) * np * kRedCap)) != hipSuccess ||
       (e = dev_alloc(&t->pmeta, sizeof(PartMeta) * np)) != hipSuccess ||
-      (e = dev_alloc(&t->gpiece, sizeof(double) * 2 * (size_t)t->flat_blocks * ng * (size_t)t->dim)) != hipSuccess ||
       (e = dev_alloc(&t->tile_cnt, sizeof(uint32_t) * (size_t)get_tiles)) != hipSuccess ||
-      (e = dev_alloc(&t->items, sizeof(uint64_t) * (size_t)want)) != hipSuccess ||
+      (e = dev_alloc(&t->items, sizeof(uint64_t) * (size_t)slots)) != hipSuccess ||
       (e = dev_alloc(&t->meta, sizeof(uint32_t) * (size_t)kMaxParts * (size_t)put_tiles)) != hipSuccess ||
       (e = dev_alloc(&t->spill, sizeof(uint64_t) * (size_t)spill_words)) != hipSuccess ||
       (e = dev_alloc(&t->partials, sizeof(double) * (size_t)want * (size_t)t->dim)) != hipSuccess) {
@@ -319,6 +312,10 @@ int mlkv_put_grad(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, i
   if (d_keys == nullptr || d_grads == nullptr) return fail(MLKV_EINVAL, "keys or grads is NULL");
   if ((rc = ensure_workspace(t, n)) != MLKV_OK) return rc;
   const uint32_t pb = part_bits(n);
+  // keys per put_probe tile: a multiple of 64, at most kPutTile, so that the
+  // tiles cover every CU when the batch is small
+  const int64_t per_cu = (n + t->flat_blocks - 1) / t->flat_blocks;
+  const int tlen = (int)std::min<int64_t>(kPutTile, std::max<int64_t>(64, (per_cu + 63) / 64 * 64));
   PutArgs a;
   a.idx = t->idx;
   a.nb_log2 = t->nb_log2;
@@ -333,6 +330,7 @@ int mlkv_put_grad(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, i
   a.lr = lr;
   a.eps = eps;
   a.pb = (int)pb;
+  a.tlen = tlen;
   a.items = t->items;
   a.partials = t->partials;
   a.meta = t->meta;
@@ -342,9 +340,7 @@ int mlkv_put_grad(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, i
   a.spill_words = t->spill_words;
   a.gitems = t->gitems;
   a.gdesc = t->gdesc;
-  a.gsd = t->gsd;
   a.pmeta = t->pmeta;
-  a.gpiece = t->gpiece;
   a.flat_blocks = t->flat_blocks;
   a.ctrl = t->ctrl;
   a.epoch = t->epoch;
@@ -470,8 +466,8 @@ int mlkv_profile_read(mlkv_table* t, double* total_ms, int64_t* launches) {
 }
 
 const char* mlkv_kernel_name(int kernel) {
-  static const char* names[K_COUNT] = {"get_probe_gather", "assign_new", "put_probe",
-                                       "put_group",        "put_sum",    "put_update"};
+  static const char* names[K_COUNT] = {"get_probe_gather", "assign_new", "put_probe", "put_group",
+                                       "put_apply"};
   return (kernel >= 0 && kernel < K_COUNT) ? names[kernel] : nullptr;
 }
 

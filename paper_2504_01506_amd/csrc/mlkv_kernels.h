@@ -23,12 +23,11 @@ enum KernelId : int {
   K_ASSIGN_NEW = 1,
   K_PUT_PROBE = 2,
   K_PUT_GROUP = 3,
-  K_PUT_SUM = 4,
-  K_PUT_UPDATE = 5,
-  K_COUNT = 6
+  K_PUT_APPLY = 4,
+  K_COUNT = 5
 };
 
-// Per-partition results of put_group, read by put_sum and put_update.
+// Per-partition results of put_group, read by put_apply.
 struct PartMeta {
   uint32_t mA;    // items of the segments that need a sum (stored first)
   uint32_t S;     // segments (distinct keys) of the partition
@@ -36,13 +35,6 @@ struct PartMeta {
   uint32_t pad;
 };
 
-// One segment (distinct key) of a partition, for put_update.
-struct SegDesc {
-  uint32_t row;    // row of the key
-  uint32_t first;  // position of its first item | in-tile-sum bit 30 | needs-sum bit 31
-  uint32_t last;   // position of its last item (where put_sum leaves g)
-  uint32_t range;  // index of its first item | index of its end << 16, within the partition
-};
 
 // Optional callback around each launch (phase 0 before, 1 after), on the launch stream.
 struct LaunchHook {
@@ -84,6 +76,7 @@ struct PutArgs {
   float lr;
   float eps;
   int pb;     // 2^pb partitions
+  int tlen;   // keys per put_probe tile (<= kPutTile)
   uint64_t* items;
   double* partials;  // [n][D] fp64 sums of keys repeated within a tile
   uint32_t* meta;
@@ -93,16 +86,11 @@ struct PutArgs {
   uint64_t spill_words;
   uint64_t* gitems;   // [partitions][kRedCap] grouped items
   uint32_t* gdesc;    // [partitions][kRedCap] segment range of each item
-  SegDesc* gsd;       // [partitions][kRedCap] segments
   PartMeta* pmeta;    // [partitions]
-  double* gpiece;     // [2 * flat groups][D] pieces of segments cut between put_sum slices
-  int flat_blocks;    // blocks of put_sum and put_update
+  int flat_blocks;    // least number of put_apply blocks (one per CU)
   Ctrl* ctrl;
   uint64_t epoch;
 };
-
-// Lane groups of a put_sum / put_update block for dim D (vec4: 16-byte rows).
-int flat_groups_per_block(int D, bool vec4);
 
 hipError_t launch_get(const GetArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook);
 hipError_t launch_put(const PutArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook);

@@ -354,7 +354,7 @@ constexpr int kTileHash = 2 * kPutTile;  // LDS hash slots per tile
 template <class M>
 __global__ __launch_bounds__(kPutThreads) void k_put_probe(
     Bucket* __restrict__ idx, uint32_t nb_log2, const uint64_t* __restrict__ keys,
-    const float* __restrict__ grads, int64_t n, int D, int pb, int ntiles, uint64_t* __restrict__ items,
+    const float* __restrict__ grads, int64_t n, int tlen, int D, int pb, int ntiles, uint64_t* __restrict__ items,
     uint32_t* __restrict__ meta, double* __restrict__ partials, NewKey* __restrict__ newlist,
     uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch) {
   constexpr int NT = kPutThreads;
@@ -375,7 +375,8 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
   const int NP = 1 << pb;
   const int tid = threadIdx.x;
   const int tile = blockIdx.x;
-  const int64_t base = (int64_t)tile * kPutTile;
+  const int64_t base = (int64_t)tile * tlen;        // batch position of the tile's entry 0
+  const int64_t sbase = (int64_t)tile * kPutTile;   // the tile's slots in items / newlist
   if (tile == 0 && tid == 0) ctrl->spill_next = 0;
   for (int d = tid; d < NP; d += NT) s_hist[d] = 0;
   for (int h = tid; h < kTileHash; h += NT) {
@@ -395,8 +396,9 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
 #pragma unroll
     for (int kk = 0; kk < KPT; ++kk) {
       const int64_t i = base + kk * NT + tid;
-      key[kk] = i < n ? keys[i] : kEmptyKey;
-      pr[kk] = {0, kPendingRow, i < n ? P_BAD : P_NONE};
+      const bool inb = kk * NT + tid < tlen && i < n;
+      key[kk] = inb ? keys[i] : kEmptyKey;
+      pr[kk] = {0, kPendingRow, inb ? P_BAD : P_NONE};
     }
 #pragma unroll
     for (int kk = 0; kk < KPT; ++kk) {
@@ -426,7 +428,7 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
     valid[kk] = pr[kk].status == P_HIT || pr[kk].status == P_NEW_MINE || pr[kk].status == P_NEW_OTHER;
     if (pr[kk].status == P_NEW_MINE) {
       const uint32_t j = atomicAdd(&s_cnt, 1u);
-      newlist[(size_t)base + j] = NewKey{key[kk], pr[kk].slot, 0u};
+      newlist[(size_t)sbase + j] = NewKey{key[kk], pr[kk].slot, 0u};
       ctrl->new_epoch = epoch;
     }
     const bool fresh = pr[kk].status != P_HIT;
@@ -596,7 +598,7 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
   __syncthreads();
 #pragma unroll
   for (int kk = 0; kk < KPT; ++kk)
-    if (emit[kk]) items[(size_t)base + s_hist[d[kk]] + r[kk]] = dup[kk] ? (x[kk] | kItemSummed) : x[kk];
+    if (emit[kk]) items[(size_t)sbase + s_hist[d[kk]] + r[kk]] = dup[kk] ? (x[kk] | kItemSummed) : x[kk];
   if (tid == 0) tile_cnt[tile] = s_cnt;
 }
 
@@ -1223,7 +1225,7 @@ __global__ __launch_bounds__(NT) void k_put_group(
     const float* __restrict__ grads, const double* __restrict__ partials, float* __restrict__ rows,
     float* __restrict__ state, int D, uint64_t seed, float lr, float eps, int64_t capacity, Ctrl* ctrl,
     uint64_t epoch, uint64_t* __restrict__ spill, uint64_t spill_words, uint64_t* __restrict__ gitems,
-    uint32_t* __restrict__ gdesc, SegDesc* __restrict__ gsd, PartMeta* __restrict__ pmeta) {
+    uint32_t* __restrict__ gdesc, PartMeta* __restrict__ pmeta) {
   using L = RedLds<NT>;
   constexpr int IPT = (kRedCap + NT - 1) / NT;
   extern __shared__ __align__(16) unsigned char s_raw[];
@@ -1333,25 +1335,13 @@ __global__ __launch_bounds__(NT) void k_put_group(
   if (any_fresh)
     resolve_new_rows<NT>(s_sorted, s_seg, S, c, newlist, tile_cnt, ntiles, s_pref, s_w, s_w64, s_chunk);
 
-  // ---- hand the grouped partition to the flat kernels ----
+  // ---- hand the grouped partition to the flat kernel ----
   uint64_t* gi = gitems + (size_t)p * kRedCap;
   uint32_t* gd = gdesc + (size_t)p * kRedCap;
-  SegDesc* sd = gsd + (size_t)p * kRedCap;
   for (uint32_t i = tid; i < mp; i += NT) {
     gi[i] = s_sorted[i];
     const uint32_t s = s_sid[i];
     gd[i] = s_seg[s] | (s_seg[s + 1] << 16);
-  }
-  for (uint32_t s = tid; s < S; s += NT) {
-    const uint32_t b = s_seg[s], e = s_seg[s + 1];
-    const uint64_t x = s_sorted[b];
-    const uint64_t xl = s_sorted[e - 1];
-    SegDesc d;
-    d.row = item_tag(x);
-    d.first = item_pos(x) | (item_summed(x) ? (1u << 30) : 0u) | (s < n_sum ? (1u << 31) : 0u);
-    d.last = item_pos(xl);
-    d.range = b | (e << 16);
-    sd[s] = d;
   }
   if (tid == 0) pmeta[p] = PartMeta{s_seg[n_sum], S, n_sum, 0u};
 }
@@ -1391,45 +1381,102 @@ __device__ __forceinline__ int partition_of(const uint32_t* pre, int np, uint32_
 }
 
 // ---------------------------------------------------------------------------
-// Put, third kernel (flat): the fp64 sum of every segment that needs one. All
-// such items of all partitions form one sequence; each lane group of the
-// grid takes an equal contiguous slice (a block: NG consecutive slices) and
-// walks it in batches. A segment cut by slice boundaries inside a block is
-// completed in LDS by the group where it starts, adding the pieces of the
-// following groups in order. A segment that ends inside the block where it
-// starts gets g = fp32(sum) written over the partials row of its last item;
-// one that crosses a block boundary leaves one fp64 piece per block (the
-// tail piece of the block where it starts at [2 * block + 1], the head piece
-// of each later block at [2 * block]) for put_update to add.
+// Put, third kernel (flat): sum and update. All items of segments that need a
+// sum (phase A items), over all partitions, form one sequence; block b takes
+// the contiguous range between b * NA / blocks and (b + 1) * NA / blocks,
+// each end moved forward to the next segment start, so that no segment is
+// split between blocks. Its lane groups split the range evenly and sum their
+// slices in fp64 (a segment cut between slices is completed by the group
+// where it starts, adding the following groups' pieces from LDS in order);
+// each completed segment leaves g = fp32(sum) over the partials row of its
+// last item and an entry (row, that position) in an LDS list. After a
+// barrier the groups split the list and the block's share of the keys seen
+// once (no sum needed, g is their gradient row) evenly and apply one
+// row-wise Adagrad step per key.
 // ---------------------------------------------------------------------------
+constexpr int kApplyItems = 2048;                    // phase-A items per block the grid is sized for
+constexpr int kApplyList = kApplyItems + kRedCap + 64;  // bound on segments one block completes
+
 template <class M, int NT>
-__global__ __launch_bounds__(NT) void k_put_sum(const uint64_t* __restrict__ gitems,
-                                                const uint32_t* __restrict__ gdesc,
-                                                const PartMeta* __restrict__ pmeta, int np,
-                                                const float* __restrict__ grads, double* __restrict__ partials,
-                                                double* __restrict__ gpiece, int D) {
+struct ApplyLds {
+  static constexpr int NG = (NT / 64) * M::RPW;
+  static constexpr int DMAX = M::LPR * M::K * M::VEC;
+  static constexpr size_t part = 0;                                              // fp64 [NG][D]
+  static constexpr size_t done = part + sizeof(double) * (size_t)NG * DMAX;       // uint2 [kApplyList]
+  static constexpr size_t pre = done + sizeof(uint2) * (size_t)kApplyList;        // u32 [2 * (np + 1)]
+  static constexpr size_t bytes(int np) { return pre + sizeof(uint32_t) * 2 * ((size_t)np + 1); }
+};
+
+template <class M, int NT>
+__global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ gitems,
+                                                  const uint32_t* __restrict__ gdesc,
+                                                  const PartMeta* __restrict__ pmeta, int np,
+                                                  const float* __restrict__ grads, double* __restrict__ partials,
+                                                  float* __restrict__ rows, float* __restrict__ state, int D,
+                                                  float lr, float eps, Ctrl* ctrl) {
   using Ops = SegmentOps<M>;
+  using LA = ApplyLds<M, NT>;
   constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
-  constexpr int NG = (NT / 64) * RPW;
+  constexpr int NG = LA::NG;
   constexpr int B = (K * VEC >= 8) ? 2 : 4;
+  constexpr int BB = (K * VEC >= 8) ? 2 : 4;
   using V = typename VecT<VEC>::T;
-  extern __shared__ __align__(16) unsigned char s_dyn[];  // pieces [NG][D] fp64, then prefix [np + 1]
-  double* s_part = reinterpret_cast<double*>(s_dyn);
-  uint32_t* s_pa = reinterpret_cast<uint32_t*>(s_dyn + sizeof(double) * (size_t)NG * D);
+  extern __shared__ __align__(16) unsigned char s_dyn[];
+  double* s_part = reinterpret_cast<double*>(s_dyn + LA::part);
+  uint2* s_done = reinterpret_cast<uint2*>(s_dyn + LA::done);
+  uint32_t* s_pa = reinterpret_cast<uint32_t*>(s_dyn + LA::pre);  // phase-A items before each partition
+  uint32_t* s_p1 = s_pa + np + 1;                                  // keys seen once before each partition
   __shared__ uint32_t s_w[NT / 64];
+  __shared__ uint32_t s_hpos[NG];     // position of the item where a group's head piece ended
+  __shared__ uint32_t s_slo[NG + 1];  // first item of each group's slice, and the block's end
+  __shared__ uint32_t s_rng[2];
+  __shared__ uint32_t s_ndone;
+
   const uint32_t NA = partition_prefix<NT>(pmeta, np, s_pa, s_w, [](const PartMeta& m) { return m.mA; });
-  if (NA == 0) return;
+  const uint32_t N1 = partition_prefix<NT>(pmeta, np, s_p1, s_w, [](const PartMeta& m) { return m.S - m.nsum; });
+  if (NA + N1 == 0) return;
   const int lane = threadIdx.x & 63;
   const int g = lane / LPR;
   const int q = lane % LPR;
   const int gid = (threadIdx.x >> 6) * RPW + g;
-  const uint32_t G = gridDim.x * NG;
-  const uint32_t L = (NA + G - 1) / G;
-  const uint32_t blo = min(NA, blockIdx.x * (uint32_t)NG * L);  // the block's items
-  const uint32_t bhi = min(NA, blo + (uint32_t)NG * L);
-  if (blo >= bhi) return;  // block-uniform
-  const uint32_t lo = min(bhi, blo + (uint32_t)gid * L);
-  const uint32_t hi = min(bhi, lo + L);
+  const uint32_t nb = gridDim.x, b = blockIdx.x;
+
+  // the block's phase-A range, both ends moved to segment starts
+  if (threadIdx.x < 2) {
+    uint32_t t = (uint32_t)((uint64_t)(b + threadIdx.x) * NA / nb);
+    if (t < NA) {
+      const int p0 = partition_of(s_pa, np, t);
+      const uint32_t d0 = gdesc[(size_t)p0 * kRedCap + (t - s_pa[p0])];
+      if (s_pa[p0] + (d0 & 0xFFFFu) != t) t = s_pa[p0] + (d0 >> 16);
+    }
+    s_rng[threadIdx.x] = t;
+  }
+  if (threadIdx.x == 0) s_ndone = 0;
+  __syncthreads();
+  const uint32_t A0 = s_rng[0], A1 = s_rng[1];
+  for (int h = threadIdx.x; h <= NG; h += NT) s_slo[h] = A0 + (uint32_t)((uint64_t)(A1 - A0) * h / NG);
+  // this group's keys seen once: [k0, k1) of the block's share
+  const uint32_t K0 = (uint32_t)((uint64_t)b * N1 / nb), K1 = (uint32_t)((uint64_t)(b + 1) * N1 / nb);
+  const uint32_t k0 = K0 + (uint32_t)((uint64_t)(K1 - K0) * gid / NG);
+  const uint32_t k1 = K0 + (uint32_t)((uint64_t)(K1 - K0) * (gid + 1) / NG);
+  // the first kPre items of this group's keys seen once are loaded now, to be
+  // used after phase A
+  constexpr int kPre = 2;
+  uint64_t xs[kPre];
+  {
+    int p1 = k0 < k1 ? partition_of(s_p1, np, k0) : 0;
+#pragma unroll
+    for (int u = 0; u < kPre; ++u) {
+      xs[u] = 0;
+      if (k0 + u < k1) {
+        while (s_p1[p1 + 1] <= k0 + u) ++p1;
+        const uint32_t first_single = s_pa[p1 + 1] - s_pa[p1];  // singles follow the phase-A items
+        xs[u] = gitems[(size_t)p1 * kRedCap + first_single + (k0 + u - s_p1[p1])];
+      }
+    }
+  }
+  __syncthreads();
+  const uint32_t lo = s_slo[gid], hi = s_slo[gid + 1];
 
   auto put_row = [&](double* dst, const double (&a)[K][VEC]) {
 #pragma unroll
@@ -1449,235 +1496,213 @@ __global__ __launch_bounds__(NT) void k_put_sum(const uint64_t* __restrict__ git
         if (col + xx < D) a[k][xx] += src[col + xx];
     }
   };
-
-  int p = partition_of(s_pa, np, lo < hi ? lo : blo);
-  double acc[K][VEC];
-  Ops::zero(acc);
-  // the batch's items are loaded one batch ahead of their gradient rows
-  uint64_t xn[B] = {};
-  uint32_t dn[B] = {}, bn[B] = {};
-  auto load_items = [&](uint32_t j0) {
-#pragma unroll
-    for (int u = 0; u < B; ++u) {
-      const uint32_t j = j0 + u;
-      xn[u] = 0;
-      dn[u] = 0;
-      bn[u] = 0;
-      if (j < hi) {
-        while (s_pa[p + 1] <= j) ++p;
-        const size_t at = (size_t)p * kRedCap + (j - s_pa[p]);
-        xn[u] = gitems[at];
-        dn[u] = gdesc[at];
-        bn[u] = s_pa[p];
-      }
+  auto complete = [&](uint32_t row, uint32_t pos) {
+    if (q == 0) {
+      const uint32_t k = atomicAdd(&s_ndone, 1u);
+      if (k < (uint32_t)kApplyList) s_done[k] = make_uint2(row, pos);
+      else atomicCAS(&ctrl->latched, 0, -4);  // cannot happen: kApplyList bounds a block's range
     }
   };
-  if (lo < hi) load_items(lo);
-  // the first item's segment (for the block's head piece) and the last one's
-  const uint32_t first_fst = bn[0] + (dn[0] & 0xFFFFu), first_end = bn[0] + (dn[0] >> 16);
-  bool last_ends = true, last_owned = true;
-  uint32_t last_end = 0, last_base = 0;
-  int last_p = p;
-  for (uint32_t j0 = lo; j0 < hi; j0 += B) {
-    uint64_t x[B];
-    uint32_t fst[B], end[B], bs[B];
-#pragma unroll
-    for (int u = 0; u < B; ++u) {
-      x[u] = xn[u];
-      bs[u] = bn[u];
-      fst[u] = bn[u] + (dn[u] & 0xFFFFu);
-      end[u] = bn[u] + (dn[u] >> 16);
-    }
-    const int pcur = p;
-    V gv[B][K];
-    double pv[B][K][VEC];
-#pragma unroll
-    for (int u = 0; u < B; ++u) {
-      if (j0 + u < hi) {
-        if (item_summed(x[u])) {
-          const double* pr = partials + (size_t)item_pos(x[u]) * (size_t)D;
-#pragma unroll
-          for (int k = 0; k < K; ++k) {
-            const int col = (k * LPR + q) * VEC;
-#pragma unroll
-            for (int v = 0; v < VEC; ++v)
-              if (col + v < D) pv[u][k][v] = pr[col + v];
-          }
-        } else {
-          const float* gr = grads + (size_t)item_pos(x[u]) * (size_t)D;
-#pragma unroll
-          for (int k = 0; k < K; ++k) {
-            const int col = (k * LPR + q) * VEC;
-            if (col < D) gv[u][k] = load_vec<VEC>(gr + col);
-          }
-        }
-      }
-    }
-    if (j0 + B < hi) load_items(j0 + B);
-#pragma unroll
-    for (int u = 0; u < B; ++u) {
-      const uint32_t j = j0 + u;
-      if (j >= hi) continue;
-      const bool summ = item_summed(x[u]);
-#pragma unroll
-      for (int k = 0; k < K; ++k) {
-        const int col = (k * LPR + q) * VEC;
-        if (col < D) {
-#pragma unroll
-          for (int xx = 0; xx < VEC; ++xx)
-            acc[k][xx] += summ ? pv[u][k][xx] : (double)VecT<VEC>::get(gv[u][k], xx);
-        }
-      }
-      last_ends = end[u] == j + 1;
-      last_owned = fst[u] >= lo;
-      last_end = end[u];
-      last_base = bs[u];
-      if (last_ends) {
-        if (last_owned) Ops::store_g(acc, partials, item_pos(x[u]), D, q);
-        else put_row(s_part + (size_t)gid * D, acc);  // the group's head piece
-        Ops::zero(acc);
-      }
-    }
-    // partition of the batch's last item (items of one segment share it)
-    last_p = pcur;
-    while (s_pa[last_p + 1] <= min(hi, j0 + B) - 1) ++last_p;
-  }
-  // the slice ends inside a segment: the piece of one that began before the
-  // slice goes to LDS; one that began in the slice stays here as the tail
-  const bool tail = lo < hi && !last_ends && last_owned;
-  if (lo < hi && !last_ends && !last_owned) put_row(s_part + (size_t)gid * D, acc);
-  __syncthreads();
-  if (tail) {
-    for (uint32_t h = gid + 1; h < (uint32_t)NG && blo + h * L < last_end; ++h) add_row(acc, s_part + (size_t)h * D);
-    if (last_end <= bhi) {
-      // ends in this block: g over the partials row of its last item
-      const uint64_t xl = gitems[(size_t)last_p * kRedCap + (last_end - 1 - last_base)];
-      Ops::store_g(acc, partials, item_pos(xl), D, q);
-    } else {
-      put_row(gpiece + (size_t)(2 * blockIdx.x + 1) * D, acc);
-    }
-  }
-  // the block's first segment began in an earlier block: the sum of its
-  // pieces in this block is the block's head piece
-  if (gid == 0 && first_fst < blo) {
-    double hacc[K][VEC];
-    Ops::zero(hacc);
-    for (uint32_t h = 0; h < (uint32_t)NG && blo + h * L < first_end; ++h) add_row(hacc, s_part + (size_t)h * D);
-    put_row(gpiece + (size_t)(2 * blockIdx.x) * D, hacc);
-  }
-}
 
-// ---------------------------------------------------------------------------
-// Put, fourth kernel (flat): one row-wise Adagrad step per segment. All
-// segments of all partitions form one sequence; each lane group takes an
-// equal contiguous share. g comes from put_sum (the partials row of the last
-// item, or the pieces of a segment that crosses put_sum blocks, added in
-// block order) or, for a single plain position, from its gradient row.
-// ---------------------------------------------------------------------------
-template <class M, int NT>
-__global__ __launch_bounds__(NT) void k_put_update(const SegDesc* __restrict__ gsd,
-                                                   const PartMeta* __restrict__ pmeta, int np,
-                                                   const float* __restrict__ grads,
-                                                   const double* __restrict__ partials,
-                                                   const double* __restrict__ gpiece, uint32_t sum_groups,
-                                                   uint32_t sum_group_block,
-                                                   float* __restrict__ rows, float* __restrict__ state, int D,
-                                                   float lr, float eps) {
-  using Ops = SegmentOps<M>;
-  constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
-  constexpr int NG = (NT / 64) * RPW;
-  constexpr int BB = (K * VEC >= 8) ? 2 : 4;
-  using V = typename VecT<VEC>::T;
-  extern __shared__ __align__(16) uint32_t s_pre[];  // [np + 1] items needing a sum, [np + 1] segments
-  __shared__ uint32_t s_w[NT / 64];
-  uint32_t* s_pa = s_pre;
-  uint32_t* s_ps = s_pre + np + 1;
-  const uint32_t NA = partition_prefix<NT>(pmeta, np, s_pa, s_w, [](const PartMeta& m) { return m.mA; });
-  const uint32_t ST = partition_prefix<NT>(pmeta, np, s_ps, s_w, [](const PartMeta& m) { return m.S; });
-  if (ST == 0) return;
-  const int lane = threadIdx.x & 63;
-  const int g = lane / LPR;
-  const int q = lane % LPR;
-  const uint32_t gidx = blockIdx.x * NG + (threadIdx.x >> 6) * RPW + g;
-  const uint32_t G = gridDim.x * NG;
-  const uint32_t per = (ST + G - 1) / G;
-  const uint32_t lo = min(ST, gidx * per);
-  const uint32_t hi = min(ST, lo + per);
-  // items of one put_sum block
-  const uint32_t LB = (NA + sum_groups - 1) / max(sum_groups, 1u) * sum_group_block;
-  const int D_ = D;
-  const bool d_pow2 = (D_ & (D_ - 1)) == 0;
-  const double inv_d = 1.0 / (double)D_;
-  int p = partition_of(s_ps, np, lo);
-
-  for (uint32_t s0 = lo; s0 < hi; s0 += BB) {
-    uint4 sd[BB];
-    uint32_t pa[BB];
+  // ---- phase A: fp64 sums of the block's segments ----
+  {
+    int p = lo < hi ? partition_of(s_pa, np, lo) : 0;
+    double acc[K][VEC];
+    Ops::zero(acc);
+    // a batch's items are loaded one batch ahead of their gradient rows
+    uint64_t xn[B] = {};
+    uint32_t dn[B] = {}, bn[B] = {};
+    auto load_items = [&](uint32_t j0) {
 #pragma unroll
-    for (int u = 0; u < BB; ++u) {
-      const uint32_t s = s0 + u;
-      sd[u] = make_uint4(0, 0, 0, 0);
-      pa[u] = 0;
-      if (s < hi) {
-        while (s_ps[p + 1] <= s) ++p;
-        sd[u] = reinterpret_cast<const uint4*>(gsd)[(size_t)p * kRedCap + (s - s_ps[p])];
-        pa[u] = s_pa[p];
-      }
-    }
-    V gf[BB][K], w[BB][K];
-    float Gs[BB];
-    bool cut[BB];
-    uint32_t g1[BB], g2[BB];
-#pragma unroll
-    for (int u = 0; u < BB; ++u) {
-      Gs[u] = 0.0f;
-      cut[u] = false;
-      g1[u] = g2[u] = 0;
-      if (s0 + u < hi) {
-        const uint32_t row = sd[u].x;
-        const bool needs = (sd[u].y >> 31) != 0;
-        const float* src = grads + (size_t)(sd[u].y & 0x3FFFFFFFu) * (size_t)D_;
-        if (needs) {
-          const uint32_t A = pa[u] + (sd[u].w & 0xFFFFu), E = pa[u] + (sd[u].w >> 16);
-          g1[u] = A / LB;
-          g2[u] = (E - 1) / LB;
-          cut[u] = g1[u] != g2[u];
-          src = reinterpret_cast<const float*>(partials + (size_t)sd[u].z * (size_t)D_);
+      for (int u = 0; u < B; ++u) {
+        const uint32_t j = j0 + u;
+        xn[u] = 0;
+        dn[u] = 0;
+        bn[u] = 0;
+        if (j < hi) {
+          while (s_pa[p + 1] <= j) ++p;
+          const size_t at = (size_t)p * kRedCap + (j - s_pa[p]);
+          xn[u] = gitems[at];
+          dn[u] = gdesc[at];
+          bn[u] = s_pa[p];
         }
+      }
+    };
+    if (lo < hi) load_items(lo);
+    bool last_ends = true, last_owned = true;
+    uint32_t last_end = 0, cur_row = 0;
+    for (uint32_t j0 = lo; j0 < hi; j0 += B) {
+      uint64_t x[B];
+      uint32_t fst[B], end[B];
+#pragma unroll
+      for (int u = 0; u < B; ++u) {
+        x[u] = xn[u];
+        fst[u] = bn[u] + (dn[u] & 0xFFFFu);
+        end[u] = bn[u] + (dn[u] >> 16);
+      }
+      V gv[B][K];
+      double pv[B][K][VEC];
+#pragma unroll
+      for (int u = 0; u < B; ++u) {
+        if (j0 + u < hi) {
+          if (item_summed(x[u])) {
+            const double* pr = partials + (size_t)item_pos(x[u]) * (size_t)D;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              const int col = (k * LPR + q) * VEC;
+#pragma unroll
+              for (int v = 0; v < VEC; ++v)
+                if (col + v < D) pv[u][k][v] = pr[col + v];
+            }
+          } else {
+            const float* gr = grads + (size_t)item_pos(x[u]) * (size_t)D;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              const int col = (k * LPR + q) * VEC;
+              if (col < D) gv[u][k] = load_vec<VEC>(gr + col);
+            }
+          }
+        }
+      }
+      if (j0 + B < hi) load_items(j0 + B);
+#pragma unroll
+      for (int u = 0; u < B; ++u) {
+        const uint32_t j = j0 + u;
+        if (j >= hi) continue;
+        if (fst[u] == j) cur_row = item_tag(x[u]);  // the first item of a segment carries its row
+        const bool summ = item_summed(x[u]);
 #pragma unroll
         for (int k = 0; k < K; ++k) {
           const int col = (k * LPR + q) * VEC;
-          if (col < D_) {
-            if (!cut[u]) gf[u][k] = load_vec<VEC>(src + col);
-            w[u][k] = load_vec<VEC>(rows + (size_t)row * (size_t)D_ + col);
+          if (col < D) {
+#pragma unroll
+            for (int xx = 0; xx < VEC; ++xx)
+              acc[k][xx] += summ ? pv[u][k][xx] : (double)VecT<VEC>::get(gv[u][k], xx);
           }
         }
-        Gs[u] = state[row];
+        last_ends = end[u] == j + 1;
+        last_owned = fst[u] >= lo;
+        last_end = end[u];
+        if (last_ends) {
+          if (last_owned) {
+            Ops::store_g(acc, partials, item_pos(x[u]), D, q);
+            complete(cur_row, item_pos(x[u]));
+          } else {
+            put_row(s_part + (size_t)gid * D, acc);  // the group's head piece
+            if (q == 0) s_hpos[gid] = item_pos(x[u]);
+          }
+          Ops::zero(acc);
+        }
       }
     }
+    // the slice ends inside a segment: the piece of one that began before the
+    // slice goes to LDS; one that began in the slice is completed below
+    const bool tail = lo < hi && !last_ends && last_owned;
+    if (lo < hi && !last_ends && !last_owned) put_row(s_part + (size_t)gid * D, acc);
+    __syncthreads();
+    if (tail) {
+      // the segment ends in slice hl, inside this block: add the pieces of
+      // slices gid+1 .. hl in order (empty slices hold no piece), loading
+      // kTU at a time
+      constexpr int kTU = 2;
+      uint32_t hl = gid + 1;
+      while (hl + 1 < (uint32_t)NG && s_slo[hl + 1] < last_end) ++hl;
+      for (uint32_t h0 = gid + 1; h0 <= hl; h0 += kTU) {
+        double pcs[kTU][K][VEC];
+        bool use[kTU];
 #pragma unroll
-    for (int u = 0; u < BB; ++u) {
-      if (s0 + u >= hi) continue;
-      if (cut[u]) {
-        // tail piece of the first block, then the head pieces of the later ones
-        double acc[K][VEC];
-        Ops::zero(acc);
-        for (uint32_t h = g1[u]; h <= g2[u]; ++h) {
-          const double* pc = gpiece + (size_t)(2 * h + (h == g1[u] ? 1 : 0)) * D_;
+        for (int t = 0; t < kTU; ++t) {
+          const uint32_t h = h0 + t;
+          use[t] = h <= hl && s_slo[h] < s_slo[h + 1];
+          if (use[t]) {
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              const int col = (k * LPR + q) * VEC;
+#pragma unroll
+              for (int xx = 0; xx < VEC; ++xx)
+                if (col + xx < D) pcs[t][k][xx] = s_part[(size_t)h * D + col + xx];
+            }
+          }
+        }
+#pragma unroll
+        for (int t = 0; t < kTU; ++t) {
+          if (!use[t]) continue;
 #pragma unroll
           for (int k = 0; k < K; ++k) {
             const int col = (k * LPR + q) * VEC;
 #pragma unroll
             for (int xx = 0; xx < VEC; ++xx)
-              if (col + xx < D_) acc[k][xx] += pc[col + xx];
+              if (col + xx < D) acc[k][xx] += pcs[t][k][xx];
           }
         }
-#pragma unroll
-        for (int k = 0; k < K; ++k)
-#pragma unroll
-          for (int xx = 0; xx < VEC; ++xx) VecT<VEC>::set(gf[u][k], xx, (float)acc[k][xx]);
       }
-      Ops::adagrad(gf[u], w[u], Gs[u], rows, state, sd[u].x, D_, q, d_pow2, inv_d, lr, eps);
+      Ops::store_g(acc, partials, s_hpos[hl], D, q);
+      complete(cur_row, s_hpos[hl]);
+    }
+    __syncthreads();
+  }
+
+  // ---- phase B: one Adagrad step per key ----
+  const bool d_pow2 = (D & (D - 1)) == 0;
+  const double inv_d = 1.0 / (double)D;
+  const uint32_t nd = min(s_ndone, (uint32_t)kApplyList);
+  auto update_batch = [&](const uint32_t (&row)[BB], const float* const (&src)[BB], const bool (&on)[BB]) {
+    V gf[BB][K], w[BB][K];
+    float Gs[BB];
+#pragma unroll
+    for (int u = 0; u < BB; ++u) {
+      Gs[u] = 0.0f;
+      if (on[u]) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const int col = (k * LPR + q) * VEC;
+          if (col < D) {
+            gf[u][k] = load_vec<VEC>(src[u] + col);
+            w[u][k] = load_vec<VEC>(rows + (size_t)row[u] * (size_t)D + col);
+          }
+        }
+        Gs[u] = state[row[u]];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < BB; ++u)
+      if (on[u]) Ops::adagrad(gf[u], w[u], Gs[u], rows, state, row[u], D, q, d_pow2, inv_d, lr, eps);
+  };
+  // this group's work: completed segments [e0, e1) (g over the partials row
+  // of their last item), then keys seen once [k0, k1) (g is their gradient row)
+  {
+    const uint32_t e0 = (uint32_t)((uint64_t)nd * gid / NG), e1 = (uint32_t)((uint64_t)nd * (gid + 1) / NG);
+    const uint32_t nm = e1 - e0, nw = nm + (k1 - k0);
+    int p1 = k0 < k1 ? partition_of(s_p1, np, k0) : 0;
+    for (uint32_t w0 = 0; w0 < nw; w0 += BB) {
+      uint32_t row[BB];
+      const float* src[BB];
+      bool on[BB];
+#pragma unroll
+      for (int u = 0; u < BB; ++u) {
+        const uint32_t w = w0 + u;
+        on[u] = w < nw;
+        row[u] = 0;
+        src[u] = grads;
+        if (w < nm) {
+          const uint2 dv = s_done[e0 + w];
+          row[u] = dv.x;
+          src[u] = reinterpret_cast<const float*>(partials + (size_t)dv.y * (size_t)D);
+        } else if (w < nw) {
+          const uint32_t sgl = w - nm;
+          uint64_t x = 0;
+#pragma unroll
+          for (int t = 0; t < kPre; ++t)
+            if (sgl == (uint32_t)t) x = xs[t];
+          if (sgl >= (uint32_t)kPre) {
+            while (s_p1[p1 + 1] <= k0 + sgl) ++p1;
+            x = gitems[(size_t)p1 * kRedCap + (s_pa[p1 + 1] - s_pa[p1]) + (k0 + sgl - s_p1[p1])];
+          }
+          row[u] = item_tag(x);
+          src[u] = grads + (size_t)item_pos(x) * (size_t)D;
+        }
+      }
+      update_batch(row, src, on);
     }
   }
 }
@@ -1758,26 +1783,27 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   using L = RedLds<NT>;
   static_assert((size_t)NG * RedCfg<M>::DMAX * sizeof(double) <= L::reuse,
                 "cut-segment pieces must fit the reused LDS region");
+  static_assert(ApplyLds<M, NT>::NG == NG, "put_apply lane groups");
   static_assert((size_t)kChunk * sizeof(uint64_t) <= L::reuse, "new-key chunk must fit the reused LDS region");
   static_assert(L::total <= 160 * 1024, "LDS budget of a gfx950 workgroup");
-  const int64_t ntiles = (a.n + kPutTile - 1) / kPutTile;
+  const int64_t ntiles = (a.n + a.tlen - 1) / a.tlen;
   const int np = 1 << a.pb;
   hook(K_PUT_PROBE, 0, st);
   hipLaunchKernelGGL(k_put_probe<M>, dim3((unsigned)ntiles), dim3(kPutThreads), 0, st, a.idx, a.nb_log2,
-                     a.keys, a.grads, a.n, a.D, a.pb, (int)ntiles, a.items, a.meta, a.partials,
+                     a.keys, a.grads, a.n, a.tlen, a.D, a.pb, (int)ntiles, a.items, a.meta, a.partials,
                      a.newlist, a.tile_cnt, a.ctrl, a.epoch);
   hook(K_PUT_PROBE, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  constexpr size_t sum_lds_max = sizeof(double) * NG * RedCfg<M>::DMAX + sizeof(uint32_t) * (kMaxParts + 1);
-  static_assert(sum_lds_max <= 160 * 1024, "LDS budget of a gfx950 workgroup");
+  constexpr size_t apply_lds_max = ApplyLds<M, NT>::bytes(kMaxParts);
+  static_assert(apply_lds_max <= 160 * 1024, "LDS budget of a gfx950 workgroup");
   static bool attr_set = false;
   if (!attr_set) {
     e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_put_group<M, NT>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)L::total);
     if (e == hipSuccess)
-      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_put_sum<M, NT>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)sum_lds_max);
+      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_put_apply<M, NT>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)apply_lds_max);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
@@ -1785,20 +1811,15 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   hipLaunchKernelGGL((k_put_group<M, NT>), dim3((unsigned)np), dim3(NT), L::total, st, a.idx, a.items,
                      a.meta, (int)ntiles, a.newlist, a.tile_cnt, a.grads, a.partials, a.rows, a.state,
                      a.D, a.seed, a.lr, a.eps, a.capacity, a.ctrl, a.epoch, a.spill, a.spill_words, a.gitems,
-                     a.gdesc, a.gsd, a.pmeta);
+                     a.gdesc, a.pmeta);
   hook(K_PUT_GROUP, 1, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hook(K_PUT_SUM, 0, st);
-  hipLaunchKernelGGL((k_put_sum<M, NT>), dim3((unsigned)a.flat_blocks), dim3(NT),
-                     sizeof(double) * NG * (size_t)a.D + sizeof(uint32_t) * (np + 1), st, a.gitems, a.gdesc,
-                     a.pmeta, np, a.grads, a.partials, a.gpiece, a.D);
-  hook(K_PUT_SUM, 1, st);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  hook(K_PUT_UPDATE, 0, st);
-  hipLaunchKernelGGL((k_put_update<M, NT>), dim3((unsigned)a.flat_blocks), dim3(NT),
-                     2 * sizeof(uint32_t) * (np + 1), st, a.gsd, a.pmeta, np, a.grads, a.partials, a.gpiece,
-                     (uint32_t)(a.flat_blocks * NG), (uint32_t)NG, a.rows, a.state, a.D, a.lr, a.eps);
-  hook(K_PUT_UPDATE, 1, st);
+  const int apply_blocks = (int)std::max<int64_t>(a.flat_blocks, (a.n + kApplyItems - 1) / kApplyItems);
+  const size_t apply_lds = ApplyLds<M, NT>::bytes(np);
+  hook(K_PUT_APPLY, 0, st);
+  hipLaunchKernelGGL((k_put_apply<M, NT>), dim3((unsigned)apply_blocks), dim3(NT), apply_lds, st, a.gitems, a.gdesc, a.pmeta, np, a.grads, a.partials,
+                     a.rows, a.state, a.D, a.lr, a.eps, a.ctrl);
+  hook(K_PUT_APPLY, 1, st);
   return hipGetLastError();
 }
 
@@ -1822,15 +1843,6 @@ static hipError_t dispatch_map(int D, bool vec4, F f) {
   if (D <= 256) return f(MapD256{});
   if (D <= 512) return f(MapD512{});
   return f(MapD1024{});
-}
-
-int flat_groups_per_block(int D, bool vec4) {
-  int ng = 0;
-  (void)dispatch_map(D, vec4, [&](auto m) {
-    ng = RedCfg<decltype(m)>::NG;
-    return hipSuccess;
-  });
-  return ng;
 }
 
 hipError_t launch_get(const GetArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook) {
