@@ -659,13 +659,21 @@ struct SegmentOps {
     const float m = (float)(d_pow2 ? sq * inv_d : sq / (double)D);
     const float Gn = __fadd_rn(G, m);
     const float den = __fadd_rn(__builtin_sqrtf(Gn), eps);  // correctly rounded sqrt
+    // g / den for the whole row from one correctly rounded reciprocal y:
+    // q0 = RN(g * y), r = RN(g - den * q0) and RN(q0 + r * y), each of the
+    // last two one FMA, give the correctly rounded quotient (Markstein's
+    // correction step; holds without underflow or overflow)
+    const float y = __fdiv_rn(1.0f, den);
 #pragma unroll
     for (int k = 0; k < K; ++k) {
       const int col = (k * LPR + q) * VEC;
       if (col < D) {
 #pragma unroll
         for (int x = 0; x < VEC; ++x) {
-          const float qv = __fdiv_rn(VecT<VEC>::get(g[k], x), den);
+          const float gx = VecT<VEC>::get(g[k], x);
+          const float q0 = __fmul_rn(gx, y);
+          const float r = __builtin_fmaf(-q0, den, gx);
+          const float qv = __builtin_fmaf(r, y, q0);
           const float p = __fmul_rn(lr, qv);
           VecT<VEC>::set(w[k], x, __fsub_rn(VecT<VEC>::get(w[k], x), p));
         }
@@ -1394,16 +1402,26 @@ __device__ __forceinline__ int partition_of(const uint32_t* pre, int np, uint32_
 // once (no sum needed, g is their gradient row) evenly and apply one
 // row-wise Adagrad step per key.
 // ---------------------------------------------------------------------------
-constexpr int kApplyItems = 2048;                    // phase-A items per block the grid is sized for
-constexpr int kApplyList = kApplyItems + kRedCap + 64;  // bound on segments one block completes
+// put_apply blocks: kPerCU per CU at least, and at most about kItems phase-A
+// items each (the grid grows with the batch). Two 512-thread blocks per CU
+// overlap one block's barriers and combination steps with the other's loads.
+template <class M>
+struct ApplyCfg {
+  static constexpr int NT = RedCfg<M>::NT < 512 ? RedCfg<M>::NT : 512;
+  static constexpr int kPerCU = 1024 / NT;
+  static constexpr int kItems = 2 * NT;
+};
 
 template <class M, int NT>
 struct ApplyLds {
   static constexpr int NG = (NT / 64) * M::RPW;
   static constexpr int DMAX = M::LPR * M::K * M::VEC;
+  // segments one block can complete: at most its items, which are at most
+  // kItems plus one segment (a partition's items) beyond the even share
+  static constexpr int kList = ApplyCfg<M>::kItems + kRedCap + 64;
   static constexpr size_t part = 0;                                              // fp64 [NG][D]
-  static constexpr size_t done = part + sizeof(double) * (size_t)NG * DMAX;       // uint2 [kApplyList]
-  static constexpr size_t pre = done + sizeof(uint2) * (size_t)kApplyList;        // u32 [2 * (np + 1)]
+  static constexpr size_t done = part + sizeof(double) * (size_t)NG * DMAX;       // uint2 [kList]
+  static constexpr size_t pre = done + sizeof(uint2) * (size_t)kList;             // u32 [2 * (np + 1)]
   static constexpr size_t bytes(int np) { return pre + sizeof(uint32_t) * 2 * ((size_t)np + 1); }
 };
 
@@ -1499,8 +1517,8 @@ __global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ g
   auto complete = [&](uint32_t row, uint32_t pos) {
     if (q == 0) {
       const uint32_t k = atomicAdd(&s_ndone, 1u);
-      if (k < (uint32_t)kApplyList) s_done[k] = make_uint2(row, pos);
-      else atomicCAS(&ctrl->latched, 0, -4);  // cannot happen: kApplyList bounds a block's range
+      if (k < (uint32_t)LA::kList) s_done[k] = make_uint2(row, pos);
+      else atomicCAS(&ctrl->latched, 0, -4);  // cannot happen: kList bounds a block's range
     }
   };
 
@@ -1645,7 +1663,7 @@ __global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ g
   // ---- phase B: one Adagrad step per key ----
   const bool d_pow2 = (D & (D - 1)) == 0;
   const double inv_d = 1.0 / (double)D;
-  const uint32_t nd = min(s_ndone, (uint32_t)kApplyList);
+  const uint32_t nd = min(s_ndone, (uint32_t)LA::kList);
   auto update_batch = [&](const uint32_t (&row)[BB], const float* const (&src)[BB], const bool (&on)[BB]) {
     V gf[BB][K], w[BB][K];
     float Gs[BB];
@@ -1783,7 +1801,7 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   using L = RedLds<NT>;
   static_assert((size_t)NG * RedCfg<M>::DMAX * sizeof(double) <= L::reuse,
                 "cut-segment pieces must fit the reused LDS region");
-  static_assert(ApplyLds<M, NT>::NG == NG, "put_apply lane groups");
+  constexpr int NTA = ApplyCfg<M>::NT;
   static_assert((size_t)kChunk * sizeof(uint64_t) <= L::reuse, "new-key chunk must fit the reused LDS region");
   static_assert(L::total <= 160 * 1024, "LDS budget of a gfx950 workgroup");
   const int64_t ntiles = (a.n + a.tlen - 1) / a.tlen;
@@ -1795,14 +1813,14 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   hook(K_PUT_PROBE, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  constexpr size_t apply_lds_max = ApplyLds<M, NT>::bytes(kMaxParts);
+  constexpr size_t apply_lds_max = ApplyLds<M, NTA>::bytes(kMaxParts);
   static_assert(apply_lds_max <= 160 * 1024, "LDS budget of a gfx950 workgroup");
   static bool attr_set = false;
   if (!attr_set) {
     e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_put_group<M, NT>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)L::total);
     if (e == hipSuccess)
-      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_put_apply<M, NT>),
+      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_put_apply<M, NTA>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)apply_lds_max);
     if (e != hipSuccess) return e;
     attr_set = true;
@@ -1814,10 +1832,11 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
                      a.gdesc, a.pmeta);
   hook(K_PUT_GROUP, 1, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  const int apply_blocks = (int)std::max<int64_t>(a.flat_blocks, (a.n + kApplyItems - 1) / kApplyItems);
-  const size_t apply_lds = ApplyLds<M, NT>::bytes(np);
+  const int apply_blocks = (int)std::max<int64_t>((int64_t)a.flat_blocks * ApplyCfg<M>::kPerCU,
+                                                  (a.n + ApplyCfg<M>::kItems - 1) / ApplyCfg<M>::kItems);
+  const size_t apply_lds = ApplyLds<M, NTA>::bytes(np);
   hook(K_PUT_APPLY, 0, st);
-  hipLaunchKernelGGL((k_put_apply<M, NT>), dim3((unsigned)apply_blocks), dim3(NT), apply_lds, st, a.gitems, a.gdesc, a.pmeta, np, a.grads, a.partials,
+  hipLaunchKernelGGL((k_put_apply<M, NTA>), dim3((unsigned)apply_blocks), dim3(NTA), apply_lds, st, a.gitems, a.gdesc, a.pmeta, np, a.grads, a.partials,
                      a.rows, a.state, a.D, a.lr, a.eps, a.ctrl);
   hook(K_PUT_APPLY, 1, st);
   return hipGetLastError();
