@@ -164,6 +164,14 @@ __device__ __forceinline__ Probe probe_key(Bucket* __restrict__ idx, uint32_t nb
 // ---------------------------------------------------------------------------
 // Block-wide helpers
 // ---------------------------------------------------------------------------
+// Barrier that orders LDS only: global loads and stores issued before it stay
+// in flight (a full __syncthreads waits for them too).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Exclusive scan over the block; NT threads, s_w needs NT/64 words.
 template <int NT>
 __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s_w, uint32_t* total) {
@@ -176,7 +184,7 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
     if (lane >= o) x += y;
   }
   if (lane == 63) s_w[w] = x;
-  __syncthreads();
+  lds_barrier();
   if (w == 0) {
     uint32_t s = lane < NT / 64 ? s_w[lane] : 0u;
 #pragma unroll
@@ -186,10 +194,10 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
     }
     if (lane < NT / 64) s_w[lane] = s;
   }
-  __syncthreads();
+  lds_barrier();
   const uint32_t pre = (w > 0 ? s_w[w - 1] : 0u) + x - v;
   *total = s_w[NT / 64 - 1];
-  __syncthreads();
+  lds_barrier();
   return pre;
 }
 
@@ -200,11 +208,11 @@ __device__ __forceinline__ uint64_t block_sum_u64(uint64_t v, unsigned long long
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor((unsigned long long)v, o, 64);
   if (lane == 0) s_w[w] = v;
-  __syncthreads();
+  lds_barrier();
   uint64_t t = 0;
 #pragma unroll
   for (int j = 0; j < NT / 64; ++j) t += s_w[j];
-  __syncthreads();
+  lds_barrier();
   return t;
 }
 

@@ -363,13 +363,13 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
   constexpr int NG = (NT / 64) * RPW;
   using V = typename VecT<VEC>::T;
   __shared__ uint32_t s_hist[kMaxParts];
-  __shared__ unsigned long long s_hkey[kTileHash];  // group of each hash slot
-  __shared__ uint32_t s_hcnt[kTileHash];            // occurrences of the group in the tile
-  __shared__ uint32_t s_hfirst[kTileHash];          // first entry holding the group
-  __shared__ uint32_t s_hcur[kTileHash];            // fill cursor of the group's entry list
-  __shared__ uint16_t s_hdup[kTileHash];            // index of a repeated group
-  __shared__ uint16_t s_lanes[kPutTile];            // entries of repeated groups, grouped
-  __shared__ uint16_t s_doff[kPutTile / 2 + 1];     // start of each repeated group's entries
+  __shared__ unsigned long long s_hkey[kTileHash];  // key of each hash slot
+  __shared__ uint32_t s_hcnt[kTileHash];            // occurrences of the key in the tile
+  __shared__ uint32_t s_hfirst[kTileHash];          // first entry holding the key
+  __shared__ uint32_t s_hcur[kTileHash];            // fill cursor of the key's entry list
+  __shared__ uint16_t s_hdup[kTileHash];            // index of a repeated key
+  __shared__ uint16_t s_lanes[kPutTile];            // entries of repeated keys, grouped
+  __shared__ uint16_t s_doff[kPutTile / 2 + 1];     // start of each repeated key's entries
   __shared__ uint32_t s_w[NT / 64];
   __shared__ uint32_t s_cnt;
   const int NP = 1 << pb;
@@ -387,60 +387,42 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
   }
   if (tid == 0) s_cnt = 0;
 
-  // entry e = kk * NT + tid of the tile is batch position base + e
+  // entry e = kk * NT + tid of the tile is batch position base + e. The
+  // index buckets of the tile's keys are loaded first; while they are in
+  // flight the tile's keys are deduplicated in LDS (a key and its slot are
+  // one to one), and the probe reads the buckets afterwards.
   uint64_t key[KPT];
-  Probe pr[KPT];
-  {
-    uint64_t hb[KPT];
-    BucketView bv[KPT];
+  bool inb[KPT];
+  uint64_t hb[KPT];
+  BucketView bv[KPT];
 #pragma unroll
-    for (int kk = 0; kk < KPT; ++kk) {
-      const int64_t i = base + kk * NT + tid;
-      const bool inb = kk * NT + tid < tlen && i < n;
-      key[kk] = inb ? keys[i] : kEmptyKey;
-      pr[kk] = {0, kPendingRow, inb ? P_BAD : P_NONE};
-    }
+  for (int kk = 0; kk < KPT; ++kk) {
+    const int64_t i = base + kk * NT + tid;
+    inb[kk] = kk * NT + tid < tlen && i < n;
+    key[kk] = inb[kk] ? keys[i] : kEmptyKey;
+  }
 #pragma unroll
-    for (int kk = 0; kk < KPT; ++kk) {
-      if (key[kk] != kEmptyKey) {
-        hb[kk] = home_bucket(key[kk], nb_log2);
-        bv[kk] = load_bucket(idx + hb[kk]);
-      }
-    }
-#pragma unroll
-    for (int kk = 0; kk < KPT; ++kk) {
-      if (key[kk] != kEmptyKey) {
-        pr[kk] = probe_with(idx, nb_log2, key[kk], true, hb[kk], bv[kk]);
-        if (pr[kk].status == P_OVERFLOW) ctrl->overflow_epoch = epoch;
-      } else if (pr[kk].status == P_BAD) {
-        ctrl->bad_epoch = epoch;
-      }
+  for (int kk = 0; kk < KPT; ++kk) {
+    if (key[kk] != kEmptyKey) {
+      hb[kk] = home_bucket(key[kk], nb_log2);
+      bv[kk] = load_bucket(idx + hb[kk]);
     }
   }
-  __syncthreads();
+  lds_barrier();  // the hash table is initialised
 
-  uint64_t x[KPT];
   uint32_t hs[KPT];
   bool valid[KPT];
 #pragma unroll
   for (int kk = 0; kk < KPT; ++kk) {
     const int e = kk * NT + tid;
-    valid[kk] = pr[kk].status == P_HIT || pr[kk].status == P_NEW_MINE || pr[kk].status == P_NEW_OTHER;
-    if (pr[kk].status == P_NEW_MINE) {
-      const uint32_t j = atomicAdd(&s_cnt, 1u);
-      newlist[(size_t)sbase + j] = NewKey{key[kk], pr[kk].slot, 0u};
-      ctrl->new_epoch = epoch;
-    }
-    const bool fresh = pr[kk].status != P_HIT;
-    x[kk] = valid[kk] ? make_item(fresh, fresh ? pr[kk].slot : pr[kk].row, (uint32_t)(base + e)) : ~0ull;
-    // count the tile's occurrences of every group
+    valid[kk] = key[kk] != kEmptyKey;
+    // count the tile's occurrences of every key
     hs[kk] = 0;
     if (valid[kk]) {
-      const uint64_t grp = item_group(x[kk]);
-      uint32_t h = (uint32_t)index_hash(grp) & (kTileHash - 1);
+      uint32_t h = (uint32_t)index_hash(key[kk]) & (kTileHash - 1);
       while (true) {
-        const unsigned long long old = atomicCAS(&s_hkey[h], ~0ull, (unsigned long long)grp);
-        if (old == ~0ull || old == grp) break;
+        const unsigned long long old = atomicCAS(&s_hkey[h], ~0ull, (unsigned long long)key[kk]);
+        if (old == ~0ull || old == key[kk]) break;
         h = (h + 1) & (kTileHash - 1);
       }
       hs[kk] = h;
@@ -448,7 +430,7 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
       atomicMin(&s_hfirst[h], (uint32_t)e);
     }
   }
-  __syncthreads();
+  lds_barrier();
   uint32_t cnt[KPT];
   bool dup[KPT], owner[KPT];
   uint32_t n_own = 0, l_own = 0;
@@ -476,7 +458,7 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
     }
   }
   if (tid == 0) s_doff[ndup] = (uint16_t)nlanes;
-  __syncthreads();
+  lds_barrier();
   uint32_t my_off[KPT];
 #pragma unroll
   for (int kk = 0; kk < KPT; ++kk) {
@@ -486,7 +468,7 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
       s_lanes[my_off[kk] + atomicAdd(&s_hcur[hs[kk]], 1u)] = (uint16_t)(kk * NT + tid);
     }
   }
-  __syncthreads();
+  lds_barrier();
   // sort each repeated group's entry list: an entry's rank is the number of
   // smaller entries in its group's list
   uint32_t rank[KPT];
@@ -498,15 +480,15 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
       for (uint32_t m = 0; m < cnt[kk]; ++m) rank[kk] += s_lanes[my_off[kk] + m] < e ? 1u : 0u;
     }
   }
-  __syncthreads();
+  lds_barrier();
 #pragma unroll
   for (int kk = 0; kk < KPT; ++kk)
     if (dup[kk]) s_lanes[my_off[kk] + rank[kk]] = (uint16_t)(kk * NT + tid);
-  __syncthreads();
+  lds_barrier();
 
-  // each lane group sums the rows of repeated groups, positions ascending
+  // each lane group sums the rows of repeated keys, positions ascending
   {
-    constexpr int UNR = (K * VEC >= 8) ? 4 : 8;
+    constexpr int UNR = (K * VEC >= 16) ? 2 : (K * VEC >= 8) ? 4 : 8;
     const int lane = tid & 63;
     const int g = lane / LPR;
     const int q = lane % LPR;
@@ -556,6 +538,32 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
     }
   }
 
+  // probe (and insert) each key now that its bucket has arrived
+  Probe pr[KPT];
+#pragma unroll
+  for (int kk = 0; kk < KPT; ++kk) {
+    pr[kk] = {0, kPendingRow, inb[kk] ? P_BAD : P_NONE};
+    if (key[kk] != kEmptyKey) {
+      pr[kk] = probe_with(idx, nb_log2, key[kk], true, hb[kk], bv[kk]);
+      if (pr[kk].status == P_OVERFLOW) ctrl->overflow_epoch = epoch;
+    } else if (pr[kk].status == P_BAD) {
+      ctrl->bad_epoch = epoch;
+    }
+  }
+  uint64_t x[KPT];
+#pragma unroll
+  for (int kk = 0; kk < KPT; ++kk) {
+    const int e = kk * NT + tid;
+    valid[kk] = pr[kk].status == P_HIT || pr[kk].status == P_NEW_MINE || pr[kk].status == P_NEW_OTHER;
+    if (pr[kk].status == P_NEW_MINE) {
+      const uint32_t j = atomicAdd(&s_cnt, 1u);
+      newlist[(size_t)sbase + j] = NewKey{key[kk], pr[kk].slot, 0u};
+      ctrl->new_epoch = epoch;
+    }
+    const bool fresh = pr[kk].status != P_HIT;
+    x[kk] = valid[kk] ? make_item(fresh, fresh ? pr[kk].slot : pr[kk].row, (uint32_t)(base + e)) : ~0ull;
+  }
+
   // emit single positions, and one summed item per repeated key
   bool emit[KPT];
   uint32_t d[KPT], r[KPT];
@@ -569,7 +577,7 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
       r[kk] = atomicAdd(&s_hist[d[kk]], 1u);
     }
   }
-  __syncthreads();
+  lds_barrier();
   constexpr int PER = kMaxParts / NT;
   uint32_t c[PER];
   uint32_t sum = 0;
@@ -589,13 +597,13 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
     if (dd < NP) meta[(size_t)dd * ntiles + tile] = off | (c[j] << 16);
     off += c[j];
   }
-  __syncthreads();
+  lds_barrier();
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
     const int dd = tid * PER + j;
     if (dd < NP) s_hist[dd] = offs[j];
   }
-  __syncthreads();
+  lds_barrier();
 #pragma unroll
   for (int kk = 0; kk < KPT; ++kk)
     if (emit[kk]) items[(size_t)sbase + s_hist[d[kk]] + r[kk]] = dup[kk] ? (x[kk] | kItemSummed) : x[kk];
@@ -1045,7 +1053,7 @@ __device__ __forceinline__ uint32_t group_items(const uint64_t* it, uint32_t mp,
     hidx[h] = kNone;
     hcnt[h] = 0u;
   }
-  __syncthreads();
+  lds_barrier();
 
   // 1. one hash slot per distinct group; count its items
   uint32_t hs[IPT];
@@ -1065,7 +1073,7 @@ __device__ __forceinline__ uint32_t group_items(const uint64_t* it, uint32_t mp,
       atomicAdd(&hcnt[h], 1u);
     }
   }
-  __syncthreads();
+  lds_barrier();
 
   // 2. position of each key within its run of occupied slots
 #pragma unroll
@@ -1081,7 +1089,7 @@ __device__ __forceinline__ uint32_t group_items(const uint64_t* it, uint32_t mp,
       inv[(cs + r) & kMask] = (uint16_t)h;
     }
   }
-  __syncthreads();
+  lds_barrier();
 
   // 3. number segments in position order, those needing a sum first;
   // seg[u] = item count of segment u, hcnt[slot] = u
@@ -1143,7 +1151,7 @@ __device__ __forceinline__ uint32_t group_items(const uint64_t* it, uint32_t mp,
     if (tid == 0) seg[S] = mp;
     for (uint32_t x = tid; x < S; x += NT) hidx[x] = 0u;
   }
-  __syncthreads();
+  lds_barrier();
 
   // 5. drop each item into its segment (any order within it)
   uint32_t rs[IPT];
@@ -1156,7 +1164,7 @@ __device__ __forceinline__ uint32_t group_items(const uint64_t* it, uint32_t mp,
       pl[seg[rs[k]] + atomicAdd(&hidx[rs[k]], 1u)] = (uint16_t)j;
     }
   }
-  __syncthreads();
+  lds_barrier();
 
   // 6. order a segment's items by gather index
 #pragma unroll
@@ -1169,7 +1177,7 @@ __device__ __forceinline__ uint32_t group_items(const uint64_t* it, uint32_t mp,
       sid[b + rank] = (uint16_t)rs[k];
     }
   }
-  __syncthreads();
+  lds_barrier();
   return S;
 }
 
@@ -1373,7 +1381,7 @@ __device__ __forceinline__ uint32_t partition_prefix(const PartMeta* __restrict_
     }
   }
   if (threadIdx.x == 0) out[np] = tot;
-  __syncthreads();
+  lds_barrier();
   return tot;
 }
 
@@ -1470,7 +1478,7 @@ __global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ g
     s_rng[threadIdx.x] = t;
   }
   if (threadIdx.x == 0) s_ndone = 0;
-  __syncthreads();
+  lds_barrier();
   const uint32_t A0 = s_rng[0], A1 = s_rng[1];
   for (int h = threadIdx.x; h <= NG; h += NT) s_slo[h] = A0 + (uint32_t)((uint64_t)(A1 - A0) * h / NG);
   // this group's keys seen once: [k0, k1) of the block's share
@@ -1493,7 +1501,7 @@ __global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ g
       }
     }
   }
-  __syncthreads();
+  lds_barrier();  // the prefetched items stay in flight
   const uint32_t lo = s_slo[gid], hi = s_slo[gid + 1];
 
   auto put_row = [&](double* dst, const double (&a)[K][VEC]) {
@@ -1617,7 +1625,7 @@ __global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ g
     // slice goes to LDS; one that began in the slice is completed below
     const bool tail = lo < hi && !last_ends && last_owned;
     if (lo < hi && !last_ends && !last_owned) put_row(s_part + (size_t)gid * D, acc);
-    __syncthreads();
+    lds_barrier();
     if (tail) {
       // the segment ends in slice hl, inside this block: add the pieces of
       // slices gid+1 .. hl in order (empty slices hold no piece), loading
