@@ -28,6 +28,13 @@
 //       all fp32 operations separate (no fused multiply-add).
 //   R5  a call that would exceed the capacity fails as a whole (EFULL) and
 //       leaves the table unchanged; a reserved key (all ones) is EINVAL.
+//   R6  Put(keys, values) (Sec. III-A, an upsert) applied as one batch: the
+//       value at the last position of a key wins; missing keys are inserted
+//       as in R1; the Adagrad accumulator of an existing key is kept, a new
+//       key's is 0.
+//   R7  the SGD variant of the Rmw applies the paper's update form itself
+//       (Sec. II-A): duplicate gradients summed as in R3, then
+//       w_c -= lr * g_c (separate fp32 operations); accumulators untouched.
 //
 // Storage is deliberately naive: std::unordered_map for key -> row, a sorted
 // array for a bulk prefill (identical result to inserting the same ascending
@@ -241,6 +248,51 @@ int oracle_put_grad(oracle_table* h, const uint64_t* keys, const float* grads, i
       w[c] = w[c] - p;
     }
     t.accum[u] = Gn;
+  }
+  return kOk;
+}
+
+// Put (Sec. III-A) as a batch upsert (R6): W[row(keys[i])] = values[i] for the
+// last position i of every distinct key.
+int oracle_put(oracle_table* h, const uint64_t* keys, const float* values, int64_t n) {
+  Table& t = *reinterpret_cast<Table*>(h);
+  int rc = check_keys(keys, n);
+  if (rc != kOk) return rc;
+  if (n > 0 && values == nullptr) return kEinval;
+  std::vector<uint32_t> rows;
+  rc = resolve(t, keys, n, &rows);
+  if (rc != kOk) return rc;
+  std::map<uint32_t, int64_t> last;  // row -> its last position
+  for (int64_t i = 0; i < n; ++i) last[rows[(size_t)i]] = i;
+  for (const auto& kv : last) {
+    float* w = writable_row(t, kv.first);
+    for (int32_t c = 0; c < t.dim; ++c) w[c] = values[kv.second * t.dim + c];
+  }
+  return kOk;
+}
+
+// Rmw with "sum duplicates, then one plain SGD step" (R7).
+int oracle_put_grad_sgd(oracle_table* h, const uint64_t* keys, const float* grads, int64_t n, float lr) {
+  Table& t = *reinterpret_cast<Table*>(h);
+  int rc = check_keys(keys, n);
+  if (rc != kOk) return rc;
+  if (n > 0 && grads == nullptr) return kEinval;
+  if (!std::isfinite(lr)) return kEinval;
+  std::vector<uint32_t> rows;
+  rc = resolve(t, keys, n, &rows);
+  if (rc != kOk) return rc;
+  std::map<uint32_t, std::vector<int64_t>> groups;
+  for (int64_t i = 0; i < n; ++i) groups[rows[(size_t)i]].push_back(i);
+  const int32_t D = t.dim;
+  for (const auto& kv : groups) {
+    float* w = writable_row(t, kv.first);
+    for (int32_t c = 0; c < D; ++c) {
+      double s = 0.0;
+      for (int64_t i : kv.second) s += (double)grads[i * D + c];
+      const float g = (float)s;
+      const float p = lr * g;
+      w[c] = w[c] - p;
+    }
   }
   return kOk;
 }

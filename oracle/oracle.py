@@ -54,6 +54,8 @@ def _load():
         "oracle_prefill_sorted": (ctypes.c_int, [P, P, I64]),
         "oracle_get": (ctypes.c_int, [P, P, I64, P]),
         "oracle_put_grad": (ctypes.c_int, [P, P, P, I64, F32, F32]),
+        "oracle_put": (ctypes.c_int, [P, P, P, I64]),
+        "oracle_put_grad_sgd": (ctypes.c_int, [P, P, P, I64, F32]),
         "oracle_lookup_rows": (ctypes.c_int, [P, P, I64, P]),
         "oracle_read_rows": (ctypes.c_int, [P, P, I64, P, P]),
         "oracle_row_keys": (ctypes.c_int, [P, P, I64, P]),
@@ -130,6 +132,22 @@ class OracleTable:
         return self._lib.oracle_put_grad(self._h, _ptr(k), _ptr(g), k.size,
                                          ctypes.c_float(lr), ctypes.c_float(eps))
 
+
+    def put(self, keys, values) -> int:
+        """Batch upsert: the value at a key's last position wins."""
+        k = _keys(keys)
+        v = np.ascontiguousarray(values, dtype=np.float32)
+        if v.size != k.size * self.dim:
+            raise ValueError("values must hold n * dim values")
+        return self._lib.oracle_put(self._h, _ptr(k), _ptr(v), k.size)
+
+    def put_grad_sgd(self, keys, grads, lr: float) -> int:
+        """Sum duplicate gradients, then one plain SGD step per key."""
+        k = _keys(keys)
+        g = np.ascontiguousarray(grads, dtype=np.float32)
+        if g.size != k.size * self.dim:
+            raise ValueError("grads must hold n * dim values")
+        return self._lib.oracle_put_grad_sgd(self._h, _ptr(k), _ptr(g), k.size, float(lr))
     def lookup_rows(self, keys):
         k = _keys(keys)
         rows = np.empty(k.size, dtype=np.int64)

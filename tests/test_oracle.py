@@ -343,3 +343,91 @@ def test_segment_sum_all_distinct_is_identity():
     p.grad = torch.tensor(g)
     opt.step()
     np.testing.assert_allclose(w, p.detach().numpy(), rtol=2e-6)
+
+
+# ---- Put (batch upsert) and the SGD variant of the Rmw ----------------------
+
+@pytest.mark.parametrize("seed", range(10))
+def test_put_matches_a_dict_model_last_position_wins(seed):
+    rng = np.random.default_rng(100 + seed)
+    dim, cap = 3, 60
+    t = O.OracleTable(dim, cap)
+    rows_model = ListModel(cap)
+    vals = {}  # key -> row values the plain dict model holds
+    for _ in range(5):
+        n = int(rng.integers(1, 15))
+        keys = rng.integers(0, 40, size=n).astype(np.uint64)
+        v = rng.normal(size=(n, dim)).astype(np.float32)
+        want_rows = rows_model.rows([int(k) for k in keys])
+        assert want_rows is not None
+        assert t.put(keys, v) == O.OK
+        for i, k in enumerate(keys.tolist()):   # sequential upserts: later positions overwrite
+            vals[k] = v[i].copy()
+        assert t.lookup_rows(keys).tolist() == want_rows
+        ks = np.array(sorted(vals), dtype=np.uint64)
+        rc, got = t.get(ks)
+        assert rc == O.OK
+        assert np.array_equal(got, np.stack([vals[k] for k in ks.tolist()]))
+
+
+def test_put_keeps_the_accumulator_of_existing_keys_and_zeroes_new_ones():
+    t = O.OracleTable(2, 10)
+    g = np.array([[0.5, -0.5]], np.float32)
+    assert t.put_grad(np.array([4], np.uint64), g, 0.1, 1e-8) == O.OK
+    _, st0 = t.read_rows([0])
+    assert st0[0] > 0
+    assert t.put(np.array([4, 9], np.uint64), np.ones((2, 2), np.float32)) == O.OK
+    w, st = t.read_rows([0, 1])
+    assert st[0] == st0[0] and st[1] == 0.0
+    assert np.array_equal(w, np.ones((2, 2), np.float32))
+
+
+def test_put_errors_leave_the_table_unchanged():
+    t = O.OracleTable(2, 3)
+    assert t.put(np.array([1, 2], np.uint64), np.zeros((2, 2), np.float32)) == O.OK
+    assert t.put(np.array([3, 4], np.uint64), np.ones((2, 2), np.float32)) == O.EFULL
+    assert t.put(np.array([1, O_RESERVED], np.uint64), np.ones((2, 2), np.float32)) == O.EINVAL
+    assert t.size == 2
+    _, w = t.get(np.array([1, 2], np.uint64))
+    assert np.array_equal(w, np.zeros((2, 2), np.float32))
+
+
+O_RESERVED = np.uint64(0xFFFFFFFFFFFFFFFF)
+
+
+@pytest.mark.parametrize("dim", [1, 8])
+def test_sgd_equals_torch_sparse_sgd_with_duplicates(dim):
+    # torch's sparse SGD coalesces (sums) duplicate indices, then w -= lr * g
+    rng = np.random.default_rng(7 + dim)
+    lr = 0.05
+    keys = np.array([7, 3, 7, 7, 9, 3, 11], dtype=np.uint64)
+    t = O.OracleTable(dim, 16)
+    _, w0 = t.get(np.array([3, 7, 9, 11], np.uint64))
+    emb = torch.nn.Embedding(4, dim, sparse=True)
+    with torch.no_grad():
+        emb.weight.copy_(torch.tensor(w0))
+    opt = torch.optim.SGD(emb.parameters(), lr=lr)
+    idx_of = {3: 0, 7: 1, 9: 2, 11: 3}
+    for _ in range(5):
+        g = rng.normal(0, 0.2, size=(keys.size, dim)).astype(np.float32)
+        assert t.put_grad_sgd(keys, g, lr) == O.OK
+        idx = torch.tensor([idx_of[int(k)] for k in keys])
+        opt.zero_grad()
+        emb(idx).backward(torch.tensor(g))
+        opt.step()
+    w, st = t.read_rows([0, 1, 2, 3])
+    np.testing.assert_allclose(w, emb.weight.detach().numpy(), rtol=2e-6, atol=1e-9)
+    assert np.all(st == 0)   # the SGD step leaves the Adagrad accumulators alone
+
+
+def test_sgd_closed_form_with_exact_sums():
+    # k copies of the same power-of-two gradient sum exactly, so the step is
+    # w1 = w0 - lr * (k * g) bit for bit
+    t = O.OracleTable(4, 8)
+    _, w0 = t.get(np.array([5], np.uint64))
+    k, gval, lr = 6, 0.25, 0.5
+    keys = np.full(k, 5, np.uint64)
+    assert t.put_grad_sgd(keys, np.full((k, 4), gval, np.float32), lr) == O.OK
+    w, _ = t.read_rows([0])
+    want = (w0[0] - np.float32(lr) * np.float32(k * gval)).astype(np.float32)
+    assert np.array_equal(w[0], want)
