@@ -82,6 +82,22 @@ int mlkv_get(mlkv_table *t, const uint64_t *d_keys, int64_t n, float *d_out, voi
 int mlkv_put_grad(mlkv_table *t, const uint64_t *d_keys, const float *d_grads, int64_t n,
                   float lr, float eps, void *hip_stream);
 
+/* Rmw (Sec. III-B, step 8) with plain SGD as the modify function, i.e. the
+ * update form of Sec. II-A applied to the summed gradient: missing keys are
+ * inserted as in mlkv_get; then for every distinct key k of the batch
+ *     g[c] = fp32( sum_j fp64(d_grads[i_j*dim + c]) )   (positions ascending)
+ *     w[c] -= lr * g[c]                                   (separate fp32 operations)
+ * Adagrad accumulators are not touched. 0 <= n <= 2^30 - 1; lr finite. */
+int mlkv_put_grad_sgd(mlkv_table *t, const uint64_t *d_keys, const float *d_grads, int64_t n, float lr,
+                      void *hip_stream);
+
+/* Put (Sec. III-A), an upsert of a batch: for every distinct key of the batch
+ * its row becomes d_values[i*dim ... i*dim + dim - 1] for the LAST position i
+ * holding the key. Missing keys are inserted as in mlkv_get (rows in ascending
+ * key order). The Adagrad accumulator of an existing key is kept; a new key's
+ * is 0. d_values: n*dim floats, row-major. 0 <= n <= 2^30 - 1. */
+int mlkv_put(mlkv_table *t, const uint64_t *d_keys, const float *d_values, int64_t n, void *hip_stream);
+
 /* Waits for all work on `hip_stream`, then returns and clears the first error
  * latched on the device since the previous mlkv_sync (MLKV_EFULL or
  * MLKV_EINVAL), or MLKV_OK. */
@@ -124,7 +140,7 @@ int mlkv_read_rows(mlkv_table *t, const int64_t *d_rows, int64_t n, float *d_row
 /* ---- per-kernel timing (benchmarks) ----
  * The library runs MLKV_NUM_KERNELS kernels: 0 get_probe_gather and
  * 1 assign_new for mlkv_get; 2 put_probe, 3 put_group and 4 put_apply for
- * mlkv_put_grad. While enabled, HIP events are recorded on
+ * mlkv_put_grad, mlkv_put_grad_sgd and mlkv_put. While enabled, HIP events are recorded on
  * the call's stream before and after every launch. mlkv_profile_read waits
  * for the recorded launches, writes per-kernel sums of their durations (ms)
  * and launch counts into the host arrays total_ms[MLKV_NUM_KERNELS] and

@@ -301,15 +301,22 @@ int mlkv_get(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, voi
   return MLKV_OK;
 }
 
-int mlkv_put_grad(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, int64_t n, float lr,
-                  float eps, void* hip_stream) {
+}  // extern "C"
+
+namespace {
+
+// The put pipeline (probe, group, apply) with update `op` for every distinct
+// key; `src` holds n rows of gradients (or values for kOpAssign).
+int put_call(mlkv_table* t, const uint64_t* d_keys, const float* src, int64_t n, int op, float lr, float eps,
+             void* hip_stream) {
   int rc = check_table(t);
   if (rc) return rc;
   if (n < 0 || n > 0x3FFFFFFFll) return fail(MLKV_EINVAL, "n must be in [0, 2^30 - 1]");
-  if (!std::isfinite(lr)) return fail(MLKV_EINVAL, "lr must be finite");
-  if (!std::isfinite(eps) || eps < 0.0f) return fail(MLKV_EINVAL, "eps must be finite and >= 0");
+  if (op != kOpAssign && !std::isfinite(lr)) return fail(MLKV_EINVAL, "lr must be finite");
+  if (op == kOpAdagrad && (!std::isfinite(eps) || eps < 0.0f))
+    return fail(MLKV_EINVAL, "eps must be finite and >= 0");
   if (n == 0) return MLKV_OK;
-  if (d_keys == nullptr || d_grads == nullptr) return fail(MLKV_EINVAL, "keys or grads is NULL");
+  if (d_keys == nullptr || src == nullptr) return fail(MLKV_EINVAL, "keys or rows is NULL");
   if ((rc = ensure_workspace(t, n)) != MLKV_OK) return rc;
   const uint32_t pb = part_bits(n);
   // keys per put_probe tile: a multiple of 64, at most kPutTile, so that the
@@ -320,7 +327,7 @@ int mlkv_put_grad(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, i
   a.idx = t->idx;
   a.nb_log2 = t->nb_log2;
   a.keys = d_keys;
-  a.grads = d_grads;
+  a.grads = src;
   a.n = n;
   a.rows = t->rows;
   a.state = t->state;
@@ -329,6 +336,7 @@ int mlkv_put_grad(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, i
   a.capacity = t->capacity;
   a.lr = lr;
   a.eps = eps;
+  a.op = op;
   a.pb = (int)pb;
   a.tlen = tlen;
   a.items = t->items;
@@ -344,11 +352,29 @@ int mlkv_put_grad(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, i
   a.flat_blocks = t->flat_blocks;
   a.ctrl = t->ctrl;
   a.epoch = t->epoch;
-  const bool vec4 = (t->dim % 4 == 0) && aligned16(d_grads);
+  const bool vec4 = (t->dim % 4 == 0) && aligned16(src);
   hipError_t e = launch_put(a, vec4, static_cast<hipStream_t>(hip_stream), hook_of(t));
-  if (e != hipSuccess) return hip_fail(e, "mlkv_put_grad launch");
+  if (e != hipSuccess) return hip_fail(e, "put launch");
   t->epoch++;
   return MLKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mlkv_put_grad(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, int64_t n, float lr,
+                  float eps, void* hip_stream) {
+  return put_call(t, d_keys, d_grads, n, kOpAdagrad, lr, eps, hip_stream);
+}
+
+int mlkv_put_grad_sgd(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, int64_t n, float lr,
+                      void* hip_stream) {
+  return put_call(t, d_keys, d_grads, n, kOpSgd, lr, 0.0f, hip_stream);
+}
+
+int mlkv_put(mlkv_table* t, const uint64_t* d_keys, const float* d_values, int64_t n, void* hip_stream) {
+  return put_call(t, d_keys, d_values, n, kOpAssign, 0.0f, 0.0f, hip_stream);
 }
 
 int mlkv_sync(mlkv_table* t, void* hip_stream) {

@@ -27,6 +27,13 @@ enum KernelId : int {
   K_COUNT = 5
 };
 
+// Update a put call applies to each distinct key's row.
+enum PutOp : int {
+  kOpAdagrad = 0,  // sum the key's gradient rows, one row-wise Adagrad step
+  kOpSgd = 1,      // sum the key's gradient rows, one SGD step
+  kOpAssign = 2    // the value row at the key's last position replaces the row
+};
+
 // Per-partition results of put_group, read by put_apply.
 struct PartMeta {
   uint32_t mA;    // items of the segments that need a sum (stored first)
@@ -75,6 +82,7 @@ struct PutArgs {
   int64_t capacity;
   float lr;
   float eps;
+  int op;     // PutOp
   int pb;     // 2^pb partitions
   int tlen;   // keys per put_probe tile (<= kPutTile)
   uint64_t* items;

@@ -354,7 +354,8 @@ constexpr int kTileHash = 2 * kPutTile;  // LDS hash slots per tile
 template <class M>
 __global__ __launch_bounds__(kPutThreads) void k_put_probe(
     Bucket* __restrict__ idx, uint32_t nb_log2, const uint64_t* __restrict__ keys,
-    const float* __restrict__ grads, int64_t n, int tlen, int D, int pb, int ntiles, uint64_t* __restrict__ items,
+    const float* __restrict__ grads, int64_t n, int tlen, int D, int op, int pb, int ntiles,
+    uint64_t* __restrict__ items,
     uint32_t* __restrict__ meta, double* __restrict__ partials, NewKey* __restrict__ newlist,
     uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch) {
   constexpr int NT = kPutThreads;
@@ -486,8 +487,9 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
     if (dup[kk]) s_lanes[my_off[kk] + rank[kk]] = (uint16_t)(kk * NT + tid);
   lds_barrier();
 
-  // each lane group sums the rows of repeated keys, positions ascending
-  {
+  // each lane group sums the rows of repeated keys, positions ascending (an
+  // assignment needs no sum: its item is the key's last position instead)
+  if (op != kOpAssign) {
     constexpr int UNR = (K * VEC >= 16) ? 2 : (K * VEC >= 8) ? 4 : 8;
     const int lane = tid & 63;
     const int g = lane / LPR;
@@ -561,7 +563,9 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
       ctrl->new_epoch = epoch;
     }
     const bool fresh = pr[kk].status != P_HIT;
-    x[kk] = valid[kk] ? make_item(fresh, fresh ? pr[kk].slot : pr[kk].row, (uint32_t)(base + e)) : ~0ull;
+    uint32_t pos = (uint32_t)(base + e);
+    if (op == kOpAssign && owner[kk]) pos = (uint32_t)(base + s_lanes[s_doff[s_hdup[hs[kk]] + 1] - 1]);
+    x[kk] = valid[kk] ? make_item(fresh, fresh ? pr[kk].slot : pr[kk].row, pos) : ~0ull;
   }
 
   // emit single positions, and one summed item per repeated key
@@ -606,7 +610,8 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
   lds_barrier();
 #pragma unroll
   for (int kk = 0; kk < KPT; ++kk)
-    if (emit[kk]) items[(size_t)sbase + s_hist[d[kk]] + r[kk]] = dup[kk] ? (x[kk] | kItemSummed) : x[kk];
+    if (emit[kk])
+      items[(size_t)sbase + s_hist[d[kk]] + r[kk]] = dup[kk] && op != kOpAssign ? (x[kk] | kItemSummed) : x[kk];
   if (tid == 0) tile_cnt[tile] = s_cnt;
 }
 
@@ -691,6 +696,42 @@ struct SegmentOps {
     if (q == 0) state[row] = Gn;
   }
 
+  // One SGD step: w -= lr * g (separate fp32 operations).
+  static __device__ __forceinline__ void sgd(const V (&g)[K], V (&w)[K], float* __restrict__ rows, uint32_t row,
+                                             int D, int q, float lr) {
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int col = (k * LPR + q) * VEC;
+      if (col < D) {
+#pragma unroll
+        for (int x = 0; x < VEC; ++x)
+          VecT<VEC>::set(w[k], x, __fsub_rn(VecT<VEC>::get(w[k], x), __fmul_rn(lr, VecT<VEC>::get(g[k], x))));
+        store_vec<VEC>(rows + (size_t)row * (size_t)D + col, w[k]);
+      }
+    }
+  }
+
+  // The row becomes g.
+  static __device__ __forceinline__ void assign(const V (&g)[K], float* __restrict__ rows, uint32_t row, int D,
+                                                int q) {
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int col = (k * LPR + q) * VEC;
+      if (col < D) store_vec<VEC>(rows + (size_t)row * (size_t)D + col, g[k]);
+    }
+  }
+
+  // The update of op for one row; w and G are the row's current values
+  // (not read for kOpAssign, G only for kOpAdagrad).
+  static __device__ __forceinline__ void update(int op, const V (&g)[K], V (&w)[K], float G,
+                                                float* __restrict__ rows, float* __restrict__ state,
+                                                uint32_t row, int D, int q, bool d_pow2, double inv_d, float lr,
+                                                float eps) {
+    if (op == kOpAdagrad) adagrad(g, w, G, rows, state, row, D, q, d_pow2, inv_d, lr, eps);
+    else if (op == kOpSgd) sgd(g, w, rows, row, D, q, lr);
+    else assign(g, rows, row, D, q);
+  }
+
   static __device__ __forceinline__ void zero(double (&acc)[K][VEC]) {
 #pragma unroll
     for (int k = 0; k < K; ++k)
@@ -717,6 +758,7 @@ struct SegmentOps {
 };
 
 struct RedCtx {
+  int op;
   Bucket* idx;
   const float* grads;
   const double* partials;
@@ -956,9 +998,11 @@ __device__ __forceinline__ void update_segments(IP it, SP seg, uint32_t S, const
         const uint32_t b = seg[s];
         const uint64_t x = it[b];
         row[u] = item_tag(x);
-        const bool from_a = (seg[s + 1] - b > 1) || item_summed(x);
-        const float* src = from_a ? reinterpret_cast<const float*>(c.partials + (size_t)item_pos(x) * (size_t)D)
-                                  : c.grads + (size_t)item_pos(x) * (size_t)D;
+        const bool from_a = c.op != kOpAssign && ((seg[s + 1] - b > 1) || item_summed(x));
+        // an assignment takes the value row at the key's last position
+        const uint32_t pos = c.op == kOpAssign ? item_pos(it[seg[s + 1] - 1]) : item_pos(x);
+        const float* src = from_a ? reinterpret_cast<const float*>(c.partials + (size_t)pos * (size_t)D)
+                                  : c.grads + (size_t)pos * (size_t)D;
 #pragma unroll
         for (int k = 0; k < K; ++k) {
           const int col = (k * LPR + q) * VEC;
@@ -967,13 +1011,13 @@ __device__ __forceinline__ void update_segments(IP it, SP seg, uint32_t S, const
             w[u][k] = load_vec<VEC>(c.rows + (size_t)row[u] * (size_t)D + col);
           }
         }
-        G[u] = c.state[row[u]];
+        if (c.op == kOpAdagrad) G[u] = c.state[row[u]];
       }
     }
 #pragma unroll
     for (int u = 0; u < BB; ++u) {
       if (s0 + u * NG < S)
-        Ops::adagrad(gf[u], w[u], G[u], c.rows, c.state, row[u], D, q, d_pow2, inv_d, c.lr, c.eps);
+        Ops::update(c.op, gf[u], w[u], G[u], c.rows, c.state, row[u], D, q, d_pow2, inv_d, c.lr, c.eps);
     }
   }
 }
@@ -1223,7 +1267,7 @@ __device__ __forceinline__ void reduce_partition_global(uint32_t p, uint32_t mp,
   const uint32_t S = encode_segments<NT>(it, mp, seg, sid, s_w);
   resolve_new_rows<NT>(it, seg, S, c, newlist, tile_cnt, ntiles, s_pref, s_w, s_w64,
                        reinterpret_cast<uint64_t*>(s_part));
-  sum_segments<M, NT>(it, seg, sid, mp, c, s_part);
+  if (c.op != kOpAssign) sum_segments<M, NT>(it, seg, sid, mp, c, s_part);
   update_segments<M, NT>(it, seg, S, c);
 }
 
@@ -1241,7 +1285,7 @@ __global__ __launch_bounds__(NT) void k_put_group(
     const float* __restrict__ grads, const double* __restrict__ partials, float* __restrict__ rows,
     float* __restrict__ state, int D, uint64_t seed, float lr, float eps, int64_t capacity, Ctrl* ctrl,
     uint64_t epoch, uint64_t* __restrict__ spill, uint64_t spill_words, uint64_t* __restrict__ gitems,
-    uint32_t* __restrict__ gdesc, PartMeta* __restrict__ pmeta) {
+    uint32_t* __restrict__ gdesc, PartMeta* __restrict__ pmeta, int op) {
   using L = RedLds<NT>;
   constexpr int IPT = (kRedCap + NT - 1) / NT;
   extern __shared__ __align__(16) unsigned char s_raw[];
@@ -1299,7 +1343,7 @@ __global__ __launch_bounds__(NT) void k_put_group(
     return;
   }
 
-  const RedCtx c{idx, grads, partials, rows, state, D, seed, lr, eps, size0};
+  const RedCtx c{op, idx, grads, partials, rows, state, D, seed, lr, eps, size0};
   if (mp > (uint32_t)kRedCap) {
     reduce_partition_global<M, NT>(p, mp, items, meta, ntiles, c, newlist, tile_cnt, ctrl, spill, spill_words,
                                    s_part, s_pref, s_w, s_w64, s_base);
@@ -1354,6 +1398,16 @@ __global__ __launch_bounds__(NT) void k_put_group(
   // ---- hand the grouped partition to the flat kernel ----
   uint64_t* gi = gitems + (size_t)p * kRedCap;
   uint32_t* gd = gdesc + (size_t)p * kRedCap;
+  if (op == kOpAssign) {
+    // one item per key, its last (the value that wins), all as keys seen once;
+    // a new key's first item carries its row
+    for (uint32_t s = tid; s < S; s += NT) {
+      const uint64_t x0 = s_sorted[s_seg[s]], xl = s_sorted[s_seg[s + 1] - 1];
+      gi[s] = make_item(item_fresh(x0), item_tag(x0), item_pos(xl));
+    }
+    if (tid == 0) pmeta[p] = PartMeta{0u, S, 0u, 0u};
+    return;
+  }
   for (uint32_t i = tid; i < mp; i += NT) {
     gi[i] = s_sorted[i];
     const uint32_t s = s_sid[i];
@@ -1439,7 +1493,7 @@ __global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ g
                                                   const PartMeta* __restrict__ pmeta, int np,
                                                   const float* __restrict__ grads, double* __restrict__ partials,
                                                   float* __restrict__ rows, float* __restrict__ state, int D,
-                                                  float lr, float eps, Ctrl* ctrl) {
+                                                  int op, float lr, float eps, Ctrl* ctrl) {
   using Ops = SegmentOps<M>;
   using LA = ApplyLds<M, NT>;
   constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
@@ -1684,15 +1738,15 @@ __global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ g
           const int col = (k * LPR + q) * VEC;
           if (col < D) {
             gf[u][k] = load_vec<VEC>(src[u] + col);
-            w[u][k] = load_vec<VEC>(rows + (size_t)row[u] * (size_t)D + col);
+            if (op != kOpAssign) w[u][k] = load_vec<VEC>(rows + (size_t)row[u] * (size_t)D + col);
           }
         }
-        Gs[u] = state[row[u]];
+        if (op == kOpAdagrad) Gs[u] = state[row[u]];
       }
     }
 #pragma unroll
     for (int u = 0; u < BB; ++u)
-      if (on[u]) Ops::adagrad(gf[u], w[u], Gs[u], rows, state, row[u], D, q, d_pow2, inv_d, lr, eps);
+      if (on[u]) Ops::update(op, gf[u], w[u], Gs[u], rows, state, row[u], D, q, d_pow2, inv_d, lr, eps);
   };
   // this group's work: completed segments [e0, e1) (g over the partials row
   // of their last item), then keys seen once [k0, k1) (g is their gradient row)
@@ -1816,7 +1870,7 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   const int np = 1 << a.pb;
   hook(K_PUT_PROBE, 0, st);
   hipLaunchKernelGGL(k_put_probe<M>, dim3((unsigned)ntiles), dim3(kPutThreads), 0, st, a.idx, a.nb_log2,
-                     a.keys, a.grads, a.n, a.tlen, a.D, a.pb, (int)ntiles, a.items, a.meta, a.partials,
+                     a.keys, a.grads, a.n, a.tlen, a.D, a.op, a.pb, (int)ntiles, a.items, a.meta, a.partials,
                      a.newlist, a.tile_cnt, a.ctrl, a.epoch);
   hook(K_PUT_PROBE, 1, st);
   hipError_t e = hipGetLastError();
@@ -1837,7 +1891,7 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   hipLaunchKernelGGL((k_put_group<M, NT>), dim3((unsigned)np), dim3(NT), L::total, st, a.idx, a.items,
                      a.meta, (int)ntiles, a.newlist, a.tile_cnt, a.grads, a.partials, a.rows, a.state,
                      a.D, a.seed, a.lr, a.eps, a.capacity, a.ctrl, a.epoch, a.spill, a.spill_words, a.gitems,
-                     a.gdesc, a.pmeta);
+                     a.gdesc, a.pmeta, a.op);
   hook(K_PUT_GROUP, 1, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int apply_blocks = (int)std::max<int64_t>((int64_t)a.flat_blocks * ApplyCfg<M>::kPerCU,
@@ -1845,7 +1899,7 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   const size_t apply_lds = ApplyLds<M, NTA>::bytes(np);
   hook(K_PUT_APPLY, 0, st);
   hipLaunchKernelGGL((k_put_apply<M, NTA>), dim3((unsigned)apply_blocks), dim3(NTA), apply_lds, st, a.gitems, a.gdesc, a.pmeta, np, a.grads, a.partials,
-                     a.rows, a.state, a.D, a.lr, a.eps, a.ctrl);
+                     a.rows, a.state, a.D, a.op, a.lr, a.eps, a.ctrl);
   hook(K_PUT_APPLY, 1, st);
   return hipGetLastError();
 }

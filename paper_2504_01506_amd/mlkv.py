@@ -45,6 +45,8 @@ def load() -> ctypes.CDLL:
         "mlkv_open_ex": (P, [I32, I64, U64, F32]),
         "mlkv_get": (INT, [P, P, I64, P, P]),
         "mlkv_put_grad": (INT, [P, P, P, I64, F32, F32, P]),
+        "mlkv_put_grad_sgd": (INT, [P, P, P, I64, F32, P]),
+        "mlkv_put": (INT, [P, P, P, I64, P]),
         "mlkv_sync": (INT, [P, P]),
         "mlkv_size": (I64, [P]),
         "mlkv_num_slots": (I64, [P]),
@@ -121,6 +123,14 @@ def mlkv_get(t: int, keys, n: int, out, stream=None) -> int:
 
 def mlkv_put_grad(t: int, keys, grads, n: int, lr: float, eps: float, stream=None) -> int:
     return load().mlkv_put_grad(t, _ptr(keys), _ptr(grads), n, lr, eps, _stream(stream))
+
+
+def mlkv_put_grad_sgd(t: int, keys, grads, n: int, lr: float, stream=None) -> int:
+    return load().mlkv_put_grad_sgd(t, _ptr(keys), _ptr(grads), n, lr, _stream(stream))
+
+
+def mlkv_put(t: int, keys, values, n: int, stream=None) -> int:
+    return load().mlkv_put(t, _ptr(keys), _ptr(values), n, _stream(stream))
 
 
 def mlkv_sync(t: int, stream=None) -> int:
@@ -201,6 +211,12 @@ class Table:
 
     def put_grad(self, keys: torch.Tensor, grads: torch.Tensor, lr: float, eps: float, stream=None):
         _check(mlkv_put_grad(self.h, keys, grads, keys.numel(), lr, eps, stream))
+
+    def put_grad_sgd(self, keys: torch.Tensor, grads: torch.Tensor, lr: float, stream=None):
+        _check(mlkv_put_grad_sgd(self.h, keys, grads, keys.numel(), lr, stream))
+
+    def put(self, keys: torch.Tensor, values: torch.Tensor, stream=None):
+        _check(mlkv_put(self.h, keys, values, keys.numel(), stream))
 
     def sync(self, stream=None) -> int:
         return mlkv_sync(self.h, stream)

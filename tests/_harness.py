@@ -96,6 +96,23 @@ class Pair:
         assert self.gpu.sync() == mlkv.MLKV_OK
         self.updated[self.ora.lookup_rows(keys)] = True
 
+    def put_sgd(self, keys: np.ndarray, grads: np.ndarray, lr: float):
+        self.gpu.put_grad_sgd(dev_keys(keys), dev(grads), lr)
+        assert self.ora.put_grad_sgd(keys, grads, lr) == O.OK
+        assert self.gpu.sync() == mlkv.MLKV_OK
+        self.updated[self.ora.lookup_rows(keys)] = True
+
+    def upsert(self, keys: np.ndarray, values: np.ndarray):
+        """Put: the rows of the batch's keys must equal the oracle's bit for bit."""
+        self.gpu.put(dev_keys(keys), dev(values))
+        assert self.ora.put(keys, values) == O.OK
+        assert self.gpu.sync() == mlkv.MLKV_OK
+        rows = np.unique(self.ora.lookup_rows(keys))
+        got = self.gpu.read_rows(torch.from_numpy(rows).cuda())[0].cpu().numpy()
+        want, _ = self.ora.read_rows(rows)
+        assert np.array_equal(got.view(np.uint32), want.view(np.uint32)), "put rows differ"
+        self.updated[rows] = True
+
     def compare_rows(self, rows: np.ndarray | None = None):
         """Key->row bit-exact for the keys of `rows`; row values and accumulators
         within RTOL (bit-exact for never-updated rows)."""
