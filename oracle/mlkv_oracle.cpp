@@ -18,9 +18,7 @@
 //
 // Readings of points the paper leaves open:
 //   R1  rows are dense in [0, size); within one call the distinct keys that
-//       are missing receive consecutive rows in ascending order of
-//       mix64(key) (the SplitMix64 output function below, a bijection on
-//       64-bit words, so the order is total and fixed by the keys alone).
+//       are missing receive consecutive rows in ascending key order.
 //   R2  the initial value of element c of key k is a fixed function of
 //       (seed, k, c) only (SplitMix64 finaliser, Steele, Lea & Flood 2014).
 //   R3  duplicate keys in one put are summed (fp64, ascending position,
@@ -39,9 +37,9 @@
 //       w_c -= lr * g_c (separate fp32 operations); accumulators untouched.
 //
 // Storage is deliberately naive: std::unordered_map for key -> row, a sorted
-// array for a bulk prefill (identical result to inserting the same keys
-// through get, chunk by chunk), and rows are materialised only when first
-// written (an untouched row equals its initial value by definition).
+// array for a bulk prefill (identical result to inserting the same ascending
+// keys through get), and rows are materialised only when first written
+// (an untouched row equals its initial value by definition).
 
 #include <algorithm>
 #include <cmath>
@@ -80,11 +78,8 @@ struct Table {
   int64_t capacity;
   uint64_t seed;
   int64_t size = 0;
+  // rows [0, prefill_n) belong to the keys of a bulk prefill, in ascending order
   std::vector<uint64_t> row_key;                 // key of every row in [0, size)
-  // rows [0, prefill_n) belong to the keys of a bulk prefill: pre_key holds
-  // them ascending, pre_row[i] the row of pre_key[i]
-  std::vector<uint64_t> pre_key;
-  std::vector<uint32_t> pre_row;
   int64_t prefill_n = 0;
   std::unordered_map<uint64_t, uint32_t> map;    // keys inserted one call at a time
   std::unordered_map<uint32_t, size_t> stored;   // row -> offset in `store` once written
@@ -94,9 +89,11 @@ struct Table {
 
 bool find_row(const Table& t, uint64_t key, uint32_t* row) {
   if (t.prefill_n > 0) {
-    auto it = std::lower_bound(t.pre_key.begin(), t.pre_key.end(), key);
-    if (it != t.pre_key.end() && *it == key) {
-      *row = t.pre_row[(size_t)(it - t.pre_key.begin())];
+    auto first = t.row_key.begin();
+    auto last = t.row_key.begin() + t.prefill_n;
+    auto it = std::lower_bound(first, last, key);
+    if (it != last && *it == key) {
+      *row = (uint32_t)(it - first);
       return true;
     }
   }
@@ -140,8 +137,6 @@ int resolve(Table& t, const uint64_t* keys, int64_t n, std::vector<uint32_t>* ro
   }
   std::sort(missing.begin(), missing.end());
   missing.erase(std::unique(missing.begin(), missing.end()), missing.end());
-  std::sort(missing.begin(), missing.end(),
-            [](uint64_t a, uint64_t b) { return splitmix64_mix(a) < splitmix64_mix(b); });
   if (t.size + (int64_t)missing.size() > t.capacity) return kEfull;
   for (size_t j = 0; j < missing.size(); ++j) {
     const uint32_t row = (uint32_t)(t.size + (int64_t)j);
@@ -182,32 +177,16 @@ float oracle_init_value(uint64_t seed, uint64_t key, int32_t c) { return init_va
 uint64_t oracle_mix64(uint64_t z) { return splitmix64_mix(z); }
 
 // Bulk prefill of an EMPTY table with strictly ascending keys: identical in
-// effect to oracle_get(chunk of keys, NULL) on consecutive chunks of `chunk`
-// keys (every key is missing, so a chunk's keys take the next rows in
-// ascending mix64 order, R1), but held as a sorted array instead of n
-// hash-map entries.
-int oracle_prefill_sorted(oracle_table* h, const uint64_t* keys, int64_t n, int64_t chunk) {
+// effect to oracle_get(keys, n, NULL) (every key is missing, so row = rank),
+// but held as a sorted array instead of n hash-map entries.
+int oracle_prefill_sorted(oracle_table* h, const uint64_t* keys, int64_t n) {
   Table& t = *reinterpret_cast<Table*>(h);
-  if (check_keys(keys, n) != kOk || chunk < 1) return kEinval;
+  if (check_keys(keys, n) != kOk) return kEinval;
   if (t.size != 0) return kEinval;
   for (int64_t i = 1; i < n; ++i)
     if (!(keys[i - 1] < keys[i])) return kEinval;
   if (n > t.capacity) return kEfull;
-  t.pre_key.assign(keys, keys + n);
-  t.pre_row.assign((size_t)n, 0u);
-  t.row_key.assign((size_t)n, 0ull);
-  std::vector<int64_t> order;
-  for (int64_t c0 = 0; c0 < n; c0 += chunk) {
-    const int64_t c1 = std::min(n, c0 + chunk);
-    order.clear();
-    for (int64_t i = c0; i < c1; ++i) order.push_back(i);
-    std::sort(order.begin(), order.end(),
-              [&](int64_t a, int64_t b) { return splitmix64_mix(keys[a]) < splitmix64_mix(keys[b]); });
-    for (int64_t r = 0; r < c1 - c0; ++r) {
-      t.pre_row[(size_t)order[(size_t)r]] = (uint32_t)(c0 + r);
-      t.row_key[(size_t)(c0 + r)] = keys[order[(size_t)r]];
-    }
-  }
+  t.row_key.assign(keys, keys + n);
   t.prefill_n = n;
   t.size = n;
   return kOk;

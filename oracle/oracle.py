@@ -51,7 +51,7 @@ def _load():
         "oracle_size": (I64, [P]),
         "oracle_init_value": (F32, [U64, U64, I32]),
         "oracle_mix64": (U64, [U64]),
-        "oracle_prefill_sorted": (ctypes.c_int, [P, P, I64, I64]),
+        "oracle_prefill_sorted": (ctypes.c_int, [P, P, I64]),
         "oracle_get": (ctypes.c_int, [P, P, I64, P]),
         "oracle_put_grad": (ctypes.c_int, [P, P, P, I64, F32, F32]),
         "oracle_put": (ctypes.c_int, [P, P, P, I64]),
@@ -113,11 +113,9 @@ class OracleTable:
     def size(self) -> int:
         return int(self._lib.oracle_size(self._h))
 
-    def prefill_sorted(self, keys, chunk: int | None = None) -> int:
-        """Inserts strictly ascending keys into an empty table as `get` calls
-        of `chunk` keys each would (one call if chunk is None)."""
+    def prefill_sorted(self, keys) -> int:
         k = _keys(keys)
-        return self._lib.oracle_prefill_sorted(self._h, _ptr(k), k.size, max(1, k.size if chunk is None else chunk))
+        return self._lib.oracle_prefill_sorted(self._h, _ptr(k), k.size)
 
     def get(self, keys, want_out: bool = True):
         """Returns (rc, out[n, dim] float32 or None)."""

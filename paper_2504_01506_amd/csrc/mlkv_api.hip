@@ -41,11 +41,6 @@ struct mlkv_table {
   uint32_t* gdesc = nullptr;
   PartMeta* pmeta = nullptr;
   int flat_blocks = 256;  // least number of put_apply blocks: one per CU
-  // order bins of the keys a call inserts: counts (zero between calls, kept
-  // for the table's life) and lists (grown with the scratch)
-  uint32_t* bin_cnt = nullptr;
-  NewKey* bin_list = nullptr;
-  uint32_t bin_cap = 0;
 
   // optional per-launch timing: HIP events recorded around each kernel
   struct ProfRec {
@@ -89,9 +84,6 @@ void free_workspace(mlkv_table* t) {
   (void)hipFree(t->gitems);
   (void)hipFree(t->gdesc);
   (void)hipFree(t->pmeta);
-  (void)hipFree(t->bin_list);
-  t->bin_list = nullptr;
-  t->bin_cap = 0;
   t->partials = nullptr;
   t->gitems = nullptr;
   t->gdesc = nullptr;
@@ -129,10 +121,7 @@ int ensure_workspace(mlkv_table* t, int64_t n) {
   const int64_t slots = std::max<int64_t>(want, put_tiles * kPutTile);
   const uint64_t spill_words = 4ull * (uint64_t)want + 4096;
   const size_t np = (size_t)1 << part_bits(want);
-  // room for twice a bin's expected share of a call that inserts all its keys
-  const uint64_t bin_cap = 2 * (((uint64_t)want + kOrderBins - 1) / kOrderBins) + 64;
   if ((e = dev_alloc(&t->newlist, sizeof(NewKey) * (size_t)slots)) != hipSuccess ||
-      (e = dev_alloc(&t->bin_list, sizeof(NewKey) * (size_t)kOrderBins * bin_cap)) != hipSuccess ||
       (e = dev_alloc(&t->gitems, sizeof(uint64_t) * np * kRedCap)) != hipSuccess ||
       (e = dev_alloc(&t->gdesc, sizeof(uint32_t) * np * kRedCap)) != hipSuccess ||
       (e = dev_alloc(&t->pmeta, sizeof(PartMeta) * np)) != hipSuccess ||
@@ -146,7 +135,6 @@ int ensure_workspace(mlkv_table* t, int64_t n) {
   }
   t->ws_n = want;
   t->spill_words = spill_words;
-  t->bin_cap = (uint32_t)bin_cap;
   return MLKV_OK;
 }
 
@@ -249,8 +237,7 @@ mlkv_table* mlkv_open_ex(int32_t dim, int64_t capacity, uint64_t seed, float max
   if ((e = dev_alloc(&t->idx, sizeof(Bucket) * t->nb)) != hipSuccess ||
       (e = dev_alloc(&t->rows, sizeof(float) * (size_t)capacity * (size_t)dim)) != hipSuccess ||
       (e = dev_alloc(&t->state, sizeof(float) * (size_t)capacity)) != hipSuccess ||
-      (e = dev_alloc(&t->ctrl, sizeof(Ctrl))) != hipSuccess ||
-      (e = dev_alloc(&t->bin_cnt, sizeof(uint32_t) * kOrderBins)) != hipSuccess) {
+      (e = dev_alloc(&t->ctrl, sizeof(Ctrl))) != hipSuccess) {
     hip_fail(e, "table allocation");
     mlkv_close(t);
     return nullptr;
@@ -260,7 +247,6 @@ mlkv_table* mlkv_open_ex(int32_t dim, int64_t capacity, uint64_t seed, float max
   std::memset(&c, 0, sizeof(c));
   if ((e = hipMemset(t->idx, 0xFF, sizeof(Bucket) * t->nb)) != hipSuccess ||
       (e = hipMemcpy(t->ctrl, &c, sizeof(Ctrl), hipMemcpyHostToDevice)) != hipSuccess ||
-      (e = hipMemset(t->bin_cnt, 0, sizeof(uint32_t) * kOrderBins)) != hipSuccess ||
       (e = hipDeviceSynchronize()) != hipSuccess) {
     hip_fail(e, "table initialisation");
     mlkv_close(t);
@@ -283,7 +269,6 @@ void mlkv_close(mlkv_table* t) {
   (void)hipFree(t->rows);
   (void)hipFree(t->state);
   (void)hipFree(t->ctrl);
-  (void)hipFree(t->bin_cnt);
   delete t;
 }
 
@@ -309,7 +294,6 @@ int mlkv_get(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, voi
   a.tile_cnt = t->tile_cnt;
   a.ctrl = t->ctrl;
   a.epoch = t->epoch;
-  a.bins = OrderBins{t->bin_cnt, t->bin_list, t->bin_cap};
   const bool vec4 = (t->dim % 4 == 0) && (d_out == nullptr || aligned16(d_out));
   hipError_t e = launch_get(a, vec4, static_cast<hipStream_t>(hip_stream), hook_of(t));
   if (e != hipSuccess) return hip_fail(e, "mlkv_get launch");
@@ -366,7 +350,6 @@ int put_call(mlkv_table* t, const uint64_t* d_keys, const float* src, int64_t n,
   a.gdesc = t->gdesc;
   a.pmeta = t->pmeta;
   a.flat_blocks = t->flat_blocks;
-  a.bins = OrderBins{t->bin_cnt, t->bin_list, t->bin_cap};
   a.ctrl = t->ctrl;
   a.epoch = t->epoch;
   const bool vec4 = (t->dim % 4 == 0) && aligned16(src);

@@ -33,10 +33,8 @@ struct Ctrl {
   unsigned long long overflow_epoch;  // epoch of a call whose inserts overran the probe bound
   unsigned long long spill_next;      // bump allocator for partitions larger than LDS
   unsigned long long new_epoch;       // epoch of a call that inserted at least one key
-  unsigned long long binover_epoch;   // epoch of a call whose new keys overran an order bin
   int latched;                        // first device-side error since mlkv_sync
-  unsigned int bins_done;             // blocks done reading the order bins (reset by the last)
-  unsigned int pad[4];
+  unsigned int pad[7];
 };
 
 // ---------------------------------------------------------------------------
@@ -58,10 +56,6 @@ __device__ __forceinline__ uint64_t splitmix_mix(uint64_t z) {
   z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
   return z ^ (z >> 31);
 }
-
-// Order value of a key: the rows of the keys a call inserts are numbered in
-// ascending order of mix64(key), a bijection, so no two keys tie.
-__device__ __forceinline__ uint64_t order_value(uint64_t key) { return splitmix_mix(key); }
 
 // Initial value of column c of a new key, given s0 = mix64(key ^ seed): the
 // top 24 bits of mix64(s0 + c * golden gamma), centred and scaled by

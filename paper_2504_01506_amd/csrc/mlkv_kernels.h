@@ -52,20 +52,6 @@ struct LaunchHook {
   }
 };
 
-// Order bins. The rows of the keys a call inserts follow the ascending order
-// of mix64(key); the probe kernels count each inserted key in bin
-// mix64(key) >> (64 - kOrderBits) and list it there (up to `cap` per bin), so
-// that a key's rank is the count of the bins below its own plus its rank
-// within its bin. The counts are all zero between calls.
-constexpr int kOrderBits = 12;
-constexpr int kOrderBins = 1 << kOrderBits;
-
-struct OrderBins {
-  uint32_t* cnt;  // [kOrderBins] keys inserted by the call, per bin
-  NewKey* list;   // [kOrderBins][cap] the first cap of them, per bin
-  uint32_t cap;
-};
-
 struct GetArgs {
   Bucket* idx;
   uint32_t nb_log2;
@@ -81,7 +67,6 @@ struct GetArgs {
   uint32_t* tile_cnt;
   Ctrl* ctrl;
   uint64_t epoch;
-  OrderBins bins;
 };
 
 struct PutArgs {
@@ -113,7 +98,6 @@ struct PutArgs {
   int flat_blocks;    // least number of put_apply blocks (one per CU)
   Ctrl* ctrl;
   uint64_t epoch;
-  OrderBins bins;
 };
 
 hipError_t launch_get(const GetArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook);

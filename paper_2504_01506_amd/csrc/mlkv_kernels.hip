@@ -103,38 +103,11 @@ __device__ __forceinline__ void wave_emit_rows(float* __restrict__ out, const fl
   }
 }
 
-// Counts a key inserted by this call in its order bin and lists it there
-// while the bin has room; a full bin marks the call, whose rows are then
-// ranked the slow way.
-__device__ __forceinline__ void bin_new_key(const OrderBins& bins, uint64_t key, uint32_t slot, Ctrl* ctrl,
-                                            uint64_t epoch) {
-  const uint32_t b = (uint32_t)(order_value(key) >> (64 - kOrderBits));
-  const uint32_t at = atomicAdd(&bins.cnt[b], 1u);
-  if (at < bins.cap) bins.list[(size_t)b * bins.cap + at] = NewKey{key, slot, 0u};
-  else ctrl->binover_epoch = epoch;
-}
-
-// Every block of a kernel that read the order bins calls this after its last
-// read; the last block to arrive clears the counts for the next call.
-__device__ __forceinline__ void release_bins(const OrderBins& bins, Ctrl* ctrl) {
-  __shared__ uint32_t s_last;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __threadfence();
-    s_last = atomicAdd(&ctrl->bins_done, 1u) == gridDim.x - 1 ? 1u : 0u;
-  }
-  __syncthreads();
-  if (s_last) {
-    for (int b = threadIdx.x; b < kOrderBins; b += blockDim.x) bins.cnt[b] = 0u;
-    if (threadIdx.x == 0) ctrl->bins_done = 0u;
-  }
-}
-
 template <class M>
 __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
     Bucket* __restrict__ idx, uint32_t nb_log2, const uint64_t* __restrict__ keys, int64_t n,
     float* __restrict__ out, const float* __restrict__ rows, int D, uint64_t seed,
-    NewKey* __restrict__ newlist, uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch, OrderBins bins) {
+    NewKey* __restrict__ newlist, uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch) {
   __shared__ uint32_t s_cnt;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -159,7 +132,6 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
     const uint32_t j = atomicAdd(&s_cnt, 1u);
     newlist[base + j] = NewKey{key, pr.slot, 0u};
     ctrl->new_epoch = epoch;
-    bin_new_key(bins, key, pr.slot, ctrl, epoch);
   }
   if (out != nullptr) {
     const uint64_t s0 = splitmix_mix(key ^ seed);
@@ -170,13 +142,12 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
 }
 
 // ===========================================================================
-// Streaming the order values of every new key of the call through LDS (the
-// slow way to rank new keys, for calls whose order bins overflowed).
+// Streaming every new key of the call through LDS (used to rank new keys).
 // ===========================================================================
 constexpr int kChunk = 2048;
 
-// Calls body(s_chunk, cnt) for consecutive chunks of the order values of this
-// call's new keys; the block's NT threads must all call it. s_pref: NT+1 words.
+// Calls body(s_chunk, cnt) for consecutive chunks of this call's new keys;
+// the block's NT threads must all call it. s_pref: NT+1 words.
 template <int NT, class Body>
 __device__ __forceinline__ void for_each_new_key_chunk(const NewKey* __restrict__ newlist,
                                        const uint32_t* __restrict__ tile_cnt, int ntiles,
@@ -205,7 +176,7 @@ __device__ __forceinline__ void for_each_new_key_chunk(const NewKey* __restrict_
             if (s_pref[mid] <= gk) lo = mid;
             else hi = mid - 1;
           }
-          v[e] = order_value(newlist[(size_t)(t0 + lo) * tile_size + (gk - s_pref[lo])].key);
+          v[e] = newlist[(size_t)(t0 + lo) * tile_size + (gk - s_pref[lo])].key;
         }
       }
 #pragma unroll
@@ -245,105 +216,31 @@ __device__ __forceinline__ int call_verdict(Ctrl* ctrl, uint64_t epoch, uint64_t
 }
 
 // ===========================================================================
-// Get, second kernel: assign rows to the call's new keys (ascending order
-// value), write their initial rows and zero accumulators; or roll the call
-// back.
+// Get, second kernel: assign rows to the call's new keys (ascending key order),
+// write their initial rows and zero accumulators; or roll the call back.
 // ===========================================================================
 constexpr int kAssignThreads = 256;
 constexpr int kAssignBatch = 8;
-constexpr int kAssignMine = kAssignBatch * kAssignThreads;  // new keys ranked per LDS pass
-constexpr int kBinBatch = 2048;                             // order-bin entries per LDS pass
-
-// Rows for the new keys ks[0, m) (index slots sl[...]) whose ranks among all
-// new keys of the call are base + rk[...]: index row ids, zero accumulators,
-// initial rows.
-template <int NT, class KP, class SP>
-__device__ __forceinline__ void write_new_rows(const KP ks, const SP sl, const uint32_t* rk, uint32_t m,
-                                               uint64_t base, Bucket* __restrict__ idx, float* __restrict__ rows,
-                                               float* __restrict__ state, int D, uint64_t seed) {
-  for (uint32_t j = threadIdx.x; j < m; j += NT) {
-    const uint32_t slot = sl[j];
-    const uint32_t row = (uint32_t)(base + rk[j]);
-    idx[slot / kSlots].row[slot % kSlots] = row;
-    state[row] = 0.0f;
-  }
-  const uint32_t total = m * (uint32_t)D;
-  for (uint32_t e = threadIdx.x; e < total; e += NT) {
-    const uint32_t j = e / (uint32_t)D;
-    const int col = (int)(e - j * (uint32_t)D);
-    rows[(base + rk[j]) * (uint64_t)D + col] = init_elem(splitmix_mix(ks[j] ^ seed), col);
-  }
-}
-
-// The bin [lo, hi) of the order bins that block g of G ranks.
-__device__ __forceinline__ void bin_range(int g, int G, int* lo, int* hi) {
-  *lo = (int)((int64_t)g * kOrderBins / G);
-  *hi = (int)((int64_t)(g + 1) * kOrderBins / G);
-}
-
-// Ranks the new keys of one order bin holding more than kBinBatch of them:
-// up to kAssignMine of its keys at a time against the whole bin, streamed
-// through LDS.
-template <int NT>
-__device__ void assign_big_bin(const NewKey* __restrict__ ent, uint32_t c, uint64_t base, uint64_t* s_cmp,
-                               uint64_t* s_key, uint32_t* s_slot, uint32_t* s_rank, Bucket* __restrict__ idx,
-                               float* __restrict__ rows, float* __restrict__ state, int D, uint64_t seed) {
-  constexpr int PER = kAssignMine / NT;
-  for (uint32_t j0 = 0; j0 < c; j0 += kAssignMine) {
-    const uint32_t m = min((uint32_t)kAssignMine, c - j0);
-    uint64_t mv[PER];
-    uint32_t r[PER];
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      const uint32_t j = threadIdx.x + q * NT;
-      mv[q] = j < m ? order_value(ent[j0 + j].key) : 0ull;
-      r[q] = 0;
-    }
-    for (uint32_t e0 = 0; e0 < c; e0 += kChunk) {
-      const uint32_t cnt = min((uint32_t)kChunk, c - e0);
-      for (uint32_t e = threadIdx.x; e < cnt; e += NT) s_cmp[e] = order_value(ent[e0 + e].key);
-      __syncthreads();
-      for (uint32_t e = 0; e < cnt; ++e) {
-        const uint64_t v = s_cmp[e];
-#pragma unroll
-        for (int q = 0; q < PER; ++q) r[q] += v < mv[q] ? 1u : 0u;
-      }
-      __syncthreads();
-    }
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      const uint32_t j = threadIdx.x + q * NT;
-      if (j < m) {
-        const NewKey nk = ent[j0 + j];
-        s_key[j] = nk.key;
-        s_slot[j] = nk.slot;
-        s_rank[j] = r[q];
-      }
-    }
-    __syncthreads();
-    write_new_rows<NT>(s_key, s_slot, s_rank, m, base, idx, rows, state, D, seed);
-    __syncthreads();
-  }
-}
+constexpr int kAssignMine = kAssignBatch * kAssignThreads;
 
 __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
     Bucket* __restrict__ idx, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
     int ntiles, int tile_size, float* __restrict__ rows, float* __restrict__ state, int D,
-    uint64_t seed, int64_t capacity, Ctrl* ctrl, uint64_t epoch, OrderBins bins) {
+    uint64_t seed, int64_t capacity, Ctrl* ctrl, uint64_t epoch) {
   constexpr int NT = kAssignThreads;
   __shared__ unsigned long long s_w64[NT / 64];
   __shared__ uint32_t s_w[NT / 64];
   __shared__ uint32_t s_pref[NT + 1];
-  __shared__ uint32_t s_btot;
-  // one LDS buffer of 48 KiB; the ranking methods lay it out differently
-  __shared__ uint64_t s_buf[kChunk + 2 * kAssignMine];
-  static_assert(kAssignMine == kBinBatch, "both layouts share the buffer");
+  __shared__ uint64_t s_chunk[kChunk];
+  __shared__ uint64_t s_key[kAssignMine];
+  __shared__ uint32_t s_slot[kAssignMine];
+  __shared__ uint32_t s_rank[kAssignMine];
 
   const uint64_t size0 = ctrl->size[epoch & 1];
   const bool any_new = ctrl->new_epoch == epoch;
   const uint64_t M = any_new ? count_new_keys<NT>(tile_cnt, ntiles, s_w64) : 0ull;
   const int err = call_verdict(ctrl, epoch, size0, M, capacity, ctrl->bad_epoch, ctrl->overflow_epoch);
-  if (M == 0) return;  // nothing was inserted, so the order bins are untouched
+  if (M == 0) return;
 
   if (err) {  // undo this call's insertions: the index returns to its state before the call
     for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
@@ -353,134 +250,68 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
         idx[slot / kSlots].key[slot % kSlots] = kEmptyKey;
       }
     }
-  } else if (ctrl->binover_epoch != epoch) {
-    // ---- the order bins: this block ranks the keys of bins [lo, hi), in
-    // batches of whole bins that fit in LDS. A key's rank is the number of
-    // keys in lower bins plus its rank among the keys of its own bin.
-    uint64_t* s_key = s_buf;                                              // [kBinBatch]
-    uint64_t* s_v = s_buf + kBinBatch;                                    // [kBinBatch]
-    uint32_t* s_slot = reinterpret_cast<uint32_t*>(s_buf + 2 * kBinBatch);  // [kBinBatch]
-    uint32_t* s_rank = s_slot + kBinBatch;                                // [kBinBatch]
-    int lo, hi;
-    bin_range(blockIdx.x, gridDim.x, &lo, &hi);
-    uint64_t below = 0;
-    for (int b = threadIdx.x; b < lo; b += NT) below += bins.cnt[b];
-    uint64_t base = size0 + block_sum_u64<NT>(below, s_w64);
-    for (int b0 = lo; b0 < hi;) {
-      const int bb = b0 + (int)threadIdx.x;
-      const uint32_t c = bb < hi ? bins.cnt[bb] : 0u;
-      uint32_t tot;
-      const uint32_t pre = block_exclusive_scan<NT>(c, s_w, &tot);
-      // the bins that fit in one batch are a prefix of [b0, hi); take at least one
-      const uint32_t fits = (bb < hi && pre + c <= (uint32_t)kBinBatch) ? 1u : 0u;
-      const uint32_t nb = max(1u, (uint32_t)block_sum_u64<NT>(fits, s_w64));
-      s_pref[threadIdx.x] = pre;
-      if (threadIdx.x == nb - 1) s_btot = pre + c;
-      __syncthreads();
-      const uint32_t total = s_btot;
-      if (total > (uint32_t)kBinBatch) {  // one bin larger than a batch
-        assign_big_bin<NT>(bins.list + (size_t)b0 * bins.cap, total, base, s_buf, s_buf + kChunk,
-                           reinterpret_cast<uint32_t*>(s_buf + kChunk + kAssignMine),
-                           reinterpret_cast<uint32_t*>(s_buf + kChunk + kAssignMine) + kAssignMine, idx, rows,
-                           state, D, seed);
-      } else {
-        if (threadIdx.x == 0) s_pref[nb] = total;
-        for (uint32_t e = threadIdx.x; e < total; e += NT) {
-          uint32_t l = 0, h = nb - 1;  // the bin of batch entry e
-          while (l < h) {
-            const uint32_t mid = (l + h + 1) >> 1;
-            if (s_pref[mid] <= e) l = mid;
-            else h = mid - 1;
-          }
-          const NewKey nk = bins.list[(size_t)(b0 + (int)l) * bins.cap + (e - s_pref[l])];
-          s_key[e] = nk.key;
-          s_v[e] = order_value(nk.key);
-          s_slot[e] = nk.slot;
-          s_rank[e] = l;
-        }
-        __syncthreads();
-        for (uint32_t e = threadIdx.x; e < total; e += NT) {
-          const uint32_t l = s_rank[e];
-          const uint32_t f = s_pref[l], t = s_pref[l + 1];
-          const uint64_t v = s_v[e];
-          uint32_t r = 0;
-          for (uint32_t k = f; k < t; ++k) r += s_v[k] < v ? 1u : 0u;
-          s_rank[e] = f + r;
-        }
-        __syncthreads();
-        write_new_rows<NT>(s_key, s_slot, s_rank, total, base, idx, rows, state, D, seed);
-      }
-      __syncthreads();
-      base += total;
-      b0 += (int)nb;
-    }
-  } else {
-    // ---- a bin overflowed: each block ranks the keys of its tiles against
-    // all M new keys of the call, streamed through LDS. This block owns the
-    // tiles t = blockIdx.x (mod gridDim.x) and takes them kAssignBatch at a
-    // time (thread j holds entry j of each tile).
-    uint64_t* s_chunk = s_buf;                                              // [kChunk]
-    uint64_t* s_key = s_buf + kChunk;                                       // [kAssignMine]
-    uint32_t* s_slot = reinterpret_cast<uint32_t*>(s_key + kAssignMine);    // [kAssignMine]
-    uint32_t* s_rank = s_slot + kAssignMine;                                // [kAssignMine]
-    static_assert(kGetTile == NT, "one thread per entry of a probe tile");
-    for (int tb = blockIdx.x; tb < ntiles; tb += gridDim.x * kAssignBatch) {
-      uint32_t have = 0;
-#pragma unroll
-      for (int b = 0; b < kAssignBatch; ++b) {
-        const int t = tb + b * (int)gridDim.x;
-        const uint32_t c = t < ntiles ? tile_cnt[t] : 0u;
-        const uint32_t j = threadIdx.x;
-        const int m = b * NT + (int)j;
-        if (j < c) {
-          const NewKey nk = newlist[(size_t)t * tile_size + j];
-          s_key[m] = nk.key;
-          s_slot[m] = nk.slot;
-          have = 1;
-        } else {
-          s_slot[m] = kPendingRow;  // marks an unused entry
-        }
-        s_rank[m] = 0;
-      }
-      if (block_sum_u64<NT>(have, s_w64) == 0) continue;
-      for_each_new_key_chunk<NT>(newlist, tile_cnt, ntiles, tile_size, s_pref, s_w, s_chunk,
-                                 [&](const uint64_t* ck, uint32_t cnt) {
-#pragma unroll
-                                   for (int b = 0; b < kAssignBatch; ++b) {
-                                     const int m = b * NT + (int)threadIdx.x;
-                                     if (s_slot[m] == kPendingRow) continue;
-                                     const uint64_t mk = order_value(s_key[m]);
-                                     uint32_t r = 0;
-                                     for (uint32_t e = 0; e < cnt; ++e) r += ck[e] < mk ? 1u : 0u;
-                                     s_rank[m] += r;
-                                   }
-                                 });
-#pragma unroll
-      for (int b = 0; b < kAssignBatch; ++b) {
-        const int m = b * NT + (int)threadIdx.x;
-        const uint32_t slot = s_slot[m];
-        if (slot == kPendingRow) continue;
-        const uint32_t row = (uint32_t)(size0 + s_rank[m]);
-        idx[slot / kSlots].row[slot % kSlots] = row;
-        state[row] = 0.0f;
-      }
-      // initial rows, written cooperatively (coalesced along each row)
-      for (int b = 0; b < kAssignBatch; ++b) {
-        const int t = tb + b * (int)gridDim.x;
-        const uint32_t c = t < ntiles ? tile_cnt[t] : 0u;
-        const uint64_t total = (uint64_t)c * (uint64_t)D;
-        for (uint64_t e = threadIdx.x; e < total; e += NT) {
-          const uint32_t j = (uint32_t)(e / (uint64_t)D);
-          const int col = (int)(e - (uint64_t)j * D);
-          const int m = b * NT + (int)j;
-          const uint64_t row = size0 + s_rank[m];
-          rows[row * (uint64_t)D + col] = init_elem(splitmix_mix(s_key[m] ^ seed), col);
-        }
-      }
-      __syncthreads();
-    }
+    return;
   }
-  release_bins(bins, ctrl);
+
+  // This block owns the tiles t = blockIdx.x (mod gridDim.x); it takes them
+  // kAssignBatch at a time (thread j holds entry j of each tile) and ranks
+  // their keys against all M new keys of the call.
+  static_assert(kGetTile == NT, "one thread per entry of a probe tile");
+  for (int tb = blockIdx.x; tb < ntiles; tb += gridDim.x * kAssignBatch) {
+    uint32_t have = 0;
+#pragma unroll
+    for (int b = 0; b < kAssignBatch; ++b) {
+      const int t = tb + b * (int)gridDim.x;
+      const uint32_t c = t < ntiles ? tile_cnt[t] : 0u;
+      const uint32_t j = threadIdx.x;
+      const int m = b * NT + (int)j;
+      if (j < c) {
+        const NewKey nk = newlist[(size_t)t * tile_size + j];
+        s_key[m] = nk.key;
+        s_slot[m] = nk.slot;
+        have = 1;
+      } else {
+        s_slot[m] = kPendingRow;  // marks an unused entry
+      }
+      s_rank[m] = 0;
+    }
+    if (block_sum_u64<NT>(have, s_w64) == 0) continue;
+    for_each_new_key_chunk<NT>(newlist, tile_cnt, ntiles, tile_size, s_pref, s_w, s_chunk,
+                               [&](const uint64_t* ck, uint32_t cnt) {
+#pragma unroll
+                                 for (int b = 0; b < kAssignBatch; ++b) {
+                                   const int m = b * NT + (int)threadIdx.x;
+                                   if (s_slot[m] == kPendingRow) continue;
+                                   const uint64_t mk = s_key[m];
+                                   uint32_t r = 0;
+                                   for (uint32_t e = 0; e < cnt; ++e) r += ck[e] < mk ? 1u : 0u;
+                                   s_rank[m] += r;
+                                 }
+                               });
+#pragma unroll
+    for (int b = 0; b < kAssignBatch; ++b) {
+      const int m = b * NT + (int)threadIdx.x;
+      const uint32_t slot = s_slot[m];
+      if (slot == kPendingRow) continue;
+      const uint32_t row = (uint32_t)(size0 + s_rank[m]);
+      idx[slot / kSlots].row[slot % kSlots] = row;
+      state[row] = 0.0f;
+    }
+    // initial rows, written cooperatively (coalesced along each row)
+    for (int b = 0; b < kAssignBatch; ++b) {
+      const int t = tb + b * (int)gridDim.x;
+      const uint32_t c = t < ntiles ? tile_cnt[t] : 0u;
+      const uint64_t total = (uint64_t)c * (uint64_t)D;
+      for (uint64_t e = threadIdx.x; e < total; e += NT) {
+        const uint32_t j = (uint32_t)(e / (uint64_t)D);
+        const int col = (int)(e - (uint64_t)j * D);
+        const int m = b * NT + (int)j;
+        const uint64_t row = size0 + s_rank[m];
+        rows[row * (uint64_t)D + col] = init_elem(splitmix_mix(s_key[m] ^ seed), col);
+      }
+    }
+    __syncthreads();
+  }
 }
 
 // ===========================================================================
@@ -526,7 +357,7 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
     const float* __restrict__ grads, int64_t n, int tlen, int D, int op, int pb, int ntiles,
     uint64_t* __restrict__ items,
     uint32_t* __restrict__ meta, double* __restrict__ partials, NewKey* __restrict__ newlist,
-    uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch, OrderBins bins) {
+    uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch) {
   constexpr int NT = kPutThreads;
   constexpr int KPT = kPutTile / kPutThreads;  // keys per thread
   constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
@@ -730,7 +561,6 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
       const uint32_t j = atomicAdd(&s_cnt, 1u);
       newlist[(size_t)sbase + j] = NewKey{key[kk], pr[kk].slot, 0u};
       ctrl->new_epoch = epoch;
-      bin_new_key(bins, key[kk], pr[kk].slot, ctrl, epoch);
     }
     const bool fresh = pr[kk].status != P_HIT;
     uint32_t pos = (uint32_t)(base + e);
@@ -939,8 +769,6 @@ struct RedCtx {
   float lr;
   float eps;
   uint64_t size0;
-  OrderBins bins;
-  bool by_bins;  // rank new keys through the order bins (none overflowed)
 };
 
 // Run-length encodes items sorted by value: seg[s] = first item of segment s,
@@ -963,36 +791,15 @@ __device__ __forceinline__ uint32_t encode_segments(IP it, uint32_t mp, SP seg, 
 }
 
 // Keys first inserted by this call get rows size0 + rank among all new keys
-// of the call (ascending order value); the row replaces the slot in the
-// segment's first item, whose "fresh" bit stays set. The new row starts from
-// its initial value and a zero accumulator. s_chunk: 16 KiB of LDS.
+// of the call; the row replaces the slot in the segment's first item, whose
+// "fresh" bit stays set. The new row starts from its initial value and a zero
+// accumulator.
 template <int NT, class IP, class SP>
 __device__ __forceinline__ void resolve_new_rows(IP it, SP seg, uint32_t S, const RedCtx& c,
                                                  const NewKey* __restrict__ newlist,
                                                  const uint32_t* __restrict__ tile_cnt, int ntiles,
                                                  uint32_t* s_pref, uint32_t* s_w,
                                                  unsigned long long* s_w64, uint64_t* s_chunk) {
-  // with the order bins: the exclusive prefix of the bin counts, in LDS
-  uint32_t* s_bin = reinterpret_cast<uint32_t*>(s_chunk);
-  static_assert(kOrderBins * sizeof(uint32_t) <= kChunk * sizeof(uint64_t), "bin prefix fits the chunk area");
-  static_assert(kOrderBins % NT == 0, "bins per thread");
-  if (c.by_bins) {
-    constexpr int PER = kOrderBins / NT;
-    uint32_t cnt[PER], sum = 0;
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      cnt[q] = c.bins.cnt[threadIdx.x * PER + q];
-      sum += cnt[q];
-    }
-    uint32_t tot;
-    uint32_t off = block_exclusive_scan<NT>(sum, s_w, &tot);
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      s_bin[threadIdx.x * PER + q] = off;
-      off += cnt[q];
-    }
-    __syncthreads();
-  }
   for (uint32_t s0 = 0; s0 < S; s0 += NT) {
     const uint32_t s = s0 + threadIdx.x;
     bool pend = false;
@@ -1006,31 +813,12 @@ __device__ __forceinline__ void resolve_new_rows(IP it, SP seg, uint32_t S, cons
     const uint64_t npend = block_sum_u64<NT>(pend ? 1u : 0u, s_w64);
     if (npend == 0) continue;
     const uint64_t key = pend ? c.idx[slot / kSlots].key[slot % kSlots] : 0ull;
-    const uint64_t v = order_value(key);
     uint32_t rank = 0;
-    if (c.by_bins) {
-      if (pend) {  // keys of lower bins, then the keys of this bin below v
-        const uint32_t b = (uint32_t)(v >> (64 - kOrderBits));
-        const uint32_t cnt = c.bins.cnt[b];
-        const NewKey* ent = c.bins.list + (size_t)b * c.bins.cap;
-        uint32_t e = 0;
-        for (; e + 8 <= cnt; e += 8) {
-          uint64_t k8[8];
-#pragma unroll
-          for (int u = 0; u < 8; ++u) k8[u] = ent[e + u].key;
-#pragma unroll
-          for (int u = 0; u < 8; ++u) rank += order_value(k8[u]) < v ? 1u : 0u;
-        }
-        for (; e < cnt; ++e) rank += order_value(ent[e].key) < v ? 1u : 0u;
-        rank += s_bin[b];
-      }
-    } else {
-      for_each_new_key_chunk<NT>(newlist, tile_cnt, ntiles, kPutTile, s_pref, s_w, s_chunk,
-                                 [&](const uint64_t* ck, uint32_t cnt) {
-                                   if (pend)
-                                     for (uint32_t e = 0; e < cnt; ++e) rank += ck[e] < v ? 1u : 0u;
-                                 });
-    }
+    for_each_new_key_chunk<NT>(newlist, tile_cnt, ntiles, kPutTile, s_pref, s_w, s_chunk,
+                               [&](const uint64_t* ck, uint32_t cnt) {
+                                 if (pend)
+                                   for (uint32_t e = 0; e < cnt; ++e) rank += ck[e] < key ? 1u : 0u;
+                               });
     if (pend) {
       const uint32_t row = (uint32_t)(c.size0 + rank);
       c.idx[slot / kSlots].row[slot % kSlots] = row;
@@ -1491,13 +1279,13 @@ __device__ __forceinline__ void reduce_partition_global(uint32_t p, uint32_t mp,
 // for LDS is summed and updated here, in a global scratch area.
 // ---------------------------------------------------------------------------
 template <class M, int NT>
-__device__ __forceinline__ void put_group_block(
+__global__ __launch_bounds__(NT) void k_put_group(
     Bucket* __restrict__ idx, const uint64_t* __restrict__ items, const uint32_t* __restrict__ meta,
     int ntiles, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
     const float* __restrict__ grads, const double* __restrict__ partials, float* __restrict__ rows,
     float* __restrict__ state, int D, uint64_t seed, float lr, float eps, int64_t capacity, Ctrl* ctrl,
     uint64_t epoch, uint64_t* __restrict__ spill, uint64_t spill_words, uint64_t* __restrict__ gitems,
-    uint32_t* __restrict__ gdesc, PartMeta* __restrict__ pmeta, int op, const OrderBins& bins) {
+    uint32_t* __restrict__ gdesc, PartMeta* __restrict__ pmeta, int op) {
   using L = RedLds<NT>;
   constexpr int IPT = (kRedCap + NT - 1) / NT;
   extern __shared__ __align__(16) unsigned char s_raw[];
@@ -1555,8 +1343,7 @@ __device__ __forceinline__ void put_group_block(
     return;
   }
 
-  const RedCtx c{op, idx, grads, partials, rows, state, D, seed, lr, eps, size0, bins,
-                 ctrl->binover_epoch != epoch};
+  const RedCtx c{op, idx, grads, partials, rows, state, D, seed, lr, eps, size0};
   if (mp > (uint32_t)kRedCap) {
     reduce_partition_global<M, NT>(p, mp, items, meta, ntiles, c, newlist, tile_cnt, ctrl, spill, spill_words,
                                    s_part, s_pref, s_w, s_w64, s_base);
@@ -1627,19 +1414,6 @@ __device__ __forceinline__ void put_group_block(
     gd[i] = s_seg[s] | (s_seg[s + 1] << 16);
   }
   if (tid == 0) pmeta[p] = PartMeta{s_seg[n_sum], S, n_sum, 0u};
-}
-
-template <class M, int NT>
-__global__ __launch_bounds__(NT) void k_put_group(
-    Bucket* __restrict__ idx, const uint64_t* __restrict__ items, const uint32_t* __restrict__ meta,
-    int ntiles, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
-    const float* __restrict__ grads, const double* __restrict__ partials, float* __restrict__ rows,
-    float* __restrict__ state, int D, uint64_t seed, float lr, float eps, int64_t capacity, Ctrl* ctrl,
-    uint64_t epoch, uint64_t* __restrict__ spill, uint64_t spill_words, uint64_t* __restrict__ gitems,
-    uint32_t* __restrict__ gdesc, PartMeta* __restrict__ pmeta, int op, OrderBins bins) {
-  put_group_block<M, NT>(idx, items, meta, ntiles, newlist, tile_cnt, grads, partials, rows, state, D, seed, lr,
-                         eps, capacity, ctrl, epoch, spill, spill_words, gitems, gdesc, pmeta, op, bins);
-  if (ctrl->new_epoch == epoch) release_bins(bins, ctrl);  // the call inserted keys: it used the bins
 }
 
 // Exclusive prefix over partitions of f(pmeta[p]) into out[0, np]; the block's
@@ -2069,7 +1843,7 @@ static hipError_t launch_get_t(const GetArgs& a, hipStream_t st, const LaunchHoo
   hook(K_GET_PROBE_GATHER, 0, st);
   hipLaunchKernelGGL(k_get_probe_gather<M>, dim3((unsigned)ntiles), dim3(kGetTile), 0, st, a.idx,
                      a.nb_log2, a.keys, a.n, a.out, a.rows, a.D, a.seed, a.newlist, a.tile_cnt, a.ctrl,
-                     a.epoch, a.bins);
+                     a.epoch);
   hook(K_GET_PROBE_GATHER, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -2077,7 +1851,7 @@ static hipError_t launch_get_t(const GetArgs& a, hipStream_t st, const LaunchHoo
   hook(K_ASSIGN_NEW, 0, st);
   hipLaunchKernelGGL(k_assign_new, dim3(grid), dim3(kAssignThreads), 0, st, a.idx, a.newlist,
                      a.tile_cnt, (int)ntiles, kGetTile, a.rows, a.state, a.D, a.seed, a.capacity,
-                     a.ctrl, a.epoch, a.bins);
+                     a.ctrl, a.epoch);
   hook(K_ASSIGN_NEW, 1, st);
   return hipGetLastError();
 }
@@ -2097,7 +1871,7 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   hook(K_PUT_PROBE, 0, st);
   hipLaunchKernelGGL(k_put_probe<M>, dim3((unsigned)ntiles), dim3(kPutThreads), 0, st, a.idx, a.nb_log2,
                      a.keys, a.grads, a.n, a.tlen, a.D, a.op, a.pb, (int)ntiles, a.items, a.meta, a.partials,
-                     a.newlist, a.tile_cnt, a.ctrl, a.epoch, a.bins);
+                     a.newlist, a.tile_cnt, a.ctrl, a.epoch);
   hook(K_PUT_PROBE, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -2117,7 +1891,7 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   hipLaunchKernelGGL((k_put_group<M, NT>), dim3((unsigned)np), dim3(NT), L::total, st, a.idx, a.items,
                      a.meta, (int)ntiles, a.newlist, a.tile_cnt, a.grads, a.partials, a.rows, a.state,
                      a.D, a.seed, a.lr, a.eps, a.capacity, a.ctrl, a.epoch, a.spill, a.spill_words, a.gitems,
-                     a.gdesc, a.pmeta, a.op, a.bins);
+                     a.gdesc, a.pmeta, a.op);
   hook(K_PUT_GROUP, 1, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int apply_blocks = (int)std::max<int64_t>((int64_t)a.flat_blocks * ApplyCfg<M>::kPerCU,

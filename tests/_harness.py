@@ -56,12 +56,12 @@ class Pair:
 
     def prefill(self, keys_sorted: np.ndarray, chunk: int = 1 << 16):
         """Inserts ascending keys through get(out=NULL) in chunks on the GPU, and
-        as a bulk prefill with the same chunks in the oracle."""
+        as one sorted prefill in the oracle (identical rows: row = rank)."""
         for s in range(0, keys_sorted.size, chunk):
             k = dev_keys(keys_sorted[s:s + chunk])
             self.gpu.get(k, None)
         assert self.gpu.sync() == mlkv.MLKV_OK
-        assert self.ora.prefill_sorted(keys_sorted, chunk) == O.OK
+        assert self.ora.prefill_sorted(keys_sorted) == O.OK
         assert self.gpu.size == self.ora.size == keys_sorted.size
 
     def get(self, keys: np.ndarray, check: bool = True):

@@ -7,7 +7,6 @@ import numpy as np
 import pytest
 import torch
 
-from oracle import oracle as O
 from paper_2504_01506_amd import mlkv, workloads as W
 from _harness import Pair, dev, dev_keys, log
 
@@ -104,108 +103,6 @@ def test_put_inserts_unseen_keys_then_updates_them():
     pr.compare_rows()
     pr.check_index()
     pr.get(keys)
-    pr.close()
-
-
-@pytest.mark.parametrize("case", ["random", "descending", "second_half_new", "clustered"])
-def test_many_new_keys_get_rows_in_mix64_order(case):
-    """A call inserting many new keys: their rows follow the ascending mix64
-    order of the keys, whatever their batch order or value distribution."""
-    rng = np.random.default_rng(21)
-    dim, n = 5, 120_000
-    pr = Pair(dim, 400_000)
-    keys = rng.choice(np.uint64(1) << np.uint64(62), size=n, replace=False).astype(np.uint64)
-    if case == "descending":
-        keys = np.sort(keys)[::-1].copy()
-    elif case == "second_half_new":  # the first half of the batch are hits
-        pr.get(np.sort(keys[: n // 2]))
-    elif case == "clustered":  # a dense run of small keys and a few huge ones
-        keys = np.concatenate([np.arange(1, n - 100, dtype=np.uint64) * np.uint64(3),
-                               (np.uint64(1) << np.uint64(63)) + np.arange(100, dtype=np.uint64)])
-        keys = keys[rng.permutation(keys.size)]
-    pr.get(keys)
-    log(f"[parity] many new keys ({case}): size={pr.gpu.size}")
-    pr.compare_rows()
-    pr.check_index()
-    pr.close()
-
-
-def _mix64(z: np.ndarray) -> np.ndarray:
-    """SplitMix64's output function on a uint64 array (wrapping products)."""
-    z = z.astype(np.uint64)
-    z = (z ^ (z >> np.uint64(30))) * np.uint64(0xBF58476D1CE4E5B9)
-    z = (z ^ (z >> np.uint64(27))) * np.uint64(0x94D049BB133111EB)
-    return z ^ (z >> np.uint64(31))
-
-
-def _one_bin_keys(count, rng, top=0x5A5):
-    """Distinct keys whose mix64 values share their top 12 bits."""
-    chk = rng.integers(1, 2**62, size=4, dtype=np.uint64)
-    assert [int(x) for x in _mix64(chk)] == [O.mix64(int(x)) for x in chk]
-    out = np.empty(0, dtype=np.uint64)
-    while out.size < count:
-        cand = rng.integers(1, 2**62, size=1 << 20, dtype=np.uint64)
-        out = np.unique(np.concatenate([out, cand[(_mix64(cand) >> np.uint64(52)) == np.uint64(top)]]))
-    return rng.permutation(out[:count])
-
-
-@pytest.mark.parametrize("call", ["get", "put_grad", "upsert"])
-def test_overflowing_order_bin_falls_back_to_full_ranking(call):
-    """More new keys in one order bin than it lists (crafted keys): the call
-    ranks them the slow way, with the same result; the next call uses the
-    bins again."""
-    rng = np.random.default_rng(31)
-    dim = 6
-    same = _one_bin_keys(300, rng)
-    keys = np.concatenate([same, rng.integers(1, 2**62, size=3000, dtype=np.uint64), same[:50]])
-    keys = keys[rng.permutation(keys.size)]
-    pr = Pair(dim, 20_000)
-    g = rng.normal(0, 0.01, size=(keys.size, dim)).astype(np.float32)
-    if call == "get":
-        pr.get(keys)
-    elif call == "put_grad":
-        pr.put(keys, g, 0.05, 1e-8)
-    else:
-        pr.upsert(keys, g)
-    pr.compare_rows()
-    pr.check_index()
-    more = rng.integers(1, 2**62, size=5000, dtype=np.uint64)
-    pr.get(more)
-    pr.put(more[:2000], rng.normal(0, 0.01, size=(2000, dim)).astype(np.float32), 0.05, 1e-8)
-    pr.compare_rows()
-    pr.check_index()
-    pr.close()
-
-
-def test_millions_of_new_keys_in_one_get():
-    """Order bins holding more keys than one LDS chunk."""
-    rng = np.random.default_rng(22)
-    n = 2_600_000
-    pr = Pair(2, n + 10)
-    keys = rng.choice(np.uint64(1) << np.uint64(40), size=n, replace=False).astype(np.uint64)
-    k = dev_keys(keys)
-    pr.gpu.get(k, None)
-    rc, _ = pr.ora.get(keys)
-    assert rc == 0 and pr.gpu.sync() == mlkv.MLKV_OK
-    got = pr.gpu.lookup_rows(k).cpu().numpy()
-    assert np.array_equal(got, pr.ora.lookup_rows(keys))
-    pr.compare_rows(np.arange(0, n, 997, dtype=np.int64))
-    pr.close()
-
-
-def test_many_new_keys_over_capacity_roll_back():
-    dim = 3
-    pr = Pair(dim, 30_000)
-    pr.get(np.arange(1000, dtype=np.uint64))
-    k = dev_keys(np.arange(10_000, 50_000, dtype=np.uint64))
-    pr.gpu.get(k, None)
-    assert pr.gpu.sync() == mlkv.MLKV_EFULL
-    assert pr.gpu.size == 1000
-    pr.check_index()
-    pr.get(np.arange(10_000, 35_000, dtype=np.uint64))  # 25,000 new keys fit
-    assert pr.gpu.size == 26_000
-    pr.compare_rows()
-    pr.check_index()
     pr.close()
 
 
