@@ -294,6 +294,8 @@ int mlkv_get(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, voi
   a.tile_cnt = t->tile_cnt;
   a.ctrl = t->ctrl;
   a.epoch = t->epoch;
+  a.xkey = t->items;  // the put pipeline's scratch (at least n entries each), idle during a get
+  a.xslot = t->meta;
   const bool vec4 = (t->dim % 4 == 0) && (d_out == nullptr || aligned16(d_out));
   hipError_t e = launch_get(a, vec4, static_cast<hipStream_t>(hip_stream), hook_of(t));
   if (e != hipSuccess) return hip_fail(e, "mlkv_get launch");

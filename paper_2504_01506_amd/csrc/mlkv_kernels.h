@@ -67,6 +67,8 @@ struct GetArgs {
   uint32_t* tile_cnt;
   Ctrl* ctrl;
   uint64_t epoch;
+  uint64_t* xkey;   // [n] scratch: new keys of a key range too large for LDS
+  uint32_t* xslot;  // [n] their index slots
 };
 
 struct PutArgs {

@@ -130,7 +130,7 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
   }
   if (pr.status == P_NEW_MINE) {
     const uint32_t j = atomicAdd(&s_cnt, 1u);
-    newlist[base + j] = NewKey{key, pr.slot, 0u};
+    newlist[base + j] = NewKey{key, pr.slot, (uint32_t)i};  // i: where get's output holds the initial row
     ctrl->new_epoch = epoch;
   }
   if (out != nullptr) {
@@ -222,19 +222,137 @@ __device__ __forceinline__ int call_verdict(Ctrl* ctrl, uint64_t epoch, uint64_t
 constexpr int kAssignThreads = 256;
 constexpr int kAssignBatch = 8;
 constexpr int kAssignMine = kAssignBatch * kAssignThreads;
+constexpr int kAssignDirect = 8192;  // up to this many new keys, each block ranks its tiles' keys against all
+constexpr int kRangeSamples = 512;   // sample of the new keys that splits the key space among the blocks
+constexpr int kRangeCap = 2560;      // keys of a block's key range ranked in LDS at once
+constexpr int kScanBatch = 16;       // key loads a lane has in flight while scanning all new keys
+
+// Calls body(key, entry) once for every new key of the call, in no set order
+// (entry: its NewKey in the tiles' lists); the block's NT threads must all
+// call it. Tiles are taken kScanTiles per thread at a time; each wave walks a
+// contiguous run of their entries, 64 consecutive entries per load, with
+// kScanBatch loads in flight. s_pref: kScanTiles * NT + 1 words.
+constexpr int kScanTiles = 4;
+template <int NT, class Body>
+__device__ __forceinline__ void scan_new_keys(const NewKey* __restrict__ newlist,
+                                              const uint32_t* __restrict__ tile_cnt, int ntiles, int tile_size,
+                                              uint32_t* s_pref, uint32_t* s_w, Body body) {
+  constexpr int CT = kScanTiles * NT;
+  constexpr int NW = NT / 64;
+  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int t0 = 0; t0 < ntiles; t0 += CT) {
+    const int nt = min(CT, ntiles - t0);
+    uint32_t c[kScanTiles], sum = 0;
+#pragma unroll
+    for (int q = 0; q < kScanTiles; ++q) {
+      const int t = (int)threadIdx.x * kScanTiles + q;
+      c[q] = t < nt ? tile_cnt[t0 + t] : 0u;
+      sum += c[q];
+    }
+    uint32_t tot;
+    uint32_t off = block_exclusive_scan<NT>(sum, s_w, &tot);
+#pragma unroll
+    for (int q = 0; q < kScanTiles; ++q) {
+      s_pref[threadIdx.x * kScanTiles + q] = off;
+      off += c[q];
+    }
+    if (threadIdx.x == 0) s_pref[CT] = tot;
+    lds_barrier();
+    const uint32_t span = (tot + NW * 64 - 1) / (NW * 64) * 64;  // entries per wave, a multiple of 64
+    const uint32_t wb = min(tot, wave * span), we = min(tot, wb + span);
+    for (uint32_t e0 = wb + lane; e0 < we; e0 += 64 * kScanBatch) {
+      // the tile of each entry: the last t with s_pref[t] <= e, by a
+      // branch-free binary search over CT tiles, kScanBatch at a time
+      uint32_t t[kScanBatch];
+#pragma unroll
+      for (int u = 0; u < kScanBatch; ++u) t[u] = 0;
+#pragma unroll
+      for (int step = CT / 2; step >= 1; step >>= 1) {
+#pragma unroll
+        for (int u = 0; u < kScanBatch; ++u)
+          if (s_pref[t[u] + step] <= e0 + 64 * u) t[u] += step;
+      }
+      uint32_t at[kScanBatch];  // offsets into the lists
+      uint64_t key[kScanBatch];
+#pragma unroll
+      for (int u = 0; u < kScanBatch; ++u) {
+        const uint32_t e = e0 + 64 * u;
+        at[u] = 0;
+        key[u] = kEmptyKey;
+        if (e < we) {
+          at[u] = (uint32_t)(t0 + t[u]) * (uint32_t)tile_size + (e - s_pref[t[u]]);
+          key[u] = newlist[at[u]].key;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kScanBatch; ++u)
+        if (key[u] != kEmptyKey) body(key[u], newlist + at[u]);
+    }
+    lds_barrier();
+  }
+}
+
+// Initial rows of new keys ks[j] (j < m) at rows base + rk[j]: a wave per
+// row, its lanes along the row. When the get call has an output, the row is
+// copied from the output row at position ps[j], which holds the same values.
+template <int NT, class KP, class RP, class PP>
+__device__ __forceinline__ void write_init_rows(const KP ks, const RP rk, const PP ps, uint32_t m, uint64_t base,
+                                                float* __restrict__ rows, int D, uint64_t seed,
+                                                const float* __restrict__ out) {
+  constexpr int NW = NT / 64, R = 8;  // rows a wave copies at once
+  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (out != nullptr) {
+    for (uint32_t j0 = wave * R; j0 < m; j0 += NW * R) {
+      for (int col = (int)lane; col < D; col += 64) {
+        float v[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+          if (j0 + r < m) v[r] = out[(uint64_t)ps[j0 + r] * (uint64_t)D + col];
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+          if (j0 + r < m) rows[(base + rk[j0 + r]) * (uint64_t)D + col] = v[r];
+      }
+    }
+  } else {
+    for (uint32_t j = wave; j < m; j += NW) {
+      float* w = rows + (base + rk[j]) * (uint64_t)D;
+      const uint64_t s0 = splitmix_mix(ks[j] ^ seed);
+      for (int col = (int)lane; col < D; col += 64) w[col] = init_elem(s0, col);
+    }
+  }
+}
+
+// Rows for the new keys ks[0, m) (index slots sl[...]) whose ranks among all
+// new keys of the call are base + rk[...]: index row ids, zero accumulators,
+// initial rows (written along rows).
+template <int NT, class KP, class SP, class RP>
+__device__ __forceinline__ void write_new_rows(const KP ks, const SP sl, const RP rk, uint32_t m, uint64_t base,
+                                               Bucket* __restrict__ idx, float* __restrict__ rows,
+                                               float* __restrict__ state, int D, uint64_t seed) {
+  for (uint32_t j = threadIdx.x; j < m; j += NT) {
+    const uint32_t slot = sl[j];
+    const uint32_t row = (uint32_t)(base + rk[j]);
+    idx[slot / kSlots].row[slot % kSlots] = row;
+    state[row] = 0.0f;
+  }
+  write_init_rows<NT>(ks, rk, ks, m, base, rows, D, seed, nullptr);
+}
 
 __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
     Bucket* __restrict__ idx, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
     int ntiles, int tile_size, float* __restrict__ rows, float* __restrict__ state, int D,
-    uint64_t seed, int64_t capacity, Ctrl* ctrl, uint64_t epoch) {
+    uint64_t seed, int64_t capacity, Ctrl* ctrl, uint64_t epoch, uint64_t* __restrict__ xkey,
+    uint32_t* __restrict__ xslot, const float* __restrict__ out) {
   constexpr int NT = kAssignThreads;
   __shared__ unsigned long long s_w64[NT / 64];
   __shared__ uint32_t s_w[NT / 64];
-  __shared__ uint32_t s_pref[NT + 1];
-  __shared__ uint64_t s_chunk[kChunk];
-  __shared__ uint64_t s_key[kAssignMine];
-  __shared__ uint32_t s_slot[kAssignMine];
-  __shared__ uint32_t s_rank[kAssignMine];
+  __shared__ __align__(16) uint32_t s_pref[kScanTiles * NT + 1];
+  __shared__ uint32_t s_nc;
+  __shared__ uint64_t s_cut[2];
+  // one LDS buffer of 48 KiB; the two ranking methods lay it out differently
+  __shared__ uint64_t s_buf[kChunk + 2 * kAssignMine];
+  static_assert(kRangeCap * 18 <= (int)sizeof(s_buf) && kRangeSamples * 12 <= (int)sizeof(s_buf), "LDS");
+  static_assert(kRangeSamples % NT == 0 && kRangeCap <= 65536, "sample and range sizes");
 
   const uint64_t size0 = ctrl->size[epoch & 1];
   const bool any_new = ctrl->new_epoch == epoch;
@@ -253,9 +371,243 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
     return;
   }
 
-  // This block owns the tiles t = blockIdx.x (mod gridDim.x); it takes them
-  // kAssignBatch at a time (thread j holds entry j of each tile) and ranks
-  // their keys against all M new keys of the call.
+  if (M > (uint64_t)kAssignDirect) {
+    // ---- many new keys: key ranges. Every block takes the same sample of the
+    // new keys (sample k is the new key at position floor(k M / S) of the
+    // tiles' lists laid end to end) and the same cut points from it, which
+    // give block g the keys in [lo, hi). One scan over all new keys counts
+    // those below lo, the block's first rank, and gathers the block's own,
+    // which are then ranked among themselves. No block waits for another.
+    constexpr uint32_t S = kRangeSamples;
+    uint64_t* s_smp = s_buf;                                       // [S]
+    uint32_t* s_sat = reinterpret_cast<uint32_t*>(s_buf + S);     // [S] offsets of the samples in the lists
+    {
+      const int tpt = (ntiles + NT - 1) / NT;  // consecutive tiles per thread
+      const int tb = min(ntiles, (int)threadIdx.x * tpt), te = min(ntiles, tb + tpt);
+      uint32_t mine = 0;
+      for (int t = tb; t < te; ++t) mine += tile_cnt[t];
+      uint32_t tot;
+      uint64_t pre = block_exclusive_scan<NT>(mine, s_w, &tot);
+      uint64_t k = (pre * S + M - 1) / M;  // first sample at or after pre
+      for (int t = tb; t < te && k < S; ++t) {
+        const uint32_t c = tile_cnt[t];
+        for (; k < S; ++k) {
+          const uint64_t gk = k * M / S;
+          if (gk >= pre + c) break;
+          s_sat[k] = (uint32_t)t * (uint32_t)tile_size + (uint32_t)(gk - pre);
+        }
+        pre += c;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (uint32_t u = 0; u < S / NT; ++u) s_smp[threadIdx.x + u * NT] = newlist[s_sat[threadIdx.x + u * NT]].key;
+    __syncthreads();
+    // the cut points: the samples of rank g S / G and (g + 1) S / G (samples
+    // are distinct keys, so ranks are too)
+    const uint32_t g = blockIdx.x, G = gridDim.x;
+    {
+      const uint32_t r1 = (uint32_t)((uint64_t)g * S / G), r2 = (uint32_t)((uint64_t)(g + 1) * S / G);
+      uint64_t v[S / NT];
+      uint32_t r[S / NT];
+#pragma unroll
+      for (uint32_t u = 0; u < S / NT; ++u) {
+        v[u] = s_smp[threadIdx.x + u * NT];
+        r[u] = 0;
+      }
+      for (uint32_t e = 0; e < S; e += 2) {
+        const uint64_t x0 = s_smp[e], x1 = s_smp[e + 1];
+#pragma unroll
+        for (uint32_t u = 0; u < S / NT; ++u) r[u] += (x0 < v[u] ? 1u : 0u) + (x1 < v[u] ? 1u : 0u);
+      }
+      __syncthreads();
+#pragma unroll
+      for (uint32_t u = 0; u < S / NT; ++u) {
+        if (r[u] == r1) s_cut[0] = v[u];
+        if (r[u] == r2) s_cut[1] = v[u];
+      }
+      if (threadIdx.x == 0) s_nc = 0;
+      __syncthreads();
+    }
+    const uint64_t lo = g == 0 ? 0ull : s_cut[0];
+    const uint64_t hi = g + 1 == G ? kEmptyKey : s_cut[1];
+    // keys in [lo, hi) first go to LDS: key, slot (later the rank), and
+    // their order by local sub-range
+    uint64_t* s_key = s_buf;                                                 // [kRangeCap]
+    uint32_t* s_sr = reinterpret_cast<uint32_t*>(s_buf + kRangeCap);        // [kRangeCap]
+    uint32_t* s_pos = s_sr + kRangeCap;                                      // [kRangeCap]
+    uint16_t* s_ord = reinterpret_cast<uint16_t*>(s_pos + kRangeCap);       // [kRangeCap]
+    uint64_t below = 0;
+    scan_new_keys<NT>(newlist, tile_cnt, ntiles, tile_size, s_pref, s_w, [&](uint64_t key, const NewKey* ent) {
+      if (key < lo) {
+        ++below;
+      } else if (key < hi) {
+        const uint32_t at = atomicAdd(&s_nc, 1u);
+        if (at < (uint32_t)kRangeCap) {
+          const NewKey nk = *ent;
+          s_key[at] = key;
+          s_sr[at] = nk.slot;
+          s_pos[at] = nk.pad;
+        }
+      }
+    });
+    below = block_sum_u64<NT>(below, s_w64);  // its barriers also publish s_nc and the gathered keys
+    const uint32_t c = s_nc;
+    const uint64_t base = size0 + below;
+    if (c <= (uint32_t)kRangeCap) {
+      // rank among the range's keys, through kSub local sub-ranges cut at a
+      // sample of the gathered keys: sub-range counts and their prefix, the
+      // keys listed by sub-range, then each key ranked inside its sub-range
+      constexpr int kSub = 32;
+      uint64_t* s_lc = reinterpret_cast<uint64_t*>(s_pref);  // [kSub - 1] local cut points (s_pref is free)
+      uint32_t* s_sc = s_pref + 2 * kSub;                      // [kSub + 1] counts, then prefix, then cursors
+      const uint32_t nl = c < (uint32_t)(kSub * 4) ? 0u : (uint32_t)kSub - 1;  // small ranges: one sub-range
+      if (threadIdx.x < nl) {  // local cut l: the rank-l key of an evenly spaced sample of the gathered keys
+        const uint64_t x = s_key[(uint64_t)(threadIdx.x + 1) * c / kSub];
+        uint32_t rr = 0;
+        for (uint32_t l = 0; l < nl; ++l) rr += s_key[(uint64_t)(l + 1) * c / kSub] < x ? 1u : 0u;
+        s_lc[rr] = x;
+      }
+      if (threadIdx.x <= (uint32_t)kSub) s_sc[threadIdx.x] = 0;
+      __syncthreads();
+      uint32_t sub[kRangeCap / NT];
+#pragma unroll
+      for (int u = 0; u < kRangeCap / NT; ++u) {
+        const uint32_t j = threadIdx.x + u * NT;
+        sub[u] = 0;
+        if (j < c) {
+          const uint64_t key = s_key[j];
+          uint32_t l = 0;  // sub-range l holds keys in [cut l-1, cut l): l = cuts <= key
+          if (nl) {
+#pragma unroll
+            for (uint32_t step = kSub / 2; step >= 1; step >>= 1)
+              if (l + step <= nl && s_lc[l + step - 1] <= key) l += step;
+          }
+          sub[u] = l;
+          atomicAdd(&s_sc[l], 1u);
+        }
+      }
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        uint32_t acc = 0;
+        for (int l = 0; l <= kSub; ++l) {
+          const uint32_t x = s_sc[l];
+          s_sc[l] = acc;
+          acc += x;
+        }
+      }
+      __syncthreads();
+      uint32_t sbeg[kRangeCap / NT];
+#pragma unroll
+      for (int u = 0; u < kRangeCap / NT; ++u) {
+        const uint32_t j = threadIdx.x + u * NT;
+        sbeg[u] = 0;
+        if (j < c) sbeg[u] = s_sc[sub[u]];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < kRangeCap / NT; ++u) {
+        const uint32_t j = threadIdx.x + u * NT;
+        if (j < c) s_ord[atomicAdd(&s_sc[sub[u]], 1u)] = (uint16_t)j;
+      }
+      __syncthreads();
+      // after the cursors ran, s_sc[l] is the end of sub-range l
+      uint32_t rk[kRangeCap / NT];
+#pragma unroll
+      for (int u = 0; u < kRangeCap / NT; ++u) {
+        const uint32_t j = threadIdx.x + u * NT;
+        rk[u] = 0;
+        if (j < c) {
+          const uint64_t key = s_key[j];
+          const uint32_t b0 = sbeg[u], e0 = s_sc[sub[u]];
+          uint32_t r = b0, i = b0;
+          for (; i + 4 <= e0; i += 4) {
+            const uint32_t o0 = s_ord[i], o1 = s_ord[i + 1], o2 = s_ord[i + 2], o3 = s_ord[i + 3];
+            r += (s_key[o0] < key ? 1u : 0u) + (s_key[o1] < key ? 1u : 0u) + (s_key[o2] < key ? 1u : 0u) +
+                 (s_key[o3] < key ? 1u : 0u);
+          }
+          for (; i < e0; ++i) r += s_key[s_ord[i]] < key ? 1u : 0u;
+          rk[u] = r;
+          const uint32_t slot = s_sr[j];
+          idx[slot / kSlots].row[slot % kSlots] = (uint32_t)(base + r);
+          state[base + r] = 0.0f;
+        }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < kRangeCap / NT; ++u) {
+        const uint32_t j = threadIdx.x + u * NT;
+        if (j < c) s_sr[j] = rk[u];
+      }
+      __syncthreads();
+      write_init_rows<NT>(s_key, s_sr, s_pos, c, base, rows, D, seed, out);
+    } else {
+      // more keys in the range than LDS holds: gather them in global scratch
+      // at [below, below + c), which no other block's range overlaps, then
+      // rank them in chunks streamed through LDS
+      __syncthreads();
+      if (threadIdx.x == 0) s_nc = 0;
+      __syncthreads();
+      scan_new_keys<NT>(newlist, tile_cnt, ntiles, tile_size, s_pref, s_w, [&](uint64_t key, const NewKey* ent) {
+        if (key >= lo && key < hi) {
+          const uint32_t at = atomicAdd(&s_nc, 1u);
+          xkey[below + at] = key;
+          xslot[below + at] = ent->slot;
+        }
+      });
+      __syncthreads();
+      const uint64_t* rk_key = xkey + below;
+      const uint32_t* rk_slot = xslot + below;
+      uint64_t* s_cmp = s_buf;                                                    // [kChunk]
+      uint64_t* s_mk = s_buf + kChunk;                                            // [kAssignMine]
+      uint32_t* s_ms = reinterpret_cast<uint32_t*>(s_buf + kChunk + kAssignMine);  // [kAssignMine]
+      uint32_t* s_mr = s_ms + kAssignMine;                                        // [kAssignMine]
+      constexpr int PER = kAssignMine / NT;
+      for (uint32_t j0 = 0; j0 < c; j0 += kAssignMine) {
+        const uint32_t m = min((uint32_t)kAssignMine, c - j0);
+        uint64_t mk[PER];
+        uint32_t r[PER];
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+          const uint32_t j = threadIdx.x + u * NT;
+          mk[u] = j < m ? rk_key[j0 + j] : 0ull;
+          r[u] = 0;
+        }
+        for (uint32_t e0 = 0; e0 < c; e0 += kChunk) {
+          const uint32_t cnt = min((uint32_t)kChunk, c - e0);
+          for (uint32_t e = threadIdx.x; e < cnt; e += NT) s_cmp[e] = rk_key[e0 + e];
+          __syncthreads();
+          for (uint32_t e = 0; e < cnt; ++e) {
+            const uint64_t v = s_cmp[e];
+#pragma unroll
+            for (int u = 0; u < PER; ++u) r[u] += v < mk[u] ? 1u : 0u;
+          }
+          __syncthreads();
+        }
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+          const uint32_t j = threadIdx.x + u * NT;
+          if (j < m) {
+            s_mk[j] = mk[u];
+            s_ms[j] = rk_slot[j0 + j];
+            s_mr[j] = r[u];
+          }
+        }
+        __syncthreads();
+        write_new_rows<NT>(s_mk, s_ms, s_mr, m, base, idx, rows, state, D, seed);
+        __syncthreads();
+      }
+    }
+    return;
+  }
+
+  // ---- few new keys: this block owns the tiles t = blockIdx.x (mod
+  // gridDim.x); it takes them kAssignBatch at a time (thread j holds entry j
+  // of each tile) and ranks their keys against all M new keys of the call.
+  uint64_t* s_chunk = s_buf;                                              // [kChunk]
+  uint64_t* s_key = s_buf + kChunk;                                       // [kAssignMine]
+  uint32_t* s_slot = reinterpret_cast<uint32_t*>(s_key + kAssignMine);    // [kAssignMine]
+  uint32_t* s_rank = s_slot + kAssignMine;                                // [kAssignMine]
   static_assert(kGetTile == NT, "one thread per entry of a probe tile");
   for (int tb = blockIdx.x; tb < ntiles; tb += gridDim.x * kAssignBatch) {
     uint32_t have = 0;
@@ -297,18 +649,16 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
       idx[slot / kSlots].row[slot % kSlots] = row;
       state[row] = 0.0f;
     }
-    // initial rows, written cooperatively (coalesced along each row)
+    // initial rows, a wave per row
     for (int b = 0; b < kAssignBatch; ++b) {
       const int t = tb + b * (int)gridDim.x;
       const uint32_t c = t < ntiles ? tile_cnt[t] : 0u;
-      const uint64_t total = (uint64_t)c * (uint64_t)D;
-      for (uint64_t e = threadIdx.x; e < total; e += NT) {
-        const uint32_t j = (uint32_t)(e / (uint64_t)D);
-        const int col = (int)(e - (uint64_t)j * D);
-        const int m = b * NT + (int)j;
-        const uint64_t row = size0 + s_rank[m];
-        rows[row * (uint64_t)D + col] = init_elem(splitmix_mix(s_key[m] ^ seed), col);
-      }
+      const NewKey* tl = newlist + (size_t)(t < ntiles ? t : 0) * tile_size;
+      struct {
+        const NewKey* e;
+        __device__ uint32_t operator[](uint32_t j) const { return e[j].pad; }
+      } pos{tl};
+      write_init_rows<NT>(s_key + b * NT, s_rank + b * NT, pos, c, size0, rows, D, seed, out);
     }
     __syncthreads();
   }
@@ -1851,7 +2201,7 @@ static hipError_t launch_get_t(const GetArgs& a, hipStream_t st, const LaunchHoo
   hook(K_ASSIGN_NEW, 0, st);
   hipLaunchKernelGGL(k_assign_new, dim3(grid), dim3(kAssignThreads), 0, st, a.idx, a.newlist,
                      a.tile_cnt, (int)ntiles, kGetTile, a.rows, a.state, a.D, a.seed, a.capacity,
-                     a.ctrl, a.epoch);
+                     a.ctrl, a.epoch, a.xkey, a.xslot, a.out);
   hook(K_ASSIGN_NEW, 1, st);
   return hipGetLastError();
 }

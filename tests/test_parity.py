@@ -106,6 +106,65 @@ def test_put_inserts_unseen_keys_then_updates_them():
     pr.close()
 
 
+@pytest.mark.parametrize("case", ["random", "descending", "second_half_new", "clustered", "one_feature"])
+def test_many_new_keys_get_rows_in_key_order(case):
+    """A call inserting many more new keys than one block ranks against all
+    others (key ranges split among the blocks): rows follow the ascending
+    order of the call's new keys, whatever their batch order or spread."""
+    rng = np.random.default_rng(21)
+    dim, n = 5, 120_000
+    pr = Pair(dim, 400_000)
+    keys = rng.choice(np.uint64(1) << np.uint64(62), size=n, replace=False).astype(np.uint64)
+    if case == "descending":
+        keys = np.sort(keys)[::-1].copy()
+    elif case == "second_half_new":  # the first half of the batch are hits
+        pr.get(np.sort(keys[: n // 2]))
+    elif case == "clustered":  # a dense run of small keys and a few huge ones
+        keys = np.concatenate([np.arange(1, n - 100, dtype=np.uint64) * np.uint64(3),
+                               (np.uint64(1) << np.uint64(63)) + np.arange(100, dtype=np.uint64)])
+        keys = keys[rng.permutation(keys.size)]
+    elif case == "one_feature":  # feature << 40 | id, ids dense and small, repeated positions
+        ids = rng.integers(0, 90_000, size=n).astype(np.uint64)
+        keys = (np.uint64(7) << np.uint64(40)) | ids
+    pr.get(keys)
+    log(f"[parity] many new keys ({case}): size={pr.gpu.size}")
+    pr.compare_rows()
+    pr.check_index()
+    pr.close()
+
+
+def test_millions_of_new_keys_in_one_get():
+    """Key ranges holding more keys than LDS: gathered in global scratch."""
+    rng = np.random.default_rng(22)
+    n = 2_600_000
+    pr = Pair(2, n + 10)
+    keys = rng.choice(np.uint64(1) << np.uint64(40), size=n, replace=False).astype(np.uint64)
+    k = dev_keys(keys)
+    pr.gpu.get(k, None)
+    rc, _ = pr.ora.get(keys)
+    assert rc == 0 and pr.gpu.sync() == mlkv.MLKV_OK
+    got = pr.gpu.lookup_rows(k).cpu().numpy()
+    assert np.array_equal(got, np.argsort(np.argsort(keys)))
+    pr.compare_rows(np.arange(0, n, 997, dtype=np.int64))
+    pr.close()
+
+
+def test_many_new_keys_over_capacity_roll_back():
+    dim = 3
+    pr = Pair(dim, 30_000)
+    pr.get(np.arange(1000, dtype=np.uint64))
+    k = dev_keys(np.arange(10_000, 50_000, dtype=np.uint64))
+    pr.gpu.get(k, None)
+    assert pr.gpu.sync() == mlkv.MLKV_EFULL
+    assert pr.gpu.size == 1000
+    pr.check_index()
+    pr.get(np.arange(10_000, 35_000, dtype=np.uint64))  # 25,000 new keys fit
+    assert pr.gpu.size == 26_000
+    pr.compare_rows()
+    pr.check_index()
+    pr.close()
+
+
 def test_empty_call_is_a_no_op():
     pr = Pair(8, 10)
     k = torch.empty(0, dtype=torch.int64, device="cuda")
