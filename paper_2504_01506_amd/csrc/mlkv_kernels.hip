@@ -1372,6 +1372,12 @@ __device__ __forceinline__ void update_segments(IP it, SP seg, uint32_t S, const
   }
 }
 
+// Segments longer than kLongSeg items are put in tile order through a bitmask
+// of their tiles (a key has at most one item per tile) when there are at most
+// 256 tiles; at most kLongMax of them fit a partition.
+constexpr int kLongSeg = 32;
+constexpr int kLongMax = kRedCap / (kLongSeg + 1) + 1;
+
 // Dynamic LDS of a reduce_update block, in bytes. The first region holds the
 // gathered items and the grouping tables; once items are grouped it is reused
 // for a chunk of new keys and then for the pieces of cut segments.
@@ -1389,7 +1395,11 @@ struct RedLds {
   static constexpr size_t w = (pref + 4 * ((size_t)NT + 1) + 15) & ~(size_t)15;          // u32[NT / 64]
   static constexpr size_t w64 = (w + 4 * (size_t)(NT / 64) + 15) & ~(size_t)15;          // u64[NT / 64]
   static constexpr size_t base = w64 + 8 * (size_t)(NT / 64);                            // u64
-  static constexpr size_t total = base + 16;
+  static constexpr size_t tl = base + 16;                                  // u8[kRedCap] source tile of each item
+  static constexpr size_t lid = (tl + (size_t)kRedCap + 15) & ~(size_t)15;  // u16[kRedHash] long-segment id per slot
+  static constexpr size_t mask = lid + 2 * (size_t)kRedHash;               // u32[kLongMax][8] tiles of each long segment
+  static constexpr size_t nlong = mask + 4 * 8 * (size_t)kLongMax;          // u32
+  static constexpr size_t total = nlong + 16;
 };
 
 // Threads of a reduce_update block: 1024 (one block per CU) unless the
@@ -1437,15 +1447,22 @@ template <int NT>
 __device__ __forceinline__ uint32_t group_items(const uint64_t* it, uint32_t mp, uint64_t* sorted,
                                                uint16_t* sid, uint32_t* seg, uint32_t* hidx,
                                                uint32_t* hcnt, uint16_t* inv, uint16_t* pl, uint32_t* s_w,
-                                               uint32_t* n_sum, bool* any_fresh) {
+                                               uint32_t* n_sum, bool* any_fresh, const uint8_t* tl,
+                                               uint16_t* lid, uint32_t* mask, uint32_t* s_nlong) {
   constexpr int IPT = (kRedCap + NT - 1) / NT;
   constexpr int HPT = kRedHash / NT;
   constexpr uint32_t kNone = 0xFFFFFFFFu;
   constexpr uint32_t kMask = kRedHash - 1;
   const int tid = threadIdx.x;
+  const bool masks = tl != nullptr;  // items carry their tile (at most 256 tiles)
   for (int h = tid; h < kRedHash; h += NT) {
     hidx[h] = kNone;
     hcnt[h] = 0u;
+  }
+  if (masks) {
+    for (int h = tid; h < kRedHash; h += NT) lid[h] = 0xFFFFu;
+    for (int w = tid; w < 8 * kLongMax; w += NT) mask[w] = 0u;
+    if (tid == 0) *s_nlong = 0u;
   }
   lds_barrier();
 
@@ -1518,6 +1535,7 @@ __device__ __forceinline__ uint32_t group_items(const uint64_t* it, uint32_t mp,
       const uint32_t u = need[q] ? u_need++ : u_one++;
       seg[u] = cnt[q];
       hcnt[hh[q]] = u;
+      if (masks && cnt[q] > (uint32_t)kLongSeg) lid[hh[q]] = (uint16_t)atomicAdd(s_nlong, 1u);  // any id will do
     }
   }
   *n_sum = NS;
@@ -1556,6 +1574,10 @@ __device__ __forceinline__ uint32_t group_items(const uint64_t* it, uint32_t mp,
     if (j < mp) {
       rs[k] = hcnt[hs[k]];
       pl[seg[rs[k]] + atomicAdd(&hidx[rs[k]], 1u)] = (uint16_t)j;
+      if (masks) {
+        const uint32_t l = lid[hs[k]];
+        if (l != 0xFFFFu) atomicOr(&mask[l * 8 + (tl[j] >> 5)], 1u << (tl[j] & 31));
+      }
     }
   }
   lds_barrier();
@@ -1566,7 +1588,19 @@ __device__ __forceinline__ uint32_t group_items(const uint64_t* it, uint32_t mp,
     const uint32_t j = tid + k * NT;
     if (j < mp) {
       const uint32_t b = seg[rs[k]], e = seg[rs[k] + 1];
-      const uint32_t rank = e - b > 1 ? count_below(pl, b, e, j) : 0u;
+      uint32_t rank = 0;
+      const uint32_t l = masks ? lid[hs[k]] : 0xFFFFu;
+      if (l != 0xFFFFu) {  // the segment's items in earlier tiles
+        const uint32_t t = tl[j], w = t >> 5;
+        const uint4 m0 = reinterpret_cast<const uint4*>(mask + l * 8)[0];
+        const uint4 m1 = reinterpret_cast<const uint4*>(mask + l * 8)[1];
+        const uint32_t mw[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
+#pragma unroll
+        for (uint32_t x = 0; x < 8; ++x)
+          rank += x < w ? __popc(mw[x]) : x == w ? __popc(mw[x] & ((1u << (t & 31)) - 1u)) : 0u;
+      } else if (e - b > 1) {
+        rank = count_below(pl, b, e, j);
+      }
       sorted[b + rank] = it[j];
       sid[b + rank] = (uint16_t)rs[k];
     }
@@ -1653,6 +1687,10 @@ __global__ __launch_bounds__(NT) void k_put_group(
   uint32_t* s_w = reinterpret_cast<uint32_t*>(s_raw + L::w);
   unsigned long long* s_w64 = reinterpret_cast<unsigned long long*>(s_raw + L::w64);
   uint64_t* s_base = reinterpret_cast<uint64_t*>(s_raw + L::base);
+  uint8_t* s_tl = s_raw + L::tl;
+  uint16_t* s_lid = reinterpret_cast<uint16_t*>(s_raw + L::lid);
+  uint32_t* s_mask = reinterpret_cast<uint32_t*>(s_raw + L::mask);
+  uint32_t* s_nlong = reinterpret_cast<uint32_t*>(s_raw + L::nlong);
 
   const uint32_t p = blockIdx.x;
   const int tid = threadIdx.x;
@@ -1713,10 +1751,12 @@ __global__ __launch_bounds__(NT) void k_put_group(
       s_pref[tid] = pre | (mt << 16);  // items before this tile | offset in the tile
       __syncthreads();
       uint64_t v[IPT];
+      uint32_t src[IPT];
 #pragma unroll
       for (int e = 0; e < IPT; ++e) {
         const uint32_t k = tid + e * NT;
         v[e] = 0;
+        src[e] = 0;
         if (k < tot) {
           int lo = 0, hi = nt - 1;
           while (lo < hi) {
@@ -1725,13 +1765,17 @@ __global__ __launch_bounds__(NT) void k_put_group(
             else hi = mid - 1;
           }
           const uint32_t pe = s_pref[lo];
+          src[e] = (uint32_t)(t0 + lo);
           v[e] = items[(size_t)(t0 + lo) * kPutTile + (pe >> 16) + (k - (pe & 0xFFFFu))];
         }
       }
 #pragma unroll
       for (int e = 0; e < IPT; ++e) {
         const uint32_t k = tid + e * NT;
-        if (k < tot) s_it[dst + k] = v[e];
+        if (k < tot) {
+          s_it[dst + k] = v[e];
+          s_tl[dst + k] = (uint8_t)src[e];
+        }
       }
       dst += tot;
       __syncthreads();
@@ -1740,8 +1784,8 @@ __global__ __launch_bounds__(NT) void k_put_group(
 
   uint32_t n_sum;
   bool any_fresh;
-  const uint32_t S =
-      group_items<NT>(s_it, mp, s_sorted, s_sid, s_seg, s_hidx, s_hcnt, s_inv, s_pl, s_w, &n_sum, &any_fresh);
+  const uint32_t S = group_items<NT>(s_it, mp, s_sorted, s_sid, s_seg, s_hidx, s_hcnt, s_inv, s_pl, s_w, &n_sum,
+                                    &any_fresh, ntiles <= 256 ? s_tl : nullptr, s_lid, s_mask, s_nlong);
   if (any_fresh)
     resolve_new_rows<NT>(s_sorted, s_seg, S, c, newlist, tile_cnt, ntiles, s_pref, s_w, s_w64, s_chunk);
 
