@@ -1915,13 +1915,15 @@ __global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ g
   const int gid = (threadIdx.x >> 6) * RPW + g;
   const uint32_t nb = gridDim.x, b = blockIdx.x;
 
-  // the block's phase-A range, both ends moved to segment starts
+  // the block's phase-A range: an even share, both ends moved to the nearer
+  // boundary of the segment they fall in
   if (threadIdx.x < 2) {
     uint32_t t = (uint32_t)((uint64_t)(b + threadIdx.x) * NA / nb);
     if (t < NA) {
       const int p0 = partition_of(s_pa, np, t);
       const uint32_t d0 = gdesc[(size_t)p0 * kRedCap + (t - s_pa[p0])];
-      if (s_pa[p0] + (d0 & 0xFFFFu) != t) t = s_pa[p0] + (d0 >> 16);
+      const uint32_t f0 = s_pa[p0] + (d0 & 0xFFFFu), e0 = s_pa[p0] + (d0 >> 16);
+      if (f0 != t) t = (t - f0 <= e0 - t) ? f0 : e0;  // the nearer end of the segment holding t
     }
     s_rng[threadIdx.x] = t;
   }
