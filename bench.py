@@ -7,6 +7,10 @@ the DLRM-shaped workload (26 features, 10M rows of dim 64 prefilled,
 row-wise Adagrad lr 0.01 eps 1e-8). All inputs are generated on the host
 from fixed seeds and copied to HBM before the timed region.
 
+With --config kv-uniform or kv-zipf a step is instead the paper's key-value
+mix: gets of half a batch of 2^20 record keys, then puts (upserts of new
+16-byte values) of the other half, over 10M prefilled records.
+
 Prints one JSON line. `value` is get+put keys per second; the line also
 carries effective HBM GB/s from algorithmic bytes, the roofline of the
 dominant kernel (per-launch durations from HIP events recorded by the
@@ -28,6 +32,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0
 METRIC = "embedding get+put keys/sec and achieved HBM GB/s (% of peak), 1 MI355X"
+METRIC_KV = "key-value operations/sec, 50% get / 50% put, 1 MI355X"
 KERNELS = ("get_probe_gather", "assign_new", "put_probe", "put_group", "put_apply")
 
 
@@ -47,6 +52,20 @@ def kernel_bytes(n, U, M, D):
         # gradient rows in, distinct rows read and written, accumulators read
         # and written
         "put_apply": 4 * D * n + 8 * D * U + 8 * U,
+    }
+
+
+def kernel_bytes_kv(nr, Ur, nw, Uw, D):
+    """The same for one step of the key-value mix: nr gets over Ur distinct
+    existing keys, then a put of nw values over Uw distinct existing keys
+    (the last value of each key is written)."""
+    return {
+        "get_probe_gather": 8 * nr + 12 * Ur + 4 * D * Ur + 4 * D * nr,
+        "assign_new": 0,
+        "put_probe": 8 * nw + 12 * Uw,
+        "put_group": 0,
+        # the winning value of each key in, its row written
+        "put_apply": 8 * D * Uw,
     }
 
 
@@ -71,7 +90,7 @@ def load_traffic(kernel, digest):
     return t.get("kernels", {}).get(kernel, {}).get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(wl, seconds):
+def cpu_baseline(wl, seconds, kv=False):
     from oracle import oracle as O
 
     t = O.OracleTable(wl.dim, wl.capacity)
@@ -80,16 +99,25 @@ def cpu_baseline(wl, seconds):
         assert t.prefill_sorted(pre) == O.OK
     steps, elapsed = 0, 0.0
     while steps == 0 or elapsed < seconds:
-        keys, grads = wl.keys(steps), wl.grads(steps)
-        t0 = time.perf_counter()
-        rc, _ = t.get(keys)
-        rc2 = t.put_grad(keys, grads, wl.lr, wl.eps)
+        keys = wl.keys(steps)
+        if kv:
+            h = wl.n // 2
+            vals = wl.values(steps)
+            t0 = time.perf_counter()
+            rc, _ = t.get(keys[:h])
+            rc2 = t.put(keys[h:], vals)
+        else:
+            grads = wl.grads(steps)
+            t0 = time.perf_counter()
+            rc, _ = t.get(keys)
+            rc2 = t.put_grad(keys, grads, wl.lr, wl.eps)
         elapsed += time.perf_counter() - t0
         assert rc == O.OK and rc2 == O.OK
         steps += 1
     t.close()
-    return {"value": wl.n * steps / elapsed, "unit": "keys/s", "cores": 1, "kind": "oracle",
-            "sample": f"first {steps} steps of the same workload ({wl.n} lookups each) after the "
+    unit = "ops/s" if kv else "keys/s"
+    return {"value": wl.n * steps / elapsed, "unit": unit, "cores": 1, "kind": "oracle",
+            "sample": f"first {steps} steps of the same workload ({wl.n} keys each) after the "
                       f"same prefill, single-threaded C++ oracle, {elapsed:.1f} s",
             "host_cpus": os.cpu_count(), "host_affinity": len(os.sched_getaffinity(0))}
 
@@ -99,7 +127,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", default="dlrm", choices=["tiny", "dlrm", "kg", "gnn", "large"])
+    ap.add_argument("--config", default="dlrm",
+                    choices=["tiny", "dlrm", "kg", "gnn", "large", "kv-uniform", "kv-zipf"])
     ap.add_argument("--scale", type=float, default=1.0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -121,6 +150,8 @@ def main():
     mlkv.load()
     wl = W.make(args.config, scale=args.scale)
     D, n = wl.dim, wl.n
+    kv = args.config.startswith("kv-")  # half gets, half puts of values
+    h = n // 2
     total_steps = args.warmup + 2 * args.steps
 
     # ---- inputs (host, seeded) -> HBM ------------------------------------
@@ -130,6 +161,11 @@ def main():
     keys_h, grads_d, keys_d, UM = [], [], [], []
     for s in range(total_steps):
         k = wl.keys(s)
+        keys_d.append(torch.from_numpy(k.view(np.int64)).cuda())
+        if kv:  # every key is a prefilled record
+            UM.append((np.unique(k[:h]).size, np.unique(k[h:]).size))
+            grads_d.append(torch.from_numpy(wl.values(s)).cuda())
+            continue
         u = np.unique(k)
         if known.size:
             pos = np.minimum(np.searchsorted(known, u), known.size - 1)
@@ -139,7 +175,6 @@ def main():
         if new.size:
             known = np.union1d(known, new)
         UM.append((u.size, new.size))
-        keys_d.append(torch.from_numpy(k.view(np.int64)).cuda())
         grads_d.append(torch.from_numpy(wl.grads(s)).cuda())
     out = torch.empty((n, D), dtype=torch.float32, device="cuda")
     log(f"inputs ready in {time.perf_counter() - t0:.1f}s: {total_steps} batches of {n} keys")
@@ -153,8 +188,12 @@ def main():
     log(f"prefill {pre.size} keys in {time.perf_counter() - t0:.2f}s, size={t.size}")
 
     def step(s):
-        t.get(keys_d[s], out)
-        t.put_grad(keys_d[s], grads_d[s], wl.lr, wl.eps)
+        if kv:
+            t.get(keys_d[s][:h], out[:h])
+            t.put(keys_d[s][h:], grads_d[s])
+        else:
+            t.get(keys_d[s], out)
+            t.put_grad(keys_d[s], grads_d[s], wl.lr, wl.eps)
 
     for s in range(args.warmup):
         step(s)
@@ -176,7 +215,10 @@ def main():
     assert t.sync() == mlkv.MLKV_OK
     ms_step = ms / args.steps
     keys_per_s = n * args.steps / (ms * 1e-3)
-    bytes_steps = [kernel_bytes(n, U, M, D) for (U, M) in UM]
+    if kv:
+        bytes_steps = [kernel_bytes_kv(h, Ur, n - h, Uw, D) for (Ur, Uw) in UM]
+    else:
+        bytes_steps = [kernel_bytes(n, U, M, D) for (U, M) in UM]
     alg_bytes = sum(sum(b.values()) for b in bytes_steps[first:first + args.steps])
     gbps = alg_bytes / (ms * 1e-3) / 1e9
     log(f"timed {args.steps} steps: {ms_step * 1e3:.2f} us/step (wall {wall * 1e3 / args.steps:.2f}), "
@@ -207,7 +249,8 @@ def main():
                         "gbps": round(b / cnt / (avg_us * 1e-6) / 1e9, 1)}
     dom = max(kinfo, key=lambda k: kinfo[k]["avg_us"] * kinfo[k]["launches"])
     digest = source_digest()
-    traffic = load_traffic(dom, digest)
+    # the committed counters were taken on the full-size DLRM-shaped workload
+    traffic = load_traffic(dom, digest) if args.config == "dlrm" and args.scale == 1.0 else None
     roof = {"kernel": dom, "bound": "hbm", "achieved": kinfo[dom]["gbps"], "peak": PEAK_HBM_GBPS,
             "unit": "GB/s", "frac": round(kinfo[dom]["gbps"] / PEAK_HBM_GBPS, 4), "traffic": traffic,
             "alg_bytes_per_launch": kinfo[dom]["alg_bytes_per_launch"],
@@ -229,14 +272,20 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline: oracle on the host")
-        cpu = cpu_baseline(wl, args.cpu_seconds)
-        log(f"cpu baseline: {cpu['value'] / 1e6:.3f} M keys/s")
+        cpu = cpu_baseline(wl, args.cpu_seconds, kv)
+        log(f"cpu baseline: {cpu['value'] / 1e6:.3f} M {cpu['unit']}")
 
-    U_avg = float(np.mean([u for u, _ in UM[first:first + args.steps]]))
+    U_avg = float(np.mean([a + b if kv else a for a, b in UM[first:first + args.steps]]))
+    if kv:
+        workload = (f"{wl.name} key-value mix: {wl.capacity} records of dim {D} fp32 (16-byte values), "
+                    f"{h} gets then {n - h} puts per step")
+    else:
+        workload = (f"{wl.name}-shaped embedding table: {wl.capacity} rows x dim {D} fp32, "
+                    f"{n} lookups per step (get + row-wise Adagrad put_grad)")
     res = {
-        "metric": METRIC,
+        "metric": METRIC_KV if kv else METRIC,
         "value": keys_per_s,
-        "unit": "keys/s",
+        "unit": "ops/s" if kv else "keys/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -247,8 +296,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": f"{wl.name}-shaped embedding table: {wl.capacity} rows x dim {D} fp32, "
-                        f"{n} lookups per step (get + row-wise Adagrad put_grad)",
+            "workload": workload,
             "rows": wl.capacity, "dim": D, "lookups_per_step": n, "prefill": int(pre.size),
             "unique_keys_per_step": round(U_avg, 1), "scale": args.scale,
         },

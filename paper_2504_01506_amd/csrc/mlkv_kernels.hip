@@ -1374,9 +1374,11 @@ __device__ __forceinline__ void update_segments(IP it, SP seg, uint32_t S, const
 
 // Segments longer than kLongSeg items are put in tile order through a bitmask
 // of their tiles (a key has at most one item per tile) when there are at most
-// 256 tiles; at most kLongMax of them fit a partition.
+// kMaskTiles tiles; at most kLongMax of them fit a partition.
 constexpr int kLongSeg = 32;
 constexpr int kLongMax = kRedCap / (kLongSeg + 1) + 1;
+constexpr int kMaskTiles = 1024;
+constexpr int kMaskWords = kMaskTiles / 32;
 
 // Dynamic LDS of a reduce_update block, in bytes. The first region holds the
 // gathered items and the grouping tables; once items are grouped it is reused
@@ -1395,10 +1397,10 @@ struct RedLds {
   static constexpr size_t w = (pref + 4 * ((size_t)NT + 1) + 15) & ~(size_t)15;          // u32[NT / 64]
   static constexpr size_t w64 = (w + 4 * (size_t)(NT / 64) + 15) & ~(size_t)15;          // u64[NT / 64]
   static constexpr size_t base = w64 + 8 * (size_t)(NT / 64);                            // u64
-  static constexpr size_t tl = base + 16;                                  // u8[kRedCap] source tile of each item
-  static constexpr size_t lid = (tl + (size_t)kRedCap + 15) & ~(size_t)15;  // u16[kRedHash] long-segment id per slot
-  static constexpr size_t mask = lid + 2 * (size_t)kRedHash;               // u32[kLongMax][8] tiles of each long segment
-  static constexpr size_t nlong = mask + 4 * 8 * (size_t)kLongMax;          // u32
+  static constexpr size_t tl = base + 16;                                      // u16[kRedCap] source tile of each item
+  static constexpr size_t lid = (tl + 2 * (size_t)kRedCap + 15) & ~(size_t)15;  // u16[kRedHash] long-segment id per slot
+  static constexpr size_t mask = lid + 2 * (size_t)kRedHash;  // u32[kLongMax][kMaskWords] tiles of each long segment
+  static constexpr size_t nlong = mask + 4 * (size_t)kMaskWords * (size_t)kLongMax;  // u32
   static constexpr size_t total = nlong + 16;
 };
 
@@ -1447,21 +1449,21 @@ template <int NT>
 __device__ __forceinline__ uint32_t group_items(const uint64_t* it, uint32_t mp, uint64_t* sorted,
                                                uint16_t* sid, uint32_t* seg, uint32_t* hidx,
                                                uint32_t* hcnt, uint16_t* inv, uint16_t* pl, uint32_t* s_w,
-                                               uint32_t* n_sum, bool* any_fresh, const uint8_t* tl,
+                                               uint32_t* n_sum, bool* any_fresh, const uint16_t* tl,
                                                uint16_t* lid, uint32_t* mask, uint32_t* s_nlong) {
   constexpr int IPT = (kRedCap + NT - 1) / NT;
   constexpr int HPT = kRedHash / NT;
   constexpr uint32_t kNone = 0xFFFFFFFFu;
   constexpr uint32_t kMask = kRedHash - 1;
   const int tid = threadIdx.x;
-  const bool masks = tl != nullptr;  // items carry their tile (at most 256 tiles)
+  const bool masks = tl != nullptr;  // items carry their tile (at most kMaskTiles tiles)
   for (int h = tid; h < kRedHash; h += NT) {
     hidx[h] = kNone;
     hcnt[h] = 0u;
   }
   if (masks) {
     for (int h = tid; h < kRedHash; h += NT) lid[h] = 0xFFFFu;
-    for (int w = tid; w < 8 * kLongMax; w += NT) mask[w] = 0u;
+    for (int w = tid; w < kMaskWords * kLongMax; w += NT) mask[w] = 0u;
     if (tid == 0) *s_nlong = 0u;
   }
   lds_barrier();
@@ -1576,7 +1578,7 @@ __device__ __forceinline__ uint32_t group_items(const uint64_t* it, uint32_t mp,
       pl[seg[rs[k]] + atomicAdd(&hidx[rs[k]], 1u)] = (uint16_t)j;
       if (masks) {
         const uint32_t l = lid[hs[k]];
-        if (l != 0xFFFFu) atomicOr(&mask[l * 8 + (tl[j] >> 5)], 1u << (tl[j] & 31));
+        if (l != 0xFFFFu) atomicOr(&mask[l * kMaskWords + (tl[j] >> 5)], 1u << (tl[j] & 31));
       }
     }
   }
@@ -1592,12 +1594,16 @@ __device__ __forceinline__ uint32_t group_items(const uint64_t* it, uint32_t mp,
       const uint32_t l = masks ? lid[hs[k]] : 0xFFFFu;
       if (l != 0xFFFFu) {  // the segment's items in earlier tiles
         const uint32_t t = tl[j], w = t >> 5;
-        const uint4 m0 = reinterpret_cast<const uint4*>(mask + l * 8)[0];
-        const uint4 m1 = reinterpret_cast<const uint4*>(mask + l * 8)[1];
-        const uint32_t mw[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
+        const uint4* m4 = reinterpret_cast<const uint4*>(mask + l * kMaskWords);
+        for (uint32_t x4 = 0; x4 <= (w >> 2); ++x4) {
+          const uint4 m = m4[x4];
+          const uint32_t mw[4] = {m.x, m.y, m.z, m.w};
 #pragma unroll
-        for (uint32_t x = 0; x < 8; ++x)
-          rank += x < w ? __popc(mw[x]) : x == w ? __popc(mw[x] & ((1u << (t & 31)) - 1u)) : 0u;
+          for (uint32_t y = 0; y < 4; ++y) {
+            const uint32_t x = x4 * 4 + y;
+            rank += x < w ? __popc(mw[y]) : x == w ? __popc(mw[y] & ((1u << (t & 31)) - 1u)) : 0u;
+          }
+        }
       } else if (e - b > 1) {
         rank = count_below(pl, b, e, j);
       }
@@ -1687,7 +1693,7 @@ __global__ __launch_bounds__(NT) void k_put_group(
   uint32_t* s_w = reinterpret_cast<uint32_t*>(s_raw + L::w);
   unsigned long long* s_w64 = reinterpret_cast<unsigned long long*>(s_raw + L::w64);
   uint64_t* s_base = reinterpret_cast<uint64_t*>(s_raw + L::base);
-  uint8_t* s_tl = s_raw + L::tl;
+  uint16_t* s_tl = reinterpret_cast<uint16_t*>(s_raw + L::tl);
   uint16_t* s_lid = reinterpret_cast<uint16_t*>(s_raw + L::lid);
   uint32_t* s_mask = reinterpret_cast<uint32_t*>(s_raw + L::mask);
   uint32_t* s_nlong = reinterpret_cast<uint32_t*>(s_raw + L::nlong);
@@ -1774,7 +1780,7 @@ __global__ __launch_bounds__(NT) void k_put_group(
         const uint32_t k = tid + e * NT;
         if (k < tot) {
           s_it[dst + k] = v[e];
-          s_tl[dst + k] = (uint8_t)src[e];
+          s_tl[dst + k] = (uint16_t)src[e];
         }
       }
       dst += tot;
@@ -1785,7 +1791,7 @@ __global__ __launch_bounds__(NT) void k_put_group(
   uint32_t n_sum;
   bool any_fresh;
   const uint32_t S = group_items<NT>(s_it, mp, s_sorted, s_sid, s_seg, s_hidx, s_hcnt, s_inv, s_pl, s_w, &n_sum,
-                                    &any_fresh, ntiles <= 256 ? s_tl : nullptr, s_lid, s_mask, s_nlong);
+                                    &any_fresh, ntiles <= kMaskTiles ? s_tl : nullptr, s_lid, s_mask, s_nlong);
   if (any_fresh)
     resolve_new_rows<NT>(s_sorted, s_seg, S, c, newlist, tile_cnt, ntiles, s_pref, s_w, s_w64, s_chunk);
 

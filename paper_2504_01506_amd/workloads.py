@@ -19,6 +19,11 @@ shapes the paper lists and skew models of the same kind:
   degree (exponent 2.0, degree cap tuned so about 30% of lookups repeat).
 * ``large`` 200M-row capacity, dim 128, half filled, 1M keys per step drawn
   Zipf(0.99) over a 300M-id space so that about 15% of lookups miss.
+* ``kv-uniform`` / ``kv-zipf``  the key-value mix of the paper's NoSQL test
+  (Sec. IV: half reads, half writes, uniform or skewed access): 10M records
+  of 16-byte values (dim 4) prefilled; per step 2^20 operations, the first
+  half gets and the second half puts (upserts of existing records with new
+  values), record ids uniform or Zipf(0.99) (the usual YCSB skew constant).
 
 Gradients are N(0, 0.01) fp32; lr = 0.01 and eps = 1e-8 everywhere.
 Every draw comes from numpy's PCG64 seeded by a SeedSequence keyed on
@@ -33,8 +38,8 @@ import numpy as np
 
 BASE_SEED = 0x250401506
 EMPTY_KEY = np.uint64(0xFFFFFFFFFFFFFFFF)
-_CFG_INDEX = {"tiny": 0, "dlrm": 1, "kg": 2, "gnn": 3, "large": 4}
-_KIND = {"struct": 0, "keys": 1, "grads": 2, "prefill": 3}
+_CFG_INDEX = {"tiny": 0, "dlrm": 1, "kg": 2, "gnn": 3, "large": 4, "kv-uniform": 5, "kv-zipf": 6}
+_KIND = {"struct": 0, "keys": 1, "grads": 2, "prefill": 3, "values": 4}
 
 M64 = np.uint64(0xFFFFFFFFFFFFFFFF)
 
@@ -349,7 +354,58 @@ class Large(Workload):
         return apply_bijection(ranks - 1, self.bij, self.space)
 
 
-CONFIGS = {"tiny": Tiny, "dlrm": Dlrm, "kg": Kg, "gnn": Gnn, "large": Large}
+class KvMix(Workload):
+    """Half gets, half puts over prefilled records: keys(step)[:n // 2] are
+    read, keys(step)[n // 2:] are written with values(step)."""
+
+    ALPHA = 0.99
+
+    def __init__(self, skew: str, scale: float = 1.0, steps: int = 100):
+        name = f"kv-{skew}"
+        records = max(1000, int(round(10_000_000 * scale)))
+        n = max(2, int(round((1 << 20) * scale)) // 2 * 2)
+        super().__init__(name, dim=4, capacity=records, n=n, steps=steps, scale=scale)
+        rng = rng_for(name, "struct")
+        self.records = records
+        self.key_seed = np.uint64(int(rng.integers(0, 2**63)))
+        self.zipf = ZipfSampler(records, self.ALPHA) if skew == "zipf" else None
+        self.bij = affine_bijection(rng, records)
+        self.info = {"records": records, "skew": skew, "alpha": self.ALPHA if self.zipf else 0.0,
+                     "reads": n // 2, "writes": n - n // 2}
+
+    def id_to_key(self, ids: np.ndarray) -> np.ndarray:
+        k = _splitmix_finalize(ids.astype(np.uint64) ^ self.key_seed)
+        assert not np.any(k == EMPTY_KEY)
+        return k
+
+    def prefill_keys(self) -> np.ndarray:
+        return np.sort(self.id_to_key(np.arange(self.records, dtype=np.int64)))
+
+    def keys(self, step: int) -> np.ndarray:
+        rng = rng_for(self.name, "keys", step)
+        if self.zipf is None:
+            ids = rng.integers(0, self.records, size=self.n)
+        else:
+            ids = apply_bijection(self.zipf.sample(rng, self.n) - 1, self.bij, self.records)
+        return self.id_to_key(ids)
+
+    def values(self, step: int) -> np.ndarray:
+        rng = rng_for(self.name, "values", step)
+        return rng.standard_normal(size=(self.n - self.n // 2, self.dim), dtype=np.float32)
+
+
+class KvUniform(KvMix):
+    def __init__(self, scale: float = 1.0, steps: int = 100):
+        super().__init__("uniform", scale, steps)
+
+
+class KvZipf(KvMix):
+    def __init__(self, scale: float = 1.0, steps: int = 100):
+        super().__init__("zipf", scale, steps)
+
+
+CONFIGS = {"tiny": Tiny, "dlrm": Dlrm, "kg": Kg, "gnn": Gnn, "large": Large,
+           "kv-uniform": KvUniform, "kv-zipf": KvZipf}
 
 
 def make(name: str, scale: float = 1.0, steps: int | None = None) -> Workload:

@@ -165,6 +165,42 @@ def test_many_new_keys_over_capacity_roll_back():
     pr.close()
 
 
+@pytest.mark.parametrize("name", ["kv-uniform", "kv-zipf"])
+def test_key_value_mix(name):
+    """The 50/50 get/put mix: gets of half a batch, then puts of values for
+    the other half, over prefilled records."""
+    wl = W.make(name, scale=0.01)
+    pr = Pair(wl.dim, wl.capacity)
+    pr.prefill(wl.prefill_keys())
+    h = wl.n // 2
+    for s in range(3):
+        k = wl.keys(s)
+        pr.get(k[:h])
+        pr.upsert(k[h:], wl.values(s))
+    pr.compare_rows()
+    pr.check_index()
+    pr.close()
+
+
+def test_hot_keys_across_many_tiles():
+    """Keys present in hundreds of put tiles (more than 256 tiles, up to the
+    1024 a tile bitmask covers), whose items are put in tile order through
+    the mask, and some beyond that."""
+    rng = np.random.default_rng(41)
+    dim = 8
+    for n in (600_000, 1_300_000):
+        pr = Pair(dim, 200_000)
+        hot = rng.integers(1, 2**62, size=40, dtype=np.uint64)
+        cold = rng.integers(1, 2**62, size=100_000, dtype=np.uint64)
+        keys = np.where(rng.random(n) < 0.3, hot[rng.integers(0, hot.size, n)], cold[rng.integers(0, cold.size, n)])
+        g = rng.normal(0, 0.01, size=(n, dim)).astype(np.float32)
+        pr.put(keys, g, 0.05, 1e-8)
+        for ks in (hot, cold[:2000]):
+            r = pr.ora.lookup_rows(ks)
+            pr.compare_rows(np.unique(r[r >= 0]))
+        pr.close()
+
+
 def test_empty_call_is_a_no_op():
     pr = Pair(8, 10)
     k = torch.empty(0, dtype=torch.int64, device="cuda")

@@ -81,3 +81,20 @@ def test_gnn_full_size_duplicate_fraction_about_30_percent():
     k = g.keys(0)
     dup = 1.0 - np.unique(k).size / k.size
     assert 0.25 < dup < 0.35
+
+
+def test_kv_mix_shapes_and_skew():
+    for name in ("kv-uniform", "kv-zipf"):
+        wl = W.make(name, scale=0.01)
+        k = wl.keys(0)
+        v = wl.values(0)
+        pre = wl.prefill_keys()
+        assert k.dtype == np.uint64 and k.size == wl.n and wl.n % 2 == 0
+        assert v.shape == (wl.n // 2, wl.dim) and v.dtype == np.float32
+        assert pre.size == wl.capacity and np.all(np.diff(pre.astype(np.float64)) >= 0)
+        assert np.isin(k, pre).all()  # every operation hits a prefilled record
+        assert np.array_equal(k, wl.keys(0)) and not np.array_equal(k, wl.keys(1))
+    u = W.make("kv-uniform", scale=0.01).keys(0)
+    z = W.make("kv-zipf", scale=0.01).keys(0)
+    # the skewed mix repeats keys far more than the uniform one
+    assert np.unique(z).size < 0.7 * np.unique(u).size
