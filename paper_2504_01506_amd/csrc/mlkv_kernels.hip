@@ -1883,7 +1883,8 @@ struct ApplyLds {
   static constexpr int kList = ApplyCfg<M>::kItems + kRedCap + 64;
   static constexpr size_t part = 0;                                              // fp64 [NG][D]
   static constexpr size_t done = part + sizeof(double) * (size_t)NG * DMAX;       // uint2 [kList]
-  static constexpr size_t pre = done + sizeof(uint2) * (size_t)kList;             // u32 [2 * (np + 1)]
+  static constexpr size_t sgl = done + sizeof(uint2) * (size_t)kList;             // u64 [kItems] the block's singles
+  static constexpr size_t pre = sgl + sizeof(uint64_t) * (size_t)ApplyCfg<M>::kItems;  // u32 [2 * (np + 1)]
   static constexpr size_t bytes(int np) { return pre + sizeof(uint32_t) * 2 * ((size_t)np + 1); }
 };
 
@@ -1904,6 +1905,7 @@ __global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ g
   extern __shared__ __align__(16) unsigned char s_dyn[];
   double* s_part = reinterpret_cast<double*>(s_dyn + LA::part);
   uint2* s_done = reinterpret_cast<uint2*>(s_dyn + LA::done);
+  uint64_t* s_sgl = reinterpret_cast<uint64_t*>(s_dyn + LA::sgl);
   uint32_t* s_pa = reinterpret_cast<uint32_t*>(s_dyn + LA::pre);  // phase-A items before each partition
   uint32_t* s_p1 = s_pa + np + 1;                                  // keys seen once before each partition
   __shared__ uint32_t s_w[NT / 64];
@@ -1941,23 +1943,21 @@ __global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ g
   const uint32_t K0 = (uint32_t)((uint64_t)b * N1 / nb), K1 = (uint32_t)((uint64_t)(b + 1) * N1 / nb);
   const uint32_t k0 = K0 + (uint32_t)((uint64_t)(K1 - K0) * gid / NG);
   const uint32_t k1 = K0 + (uint32_t)((uint64_t)(K1 - K0) * (gid + 1) / NG);
-  // the first kPre items of this group's keys seen once are loaded now, to be
-  // used after phase A
-  constexpr int kPre = 2;
-  uint64_t xs[kPre];
-  {
-    int p1 = k0 < k1 ? partition_of(s_p1, np, k0) : 0;
+  // the items of the block's keys seen once, [K0, K1) (at most kItems), are
+  // loaded now, a few per thread, and kept in LDS for phase B
+  constexpr int SPT = (ApplyCfg<M>::kItems + NT - 1) / NT;
+  uint64_t xs[SPT];
 #pragma unroll
-    for (int u = 0; u < kPre; ++u) {
-      xs[u] = 0;
-      if (k0 + u < k1) {
-        while (s_p1[p1 + 1] <= k0 + u) ++p1;
-        const uint32_t first_single = s_pa[p1 + 1] - s_pa[p1];  // singles follow the phase-A items
-        xs[u] = gitems[(size_t)p1 * kRedCap + first_single + (k0 + u - s_p1[p1])];
-      }
+  for (int u = 0; u < SPT; ++u) {
+    const uint32_t k = K0 + threadIdx.x + u * NT;
+    xs[u] = 0;
+    if (k < K1) {
+      const int p1 = partition_of(s_p1, np, k);
+      const uint32_t first_single = s_pa[p1 + 1] - s_pa[p1];  // singles follow the phase-A items
+      xs[u] = gitems[(size_t)p1 * kRedCap + first_single + (k - s_p1[p1])];
     }
   }
-  lds_barrier();  // the prefetched items stay in flight
+  lds_barrier();  // the loaded items stay in flight
   const uint32_t lo = s_slo[gid], hi = s_slo[gid + 1];
 
   auto put_row = [&](double* dst, const double (&a)[K][VEC]) {
@@ -2121,6 +2121,11 @@ __global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ g
       Ops::store_g(acc, partials, s_hpos[hl], D, q);
       complete(cur_row, s_hpos[hl]);
     }
+#pragma unroll
+    for (int u = 0; u < SPT; ++u) {
+      const uint32_t k = K0 + threadIdx.x + u * NT;
+      if (k < K1) s_sgl[k - K0] = xs[u];
+    }
     __syncthreads();
   }
 
@@ -2155,7 +2160,6 @@ __global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ g
   {
     const uint32_t e0 = (uint32_t)((uint64_t)nd * gid / NG), e1 = (uint32_t)((uint64_t)nd * (gid + 1) / NG);
     const uint32_t nm = e1 - e0, nw = nm + (k1 - k0);
-    int p1 = k0 < k1 ? partition_of(s_p1, np, k0) : 0;
     for (uint32_t w0 = 0; w0 < nw; w0 += BB) {
       uint32_t row[BB];
       const float* src[BB];
@@ -2171,15 +2175,7 @@ __global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ g
           row[u] = dv.x;
           src[u] = reinterpret_cast<const float*>(partials + (size_t)dv.y * (size_t)D);
         } else if (w < nw) {
-          const uint32_t sgl = w - nm;
-          uint64_t x = 0;
-#pragma unroll
-          for (int t = 0; t < kPre; ++t)
-            if (sgl == (uint32_t)t) x = xs[t];
-          if (sgl >= (uint32_t)kPre) {
-            while (s_p1[p1 + 1] <= k0 + sgl) ++p1;
-            x = gitems[(size_t)p1 * kRedCap + (s_pa[p1 + 1] - s_pa[p1]) + (k0 + sgl - s_p1[p1])];
-          }
+          const uint64_t x = s_sgl[k0 + (w - nm) - K0];
           row[u] = item_tag(x);
           src[u] = grads + (size_t)item_pos(x) * (size_t)D;
         }
