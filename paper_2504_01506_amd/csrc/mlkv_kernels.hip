@@ -443,11 +443,9 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
         ++below;
       } else if (key < hi) {
         const uint32_t at = atomicAdd(&s_nc, 1u);
-        if (at < (uint32_t)kRangeCap) {
-          const NewKey nk = *ent;
+        if (at < (uint32_t)kRangeCap) {  // the entry's slot and position are read after the scan
           s_key[at] = key;
-          s_sr[at] = nk.slot;
-          s_pos[at] = nk.pad;
+          s_sr[at] = (uint32_t)(ent - newlist);
         }
       }
     });
@@ -455,6 +453,13 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
     const uint32_t c = s_nc;
     const uint64_t base = size0 + below;
     if (c <= (uint32_t)kRangeCap) {
+      // slot and position of each gathered key, from its list entry
+      for (uint32_t j = threadIdx.x; j < c; j += NT) {
+        const NewKey nk = newlist[s_sr[j]];
+        s_sr[j] = nk.slot;
+        s_pos[j] = nk.pad;
+      }
+      __syncthreads();
       // rank among the range's keys, through kSub local sub-ranges cut at a
       // sample of the gathered keys: sub-range counts and their prefix, the
       // keys listed by sub-range, then each key ranked inside its sub-range
