@@ -109,6 +109,8 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
     float* __restrict__ out, const float* __restrict__ rows, int D, uint64_t seed,
     NewKey* __restrict__ newlist, uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch) {
   __shared__ uint32_t s_cnt;
+  __shared__ uint64_t s_nkey[kGetTile];  // the tile's new keys and their slots
+  __shared__ uint32_t s_nslot[kGetTile];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -130,7 +132,8 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
   }
   if (pr.status == P_NEW_MINE) {
     const uint32_t j = atomicAdd(&s_cnt, 1u);
-    newlist[base + j] = NewKey{key, pr.slot, (uint32_t)i};  // i: where get's output holds the initial row
+    s_nkey[j] = key;
+    s_nslot[j] = pr.slot;
     ctrl->new_epoch = epoch;
   }
   if (out != nullptr) {
@@ -138,7 +141,15 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
     wave_emit_rows<M>(out, rows, D, base + wave * 64, n, pr.status == P_HIT, pr.row, s0, lane);
   }
   __syncthreads();
-  if (tid == 0) tile_cnt[blockIdx.x] = s_cnt;
+  // the tile's list of new keys, in ascending key order (each at its rank)
+  const uint32_t c = s_cnt;
+  if ((uint32_t)tid < c) {
+    const uint64_t k = s_nkey[tid];
+    uint32_t r = 0;
+    for (uint32_t e = 0; e < c; ++e) r += s_nkey[e] < k ? 1u : 0u;
+    newlist[base + r] = NewKey{k, s_nslot[tid], 0u};
+  }
+  if (tid == 0) tile_cnt[blockIdx.x] = c;
 }
 
 // ===========================================================================
@@ -224,101 +235,57 @@ constexpr int kAssignBatch = 8;
 constexpr int kAssignMine = kAssignBatch * kAssignThreads;
 constexpr int kAssignDirect = 8192;  // up to this many new keys, each block ranks its tiles' keys against all
 constexpr int kRangeSamples = 512;   // sample of the new keys that splits the key space among the blocks
-constexpr int kRangeCap = 2560;      // keys of a block's key range ranked in LDS at once
-constexpr int kScanBatch = 16;       // key loads a lane has in flight while scanning all new keys
+constexpr int kRangeCap = 3072;      // keys of a block's key range ranked in LDS at once
 
-// Calls body(key, entry) once for every new key of the call, in no set order
-// (entry: its NewKey in the tiles' lists); the block's NT threads must all
-// call it. Tiles are taken kScanTiles per thread at a time; each wave walks a
-// contiguous run of their entries, 64 consecutive entries per load, with
-// kScanBatch loads in flight. s_pref: kScanTiles * NT + 1 words.
-constexpr int kScanTiles = 4;
-template <int NT, class Body>
-__device__ __forceinline__ void scan_new_keys(const NewKey* __restrict__ newlist,
-                                              const uint32_t* __restrict__ tile_cnt, int ntiles, int tile_size,
-                                              uint32_t* s_pref, uint32_t* s_w, Body body) {
-  constexpr int CT = kScanTiles * NT;
-  constexpr int NW = NT / 64;
-  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int t0 = 0; t0 < ntiles; t0 += CT) {
-    const int nt = min(CT, ntiles - t0);
-    uint32_t c[kScanTiles], sum = 0;
+// Each tile's list of new keys is sorted (ascending key). For the key range
+// [lo, hi) this returns the thread's share of the number of new keys below lo
+// and calls emit(offset, n) for each tile run of the range's keys (offset
+// into the lists, n > 0 entries). Threads take kSearchTiles tiles at a time
+// and search both bounds in all of them together (branch-free binary search,
+// each step one load per bound and tile in flight).
+constexpr int kSearchTiles = 16;
+template <int NT, class Emit>
+__device__ __forceinline__ uint64_t search_tile_lists(const NewKey* __restrict__ newlist,
+                                                      const uint32_t* __restrict__ tile_cnt, int ntiles,
+                                                      int tile_size, uint64_t lo, uint64_t hi, Emit emit) {
+  uint64_t below = 0;
+  for (int t0 = threadIdx.x; t0 < ntiles; t0 += NT * kSearchTiles) {
+    uint32_t c[kSearchTiles], a[kSearchTiles], b[kSearchTiles];
 #pragma unroll
-    for (int q = 0; q < kScanTiles; ++q) {
-      const int t = (int)threadIdx.x * kScanTiles + q;
-      c[q] = t < nt ? tile_cnt[t0 + t] : 0u;
-      sum += c[q];
+    for (int u = 0; u < kSearchTiles; ++u) {
+      const int t = t0 + u * NT;
+      c[u] = t < ntiles ? tile_cnt[t] : 0u;
+      a[u] = 0;  // keys below lo
+      b[u] = 0;  // keys below hi
     }
-    uint32_t tot;
-    uint32_t off = block_exclusive_scan<NT>(sum, s_w, &tot);
+    // a tile holds at most tile_size (a power of two) keys
+    for (uint32_t step = (uint32_t)tile_size; step >= 1; step >>= 1) {
 #pragma unroll
-    for (int q = 0; q < kScanTiles; ++q) {
-      s_pref[threadIdx.x * kScanTiles + q] = off;
-      off += c[q];
-    }
-    if (threadIdx.x == 0) s_pref[CT] = tot;
-    lds_barrier();
-    const uint32_t span = (tot + NW * 64 - 1) / (NW * 64) * 64;  // entries per wave, a multiple of 64
-    const uint32_t wb = min(tot, wave * span), we = min(tot, wb + span);
-    for (uint32_t e0 = wb + lane; e0 < we; e0 += 64 * kScanBatch) {
-      // the tile of each entry: the last t with s_pref[t] <= e, by a
-      // branch-free binary search over CT tiles, kScanBatch at a time
-      uint32_t t[kScanBatch];
-#pragma unroll
-      for (int u = 0; u < kScanBatch; ++u) t[u] = 0;
-#pragma unroll
-      for (int step = CT / 2; step >= 1; step >>= 1) {
-#pragma unroll
-        for (int u = 0; u < kScanBatch; ++u)
-          if (s_pref[t[u] + step] <= e0 + 64 * u) t[u] += step;
+      for (int u = 0; u < kSearchTiles; ++u) {
+        const NewKey* l = newlist + (size_t)(t0 + u * NT) * tile_size;
+        if (a[u] + step <= c[u] && l[a[u] + step - 1].key < lo) a[u] += step;
+        if (b[u] + step <= c[u] && l[b[u] + step - 1].key < hi) b[u] += step;
       }
-      uint32_t at[kScanBatch];  // offsets into the lists
-      uint64_t key[kScanBatch];
-#pragma unroll
-      for (int u = 0; u < kScanBatch; ++u) {
-        const uint32_t e = e0 + 64 * u;
-        at[u] = 0;
-        key[u] = kEmptyKey;
-        if (e < we) {
-          at[u] = (uint32_t)(t0 + t[u]) * (uint32_t)tile_size + (e - s_pref[t[u]]);
-          key[u] = newlist[at[u]].key;
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < kScanBatch; ++u)
-        if (key[u] != kEmptyKey) body(key[u], newlist + at[u]);
     }
-    lds_barrier();
+#pragma unroll
+    for (int u = 0; u < kSearchTiles; ++u) {
+      below += a[u];
+      if (b[u] > a[u]) emit((uint32_t)(t0 + u * NT) * (uint32_t)tile_size + a[u], b[u] - a[u]);
+    }
   }
+  return below;
 }
 
 // Initial rows of new keys ks[j] (j < m) at rows base + rk[j]: a wave per
-// row, its lanes along the row. When the get call has an output, the row is
-// copied from the output row at position ps[j], which holds the same values.
-template <int NT, class KP, class RP, class PP>
-__device__ __forceinline__ void write_init_rows(const KP ks, const RP rk, const PP ps, uint32_t m, uint64_t base,
-                                                float* __restrict__ rows, int D, uint64_t seed,
-                                                const float* __restrict__ out) {
-  constexpr int NW = NT / 64, R = 8;  // rows a wave copies at once
+// row, its lanes along the row.
+template <int NT, class KP, class RP>
+__device__ __forceinline__ void write_init_rows(const KP ks, const RP rk, uint32_t m, uint64_t base,
+                                                float* __restrict__ rows, int D, uint64_t seed) {
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  if (out != nullptr) {
-    for (uint32_t j0 = wave * R; j0 < m; j0 += NW * R) {
-      for (int col = (int)lane; col < D; col += 64) {
-        float v[R];
-#pragma unroll
-        for (int r = 0; r < R; ++r)
-          if (j0 + r < m) v[r] = out[(uint64_t)ps[j0 + r] * (uint64_t)D + col];
-#pragma unroll
-        for (int r = 0; r < R; ++r)
-          if (j0 + r < m) rows[(base + rk[j0 + r]) * (uint64_t)D + col] = v[r];
-      }
-    }
-  } else {
-    for (uint32_t j = wave; j < m; j += NW) {
-      float* w = rows + (base + rk[j]) * (uint64_t)D;
-      const uint64_t s0 = splitmix_mix(ks[j] ^ seed);
-      for (int col = (int)lane; col < D; col += 64) w[col] = init_elem(s0, col);
-    }
+  for (uint32_t j = wave; j < m; j += NT / 64) {
+    float* w = rows + (base + rk[j]) * (uint64_t)D;
+    const uint64_t s0 = splitmix_mix(ks[j] ^ seed);
+    for (int col = (int)lane; col < D; col += 64) w[col] = init_elem(s0, col);
   }
 }
 
@@ -335,23 +302,23 @@ __device__ __forceinline__ void write_new_rows(const KP ks, const SP sl, const R
     idx[slot / kSlots].row[slot % kSlots] = row;
     state[row] = 0.0f;
   }
-  write_init_rows<NT>(ks, rk, ks, m, base, rows, D, seed, nullptr);
+  write_init_rows<NT>(ks, rk, m, base, rows, D, seed);
 }
 
 __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
     Bucket* __restrict__ idx, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
     int ntiles, int tile_size, float* __restrict__ rows, float* __restrict__ state, int D,
     uint64_t seed, int64_t capacity, Ctrl* ctrl, uint64_t epoch, uint64_t* __restrict__ xkey,
-    uint32_t* __restrict__ xslot, const float* __restrict__ out) {
+    uint32_t* __restrict__ xslot) {
   constexpr int NT = kAssignThreads;
   __shared__ unsigned long long s_w64[NT / 64];
   __shared__ uint32_t s_w[NT / 64];
-  __shared__ __align__(16) uint32_t s_pref[kScanTiles * NT + 1];
+  __shared__ __align__(16) uint32_t s_pref[NT + 1];
   __shared__ uint32_t s_nc;
   __shared__ uint64_t s_cut[2];
   // one LDS buffer of 48 KiB; the two ranking methods lay it out differently
   __shared__ uint64_t s_buf[kChunk + 2 * kAssignMine];
-  static_assert(kRangeCap * 18 <= (int)sizeof(s_buf) && kRangeSamples * 12 <= (int)sizeof(s_buf), "LDS");
+  static_assert(kRangeCap * 14 <= (int)sizeof(s_buf) && kRangeSamples * 12 <= (int)sizeof(s_buf), "LDS");
   static_assert(kRangeSamples % NT == 0 && kRangeCap <= 65536, "sample and range sizes");
 
   const uint64_t size0 = ctrl->size[epoch & 1];
@@ -375,9 +342,10 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
     // ---- many new keys: key ranges. Every block takes the same sample of the
     // new keys (sample k is the new key at position floor(k M / S) of the
     // tiles' lists laid end to end) and the same cut points from it, which
-    // give block g the keys in [lo, hi). One scan over all new keys counts
-    // those below lo, the block's first rank, and gathers the block's own,
-    // which are then ranked among themselves. No block waits for another.
+    // give block g the keys in [lo, hi). A binary search of both bounds in
+    // every tile's sorted list of new keys counts the keys below lo, the
+    // block's first rank, and finds the block's own, which are then ranked
+    // among themselves. No block waits for another.
     constexpr uint32_t S = kRangeSamples;
     uint64_t* s_smp = s_buf;                                       // [S]
     uint32_t* s_sat = reinterpret_cast<uint32_t*>(s_buf + S);     // [S] offsets of the samples in the lists
@@ -435,30 +403,21 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
     // their order by local sub-range
     uint64_t* s_key = s_buf;                                                 // [kRangeCap]
     uint32_t* s_sr = reinterpret_cast<uint32_t*>(s_buf + kRangeCap);        // [kRangeCap]
-    uint32_t* s_pos = s_sr + kRangeCap;                                      // [kRangeCap]
-    uint16_t* s_ord = reinterpret_cast<uint16_t*>(s_pos + kRangeCap);       // [kRangeCap]
-    uint64_t below = 0;
-    scan_new_keys<NT>(newlist, tile_cnt, ntiles, tile_size, s_pref, s_w, [&](uint64_t key, const NewKey* ent) {
-      if (key < lo) {
-        ++below;
-      } else if (key < hi) {
-        const uint32_t at = atomicAdd(&s_nc, 1u);
-        if (at < (uint32_t)kRangeCap) {  // the entry's slot and position are read after the scan
-          s_key[at] = key;
-          s_sr[at] = (uint32_t)(ent - newlist);
-        }
-      }
-    });
+    uint16_t* s_ord = reinterpret_cast<uint16_t*>(s_sr + kRangeCap);        // [kRangeCap]
+    uint64_t below = search_tile_lists<NT>(newlist, tile_cnt, ntiles, tile_size, lo, hi,
+                                           [&](uint32_t off, uint32_t cnt) {
+                                             const uint32_t at = atomicAdd(&s_nc, cnt);
+                                             for (uint32_t e = 0; e < cnt && at + e < (uint32_t)kRangeCap; ++e) {
+                                               s_key[at + e] = newlist[off + e].key;
+                                               s_sr[at + e] = off + e;  // slot and position are read later
+                                             }
+                                           });
     below = block_sum_u64<NT>(below, s_w64);  // its barriers also publish s_nc and the gathered keys
     const uint32_t c = s_nc;
     const uint64_t base = size0 + below;
     if (c <= (uint32_t)kRangeCap) {
-      // slot and position of each gathered key, from its list entry
-      for (uint32_t j = threadIdx.x; j < c; j += NT) {
-        const NewKey nk = newlist[s_sr[j]];
-        s_sr[j] = nk.slot;
-        s_pos[j] = nk.pad;
-      }
+      // the slot of each gathered key, from its list entry
+      for (uint32_t j = threadIdx.x; j < c; j += NT) s_sr[j] = newlist[s_sr[j]].slot;
       __syncthreads();
       // rank among the range's keys, through kSub local sub-ranges cut at a
       // sample of the gathered keys: sub-range counts and their prefix, the
@@ -545,7 +504,7 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
         if (j < c) s_sr[j] = rk[u];
       }
       __syncthreads();
-      write_init_rows<NT>(s_key, s_sr, s_pos, c, base, rows, D, seed, out);
+      write_init_rows<NT>(s_key, s_sr, c, base, rows, D, seed);
     } else {
       // more keys in the range than LDS holds: gather them in global scratch
       // at [below, below + c), which no other block's range overlaps, then
@@ -553,11 +512,12 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
       __syncthreads();
       if (threadIdx.x == 0) s_nc = 0;
       __syncthreads();
-      scan_new_keys<NT>(newlist, tile_cnt, ntiles, tile_size, s_pref, s_w, [&](uint64_t key, const NewKey* ent) {
-        if (key >= lo && key < hi) {
-          const uint32_t at = atomicAdd(&s_nc, 1u);
-          xkey[below + at] = key;
-          xslot[below + at] = ent->slot;
+      search_tile_lists<NT>(newlist, tile_cnt, ntiles, tile_size, lo, hi, [&](uint32_t off, uint32_t cnt) {
+        const uint32_t at = atomicAdd(&s_nc, cnt);
+        for (uint32_t e = 0; e < cnt; ++e) {
+          const NewKey nk = newlist[off + e];
+          xkey[below + at + e] = nk.key;
+          xslot[below + at + e] = nk.slot;
         }
       });
       __syncthreads();
@@ -658,12 +618,7 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
     for (int b = 0; b < kAssignBatch; ++b) {
       const int t = tb + b * (int)gridDim.x;
       const uint32_t c = t < ntiles ? tile_cnt[t] : 0u;
-      const NewKey* tl = newlist + (size_t)(t < ntiles ? t : 0) * tile_size;
-      struct {
-        const NewKey* e;
-        __device__ uint32_t operator[](uint32_t j) const { return e[j].pad; }
-      } pos{tl};
-      write_init_rows<NT>(s_key + b * NT, s_rank + b * NT, pos, c, size0, rows, D, seed, out);
+      write_init_rows<NT>(s_key + b * NT, s_rank + b * NT, c, size0, rows, D, seed);
     }
     __syncthreads();
   }
@@ -2254,7 +2209,7 @@ static hipError_t launch_get_t(const GetArgs& a, hipStream_t st, const LaunchHoo
   hook(K_ASSIGN_NEW, 0, st);
   hipLaunchKernelGGL(k_assign_new, dim3(grid), dim3(kAssignThreads), 0, st, a.idx, a.newlist,
                      a.tile_cnt, (int)ntiles, kGetTile, a.rows, a.state, a.D, a.seed, a.capacity,
-                     a.ctrl, a.epoch, a.xkey, a.xslot, a.out);
+                     a.ctrl, a.epoch, a.xkey, a.xslot);
   hook(K_ASSIGN_NEW, 1, st);
   return hipGetLastError();
 }
