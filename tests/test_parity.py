@@ -106,6 +106,25 @@ def test_put_inserts_unseen_keys_then_updates_them():
     pr.close()
 
 
+@pytest.mark.parametrize("n_new,n", [(8193, 8193), (9000, 9000), (10_000, 65_536), (20_000, 300_000)])
+def test_new_keys_just_past_the_direct_ranking(n_new, n):
+    """Calls with a little more than 8192 new keys, few blocks or many blocks
+    each with a small key range (one local sub-range), hits mixed in."""
+    rng = np.random.default_rng(n_new + n)
+    dim = 3
+    pr = Pair(dim, n + n_new + 10)
+    old = rng.choice(np.uint64(1) << np.uint64(62), size=max(1, n - n_new), replace=False).astype(np.uint64)
+    if n > n_new:
+        pr.get(np.sort(old))
+    new = rng.choice(np.uint64(1) << np.uint64(62), size=n_new, replace=False).astype(np.uint64) | (np.uint64(1) << np.uint64(62))
+    keys = np.concatenate([new, old[: n - n_new]]) if n > n_new else new
+    keys = keys[rng.permutation(keys.size)]
+    pr.get(keys)
+    pr.compare_rows()
+    pr.check_index()
+    pr.close()
+
+
 @pytest.mark.parametrize("case", ["random", "descending", "second_half_new", "clustered", "one_feature"])
 def test_many_new_keys_get_rows_in_key_order(case):
     """A call inserting many more new keys than one block ranks against all
