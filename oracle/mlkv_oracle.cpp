@@ -7,8 +7,9 @@
 //
 // What it computes (MLKV, arXiv 2504.01506):
 //   * Open(model_id, dim, staleness_bound) creates a table of `dim`-wide
-//     embedding rows (Sec. III-A, "Interfaces Summary"). Here: one table,
-//     staleness bound 0 (BSP, Sec. III-C1), plus a capacity.
+//     embedding rows (Sec. III-A, "Interfaces Summary"). Here: one table
+//     with a capacity, and either no staleness bound or a bound s >= 0 kept
+//     with the per-key counts of R8 (Sec. III-C1).
 //   * Get(keys) returns the embedding vector of each key (Sec. III-A). A key
 //     that is not present is inserted with a seeded initial row first.
 //   * Rmw (Sec. III-B, workflow step 8) with the modify function
@@ -35,6 +36,22 @@
 //   R7  the SGD variant of the Rmw applies the paper's update form itself
 //       (Sec. II-A): duplicate gradients summed as in R3, then
 //       w_c -= lr * g_c (separate fp32 operations); accumulators untouched.
+//   R8  bounded staleness (Sec. III-C1, the per-record vector clock): a table
+//       opened with a staleness bound s >= 0 keeps a count c_k per key, the
+//       gets served on k not yet matched by a put. A get call serves an
+//       already present key only while c_k <= s (the paper's strict "below
+//       the bound" could never serve anything at s = 0, its bulk-synchronous
+//       setting, so the test is read as <=) and then raises c_k by one; a key
+//       that fails the test is blocked: its positions of `out` are left as
+//       they are, c_k is unchanged, and the call reports the positions. The
+//       count moves once per call and key, however often the key occurs in
+//       the call. A key that the get inserts is served with c_k = 1. Every
+//       put call (any modify function) lowers c_k of each distinct key by one,
+//       never below 0 (the paper's Put only reduces the staleness); a key a
+//       put inserts starts at 0. Without a bound nothing is counted and every
+//       get is served (the asynchronous end, bound = infinity). Waiting is
+//       left to the caller, which repeats a blocked get after the puts it
+//       waits for.
 //
 // Storage is deliberately naive: std::unordered_map for key -> row, a sorted
 // array for a bulk prefill (identical result to inserting the same ascending
@@ -85,7 +102,21 @@ struct Table {
   std::unordered_map<uint32_t, size_t> stored;   // row -> offset in `store` once written
   std::vector<float> store;
   std::unordered_map<uint32_t, float> accum;     // row -> Adagrad accumulator G (0 if absent)
+  int64_t bound = -1;                            // staleness bound (R8); -1: not tracked
+  std::unordered_map<uint32_t, uint32_t> stale;  // row -> c_k (0 if absent), when tracked
 };
+
+// R8, put side: one completed update for every distinct row of the call.
+void put_done(Table& t, const std::vector<uint32_t>& rows) {
+  if (t.bound < 0) return;
+  std::vector<uint32_t> u(rows);
+  std::sort(u.begin(), u.end());
+  u.erase(std::unique(u.begin(), u.end()), u.end());
+  for (uint32_t r : u) {
+    auto it = t.stale.find(r);
+    if (it != t.stale.end() && it->second > 0) it->second -= 1;
+  }
+}
 
 bool find_row(const Table& t, uint64_t key, uint32_t* row) {
   if (t.prefill_n > 0) {
@@ -168,6 +199,14 @@ oracle_table* oracle_open(int32_t dim, int64_t capacity, uint64_t seed) {
   return reinterpret_cast<oracle_table*>(t);
 }
 
+// Open with a staleness bound s >= 0 (R8; Sec. III-C1: s = 0 is bulk-synchronous).
+oracle_table* oracle_open_bounded(int32_t dim, int64_t capacity, uint64_t seed, int64_t bound) {
+  if (bound < 0) return nullptr;
+  oracle_table* h = oracle_open(dim, capacity, seed);
+  if (h) reinterpret_cast<Table*>(h)->bound = bound;
+  return h;
+}
+
 void oracle_close(oracle_table* h) { delete reinterpret_cast<Table*>(h); }
 
 int64_t oracle_size(oracle_table* h) { return reinterpret_cast<Table*>(h)->size; }
@@ -195,6 +234,7 @@ int oracle_prefill_sorted(oracle_table* h, const uint64_t* keys, int64_t n) {
 // Get (Sec. III-A): out[i][c] = W[row(keys[i])][c]; `out` may be NULL (insert only).
 int oracle_get(oracle_table* h, const uint64_t* keys, int64_t n, float* out) {
   Table& t = *reinterpret_cast<Table*>(h);
+  if (t.bound >= 0) return kEinval;  // a bounded table reports blocked keys: oracle_get_bounded
   int rc = check_keys(keys, n);
   if (rc != kOk) return rc;
   std::vector<uint32_t> rows;
@@ -204,6 +244,39 @@ int oracle_get(oracle_table* h, const uint64_t* keys, int64_t n, float* out) {
     for (int64_t i = 0; i < n; ++i)
       for (int32_t c = 0; c < t.dim; ++c)
         out[i * t.dim + c] = read_elem(t, rows[(size_t)i], c);
+  }
+  return kOk;
+}
+
+// Get under the staleness bound (R8): each distinct key of the call is served
+// if its count before the call is at most the bound (a key the call inserts
+// has count 0), and a served key's count then grows by one. blocked[i] = 1
+// where keys[i] is blocked (out row i left as it is), else 0 and out row i is
+// the key's row as in oracle_get.
+int oracle_get_bounded(oracle_table* h, const uint64_t* keys, int64_t n, float* out, uint8_t* blocked) {
+  Table& t = *reinterpret_cast<Table*>(h);
+  if (t.bound < 0) return kEinval;
+  int rc = check_keys(keys, n);
+  if (rc != kOk) return rc;
+  if (n > 0 && blocked == nullptr) return kEinval;
+  std::vector<uint32_t> rows;
+  rc = resolve(t, keys, n, &rows);
+  if (rc != kOk) return rc;
+  std::map<uint32_t, bool> served;  // verdict of every distinct row, on its count before the call
+  for (int64_t i = 0; i < n; ++i) {
+    const uint32_t r = rows[(size_t)i];
+    if (served.count(r)) continue;
+    auto it = t.stale.find(r);
+    const uint32_t c = it == t.stale.end() ? 0u : it->second;
+    served[r] = (int64_t)c <= t.bound;
+  }
+  for (const auto& kv : served)
+    if (kv.second) t.stale[kv.first] += 1;
+  for (int64_t i = 0; i < n; ++i) {
+    const bool ok = served[rows[(size_t)i]];
+    blocked[i] = ok ? 0 : 1;
+    if (ok && out)
+      for (int32_t c = 0; c < t.dim; ++c) out[i * t.dim + c] = read_elem(t, rows[(size_t)i], c);
   }
   return kOk;
 }
@@ -249,6 +322,7 @@ int oracle_put_grad(oracle_table* h, const uint64_t* keys, const float* grads, i
     }
     t.accum[u] = Gn;
   }
+  put_done(t, rows);
   return kOk;
 }
 
@@ -268,6 +342,7 @@ int oracle_put(oracle_table* h, const uint64_t* keys, const float* values, int64
     float* w = writable_row(t, kv.first);
     for (int32_t c = 0; c < t.dim; ++c) w[c] = values[kv.second * t.dim + c];
   }
+  put_done(t, rows);
   return kOk;
 }
 
@@ -294,6 +369,7 @@ int oracle_put_grad_sgd(oracle_table* h, const uint64_t* keys, const float* grad
       w[c] = w[c] - p;
     }
   }
+  put_done(t, rows);
   return kOk;
 }
 
@@ -323,6 +399,18 @@ int oracle_read_rows(oracle_table* h, const int64_t* rows, int64_t nr, float* ou
       auto it = t.accum.find(r);
       state_out[j] = it == t.accum.end() ? 0.0f : it->second;
     }
+  }
+  return kOk;
+}
+
+// count_out[j] = staleness count c_k (R8) of row rows[j]; 0 when not tracked.
+int oracle_staleness(oracle_table* h, const int64_t* rows, int64_t nr, uint32_t* count_out) {
+  Table& t = *reinterpret_cast<Table*>(h);
+  if (nr < 0 || (nr > 0 && (rows == nullptr || count_out == nullptr))) return kEinval;
+  for (int64_t j = 0; j < nr; ++j) {
+    if (rows[j] < 0 || rows[j] >= t.size) return kEinval;
+    auto it = t.stale.find((uint32_t)rows[j]);
+    count_out[j] = it == t.stale.end() ? 0u : it->second;
   }
   return kOk;
 }

@@ -47,6 +47,9 @@ def _load():
     sig = {
         "oracle_abi_version": (ctypes.c_int, []),
         "oracle_open": (P, [I32, I64, U64]),
+        "oracle_open_bounded": (P, [I32, I64, U64, I64]),
+        "oracle_get_bounded": (ctypes.c_int, [P, P, I64, P, P]),
+        "oracle_staleness": (ctypes.c_int, [P, P, I64, P]),
         "oracle_close": (None, [P]),
         "oracle_size": (I64, [P]),
         "oracle_init_value": (F32, [U64, U64, I32]),
@@ -88,12 +91,16 @@ def mix64(z: int) -> int:
 class OracleTable:
     """One embedding table: plain CPU definition, single-threaded."""
 
-    def __init__(self, dim: int, capacity: int, seed: int = DEFAULT_SEED):
+    def __init__(self, dim: int, capacity: int, seed: int = DEFAULT_SEED, staleness_bound: int | None = None):
         self._lib = _load()
         self.dim = int(dim)
         self.capacity = int(capacity)
         self.seed = int(seed)
-        h = self._lib.oracle_open(self.dim, self.capacity, self.seed)
+        self.staleness_bound = staleness_bound
+        if staleness_bound is None:
+            h = self._lib.oracle_open(self.dim, self.capacity, self.seed)
+        else:
+            h = self._lib.oracle_open_bounded(self.dim, self.capacity, self.seed, int(staleness_bound))
         if not h:
             raise ValueError("oracle_open rejected its arguments")
         self._h = h
@@ -124,6 +131,26 @@ class OracleTable:
         rc = self._lib.oracle_get(self._h, _ptr(k), k.size, _ptr(out))
         return rc, out
 
+    def get_bounded(self, keys, out=None):
+        """Get under the staleness bound. Returns (rc, out, blocked[n] uint8);
+        rows of blocked positions keep what `out` held (zeros if not given)."""
+        k = _keys(keys)
+        if out is None:
+            out = np.zeros((k.size, self.dim), dtype=np.float32)
+        out = np.ascontiguousarray(out, dtype=np.float32)
+        blocked = np.zeros(k.size, dtype=np.uint8)
+        rc = self._lib.oracle_get_bounded(self._h, _ptr(k), k.size, _ptr(out), _ptr(blocked))
+        return rc, out, blocked
+
+    def staleness(self, rows):
+        """Per-row staleness counts (gets served not yet matched by a put)."""
+        r = np.ascontiguousarray(rows, dtype=np.int64)
+        out = np.empty(r.size, dtype=np.uint32)
+        rc = self._lib.oracle_staleness(self._h, _ptr(r), r.size, _ptr(out))
+        if rc != OK:
+            raise ValueError(f"oracle_staleness rc={rc}")
+        return out
+
     def put_grad(self, keys, grads, lr: float, eps: float) -> int:
         k = _keys(keys)
         g = np.ascontiguousarray(grads, dtype=np.float32)
@@ -148,6 +175,7 @@ class OracleTable:
         if g.size != k.size * self.dim:
             raise ValueError("grads must hold n * dim values")
         return self._lib.oracle_put_grad_sgd(self._h, _ptr(k), _ptr(g), k.size, float(lr))
+
     def lookup_rows(self, keys):
         k = _keys(keys)
         rows = np.empty(k.size, dtype=np.int64)

@@ -431,3 +431,110 @@ def test_sgd_closed_form_with_exact_sums():
     w, _ = t.read_rows([0])
     want = (w0[0] - np.float32(lr) * np.float32(k * gval)).astype(np.float32)
     assert np.array_equal(w[0], want)
+
+
+# --------------------------------------------------------------------------
+# bounded staleness (Sec. III-C1): closed forms of the per-key counts
+# --------------------------------------------------------------------------
+def _blocked_keys(keys, blocked):
+    return {int(k) for k, b in zip(keys, blocked) if b}
+
+
+@pytest.mark.parametrize("bound", [0, 1, 3])
+def test_staleness_bound_serves_exactly_bound_plus_one_gets_before_a_put(bound):
+    # a key fetched again and again without any put is served bound + 1 times
+    # (the stale-synchronous window), then blocked until one put completes
+    t = O.OracleTable(4, 16, staleness_bound=bound)
+    k = np.array([42], np.uint64)
+    for _ in range(bound + 1):
+        rc, _, bl = t.get_bounded(k)
+        assert rc == O.OK and bl[0] == 0
+    for _ in range(3):
+        rc, _, bl = t.get_bounded(k)
+        assert rc == O.OK and bl[0] == 1   # blocked gets do not count
+    # one put call completes one get, however often it holds the key
+    assert t.put_grad(np.repeat(k, 2), np.zeros((2, 4), np.float32), 0.1, 1e-8) == O.OK
+    rc, _, bl = t.get_bounded(k)
+    assert rc == O.OK and bl[0] == 0
+    rc, _, bl = t.get_bounded(k)
+    assert bl[0] == 1
+
+
+def test_bsp_pipeline_blocks_exactly_the_keys_shared_with_the_pending_step():
+    # bound 0 with get(s) issued before put(s-1): the blocked keys are the
+    # intersection of the two batches; once put(s-1) is done a second get of
+    # the blocked keys is served. Strictly alternating get and put never blocks.
+    rng = np.random.default_rng(7)
+    t = O.OracleTable(4, 4096, staleness_bound=0)
+    batches = [rng.integers(0, 300, size=200).astype(np.uint64) for _ in range(6)]
+    assert not t.get_bounded(batches[0])[2].any()
+    for s in range(1, 6):
+        rc, _, bl = t.get_bounded(batches[s])
+        assert rc == O.OK
+        want = set(int(x) for x in batches[s]) & set(int(x) for x in batches[s - 1])
+        assert want and _blocked_keys(batches[s], bl) == want
+        g = np.zeros((batches[s - 1].size, 4), np.float32)
+        assert t.put_grad(batches[s - 1], g, 0.1, 1e-8) == O.OK
+        again = batches[s][bl == 1]
+        rc, _, bl2 = t.get_bounded(again)
+        assert rc == O.OK and not bl2.any()
+    t2 = O.OracleTable(4, 4096, staleness_bound=0)
+    for s in range(6):
+        rc, _, bl = t2.get_bounded(batches[s])
+        assert rc == O.OK and not bl.any()
+        assert t2.put(batches[s], np.zeros((batches[s].size, 4), np.float32)) == O.OK
+
+
+def test_bound_one_three_deep_pipeline_blocks_the_triple_intersection():
+    # bound 1, gets of steps 0, 1, 2 before any put: the third get blocks the
+    # keys present in all three batches and nothing else
+    rng = np.random.default_rng(11)
+    t = O.OracleTable(4, 4096, staleness_bound=1)
+    b = [rng.integers(0, 120, size=100).astype(np.uint64) for _ in range(3)]
+    for s in range(2):
+        rc, _, bl = t.get_bounded(b[s])
+        assert rc == O.OK and not bl.any()
+    rc, _, bl = t.get_bounded(b[2])
+    want = set(int(x) for x in b[0]) & set(int(x) for x in b[1]) & set(int(x) for x in b[2])
+    assert _blocked_keys(b[2], bl) == want
+
+
+def test_staleness_duplicates_in_one_call_count_once_and_rows_match_an_untracked_table():
+    # a key repeated within one get is served at every position and counted
+    # once; served rows are exactly those of a table without a bound that saw
+    # the same served calls
+    rng = np.random.default_rng(3)
+    dim = 8
+    t = O.OracleTable(dim, 1024, staleness_bound=0)
+    u = O.OracleTable(dim, 1024)
+    keys = np.repeat(np.array([9, 4, 9, 1], np.uint64), 25)
+    rc, out, bl = t.get_bounded(keys)
+    assert rc == O.OK and not bl.any()
+    rc2, out2 = u.get(keys)
+    assert np.array_equal(out, out2)
+    rows = t.lookup_rows(np.array([9, 4, 1], np.uint64))
+    assert list(t.staleness(rows)) == [1, 1, 1]
+    g = rng.normal(0, 0.01, size=(keys.size, dim)).astype(np.float32)
+    assert t.put_grad(keys, g, 0.01, 1e-8) == O.OK and u.put_grad(keys, g, 0.01, 1e-8) == O.OK
+    assert list(t.staleness(rows)) == [0, 0, 0]
+    rc, out, bl = t.get_bounded(keys)
+    assert not bl.any() and np.array_equal(out, u.get(keys)[1])
+
+
+def test_staleness_blocked_rows_are_untouched_and_counts_floor_at_zero():
+    t = O.OracleTable(4, 64, staleness_bound=0)
+    k = np.array([1, 2], np.uint64)
+    t.get_bounded(k)
+    sentinel = np.full((2, 4), 7.0, np.float32)
+    rc, out, bl = t.get_bounded(k, out=sentinel.copy())
+    assert list(bl) == [1, 1] and np.array_equal(out, sentinel)
+    # puts on keys without pending gets (and a new key) leave counts at 0
+    assert t.put(np.array([1, 2, 3], np.uint64), np.zeros((3, 4), np.float32)) == O.OK
+    assert t.put(np.array([1, 2, 3], np.uint64), np.zeros((3, 4), np.float32)) == O.OK
+    assert list(t.staleness(t.lookup_rows(np.array([1, 2, 3], np.uint64)))) == [0, 0, 0]
+    # a plain get is refused on a bounded table; a failed call changes no count
+    assert t.get(k)[0] == O.EINVAL
+    t3 = O.OracleTable(4, 3, staleness_bound=0)
+    assert t3.get_bounded(np.array([1, 2], np.uint64))[0] == O.OK
+    assert t3.get_bounded(np.array([1, 5, 6], np.uint64))[0] == O.EFULL
+    assert list(t3.staleness([0, 1])) == [1, 1] and t3.size == 2
