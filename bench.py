@@ -132,12 +132,19 @@ def main():
     ap.add_argument("--scale", type=float, default=1.0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--staleness-bound", type=int, default=None,
+                    help="open the table with this staleness bound (gets then report blocked keys)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the path is single-GPU by design)", file=sys.stderr)
+        sys.exit(2)
+
+    if args.staleness_bound is not None and args.config.startswith("kv-"):
+        print("--staleness-bound applies to the training-step workloads (get then put_grad of the same keys)",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -179,20 +186,35 @@ def main():
     out = torch.empty((n, D), dtype=torch.float32, device="cuda")
     log(f"inputs ready in {time.perf_counter() - t0:.1f}s: {total_steps} batches of {n} keys")
 
-    t = mlkv.Table(D, wl.capacity)
+    bounded = args.staleness_bound is not None
+    t = mlkv.Table(D, wl.capacity, staleness_bound=args.staleness_bound)
+    blocked = torch.empty(n, dtype=torch.uint8, device="cuda")
     t0 = time.perf_counter()
     chunk = 1 << 16
+    zero_rows = torch.zeros((chunk, D), dtype=torch.float32, device="cuda") if bounded else None
     for s in range(0, pre.size, chunk):
-        t.get(torch.from_numpy(pre[s:s + chunk].view(np.int64)).cuda(), None)
+        kc = torch.from_numpy(pre[s:s + chunk].view(np.int64)).cuda()
+        if bounded:
+            # insert, then complete the inserting get with a put that changes no row
+            t.get_bounded(kc, None, blocked[:kc.numel()])
+            t.put_grad_sgd(kc, zero_rows[:kc.numel()], 0.0)
+        else:
+            t.get(kc, None)
     assert t.sync() == mlkv.MLKV_OK
     log(f"prefill {pre.size} keys in {time.perf_counter() - t0:.2f}s, size={t.size}")
 
+    def get(k, o):
+        if bounded:
+            t.get_bounded(k, o, blocked[:k.numel()])
+        else:
+            t.get(k, o)
+
     def step(s):
         if kv:
-            t.get(keys_d[s][:h], out[:h])
+            get(keys_d[s][:h], out[:h])
             t.put(keys_d[s][h:], grads_d[s])
         else:
-            t.get(keys_d[s], out)
+            get(keys_d[s], out)
             t.put_grad(keys_d[s], grads_d[s], wl.lr, wl.eps)
 
     for s in range(args.warmup):
@@ -213,6 +235,9 @@ def main():
     wall = time.perf_counter() - w0
     ms = ev0.elapsed_time(ev1)
     assert t.sync() == mlkv.MLKV_OK
+    if bounded:  # each step's put completes its get, so no get is ever blocked
+        assert int(blocked.sum()) == 0, "a get was blocked"
+
     ms_step = ms / args.steps
     keys_per_s = n * args.steps / (ms * 1e-3)
     if kv:
@@ -250,7 +275,8 @@ def main():
     dom = max(kinfo, key=lambda k: kinfo[k]["avg_us"] * kinfo[k]["launches"])
     digest = source_digest()
     # the committed counters were taken on the full-size DLRM-shaped workload
-    traffic = load_traffic(dom, digest) if args.config == "dlrm" and args.scale == 1.0 else None
+    traffic = (load_traffic(dom, digest) if args.config == "dlrm" and args.scale == 1.0 and not bounded
+               else None)
     roof = {"kernel": dom, "bound": "hbm", "achieved": kinfo[dom]["gbps"], "peak": PEAK_HBM_GBPS,
             "unit": "GB/s", "frac": round(kinfo[dom]["gbps"] / PEAK_HBM_GBPS, 4), "traffic": traffic,
             "alg_bytes_per_launch": kinfo[dom]["alg_bytes_per_launch"],
@@ -299,6 +325,7 @@ def main():
             "workload": workload,
             "rows": wl.capacity, "dim": D, "lookups_per_step": n, "prefill": int(pre.size),
             "unique_keys_per_step": round(U_avg, 1), "scale": args.scale,
+            **({"staleness_bound": args.staleness_bound} if bounded else {}),
         },
         "gbps_effective": round(gbps, 1),
         "pct_of_peak_hbm": round(100.0 * gbps / PEAK_HBM_GBPS, 2),

@@ -10,8 +10,9 @@
  *                                         modify function is "sum the gradients
  *                                         of duplicate keys, then one row-wise
  *                                         Adagrad step"
- * Tables live entirely in HBM. Staleness bound is 0 (bulk-synchronous, Sec.
- * III-C1): calls on one table must be ordered on one HIP stream.
+ * Tables live entirely in HBM. Calls on one table must be ordered on one HIP
+ * stream. A table may carry a staleness bound (Sec. III-C1, see
+ * mlkv_open_bounded); without one every get is served.
  *
  * Conventions for every call below
  *   - Pointers named d_* are DEVICE pointers (HBM), owned by the caller, that
@@ -48,8 +49,8 @@ enum {
 #define MLKV_RESERVED_KEY 0xFFFFFFFFFFFFFFFFull
 
 /* Creates a table of `dim`-wide fp32 rows with room for `capacity` keys
- * (Open, Sec. III-A; model_id and staleness_bound are not needed: one table,
- * bound 0). Limits: 1 <= dim <= 1024, 1 <= capacity <= 2^32 - 2. The table
+ * (Open, Sec. III-A; model_id is not needed: one table per handle; no
+ * staleness bound, see mlkv_open_bounded). Limits: 1 <= dim <= 1024, 1 <= capacity <= 2^32 - 2. The table
  * owns all of its device memory (hash index, rows, optimizer state,
  * scratch), allocated on the current HIP device. Returns NULL on failure
  * (see mlkv_last_error). Uses seed MLKV_DEFAULT_SEED and max load 0.75. */
@@ -58,6 +59,26 @@ mlkv_table *mlkv_open(int32_t dim, int64_t capacity);
 /* As mlkv_open with an explicit initial-row seed and the largest fraction of
  * hash-index slots that may hold keys (0 < max_load <= 0.9). */
 mlkv_table *mlkv_open_ex(int32_t dim, int64_t capacity, uint64_t seed, float max_load);
+
+/* Open (Sec. III-A) with a staleness bound s (Sec. III-C1: bulk-synchronous
+ * at s = 0, stale-synchronous above; a table without a bound is the
+ * asynchronous end). The table keeps, per key, the number of gets served on
+ * it that no put has completed yet (the count of the paper's per-record
+ * vector clock, a word per row next to the Adagrad accumulator):
+ *   - mlkv_get_bounded serves a key present before the call only while its
+ *     count is at most s, then raises the count by one; otherwise the key is
+ *     blocked. A key inserted by the call is served (count 1). The count
+ *     moves once per call and key, however often the key occurs.
+ *   - every put call (mlkv_put_grad, mlkv_put_grad_sgd, mlkv_put) lowers the
+ *     count of each of its distinct keys by one, not below 0; a key a put
+ *     inserts starts at 0.
+ * The paper's "wait until below the bound" is left to the caller: it repeats
+ * the blocked positions after the puts they wait for (the library never
+ * waits on the device). Limits: 0 <= staleness_bound <= 2^24 - 2, at most
+ * 2^40 get calls per table; otherwise as mlkv_open_ex. mlkv_get is refused
+ * (MLKV_EINVAL) on such a table. Extra device memory: 8 bytes per row. */
+mlkv_table *mlkv_open_bounded(int32_t dim, int64_t capacity, uint64_t seed, float max_load,
+                              int64_t staleness_bound);
 
 /* Get (Sec. III-A): d_out[i*dim + c] = row(d_keys[i])[c] for i < n, where a key
  * that is not yet in the table is first inserted. Within one call, the
@@ -68,6 +89,14 @@ mlkv_table *mlkv_open_ex(int32_t dim, int64_t capacity, uint64_t seed, float max
  * with mix64 the SplitMix64 output function. d_out may be NULL (insert only).
  * 0 <= n <= 2^31 - 1. d_keys: n uint64 keys. d_out: n*dim floats, row-major. */
 int mlkv_get(mlkv_table *t, const uint64_t *d_keys, int64_t n, float *d_out, void *hip_stream);
+
+/* Get on a table opened with mlkv_open_bounded (Sec. III-C1): as mlkv_get
+ * for the served positions; d_blocked[i] = 1 where d_keys[i] is blocked (row
+ * i of d_out is then left as it was), else 0. d_blocked: n bytes (device).
+ * A failed call (see mlkv_sync) changes no count. MLKV_EINVAL on a table
+ * without a bound. */
+int mlkv_get_bounded(mlkv_table *t, const uint64_t *d_keys, int64_t n, float *d_out, uint8_t *d_blocked,
+                     void *hip_stream);
 
 /* Rmw (Sec. III-B, step 8) with row-wise Adagrad as the modify function:
  * missing keys are inserted as in mlkv_get; then for every distinct key k of
@@ -136,6 +165,11 @@ int mlkv_export(mlkv_table *t, int64_t nrows, float *d_rows_out, float *d_state_
  * the next mlkv_sync return MLKV_EINVAL. */
 int mlkv_read_rows(mlkv_table *t, const int64_t *d_rows, int64_t n, float *d_rows_out,
                    float *d_state_out, void *hip_stream);
+
+/* d_out[i] = staleness count of row d_rows[i] (table opened with
+ * mlkv_open_bounded, else MLKV_EINVAL). A row id outside [0, size) gives
+ * 0xFFFFFFFF and makes the next mlkv_sync return MLKV_EINVAL. */
+int mlkv_read_staleness(mlkv_table *t, const int64_t *d_rows, int64_t n, uint32_t *d_out, void *hip_stream);
 
 /* ---- per-kernel timing (benchmarks) ----
  * The library runs MLKV_NUM_KERNELS kernels: 0 get_probe_gather and

@@ -28,6 +28,12 @@ struct mlkv_table {
   // the control block's epoch markers start at 0 ("no call")
   uint64_t epoch = 1;
 
+  // bounded staleness: one word per row (count | get-call epoch), the bound,
+  // and the epoch of the next get call (from 1: a cleared stamp is 0)
+  unsigned long long* clock = nullptr;
+  int64_t bound = -1;
+  uint64_t cepoch = 1;
+
   // per-call scratch, grown on demand
   int64_t ws_n = 0;
   NewKey* newlist = nullptr;
@@ -259,6 +265,26 @@ mlkv_table* mlkv_open(int32_t dim, int64_t capacity) {
   return mlkv_open_ex(dim, capacity, MLKV_DEFAULT_SEED, 0.75f);
 }
 
+mlkv_table* mlkv_open_bounded(int32_t dim, int64_t capacity, uint64_t seed, float max_load,
+                              int64_t staleness_bound) {
+  if (staleness_bound < 0 || staleness_bound > (int64_t)kClockCount - 1) {
+    fail(MLKV_EINVAL, "staleness_bound must be in [0, 2^24 - 2]");
+    return nullptr;
+  }
+  mlkv_table* t = mlkv_open_ex(dim, capacity, seed, max_load);
+  if (t == nullptr) return nullptr;
+  hipError_t e = dev_alloc(&t->clock, sizeof(unsigned long long) * (size_t)capacity);
+  if (e == hipSuccess) e = hipMemset(t->clock, 0, sizeof(unsigned long long) * (size_t)capacity);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    hip_fail(e, "staleness counts allocation");
+    mlkv_close(t);
+    return nullptr;
+  }
+  t->bound = staleness_bound;
+  return t;
+}
+
 void mlkv_close(mlkv_table* t) {
   if (t == nullptr) return;
   (void)hipSetDevice(t->device);
@@ -269,15 +295,26 @@ void mlkv_close(mlkv_table* t) {
   (void)hipFree(t->rows);
   (void)hipFree(t->state);
   (void)hipFree(t->ctrl);
+  (void)hipFree(t->clock);
   delete t;
 }
 
-int mlkv_get(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, void* hip_stream) {
+}  // extern "C"
+
+namespace {
+
+// The get pipeline (probe + gather, then rows for new keys); d_blocked is
+// written when the table has a staleness bound.
+int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uint8_t* d_blocked,
+             void* hip_stream) {
   int rc = check_table(t);
   if (rc) return rc;
   if (n < 0 || n > 0x7FFFFFFFll) return fail(MLKV_EINVAL, "n must be in [0, 2^31 - 1]");
   if (n == 0) return MLKV_OK;
   if (d_keys == nullptr) return fail(MLKV_EINVAL, "keys is NULL");
+  if (t->clock != nullptr && d_blocked == nullptr) return fail(MLKV_EINVAL, "blocked is NULL");
+  if (t->clock != nullptr && t->cepoch >= (1ull << (64 - kClockBits)))
+    return fail(MLKV_EINVAL, "the table has served 2^40 get calls, the most a bounded table counts");
   if ((rc = ensure_workspace(t, n)) != MLKV_OK) return rc;
   GetArgs a;
   a.idx = t->idx;
@@ -296,10 +333,45 @@ int mlkv_get(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, voi
   a.epoch = t->epoch;
   a.xkey = t->items;  // the put pipeline's scratch (at least n entries each), idle during a get
   a.xslot = t->meta;
+  a.clock = t->clock;
+  a.cepoch = t->cepoch;
+  a.bound = (uint32_t)std::max<int64_t>(t->bound, 0);
+  a.blocked = d_blocked;
   const bool vec4 = (t->dim % 4 == 0) && (d_out == nullptr || aligned16(d_out));
   hipError_t e = launch_get(a, vec4, static_cast<hipStream_t>(hip_stream), hook_of(t));
   if (e != hipSuccess) return hip_fail(e, "mlkv_get launch");
   t->epoch++;
+  if (t->clock != nullptr) t->cepoch++;
+  return MLKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mlkv_get(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, void* hip_stream) {
+  if (t != nullptr && t->clock != nullptr)
+    return fail(MLKV_EINVAL, "the table has a staleness bound: use mlkv_get_bounded");
+  return get_call(t, d_keys, n, d_out, nullptr, hip_stream);
+}
+
+int mlkv_get_bounded(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uint8_t* d_blocked,
+                     void* hip_stream) {
+  if (t != nullptr && t->clock == nullptr)
+    return fail(MLKV_EINVAL, "the table has no staleness bound: use mlkv_get");
+  return get_call(t, d_keys, n, d_out, d_blocked, hip_stream);
+}
+
+int mlkv_read_staleness(mlkv_table* t, const int64_t* d_rows, int64_t n, uint32_t* d_out, void* hip_stream) {
+  int rc = check_table(t);
+  if (rc) return rc;
+  if (t->clock == nullptr) return fail(MLKV_EINVAL, "the table has no staleness bound");
+  if (n < 0 || n > 0x7FFFFFFFll) return fail(MLKV_EINVAL, "n must be in [0, 2^31 - 1]");
+  if (n == 0) return MLKV_OK;
+  if (d_rows == nullptr || d_out == nullptr) return fail(MLKV_EINVAL, "rows or out is NULL");
+  hipError_t e = launch_read_clock(t->clock, &t->ctrl->size[t->epoch & 1], d_rows, n, d_out, t->ctrl,
+                                   static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail(e, "mlkv_read_staleness launch");
   return MLKV_OK;
 }
 
@@ -354,6 +426,7 @@ int put_call(mlkv_table* t, const uint64_t* d_keys, const float* src, int64_t n,
   a.flat_blocks = t->flat_blocks;
   a.ctrl = t->ctrl;
   a.epoch = t->epoch;
+  a.clock = t->clock;
   const bool vec4 = (t->dim % 4 == 0) && aligned16(src);
   hipError_t e = launch_put(a, vec4, static_cast<hipStream_t>(hip_stream), hook_of(t));
   if (e != hipSuccess) return hip_fail(e, "put launch");

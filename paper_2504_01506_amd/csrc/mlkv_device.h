@@ -19,6 +19,13 @@ struct __align__(128) Bucket {
 };
 static_assert(sizeof(Bucket) == 128, "bucket must be one 128-byte line");
 
+// Staleness word of a row (bounded staleness, Sec. III-C1): the low
+// kClockBits bits count the gets served on the row that no put has completed
+// yet, the high bits hold the epoch of the last get call that counted it (so
+// that a key occurring several times in one call is counted once).
+constexpr int kClockBits = 24;
+constexpr unsigned long long kClockCount = (1ull << kClockBits) - 1;
+
 // A key first inserted by the current call, owned by the lane that won its slot.
 struct NewKey {
   uint64_t key;

@@ -69,6 +69,13 @@ struct GetArgs {
   uint64_t epoch;
   uint64_t* xkey;   // [n] scratch: new keys of a key range too large for LDS
   uint32_t* xslot;  // [n] their index slots
+  // staleness bound (nullptr clock: not tracked): per-row words of
+  // (get-call epoch << kClockBits) | count, this call's epoch, the bound, and
+  // the per-position blocked flags the call writes
+  unsigned long long* clock;
+  uint64_t cepoch;
+  uint32_t bound;
+  uint8_t* blocked;
 };
 
 struct PutArgs {
@@ -100,6 +107,7 @@ struct PutArgs {
   int flat_blocks;    // least number of put_apply blocks (one per CU)
   Ctrl* ctrl;
   uint64_t epoch;
+  unsigned long long* clock;  // per-row staleness words, or nullptr when not tracked
 };
 
 hipError_t launch_get(const GetArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook);
@@ -108,6 +116,8 @@ hipError_t launch_lookup(Bucket* idx, uint32_t nb_log2, const uint64_t* keys, in
                          int64_t* rows_out, hipStream_t st);
 hipError_t launch_export_slots(const Bucket* idx, uint64_t nslots, uint64_t* keys_out,
                                uint32_t* rows_out, hipStream_t st);
+hipError_t launch_read_clock(const unsigned long long* clock, const unsigned long long* size_now,
+                             const int64_t* ids, int64_t n, uint32_t* out, Ctrl* ctrl, hipStream_t st);
 hipError_t launch_read_rows(const float* rows, const float* state, int D, const unsigned long long* size_now,
                             const int64_t* ids, int64_t n, float* w_out, float* st_out, Ctrl* ctrl,
                             hipStream_t st);

@@ -58,11 +58,14 @@ __device__ __forceinline__ typename VecT<VEC>::T init_vec(uint64_t s0, int col) 
 }
 
 // The wave copies the rows of its 64 positions into `out`: rows of keys that
-// were present are read from the table, rows of keys new in this call are
-// generated from their seed (they equal what the table will hold).
-template <class M>
+// were present are read from the table (how = 1), rows of keys new in this
+// call are generated from their seed (how = 0; they equal what the table will
+// hold), and positions of blocked keys are not written (how = 2, only with
+// kTrack: skipping stores costs registers, so tables without a staleness
+// bound use a variant without it).
+template <class M, bool kTrack>
 __device__ __forceinline__ void wave_emit_rows(float* __restrict__ out, const float* __restrict__ rows,
-                                               int D, int64_t wave_base, int64_t n, bool hit,
+                                               int D, int64_t wave_base, int64_t n, int how,
                                                uint32_t row, uint64_t s0, int lane) {
   constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
   constexpr int ITERS = 64 / RPW;
@@ -70,10 +73,10 @@ __device__ __forceinline__ void wave_emit_rows(float* __restrict__ out, const fl
   constexpr int CH = UNITS < 16 ? UNITS : 16;
   const int g = lane / LPR;
   const int q = lane % LPR;
-  const int ihit = hit ? 1 : 0;
 #pragma unroll 1
   for (int u0 = 0; u0 < UNITS; u0 += CH) {
     typename VecT<VEC>::T v[CH];
+    uint32_t skip = 0;  // units whose position is blocked
 #pragma unroll
     for (int u = 0; u < CH; ++u) {
       const int uu = u0 + u;
@@ -81,13 +84,14 @@ __device__ __forceinline__ void wave_emit_rows(float* __restrict__ out, const fl
       const int k = uu % K;
       const int r = it * RPW + g;
       const uint32_t rr = __shfl(row, r, 64);
-      const int hh = __shfl(ihit, r, 64);
+      const int hh = __shfl(how, r, 64);
       const uint64_t ss = __shfl((unsigned long long)s0, r, 64);
       const int col = (k * LPR + q) * VEC;
       const int64_t p = wave_base + r;
+      if constexpr (kTrack) skip |= (hh == 2 ? 1u : 0u) << u;
       if (uu < UNITS && p < n && col < D) {
-        if (hh) v[u] = load_vec<VEC>(rows + (size_t)rr * (size_t)D + col);
-        else v[u] = init_vec<VEC>(ss, col);
+        if (hh == 1) v[u] = load_vec<VEC>(rows + (size_t)rr * (size_t)D + col);
+        else if (hh == 0) v[u] = init_vec<VEC>(ss, col);
       }
     }
 #pragma unroll
@@ -98,16 +102,18 @@ __device__ __forceinline__ void wave_emit_rows(float* __restrict__ out, const fl
       const int r = it * RPW + g;
       const int col = (k * LPR + q) * VEC;
       const int64_t p = wave_base + r;
-      if (uu < UNITS && p < n && col < D) store_vec<VEC>(out + (size_t)p * (size_t)D + col, v[u]);
+      if (uu < UNITS && p < n && col < D && (!kTrack || !((skip >> u) & 1u)))
+        store_vec<VEC>(out + (size_t)p * (size_t)D + col, v[u]);
     }
   }
 }
 
-template <class M>
+template <class M, bool kTrack>
 __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
     Bucket* __restrict__ idx, uint32_t nb_log2, const uint64_t* __restrict__ keys, int64_t n,
     float* __restrict__ out, const float* __restrict__ rows, int D, uint64_t seed,
-    NewKey* __restrict__ newlist, uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch) {
+    NewKey* __restrict__ newlist, uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch,
+    unsigned long long* __restrict__ clock, uint64_t cepoch, uint32_t bound, uint8_t* __restrict__ blocked) {
   __shared__ uint32_t s_cnt;
   __shared__ uint64_t s_nkey[kGetTile];  // the tile's new keys and their slots
   __shared__ uint32_t s_nslot[kGetTile];
@@ -136,9 +142,30 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
     s_nslot[j] = pr.slot;
     ctrl->new_epoch = epoch;
   }
+  int how = pr.status == P_HIT ? 1 : 0;
+  if (kTrack && i < n) {
+    // bounded staleness: a present key is served while its count before the
+    // call is at most the bound. Serving it stamps the word with the call's
+    // epoch and that count plus one. Nothing else writes the word during the
+    // call, so a position reads either the word from before the call or the
+    // stamp; every position that reads the former stores the same stamp, and
+    // a plain store suffices (hot keys would serialise atomics). The count
+    // thus rises once per call, however often the key occurs.
+    bool blk = false;
+    if (pr.status == P_HIT) {
+      unsigned long long* cw = clock + pr.row;
+      const unsigned long long w = *cw;
+      if ((w >> kClockBits) != cepoch) {
+        if ((w & kClockCount) > bound) blk = true;
+        else *cw = (cepoch << kClockBits) | ((w & kClockCount) + 1);
+      }
+    }
+    if (blk) how = 2;
+    blocked[i] = blk ? 1 : 0;
+  }
   if (out != nullptr) {
     const uint64_t s0 = splitmix_mix(key ^ seed);
-    wave_emit_rows<M>(out, rows, D, base + wave * 64, n, pr.status == P_HIT, pr.row, s0, lane);
+    wave_emit_rows<M, kTrack>(out, rows, D, base + wave * 64, n, how, pr.row, s0, lane);
   }
   __syncthreads();
   // the tile's list of new keys, in ascending key order (each at its rank)
@@ -276,6 +303,22 @@ __device__ __forceinline__ uint64_t search_tile_lists(const NewKey* __restrict__
   return below;
 }
 
+// Staleness word of a row that a get inserts: served once by this call.
+__device__ __forceinline__ unsigned long long new_row_clock(uint64_t cepoch) {
+  return ((unsigned long long)cepoch << kClockBits) | 1ull;
+}
+
+// A failed get call gives back the counts it raised: every row stamped with
+// its epoch loses one, and the stamp (needed only within the call) is cleared.
+__device__ __forceinline__ void rollback_clocks(unsigned long long* __restrict__ clock, uint64_t nrows,
+                                                uint64_t cepoch) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t r = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; r < nrows; r += stride) {
+    const unsigned long long w = clock[r];
+    if ((w >> kClockBits) == cepoch) clock[r] = (w & kClockCount) - 1;
+  }
+}
+
 // Initial rows of new keys ks[j] (j < m) at rows base + rk[j]: a wave per
 // row, its lanes along the row.
 template <int NT, class KP, class RP>
@@ -295,12 +338,14 @@ __device__ __forceinline__ void write_init_rows(const KP ks, const RP rk, uint32
 template <int NT, class KP, class SP, class RP>
 __device__ __forceinline__ void write_new_rows(const KP ks, const SP sl, const RP rk, uint32_t m, uint64_t base,
                                                Bucket* __restrict__ idx, float* __restrict__ rows,
-                                               float* __restrict__ state, int D, uint64_t seed) {
+                                               float* __restrict__ state, int D, uint64_t seed,
+                                               unsigned long long* __restrict__ clock, uint64_t cepoch) {
   for (uint32_t j = threadIdx.x; j < m; j += NT) {
     const uint32_t slot = sl[j];
     const uint32_t row = (uint32_t)(base + rk[j]);
     idx[slot / kSlots].row[slot % kSlots] = row;
     state[row] = 0.0f;
+    if (clock != nullptr) clock[row] = new_row_clock(cepoch);
   }
   write_init_rows<NT>(ks, rk, m, base, rows, D, seed);
 }
@@ -309,7 +354,7 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
     Bucket* __restrict__ idx, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
     int ntiles, int tile_size, float* __restrict__ rows, float* __restrict__ state, int D,
     uint64_t seed, int64_t capacity, Ctrl* ctrl, uint64_t epoch, uint64_t* __restrict__ xkey,
-    uint32_t* __restrict__ xslot) {
+    uint32_t* __restrict__ xslot, unsigned long long* __restrict__ clock, uint64_t cepoch) {
   constexpr int NT = kAssignThreads;
   __shared__ unsigned long long s_w64[NT / 64];
   __shared__ uint32_t s_w[NT / 64];
@@ -325,6 +370,7 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
   const bool any_new = ctrl->new_epoch == epoch;
   const uint64_t M = any_new ? count_new_keys<NT>(tile_cnt, ntiles, s_w64) : 0ull;
   const int err = call_verdict(ctrl, epoch, size0, M, capacity, ctrl->bad_epoch, ctrl->overflow_epoch);
+  if (err && clock != nullptr) rollback_clocks(clock, size0, cepoch);
   if (M == 0) return;
 
   if (err) {  // undo this call's insertions: the index returns to its state before the call
@@ -495,6 +541,7 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
           const uint32_t slot = s_sr[j];
           idx[slot / kSlots].row[slot % kSlots] = (uint32_t)(base + r);
           state[base + r] = 0.0f;
+          if (clock != nullptr) clock[base + r] = new_row_clock(cepoch);
         }
       }
       __syncthreads();
@@ -559,7 +606,7 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
           }
         }
         __syncthreads();
-        write_new_rows<NT>(s_mk, s_ms, s_mr, m, base, idx, rows, state, D, seed);
+        write_new_rows<NT>(s_mk, s_ms, s_mr, m, base, idx, rows, state, D, seed, clock, cepoch);
         __syncthreads();
       }
     }
@@ -613,6 +660,7 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
       const uint32_t row = (uint32_t)(size0 + s_rank[m]);
       idx[slot / kSlots].row[slot % kSlots] = row;
       state[row] = 0.0f;
+      if (clock != nullptr) clock[row] = new_row_clock(cepoch);
     }
     // initial rows, a wave per row
     for (int b = 0; b < kAssignBatch; ++b) {
@@ -1079,7 +1127,15 @@ struct RedCtx {
   float lr;
   float eps;
   uint64_t size0;
+  unsigned long long* clock;  // staleness words, or nullptr
 };
+
+// A put completes one served get on the row (bounded staleness, Sec.
+// III-C1): its count drops by one, never below 0. One lane per row.
+__device__ __forceinline__ void put_clock(unsigned long long* __restrict__ clock, uint32_t row) {
+  const unsigned long long w = clock[row];
+  if ((w & kClockCount) != 0) clock[row] = w - 1;
+}
 
 // Run-length encodes items sorted by value: seg[s] = first item of segment s,
 // seg[S] = mp, sid[j] = segment of item j. Returns S (block-uniform).
@@ -1326,8 +1382,10 @@ __device__ __forceinline__ void update_segments(IP it, SP seg, uint32_t S, const
     }
 #pragma unroll
     for (int u = 0; u < BB; ++u) {
-      if (s0 + u * NG < S)
+      if (s0 + u * NG < S) {
         Ops::update(c.op, gf[u], w[u], G[u], c.rows, c.state, row[u], D, q, d_pow2, inv_d, c.lr, c.eps);
+        if (c.clock != nullptr && q == 0) put_clock(c.clock, row[u]);
+      }
     }
   }
 }
@@ -1635,7 +1693,7 @@ __global__ __launch_bounds__(NT) void k_put_group(
     const float* __restrict__ grads, const double* __restrict__ partials, float* __restrict__ rows,
     float* __restrict__ state, int D, uint64_t seed, float lr, float eps, int64_t capacity, Ctrl* ctrl,
     uint64_t epoch, uint64_t* __restrict__ spill, uint64_t spill_words, uint64_t* __restrict__ gitems,
-    uint32_t* __restrict__ gdesc, PartMeta* __restrict__ pmeta, int op) {
+    uint32_t* __restrict__ gdesc, PartMeta* __restrict__ pmeta, int op, unsigned long long* __restrict__ clock) {
   using L = RedLds<NT>;
   constexpr int IPT = (kRedCap + NT - 1) / NT;
   extern __shared__ __align__(16) unsigned char s_raw[];
@@ -1697,7 +1755,7 @@ __global__ __launch_bounds__(NT) void k_put_group(
     return;
   }
 
-  const RedCtx c{op, idx, grads, partials, rows, state, D, seed, lr, eps, size0};
+  const RedCtx c{op, idx, grads, partials, rows, state, D, seed, lr, eps, size0, clock};
   if (mp > (uint32_t)kRedCap) {
     reduce_partition_global<M, NT>(p, mp, items, meta, ntiles, c, newlist, tile_cnt, ctrl, spill, spill_words,
                                    s_part, s_pref, s_w, s_w64, s_base);
@@ -1854,7 +1912,8 @@ __global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ g
                                                   const PartMeta* __restrict__ pmeta, int np,
                                                   const float* __restrict__ grads, double* __restrict__ partials,
                                                   float* __restrict__ rows, float* __restrict__ state, int D,
-                                                  int op, float lr, float eps, Ctrl* ctrl) {
+                                                  int op, float lr, float eps, Ctrl* ctrl,
+                                                  unsigned long long* __restrict__ clock) {
   using Ops = SegmentOps<M>;
   using LA = ApplyLds<M, NT>;
   constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
@@ -1927,15 +1986,6 @@ __global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ g
 #pragma unroll
       for (int xx = 0; xx < VEC; ++xx)
         if (col + xx < D) dst[col + xx] = a[k][xx];
-    }
-  };
-  auto add_row = [&](double (&a)[K][VEC], const double* src) {
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-      const int col = (k * LPR + q) * VEC;
-#pragma unroll
-      for (int xx = 0; xx < VEC; ++xx)
-        if (col + xx < D) a[k][xx] += src[col + xx];
     }
   };
   auto complete = [&](uint32_t row, uint32_t pos) {
@@ -2113,7 +2163,10 @@ __global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ g
     }
 #pragma unroll
     for (int u = 0; u < BB; ++u)
-      if (on[u]) Ops::update(op, gf[u], w[u], Gs[u], rows, state, row[u], D, q, d_pow2, inv_d, lr, eps);
+      if (on[u]) {
+        Ops::update(op, gf[u], w[u], Gs[u], rows, state, row[u], D, q, d_pow2, inv_d, lr, eps);
+        if (clock != nullptr && q == 0) put_clock(clock, row[u]);
+      }
   };
   // this group's work: completed segments [e0, e1) (g over the partials row
   // of their last item), then keys seen once [k0, k1) (g is their gradient row)
@@ -2192,6 +2245,21 @@ __global__ __launch_bounds__(256) void k_read_rows(const float* __restrict__ row
   }
 }
 
+// Staleness counts by row id; ids outside [0, size) give 0xFFFFFFFF and
+// latch MLKV_EINVAL (-1).
+__global__ __launch_bounds__(256) void k_read_clock(const unsigned long long* __restrict__ clock,
+                                                    const unsigned long long* size_now,
+                                                    const int64_t* __restrict__ ids, int64_t n,
+                                                    uint32_t* __restrict__ out, Ctrl* ctrl) {
+  const uint64_t size = *size_now;
+  for (uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x; i < (uint64_t)n; i += (uint64_t)gridDim.x * 256) {
+    const int64_t r = ids[i];
+    const bool ok = r >= 0 && (uint64_t)r < size;
+    if (!ok) atomicCAS(&ctrl->latched, 0, -1);
+    out[i] = ok ? (uint32_t)(clock[r] & kClockCount) : 0xFFFFFFFFu;
+  }
+}
+
 // ===========================================================================
 // Launchers
 // ===========================================================================
@@ -2199,9 +2267,10 @@ template <class M>
 static hipError_t launch_get_t(const GetArgs& a, hipStream_t st, const LaunchHook& hook) {
   const int64_t ntiles = (a.n + kGetTile - 1) / kGetTile;
   hook(K_GET_PROBE_GATHER, 0, st);
-  hipLaunchKernelGGL(k_get_probe_gather<M>, dim3((unsigned)ntiles), dim3(kGetTile), 0, st, a.idx,
-                     a.nb_log2, a.keys, a.n, a.out, a.rows, a.D, a.seed, a.newlist, a.tile_cnt, a.ctrl,
-                     a.epoch);
+  auto kern = a.clock != nullptr ? k_get_probe_gather<M, true> : k_get_probe_gather<M, false>;
+  hipLaunchKernelGGL(kern, dim3((unsigned)ntiles), dim3(kGetTile), 0, st, a.idx, a.nb_log2, a.keys, a.n,
+                     a.out, a.rows, a.D, a.seed, a.newlist, a.tile_cnt, a.ctrl, a.epoch, a.clock, a.cepoch,
+                     a.bound, a.blocked);
   hook(K_GET_PROBE_GATHER, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -2209,7 +2278,7 @@ static hipError_t launch_get_t(const GetArgs& a, hipStream_t st, const LaunchHoo
   hook(K_ASSIGN_NEW, 0, st);
   hipLaunchKernelGGL(k_assign_new, dim3(grid), dim3(kAssignThreads), 0, st, a.idx, a.newlist,
                      a.tile_cnt, (int)ntiles, kGetTile, a.rows, a.state, a.D, a.seed, a.capacity,
-                     a.ctrl, a.epoch, a.xkey, a.xslot);
+                     a.ctrl, a.epoch, a.xkey, a.xslot, a.clock, a.cepoch);
   hook(K_ASSIGN_NEW, 1, st);
   return hipGetLastError();
 }
@@ -2249,7 +2318,7 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   hipLaunchKernelGGL((k_put_group<M, NT>), dim3((unsigned)np), dim3(NT), L::total, st, a.idx, a.items,
                      a.meta, (int)ntiles, a.newlist, a.tile_cnt, a.grads, a.partials, a.rows, a.state,
                      a.D, a.seed, a.lr, a.eps, a.capacity, a.ctrl, a.epoch, a.spill, a.spill_words, a.gitems,
-                     a.gdesc, a.pmeta, a.op);
+                     a.gdesc, a.pmeta, a.op, a.clock);
   hook(K_PUT_GROUP, 1, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int apply_blocks = (int)std::max<int64_t>((int64_t)a.flat_blocks * ApplyCfg<M>::kPerCU,
@@ -2257,7 +2326,7 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   const size_t apply_lds = ApplyLds<M, NTA>::bytes(np);
   hook(K_PUT_APPLY, 0, st);
   hipLaunchKernelGGL((k_put_apply<M, NTA>), dim3((unsigned)apply_blocks), dim3(NTA), apply_lds, st, a.gitems, a.gdesc, a.pmeta, np, a.grads, a.partials,
-                     a.rows, a.state, a.D, a.op, a.lr, a.eps, a.ctrl);
+                     a.rows, a.state, a.D, a.op, a.lr, a.eps, a.ctrl, a.clock);
   hook(K_PUT_APPLY, 1, st);
   return hipGetLastError();
 }
@@ -2313,6 +2382,13 @@ hipError_t launch_read_rows(const float* rows, const float* state, int D, const 
   const uint64_t grid = std::min<uint64_t>((total + 255) / 256, 65536);
   hipLaunchKernelGGL(k_read_rows, dim3((unsigned)grid), dim3(256), 0, st, rows, state, D, size_now, ids, n,
                      w_out, st_out, ctrl);
+  return hipGetLastError();
+}
+
+hipError_t launch_read_clock(const unsigned long long* clock, const unsigned long long* size_now,
+                             const int64_t* ids, int64_t n, uint32_t* out, Ctrl* ctrl, hipStream_t st) {
+  const uint64_t grid = std::min<uint64_t>(((uint64_t)n + 255) / 256, 65536);
+  hipLaunchKernelGGL(k_read_clock, dim3((unsigned)grid), dim3(256), 0, st, clock, size_now, ids, n, out, ctrl);
   return hipGetLastError();
 }
 

@@ -43,7 +43,10 @@ def load() -> ctypes.CDLL:
     sig = {
         "mlkv_open": (P, [I32, I64]),
         "mlkv_open_ex": (P, [I32, I64, U64, F32]),
+        "mlkv_open_bounded": (P, [I32, I64, U64, F32, I64]),
         "mlkv_get": (INT, [P, P, I64, P, P]),
+        "mlkv_get_bounded": (INT, [P, P, I64, P, P, P]),
+        "mlkv_read_staleness": (INT, [P, P, I64, P, P]),
         "mlkv_put_grad": (INT, [P, P, P, I64, F32, F32, P]),
         "mlkv_put_grad_sgd": (INT, [P, P, P, I64, F32, P]),
         "mlkv_put": (INT, [P, P, P, I64, P]),
@@ -117,8 +120,23 @@ def mlkv_open_ex(dim: int, capacity: int, seed: int, max_load: float) -> int:
     return h
 
 
+def mlkv_open_bounded(dim: int, capacity: int, seed: int, max_load: float, staleness_bound: int) -> int:
+    h = load().mlkv_open_bounded(dim, capacity, seed, max_load, staleness_bound)
+    if not h:
+        raise MlkvError(MLKV_EINVAL, last_error())
+    return h
+
+
 def mlkv_get(t: int, keys, n: int, out, stream=None) -> int:
     return load().mlkv_get(t, _ptr(keys), n, _ptr(out), _stream(stream))
+
+
+def mlkv_get_bounded(t: int, keys, n: int, out, blocked, stream=None) -> int:
+    return load().mlkv_get_bounded(t, _ptr(keys), n, _ptr(out), _ptr(blocked), _stream(stream))
+
+
+def mlkv_read_staleness(t: int, rows, n: int, out, stream=None) -> int:
+    return load().mlkv_read_staleness(t, _ptr(rows), n, _ptr(out), _stream(stream))
 
 
 def mlkv_put_grad(t: int, keys, grads, n: int, lr: float, eps: float, stream=None) -> int:
@@ -189,10 +207,15 @@ class Table:
     """One embedding table on the current GPU. Keys are uint64 (stored in an
     int64 tensor), rows fp32. Methods raise MlkvError on a non-zero code."""
 
-    def __init__(self, dim: int, capacity: int, seed: int = MLKV_DEFAULT_SEED, max_load: float = 0.75):
+    def __init__(self, dim: int, capacity: int, seed: int = MLKV_DEFAULT_SEED, max_load: float = 0.75,
+                 staleness_bound: int | None = None):
         self.dim = int(dim)
         self.capacity = int(capacity)
-        self.h = mlkv_open_ex(self.dim, self.capacity, seed, max_load)
+        self.staleness_bound = staleness_bound
+        if staleness_bound is None:
+            self.h = mlkv_open_ex(self.dim, self.capacity, seed, max_load)
+        else:
+            self.h = mlkv_open_bounded(self.dim, self.capacity, seed, max_load, int(staleness_bound))
 
     def close(self):
         if self.h:
@@ -207,6 +230,20 @@ class Table:
 
     def get(self, keys: torch.Tensor, out: torch.Tensor | None = None, stream=None):
         _check(mlkv_get(self.h, keys, keys.numel(), out, stream))
+        return out
+
+    def get_bounded(self, keys: torch.Tensor, out: torch.Tensor | None = None,
+                    blocked: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        """Get under the table's staleness bound; returns the uint8 blocked flags."""
+        if blocked is None:
+            blocked = torch.empty(keys.numel(), dtype=torch.uint8, device=keys.device)
+        _check(mlkv_get_bounded(self.h, keys, keys.numel(), out, blocked, stream))
+        return blocked
+
+    def read_staleness(self, rows: torch.Tensor, stream=None) -> torch.Tensor:
+        """Staleness counts (int32 view of uint32) of the given row ids (int64)."""
+        out = torch.empty(rows.numel(), dtype=torch.int32, device=rows.device)
+        _check(mlkv_read_staleness(self.h, rows, rows.numel(), out, stream))
         return out
 
     def put_grad(self, keys: torch.Tensor, grads: torch.Tensor, lr: float, eps: float, stream=None):

@@ -43,10 +43,11 @@ def ulp_diff(a: np.ndarray, b: np.ndarray) -> int:
 class Pair:
     """A GPU table and an oracle table that receive exactly the same calls."""
 
-    def __init__(self, dim, capacity, seed=mlkv.MLKV_DEFAULT_SEED, max_load=0.75, lazy_oracle=False):
+    def __init__(self, dim, capacity, seed=mlkv.MLKV_DEFAULT_SEED, max_load=0.75, lazy_oracle=False,
+                 staleness_bound=None):
         self.dim = dim
-        self.gpu = mlkv.Table(dim, capacity, seed=seed, max_load=max_load)
-        self.ora = O.OracleTable(dim, capacity, seed=seed)
+        self.gpu = mlkv.Table(dim, capacity, seed=seed, max_load=max_load, staleness_bound=staleness_bound)
+        self.ora = O.OracleTable(dim, capacity, seed=seed, staleness_bound=staleness_bound)
         self.updated = np.zeros(capacity, dtype=bool)  # rows written by put_grad at least once
         self.stats = {"max_err": 0.0, "max_ulp": 0, "exact_mismatch": 0}
 
@@ -75,6 +76,35 @@ class Pair:
         if check:
             self.compare_get(keys, got, want)
         return got, want
+
+    def get_bounded(self, keys: np.ndarray):
+        """Get under the staleness bound on both sides: the blocked flags must
+        agree bit for bit, served rows as in get(); blocked rows keep the
+        sentinel the output held. Returns the blocked flags."""
+        k = dev_keys(keys)
+        sentinel = np.float32(-7.25)
+        out = torch.full((keys.size, self.dim), float(sentinel), dtype=torch.float32, device="cuda")
+        bl_d = self.gpu.get_bounded(k, out)
+        rc, want, bl = self.ora.get_bounded(keys)
+        assert rc == O.OK
+        assert self.gpu.sync() == mlkv.MLKV_OK
+        got = out.cpu().numpy()
+        got_bl = bl_d.cpu().numpy()
+        assert np.array_equal(got_bl, bl), f"blocked flags differ at {int(np.sum(got_bl != bl))} positions"
+        served = bl == 0
+        if served.any():
+            self.compare_get(keys[served], got[served], want[served])
+        assert np.all(got[~served] == sentinel), "a blocked position was written"
+        return bl
+
+    def compare_staleness(self):
+        """Staleness counts of every row, bit-exact."""
+        rows = np.arange(self.ora.size, dtype=np.int64)
+        got = self.gpu.read_staleness(torch.from_numpy(rows).cuda()).cpu().numpy().view(np.uint32)
+        assert self.gpu.sync() == mlkv.MLKV_OK
+        want = self.ora.staleness(rows)
+        assert np.array_equal(got, want), f"staleness counts differ at {int(np.sum(got != want))} rows"
+        return want
 
     def compare_get(self, keys, got, want):
         rows = self.ora.lookup_rows(keys)

@@ -61,6 +61,11 @@ def test_host_side_validation_without_a_gpu(lib):
     assert lib.mlkv_sync(None, None) == mlkv.MLKV_EINVAL
     assert lib.mlkv_size(None) == -1
     assert lib.mlkv_num_slots(None) == -1
+    assert lib.mlkv_open_bounded(16, 100, 1, 0.5, -1) is None
+    assert "staleness_bound" in mlkv.last_error()
+    assert lib.mlkv_open_bounded(16, 100, 1, 0.5, 2**24 - 1) is None
+    assert lib.mlkv_get_bounded(None, None, 10, None, None, None) == mlkv.MLKV_EINVAL
+    assert lib.mlkv_read_staleness(None, None, 10, None, None) == mlkv.MLKV_EINVAL
     lib.mlkv_close(None)  # no-op
 
 

@@ -1,0 +1,129 @@
+"""Bounded staleness (per-key counts of served gets not yet completed by a
+put, Sec. III-C1) on the GPU against the CPU oracle.
+
+Bar: blocked flags and staleness counts bit-exact; served rows as for every
+get (bit-exact until a row is updated, then within 1e-5 row-scaled); blocked
+positions of the output untouched; a failed call changes no count.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2504_01506_amd import mlkv
+from _harness import Pair, dev_keys, log
+
+pytestmark = pytest.mark.gpu
+
+
+def _keys(rng, n, space):
+    # spread ids over the key space (an odd multiplier is a bijection mod 2^64)
+    k = rng.integers(0, space, size=n).astype(np.uint64) * np.uint64(0x9E3779B97F4A7C15)
+    k[k == np.uint64(mlkv.MLKV_RESERVED_KEY)] = np.uint64(3)
+    return k
+
+
+@pytest.mark.parametrize("bound", [0, 1, 2])
+@pytest.mark.parametrize("dim", [4, 64])
+def test_pipelined_steps_match_the_oracle(bound, dim):
+    # gets run `depth` steps ahead of the puts (deeper than the bound, so
+    # keys block); blocked positions are fetched again once the pending puts
+    # are done; the puts alternate between the three modify functions
+    rng = np.random.default_rng(100 * bound + dim)
+    pr = Pair(dim, 40_000, staleness_bound=bound)
+    depth = bound + 2
+    batches, nblocked = [], 0
+    for s in range(10):
+        n = int(rng.integers(1, 6000)) if s % 3 else 4097
+        batches.append(_keys(rng, n, 9000))
+        bl = pr.get_bounded(batches[-1])
+        nblocked += int(bl.sum())
+        if len(batches) > depth:
+            done = batches.pop(0)
+            g = rng.normal(0, 0.01, size=(done.size, dim)).astype(np.float32)
+            if s % 3 == 0:
+                pr.put(done, g, 0.01, 1e-8)
+            elif s % 3 == 1:
+                pr.put_sgd(done, g, 0.05)
+            else:
+                pr.upsert(done, g)
+            if bl.any():
+                pr.get_bounded(batches[-1][bl == 1])
+        if s % 4 == 3:
+            pr.compare_staleness()
+    while batches:
+        done = batches.pop(0)
+        pr.put(done, rng.normal(0, 0.01, size=(done.size, dim)).astype(np.float32), 0.01, 1e-8)
+    counts = pr.compare_staleness()
+    assert nblocked > 0
+    pr.compare_rows()
+    pr.check_index()
+    log(f"[stale] bound {bound} dim {dim}: {nblocked} blocked positions, max count {int(counts.max())} "
+        f"stats={pr.stats}")
+    pr.close()
+
+
+def test_one_key_everywhere_counts_once_per_call():
+    # every position of a 300k batch (about 1200 get tiles) holds one of
+    # three keys: all blocks race for the same three words
+    rng = np.random.default_rng(5)
+    pr = Pair(8, 100, staleness_bound=1)
+    keys = rng.choice(np.array([11, 12, 13], np.uint64), size=300_000)
+    for want_blocked, want_count in ((0, 1), (0, 2), (1, 2)):
+        bl = pr.get_bounded(keys)
+        assert np.all(bl == want_blocked)
+        assert list(pr.compare_staleness()) == [want_count] * 3
+    pr.put(keys[:10], rng.normal(0, 0.01, size=(10, 8)).astype(np.float32), 0.01, 1e-8)
+    pr.get_bounded(keys)
+    pr.compare_staleness()
+    pr.close()
+
+
+@pytest.mark.parametrize("m", [3000, 100_000, 2_600_000])
+def test_new_keys_start_served_once(m):
+    # keys inserted by a bounded get, through each way of giving new keys
+    # their rows (few, key ranges in LDS, key ranges in global scratch)
+    rng = np.random.default_rng(m)
+    pr = Pair(2, m + 5000, staleness_bound=0)
+    keys = rng.choice(np.uint64(1) << np.uint64(40), size=m, replace=False).astype(np.uint64)
+    pr.get_bounded(keys)
+    counts = pr.compare_staleness()
+    assert np.all(counts == 1)
+    bl = pr.get_bounded(keys[: m // 2])
+    assert np.all(bl == 1)
+    pr.close()
+
+
+def test_failed_bounded_get_changes_no_count():
+    rng = np.random.default_rng(9)
+    pr = Pair(4, 5000, staleness_bound=3)
+    base = _keys(rng, 3000, 2000)
+    pr.get_bounded(base)
+    before = pr.compare_staleness()
+    # over capacity (many new keys) and a reserved key: both fail as a whole
+    over = np.concatenate([base[:500], np.arange(10**6, 10**6 + 8000, dtype=np.uint64)])
+    blocked = torch.empty(over.size, dtype=torch.uint8, device="cuda")
+    assert mlkv.mlkv_get_bounded(pr.gpu.h, dev_keys(over), over.size, None, blocked) == mlkv.MLKV_OK
+    assert pr.gpu.sync() == mlkv.MLKV_EFULL
+    bad = base[:700].copy()
+    bad[350] = np.uint64(mlkv.MLKV_RESERVED_KEY)
+    blocked = torch.empty(bad.size, dtype=torch.uint8, device="cuda")
+    assert mlkv.mlkv_get_bounded(pr.gpu.h, dev_keys(bad), bad.size, None, blocked) == mlkv.MLKV_OK
+    assert pr.gpu.sync() == mlkv.MLKV_EINVAL
+    assert np.array_equal(pr.compare_staleness(), before)
+    # the table goes on as if the failed calls had not been made
+    pr.get_bounded(base[::-1].copy())
+    pr.compare_staleness()
+    pr.check_index()
+    pr.close()
+
+
+def test_plain_get_is_refused_on_a_bounded_table_and_bounded_get_on_a_plain_one():
+    t = mlkv.Table(4, 100, staleness_bound=0)
+    k = dev_keys(np.array([1, 2], np.uint64))
+    assert mlkv.mlkv_get(t.h, k, 2, None) == mlkv.MLKV_EINVAL
+    t.close()
+    u = mlkv.Table(4, 100)
+    blocked = torch.empty(2, dtype=torch.uint8, device="cuda")
+    assert mlkv.mlkv_get_bounded(u.h, k, 2, None, blocked) == mlkv.MLKV_EINVAL
+    assert mlkv.mlkv_read_staleness(u.h, None, 0, None) == mlkv.MLKV_EINVAL
+    u.close()
