@@ -183,6 +183,8 @@ def main():
             known = np.union1d(known, new)
         UM.append((u.size, new.size))
         grads_d.append(torch.from_numpy(wl.grads(s)).cuda())
+        if (s + 1) % 20 == 0:
+            log(f"inputs: {s + 1} of {total_steps} batches")
     out = torch.empty((n, D), dtype=torch.float32, device="cuda")
     log(f"inputs ready in {time.perf_counter() - t0:.1f}s: {total_steps} batches of {n} keys")
 

@@ -23,7 +23,7 @@ def _keys(rng, n, space):
 
 
 @pytest.mark.parametrize("bound", [0, 1, 2])
-@pytest.mark.parametrize("dim", [4, 64])
+@pytest.mark.parametrize("dim", [1, 4, 7, 64, 400])
 def test_pipelined_steps_match_the_oracle(bound, dim):
     # gets run `depth` steps ahead of the puts (deeper than the bound, so
     # keys block); blocked positions are fetched again once the pending puts
