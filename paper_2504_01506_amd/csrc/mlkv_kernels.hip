@@ -261,7 +261,7 @@ constexpr int kAssignThreads = 256;
 constexpr int kAssignBatch = 8;
 constexpr int kAssignMine = kAssignBatch * kAssignThreads;
 constexpr int kAssignDirect = 8192;  // up to this many new keys, each block ranks its tiles' keys against all
-constexpr int kRangeSamples = 512;   // sample of the new keys that splits the key space among the blocks
+constexpr int kRangeSamples = 2048;  // sample of the new keys that splits the key space among the blocks
 constexpr int kRangeCap = 3072;      // keys of a block's key range ranked in LDS at once
 
 // Each tile's list of new keys is sorted (ascending key). For the key range
@@ -301,6 +301,53 @@ __device__ __forceinline__ uint64_t search_tile_lists(const NewKey* __restrict__
     }
   }
   return below;
+}
+
+// Ascending bitonic sort of NT * kSortPT distinct keys, thread t holding the
+// elements kSortPT t .. kSortPT t + kSortPT - 1 in v. Compare-exchanges whose
+// partner lies in the same thread run in registers; the others exchange
+// through LDS, alternating between buf0 and buf1 (NT * kSortPT keys each), so
+// one barrier per such stage suffices.
+constexpr int kSortPT = 8;
+template <int NT>
+__device__ __forceinline__ void sort_keys_8pt(uint64_t (&v)[kSortPT], uint64_t* buf0, uint64_t* buf1) {
+  constexpr uint32_t N = (uint32_t)NT * kSortPT;
+  const uint32_t t = threadIdx.x;
+  auto reg_stage = [&](auto J, uint32_t k) {
+    constexpr uint32_t j = decltype(J)::value;
+#pragma unroll
+    for (uint32_t r = 0; r < kSortPT; ++r) {
+      if ((r & j) == 0) {
+        const bool asc = ((t * kSortPT + r) & k) == 0;
+        const uint64_t a = v[r], b = v[r + j];
+        if ((a > b) == asc) {
+          v[r] = b;
+          v[r + j] = a;
+        }
+      }
+    }
+  };
+  bool second = false;
+  for (uint32_t k = 2; k <= N; k <<= 1) {
+    for (uint32_t j = k >> 1; j >= kSortPT; j >>= 1) {
+      uint64_t* b = second ? buf1 : buf0;
+      second = !second;
+#pragma unroll
+      for (uint32_t r = 0; r < kSortPT; ++r) b[r * NT + t] = v[r];
+      lds_barrier();
+      const uint32_t pt = t ^ (j / kSortPT);
+#pragma unroll
+      for (uint32_t r = 0; r < kSortPT; ++r) {
+        const uint32_t i = t * kSortPT + r;
+        const uint64_t p = b[r * NT + pt];
+        const bool asc = (i & k) == 0, low = (i & j) == 0;
+        v[r] = (asc == low) ? (v[r] < p ? v[r] : p) : (v[r] > p ? v[r] : p);
+      }
+    }
+    if (k >= 8) reg_stage(std::integral_constant<uint32_t, 4>{}, k);
+    if (k >= 4) reg_stage(std::integral_constant<uint32_t, 2>{}, k);
+    reg_stage(std::integral_constant<uint32_t, 1>{}, k);
+  }
 }
 
 // Staleness word of a row that a get inserts: served once by this call.
@@ -364,7 +411,7 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
   // one LDS buffer of 48 KiB; the two ranking methods lay it out differently
   __shared__ uint64_t s_buf[kChunk + 2 * kAssignMine];
   static_assert(kRangeCap * 14 <= (int)sizeof(s_buf) && kRangeSamples * 12 <= (int)sizeof(s_buf), "LDS");
-  static_assert(kRangeSamples % NT == 0 && kRangeCap <= 65536, "sample and range sizes");
+  static_assert(kRangeSamples == NT * kSortPT && kRangeCap <= 65536, "sample and range sizes");
 
   const uint64_t size0 = ctrl->size[epoch & 1];
   const bool any_new = ctrl->new_epoch == epoch;
@@ -393,7 +440,6 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
     // block's first rank, and finds the block's own, which are then ranked
     // among themselves. No block waits for another.
     constexpr uint32_t S = kRangeSamples;
-    uint64_t* s_smp = s_buf;                                       // [S]
     uint32_t* s_sat = reinterpret_cast<uint32_t*>(s_buf + S);     // [S] offsets of the samples in the lists
     {
       const int tpt = (ntiles + NT - 1) / NT;  // consecutive tiles per thread
@@ -414,35 +460,24 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
       }
     }
     __syncthreads();
+    uint64_t v[kSortPT];
 #pragma unroll
-    for (uint32_t u = 0; u < S / NT; ++u) s_smp[threadIdx.x + u * NT] = newlist[s_sat[threadIdx.x + u * NT]].key;
-    __syncthreads();
-    // the cut points: the samples of rank g S / G and (g + 1) S / G (samples
-    // are distinct keys, so ranks are too)
+    for (uint32_t u = 0; u < kSortPT; ++u) v[u] = newlist[s_sat[threadIdx.x + u * NT]].key;
+    // the cut points: the samples of rank g S / G and (g + 1) S / G of the
+    // sorted sample (samples are distinct keys, so ranks are too); eight
+    // sample gaps per range keep the largest range near twice the mean
     const uint32_t g = blockIdx.x, G = gridDim.x;
+    sort_keys_8pt<NT>(v, s_buf, s_buf + S);
     {
       const uint32_t r1 = (uint32_t)((uint64_t)g * S / G), r2 = (uint32_t)((uint64_t)(g + 1) * S / G);
-      uint64_t v[S / NT];
-      uint32_t r[S / NT];
 #pragma unroll
-      for (uint32_t u = 0; u < S / NT; ++u) {
-        v[u] = s_smp[threadIdx.x + u * NT];
-        r[u] = 0;
-      }
-      for (uint32_t e = 0; e < S; e += 2) {
-        const uint64_t x0 = s_smp[e], x1 = s_smp[e + 1];
-#pragma unroll
-        for (uint32_t u = 0; u < S / NT; ++u) r[u] += (x0 < v[u] ? 1u : 0u) + (x1 < v[u] ? 1u : 0u);
-      }
-      __syncthreads();
-#pragma unroll
-      for (uint32_t u = 0; u < S / NT; ++u) {
-        if (r[u] == r1) s_cut[0] = v[u];
-        if (r[u] == r2) s_cut[1] = v[u];
+      for (uint32_t u = 0; u < kSortPT; ++u) {
+        if (threadIdx.x * kSortPT + u == r1) s_cut[0] = v[u];
+        if (threadIdx.x * kSortPT + u == r2) s_cut[1] = v[u];
       }
       if (threadIdx.x == 0) s_nc = 0;
-      __syncthreads();
     }
+    __syncthreads();
     const uint64_t lo = g == 0 ? 0ull : s_cut[0];
     const uint64_t hi = g + 1 == G ? kEmptyKey : s_cut[1];
     // keys in [lo, hi) first go to LDS: key, slot (later the rank), and
