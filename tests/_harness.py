@@ -57,10 +57,20 @@ class Pair:
 
     def prefill(self, keys_sorted: np.ndarray, chunk: int = 1 << 16):
         """Inserts ascending keys through get(out=NULL) in chunks on the GPU, and
-        as one sorted prefill in the oracle (identical rows: row = rank)."""
+        as one sorted prefill in the oracle (identical rows: row = rank; on a
+        bounded table every count is back at 0 on both sides)."""
+        zero = None
         for s in range(0, keys_sorted.size, chunk):
             k = dev_keys(keys_sorted[s:s + chunk])
-            self.gpu.get(k, None)
+            if self.gpu.staleness_bound is None:
+                self.gpu.get(k, None)
+            else:
+                # a bounded table counts the inserting get: a put that changes
+                # no row (SGD with zero gradients and lr 0) completes it
+                if zero is None:
+                    zero = torch.zeros((chunk, self.dim), dtype=torch.float32, device="cuda")
+                self.gpu.get_bounded(k, None)
+                self.gpu.put_grad_sgd(k, zero[:k.numel()], 0.0)
         assert self.gpu.sync() == mlkv.MLKV_OK
         assert self.ora.prefill_sorted(keys_sorted) == O.OK
         assert self.gpu.size == self.ora.size == keys_sorted.size

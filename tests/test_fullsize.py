@@ -83,3 +83,32 @@ def test_full_size_max_batch_of_one_hot_key():
     pr.compare_rows()
     log(f"[full] one-hot ok, stats={pr.stats}")
     pr.close()
+
+
+def test_full_size_dlrm_bounded_staleness_pipeline():
+    """DLRM-sized table with staleness bound 0, each step's get issued before
+    the previous step's put: the keys shared with the pending step are blocked
+    (flags compared at every position), fetched again after the put, and the
+    counts end at 0 for every key."""
+    wl = W.make("dlrm", scale=1.0)
+    pr = Pair(wl.dim, wl.capacity, staleness_bound=0)
+    pr.prefill(wl.prefill_keys())
+    rng = np.random.default_rng(12)
+    prev = wl.keys(0)
+    bl = pr.get_bounded(prev)
+    assert not bl.any()
+    for s in range(1, 3):
+        keys = wl.keys(s)
+        bl = pr.get_bounded(keys)
+        assert bl.any()
+        pr.put(prev, wl.grads(s - 1), wl.lr, wl.eps)
+        again = pr.get_bounded(keys[bl == 1])
+        assert not again.any()
+        log(f"[full] bounded step {s}: {int(bl.sum())} blocked positions, stats={pr.stats}")
+        prev = keys
+    pr.put(prev, wl.grads(2), wl.lr, wl.eps)
+    rows = np.unique(pr.ora.lookup_rows(np.concatenate([wl.keys(s) for s in range(3)])))
+    got = pr.gpu.read_staleness(torch.from_numpy(rows).cuda()).cpu().numpy()
+    assert np.all(got == 0) and np.all(pr.ora.staleness(rows) == 0)
+    pr.compare_rows(rows)
+    pr.close()
