@@ -838,17 +838,33 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
     l_own += owner[kk] ? cnt[kk] : 0u;
   }
 
-  // repeated groups: index them, then list their entries contiguously
-  uint32_t ndup, nlanes;
-  uint32_t dpre = block_exclusive_scan<NT>(n_own, s_w, &ndup);
-  uint32_t lpre = block_exclusive_scan<NT>(l_own, s_w, &nlanes);
+  // repeated groups: index them, then list their entries contiguously. The
+  // in-tile sums below take one work item per repeated key, or, for a key
+  // with more than kSumChunk entries, one per chunk of kSumChunk entries.
+  constexpr int UNR = (K * VEC >= 16) ? 2 : (K * VEC >= 8) ? 4 : 8;  // rows loaded together
+  constexpr uint32_t kSumChunk = 2 * UNR;
+  auto n_items = [](uint32_t c) { return c <= kSumChunk ? 1u : (c + kSumChunk - 1) / kSumChunk; };
+  uint32_t w_own = 0;
+#pragma unroll
+  for (int kk = 0; kk < KPT; ++kk) w_own += owner[kk] ? n_items(cnt[kk]) : 0u;
+  // one scan for the three prefixes, packed 10 | 11 | 11 bits (a tile holds
+  // at most 512 repeated keys and 1024 entries, so no field overflows)
+  static_assert(kPutTile <= 1024, "packed prefix fields");
+  uint32_t ptot;
+  const uint32_t ppre = block_exclusive_scan<NT>(n_own | (l_own << 10) | (w_own << 21), s_w, &ptot);
+  const uint32_t ndup = ptot & 0x3FFu, nlanes = (ptot >> 10) & 0x7FFu, nwork = ptot >> 21;
+  uint32_t dpre = ppre & 0x3FFu, lpre = (ppre >> 10) & 0x7FFu, wpre = ppre >> 21;
+  uint32_t my_d[KPT], my_w[KPT];
 #pragma unroll
   for (int kk = 0; kk < KPT; ++kk) {
+    my_d[kk] = dpre;
+    my_w[kk] = wpre;
     if (owner[kk]) {
       s_hdup[hs[kk]] = (uint16_t)dpre;
       s_doff[dpre] = (uint16_t)lpre;
       ++dpre;
       lpre += cnt[kk];
+      wpre += n_items(cnt[kk]);
     }
   }
   if (tid == 0) s_doff[ndup] = (uint16_t)nlanes;
@@ -863,6 +879,12 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
     }
   }
   lds_barrier();
+  // first work item of each repeated key (the fill cursors are no longer needed)
+  uint16_t* s_wfirst = reinterpret_cast<uint16_t*>(s_hcur);
+#pragma unroll
+  for (int kk = 0; kk < KPT; ++kk)
+    if (owner[kk]) s_wfirst[my_d[kk]] = (uint16_t)my_w[kk];
+  if (tid == 0) s_wfirst[ndup] = (uint16_t)nwork;
   // sort each repeated group's entry list: an entry's rank is the number of
   // smaller entries in its group's list
   uint32_t rank[KPT];
@@ -881,16 +903,44 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
   lds_barrier();
 
   // each lane group sums the rows of repeated keys, positions ascending (an
-  // assignment needs no sum: its item is the key's last position instead)
+  // assignment needs no sum: its item is the key's last position instead).
+  // Work items are dealt to the groups in turn. A key of at most kSumChunk
+  // entries leaves its fp64 sum over the partials row of its first entry; a
+  // longer key's chunks leave partial sums over the rows of their own first
+  // entries (the first chunk over the key's second entry), which are added
+  // in chunk order at the end of the kernel.
+  const int lane = tid & 63;
+  const int g = lane / LPR;
+  const int q = lane % LPR;
+  const int gid = (tid >> 6) * RPW + g;
+  const bool chunked = nwork > ndup;  // some key has more than kSumChunk entries
+  double acc[K][VEC];
+  auto store_row = [&](uint32_t entry) {
+    double* dst = partials + (size_t)(base + s_lanes[entry]) * (size_t)D;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int col = (k * LPR + q) * VEC;
+#pragma unroll
+      for (int v = 0; v < VEC; ++v)
+        if (col + v < D) dst[col + v] = acc[k][v];
+    }
+  };
   if (op != kOpAssign) {
-    constexpr int UNR = (K * VEC >= 16) ? 2 : (K * VEC >= 8) ? 4 : 8;
-    const int lane = tid & 63;
-    const int g = lane / LPR;
-    const int q = lane % LPR;
-    const int gid = (tid >> 6) * RPW + g;
-    for (uint32_t dg = gid; dg < ndup; dg += NG) {
-      const uint32_t b = s_doff[dg], e = s_doff[dg + 1];
-      double acc[K][VEC];
+    for (uint32_t w = gid; w < nwork; w += NG) {
+      uint32_t d = w, c = 0;
+      if (chunked) {  // the key of item w: last d with s_wfirst[d] <= w
+        uint32_t dh = ndup;
+        d = 0;
+        while (d + 1 < dh) {
+          const uint32_t mid = (d + dh) >> 1;
+          if (s_wfirst[mid] <= w) d = mid;
+          else dh = mid;
+        }
+        c = w - s_wfirst[d];
+      }
+      const uint32_t kb = s_doff[d], kend = s_doff[d + 1];
+      const bool whole = kend - kb <= kSumChunk;
+      const uint32_t b = kb + c * kSumChunk, e = whole ? kend : min(b + kSumChunk, kend);
 #pragma unroll
       for (int k = 0; k < K; ++k)
 #pragma unroll
@@ -922,14 +972,7 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
           }
         }
       }
-      double* dst = partials + (size_t)(base + s_lanes[b]) * (size_t)D;
-#pragma unroll
-      for (int k = 0; k < K; ++k) {
-        const int col = (k * LPR + q) * VEC;
-#pragma unroll
-        for (int v = 0; v < VEC; ++v)
-          if (col + v < D) dst[col + v] = acc[k][v];
-      }
+      store_row(whole ? kb : (c == 0 ? kb + 1 : b));
     }
   }
 
@@ -1006,6 +1049,29 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
     if (emit[kk])
       items[(size_t)sbase + s_hist[d[kk]] + r[kk]] = dup[kk] && op != kOpAssign ? (x[kk] | kItemSummed) : x[kk];
   if (tid == 0) tile_cnt[tile] = s_cnt;
+  // keys summed in chunks: add the chunks' partial sums in order
+  if (op != kOpAssign && chunked) {
+    __syncthreads();
+    for (uint32_t d = gid; d < ndup; d += NG) {
+      const uint32_t kb = s_doff[d], kend = s_doff[d + 1];
+      if (kend - kb <= kSumChunk) continue;
+#pragma unroll
+      for (int k = 0; k < K; ++k)
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) acc[k][v] = 0.0;
+      for (uint32_t b = kb; b < kend; b += kSumChunk) {
+        const double* src = partials + (size_t)(base + s_lanes[b == kb ? kb + 1 : b]) * (size_t)D;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const int col = (k * LPR + q) * VEC;
+#pragma unroll
+          for (int v = 0; v < VEC; ++v)
+            if (col + v < D) acc[k][v] += src[col + v];
+        }
+      }
+      store_row(kb);
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
