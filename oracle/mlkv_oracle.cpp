@@ -52,6 +52,12 @@
 //       get is served (the asynchronous end, bound = infinity). Waiting is
 //       left to the caller, which repeats a blocked get after the puts it
 //       waits for.
+//   R9  Lookahead(keys) (Sec. III-A; look-ahead prefetching, Sec. III-C2)
+//       with the whole table in memory: the keys are made resident ahead of
+//       the gets that will read them, i.e. the missing ones are inserted as
+//       in R1 with their initial rows; nothing is returned, and no staleness
+//       count changes (a prefetched record keeps its staleness; a new one
+//       starts at 0).
 //
 // Storage is deliberately naive: std::unordered_map for key -> row, a sorted
 // array for a bulk prefill (identical result to inserting the same ascending
@@ -279,6 +285,14 @@ int oracle_get_bounded(oracle_table* h, const uint64_t* keys, int64_t n, float* 
       for (int32_t c = 0; c < t.dim; ++c) out[i * t.dim + c] = read_elem(t, rows[(size_t)i], c);
   }
   return kOk;
+}
+
+// Lookahead (R9): insert the missing keys (R1, R5); no output, no counts.
+int oracle_lookahead(oracle_table* h, const uint64_t* keys, int64_t n) {
+  Table& t = *reinterpret_cast<Table*>(h);
+  int rc = check_keys(keys, n);
+  if (rc != kOk) return rc;
+  return resolve(t, keys, n, nullptr);
 }
 
 // Rmw with "sum duplicates, then row-wise Adagrad" (R3, R4).

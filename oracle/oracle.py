@@ -50,6 +50,7 @@ def _load():
         "oracle_open_bounded": (P, [I32, I64, U64, I64]),
         "oracle_get_bounded": (ctypes.c_int, [P, P, I64, P, P]),
         "oracle_staleness": (ctypes.c_int, [P, P, I64, P]),
+        "oracle_lookahead": (ctypes.c_int, [P, P, I64]),
         "oracle_close": (None, [P]),
         "oracle_size": (I64, [P]),
         "oracle_init_value": (F32, [U64, U64, I32]),
@@ -141,6 +142,11 @@ class OracleTable:
         blocked = np.zeros(k.size, dtype=np.uint8)
         rc = self._lib.oracle_get_bounded(self._h, _ptr(k), k.size, _ptr(out), _ptr(blocked))
         return rc, out, blocked
+
+    def lookahead(self, keys) -> int:
+        """Insert the missing keys ahead of their gets; no output, no counts."""
+        k = _keys(keys)
+        return self._lib.oracle_lookahead(self._h, _ptr(k), k.size)
 
     def staleness(self, rows):
         """Per-row staleness counts (gets served not yet matched by a put)."""

@@ -538,3 +538,35 @@ def test_staleness_blocked_rows_are_untouched_and_counts_floor_at_zero():
     assert t3.get_bounded(np.array([1, 2], np.uint64))[0] == O.OK
     assert t3.get_bounded(np.array([1, 5, 6], np.uint64))[0] == O.EFULL
     assert list(t3.staleness([0, 1])) == [1, 1] and t3.size == 2
+
+
+# --------------------------------------------------------------------------
+# Lookahead with the table in memory: insert ahead, count nothing
+# --------------------------------------------------------------------------
+def test_lookahead_then_get_equals_get_alone_and_moves_no_count():
+    rng = np.random.default_rng(21)
+    keys = rng.integers(0, 500, size=800).astype(np.uint64)
+    later = rng.integers(0, 700, size=600).astype(np.uint64)
+    a = O.OracleTable(4, 2000)
+    b = O.OracleTable(4, 2000)
+    assert a.get(keys)[0] == O.OK and b.get(keys)[0] == O.OK
+    # rows of the keys a lookahead inserts: the R1 rule on the lookahead's
+    # own batch (ascending among its missing keys), the same as an
+    # insert-only get
+    assert a.lookahead(later) == O.OK
+    assert b.get(later, want_out=False)[0] == O.OK
+    assert a.size == b.size
+    assert np.array_equal(a.lookup_rows(later), b.lookup_rows(later))
+    assert np.array_equal(a.get(later)[1], b.get(later)[1])
+    # bounded table: a lookahead neither blocks nor counts
+    t = O.OracleTable(4, 2000, staleness_bound=0)
+    k = np.array([1, 2, 3], np.uint64)
+    assert t.lookahead(k) == O.OK
+    assert list(t.staleness(t.lookup_rows(k))) == [0, 0, 0]
+    assert not t.get_bounded(k)[2].any()
+    assert t.lookahead(k) == O.OK
+    assert list(t.staleness(t.lookup_rows(k))) == [1, 1, 1]
+    # failures leave the table unchanged
+    full = O.OracleTable(4, 3)
+    assert full.lookahead(np.array([1, 2, 3, 4], np.uint64)) == O.EFULL and full.size == 0
+    assert full.lookahead(np.array([1, 2**64 - 1], np.uint64)) == O.EINVAL
