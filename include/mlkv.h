@@ -98,6 +98,15 @@ int mlkv_get(mlkv_table *t, const uint64_t *d_keys, int64_t n, float *d_out, voi
 int mlkv_get_bounded(mlkv_table *t, const uint64_t *d_keys, int64_t n, float *d_out, uint8_t *d_blocked,
                      void *hip_stream);
 
+/* Lookahead (Sec. III-A; look-ahead prefetching, Sec. III-C2) with the whole
+ * table in HBM: makes d_keys resident ahead of the gets that will read them,
+ * i.e. inserts the missing keys exactly as mlkv_get with d_out = NULL would
+ * (rows in ascending key order, seeded initial rows), and returns nothing.
+ * It never blocks and changes no staleness count (a new key starts at 0).
+ * A table larger than HBM, which would make this a copy from host memory,
+ * is not supported. 0 <= n <= 2^31 - 1; errors as for mlkv_get. */
+int mlkv_lookahead(mlkv_table *t, const uint64_t *d_keys, int64_t n, void *hip_stream);
+
 /* Rmw (Sec. III-B, step 8) with row-wise Adagrad as the modify function:
  * missing keys are inserted as in mlkv_get; then for every distinct key k of
  * the batch, with positions i_1 < i_2 < ... holding k,

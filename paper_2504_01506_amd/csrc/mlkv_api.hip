@@ -304,16 +304,18 @@ void mlkv_close(mlkv_table* t) {
 namespace {
 
 // The get pipeline (probe + gather, then rows for new keys); d_blocked is
-// written when the table has a staleness bound.
+// written when the table has a staleness bound and the call counts (a
+// lookahead does not).
 int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uint8_t* d_blocked,
-             void* hip_stream) {
+             bool count, void* hip_stream) {
   int rc = check_table(t);
   if (rc) return rc;
   if (n < 0 || n > 0x7FFFFFFFll) return fail(MLKV_EINVAL, "n must be in [0, 2^31 - 1]");
   if (n == 0) return MLKV_OK;
   if (d_keys == nullptr) return fail(MLKV_EINVAL, "keys is NULL");
-  if (t->clock != nullptr && d_blocked == nullptr) return fail(MLKV_EINVAL, "blocked is NULL");
-  if (t->clock != nullptr && t->cepoch >= (1ull << (64 - kClockBits)))
+  const bool track = count && t->clock != nullptr;
+  if (track && d_blocked == nullptr) return fail(MLKV_EINVAL, "blocked is NULL");
+  if (track && t->cepoch >= (1ull << (64 - kClockBits)))
     return fail(MLKV_EINVAL, "the table has served 2^40 get calls, the most a bounded table counts");
   if ((rc = ensure_workspace(t, n)) != MLKV_OK) return rc;
   GetArgs a;
@@ -333,7 +335,7 @@ int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uin
   a.epoch = t->epoch;
   a.xkey = t->items;  // the put pipeline's scratch (at least n entries each), idle during a get
   a.xslot = t->meta;
-  a.clock = t->clock;
+  a.clock = track ? t->clock : nullptr;
   a.cepoch = t->cepoch;
   a.bound = (uint32_t)std::max<int64_t>(t->bound, 0);
   a.blocked = d_blocked;
@@ -341,7 +343,7 @@ int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uin
   hipError_t e = launch_get(a, vec4, static_cast<hipStream_t>(hip_stream), hook_of(t));
   if (e != hipSuccess) return hip_fail(e, "mlkv_get launch");
   t->epoch++;
-  if (t->clock != nullptr) t->cepoch++;
+  if (track) t->cepoch++;
   return MLKV_OK;
 }
 
@@ -352,14 +354,18 @@ extern "C" {
 int mlkv_get(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, void* hip_stream) {
   if (t != nullptr && t->clock != nullptr)
     return fail(MLKV_EINVAL, "the table has a staleness bound: use mlkv_get_bounded");
-  return get_call(t, d_keys, n, d_out, nullptr, hip_stream);
+  return get_call(t, d_keys, n, d_out, nullptr, true, hip_stream);
+}
+
+int mlkv_lookahead(mlkv_table* t, const uint64_t* d_keys, int64_t n, void* hip_stream) {
+  return get_call(t, d_keys, n, nullptr, nullptr, false, hip_stream);
 }
 
 int mlkv_get_bounded(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uint8_t* d_blocked,
                      void* hip_stream) {
   if (t != nullptr && t->clock == nullptr)
     return fail(MLKV_EINVAL, "the table has no staleness bound: use mlkv_get");
-  return get_call(t, d_keys, n, d_out, d_blocked, hip_stream);
+  return get_call(t, d_keys, n, d_out, d_blocked, true, hip_stream);
 }
 
 int mlkv_read_staleness(mlkv_table* t, const int64_t* d_rows, int64_t n, uint32_t* d_out, void* hip_stream) {

@@ -46,6 +46,7 @@ def load() -> ctypes.CDLL:
         "mlkv_open_bounded": (P, [I32, I64, U64, F32, I64]),
         "mlkv_get": (INT, [P, P, I64, P, P]),
         "mlkv_get_bounded": (INT, [P, P, I64, P, P, P]),
+        "mlkv_lookahead": (INT, [P, P, I64, P]),
         "mlkv_read_staleness": (INT, [P, P, I64, P, P]),
         "mlkv_put_grad": (INT, [P, P, P, I64, F32, F32, P]),
         "mlkv_put_grad_sgd": (INT, [P, P, P, I64, F32, P]),
@@ -133,6 +134,10 @@ def mlkv_get(t: int, keys, n: int, out, stream=None) -> int:
 
 def mlkv_get_bounded(t: int, keys, n: int, out, blocked, stream=None) -> int:
     return load().mlkv_get_bounded(t, _ptr(keys), n, _ptr(out), _ptr(blocked), _stream(stream))
+
+
+def mlkv_lookahead(t: int, keys, n: int, stream=None) -> int:
+    return load().mlkv_lookahead(t, _ptr(keys), n, _stream(stream))
 
 
 def mlkv_read_staleness(t: int, rows, n: int, out, stream=None) -> int:
@@ -239,6 +244,10 @@ class Table:
             blocked = torch.empty(keys.numel(), dtype=torch.uint8, device=keys.device)
         _check(mlkv_get_bounded(self.h, keys, keys.numel(), out, blocked, stream))
         return blocked
+
+    def lookahead(self, keys: torch.Tensor, stream=None):
+        """Insert the missing keys ahead of their gets (no output, no staleness count)."""
+        _check(mlkv_lookahead(self.h, keys, keys.numel(), stream))
 
     def read_staleness(self, rows: torch.Tensor, stream=None) -> torch.Tensor:
         """Staleness counts (int32 view of uint32) of the given row ids (int64)."""

@@ -107,6 +107,15 @@ class Pair:
         assert np.all(got[~served] == sentinel), "a blocked position was written"
         return bl
 
+    def lookahead(self, keys: np.ndarray):
+        """Lookahead on both sides; key -> row of the batch and the size must agree."""
+        self.gpu.lookahead(dev_keys(keys))
+        assert self.ora.lookahead(keys) == O.OK
+        assert self.gpu.sync() == mlkv.MLKV_OK
+        assert self.gpu.size == self.ora.size
+        got = self.gpu.lookup_rows(dev_keys(keys)).cpu().numpy()
+        assert np.array_equal(got, self.ora.lookup_rows(keys)), "key -> row differs after lookahead"
+
     def compare_staleness(self):
         """Staleness counts of every row, bit-exact."""
         rows = np.arange(self.ora.size, dtype=np.int64)

@@ -66,6 +66,7 @@ def test_host_side_validation_without_a_gpu(lib):
     assert lib.mlkv_open_bounded(16, 100, 1, 0.5, 2**24 - 1) is None
     assert lib.mlkv_get_bounded(None, None, 10, None, None, None) == mlkv.MLKV_EINVAL
     assert lib.mlkv_read_staleness(None, None, 10, None, None) == mlkv.MLKV_EINVAL
+    assert lib.mlkv_lookahead(None, None, 10, None) == mlkv.MLKV_EINVAL
     lib.mlkv_close(None)  # no-op
 
 

@@ -1,7 +1,7 @@
 """Random call sequences on the GPU and the CPU oracle side by side.
 
 Each sequence draws a row width, a capacity, optionally a staleness bound,
-and 30 calls, each one of: get (with or without an output), put_grad,
+and 30 calls, each one of: get (with or without an output), lookahead, put_grad,
 put_grad_sgd, put (upsert), a get whose new keys overflow the capacity, or a
 call holding the reserved key. Batch lengths cover the tile boundaries
 (1, 63..65, 255..257, 1023..1025) and random lengths; keys mix present keys,
@@ -55,7 +55,8 @@ def test_random_call_sequences(seed):
     space = int(rng.choice([cap // 8, cap // 2, 4 * cap]))  # many repeats .. mostly new keys
     counts = {}
     for step in range(30):
-        op = str(rng.choice(["get", "get", "get_null", "put_grad", "put_grad", "put_sgd", "put", "over", "bad"]))
+        op = str(rng.choice(["get", "get", "get_null", "lookahead", "put_grad", "put_grad", "put_sgd", "put",
+                             "over", "bad"]))
         n = int(rng.choice(LENGTHS)) if rng.random() < 0.6 else int(rng.integers(1, 20000))
         size = pr.ora.size
         if op == "over":
@@ -91,6 +92,8 @@ def test_random_call_sequences(seed):
                 pr.get(keys)
             else:
                 pr.get_bounded(keys)
+        elif op == "lookahead":
+            pr.lookahead(keys)
         elif op == "get_null":
             assert _raw_get(pr, keys) == mlkv.MLKV_OK
             assert _ora_get(pr, keys) == O.OK

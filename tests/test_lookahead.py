@@ -1,0 +1,61 @@
+"""Lookahead with the table in HBM (insert ahead of the gets, no output, no
+staleness count) on the GPU against the CPU oracle.
+
+Bar: key -> row and size bit-exact after every call; rows of keys inserted
+ahead equal their initial values bit for bit when read by a later get;
+staleness counts unchanged by a lookahead; failures leave the table as it was.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2504_01506_amd import mlkv
+from _harness import Pair, dev_keys, log
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("bound", [None, 0])
+@pytest.mark.parametrize("m", [1, 700, 20_000, 300_000])
+def test_lookahead_then_steps(bound, m):
+    # m keys looked ahead (few, one block's worth, key ranges), then gets and
+    # puts that find them present
+    rng = np.random.default_rng(m + (0 if bound is None else 1))
+    dim = 16
+    pr = Pair(dim, 2 * m + 10_000, staleness_bound=bound)
+    keys = rng.choice(np.uint64(1) << np.uint64(50), size=m, replace=False).astype(np.uint64)
+    batch = np.concatenate([keys, keys[: m // 3]])
+    rng.shuffle(batch)
+    pr.lookahead(batch)
+    if bound is not None:
+        assert not pr.compare_staleness().any()
+    pr.lookahead(batch[: m // 2 + 1])   # all present: nothing changes
+    for s in range(2):
+        k = batch[rng.integers(0, batch.size, size=min(batch.size, 5000))]
+        if bound is None:
+            pr.get(k)
+        else:
+            assert not pr.get_bounded(k).any()
+        pr.put(k, rng.normal(0, 0.01, size=(k.size, dim)).astype(np.float32), 0.01, 1e-8)
+    pr.compare_rows()
+    pr.check_index()
+    if bound is not None:
+        pr.compare_staleness()
+    log(f"[lookahead] m {m} bound {bound}: size {pr.ora.size} stats={pr.stats}")
+    pr.close()
+
+
+def test_failed_lookahead_leaves_the_table_unchanged():
+    pr = Pair(4, 100, staleness_bound=1)
+    pr.get_bounded(np.arange(1, 51, dtype=np.uint64))
+    before = pr.compare_staleness()
+    k = dev_keys(np.arange(1000, 1100, dtype=np.uint64))       # 100 new keys, 50 fit
+    assert mlkv.mlkv_lookahead(pr.gpu.h, k, 100) == mlkv.MLKV_OK
+    assert pr.gpu.sync() == mlkv.MLKV_EFULL
+    bad = np.array([3, 7, mlkv.MLKV_RESERVED_KEY], np.uint64)
+    assert mlkv.mlkv_lookahead(pr.gpu.h, dev_keys(bad), 3) == mlkv.MLKV_OK
+    assert pr.gpu.sync() == mlkv.MLKV_EINVAL
+    assert pr.gpu.size == 50
+    assert np.array_equal(pr.compare_staleness(), before)
+    pr.check_index()
+    pr.close()
