@@ -367,15 +367,33 @@ __device__ __forceinline__ void rollback_clocks(unsigned long long* __restrict__
 }
 
 // Initial rows of new keys ks[j] (j < m) at rows base + rk[j]: a wave per
-// row, its lanes along the row.
+// row, its lanes along the row, kInitRows rows of a wave at a time so that
+// each lane has that many independent hash chains in flight (the 64-bit
+// multiplies of one chain are serial).
+constexpr int kInitRows = 4;
 template <int NT, class KP, class RP>
 __device__ __forceinline__ void write_init_rows(const KP ks, const RP rk, uint32_t m, uint64_t base,
                                                 float* __restrict__ rows, int D, uint64_t seed) {
+  constexpr uint32_t NW = NT / 64;
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (uint32_t j = wave; j < m; j += NT / 64) {
-    float* w = rows + (base + rk[j]) * (uint64_t)D;
-    const uint64_t s0 = splitmix_mix(ks[j] ^ seed);
-    for (int col = (int)lane; col < D; col += 64) w[col] = init_elem(s0, col);
+  for (uint32_t j0 = wave; j0 < m; j0 += NW * kInitRows) {
+    float* w[kInitRows];
+    uint64_t s0[kInitRows];
+#pragma unroll
+    for (int r = 0; r < kInitRows; ++r) {
+      const uint32_t j = j0 + (uint32_t)r * NW;
+      w[r] = nullptr;
+      s0[r] = 0;
+      if (j < m) {
+        w[r] = rows + (base + rk[j]) * (uint64_t)D;
+        s0[r] = splitmix_mix(ks[j] ^ seed);
+      }
+    }
+    for (int col = (int)lane; col < D; col += 64) {
+#pragma unroll
+      for (int r = 0; r < kInitRows; ++r)
+        if (w[r] != nullptr) w[r][col] = init_elem(s0[r], col);
+    }
   }
 }
 
