@@ -182,7 +182,8 @@ int mlkv_read_staleness(mlkv_table *t, const int64_t *d_rows, int64_t n, uint32_
 
 /* ---- per-kernel timing (benchmarks) ----
  * The library runs MLKV_NUM_KERNELS kernels: 0 get_probe_gather and
- * 1 assign_new for mlkv_get; 2 put_probe, 3 put_group and 4 put_apply for
+ * 1 assign_new for mlkv_get, mlkv_get_bounded and mlkv_lookahead;
+ * 2 put_probe, 3 put_group and 4 put_apply for
  * mlkv_put_grad, mlkv_put_grad_sgd and mlkv_put. While enabled, HIP events are recorded on
  * the call's stream before and after every launch. mlkv_profile_read waits
  * for the recorded launches, writes per-kernel sums of their durations (ms)
