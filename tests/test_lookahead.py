@@ -16,12 +16,11 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("bound", [None, 0])
-@pytest.mark.parametrize("m", [1, 700, 20_000, 300_000])
-def test_lookahead_then_steps(bound, m):
+@pytest.mark.parametrize("m,dim", [(1, 16), (700, 1), (700, 1024), (20_000, 16), (300_000, 16), (300_000, 7)])
+def test_lookahead_then_steps(bound, m, dim):
     # m keys looked ahead (few, one block's worth, key ranges), then gets and
     # puts that find them present
-    rng = np.random.default_rng(m + (0 if bound is None else 1))
-    dim = 16
+    rng = np.random.default_rng(m + dim + (0 if bound is None else 1))
     pr = Pair(dim, 2 * m + 10_000, staleness_bound=bound)
     keys = rng.choice(np.uint64(1) << np.uint64(50), size=m, replace=False).astype(np.uint64)
     batch = np.concatenate([keys, keys[: m // 3]])
