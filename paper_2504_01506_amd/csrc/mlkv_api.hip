@@ -111,6 +111,15 @@ uint32_t part_bits(int64_t n) {
   return pb;
 }
 
+// Partitions used by a put call: as part_bits (never more, so the scratch
+// sized by part_bits suffices), but one partition per CU, up to twice the
+// target each, when that keeps put_group's blocks to one round.
+uint32_t call_part_bits(int64_t n, int cus) {
+  uint32_t pb = part_bits(n);
+  if (pb > 0 && (1 << pb) > cus && (1 << (pb - 1)) >= cus && (int64_t)(2 * kPartTarget) * cus >= n) --pb;
+  return pb;
+}
+
 // Scratch for calls of up to n keys: new-key lists, per-tile counts, the
 // partitioned items, partition metadata, the spill area, in-tile sums and the
 // grouped partitions handed to the flat put kernels.
@@ -398,7 +407,7 @@ int put_call(mlkv_table* t, const uint64_t* d_keys, const float* src, int64_t n,
   if (n == 0) return MLKV_OK;
   if (d_keys == nullptr || src == nullptr) return fail(MLKV_EINVAL, "keys or rows is NULL");
   if ((rc = ensure_workspace(t, n)) != MLKV_OK) return rc;
-  const uint32_t pb = part_bits(n);
+  const uint32_t pb = call_part_bits(n, t->flat_blocks);
   // keys per put_probe tile: a multiple of 64, at most kPutTile, so that the
   // tiles cover every CU when the batch is small
   const int64_t per_cu = (n + t->flat_blocks - 1) / t->flat_blocks;
