@@ -260,7 +260,13 @@ __device__ __forceinline__ int call_verdict(Ctrl* ctrl, uint64_t epoch, uint64_t
 constexpr int kAssignThreads = 256;
 constexpr int kAssignBatch = 8;
 constexpr int kAssignMine = kAssignBatch * kAssignThreads;
-constexpr int kAssignDirect = 8192;  // up to this many new keys, each block ranks its tiles' keys against all
+// With few new keys each block ranks its tiles' keys against all of them,
+// streamed through LDS once per NT tiles of the call: about 13 us plus 44 ns
+// per (new key x NT tiles) on MI355X (55 us at 256 new keys of a 213k-key,
+// 832-tile batch; 1.4 ms at 8192), while key ranges take 44-50 us from a few
+// hundred keys up. The direct ranking is used up to kAssignDirectWork new
+// keys x tile chunks.
+constexpr uint64_t kAssignDirectWork = 768;
 constexpr int kRangeSamples = 2048;  // sample of the new keys that splits the key space among the blocks
 constexpr int kRangeCap = 3072;      // keys of a block's key range ranked in LDS at once
 
@@ -303,7 +309,7 @@ __device__ __forceinline__ uint64_t search_tile_lists(const NewKey* __restrict__
   return below;
 }
 
-// Ascending bitonic sort of NT * kSortPT distinct keys, thread t holding the
+// Ascending bitonic sort of NT * kSortPT keys, thread t holding the
 // elements kSortPT t .. kSortPT t + kSortPT - 1 in v. Compare-exchanges whose
 // partner lies in the same thread run in registers; the others exchange
 // through LDS, alternating between buf0 and buf1 (NT * kSortPT keys each), so
@@ -449,7 +455,7 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
     return;
   }
 
-  if (M > (uint64_t)kAssignDirect) {
+  if (M * (uint64_t)((ntiles + NT - 1) / NT) > kAssignDirectWork) {
     // ---- many new keys: key ranges. Every block takes the same sample of the
     // new keys (sample k is the new key at position floor(k M / S) of the
     // tiles' lists laid end to end) and the same cut points from it, which
@@ -482,8 +488,9 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
 #pragma unroll
     for (uint32_t u = 0; u < kSortPT; ++u) v[u] = newlist[s_sat[threadIdx.x + u * NT]].key;
     // the cut points: the samples of rank g S / G and (g + 1) S / G of the
-    // sorted sample (samples are distinct keys, so ranks are too); eight
-    // sample gaps per range keep the largest range near twice the mean
+    // sorted sample (with fewer new keys than samples a key is sampled more
+    // than once, and equal cut points give an empty range); eight sample
+    // gaps per range keep the largest range near twice the mean
     const uint32_t g = blockIdx.x, G = gridDim.x;
     sort_keys_8pt<NT>(v, s_buf, s_buf + S);
     {

@@ -106,10 +106,14 @@ def test_put_inserts_unseen_keys_then_updates_them():
     pr.close()
 
 
-@pytest.mark.parametrize("n_new,n", [(8193, 8193), (9000, 9000), (10_000, 65_536), (20_000, 300_000)])
+# direct ranking up to 768 new keys x chunks of 256 get tiles: 768 for a
+# batch of up to 65,536 keys, 192 for 213k keys (832 tiles)
+@pytest.mark.parametrize("n_new,n", [(1, 213_000), (192, 213_000), (193, 213_000), (768, 768), (769, 769),
+                                     (1000, 1000), (4096, 213_000), (8193, 8193), (20_000, 300_000)])
 def test_new_keys_just_past_the_direct_ranking(n_new, n):
-    """Calls with a little more than 8192 new keys, few blocks or many blocks
-    each with a small key range (one local sub-range), hits mixed in."""
+    """Calls on either side of the limit of the direct ranking,
+    few blocks or many blocks each with a small key range (one local
+    sub-range, or none: fewer new keys than samples), hits mixed in."""
     rng = np.random.default_rng(n_new + n)
     dim = 3
     pr = Pair(dim, n + n_new + 10)
