@@ -1282,16 +1282,22 @@ __device__ __forceinline__ uint32_t encode_segments(IP it, uint32_t mp, SP seg, 
   return S;
 }
 
-// Keys first inserted by this call get rows size0 + rank among all new keys
-// of the call; the row replaces the slot in the segment's first item, whose
-// "fresh" bit stays set. The new row starts from its initial value and a zero
-// accumulator.
+// Keys new in this call (fresh items) get their rows: row = size + rank of
+// the key among all new keys of the call. The block's new keys (up to NT at a
+// time) are sorted in LDS; every new key of the call, streamed through LDS,
+// adds one to the count of the first of them above it, and a key's rank is
+// the sum of the counts up to its own position. Initial row and zero
+// accumulator are written, and the row replaces the slot in the segment's
+// first item, whose "fresh" bit stays set. s_chunk: at least (kChunk + NT)
+// 64-bit words plus NT + 1 32-bit words of LDS.
 template <int NT, class IP, class SP>
 __device__ __forceinline__ void resolve_new_rows(IP it, SP seg, uint32_t S, const RedCtx& c,
                                                  const NewKey* __restrict__ newlist,
                                                  const uint32_t* __restrict__ tile_cnt, int ntiles,
                                                  uint32_t* s_pref, uint32_t* s_w,
                                                  unsigned long long* s_w64, uint64_t* s_chunk) {
+  uint64_t* s_pk = s_chunk + kChunk;                          // [NT] the batch's new keys, sorted
+  uint32_t* s_cnt = reinterpret_cast<uint32_t*>(s_pk + NT);  // [NT + 1] counts, then their prefix
   for (uint32_t s0 = 0; s0 < S; s0 += NT) {
     const uint32_t s = s0 + threadIdx.x;
     bool pend = false;
@@ -1302,16 +1308,46 @@ __device__ __forceinline__ void resolve_new_rows(IP it, SP seg, uint32_t S, cons
       pend = item_fresh(x);
       slot = item_tag(x);
     }
-    const uint64_t npend = block_sum_u64<NT>(pend ? 1u : 0u, s_w64);
-    if (npend == 0) continue;
+    uint32_t np;
+    const uint32_t pi = block_exclusive_scan<NT>(pend ? 1u : 0u, s_w, &np);
+    if (np == 0) continue;
     const uint64_t key = pend ? c.idx[slot / kSlots].key[slot % kSlots] : 0ull;
-    uint32_t rank = 0;
+    uint32_t np2 = 1;
+    while (np2 < np) np2 <<= 1;
+    for (uint32_t j = threadIdx.x; j < np2; j += NT) s_pk[j] = kEmptyKey;  // no key equals it
+    for (uint32_t j = threadIdx.x; j <= np; j += NT) s_cnt[j] = 0;
+    __syncthreads();
+    if (pend) s_pk[pi] = key;
+    __syncthreads();
+    block_bitonic_sort<NT>(s_pk, np2);
     for_each_new_key_chunk<NT>(newlist, tile_cnt, ntiles, kPutTile, s_pref, s_w, s_chunk,
                                [&](const uint64_t* ck, uint32_t cnt) {
-                                 if (pend)
-                                   for (uint32_t e = 0; e < cnt; ++e) rank += ck[e] < key ? 1u : 0u;
+                                 for (uint32_t e = threadIdx.x; e < cnt; e += NT) {
+                                   const uint64_t xk = ck[e];
+                                   uint32_t lo = 0, hi = np;  // first pending key above xk
+                                   while (lo < hi) {
+                                     const uint32_t mid = (lo + hi) >> 1;
+                                     if (s_pk[mid] <= xk) lo = mid + 1;
+                                     else hi = mid;
+                                   }
+                                   if (lo < np) atomicAdd(&s_cnt[lo], 1u);
+                                 }
                                });
+    {
+      const uint32_t v = threadIdx.x < np ? s_cnt[threadIdx.x] : 0u;
+      uint32_t tot;
+      const uint32_t ex = block_exclusive_scan<NT>(v, s_w, &tot);
+      if (threadIdx.x < np) s_cnt[threadIdx.x] = ex + v;  // new keys below the key at this position
+      __syncthreads();
+    }
     if (pend) {
+      uint32_t lo = 0, hi = np - 1;  // the key's own position
+      while (lo < hi) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (s_pk[mid] < key) lo = mid + 1;
+        else hi = mid;
+      }
+      const uint32_t rank = s_cnt[lo];
       const uint32_t row = (uint32_t)(c.size0 + rank);
       c.idx[slot / kSlots].row[slot % kSlots] = row;
       it[seg[s]] = make_item(true, row, item_low31(x));
@@ -1320,6 +1356,7 @@ __device__ __forceinline__ void resolve_new_rows(IP it, SP seg, uint32_t S, cons
       for (int col = 0; col < c.D; ++col) w[col] = init_elem(s0k, col);
       c.state[row] = 0.0f;
     }
+    __syncthreads();
   }
   __syncthreads();
 }
@@ -2417,7 +2454,8 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   static_assert((size_t)NG * RedCfg<M>::DMAX * sizeof(double) <= L::reuse,
                 "cut-segment pieces must fit the reused LDS region");
   constexpr int NTA = ApplyCfg<M>::NT;
-  static_assert((size_t)kChunk * sizeof(uint64_t) <= L::reuse, "new-key chunk must fit the reused LDS region");
+  static_assert((size_t)(kChunk + NT) * sizeof(uint64_t) + (size_t)(NT + 1) * sizeof(uint32_t) <= L::reuse,
+                "new-key chunk, sorted new keys and their counts must fit the reused LDS region");
   static_assert(L::total <= 160 * 1024, "LDS budget of a gfx950 workgroup");
   const int64_t ntiles = (a.n + a.tlen - 1) / a.tlen;
   const int np = 1 << a.pb;
