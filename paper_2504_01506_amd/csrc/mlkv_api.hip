@@ -46,6 +46,8 @@ struct mlkv_table {
   uint64_t* gitems = nullptr;
   uint32_t* gdesc = nullptr;
   PartMeta* pmeta = nullptr;
+  uint64_t* pc_key = nullptr;  // the last get's present keys and rows by position
+  uint32_t* pc_row = nullptr;
   int flat_blocks = 256;  // least number of put_apply blocks: one per CU
 
   // optional per-launch timing: HIP events recorded around each kernel
@@ -90,6 +92,10 @@ void free_workspace(mlkv_table* t) {
   (void)hipFree(t->gitems);
   (void)hipFree(t->gdesc);
   (void)hipFree(t->pmeta);
+  (void)hipFree(t->pc_key);
+  (void)hipFree(t->pc_row);
+  t->pc_key = nullptr;
+  t->pc_row = nullptr;
   t->partials = nullptr;
   t->gitems = nullptr;
   t->gdesc = nullptr;
@@ -144,9 +150,17 @@ int ensure_workspace(mlkv_table* t, int64_t n) {
       (e = dev_alloc(&t->items, sizeof(uint64_t) * (size_t)slots)) != hipSuccess ||
       (e = dev_alloc(&t->meta, sizeof(uint32_t) * (size_t)kMaxParts * (size_t)put_tiles)) != hipSuccess ||
       (e = dev_alloc(&t->spill, sizeof(uint64_t) * (size_t)spill_words)) != hipSuccess ||
-      (e = dev_alloc(&t->partials, sizeof(double) * (size_t)want * (size_t)t->dim)) != hipSuccess) {
+      (e = dev_alloc(&t->partials, sizeof(double) * (size_t)want * (size_t)t->dim)) != hipSuccess ||
+      (e = dev_alloc(&t->pc_key, sizeof(uint64_t) * (size_t)slots)) != hipSuccess ||
+      (e = dev_alloc(&t->pc_row, sizeof(uint32_t) * (size_t)slots)) != hipSuccess ||
+      (e = hipMemset(t->pc_key, 0xFF, sizeof(uint64_t) * (size_t)slots)) != hipSuccess) {  // no key cached
     free_workspace(t);
     return hip_fail(e, "scratch allocation");
+  }
+  // the cleared cache must be in place before any stream's kernels read it
+  if ((e = hipDeviceSynchronize()) != hipSuccess) {
+    free_workspace(t);
+    return hip_fail(e, "hipDeviceSynchronize");
   }
   t->ws_n = want;
   t->spill_words = spill_words;
@@ -348,6 +362,8 @@ int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uin
   a.cepoch = t->cepoch;
   a.bound = (uint32_t)std::max<int64_t>(t->bound, 0);
   a.blocked = d_blocked;
+  a.pc_key = t->pc_key;
+  a.pc_row = t->pc_row;
   const bool vec4 = (t->dim % 4 == 0) && (d_out == nullptr || aligned16(d_out));
   hipError_t e = launch_get(a, vec4, static_cast<hipStream_t>(hip_stream), hook_of(t));
   if (e != hipSuccess) return hip_fail(e, "mlkv_get launch");
@@ -442,6 +458,8 @@ int put_call(mlkv_table* t, const uint64_t* d_keys, const float* src, int64_t n,
   a.ctrl = t->ctrl;
   a.epoch = t->epoch;
   a.clock = t->clock;
+  a.pc_key = t->pc_key;
+  a.pc_row = t->pc_row;
   const bool vec4 = (t->dim % 4 == 0) && aligned16(src);
   hipError_t e = launch_put(a, vec4, static_cast<hipStream_t>(hip_stream), hook_of(t));
   if (e != hipSuccess) return hip_fail(e, "put launch");

@@ -76,6 +76,10 @@ struct GetArgs {
   uint64_t cepoch;
   uint32_t bound;
   uint8_t* blocked;
+  // per position: the key found present and its row (the key is the empty
+  // key where the position held no present key); a later put reads them
+  uint64_t* pc_key;
+  uint32_t* pc_row;
 };
 
 struct PutArgs {
@@ -108,6 +112,8 @@ struct PutArgs {
   Ctrl* ctrl;
   uint64_t epoch;
   unsigned long long* clock;  // per-row staleness words, or nullptr when not tracked
+  const uint64_t* pc_key;     // the last get's present keys and rows by position
+  const uint32_t* pc_row;
 };
 
 hipError_t launch_get(const GetArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook);

@@ -113,7 +113,8 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
     Bucket* __restrict__ idx, uint32_t nb_log2, const uint64_t* __restrict__ keys, int64_t n,
     float* __restrict__ out, const float* __restrict__ rows, int D, uint64_t seed,
     NewKey* __restrict__ newlist, uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch,
-    unsigned long long* __restrict__ clock, uint64_t cepoch, uint32_t bound, uint8_t* __restrict__ blocked) {
+    unsigned long long* __restrict__ clock, uint64_t cepoch, uint32_t bound, uint8_t* __restrict__ blocked,
+    uint64_t* __restrict__ pc_key, uint32_t* __restrict__ pc_row) {
   __shared__ uint32_t s_cnt;
   __shared__ uint64_t s_nkey[kGetTile];  // the tile's new keys and their slots
   __shared__ uint32_t s_nslot[kGetTile];
@@ -141,6 +142,12 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
     s_nkey[j] = key;
     s_nslot[j] = pr.slot;
     ctrl->new_epoch = epoch;
+  }
+  // a key present before the call, with its row, for a put of the same
+  // batch: a key's row never changes once assigned, so the pair stays valid
+  if (i < n) {
+    pc_key[i] = pr.status == P_HIT ? key : kEmptyKey;
+    pc_row[i] = pr.row;
   }
   int how = pr.status == P_HIT ? 1 : 0;
   if (kTrack && i < n) {
@@ -775,7 +782,8 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
     const float* __restrict__ grads, int64_t n, int tlen, int D, int op, int pb, int ntiles,
     uint64_t* __restrict__ items,
     uint32_t* __restrict__ meta, double* __restrict__ partials, NewKey* __restrict__ newlist,
-    uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch) {
+    uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch, const uint64_t* __restrict__ pc_key,
+    const uint32_t* __restrict__ pc_row) {
   constexpr int NT = kPutThreads;
   constexpr int KPT = kPutTile / kPutThreads;  // keys per thread
   constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
@@ -810,19 +818,27 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
   // index buckets of the tile's keys are loaded first; while they are in
   // flight the tile's keys are deduplicated in LDS (a key and its slot are
   // one to one), and the probe reads the buckets afterwards.
+  // a key that the last get found present at the same position takes the
+  // row it found there; the others load their home bucket
   uint64_t key[KPT];
   bool inb[KPT];
   uint64_t hb[KPT];
   BucketView bv[KPT];
+  uint64_t ck[KPT];
+  uint32_t crow[KPT];
 #pragma unroll
   for (int kk = 0; kk < KPT; ++kk) {
     const int64_t i = base + kk * NT + tid;
     inb[kk] = kk * NT + tid < tlen && i < n;
     key[kk] = inb[kk] ? keys[i] : kEmptyKey;
+    ck[kk] = inb[kk] ? pc_key[i] : kEmptyKey;
+    crow[kk] = inb[kk] ? pc_row[i] : kPendingRow;
   }
+  bool cached[KPT];
 #pragma unroll
   for (int kk = 0; kk < KPT; ++kk) {
-    if (key[kk] != kEmptyKey) {
+    cached[kk] = key[kk] != kEmptyKey && ck[kk] == key[kk];
+    if (key[kk] != kEmptyKey && !cached[kk]) {
       hb[kk] = home_bucket(key[kk], nb_log2);
       bv[kk] = load_bucket(idx + hb[kk]);
     }
@@ -1006,7 +1022,9 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
 #pragma unroll
   for (int kk = 0; kk < KPT; ++kk) {
     pr[kk] = {0, kPendingRow, inb[kk] ? P_BAD : P_NONE};
-    if (key[kk] != kEmptyKey) {
+    if (cached[kk]) {
+      pr[kk] = {0, crow[kk], P_HIT};
+    } else if (key[kk] != kEmptyKey) {
       pr[kk] = probe_with(idx, nb_log2, key[kk], true, hb[kk], bv[kk]);
       if (pr[kk].status == P_OVERFLOW) ctrl->overflow_epoch = epoch;
     } else if (pr[kk].status == P_BAD) {
@@ -2433,7 +2451,7 @@ static hipError_t launch_get_t(const GetArgs& a, hipStream_t st, const LaunchHoo
   auto kern = a.clock != nullptr ? k_get_probe_gather<M, true> : k_get_probe_gather<M, false>;
   hipLaunchKernelGGL(kern, dim3((unsigned)ntiles), dim3(kGetTile), 0, st, a.idx, a.nb_log2, a.keys, a.n,
                      a.out, a.rows, a.D, a.seed, a.newlist, a.tile_cnt, a.ctrl, a.epoch, a.clock, a.cepoch,
-                     a.bound, a.blocked);
+                     a.bound, a.blocked, a.pc_key, a.pc_row);
   hook(K_GET_PROBE_GATHER, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -2462,7 +2480,7 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   hook(K_PUT_PROBE, 0, st);
   hipLaunchKernelGGL(k_put_probe<M>, dim3((unsigned)ntiles), dim3(kPutThreads), 0, st, a.idx, a.nb_log2,
                      a.keys, a.grads, a.n, a.tlen, a.D, a.op, a.pb, (int)ntiles, a.items, a.meta, a.partials,
-                     a.newlist, a.tile_cnt, a.ctrl, a.epoch);
+                     a.newlist, a.tile_cnt, a.ctrl, a.epoch, a.pc_key, a.pc_row);
   hook(K_PUT_PROBE, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -335,3 +335,24 @@ def test_get_output_equals_exported_rows():
     assert t.sync() == 0
     assert torch.equal(out, w[rows])
     t.close()
+
+
+def test_put_after_get_with_shuffled_and_replaced_positions():
+    """A put reuses the rows its preceding get found, position by position,
+    only where the key is the same: positions holding another present key, a
+    new key, or a key the get inserted must be probed."""
+    rng = np.random.default_rng(31)
+    dim = 8
+    pr = Pair(dim, 50_000)
+    pr.get(np.arange(1, 20_001, dtype=np.uint64) * np.uint64(7919))
+    keys = rng.integers(1, 20_001, size=30_000).astype(np.uint64) * np.uint64(7919)
+    keys[::7] = np.arange(100_000, 100_000 + keys[::7].size, dtype=np.uint64)  # new in the get
+    pr.get(keys)
+    later = keys.copy()
+    later[1::3] = rng.integers(1, 20_001, size=later[1::3].size).astype(np.uint64) * np.uint64(7919)
+    later[2::11] = np.arange(500_000, 500_000 + later[2::11].size, dtype=np.uint64)  # new in the put
+    pr.put(later, rng.normal(0, 0.01, size=(later.size, dim)).astype(np.float32), 0.01, 1e-8)
+    pr.put(later[::-1].copy(), rng.normal(0, 0.01, size=(later.size, dim)).astype(np.float32), 0.01, 1e-8)
+    pr.compare_rows()
+    pr.check_index()
+    pr.close()
