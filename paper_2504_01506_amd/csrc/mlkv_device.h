@@ -208,6 +208,36 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
   return pre;
 }
 
+// As block_exclusive_scan, on 64-bit values (two 32-bit fields can be
+// scanned at once when the low field's total stays below 2^32).
+template <int NT>
+__device__ __forceinline__ uint64_t block_exclusive_scan_u64(uint64_t v, unsigned long long* s_w, uint64_t* total) {
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  unsigned long long x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const unsigned long long y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) s_w[w] = x;
+  lds_barrier();
+  if (w == 0) {
+    unsigned long long s = lane < NT / 64 ? s_w[lane] : 0ull;
+#pragma unroll
+    for (int o = 1; o < NT / 64; o <<= 1) {
+      const unsigned long long y = __shfl_up(s, o, 64);
+      if (lane >= o) s += y;
+    }
+    if (lane < NT / 64) s_w[lane] = s;
+  }
+  lds_barrier();
+  const uint64_t pre = (w > 0 ? s_w[w - 1] : 0ull) + x - v;
+  *total = s_w[NT / 64 - 1];
+  lds_barrier();
+  return pre;
+}
+
 template <int NT>
 __device__ __forceinline__ uint64_t block_sum_u64(uint64_t v, unsigned long long* s_w) {
   const int lane = threadIdx.x & 63;

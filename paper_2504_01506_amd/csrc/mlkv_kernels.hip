@@ -2015,27 +2015,42 @@ __global__ __launch_bounds__(NT) void k_put_group(
   if (tid == 0) pmeta[p] = PartMeta{s_seg[n_sum], S, n_sum, 0u};
 }
 
-// Exclusive prefix over partitions of f(pmeta[p]) into out[0, np]; the block's
-// NT threads each take consecutive partitions. Returns the total.
-template <int NT, class F>
-__device__ __forceinline__ uint32_t partition_prefix(const PartMeta* __restrict__ pmeta, int np, uint32_t* out,
-                                                     uint32_t* s_w, F f) {
+// The exclusive prefixes over partitions of the phase-A items (into outA)
+// and of the keys seen once (into out1), np + 1 entries each, from one scan of
+// both counts packed in 64 bits. Returns the two totals.
+template <int NT>
+__device__ __forceinline__ uint2 partition_prefix2(const PartMeta* __restrict__ pmeta, int np, uint32_t* outA,
+                                                   uint32_t* out1, unsigned long long* s_w64) {
+  constexpr int kPer = (kMaxParts + NT - 1) / NT;
   const int per = (np + NT - 1) / NT;
   const int b = threadIdx.x * per;
-  uint32_t sum = 0;
-  for (int k = 0; k < per; ++k)
-    if (b + k < np) sum += f(pmeta[b + k]);
-  uint32_t tot;
-  uint32_t off = block_exclusive_scan<NT>(sum, s_w, &tot);
-  for (int k = 0; k < per; ++k) {
-    if (b + k < np) {
-      out[b + k] = off;
-      off += f(pmeta[b + k]);
+  uint64_t pv[kPer];
+  uint64_t sum = 0;
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    pv[k] = 0;
+    if (k < per && b + k < np) {
+      const PartMeta m = pmeta[b + k];
+      pv[k] = ((uint64_t)m.mA << 32) | (uint64_t)(m.S - m.nsum);
+      sum += pv[k];
     }
   }
-  if (threadIdx.x == 0) out[np] = tot;
+  uint64_t tot;
+  uint64_t off = block_exclusive_scan_u64<NT>(sum, s_w64, &tot);
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    if (k < per && b + k < np) {
+      outA[b + k] = (uint32_t)(off >> 32);
+      out1[b + k] = (uint32_t)off;
+      off += pv[k];
+    }
+  }
+  if (threadIdx.x == 0) {
+    outA[np] = (uint32_t)(tot >> 32);
+    out1[np] = (uint32_t)tot;
+  }
   lds_barrier();
-  return tot;
+  return make_uint2((uint32_t)(tot >> 32), (uint32_t)tot);
 }
 
 // Largest partition p with pre[p] <= j (pre: np + 1 ascending prefix values).
@@ -2108,14 +2123,14 @@ __global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ g
   uint64_t* s_sgl = reinterpret_cast<uint64_t*>(s_dyn + LA::sgl);
   uint32_t* s_pa = reinterpret_cast<uint32_t*>(s_dyn + LA::pre);  // phase-A items before each partition
   uint32_t* s_p1 = s_pa + np + 1;                                  // keys seen once before each partition
-  __shared__ uint32_t s_w[NT / 64];
   __shared__ uint32_t s_hpos[NG];     // position of the item where a group's head piece ended
   __shared__ uint32_t s_slo[NG + 1];  // first item of each group's slice, and the block's end
   __shared__ uint32_t s_rng[2];
   __shared__ uint32_t s_ndone;
 
-  const uint32_t NA = partition_prefix<NT>(pmeta, np, s_pa, s_w, [](const PartMeta& m) { return m.mA; });
-  const uint32_t N1 = partition_prefix<NT>(pmeta, np, s_p1, s_w, [](const PartMeta& m) { return m.S - m.nsum; });
+  __shared__ unsigned long long s_w64[NT / 64];
+  const uint2 totals = partition_prefix2<NT>(pmeta, np, s_pa, s_p1, s_w64);
+  const uint32_t NA = totals.x, N1 = totals.y;
   if (NA + N1 == 0) return;
   const int lane = threadIdx.x & 63;
   const int g = lane / LPR;
