@@ -22,6 +22,7 @@ import argparse
 import hashlib
 import json
 import os
+import platform
 import sys
 import time
 
@@ -119,7 +120,20 @@ def cpu_baseline(wl, seconds, kv=False):
     return {"value": wl.n * steps / elapsed, "unit": unit, "cores": 1, "kind": "oracle",
             "sample": f"first {steps} steps of the same workload ({wl.n} keys each) after the "
                       f"same prefill, single-threaded C++ oracle, {elapsed:.1f} s",
-            "host_cpus": os.cpu_count(), "host_affinity": len(os.sched_getaffinity(0))}
+            "host_cpus": os.cpu_count(), "host_affinity": len(os.sched_getaffinity(0)),
+            "cpu_model": host_cpu_model()}
+
+
+def host_cpu_model():
+    """The host CPU's model name, as /proc/cpuinfo states it."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
 
 
 def main():
