@@ -14,7 +14,9 @@ mix: gets of half a batch of 2^20 record keys, then puts (upserts of new
 Prints one JSON line. `value` is get+put keys per second; the line also
 carries effective HBM GB/s from algorithmic bytes, the roofline of the
 dominant kernel (per-launch durations from HIP events recorded by the
-library around every launch) and the CPU oracle timed on this host.
+library around every launch, beside the kernel's rocprofv3 duration from the
+committed profile when that was taken on the same kernel sources) and the
+CPU oracle timed on this host.
 """
 from __future__ import annotations
 
@@ -78,9 +80,10 @@ def source_digest():
     return h.hexdigest()[:16]
 
 
-def load_traffic(kernel, digest):
-    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
-    taken on the current kernel sources."""
+def load_profile(kernel, digest, field):
+    """A per-launch figure of `kernel` from the committed rocprofv3 runs on the
+    DLRM-shaped workload (HBM bytes from the counter runs, average duration
+    from the kernel trace), if they were taken on the current kernel sources."""
     p = os.path.join(ROOT, "profiles", "traffic_dlrm.json")
     if not os.path.exists(p):
         return None
@@ -88,7 +91,11 @@ def load_traffic(kernel, digest):
         t = json.load(f)
     if t.get("source_digest") != digest:
         return None
-    return t.get("kernels", {}).get(kernel, {}).get("hbm_bytes_per_launch")
+    return t.get("kernels", {}).get(kernel, {}).get(field)
+
+
+def load_traffic(kernel, digest):
+    return load_profile(kernel, digest, "hbm_bytes_per_launch")
 
 
 def cpu_baseline(wl, seconds, kv=False):
@@ -304,12 +311,15 @@ def main():
     dom = max(kinfo, key=lambda k: kinfo[k]["avg_us"] * kinfo[k]["launches"])
     digest = source_digest()
     # the committed counters were taken on the full-size DLRM-shaped workload
-    traffic = (load_traffic(dom, digest) if args.config == "dlrm" and args.scale == 1.0 and not bounded
-               else None)
+    same_workload = args.config == "dlrm" and args.scale == 1.0 and not bounded
+    traffic = load_traffic(dom, digest) if same_workload else None
+    # the kernel's rocprofv3 duration, for comparison with the event-timed one
+    # (an event pair around every launch adds about 2 us to each)
+    traced_us = load_profile(dom, digest, "avg_us") if same_workload else None
     roof = {"kernel": dom, "bound": "hbm", "achieved": kinfo[dom]["gbps"], "peak": PEAK_HBM_GBPS,
             "unit": "GB/s", "frac": round(kinfo[dom]["gbps"] / PEAK_HBM_GBPS, 4), "traffic": traffic,
             "alg_bytes_per_launch": kinfo[dom]["alg_bytes_per_launch"],
-            "avg_launch_us": kinfo[dom]["avg_us"]}
+            "avg_launch_us": kinfo[dom]["avg_us"], "rocprofv3_avg_us": traced_us}
     log(f"kernels (events around every launch, {ms_prof * 1e3:.2f} us/step): {kinfo}")
 
     if args.copy_mib:
