@@ -147,6 +147,16 @@ int64_t mlkv_size(mlkv_table *t);
 /* Number of hash-index slots (8 per bucket). */
 int64_t mlkv_num_slots(mlkv_table *t);
 
+/* Sizes the table's per-call scratch for calls of up to n keys (0 <= n <=
+ * 2^31 - 1), so that later calls of at most n keys allocate nothing. A call
+ * larger than any reserved or seen before grows the scratch itself: it
+ * allocates device memory (hipMalloc) but does not wait for the device; the
+ * replaced buffers are freed by the next mlkv_sync, mlkv_reserve or
+ * mlkv_close once the work queued before the replacement has finished. This
+ * call synchronizes the device. Not part of the paper's interface: a setup
+ * call for callers that want no allocation on the path of their steps. */
+int mlkv_reserve(mlkv_table *t, int64_t n);
+
 /* Releases the table and all of its device memory (synchronizes the device). */
 void mlkv_close(mlkv_table *t);
 

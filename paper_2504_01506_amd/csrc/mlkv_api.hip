@@ -12,6 +12,13 @@
 
 using namespace mlkv;
 
+// A set of scratch buffers replaced by a larger one; freed once `done` (an
+// event recorded behind the last work that may use them) has completed.
+struct ScratchSet {
+  std::vector<void*> ptrs;
+  hipEvent_t done = nullptr;
+};
+
 struct mlkv_table {
   int device = 0;
   int32_t dim = 0;
@@ -48,7 +55,8 @@ struct mlkv_table {
   PartMeta* pmeta = nullptr;
   uint64_t* pc_key = nullptr;  // the last get's present keys and rows by position
   uint32_t* pc_row = nullptr;
-  int flat_blocks = 256;  // least number of put_apply blocks: one per CU
+  std::vector<ScratchSet> retired;  // replaced scratch, freed at sync / reserve / close
+  int flat_blocks = 256;  // compute units of the device
 
   // optional per-launch timing: HIP events recorded around each kernel
   struct ProfRec {
@@ -82,18 +90,19 @@ hipError_t dev_alloc(T** p, size_t bytes) {
   return hipMalloc(reinterpret_cast<void**>(p), bytes);
 }
 
-void free_workspace(mlkv_table* t) {
-  (void)hipFree(t->newlist);
-  (void)hipFree(t->tile_cnt);
-  (void)hipFree(t->items);
-  (void)hipFree(t->meta);
-  (void)hipFree(t->spill);
-  (void)hipFree(t->partials);
-  (void)hipFree(t->gitems);
-  (void)hipFree(t->gdesc);
-  (void)hipFree(t->pmeta);
-  (void)hipFree(t->pc_key);
-  (void)hipFree(t->pc_row);
+// The scratch buffers of a table, as one set (grown as a whole).
+void free_scratch_set(const ScratchSet& s) {
+  for (void* p : s.ptrs) (void)hipFree(p);
+}
+
+ScratchSet current_set(mlkv_table* t) {
+  ScratchSet s;
+  s.ptrs = {t->newlist, t->tile_cnt, t->items, t->meta, t->spill, t->partials,
+            t->gitems, t->gdesc, t->pmeta, t->pc_key, t->pc_row};
+  return s;
+}
+
+void clear_workspace_ptrs(mlkv_table* t) {
   t->pc_key = nullptr;
   t->pc_row = nullptr;
   t->partials = nullptr;
@@ -109,6 +118,27 @@ void free_workspace(mlkv_table* t) {
   t->spill_words = 0;
 }
 
+void free_workspace(mlkv_table* t) {
+  free_scratch_set(current_set(t));
+  clear_workspace_ptrs(t);
+}
+
+// Frees the scratch sets replaced by larger ones, once the work queued
+// before each replacement has finished (their events have completed).
+int release_retired(mlkv_table* t) {
+  int rc = MLKV_OK;
+  for (auto& r : t->retired) {
+    if (r.done != nullptr) {
+      hipError_t e = hipEventSynchronize(r.done);
+      if (e != hipSuccess && rc == MLKV_OK) rc = hip_fail(e, "hipEventSynchronize");
+      (void)hipEventDestroy(r.done);
+    }
+    free_scratch_set(r);
+  }
+  t->retired.clear();
+  return rc;
+}
+
 // Partitions of a put call of n keys: a power of two, at most kMaxParts,
 // with at most kPartTarget keys each on average before in-tile merging.
 uint32_t part_bits(int64_t n) {
@@ -119,7 +149,7 @@ uint32_t part_bits(int64_t n) {
 
 // Partitions used by a put call: as part_bits (never more, so the scratch
 // sized by part_bits suffices), but one partition per CU, up to twice the
-// target each, when that keeps put_group's blocks to one round.
+// target each, when that keeps the grouping blocks to one round.
 uint32_t call_part_bits(int64_t n, int cus) {
   uint32_t pb = part_bits(n);
   if (pb > 0 && (1 << pb) > cus && (1 << (pb - 1)) >= cus && (int64_t)(2 * kPartTarget) * cus >= n) --pb;
@@ -127,15 +157,27 @@ uint32_t call_part_bits(int64_t n, int cus) {
 }
 
 // Scratch for calls of up to n keys: new-key lists, per-tile counts, the
-// partitioned items, partition metadata, the spill area, in-tile sums and the
-// grouped partitions handed to the flat put kernels.
-int ensure_workspace(mlkv_table* t, int64_t n) {
+// partitioned items, partition metadata, the spill area, in-tile sums, the
+// grouped partitions and the last get's rows by position. A larger set
+// replaces the current one without waiting for the device: the old set is
+// retired behind an event recorded on `st` (the work queued before uses it)
+// and freed by mlkv_sync, mlkv_reserve or mlkv_close. The new row cache is
+// cleared on `st`, ahead of the kernels that read it.
+int ensure_workspace(mlkv_table* t, int64_t n, hipStream_t st) {
   if (n <= t->ws_n) return MLKV_OK;
   int64_t want = std::max<int64_t>(n, std::max<int64_t>(65536, 2 * t->ws_n));
   want = (want + kPutTile - 1) / kPutTile * kPutTile;
-  hipError_t e = hipDeviceSynchronize();  // old scratch may still be in use
-  if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
-  free_workspace(t);
+  hipError_t e = hipSuccess;
+  if (t->ws_n > 0) {
+    ScratchSet old = current_set(t);
+    if ((e = hipEventCreateWithFlags(&old.done, hipEventDisableTiming)) != hipSuccess ||
+        (e = hipEventRecord(old.done, st)) != hipSuccess) {
+      if (old.done != nullptr) (void)hipEventDestroy(old.done);
+      return hip_fail(e, "retiring scratch");
+    }
+    t->retired.push_back(old);
+    clear_workspace_ptrs(t);
+  }
   const int64_t get_tiles = std::max<int64_t>((want + kGetTile - 1) / kGetTile, t->flat_blocks + 1);
   // put tiles are kPutTile keys, or fewer so that every CU gets one
   const int64_t put_tiles = std::max<int64_t>(want / kPutTile, t->flat_blocks + 1);
@@ -153,14 +195,9 @@ int ensure_workspace(mlkv_table* t, int64_t n) {
       (e = dev_alloc(&t->partials, sizeof(double) * (size_t)want * (size_t)t->dim)) != hipSuccess ||
       (e = dev_alloc(&t->pc_key, sizeof(uint64_t) * (size_t)slots)) != hipSuccess ||
       (e = dev_alloc(&t->pc_row, sizeof(uint32_t) * (size_t)slots)) != hipSuccess ||
-      (e = hipMemset(t->pc_key, 0xFF, sizeof(uint64_t) * (size_t)slots)) != hipSuccess) {  // no key cached
+      (e = hipMemsetAsync(t->pc_key, 0xFF, sizeof(uint64_t) * (size_t)slots, st)) != hipSuccess) {  // no key cached
     free_workspace(t);
     return hip_fail(e, "scratch allocation");
-  }
-  // the cleared cache must be in place before any stream's kernels read it
-  if ((e = hipDeviceSynchronize()) != hipSuccess) {
-    free_workspace(t);
-    return hip_fail(e, "hipDeviceSynchronize");
   }
   t->ws_n = want;
   t->spill_words = spill_words;
@@ -312,6 +349,7 @@ void mlkv_close(mlkv_table* t) {
   if (t == nullptr) return;
   (void)hipSetDevice(t->device);
   (void)hipDeviceSynchronize();
+  (void)release_retired(t);
   free_workspace(t);
   prof_release(t);
   (void)hipFree(t->idx);
@@ -340,7 +378,7 @@ int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uin
   if (track && d_blocked == nullptr) return fail(MLKV_EINVAL, "blocked is NULL");
   if (track && t->cepoch >= (1ull << (64 - kClockBits)))
     return fail(MLKV_EINVAL, "the table has served 2^40 get calls, the most a bounded table counts");
-  if ((rc = ensure_workspace(t, n)) != MLKV_OK) return rc;
+  if ((rc = ensure_workspace(t, n, static_cast<hipStream_t>(hip_stream))) != MLKV_OK) return rc;
   GetArgs a;
   a.idx = t->idx;
   a.nb_log2 = t->nb_log2;
@@ -422,7 +460,7 @@ int put_call(mlkv_table* t, const uint64_t* d_keys, const float* src, int64_t n,
     return fail(MLKV_EINVAL, "eps must be finite and >= 0");
   if (n == 0) return MLKV_OK;
   if (d_keys == nullptr || src == nullptr) return fail(MLKV_EINVAL, "keys or rows is NULL");
-  if ((rc = ensure_workspace(t, n)) != MLKV_OK) return rc;
+  if ((rc = ensure_workspace(t, n, static_cast<hipStream_t>(hip_stream))) != MLKV_OK) return rc;
   const uint32_t pb = call_part_bits(n, t->flat_blocks);
   // keys per put_probe tile: a multiple of 64, at most kPutTile, so that the
   // tiles cover every CU when the batch is small
@@ -490,6 +528,7 @@ int mlkv_sync(mlkv_table* t, void* hip_stream) {
   if (rc) return rc;
   hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  if ((rc = release_retired(t)) != MLKV_OK) return rc;
   int latched = 0;
   e = hipMemcpy(&latched, &t->ctrl->latched, sizeof(int), hipMemcpyDeviceToHost);
   if (e != hipSuccess) return hip_fail(e, "read error latch");
@@ -522,6 +561,16 @@ int64_t mlkv_size(mlkv_table* t) {
 int64_t mlkv_num_slots(mlkv_table* t) {
   if (t == nullptr) return -1;
   return (int64_t)(t->nb * kSlots);
+}
+
+int mlkv_reserve(mlkv_table* t, int64_t n) {
+  int rc = check_table(t);
+  if (rc) return rc;
+  if (n < 0 || n > 0x7FFFFFFFll) return fail(MLKV_EINVAL, "n must be in [0, 2^31 - 1]");
+  if ((rc = ensure_workspace(t, n, nullptr)) != MLKV_OK) return rc;
+  hipError_t e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+  return release_retired(t);
 }
 
 int mlkv_lookup_rows(mlkv_table* t, const uint64_t* d_keys, int64_t n, int64_t* d_rows_out,

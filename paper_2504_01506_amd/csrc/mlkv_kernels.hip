@@ -1174,11 +1174,9 @@ struct SegmentOps {
     const float m = (float)(d_pow2 ? sq * inv_d : sq / (double)D);
     const float Gn = __fadd_rn(G, m);
     const float den = __fadd_rn(__builtin_sqrtf(Gn), eps);  // correctly rounded sqrt
-    // g / den for the whole row from one correctly rounded reciprocal y:
-    // q0 = RN(g * y), r = RN(g - den * q0) and RN(q0 + r * y), each of the
-    // last two one FMA, give the correctly rounded quotient (Markstein's
-    // correction step; holds without underflow or overflow)
-    const float y = __fdiv_rn(1.0f, den);
+    // g / den: a correctly rounded IEEE quotient per element, so that den = 0
+    // (eps = 0 with an underflowing m), subnormal denominators and overflowing
+    // quotients give the same infinities and NaNs as a plain fp32 division
 #pragma unroll
     for (int k = 0; k < K; ++k) {
       const int col = (k * LPR + q) * VEC;
@@ -1186,9 +1184,7 @@ struct SegmentOps {
 #pragma unroll
         for (int x = 0; x < VEC; ++x) {
           const float gx = VecT<VEC>::get(g[k], x);
-          const float q0 = __fmul_rn(gx, y);
-          const float r = __builtin_fmaf(-q0, den, gx);
-          const float qv = __builtin_fmaf(r, y, q0);
+          const float qv = __fdiv_rn(gx, den);
           const float p = __fmul_rn(lr, qv);
           VecT<VEC>::set(w[k], x, __fsub_rn(VecT<VEC>::get(w[k], x), p));
         }

@@ -54,6 +54,7 @@ def load() -> ctypes.CDLL:
         "mlkv_sync": (INT, [P, P]),
         "mlkv_size": (I64, [P]),
         "mlkv_num_slots": (I64, [P]),
+        "mlkv_reserve": (INT, [P, I64]),
         "mlkv_close": (None, [P]),
         "mlkv_last_error": (ctypes.c_char_p, []),
         "mlkv_lookup_rows": (INT, [P, P, I64, P, P]),
@@ -168,6 +169,10 @@ def mlkv_num_slots(t: int) -> int:
     return load().mlkv_num_slots(t)
 
 
+def mlkv_reserve(t: int, n: int) -> int:
+    return load().mlkv_reserve(t, n)
+
+
 def mlkv_close(t: int) -> None:
     load().mlkv_close(t)
 
@@ -270,6 +275,10 @@ class Table:
     @property
     def size(self) -> int:
         return mlkv_size(self.h)
+
+    def reserve(self, n: int):
+        """Size the per-call scratch for calls of up to n keys (no allocation on later calls)."""
+        _check(mlkv_reserve(self.h, int(n)))
 
     @property
     def num_slots(self) -> int:

@@ -1,6 +1,8 @@
 """Runs the GPU library and the CPU oracle side by side on identical inputs."""
 from __future__ import annotations
 
+import json
+import os
 import sys
 
 import numpy as np
@@ -17,6 +19,16 @@ def log(*a):
     sys.stdout.flush()
 
 
+def record(name: str, stats: dict):
+    """Appends a parity record (max row-scaled error, max ulp, ...) as a JSON
+    line to the file named by MLKV_PARITY_LOG, when set."""
+    path = os.environ.get("MLKV_PARITY_LOG")
+    log(f"[parity-record] {name} {stats}")
+    if path:
+        with open(path, "a") as f:
+            f.write(json.dumps({"case": name, **stats}) + "\n")
+
+
 def dev_keys(k: np.ndarray) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(k, dtype=np.uint64).view(np.int64)).cuda()
 
@@ -26,13 +38,44 @@ def dev(a: np.ndarray) -> torch.Tensor:
 
 
 def row_scaled_err(a: np.ndarray, b: np.ndarray) -> np.ndarray:
-    """|a - b| / max(|b|, max |b| over the row): the error measure for rows."""
-    scale = np.maximum(np.abs(b), np.max(np.abs(b), axis=-1, keepdims=True))
+    """|a - b| / max(|b|, max |b| over the row): the error measure for rows.
+
+    Non-finite elements must agree in kind (the same infinity, or NaN on both
+    sides; NaN payloads are not compared): agreement counts as error 0, any
+    other pairing as an infinite error. The row scale uses finite elements."""
+    a64 = a.astype(np.float64)
+    b64 = b.astype(np.float64)
+    nonfin = ~np.isfinite(a64) | ~np.isfinite(b64)
+    fb = np.where(np.isfinite(b64), np.abs(b64), 0.0)
+    scale = np.maximum(fb, np.max(fb, axis=-1, keepdims=True))
     scale = np.where(scale == 0, 1.0, scale)
-    return np.abs(a.astype(np.float64) - b.astype(np.float64)) / scale
+    with np.errstate(invalid="ignore"):
+        err = np.where(nonfin, 0.0, np.abs(a64 - b64) / scale)
+    if nonfin.any():
+        same = (np.isnan(a64) & np.isnan(b64)) | (a64 == b64)
+        err = np.where(nonfin & ~same, np.inf, err)
+    return err
+
+
+def rel_err(a: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """|a - b| / |b| element by element (accumulators), with the same rule
+    for non-finite values as row_scaled_err."""
+    a64 = a.astype(np.float64)
+    b64 = b.astype(np.float64)
+    nonfin = ~np.isfinite(a64) | ~np.isfinite(b64)
+    with np.errstate(invalid="ignore", divide="ignore"):
+        err = np.where(nonfin, 0.0, np.abs(a64 - b64) / np.maximum(np.abs(b64), 1e-30))
+    err = np.where((a64 == b64) & ~nonfin, 0.0, err)
+    if nonfin.any():
+        same = (np.isnan(a64) & np.isnan(b64)) | (a64 == b64)
+        err = np.where(nonfin & ~same, np.inf, err)
+    return err
 
 
 def ulp_diff(a: np.ndarray, b: np.ndarray) -> int:
+    """Largest distance in units in the last place over the finite pairs."""
+    fin = np.isfinite(a) & np.isfinite(b)
+    a, b = a[fin], b[fin]
     ia = a.astype(np.float32).view(np.int32).astype(np.int64)
     ib = b.astype(np.float32).view(np.int32).astype(np.int64)
     ia = np.where(ia < 0, -(ia & 0x7FFFFFFF), ia)
@@ -136,7 +179,8 @@ class Pair:
             err = row_scaled_err(got[~fresh], want[~fresh])
             self.stats["max_err"] = max(self.stats["max_err"], float(err.max()))
             self.stats["max_ulp"] = max(self.stats["max_ulp"], ulp_diff(got[~fresh], want[~fresh]))
-            self.stats["exact_mismatch"] += int(np.sum(got[~fresh].view(np.uint32) != want[~fresh].view(np.uint32)))
+            self.stats["exact_mismatch"] += int(np.sum((got[~fresh].view(np.uint32) != want[~fresh].view(np.uint32))
+                                                       & ~(np.isnan(got[~fresh]) & np.isnan(want[~fresh]))))
             assert err.max() <= RTOL, f"updated rows differ: max row-scaled error {err.max():.3e}"
 
     def put(self, keys: np.ndarray, grads: np.ndarray, lr: float, eps: float):
@@ -183,8 +227,9 @@ class Pair:
         if (~fresh).any():
             err = row_scaled_err(w[~fresh], want_w[~fresh])
             assert err.max() <= RTOL, f"rows differ: {err.max():.3e}"
-            st_err = np.abs(st[~fresh].astype(np.float64) - want_st[~fresh]) / np.maximum(np.abs(want_st[~fresh]), 1e-30)
+            st_err = rel_err(st[~fresh], want_st[~fresh])
             assert st_err.max() <= RTOL, f"accumulators differ: {st_err.max():.3e}"
+            self.stats["max_state_err"] = max(self.stats.get("max_state_err", 0.0), float(st_err.max()))
             self.stats["max_err"] = max(self.stats["max_err"], float(err.max()))
             self.stats["max_ulp"] = max(self.stats["max_ulp"], ulp_diff(w[~fresh], want_w[~fresh]))
 

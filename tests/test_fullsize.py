@@ -12,7 +12,7 @@ import pytest
 import torch
 
 from paper_2504_01506_amd import mlkv, workloads as W
-from _harness import Pair, dev, dev_keys, log
+from _harness import Pair, dev, dev_keys, log, record
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -52,6 +52,28 @@ def test_full_size_config(name):
         pr.put(keys, wl.grads(s), wl.lr, wl.eps)
         check_step(pr, keys, rng)
         log(f"[full] {name} step {s}: put ok, stats={pr.stats}")
+    record(f"full-{name}-{steps}steps", pr.stats)
+    pr.close()
+
+
+def test_full_size_dlrm_all_100_steps():
+    """The DLRM-shaped workload for its stated 100 steps: every get and put
+    on both sides; the get output compared in full, key -> row of the batch,
+    the rows each step updated and a sample of the others every 10th step
+    (fp32 drift over a real run stays within the bound)."""
+    wl = W.make("dlrm", scale=1.0)
+    pr = Pair(wl.dim, wl.capacity)
+    pr.prefill(wl.prefill_keys())
+    rng = np.random.default_rng(100)
+    for s in range(100):
+        keys = wl.keys(s)
+        check = s % 10 == 9
+        pr.get(keys, check=check)
+        pr.put(keys, wl.grads(s), wl.lr, wl.eps)
+        if check:
+            check_step(pr, keys, rng, n_sample=5000)
+            log(f"[full] dlrm step {s}: ok, stats={pr.stats}")
+    record("full-dlrm-100steps", pr.stats)
     pr.close()
 
 

@@ -8,7 +8,7 @@ import pytest
 import torch
 
 from paper_2504_01506_amd import mlkv, workloads as W
-from _harness import Pair, dev, dev_keys, log
+from _harness import Pair, dev, dev_keys, log, record
 
 pytestmark = pytest.mark.gpu
 
@@ -28,6 +28,7 @@ def run_config(name, scale, steps, full_check_every=1):
             pr.compare_rows()
         log(f"[parity] {name} step {s} ok size={pr.ora.size} stats={pr.stats}")
     pr.check_index()
+    record(f"{name}@{scale}x{steps}", pr.stats)
     pr.close()
     return pr.stats
 
