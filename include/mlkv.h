@@ -90,6 +90,24 @@ mlkv_table *mlkv_open_bounded(int32_t dim, int64_t capacity, uint64_t seed, floa
  * 0 <= n <= 2^31 - 1. d_keys: n uint64 keys. d_out: n*dim floats, row-major. */
 int mlkv_get(mlkv_table *t, const uint64_t *d_keys, int64_t n, float *d_out, void *hip_stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): mlkv_get
+ * with the same results (rows, key -> row, size, errors), that allocates
+ * nothing. Its per-call scratch (new-key lists and per-tile counts) lives in
+ * a fixed device array of about 1.8 MiB per GPU, part of the library's code
+ * object, which each GPU the library runs on holds until the process ends.
+ *   - 0 <= n <= MLKV_NOALLOC_MAX_KEYS; larger n is refused with MLKV_EINVAL.
+ *   - Every call on a GPU shares that GPU's array: calls of this function on
+ *     one GPU (any tables, any streams) that may run at the same time race
+ *     and give undefined results; order them on one stream or synchronize.
+ *   - It does not record the rows it found for reuse by a later put_grad
+ *     (that put probes the index itself where no earlier get recorded them).
+ *   - Refused (MLKV_EINVAL) on a table with a staleness bound.
+ * Calls no hipMalloc, hipFree or other allocating routine; launch timing
+ * (mlkv_profile_enable) is not recorded for it. */
+#define MLKV_NOALLOC_MAX_KEYS 65536
+int mlkv_get_noalloc(mlkv_table *t, const uint64_t *d_keys, int64_t n, float *d_out, void *hip_stream);
+
 /* Get on a table opened with mlkv_open_bounded (Sec. III-C1): as mlkv_get
  * for the served positions; d_blocked[i] = 1 where d_keys[i] is blocked (row
  * i of d_out is then left as it was), else 0. d_blocked: n bytes (device).

@@ -4,6 +4,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -364,11 +365,22 @@ void mlkv_close(mlkv_table* t) {
 
 namespace {
 
+// Per-call scratch of a get held outside the table (the allocation-free
+// entry point): the new-key lists, the per-tile counts and the key-range
+// overflow lists. Such a get leaves the table's record of found rows alone.
+struct GetScratch {
+  NewKey* newlist;
+  uint32_t* tile_cnt;
+  uint64_t* xkey;
+  uint32_t* xslot;
+};
+
 // The get pipeline (probe + gather, then rows for new keys); d_blocked is
 // written when the table has a staleness bound and the call counts (a
-// lookahead does not).
+// lookahead does not). With `fixed`, the call uses that scratch, allocates
+// nothing and records no launch timings.
 int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uint8_t* d_blocked,
-             bool count, void* hip_stream) {
+             bool count, void* hip_stream, const GetScratch* fixed = nullptr) {
   int rc = check_table(t);
   if (rc) return rc;
   if (n < 0 || n > 0x7FFFFFFFll) return fail(MLKV_EINVAL, "n must be in [0, 2^31 - 1]");
@@ -378,7 +390,8 @@ int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uin
   if (track && d_blocked == nullptr) return fail(MLKV_EINVAL, "blocked is NULL");
   if (track && t->cepoch >= (1ull << (64 - kClockBits)))
     return fail(MLKV_EINVAL, "the table has served 2^40 get calls, the most a bounded table counts");
-  if ((rc = ensure_workspace(t, n, static_cast<hipStream_t>(hip_stream))) != MLKV_OK) return rc;
+  if (fixed == nullptr && (rc = ensure_workspace(t, n, static_cast<hipStream_t>(hip_stream))) != MLKV_OK)
+    return rc;
   GetArgs a;
   a.idx = t->idx;
   a.nb_log2 = t->nb_log2;
@@ -390,23 +403,63 @@ int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uin
   a.D = t->dim;
   a.seed = t->seed;
   a.capacity = t->capacity;
-  a.newlist = t->newlist;
-  a.tile_cnt = t->tile_cnt;
+  a.newlist = fixed ? fixed->newlist : t->newlist;
+  a.tile_cnt = fixed ? fixed->tile_cnt : t->tile_cnt;
   a.ctrl = t->ctrl;
   a.epoch = t->epoch;
-  a.xkey = t->items;  // the put pipeline's scratch (at least n entries each), idle during a get
-  a.xslot = t->meta;
+  // key-range overflow lists: the put pipeline's scratch (at least n entries
+  // each), idle during a get
+  a.xkey = fixed ? fixed->xkey : t->items;
+  a.xslot = fixed ? fixed->xslot : t->meta;
   a.clock = track ? t->clock : nullptr;
   a.cepoch = t->cepoch;
   a.bound = (uint32_t)std::max<int64_t>(t->bound, 0);
   a.blocked = d_blocked;
-  a.pc_key = t->pc_key;
-  a.pc_row = t->pc_row;
+  a.pc_key = fixed ? nullptr : t->pc_key;
+  a.pc_row = fixed ? nullptr : t->pc_row;
   const bool vec4 = (t->dim % 4 == 0) && (d_out == nullptr || aligned16(d_out));
-  hipError_t e = launch_get(a, vec4, static_cast<hipStream_t>(hip_stream), hook_of(t));
+  hipError_t e = launch_get(a, vec4, static_cast<hipStream_t>(hip_stream), fixed ? LaunchHook{} : hook_of(t));
   if (e != hipSuccess) return hip_fail(e, "mlkv_get launch");
   t->epoch++;
   if (track) t->cepoch++;
+  return MLKV_OK;
+}
+
+// ---- scratch of the allocation-free get ----
+// A file-scope device array, one copy per GPU, sized for kNoAllocMaxKeys keys:
+// new-key lists (16 B per key), per-tile counts, key-range lists (12 B per key).
+constexpr int64_t kNoAllocMaxKeys = MLKV_NOALLOC_MAX_KEYS;
+constexpr size_t kNaNewlist = 0;
+constexpr size_t kNaTileCnt = kNaNewlist + sizeof(NewKey) * (size_t)kNoAllocMaxKeys;
+constexpr size_t kNaXkey = kNaTileCnt + 4096;
+constexpr size_t kNaXslot = kNaXkey + sizeof(uint64_t) * (size_t)kNoAllocMaxKeys;
+constexpr size_t kNaBytes = kNaXslot + sizeof(uint32_t) * (size_t)kNoAllocMaxKeys;
+static_assert(kNaTileCnt + sizeof(uint32_t) * ((kNoAllocMaxKeys + kGetTile - 1) / kGetTile) <= kNaXkey,
+              "tile counts fit their region");
+
+__device__ __align__(256) unsigned char scratch[kNaBytes];
+
+// Device address of `scratch` on each device (the name itself is only a
+// host-side stand-in), taken once per device with that device current.
+std::mutex g_scratch_mu;
+constexpr int kMaxDevices = 64;
+void* g_scratch_addr[kMaxDevices] = {};
+
+int noalloc_scratch(int device, GetScratch* out) {
+  if (device < 0 || device >= kMaxDevices) return fail(MLKV_EDEVICE, "device ordinal out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_addr[device] == nullptr) {
+    void* p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (p == nullptr) return fail(MLKV_EDEVICE, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_addr[device] = p;
+  }
+  unsigned char* base = static_cast<unsigned char*>(g_scratch_addr[device]);
+  out->newlist = reinterpret_cast<NewKey*>(base + kNaNewlist);
+  out->tile_cnt = reinterpret_cast<uint32_t*>(base + kNaTileCnt);
+  out->xkey = reinterpret_cast<uint64_t*>(base + kNaXkey);
+  out->xslot = reinterpret_cast<uint32_t*>(base + kNaXslot);
   return MLKV_OK;
 }
 
@@ -418,6 +471,17 @@ int mlkv_get(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, voi
   if (t != nullptr && t->clock != nullptr)
     return fail(MLKV_EINVAL, "the table has a staleness bound: use mlkv_get_bounded");
   return get_call(t, d_keys, n, d_out, nullptr, true, hip_stream);
+}
+
+int mlkv_get_noalloc(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, void* hip_stream) {
+  int rc = check_table(t);  // makes the table's device current
+  if (rc) return rc;
+  if (t->clock != nullptr) return fail(MLKV_EINVAL, "the table has a staleness bound: use mlkv_get_bounded");
+  if (n < 0 || n > kNoAllocMaxKeys)
+    return fail(MLKV_EINVAL, "mlkv_get_noalloc takes at most MLKV_NOALLOC_MAX_KEYS (65536) keys");
+  GetScratch s;
+  if ((rc = noalloc_scratch(t->device, &s)) != MLKV_OK) return rc;
+  return get_call(t, d_keys, n, d_out, nullptr, true, hip_stream, &s);
 }
 
 int mlkv_lookahead(mlkv_table* t, const uint64_t* d_keys, int64_t n, void* hip_stream) {

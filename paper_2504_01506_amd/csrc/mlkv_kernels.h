@@ -77,7 +77,8 @@ struct GetArgs {
   uint32_t bound;
   uint8_t* blocked;
   // per position: the key found present and its row (the key is the empty
-  // key where the position held no present key); a later put reads them
+  // key where the position held no present key); a later put reads them.
+  // nullptr: not recorded
   uint64_t* pc_key;
   uint32_t* pc_row;
 };

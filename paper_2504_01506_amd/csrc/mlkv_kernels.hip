@@ -145,7 +145,7 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
   }
   // a key present before the call, with its row, for a put of the same
   // batch: a key's row never changes once assigned, so the pair stays valid
-  if (i < n) {
+  if (i < n && pc_key != nullptr) {
     pc_key[i] = pr.status == P_HIT ? key : kEmptyKey;
     pc_row[i] = pr.row;
   }

@@ -19,6 +19,7 @@ MLKV_DEFAULT_SEED = 0x4D4C4B56
 MLKV_RESERVED_KEY = 0xFFFFFFFFFFFFFFFF
 
 MLKV_NUM_KERNELS = 5
+MLKV_NOALLOC_MAX_KEYS = 65536
 
 _lib = None
 
@@ -46,6 +47,7 @@ def load() -> ctypes.CDLL:
         "mlkv_open_bounded": (P, [I32, I64, U64, F32, I64]),
         "mlkv_get": (INT, [P, P, I64, P, P]),
         "mlkv_get_bounded": (INT, [P, P, I64, P, P, P]),
+        "mlkv_get_noalloc": (INT, [P, P, I64, P, P]),
         "mlkv_lookahead": (INT, [P, P, I64, P]),
         "mlkv_read_staleness": (INT, [P, P, I64, P, P]),
         "mlkv_put_grad": (INT, [P, P, P, I64, F32, F32, P]),
@@ -131,6 +133,10 @@ def mlkv_open_bounded(dim: int, capacity: int, seed: int, max_load: float, stale
 
 def mlkv_get(t: int, keys, n: int, out, stream=None) -> int:
     return load().mlkv_get(t, _ptr(keys), n, _ptr(out), _stream(stream))
+
+
+def mlkv_get_noalloc(t: int, keys, n: int, out, stream=None) -> int:
+    return load().mlkv_get_noalloc(t, _ptr(keys), n, _ptr(out), _stream(stream))
 
 
 def mlkv_get_bounded(t: int, keys, n: int, out, blocked, stream=None) -> int:
