@@ -36,7 +36,7 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBPS = 8000.0
 METRIC = "embedding get+put keys/sec and achieved HBM GB/s (% of peak), 1 MI355X"
 METRIC_KV = "key-value operations/sec, 50% get / 50% put, 1 MI355X"
-KERNELS = ("get_probe_gather", "assign_new", "put_probe", "put_group", "put_apply")
+KERNELS = ("get_probe_gather", "assign_new", "put_probe", "put_reduce")
 
 
 def kernel_bytes(n, U, M, D):
@@ -50,11 +50,9 @@ def kernel_bytes(n, U, M, D):
         "assign_new": (4 * D + 16) * M,
         # keys in, one index entry per distinct key
         "put_probe": 8 * n + 12 * U,
-        # grouping works on scratch only
-        "put_group": 0,
         # gradient rows in, distinct rows read and written, accumulators read
         # and written
-        "put_apply": 4 * D * n + 8 * D * U + 8 * U,
+        "put_reduce": 4 * D * n + 8 * D * U + 8 * U,
     }
 
 
@@ -66,9 +64,8 @@ def kernel_bytes_kv(nr, Ur, nw, Uw, D):
         "get_probe_gather": 8 * nr + 12 * Ur + 4 * D * Ur + 4 * D * nr,
         "assign_new": 0,
         "put_probe": 8 * nw + 12 * Uw,
-        "put_group": 0,
         # the winning value of each key in, its row written
-        "put_apply": 8 * D * Uw,
+        "put_reduce": 8 * D * Uw,
     }
 
 

@@ -211,13 +211,13 @@ int mlkv_read_staleness(mlkv_table *t, const int64_t *d_rows, int64_t n, uint32_
 /* ---- per-kernel timing (benchmarks) ----
  * The library runs MLKV_NUM_KERNELS kernels: 0 get_probe_gather and
  * 1 assign_new for mlkv_get, mlkv_get_bounded and mlkv_lookahead;
- * 2 put_probe, 3 put_group and 4 put_apply for
- * mlkv_put_grad, mlkv_put_grad_sgd and mlkv_put. While enabled, HIP events are recorded on
+ * 2 put_probe and 3 put_reduce for mlkv_put_grad, mlkv_put_grad_sgd and
+ * mlkv_put. While enabled, HIP events are recorded on
  * the call's stream before and after every launch. mlkv_profile_read waits
  * for the recorded launches, writes per-kernel sums of their durations (ms)
  * and launch counts into the host arrays total_ms[MLKV_NUM_KERNELS] and
  * launches[MLKV_NUM_KERNELS], and forgets them. */
-#define MLKV_NUM_KERNELS 5
+#define MLKV_NUM_KERNELS 4
 int mlkv_profile_enable(mlkv_table *t, int enable);
 int mlkv_profile_read(mlkv_table *t, double *total_ms, int64_t *launches);
 /* Name of kernel `kernel` (0 <= kernel < MLKV_NUM_KERNELS), else NULL. */

@@ -51,13 +51,10 @@ struct mlkv_table {
   uint64_t* spill = nullptr;
   uint64_t spill_words = 0;
   double* partials = nullptr;
-  uint64_t* gitems = nullptr;
-  uint32_t* gdesc = nullptr;
-  PartMeta* pmeta = nullptr;
   uint64_t* pc_key = nullptr;  // the last get's present keys and rows by position
   uint32_t* pc_row = nullptr;
   std::vector<ScratchSet> retired;  // replaced scratch, freed at sync / reserve / close
-  int flat_blocks = 256;  // compute units of the device
+  int cus = 256;  // compute units of the device
 
   // optional per-launch timing: HIP events recorded around each kernel
   struct ProfRec {
@@ -98,8 +95,7 @@ void free_scratch_set(const ScratchSet& s) {
 
 ScratchSet current_set(mlkv_table* t) {
   ScratchSet s;
-  s.ptrs = {t->newlist, t->tile_cnt, t->items, t->meta, t->spill, t->partials,
-            t->gitems, t->gdesc, t->pmeta, t->pc_key, t->pc_row};
+  s.ptrs = {t->newlist, t->tile_cnt, t->items, t->meta, t->spill, t->partials, t->pc_key, t->pc_row};
   return s;
 }
 
@@ -107,9 +103,6 @@ void clear_workspace_ptrs(mlkv_table* t) {
   t->pc_key = nullptr;
   t->pc_row = nullptr;
   t->partials = nullptr;
-  t->gitems = nullptr;
-  t->gdesc = nullptr;
-  t->pmeta = nullptr;
   t->newlist = nullptr;
   t->tile_cnt = nullptr;
   t->items = nullptr;
@@ -179,16 +172,12 @@ int ensure_workspace(mlkv_table* t, int64_t n, hipStream_t st) {
     t->retired.push_back(old);
     clear_workspace_ptrs(t);
   }
-  const int64_t get_tiles = std::max<int64_t>((want + kGetTile - 1) / kGetTile, t->flat_blocks + 1);
+  const int64_t get_tiles = std::max<int64_t>((want + kGetTile - 1) / kGetTile, t->cus + 1);
   // put tiles are kPutTile keys, or fewer so that every CU gets one
-  const int64_t put_tiles = std::max<int64_t>(want / kPutTile, t->flat_blocks + 1);
+  const int64_t put_tiles = std::max<int64_t>(want / kPutTile, t->cus + 1);
   const int64_t slots = std::max<int64_t>(want, put_tiles * kPutTile);
   const uint64_t spill_words = 4ull * (uint64_t)want + 4096;
-  const size_t np = (size_t)1 << part_bits(want);
   if ((e = dev_alloc(&t->newlist, sizeof(NewKey) * (size_t)slots)) != hipSuccess ||
-      (e = dev_alloc(&t->gitems, sizeof(uint64_t) * np * kRedCap)) != hipSuccess ||
-      (e = dev_alloc(&t->gdesc, sizeof(uint32_t) * np * kRedCap)) != hipSuccess ||
-      (e = dev_alloc(&t->pmeta, sizeof(PartMeta) * np)) != hipSuccess ||
       (e = dev_alloc(&t->tile_cnt, sizeof(uint32_t) * (size_t)get_tiles)) != hipSuccess ||
       (e = dev_alloc(&t->items, sizeof(uint64_t) * (size_t)slots)) != hipSuccess ||
       (e = dev_alloc(&t->meta, sizeof(uint32_t) * (size_t)kMaxParts * (size_t)put_tiles)) != hipSuccess ||
@@ -294,13 +283,13 @@ mlkv_table* mlkv_open_ex(int32_t dim, int64_t capacity, uint64_t seed, float max
   t->nb_log2 = lg;
   t->nb = 1ull << lg;
   hipError_t e = hipGetDevice(&t->device);
-  if (e == hipSuccess) e = hipDeviceGetAttribute(&t->flat_blocks, hipDeviceAttributeMultiprocessorCount, t->device);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&t->cus, hipDeviceAttributeMultiprocessorCount, t->device);
   if (e != hipSuccess) {
     hip_fail(e, "hipGetDevice");
     delete t;
     return nullptr;
   }
-  t->flat_blocks = std::max(1, t->flat_blocks);
+  t->cus = std::max(1, t->cus);
   if ((e = dev_alloc(&t->idx, sizeof(Bucket) * t->nb)) != hipSuccess ||
       (e = dev_alloc(&t->rows, sizeof(float) * (size_t)capacity * (size_t)dim)) != hipSuccess ||
       (e = dev_alloc(&t->state, sizeof(float) * (size_t)capacity)) != hipSuccess ||
@@ -525,10 +514,10 @@ int put_call(mlkv_table* t, const uint64_t* d_keys, const float* src, int64_t n,
   if (n == 0) return MLKV_OK;
   if (d_keys == nullptr || src == nullptr) return fail(MLKV_EINVAL, "keys or rows is NULL");
   if ((rc = ensure_workspace(t, n, static_cast<hipStream_t>(hip_stream))) != MLKV_OK) return rc;
-  const uint32_t pb = call_part_bits(n, t->flat_blocks);
+  const uint32_t pb = call_part_bits(n, t->cus);
   // keys per put_probe tile: a multiple of 64, at most kPutTile, so that the
   // tiles cover every CU when the batch is small
-  const int64_t per_cu = (n + t->flat_blocks - 1) / t->flat_blocks;
+  const int64_t per_cu = (n + t->cus - 1) / t->cus;
   const int tlen = (int)std::min<int64_t>(kPutTile, std::max<int64_t>(64, (per_cu + 63) / 64 * 64));
   PutArgs a;
   a.idx = t->idx;
@@ -553,10 +542,6 @@ int put_call(mlkv_table* t, const uint64_t* d_keys, const float* src, int64_t n,
   a.tile_cnt = t->tile_cnt;
   a.spill = t->spill;
   a.spill_words = t->spill_words;
-  a.gitems = t->gitems;
-  a.gdesc = t->gdesc;
-  a.pmeta = t->pmeta;
-  a.flat_blocks = t->flat_blocks;
   a.ctrl = t->ctrl;
   a.epoch = t->epoch;
   a.clock = t->clock;
@@ -713,8 +698,7 @@ int mlkv_profile_read(mlkv_table* t, double* total_ms, int64_t* launches) {
 }
 
 const char* mlkv_kernel_name(int kernel) {
-  static const char* names[K_COUNT] = {"get_probe_gather", "assign_new", "put_probe", "put_group",
-                                       "put_apply"};
+  static const char* names[K_COUNT] = {"get_probe_gather", "assign_new", "put_probe", "put_reduce"};
   return (kernel >= 0 && kernel < K_COUNT) ? names[kernel] : nullptr;
 }
 

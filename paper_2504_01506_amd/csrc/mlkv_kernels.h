@@ -13,18 +13,18 @@ constexpr int kGetTile = 256;    // keys per probe_gather block (one per lane)
 constexpr int kPutTile = 1024;   // keys per put_probe block
 constexpr int kPutThreads = 1024; // threads of a put_probe block
 constexpr int kMaxParts = 4096;  // partitions (MSD digits) per put call
-constexpr int kRedCap = 3072;    // partition entries grouped in LDS by a reduce_update block
+constexpr int kRedCap = 3072;    // partition items grouped in LDS by a put_reduce block
 constexpr int kRedHash = 4096;   // LDS hash slots for that grouping (load <= 0.75)
 constexpr int kPartTarget = 1024; // put keys per partition the partition count aims for
+constexpr int kPresumMin = 2;    // a key repeated this often in a put_probe tile is summed there
 
 // Kernels of the library, for per-launch timing.
 enum KernelId : int {
   K_GET_PROBE_GATHER = 0,
   K_ASSIGN_NEW = 1,
   K_PUT_PROBE = 2,
-  K_PUT_GROUP = 3,
-  K_PUT_APPLY = 4,
-  K_COUNT = 5
+  K_PUT_REDUCE = 3,
+  K_COUNT = 4
 };
 
 // Update a put call applies to each distinct key's row.
@@ -32,14 +32,6 @@ enum PutOp : int {
   kOpAdagrad = 0,  // sum the key's gradient rows, one row-wise Adagrad step
   kOpSgd = 1,      // sum the key's gradient rows, one SGD step
   kOpAssign = 2    // the value row at the key's last position replaces the row
-};
-
-// Per-partition results of put_group, read by put_apply.
-struct PartMeta {
-  uint32_t mA;    // items of the segments that need a sum (stored first)
-  uint32_t S;     // segments (distinct keys) of the partition
-  uint32_t nsum;  // segments that need a sum
-  uint32_t pad;
 };
 
 
@@ -106,10 +98,6 @@ struct PutArgs {
   uint32_t* tile_cnt;
   uint64_t* spill;
   uint64_t spill_words;
-  uint64_t* gitems;   // [partitions][kRedCap] grouped items
-  uint32_t* gdesc;    // [partitions][kRedCap] segment range of each item
-  PartMeta* pmeta;    // [partitions]
-  int flat_blocks;    // least number of put_apply blocks (one per CU)
   Ctrl* ctrl;
   uint64_t epoch;
   unsigned long long* clock;  // per-row staleness words, or nullptr when not tracked

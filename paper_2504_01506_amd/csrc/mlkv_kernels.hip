@@ -866,14 +866,21 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
     }
   }
   lds_barrier();
+  // a key repeated in the tile ("dup") gets the sorted list of its entries;
+  // one repeated at least dup_min times is merged into one item (an
+  // assignment keeps the last position; a sum adds the key's gradient rows
+  // here, in fp64), the entries of the others stay items of their own, which
+  // the key's first entry emits together in position order
+  const uint32_t dup_min = op == kOpAssign ? 2u : (uint32_t)kPresumMin;
   uint32_t cnt[KPT];
-  bool dup[KPT], owner[KPT];
+  bool dup[KPT], merged[KPT], owner[KPT];
   uint32_t n_own = 0, l_own = 0;
 #pragma unroll
   for (int kk = 0; kk < KPT; ++kk) {
     const int e = kk * NT + tid;
     cnt[kk] = valid[kk] ? s_hcnt[hs[kk]] : 0u;
     dup[kk] = cnt[kk] >= 2;
+    merged[kk] = cnt[kk] >= dup_min;
     owner[kk] = dup[kk] && s_hfirst[hs[kk]] == (uint32_t)e;
     n_own += owner[kk] ? 1u : 0u;
     l_own += owner[kk] ? cnt[kk] : 0u;
@@ -887,7 +894,7 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
   auto n_items = [](uint32_t c) { return c <= kSumChunk ? 1u : (c + kSumChunk - 1) / kSumChunk; };
   uint32_t w_own = 0;
 #pragma unroll
-  for (int kk = 0; kk < KPT; ++kk) w_own += owner[kk] ? n_items(cnt[kk]) : 0u;
+  for (int kk = 0; kk < KPT; ++kk) w_own += owner[kk] && merged[kk] ? n_items(cnt[kk]) : 0u;
   // one scan for the three prefixes, packed 10 | 11 | 11 bits (a tile holds
   // at most 512 repeated keys and 1024 entries, so no field overflows)
   static_assert(kPutTile <= 1024, "packed prefix fields");
@@ -905,7 +912,7 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
       s_doff[dpre] = (uint16_t)lpre;
       ++dpre;
       lpre += cnt[kk];
-      wpre += n_items(cnt[kk]);
+      wpre += merged[kk] ? n_items(cnt[kk]) : 0u;
     }
   }
   if (tid == 0) s_doff[ndup] = (uint16_t)nlanes;
@@ -954,7 +961,11 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
   const int g = lane / LPR;
   const int q = lane % LPR;
   const int gid = (tid >> 6) * RPW + g;
-  const bool chunked = nwork > ndup;  // some key has more than kSumChunk entries
+  // some merged key has more than kSumChunk entries
+  bool my_chunked = false;
+#pragma unroll
+  for (int kk = 0; kk < KPT; ++kk) my_chunked |= owner[kk] && cnt[kk] > kSumChunk;
+  const bool chunked = __syncthreads_or(my_chunked ? 1 : 0) != 0;
   double acc[K][VEC];
   auto store_row = [&](uint32_t entry) {
     double* dst = partials + (size_t)(base + s_lanes[entry]) * (size_t)D;
@@ -968,17 +979,15 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
   };
   if (op != kOpAssign) {
     for (uint32_t w = gid; w < nwork; w += NG) {
-      uint32_t d = w, c = 0;
-      if (chunked) {  // the key of item w: last d with s_wfirst[d] <= w
-        uint32_t dh = ndup;
-        d = 0;
-        while (d + 1 < dh) {
-          const uint32_t mid = (d + dh) >> 1;
-          if (s_wfirst[mid] <= w) d = mid;
-          else dh = mid;
-        }
-        c = w - s_wfirst[d];
+      // the key of item w: the last d with s_wfirst[d] <= w (keys that are
+      // not merged have no work item and share the next key's first one)
+      uint32_t d = 0, dh = ndup;
+      while (d + 1 < dh) {
+        const uint32_t mid = (d + dh) >> 1;
+        if (s_wfirst[mid] <= w) d = mid;
+        else dh = mid;
       }
+      const uint32_t c = w - s_wfirst[d];
       const uint32_t kb = s_doff[d], kend = s_doff[d + 1];
       const bool whole = kend - kb <= kSumChunk;
       const uint32_t b = kb + c * kSumChunk, e = whole ? kend : min(b + kSumChunk, kend);
@@ -1047,17 +1056,19 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
     x[kk] = valid[kk] ? make_item(fresh, fresh ? pr[kk].slot : pr[kk].row, pos) : ~0ull;
   }
 
-  // emit single positions, and one summed item per repeated key
+  // emit single positions, one item per merged key, and the entries of each
+  // other repeated key together, in position order, from its first entry
   bool emit[KPT];
-  uint32_t d[KPT], r[KPT];
+  uint32_t d[KPT], r[KPT], ne[KPT];
 #pragma unroll
   for (int kk = 0; kk < KPT; ++kk) {
     emit[kk] = valid[kk] && (!dup[kk] || owner[kk]);
+    ne[kk] = dup[kk] && !merged[kk] ? cnt[kk] : 1u;
     d[kk] = 0;
     r[kk] = 0;
     if (emit[kk]) {
       d[kk] = group_partition(item_group(x[kk]), pb);
-      r[kk] = atomicAdd(&s_hist[d[kk]], 1u);
+      r[kk] = atomicAdd(&s_hist[d[kk]], ne[kk]);
     }
   }
   lds_barrier();
@@ -1088,9 +1099,17 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
   }
   lds_barrier();
 #pragma unroll
-  for (int kk = 0; kk < KPT; ++kk)
-    if (emit[kk])
-      items[(size_t)sbase + s_hist[d[kk]] + r[kk]] = dup[kk] && op != kOpAssign ? (x[kk] | kItemSummed) : x[kk];
+  for (int kk = 0; kk < KPT; ++kk) {
+    if (!emit[kk]) continue;
+    uint64_t* dst = items + (size_t)sbase + s_hist[d[kk]] + r[kk];
+    if (dup[kk] && !merged[kk]) {
+      const uint32_t kb = s_doff[s_hdup[hs[kk]]];
+      for (uint32_t i = 0; i < cnt[kk]; ++i)
+        dst[i] = (x[kk] & ~0x7FFFFFFFull) | (uint64_t)(uint32_t)(base + s_lanes[kb + i]);
+    } else {
+      dst[0] = merged[kk] && op != kOpAssign ? (x[kk] | kItemSummed) : x[kk];
+    }
+  }
   if (tid == 0) tile_cnt[tile] = s_cnt;
   // keys summed in chunks: add the chunks' partial sums in order
   if (op != kOpAssign && chunked) {
@@ -1567,108 +1586,103 @@ __device__ __forceinline__ void update_segments(IP it, SP seg, uint32_t S, const
   }
 }
 
-// Segments longer than kLongSeg items are put in tile order through a bitmask
-// of their tiles (a key has at most one item per tile) when there are at most
-// kMaskTiles tiles; at most kLongMax of them fit a partition.
-constexpr int kLongSeg = 32;
-constexpr int kLongMax = kRedCap / (kLongSeg + 1) + 1;
-constexpr int kMaskTiles = 1024;
-constexpr int kMaskWords = kMaskTiles / 32;
-
-// Dynamic LDS of a reduce_update block, in bytes. The first region holds the
-// gathered items and the grouping tables; once items are grouped it is reused
-// for a chunk of new keys and then for the pieces of cut segments.
-template <int NT>
-struct RedLds {
-  static constexpr size_t it = 0;                                  // u64[kRedCap] gather order
-  static constexpr size_t hash = it + 8 * (size_t)kRedCap;          // u32[2 * kRedHash]
-  static constexpr size_t inv = hash + 8 * (size_t)kRedHash;        // u16[kRedHash]
-  static constexpr size_t pl = inv + 2 * (size_t)kRedHash;          // u16[kRedCap]
-  static constexpr size_t reuse = pl + 2 * (size_t)kRedCap;         // end of the reused region
-  static constexpr size_t sorted = reuse;                           // u64[kRedCap] grouped items
-  static constexpr size_t sid = sorted + 8 * (size_t)kRedCap;       // u16[kRedCap]
-  static constexpr size_t seg = sid + 2 * (size_t)kRedCap;          // u32[kRedCap + 1]
-  static constexpr size_t pref = (seg + 4 * ((size_t)kRedCap + 1) + 15) & ~(size_t)15;  // u32[NT + 1]
-  static constexpr size_t w = (pref + 4 * ((size_t)NT + 1) + 15) & ~(size_t)15;          // u32[NT / 64]
-  static constexpr size_t w64 = (w + 4 * (size_t)(NT / 64) + 15) & ~(size_t)15;          // u64[NT / 64]
-  static constexpr size_t base = w64 + 8 * (size_t)(NT / 64);                            // u64
-  static constexpr size_t tl = base + 16;                                      // u16[kRedCap] source tile of each item
-  static constexpr size_t lid = (tl + 2 * (size_t)kRedCap + 15) & ~(size_t)15;  // u16[kRedHash] long-segment id per slot
-  static constexpr size_t mask = lid + 2 * (size_t)kRedHash;  // u32[kLongMax][kMaskWords] tiles of each long segment
-  static constexpr size_t nlong = mask + 4 * (size_t)kMaskWords * (size_t)kLongMax;  // u32
-  static constexpr size_t total = nlong + 16;
-};
-
-// Threads of a reduce_update block: 1024 (one block per CU) unless the
-// pieces of cut segments (one fp64 row per lane group) would not fit the
-// reused LDS region.
+// ---------------------------------------------------------------------------
+// Put, second kernel: one block per partition. The block gathers the
+// partition's items, groups them by key in LDS with each key's items in
+// ascending position, gives keys new in the call their rows, then sums every
+// key's gradient rows in fp64 and applies the update to its row. A partition
+// larger than the block's LDS share takes the global spill path.
+// ---------------------------------------------------------------------------
 template <class M>
-struct RedCfg {
+struct ReduceCfg {
   static constexpr int DMAX = M::LPR * M::K * M::VEC;
-  static constexpr int NT = DMAX <= 512 ? 1024 : 512;
+  // the pieces of segments cut between lane groups (one fp64 row per group,
+  // NT * K * VEC doubles) take 32 KiB at every row map
+  static constexpr int NT = DMAX <= 256 ? 1024 : DMAX <= 512 ? 512 : 256;
   static constexpr int NG = (NT / 64) * M::RPW;
+  // gradient rows a lane group has in flight in the sums, and rows it
+  // updates at a time for keys seen once (at 1024 threads a lane has 128
+  // registers: four rows in flight fit them without spilling)
+  static constexpr int B = (M::K * M::VEC >= 16) ? 2 : (M::K * M::VEC >= 8 || NT >= 1024) ? 4 : 8;
+  static constexpr int BS = B;
 };
 
-// Number of entries of pl[b, e) (u16, LDS) below j.
-__device__ __forceinline__ uint32_t count_below(const uint16_t* pl, uint32_t b, uint32_t e, uint32_t j) {
-  uint32_t r = 0;
-  uint32_t i = b;
-  for (; i < e && (i & 7u); ++i) r += pl[i] < j ? 1u : 0u;
-  const uint4* p8 = reinterpret_cast<const uint4*>(pl);
-  for (; i + 16 <= e; i += 16) {
-    const uint4 a = p8[i >> 3], c = p8[(i >> 3) + 1];
-    const uint32_t wv[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
-#pragma unroll
-    for (int t = 0; t < 8; ++t) r += ((wv[t] & 0xFFFFu) < j ? 1u : 0u) + ((wv[t] >> 16) < j ? 1u : 0u);
-  }
-  for (; i < e; ++i) r += pl[i] < j ? 1u : 0u;
-  return r;
-}
+constexpr size_t align16(size_t x) { return (x + 15) & ~(size_t)15; }
+constexpr int kMaxGroups = 256;  // lane groups of a reduce block at most
+// Segments of more than kLongSeg items are put in order through a bitmask of
+// their items' places in the gathered list (at most kMaskSegs of them per
+// partition; others compare their items pairwise).
+constexpr uint32_t kLongSeg = 32;
+constexpr int kMaskSegs = 32;
+constexpr int kMaskWords = kRedCap / 32;
+
+// Dynamic LDS of a reduce block, in bytes. The first region (gathered items
+// and grouping tables) is dead once the items are grouped; it then holds a
+// chunk of new keys (rows for keys new in the call) and after that the
+// pieces of cut segments.
+template <int NT>
+struct ReduceLds {
+  static constexpr size_t it = 0;                                    // u64[kRedCap] gather order
+  static constexpr size_t hidx = it + 8 * (size_t)kRedCap;            // u32[kRedHash]
+  static constexpr size_t hcnt = hidx + 4 * (size_t)kRedHash;         // u32[kRedHash]
+  static constexpr size_t inv = hcnt + 4 * (size_t)kRedHash;          // u16[kRedHash]
+  static constexpr size_t slot = inv + 2 * (size_t)kRedHash;          // u16[kRedCap]
+  static constexpr size_t ord = slot + 2 * (size_t)kRedCap;           // u16[kRedCap]
+  static constexpr size_t reuse = align16(ord + 2 * (size_t)kRedCap);  // end of the reused region
+  static constexpr size_t srt = reuse;                                // u64[kRedCap] grouped items
+  static constexpr size_t seg = srt + 8 * (size_t)kRedCap;            // u32[kRedCap + 1]
+  static constexpr size_t sid = align16(seg + 4 * ((size_t)kRedCap + 1));  // u16[kRedCap]
+  static constexpr size_t lid = align16(sid + 2 * (size_t)kRedCap);   // u16[kRedCap] mask of each segment
+  static constexpr size_t mask = align16(lid + 2 * (size_t)kRedCap);  // u32[kMaskSegs][kMaskWords]
+  static constexpr size_t pref = align16(mask + 4 * (size_t)kMaskSegs * kMaskWords);  // u32[NT + 1]
+  static constexpr size_t w = align16(pref + 4 * ((size_t)NT + 1));   // u32[NT / 64]
+  static constexpr size_t w64 = align16(w + 4 * (size_t)(NT / 64));   // u64[NT / 64]
+  static constexpr size_t misc = align16(w64 + 8 * (size_t)(NT / 64));  // u32[8]
+  static constexpr size_t base = misc + 32;                           // u64
+  static constexpr size_t slo = base + 16;                            // u32[kMaxGroups + 1]
+  static constexpr size_t total = align16(slo + 4 * ((size_t)kMaxGroups + 1));
+};
 
 // Groups a partition's items by key in LDS.
-// In:  it[0, mp) in gather order (tiles ascending; a tile holds at most one
-//      item per key, so a key's items are in position order).
-// Out: sorted[] = the items grouped into segments, one per distinct key; the
-//      segments that need a sum (more than one item, or an in-tile sum) come
-//      first; items of a segment in gather order; seg[s] = first item of
-//      segment s, seg[S] = mp; sid[i] = segment of sorted item i.
-//      Returns S; *n_sum = segments of the first kind; *any_fresh = whether
-//      a segment holds a key new in the call.
+// In:  it[0, mp), the partition's items in the order put_probe's tiles
+//      listed them: tiles ascending, and within a tile a key's items
+//      together in ascending position; so the items of each key appear in
+//      position order (an in-tile sum is one item at the first position it
+//      covers).
+// Out: srt[0, mp) = the items grouped into segments, one per key, each
+//      segment's items in ascending position; segments [0, SA) need a sum
+//      (more than one item, or an in-tile sum as the only item) and hold the
+//      items [0, MA); segments [SA, S) are single items that need none.
+//      seg[s] = first item of segment s, seg[S] = mp; sid[i] = segment of
+//      item i; info = {S, SA, MA, any key new in the call}.
 // Segment order: keys go to an LDS hash table with linear probing. The set of
 // occupied slots does not depend on the order of insertion, only which key
 // sits where inside a run of occupied slots does; keys are therefore given
 // the slots of their run in ascending order, and segments follow these
-// positions. So every order above depends only on the set of items, and sums
-// over segments are reproducible.
+// places. Every order above thus depends only on the set of items.
 template <int NT>
-__device__ __forceinline__ uint32_t group_items(const uint64_t* it, uint32_t mp, uint64_t* sorted,
-                                               uint16_t* sid, uint32_t* seg, uint32_t* hidx,
-                                               uint32_t* hcnt, uint16_t* inv, uint16_t* pl, uint32_t* s_w,
-                                               uint32_t* n_sum, bool* any_fresh, const uint16_t* tl,
-                                               uint16_t* lid, uint32_t* mask, uint32_t* s_nlong) {
+__device__ __forceinline__ void group_by_key(const uint64_t* it, uint32_t mp, uint64_t* srt, uint32_t* seg,
+                                             uint16_t* sid, uint32_t* hidx, uint32_t* hcnt, uint16_t* inv,
+                                             uint16_t* slot, uint16_t* ord, uint16_t* lid, uint32_t* mask,
+                                             unsigned long long* s_w64, uint32_t* info) {
   constexpr int IPT = (kRedCap + NT - 1) / NT;
   constexpr int HPT = kRedHash / NT;
+  static_assert(kRedHash % NT == 0 && kRedCap < kRedHash && kRedHash <= 65536, "grouping table sizes");
   constexpr uint32_t kNone = 0xFFFFFFFFu;
   constexpr uint32_t kMask = kRedHash - 1;
   const int tid = threadIdx.x;
-  const bool masks = tl != nullptr;  // items carry their tile (at most kMaskTiles tiles)
   for (int h = tid; h < kRedHash; h += NT) {
     hidx[h] = kNone;
     hcnt[h] = 0u;
   }
-  if (masks) {
-    for (int h = tid; h < kRedHash; h += NT) lid[h] = 0xFFFFu;
-    for (int w = tid; w < kMaskWords * kLongMax; w += NT) mask[w] = 0u;
-    if (tid == 0) *s_nlong = 0u;
-  }
+  for (int w = tid; w < kMaskSegs * kMaskWords; w += NT) mask[w] = 0u;
+  if (tid == 0) info[4] = 0u;  // masks handed out
   lds_barrier();
 
-  // 1. one hash slot per distinct group; count its items
-  uint32_t hs[IPT];
+  // 1. one slot per key (the first item to take it), and its item count
 #pragma unroll
   for (int k = 0; k < IPT; ++k) {
     const uint32_t j = tid + k * NT;
-    hs[k] = 0;
     if (j < mp) {
       const uint64_t gr = item_group(it[j]);
       uint32_t h = (uint32_t)index_hash(gr) & kMask;
@@ -1677,13 +1691,14 @@ __device__ __forceinline__ uint32_t group_items(const uint64_t* it, uint32_t mp,
         if (old == kNone || item_group(it[old]) == gr) break;
         h = (h + 1) & kMask;
       }
-      hs[k] = h;
+      slot[j] = (uint16_t)h;
       atomicAdd(&hcnt[h], 1u);
     }
   }
   lds_barrier();
 
-  // 2. position of each key within its run of occupied slots
+  // 2. the place of each key within its run of occupied slots (a run always
+  // ends: fewer items than slots)
 #pragma unroll
   for (int q = 0; q < HPT; ++q) {
     const uint32_t h = tid * HPT + q;
@@ -1699,115 +1714,407 @@ __device__ __forceinline__ uint32_t group_items(const uint64_t* it, uint32_t mp,
   }
   lds_barrier();
 
-  // 3. number segments in position order, those needing a sum first;
-  // seg[u] = item count of segment u, hcnt[slot] = u
-  uint32_t cnt[HPT], hh[HPT];
+  // 3. segment numbers and first items, places in order, segments that need
+  // a sum first (one scan of three counts of 21 bits each)
+  uint32_t cnt[HPT], hs[HPT];
   bool need[HPT], occ[HPT];
-  uint32_t n_need = 0, n_one = 0;
+  uint64_t mine = 0;
   bool fresh = false;
 #pragma unroll
   for (int q = 0; q < HPT; ++q) {
-    const uint32_t pos = tid * HPT + q;
-    occ[q] = hidx[pos] != kNone;
+    const uint32_t pl = tid * HPT + q;
+    occ[q] = hidx[pl] != kNone;  // occupied places are the occupied slots
     need[q] = false;
     cnt[q] = 0;
-    hh[q] = 0;
+    hs[q] = 0;
     if (occ[q]) {
-      hh[q] = inv[pos];
-      const uint64_t x = it[hidx[hh[q]]];
-      cnt[q] = hcnt[hh[q]];
+      hs[q] = inv[pl];
+      const uint64_t x = it[hidx[hs[q]]];
+      cnt[q] = hcnt[hs[q]];
       need[q] = cnt[q] > 1 || item_summed(x);
       fresh |= item_fresh(x);
-      n_need += need[q] ? 1u : 0u;
-      n_one += need[q] ? 0u : 1u;
+      mine += need[q] ? (1ull | ((uint64_t)cnt[q] << 21)) : (1ull << 42);
     }
   }
-  uint32_t tot;
-  const uint32_t pre = block_exclusive_scan<NT>(n_need | (n_one << 16), s_w, &tot);
-  const uint32_t NS = tot & 0xFFFFu, S = NS + (tot >> 16);
-  uint32_t u_need = pre & 0xFFFFu, u_one = NS + (pre >> 16);
+  uint64_t tot;
+  const uint64_t pre = block_exclusive_scan_u64<NT>(mine, s_w64, &tot);  // barriers: every read above is done
+  constexpr uint64_t F = (1ull << 21) - 1;
+  const uint32_t SA = (uint32_t)(tot & F), MA = (uint32_t)((tot >> 21) & F), S = SA + (uint32_t)(tot >> 42);
+  uint32_t sa = (uint32_t)(pre & F), ia = (uint32_t)((pre >> 21) & F), sb = (uint32_t)(pre >> 42);
 #pragma unroll
   for (int q = 0; q < HPT; ++q) {
     if (occ[q]) {
-      const uint32_t u = need[q] ? u_need++ : u_one++;
-      seg[u] = cnt[q];
-      hcnt[hh[q]] = u;
-      if (masks && cnt[q] > (uint32_t)kLongSeg) lid[hh[q]] = (uint16_t)atomicAdd(s_nlong, 1u);  // any id will do
+      uint32_t s, off;
+      if (need[q]) {
+        s = sa++;
+        off = ia;
+        ia += cnt[q];
+      } else {
+        s = SA + sb;
+        off = MA + sb;
+        ++sb;
+      }
+      seg[s] = off;
+      hcnt[hs[q]] = off | (s << 16);
+      hidx[hs[q]] = 0u;  // fill cursor
+      uint32_t l = 0xFFFFu;
+      if (cnt[q] > kLongSeg) {
+        l = atomicAdd(&info[4], 1u);  // which mask a long segment gets does not matter
+        if (l >= (uint32_t)kMaskSegs) l = 0xFFFFu;
+      }
+      lid[s] = (uint16_t)l;
     }
   }
-  *n_sum = NS;
-  *any_fresh = __syncthreads_or(fresh ? 1 : 0) != 0;
-
-  // 4. segment offsets (exclusive scan of counts); hidx becomes the fill
-  // cursor of each segment
-  {
-    uint32_t c[IPT];
-    uint32_t sum = 0;
-#pragma unroll
-    for (int k = 0; k < IPT; ++k) {
-      const uint32_t x = tid * IPT + k;
-      c[k] = x < S ? seg[x] : 0u;
-      sum += c[k];
-    }
-    uint32_t t2;
-    uint32_t off = block_exclusive_scan<NT>(sum, s_w, &t2);
-#pragma unroll
-    for (int k = 0; k < IPT; ++k) {
-      const uint32_t x = tid * IPT + k;
-      if (x < S) seg[x] = off;
-      off += c[k];
-    }
-    if (tid == 0) seg[S] = mp;
-    for (uint32_t x = tid; x < S; x += NT) hidx[x] = 0u;
+  if (tid == 0) {
+    seg[S] = mp;
+    info[0] = S;
+    info[1] = SA;
+    info[2] = MA;
   }
-  lds_barrier();
+  const bool any_fresh = __syncthreads_or(fresh ? 1 : 0) != 0;
+  if (tid == 0) info[3] = any_fresh ? 1u : 0u;
 
-  // 5. drop each item into its segment (any order within it)
-  uint32_t rs[IPT];
+  // 4. drop each item into its segment (any order within it); a long
+  // segment also marks its items' places in its mask
+  uint32_t sg[IPT];
 #pragma unroll
   for (int k = 0; k < IPT; ++k) {
     const uint32_t j = tid + k * NT;
-    rs[k] = 0;
+    sg[k] = 0;
     if (j < mp) {
-      rs[k] = hcnt[hs[k]];
-      pl[seg[rs[k]] + atomicAdd(&hidx[rs[k]], 1u)] = (uint16_t)j;
-      if (masks) {
-        const uint32_t l = lid[hs[k]];
-        if (l != 0xFFFFu) atomicOr(&mask[l * kMaskWords + (tl[j] >> 5)], 1u << (tl[j] & 31));
+      const uint32_t v = hcnt[slot[j]];
+      sg[k] = v >> 16;
+      ord[(v & 0xFFFFu) + atomicAdd(&hidx[slot[j]], 1u)] = (uint16_t)j;
+      const uint32_t l = lid[sg[k]];
+      if (l != 0xFFFFu) atomicOr(&mask[l * kMaskWords + (j >> 5)], 1u << (j & 31));
+    }
+  }
+  lds_barrier();
+  // 5. each item at its rank within its segment: the number of the segment's
+  // items at earlier places (the items of a key come in position order)
+#pragma unroll
+  for (int k = 0; k < IPT; ++k) {
+    const uint32_t j = tid + k * NT;
+    if (j < mp) {
+      const uint32_t b = seg[sg[k]], e = seg[sg[k] + 1];
+      uint32_t r = 0;
+      if (e - b > 1) {
+        const uint32_t l = lid[sg[k]];
+        if (l != 0xFFFFu) {
+          const uint32_t* mw = mask + l * kMaskWords;
+          const uint32_t wj = j >> 5;
+          for (uint32_t w = 0; w < wj; ++w) r += __popc(mw[w]);
+          r += __popc(mw[wj] & ((1u << (j & 31)) - 1u));
+        } else {
+          for (uint32_t i = b; i < e; ++i) r += ord[i] < j ? 1u : 0u;
+        }
+      }
+      srt[b + r] = it[j];
+      sid[b + r] = (uint16_t)sg[k];
+    }
+  }
+  lds_barrier();
+}
+
+// One lane's VEC elements of a row, fp32 (a gradient row) or fp64 (an in-tile
+// sum), as loaded.
+template <int VEC>
+struct RawRow;
+template <>
+struct RawRow<4> {
+  uint4 lo, hi;
+};
+template <>
+struct RawRow<1> {
+  uint2 lo;
+};
+
+template <int VEC>
+__device__ __forceinline__ void load_raw(RawRow<VEC>& r, const float* __restrict__ grads,
+                                         const double* __restrict__ partials, size_t off, bool summed) {
+  if constexpr (VEC == 4) {
+    if (summed) {
+      const uint4* p = reinterpret_cast<const uint4*>(partials + off);
+      r.lo = p[0];
+      r.hi = p[1];
+    } else {
+      r.lo = *reinterpret_cast<const uint4*>(grads + off);
+    }
+  } else {
+    if (summed) r.lo = *reinterpret_cast<const uint2*>(partials + off);
+    else r.lo.x = *reinterpret_cast<const uint32_t*>(grads + off);
+  }
+}
+
+template <int VEC>
+__device__ __forceinline__ void add_raw(double* acc, const RawRow<VEC>& r, bool summed) {
+  if constexpr (VEC == 4) {
+    if (summed) {
+      acc[0] += __hiloint2double((int)r.lo.y, (int)r.lo.x);
+      acc[1] += __hiloint2double((int)r.lo.w, (int)r.lo.z);
+      acc[2] += __hiloint2double((int)r.hi.y, (int)r.hi.x);
+      acc[3] += __hiloint2double((int)r.hi.w, (int)r.hi.z);
+    } else {
+      acc[0] += (double)__uint_as_float(r.lo.x);
+      acc[1] += (double)__uint_as_float(r.lo.y);
+      acc[2] += (double)__uint_as_float(r.lo.z);
+      acc[3] += (double)__uint_as_float(r.lo.w);
+    }
+  } else {
+    acc[0] += summed ? __hiloint2double((int)r.lo.y, (int)r.lo.x) : (double)__uint_as_float(r.lo.x);
+  }
+}
+
+// One update step (op of c) for the rows rw[u] with on[u], given their summed
+// gradients gq[u]: the rows (and accumulators) of the N keys are loaded
+// together, updated and written back; a bounded table's counts drop.
+template <class M, int N>
+__device__ __forceinline__ void update_rows(const bool (&on)[N], const uint32_t (&rw)[N],
+                                            const typename VecT<M::VEC>::T (&gq)[N][M::K], const RedCtx& c, int q,
+                                            bool d_pow2, double inv_d) {
+  constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K;
+  using V = typename VecT<VEC>::T;
+  const int D = c.D;
+  V w[N][K];
+  float G[N];
+#pragma unroll
+  for (int u = 0; u < N; ++u) {
+    G[u] = 0.0f;
+    if (on[u]) {
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const int col = (k * LPR + q) * VEC;
+        if (col < D) w[u][k] = load_vec<VEC>(c.rows + (size_t)rw[u] * (size_t)D + col);
+      }
+      if (c.op == kOpAdagrad) G[u] = c.state[rw[u]];
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < N; ++u)
+    if (on[u]) {
+      SegmentOps<M>::update(c.op, gq[u], w[u], G[u], c.rows, c.state, rw[u], D, q, d_pow2, inv_d, c.lr, c.eps);
+      if (c.clock != nullptr && q == 0) put_clock(c.clock, rw[u]);
+    }
+}
+
+// Sums and updates of a grouped partition (update op != kOpAssign).
+// Lane group gid takes an even share [lo, hi) of the items of segments that
+// need a sum and walks it B items at a time (their gradient rows, and the row
+// and accumulator of each segment starting among them, loaded together),
+// accumulating in fp64; a segment that starts and ends in the share is updated
+// as soon as it ends. The part of a segment begun in an earlier share goes to
+// LDS (a group has at most one); after a barrier, the group where a segment
+// cut between shares began adds the later parts in share order and updates
+// it. Each group also updates an even share of the keys seen once (g is their
+// gradient row).
+template <class M, int NT>
+__device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32_t* seg, const uint16_t* sid,
+                                               uint32_t S, uint32_t SA, uint32_t MA, const RedCtx& c,
+                                               double* s_piece, uint32_t* s_slo) {
+  using Ops = SegmentOps<M>;
+  using Cfg = ReduceCfg<M>;
+  constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K;
+  constexpr int NG = Cfg::NG, B = Cfg::B, BS = Cfg::BS, DMAX = Cfg::DMAX;
+  static_assert(NG <= kMaxGroups, "lane groups");
+  using V = typename VecT<VEC>::T;
+  const int lane = threadIdx.x & 63;
+  const int q = lane % LPR;
+  const int gid = (threadIdx.x >> 6) * M::RPW + lane / LPR;
+  const int D = c.D;
+  const bool d_pow2 = (D & (D - 1)) == 0;
+  const double inv_d = 1.0 / (double)D;
+
+  for (int h = threadIdx.x; h <= NG; h += NT) s_slo[h] = (uint32_t)((uint64_t)MA * h / NG);
+  lds_barrier();
+  const uint32_t lo = s_slo[gid], hi = s_slo[gid + 1];
+
+  auto put_piece = [&](const double (&a)[K][VEC]) {
+    double* dst = s_piece + (size_t)gid * DMAX;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int col = (k * LPR + q) * VEC;
+#pragma unroll
+      for (int x = 0; x < VEC; ++x)
+        if (col + x < D) dst[col + x] = a[k][x];
+    }
+  };
+  auto to_f32 = [&](V (&g)[K], const double (&a)[K][VEC]) {
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+#pragma unroll
+      for (int x = 0; x < VEC; ++x) VecT<VEC>::set(g[k], x, (float)a[k][x]);
+  };
+  // ---- segments that need a sum ----
+  // The row and accumulator of a segment this group owns are loaded with the
+  // batch that holds its first item; at most one segment is open at a time.
+  double acc[K][VEC];
+  Ops::zero(acc);
+  V wc[K];
+  float Gc = 0.0f;
+  uint32_t rowc = 0;
+  bool last_ends = true, last_owned = true;
+  uint32_t last_end = 0;
+  for (uint32_t j0 = lo; j0 < hi; j0 += B) {
+    uint64_t x[B];
+    uint32_t fst[B], end[B];
+    RawRow<VEC> raw[B][K];
+    V wl[B][K];
+    float Gl[B];
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const uint32_t j = j0 + u;
+      x[u] = 0;
+      fst[u] = 0;
+      end[u] = 0;
+      Gl[u] = 0.0f;
+      if (j < hi) {
+        x[u] = srt[j];
+        const uint32_t s = sid[j];
+        fst[u] = seg[s];
+        end[u] = seg[s + 1];
+        const bool summ = item_summed(x[u]);
+        const size_t base = (size_t)item_pos(x[u]) * (size_t)D;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const int col = (k * LPR + q) * VEC;
+          if (col < D) load_raw<VEC>(raw[u][k], c.grads, c.partials, base + col, summ);
+        }
+        if (fst[u] == j && j >= lo) {  // an owned segment starts: its row (the first item carries it)
+          const uint32_t r = item_tag(x[u]);
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            const int col = (k * LPR + q) * VEC;
+            if (col < D) wl[u][k] = load_vec<VEC>(c.rows + (size_t)r * (size_t)D + col);
+          }
+          if (c.op == kOpAdagrad) Gl[u] = c.state[r];
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const uint32_t j = j0 + u;
+      if (j < hi) {
+        if (fst[u] == j) {  // (j >= lo here)
+          rowc = item_tag(x[u]);
+#pragma unroll
+          for (int k = 0; k < K; ++k) wc[k] = wl[u][k];
+          Gc = Gl[u];
+        }
+        const bool summ = item_summed(x[u]);
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const int col = (k * LPR + q) * VEC;
+          if (col < D) add_raw<VEC>(acc[k], raw[u][k], summ);
+        }
+        last_ends = end[u] == j + 1;
+        last_owned = fst[u] >= lo;
+        last_end = end[u];
+        if (last_ends) {
+          if (last_owned) {
+            V g[K];
+            to_f32(g, acc);
+            Ops::update(c.op, g, wc, Gc, c.rows, c.state, rowc, D, q, d_pow2, inv_d, c.lr, c.eps);
+            if (c.clock != nullptr && q == 0) put_clock(c.clock, rowc);
+          } else {
+            put_piece(acc);  // the end of a segment begun in an earlier share
+          }
+          Ops::zero(acc);
+        }
       }
     }
   }
-  lds_barrier();
+  const bool tail = lo < hi && !last_ends && last_owned;
+  if (lo < hi && !last_ends && !last_owned) put_piece(acc);  // the share lies inside one segment
 
-  // 6. order a segment's items by gather index
+  // ---- keys seen once: g is the key's gradient row ----
+  {
+    const uint32_t S1 = S - SA;
+    const uint32_t k0 = SA + (uint32_t)((uint64_t)S1 * gid / NG), k1 = SA + (uint32_t)((uint64_t)S1 * (gid + 1) / NG);
+    for (uint32_t s0 = k0; s0 < k1; s0 += BS) {
+      bool on[BS];
+      uint32_t rw[BS];
+      V gq[BS][K];
 #pragma unroll
-  for (int k = 0; k < IPT; ++k) {
-    const uint32_t j = tid + k * NT;
-    if (j < mp) {
-      const uint32_t b = seg[rs[k]], e = seg[rs[k] + 1];
-      uint32_t rank = 0;
-      const uint32_t l = masks ? lid[hs[k]] : 0xFFFFu;
-      if (l != 0xFFFFu) {  // the segment's items in earlier tiles
-        const uint32_t t = tl[j], w = t >> 5;
-        const uint4* m4 = reinterpret_cast<const uint4*>(mask + l * kMaskWords);
-        for (uint32_t x4 = 0; x4 <= (w >> 2); ++x4) {
-          const uint4 m = m4[x4];
-          const uint32_t mw[4] = {m.x, m.y, m.z, m.w};
+      for (int u = 0; u < BS; ++u) {
+        const uint32_t s = s0 + u;
+        on[u] = s < k1;
+        rw[u] = 0;
+        if (on[u]) {
+          const uint64_t xs = srt[MA + (s - SA)];
+          rw[u] = item_tag(xs);
+          const float* gr = c.grads + (size_t)item_pos(xs) * (size_t)D;
 #pragma unroll
-          for (uint32_t y = 0; y < 4; ++y) {
-            const uint32_t x = x4 * 4 + y;
-            rank += x < w ? __popc(mw[y]) : x == w ? __popc(mw[y] & ((1u << (t & 31)) - 1u)) : 0u;
+          for (int k = 0; k < K; ++k) {
+            const int col = (k * LPR + q) * VEC;
+            if (col < D) gq[u][k] = load_vec<VEC>(gr + col);
           }
         }
-      } else if (e - b > 1) {
-        rank = count_below(pl, b, e, j);
       }
-      sorted[b + rank] = it[j];
-      sid[b + rank] = (uint16_t)rs[k];
+      update_rows<M, BS>(on, rw, gq, c, q, d_pow2, inv_d);
     }
   }
-  lds_barrier();
-  return S;
+
+  __syncthreads();  // the pieces of cut segments are in LDS
+  if (tail) {
+    // the segment ends in share hl: add the pieces of shares gid+1 .. hl in
+    // order (an empty share holds none)
+    uint32_t hl = gid + 1;
+    while (hl + 1 < (uint32_t)NG && s_slo[hl + 1] < last_end) ++hl;
+    for (uint32_t h = gid + 1; h <= hl; ++h) {
+      if (s_slo[h] >= s_slo[h + 1]) continue;
+      const double* src = s_piece + (size_t)h * DMAX;
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const int col = (k * LPR + q) * VEC;
+#pragma unroll
+        for (int xx = 0; xx < VEC; ++xx)
+          if (col + xx < D) acc[k][xx] += src[col + xx];
+      }
+    }
+    V g[K];
+    to_f32(g, acc);  // the row and accumulator were loaded with the segment's first item
+    Ops::update(c.op, g, wc, Gc, c.rows, c.state, rowc, D, q, d_pow2, inv_d, c.lr, c.eps);
+    if (c.clock != nullptr && q == 0) put_clock(c.clock, rowc);
+  }
+}
+
+// Put with the assignment op: each key's row becomes the value row at its
+// last position. Lane groups take even shares of the segments.
+template <class M, int NT>
+__device__ __forceinline__ void assign_segments(const uint64_t* srt, const uint32_t* seg, uint32_t S,
+                                                const RedCtx& c) {
+  using Cfg = ReduceCfg<M>;
+  constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, NG = Cfg::NG, BS = Cfg::BS;
+  using V = typename VecT<VEC>::T;
+  const int lane = threadIdx.x & 63;
+  const int q = lane % LPR;
+  const int gid = (threadIdx.x >> 6) * M::RPW + lane / LPR;
+  const int D = c.D;
+  const uint32_t k0 = (uint32_t)((uint64_t)S * gid / NG), k1 = (uint32_t)((uint64_t)S * (gid + 1) / NG);
+  for (uint32_t s0 = k0; s0 < k1; s0 += BS) {
+    V v[BS][K];
+    uint32_t rw[BS];
+#pragma unroll
+    for (int u = 0; u < BS; ++u) {
+      const uint32_t s = s0 + u;
+      rw[u] = 0;
+      if (s < k1) {
+        rw[u] = item_tag(srt[seg[s]]);
+        const float* src = c.grads + (size_t)item_pos(srt[seg[s + 1] - 1]) * (size_t)D;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const int col = (k * LPR + q) * VEC;
+          if (col < D) v[u][k] = load_vec<VEC>(src + col);
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < BS; ++u) {
+      if (s0 + u >= k1) continue;
+      SegmentOps<M>::assign(v[u], c.rows, rw[u], D, q);
+      if (c.clock != nullptr && q == 0) put_clock(c.clock, rw[u]);
+    }
+  }
 }
 
 // Partition larger than the block's LDS share: the same steps on a global
@@ -1856,42 +2163,36 @@ __device__ __forceinline__ void reduce_partition_global(uint32_t p, uint32_t mp,
   update_segments<M, NT>(it, seg, S, c);
 }
 
-// ---------------------------------------------------------------------------
-// Put, second kernel (one block per partition): gathers the partition's
-// items, groups them into segments, gives keys new in the call their rows,
-// and writes the grouped items, per-item segment ranges and per-segment
-// descriptors for the two flat kernels that follow. A partition too large
-// for LDS is summed and updated here, in a global scratch area.
-// ---------------------------------------------------------------------------
 template <class M, int NT>
-__global__ __launch_bounds__(NT) void k_put_group(
+__global__ __launch_bounds__(NT) void k_put_reduce(
     Bucket* __restrict__ idx, const uint64_t* __restrict__ items, const uint32_t* __restrict__ meta,
     int ntiles, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
-    const float* __restrict__ grads, const double* __restrict__ partials, float* __restrict__ rows,
+    const float* __restrict__ grads, double* __restrict__ partials, float* __restrict__ rows,
     float* __restrict__ state, int D, uint64_t seed, float lr, float eps, int64_t capacity, Ctrl* ctrl,
-    uint64_t epoch, uint64_t* __restrict__ spill, uint64_t spill_words, uint64_t* __restrict__ gitems,
-    uint32_t* __restrict__ gdesc, PartMeta* __restrict__ pmeta, int op, unsigned long long* __restrict__ clock) {
-  using L = RedLds<NT>;
+    uint64_t epoch, uint64_t* __restrict__ spill, uint64_t spill_words, int op,
+    unsigned long long* __restrict__ clock) {
+  using L = ReduceLds<NT>;
   constexpr int IPT = (kRedCap + NT - 1) / NT;
   extern __shared__ __align__(16) unsigned char s_raw[];
   uint64_t* s_it = reinterpret_cast<uint64_t*>(s_raw + L::it);
-  uint32_t* s_hidx = reinterpret_cast<uint32_t*>(s_raw + L::hash);
-  uint32_t* s_hcnt = s_hidx + kRedHash;
+  uint32_t* s_hidx = reinterpret_cast<uint32_t*>(s_raw + L::hidx);
+  uint32_t* s_hcnt = reinterpret_cast<uint32_t*>(s_raw + L::hcnt);
   uint16_t* s_inv = reinterpret_cast<uint16_t*>(s_raw + L::inv);
-  uint16_t* s_pl = reinterpret_cast<uint16_t*>(s_raw + L::pl);
-  double* s_part = reinterpret_cast<double*>(s_raw);              // reused region
-  uint64_t* s_chunk = reinterpret_cast<uint64_t*>(s_raw);         // reused region
-  uint64_t* s_sorted = reinterpret_cast<uint64_t*>(s_raw + L::sorted);
-  uint16_t* s_sid = reinterpret_cast<uint16_t*>(s_raw + L::sid);
+  uint16_t* s_slot = reinterpret_cast<uint16_t*>(s_raw + L::slot);
+  uint16_t* s_ord = reinterpret_cast<uint16_t*>(s_raw + L::ord);
+  double* s_piece = reinterpret_cast<double*>(s_raw);       // reused region
+  uint64_t* s_chunk = reinterpret_cast<uint64_t*>(s_raw);   // reused region
+  uint64_t* s_srt = reinterpret_cast<uint64_t*>(s_raw + L::srt);
   uint32_t* s_seg = reinterpret_cast<uint32_t*>(s_raw + L::seg);
+  uint16_t* s_sid = reinterpret_cast<uint16_t*>(s_raw + L::sid);
+  uint16_t* s_lid = reinterpret_cast<uint16_t*>(s_raw + L::lid);
+  uint32_t* s_mask = reinterpret_cast<uint32_t*>(s_raw + L::mask);
   uint32_t* s_pref = reinterpret_cast<uint32_t*>(s_raw + L::pref);
   uint32_t* s_w = reinterpret_cast<uint32_t*>(s_raw + L::w);
   unsigned long long* s_w64 = reinterpret_cast<unsigned long long*>(s_raw + L::w64);
+  uint32_t* s_info = reinterpret_cast<uint32_t*>(s_raw + L::misc);
   uint64_t* s_base = reinterpret_cast<uint64_t*>(s_raw + L::base);
-  uint16_t* s_tl = reinterpret_cast<uint16_t*>(s_raw + L::tl);
-  uint16_t* s_lid = reinterpret_cast<uint16_t*>(s_raw + L::lid);
-  uint32_t* s_mask = reinterpret_cast<uint32_t*>(s_raw + L::mask);
-  uint32_t* s_nlong = reinterpret_cast<uint32_t*>(s_raw + L::nlong);
+  uint32_t* s_slo = reinterpret_cast<uint32_t*>(s_raw + L::slo);
 
   const uint32_t p = blockIdx.x;
   const int tid = threadIdx.x;
@@ -1900,7 +2201,6 @@ __global__ __launch_bounds__(NT) void k_put_group(
   const uint32_t* pm = meta + (size_t)p * ntiles;
   const bool one_chunk = ntiles <= NT;  // common case: one thread per tile
   const uint32_t mt0 = one_chunk && tid < ntiles ? pm[tid] : 0u;
-  if (tid == 0) pmeta[p] = PartMeta{0u, 0u, 0u, 0u};  // nothing for the flat kernels unless set below
 
   // entries of this partition in every tile
   uint32_t mp, pre0 = 0;
@@ -1935,7 +2235,7 @@ __global__ __launch_bounds__(NT) void k_put_group(
   const RedCtx c{op, idx, grads, partials, rows, state, D, seed, lr, eps, size0, clock};
   if (mp > (uint32_t)kRedCap) {
     reduce_partition_global<M, NT>(p, mp, items, meta, ntiles, c, newlist, tile_cnt, ctrl, spill, spill_words,
-                                   s_part, s_pref, s_w, s_w64, s_base);
+                                   s_piece, s_pref, s_w, s_w64, s_base);
     return;
   }
 
@@ -1952,12 +2252,10 @@ __global__ __launch_bounds__(NT) void k_put_group(
       s_pref[tid] = pre | (mt << 16);  // items before this tile | offset in the tile
       __syncthreads();
       uint64_t v[IPT];
-      uint32_t src[IPT];
 #pragma unroll
       for (int e = 0; e < IPT; ++e) {
         const uint32_t k = tid + e * NT;
         v[e] = 0;
-        src[e] = 0;
         if (k < tot) {
           int lo = 0, hi = nt - 1;
           while (lo < hi) {
@@ -1966,428 +2264,25 @@ __global__ __launch_bounds__(NT) void k_put_group(
             else hi = mid - 1;
           }
           const uint32_t pe = s_pref[lo];
-          src[e] = (uint32_t)(t0 + lo);
           v[e] = items[(size_t)(t0 + lo) * kPutTile + (pe >> 16) + (k - (pe & 0xFFFFu))];
         }
       }
 #pragma unroll
       for (int e = 0; e < IPT; ++e) {
         const uint32_t k = tid + e * NT;
-        if (k < tot) {
-          s_it[dst + k] = v[e];
-          s_tl[dst + k] = (uint16_t)src[e];
-        }
+        if (k < tot) s_it[dst + k] = v[e];
       }
       dst += tot;
       __syncthreads();
     }
   }
 
-  uint32_t n_sum;
-  bool any_fresh;
-  const uint32_t S = group_items<NT>(s_it, mp, s_sorted, s_sid, s_seg, s_hidx, s_hcnt, s_inv, s_pl, s_w, &n_sum,
-                                    &any_fresh, ntiles <= kMaskTiles ? s_tl : nullptr, s_lid, s_mask, s_nlong);
-  if (any_fresh)
-    resolve_new_rows<NT>(s_sorted, s_seg, S, c, newlist, tile_cnt, ntiles, s_pref, s_w, s_w64, s_chunk);
-
-  // ---- hand the grouped partition to the flat kernel ----
-  uint64_t* gi = gitems + (size_t)p * kRedCap;
-  uint32_t* gd = gdesc + (size_t)p * kRedCap;
-  if (op == kOpAssign) {
-    // one item per key, its last (the value that wins), all as keys seen once;
-    // a new key's first item carries its row
-    for (uint32_t s = tid; s < S; s += NT) {
-      const uint64_t x0 = s_sorted[s_seg[s]], xl = s_sorted[s_seg[s + 1] - 1];
-      gi[s] = make_item(item_fresh(x0), item_tag(x0), item_pos(xl));
-    }
-    if (tid == 0) pmeta[p] = PartMeta{0u, S, 0u, 0u};
-    return;
-  }
-  for (uint32_t i = tid; i < mp; i += NT) {
-    gi[i] = s_sorted[i];
-    const uint32_t s = s_sid[i];
-    gd[i] = s_seg[s] | (s_seg[s + 1] << 16);
-  }
-  if (tid == 0) pmeta[p] = PartMeta{s_seg[n_sum], S, n_sum, 0u};
-}
-
-// The exclusive prefixes over partitions of the phase-A items (into outA)
-// and of the keys seen once (into out1), np + 1 entries each, from one scan of
-// both counts packed in 64 bits. Returns the two totals.
-template <int NT>
-__device__ __forceinline__ uint2 partition_prefix2(const PartMeta* __restrict__ pmeta, int np, uint32_t* outA,
-                                                   uint32_t* out1, unsigned long long* s_w64) {
-  constexpr int kPer = (kMaxParts + NT - 1) / NT;
-  const int per = (np + NT - 1) / NT;
-  const int b = threadIdx.x * per;
-  uint64_t pv[kPer];
-  uint64_t sum = 0;
-#pragma unroll
-  for (int k = 0; k < kPer; ++k) {
-    pv[k] = 0;
-    if (k < per && b + k < np) {
-      const PartMeta m = pmeta[b + k];
-      pv[k] = ((uint64_t)m.mA << 32) | (uint64_t)(m.S - m.nsum);
-      sum += pv[k];
-    }
-  }
-  uint64_t tot;
-  uint64_t off = block_exclusive_scan_u64<NT>(sum, s_w64, &tot);
-#pragma unroll
-  for (int k = 0; k < kPer; ++k) {
-    if (k < per && b + k < np) {
-      outA[b + k] = (uint32_t)(off >> 32);
-      out1[b + k] = (uint32_t)off;
-      off += pv[k];
-    }
-  }
-  if (threadIdx.x == 0) {
-    outA[np] = (uint32_t)(tot >> 32);
-    out1[np] = (uint32_t)tot;
-  }
-  lds_barrier();
-  return make_uint2((uint32_t)(tot >> 32), (uint32_t)tot);
-}
-
-// Largest partition p with pre[p] <= j (pre: np + 1 ascending prefix values).
-__device__ __forceinline__ int partition_of(const uint32_t* pre, int np, uint32_t j) {
-  int lo = 0, hi = np - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (pre[mid] <= j) lo = mid;
-    else hi = mid - 1;
-  }
-  return lo;
-}
-
-// ---------------------------------------------------------------------------
-// Put, third kernel (flat): sum and update. All items of segments that need a
-// sum (phase A items), over all partitions, form one sequence; block b takes
-// the contiguous range between b * NA / blocks and (b + 1) * NA / blocks,
-// each end moved forward to the next segment start, so that no segment is
-// split between blocks. Its lane groups split the range evenly and sum their
-// slices in fp64 (a segment cut between slices is completed by the group
-// where it starts, adding the following groups' pieces from LDS in order);
-// each completed segment leaves g = fp32(sum) over the partials row of its
-// last item and an entry (row, that position) in an LDS list. After a
-// barrier the groups split the list and the block's share of the keys seen
-// once (no sum needed, g is their gradient row) evenly and apply one
-// row-wise Adagrad step per key.
-// ---------------------------------------------------------------------------
-// put_apply blocks: kPerCU per CU at least, and at most about kItems phase-A
-// items each (the grid grows with the batch). Two 512-thread blocks per CU
-// overlap one block's barriers and combination steps with the other's loads.
-template <class M>
-struct ApplyCfg {
-  static constexpr int NT = RedCfg<M>::NT < 512 ? RedCfg<M>::NT : 512;
-  static constexpr int kPerCU = 1024 / NT;
-  static constexpr int kItems = 2 * NT;
-};
-
-template <class M, int NT>
-struct ApplyLds {
-  static constexpr int NG = (NT / 64) * M::RPW;
-  static constexpr int DMAX = M::LPR * M::K * M::VEC;
-  // segments one block can complete: at most its items, which are at most
-  // kItems plus one segment (a partition's items) beyond the even share
-  static constexpr int kList = ApplyCfg<M>::kItems + kRedCap + 64;
-  static constexpr size_t part = 0;                                              // fp64 [NG][D]
-  static constexpr size_t done = part + sizeof(double) * (size_t)NG * DMAX;       // uint2 [kList]
-  static constexpr size_t sgl = done + sizeof(uint2) * (size_t)kList;             // u64 [kItems] the block's singles
-  static constexpr size_t pre = sgl + sizeof(uint64_t) * (size_t)ApplyCfg<M>::kItems;  // u32 [2 * (np + 1)]
-  static constexpr size_t bytes(int np) { return pre + sizeof(uint32_t) * 2 * ((size_t)np + 1); }
-};
-
-template <class M, int NT>
-__global__ __launch_bounds__(NT) void k_put_apply(const uint64_t* __restrict__ gitems,
-                                                  const uint32_t* __restrict__ gdesc,
-                                                  const PartMeta* __restrict__ pmeta, int np,
-                                                  const float* __restrict__ grads, double* __restrict__ partials,
-                                                  float* __restrict__ rows, float* __restrict__ state, int D,
-                                                  int op, float lr, float eps, Ctrl* ctrl,
-                                                  unsigned long long* __restrict__ clock) {
-  using Ops = SegmentOps<M>;
-  using LA = ApplyLds<M, NT>;
-  constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
-  constexpr int NG = LA::NG;
-  constexpr int B = (K * VEC >= 8) ? 2 : 4;
-  constexpr int BB = (K * VEC >= 8) ? 2 : 4;
-  using V = typename VecT<VEC>::T;
-  extern __shared__ __align__(16) unsigned char s_dyn[];
-  double* s_part = reinterpret_cast<double*>(s_dyn + LA::part);
-  uint2* s_done = reinterpret_cast<uint2*>(s_dyn + LA::done);
-  uint64_t* s_sgl = reinterpret_cast<uint64_t*>(s_dyn + LA::sgl);
-  uint32_t* s_pa = reinterpret_cast<uint32_t*>(s_dyn + LA::pre);  // phase-A items before each partition
-  uint32_t* s_p1 = s_pa + np + 1;                                  // keys seen once before each partition
-  __shared__ uint32_t s_hpos[NG];     // position of the item where a group's head piece ended
-  __shared__ uint32_t s_slo[NG + 1];  // first item of each group's slice, and the block's end
-  __shared__ uint32_t s_rng[2];
-  __shared__ uint32_t s_ndone;
-
-  __shared__ unsigned long long s_w64[NT / 64];
-  const uint2 totals = partition_prefix2<NT>(pmeta, np, s_pa, s_p1, s_w64);
-  const uint32_t NA = totals.x, N1 = totals.y;
-  if (NA + N1 == 0) return;
-  const int lane = threadIdx.x & 63;
-  const int g = lane / LPR;
-  const int q = lane % LPR;
-  const int gid = (threadIdx.x >> 6) * RPW + g;
-  const uint32_t nb = gridDim.x, b = blockIdx.x;
-
-  // the block's phase-A range: an even share, both ends moved to the nearer
-  // boundary of the segment they fall in
-  if (threadIdx.x < 2) {
-    uint32_t t = (uint32_t)((uint64_t)(b + threadIdx.x) * NA / nb);
-    if (t < NA) {
-      const int p0 = partition_of(s_pa, np, t);
-      const uint32_t d0 = gdesc[(size_t)p0 * kRedCap + (t - s_pa[p0])];
-      const uint32_t f0 = s_pa[p0] + (d0 & 0xFFFFu), e0 = s_pa[p0] + (d0 >> 16);
-      if (f0 != t) t = (t - f0 <= e0 - t) ? f0 : e0;  // the nearer end of the segment holding t
-    }
-    s_rng[threadIdx.x] = t;
-  }
-  if (threadIdx.x == 0) s_ndone = 0;
-  lds_barrier();
-  const uint32_t A0 = s_rng[0], A1 = s_rng[1];
-  for (int h = threadIdx.x; h <= NG; h += NT) s_slo[h] = A0 + (uint32_t)((uint64_t)(A1 - A0) * h / NG);
-  // this group's keys seen once: [k0, k1) of the block's share
-  const uint32_t K0 = (uint32_t)((uint64_t)b * N1 / nb), K1 = (uint32_t)((uint64_t)(b + 1) * N1 / nb);
-  const uint32_t k0 = K0 + (uint32_t)((uint64_t)(K1 - K0) * gid / NG);
-  const uint32_t k1 = K0 + (uint32_t)((uint64_t)(K1 - K0) * (gid + 1) / NG);
-  // the items of the block's keys seen once, [K0, K1) (at most kItems), are
-  // loaded now, a few per thread, and kept in LDS for phase B
-  constexpr int SPT = (ApplyCfg<M>::kItems + NT - 1) / NT;
-  uint64_t xs[SPT];
-#pragma unroll
-  for (int u = 0; u < SPT; ++u) {
-    const uint32_t k = K0 + threadIdx.x + u * NT;
-    xs[u] = 0;
-    if (k < K1) {
-      const int p1 = partition_of(s_p1, np, k);
-      const uint32_t first_single = s_pa[p1 + 1] - s_pa[p1];  // singles follow the phase-A items
-      xs[u] = gitems[(size_t)p1 * kRedCap + first_single + (k - s_p1[p1])];
-    }
-  }
-  lds_barrier();  // the loaded items stay in flight
-  const uint32_t lo = s_slo[gid], hi = s_slo[gid + 1];
-
-  auto put_row = [&](double* dst, const double (&a)[K][VEC]) {
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-      const int col = (k * LPR + q) * VEC;
-#pragma unroll
-      for (int xx = 0; xx < VEC; ++xx)
-        if (col + xx < D) dst[col + xx] = a[k][xx];
-    }
-  };
-  auto complete = [&](uint32_t row, uint32_t pos) {
-    if (q == 0) {
-      const uint32_t k = atomicAdd(&s_ndone, 1u);
-      if (k < (uint32_t)LA::kList) s_done[k] = make_uint2(row, pos);
-      else atomicCAS(&ctrl->latched, 0, -4);  // cannot happen: kList bounds a block's range
-    }
-  };
-
-  // ---- phase A: fp64 sums of the block's segments ----
-  {
-    int p = lo < hi ? partition_of(s_pa, np, lo) : 0;
-    double acc[K][VEC];
-    Ops::zero(acc);
-    // a batch's items are loaded one batch ahead of their gradient rows
-    uint64_t xn[B] = {};
-    uint32_t dn[B] = {}, bn[B] = {};
-    auto load_items = [&](uint32_t j0) {
-#pragma unroll
-      for (int u = 0; u < B; ++u) {
-        const uint32_t j = j0 + u;
-        xn[u] = 0;
-        dn[u] = 0;
-        bn[u] = 0;
-        if (j < hi) {
-          while (s_pa[p + 1] <= j) ++p;
-          const size_t at = (size_t)p * kRedCap + (j - s_pa[p]);
-          xn[u] = gitems[at];
-          dn[u] = gdesc[at];
-          bn[u] = s_pa[p];
-        }
-      }
-    };
-    if (lo < hi) load_items(lo);
-    bool last_ends = true, last_owned = true;
-    uint32_t last_end = 0, cur_row = 0;
-    for (uint32_t j0 = lo; j0 < hi; j0 += B) {
-      uint64_t x[B];
-      uint32_t fst[B], end[B];
-#pragma unroll
-      for (int u = 0; u < B; ++u) {
-        x[u] = xn[u];
-        fst[u] = bn[u] + (dn[u] & 0xFFFFu);
-        end[u] = bn[u] + (dn[u] >> 16);
-      }
-      V gv[B][K];
-      double pv[B][K][VEC];
-#pragma unroll
-      for (int u = 0; u < B; ++u) {
-        if (j0 + u < hi) {
-          if (item_summed(x[u])) {
-            const double* pr = partials + (size_t)item_pos(x[u]) * (size_t)D;
-#pragma unroll
-            for (int k = 0; k < K; ++k) {
-              const int col = (k * LPR + q) * VEC;
-#pragma unroll
-              for (int v = 0; v < VEC; ++v)
-                if (col + v < D) pv[u][k][v] = pr[col + v];
-            }
-          } else {
-            const float* gr = grads + (size_t)item_pos(x[u]) * (size_t)D;
-#pragma unroll
-            for (int k = 0; k < K; ++k) {
-              const int col = (k * LPR + q) * VEC;
-              if (col < D) gv[u][k] = load_vec<VEC>(gr + col);
-            }
-          }
-        }
-      }
-      if (j0 + B < hi) load_items(j0 + B);
-#pragma unroll
-      for (int u = 0; u < B; ++u) {
-        const uint32_t j = j0 + u;
-        if (j >= hi) continue;
-        if (fst[u] == j) cur_row = item_tag(x[u]);  // the first item of a segment carries its row
-        const bool summ = item_summed(x[u]);
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-          const int col = (k * LPR + q) * VEC;
-          if (col < D) {
-#pragma unroll
-            for (int xx = 0; xx < VEC; ++xx)
-              acc[k][xx] += summ ? pv[u][k][xx] : (double)VecT<VEC>::get(gv[u][k], xx);
-          }
-        }
-        last_ends = end[u] == j + 1;
-        last_owned = fst[u] >= lo;
-        last_end = end[u];
-        if (last_ends) {
-          if (last_owned) {
-            Ops::store_g(acc, partials, item_pos(x[u]), D, q);
-            complete(cur_row, item_pos(x[u]));
-          } else {
-            put_row(s_part + (size_t)gid * D, acc);  // the group's head piece
-            if (q == 0) s_hpos[gid] = item_pos(x[u]);
-          }
-          Ops::zero(acc);
-        }
-      }
-    }
-    // the slice ends inside a segment: the piece of one that began before the
-    // slice goes to LDS; one that began in the slice is completed below
-    const bool tail = lo < hi && !last_ends && last_owned;
-    if (lo < hi && !last_ends && !last_owned) put_row(s_part + (size_t)gid * D, acc);
-    lds_barrier();
-    if (tail) {
-      // the segment ends in slice hl, inside this block: add the pieces of
-      // slices gid+1 .. hl in order (empty slices hold no piece), loading
-      // kTU at a time
-      constexpr int kTU = 2;
-      uint32_t hl = gid + 1;
-      while (hl + 1 < (uint32_t)NG && s_slo[hl + 1] < last_end) ++hl;
-      for (uint32_t h0 = gid + 1; h0 <= hl; h0 += kTU) {
-        double pcs[kTU][K][VEC];
-        bool use[kTU];
-#pragma unroll
-        for (int t = 0; t < kTU; ++t) {
-          const uint32_t h = h0 + t;
-          use[t] = h <= hl && s_slo[h] < s_slo[h + 1];
-          if (use[t]) {
-#pragma unroll
-            for (int k = 0; k < K; ++k) {
-              const int col = (k * LPR + q) * VEC;
-#pragma unroll
-              for (int xx = 0; xx < VEC; ++xx)
-                if (col + xx < D) pcs[t][k][xx] = s_part[(size_t)h * D + col + xx];
-            }
-          }
-        }
-#pragma unroll
-        for (int t = 0; t < kTU; ++t) {
-          if (!use[t]) continue;
-#pragma unroll
-          for (int k = 0; k < K; ++k) {
-            const int col = (k * LPR + q) * VEC;
-#pragma unroll
-            for (int xx = 0; xx < VEC; ++xx)
-              if (col + xx < D) acc[k][xx] += pcs[t][k][xx];
-          }
-        }
-      }
-      Ops::store_g(acc, partials, s_hpos[hl], D, q);
-      complete(cur_row, s_hpos[hl]);
-    }
-#pragma unroll
-    for (int u = 0; u < SPT; ++u) {
-      const uint32_t k = K0 + threadIdx.x + u * NT;
-      if (k < K1) s_sgl[k - K0] = xs[u];
-    }
-    __syncthreads();
-  }
-
-  // ---- phase B: one Adagrad step per key ----
-  const bool d_pow2 = (D & (D - 1)) == 0;
-  const double inv_d = 1.0 / (double)D;
-  const uint32_t nd = min(s_ndone, (uint32_t)LA::kList);
-  auto update_batch = [&](const uint32_t (&row)[BB], const float* const (&src)[BB], const bool (&on)[BB]) {
-    V gf[BB][K], w[BB][K];
-    float Gs[BB];
-#pragma unroll
-    for (int u = 0; u < BB; ++u) {
-      Gs[u] = 0.0f;
-      if (on[u]) {
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-          const int col = (k * LPR + q) * VEC;
-          if (col < D) {
-            gf[u][k] = load_vec<VEC>(src[u] + col);
-            if (op != kOpAssign) w[u][k] = load_vec<VEC>(rows + (size_t)row[u] * (size_t)D + col);
-          }
-        }
-        if (op == kOpAdagrad) Gs[u] = state[row[u]];
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < BB; ++u)
-      if (on[u]) {
-        Ops::update(op, gf[u], w[u], Gs[u], rows, state, row[u], D, q, d_pow2, inv_d, lr, eps);
-        if (clock != nullptr && q == 0) put_clock(clock, row[u]);
-      }
-  };
-  // this group's work: completed segments [e0, e1) (g over the partials row
-  // of their last item), then keys seen once [k0, k1) (g is their gradient row)
-  {
-    const uint32_t e0 = (uint32_t)((uint64_t)nd * gid / NG), e1 = (uint32_t)((uint64_t)nd * (gid + 1) / NG);
-    const uint32_t nm = e1 - e0, nw = nm + (k1 - k0);
-    for (uint32_t w0 = 0; w0 < nw; w0 += BB) {
-      uint32_t row[BB];
-      const float* src[BB];
-      bool on[BB];
-#pragma unroll
-      for (int u = 0; u < BB; ++u) {
-        const uint32_t w = w0 + u;
-        on[u] = w < nw;
-        row[u] = 0;
-        src[u] = grads;
-        if (w < nm) {
-          const uint2 dv = s_done[e0 + w];
-          row[u] = dv.x;
-          src[u] = reinterpret_cast<const float*>(partials + (size_t)dv.y * (size_t)D);
-        } else if (w < nw) {
-          const uint64_t x = s_sgl[k0 + (w - nm) - K0];
-          row[u] = item_tag(x);
-          src[u] = grads + (size_t)item_pos(x) * (size_t)D;
-        }
-      }
-      update_batch(row, src, on);
-    }
-  }
+  group_by_key<NT>(s_it, mp, s_srt, s_seg, s_sid, s_hidx, s_hcnt, s_inv, s_slot, s_ord, s_lid, s_mask, s_w64, s_info);
+  const uint32_t S = s_info[0], SA = s_info[1], MA = s_info[2];
+  if (s_info[3] != 0u)
+    resolve_new_rows<NT>(s_srt, s_seg, S, c, newlist, tile_cnt, ntiles, s_pref, s_w, s_w64, s_chunk);
+  if (op == kOpAssign) assign_segments<M, NT>(s_srt, s_seg, S, c);
+  else sum_and_update<M, NT>(s_srt, s_seg, s_sid, S, SA, MA, c, s_piece, s_slo);
 }
 
 // ===========================================================================
@@ -2475,14 +2370,29 @@ static hipError_t launch_get_t(const GetArgs& a, hipStream_t st, const LaunchHoo
   return hipGetLastError();
 }
 
+// Whether the put_reduce instance of row map M may use its dynamic LDS on
+// each device (set once per device).
+template <class M>
+static hipError_t reduce_lds_attr() {
+  constexpr int kMaxDev = 64;
+  static bool done[kMaxDev] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < kMaxDev && done[dev]) return hipSuccess;
+  constexpr int NT = ReduceCfg<M>::NT;
+  e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_put_reduce<M, NT>),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)ReduceLds<NT>::total);
+  if (e == hipSuccess && dev >= 0 && dev < kMaxDev) done[dev] = true;
+  return e;
+}
+
 template <class M>
 static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHook& hook) {
-  constexpr int NT = RedCfg<M>::NT;
-  constexpr int NG = RedCfg<M>::NG;
-  using L = RedLds<NT>;
-  static_assert((size_t)NG * RedCfg<M>::DMAX * sizeof(double) <= L::reuse,
-                "cut-segment pieces must fit the reused LDS region");
-  constexpr int NTA = ApplyCfg<M>::NT;
+  constexpr int NT = ReduceCfg<M>::NT;
+  using L = ReduceLds<NT>;
+  static_assert((size_t)ReduceCfg<M>::NG * ReduceCfg<M>::DMAX * sizeof(double) <= L::reuse,
+                "pieces of cut segments must fit the reused LDS region");
   static_assert((size_t)(kChunk + NT) * sizeof(uint64_t) + (size_t)(NT + 1) * sizeof(uint32_t) <= L::reuse,
                 "new-key chunk, sorted new keys and their counts must fit the reused LDS region");
   static_assert(L::total <= 160 * 1024, "LDS budget of a gfx950 workgroup");
@@ -2495,32 +2405,12 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   hook(K_PUT_PROBE, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  constexpr size_t apply_lds_max = ApplyLds<M, NTA>::bytes(kMaxParts);
-  static_assert(apply_lds_max <= 160 * 1024, "LDS budget of a gfx950 workgroup");
-  static bool attr_set = false;
-  if (!attr_set) {
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_put_group<M, NT>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)L::total);
-    if (e == hipSuccess)
-      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_put_apply<M, NTA>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)apply_lds_max);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  hook(K_PUT_GROUP, 0, st);
-  hipLaunchKernelGGL((k_put_group<M, NT>), dim3((unsigned)np), dim3(NT), L::total, st, a.idx, a.items,
-                     a.meta, (int)ntiles, a.newlist, a.tile_cnt, a.grads, a.partials, a.rows, a.state,
-                     a.D, a.seed, a.lr, a.eps, a.capacity, a.ctrl, a.epoch, a.spill, a.spill_words, a.gitems,
-                     a.gdesc, a.pmeta, a.op, a.clock);
-  hook(K_PUT_GROUP, 1, st);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  const int apply_blocks = (int)std::max<int64_t>((int64_t)a.flat_blocks * ApplyCfg<M>::kPerCU,
-                                                  (a.n + ApplyCfg<M>::kItems - 1) / ApplyCfg<M>::kItems);
-  const size_t apply_lds = ApplyLds<M, NTA>::bytes(np);
-  hook(K_PUT_APPLY, 0, st);
-  hipLaunchKernelGGL((k_put_apply<M, NTA>), dim3((unsigned)apply_blocks), dim3(NTA), apply_lds, st, a.gitems, a.gdesc, a.pmeta, np, a.grads, a.partials,
-                     a.rows, a.state, a.D, a.op, a.lr, a.eps, a.ctrl, a.clock);
-  hook(K_PUT_APPLY, 1, st);
+  if ((e = reduce_lds_attr<M>()) != hipSuccess) return e;
+  hook(K_PUT_REDUCE, 0, st);
+  hipLaunchKernelGGL((k_put_reduce<M, NT>), dim3((unsigned)np), dim3(NT), L::total, st, a.idx, a.items, a.meta,
+                     (int)ntiles, a.newlist, a.tile_cnt, a.grads, a.partials, a.rows, a.state, a.D, a.seed,
+                     a.lr, a.eps, a.capacity, a.ctrl, a.epoch, a.spill, a.spill_words, a.op, a.clock);
+  hook(K_PUT_REDUCE, 1, st);
   return hipGetLastError();
 }
 

@@ -18,7 +18,7 @@ MLKV_OK, MLKV_EINVAL, MLKV_EFULL, MLKV_ENOMEM, MLKV_EDEVICE = 0, -1, -2, -3, -4
 MLKV_DEFAULT_SEED = 0x4D4C4B56
 MLKV_RESERVED_KEY = 0xFFFFFFFFFFFFFFFF
 
-MLKV_NUM_KERNELS = 5
+MLKV_NUM_KERNELS = 4
 MLKV_NOALLOC_MAX_KEYS = 65536
 
 _lib = None
