@@ -172,12 +172,12 @@ int ensure_workspace(mlkv_table* t, int64_t n, hipStream_t st) {
     t->retired.push_back(old);
     clear_workspace_ptrs(t);
   }
-  const int64_t get_tiles = std::max<int64_t>((want + kGetTile - 1) / kGetTile, t->cus + 1);
+  const int64_t get_tiles = (want + kGetTileMin - 1) / kGetTileMin + t->cus + 1;
   // put tiles are kPutTile keys, or fewer so that every CU gets one
   const int64_t put_tiles = std::max<int64_t>(want / kPutTile, t->cus + 1);
   const int64_t slots = std::max<int64_t>(want, put_tiles * kPutTile);
   const uint64_t spill_words = 4ull * (uint64_t)want + 4096;
-  if ((e = dev_alloc(&t->newlist, sizeof(NewKey) * (size_t)slots)) != hipSuccess ||
+  if ((e = dev_alloc(&t->newlist, sizeof(NewKey) * ((size_t)slots + kGetTile))) != hipSuccess ||
       (e = dev_alloc(&t->tile_cnt, sizeof(uint32_t) * (size_t)get_tiles)) != hipSuccess ||
       (e = dev_alloc(&t->items, sizeof(uint64_t) * (size_t)slots)) != hipSuccess ||
       (e = dev_alloc(&t->meta, sizeof(uint32_t) * (size_t)kMaxParts * (size_t)put_tiles)) != hipSuccess ||
@@ -406,6 +406,7 @@ int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uin
   a.blocked = d_blocked;
   a.pc_key = fixed ? nullptr : t->pc_key;
   a.pc_row = fixed ? nullptr : t->pc_row;
+  a.cus = t->cus;
   const bool vec4 = (t->dim % 4 == 0) && (d_out == nullptr || aligned16(d_out));
   hipError_t e = launch_get(a, vec4, static_cast<hipStream_t>(hip_stream), fixed ? LaunchHook{} : hook_of(t));
   if (e != hipSuccess) return hip_fail(e, "mlkv_get launch");
@@ -419,11 +420,12 @@ int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uin
 // new-key lists (16 B per key), per-tile counts, key-range lists (12 B per key).
 constexpr int64_t kNoAllocMaxKeys = MLKV_NOALLOC_MAX_KEYS;
 constexpr size_t kNaNewlist = 0;
-constexpr size_t kNaTileCnt = kNaNewlist + sizeof(NewKey) * (size_t)kNoAllocMaxKeys;
+// a tile's list starts at its first position; the last tile may reach past n
+constexpr size_t kNaTileCnt = kNaNewlist + sizeof(NewKey) * ((size_t)kNoAllocMaxKeys + kGetTile);
 constexpr size_t kNaXkey = kNaTileCnt + 4096;
 constexpr size_t kNaXslot = kNaXkey + sizeof(uint64_t) * (size_t)kNoAllocMaxKeys;
 constexpr size_t kNaBytes = kNaXslot + sizeof(uint32_t) * (size_t)kNoAllocMaxKeys;
-static_assert(kNaTileCnt + sizeof(uint32_t) * ((kNoAllocMaxKeys + kGetTile - 1) / kGetTile) <= kNaXkey,
+static_assert(kNaTileCnt + sizeof(uint32_t) * ((kNoAllocMaxKeys + kGetTileMin - 1) / kGetTileMin) <= kNaXkey,
               "tile counts fit their region");
 
 __device__ __align__(256) unsigned char scratch[kNaBytes];

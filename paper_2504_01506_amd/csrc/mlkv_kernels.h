@@ -9,7 +9,20 @@
 
 namespace mlkv {
 
-constexpr int kGetTile = 256;    // keys per probe_gather block (one per lane)
+constexpr int kGetTile = 256;    // keys per probe_gather block at most (one per lane)
+constexpr int kGetTileMin = 64;  // ... and at least, unless the batch is smaller
+
+// Positions per get_probe_gather block for a batch of n keys on a device of
+// `cus` compute units: the blocks come in whole rounds of one per CU, with
+// equal tiles, so that no CU runs a block more than another.
+inline int get_tile_len(int64_t n, int cus) {
+  const int64_t per_round = (int64_t)kGetTile * cus;
+  const int64_t rounds = (n + per_round - 1) / per_round;
+  int64_t t = (n + rounds * cus - 1) / (rounds * cus);
+  if (t < kGetTileMin) t = kGetTileMin;
+  if (t > kGetTile) t = kGetTile;
+  return (int)t;
+}
 constexpr int kPutTile = 1024;   // keys per put_probe block
 constexpr int kPutThreads = 1024; // threads of a put_probe block
 constexpr int kMaxParts = 4096;  // partitions (MSD digits) per put call
@@ -73,6 +86,7 @@ struct GetArgs {
   // nullptr: not recorded
   uint64_t* pc_key;
   uint32_t* pc_row;
+  int cus;  // compute units of the device
 };
 
 struct PutArgs {

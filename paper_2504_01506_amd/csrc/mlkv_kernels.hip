@@ -114,20 +114,23 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
     float* __restrict__ out, const float* __restrict__ rows, int D, uint64_t seed,
     NewKey* __restrict__ newlist, uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch,
     unsigned long long* __restrict__ clock, uint64_t cepoch, uint32_t bound, uint8_t* __restrict__ blocked,
-    uint64_t* __restrict__ pc_key, uint32_t* __restrict__ pc_row) {
+    uint64_t* __restrict__ pc_key, uint32_t* __restrict__ pc_row, int tlen) {
   __shared__ uint32_t s_cnt;
   __shared__ uint64_t s_nkey[kGetTile];  // the tile's new keys and their slots
   __shared__ uint32_t s_nslot[kGetTile];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int64_t base = (int64_t)blockIdx.x * kGetTile;
+  // the block's tile: tlen (<= kGetTile) positions, so that every CU gets the
+  // same number of positions
+  const int64_t base = (int64_t)blockIdx.x * tlen;
+  const int64_t end = min(n, base + tlen);
   const int64_t i = base + tid;
   if (tid == 0) s_cnt = 0;
   __syncthreads();
   uint64_t key = 0;
   Probe pr = {0, kPendingRow, P_NONE};
-  if (i < n) {
+  if (i < end) {
     key = keys[i];
     if (key == kEmptyKey) {
       pr.status = P_BAD;
@@ -145,12 +148,12 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
   }
   // a key present before the call, with its row, for a put of the same
   // batch: a key's row never changes once assigned, so the pair stays valid
-  if (i < n && pc_key != nullptr) {
+  if (i < end && pc_key != nullptr) {
     pc_key[i] = pr.status == P_HIT ? key : kEmptyKey;
     pc_row[i] = pr.row;
   }
   int how = pr.status == P_HIT ? 1 : 0;
-  if (kTrack && i < n) {
+  if (kTrack && i < end) {
     // bounded staleness: a present key is served while its count before the
     // call is at most the bound. Serving it stamps the word with the call's
     // epoch and that count plus one. Nothing else writes the word during the
@@ -172,7 +175,7 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
   }
   if (out != nullptr) {
     const uint64_t s0 = splitmix_mix(key ^ seed);
-    wave_emit_rows<M, kTrack>(out, rows, D, base + wave * 64, n, how, pr.row, s0, lane);
+    wave_emit_rows<M, kTrack>(out, rows, D, base + wave * 64, end, how, pr.row, s0, lane);
   }
   __syncthreads();
   // the tile's list of new keys, in ascending key order (each at its rank)
@@ -298,8 +301,8 @@ __device__ __forceinline__ uint64_t search_tile_lists(const NewKey* __restrict__
       a[u] = 0;  // keys below lo
       b[u] = 0;  // keys below hi
     }
-    // a tile holds at most tile_size (a power of two) keys
-    for (uint32_t step = (uint32_t)tile_size; step >= 1; step >>= 1) {
+    // a tile holds at most kGetTile (a power of two) keys
+    for (uint32_t step = (uint32_t)kGetTile; step >= 1; step >>= 1) {
 #pragma unroll
       for (int u = 0; u < kSearchTiles; ++u) {
         const NewKey* l = newlist + (size_t)(t0 + u * NT) * tile_size;
@@ -1137,10 +1140,7 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
 }
 
 // ---------------------------------------------------------------------------
-// Put, second kernel: one block per partition. Gathers the partition's items,
-// groups them into segments (one per distinct key, positions ascending), sums
-// each segment's gradient rows in fp64 and applies one row-wise Adagrad step
-// to the key's row.
+// Segment sums and row updates (shared by put_reduce and its spill path)
 // ---------------------------------------------------------------------------
 
 // Sum over the LPR lanes of a lane group (LPR a power of two, groups aligned);
@@ -2352,19 +2352,20 @@ __global__ __launch_bounds__(256) void k_read_clock(const unsigned long long* __
 // ===========================================================================
 template <class M>
 static hipError_t launch_get_t(const GetArgs& a, hipStream_t st, const LaunchHook& hook) {
-  const int64_t ntiles = (a.n + kGetTile - 1) / kGetTile;
+  const int tlen = get_tile_len(a.n, a.cus);
+  const int64_t ntiles = (a.n + tlen - 1) / tlen;
   hook(K_GET_PROBE_GATHER, 0, st);
   auto kern = a.clock != nullptr ? k_get_probe_gather<M, true> : k_get_probe_gather<M, false>;
   hipLaunchKernelGGL(kern, dim3((unsigned)ntiles), dim3(kGetTile), 0, st, a.idx, a.nb_log2, a.keys, a.n,
                      a.out, a.rows, a.D, a.seed, a.newlist, a.tile_cnt, a.ctrl, a.epoch, a.clock, a.cepoch,
-                     a.bound, a.blocked, a.pc_key, a.pc_row);
+                     a.bound, a.blocked, a.pc_key, a.pc_row, tlen);
   hook(K_GET_PROBE_GATHER, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int grid = (int)std::min<int64_t>(ntiles, 256);
   hook(K_ASSIGN_NEW, 0, st);
   hipLaunchKernelGGL(k_assign_new, dim3(grid), dim3(kAssignThreads), 0, st, a.idx, a.newlist,
-                     a.tile_cnt, (int)ntiles, kGetTile, a.rows, a.state, a.D, a.seed, a.capacity,
+                     a.tile_cnt, (int)ntiles, tlen, a.rows, a.state, a.D, a.seed, a.capacity,
                      a.ctrl, a.epoch, a.xkey, a.xslot, a.clock, a.cepoch);
   hook(K_ASSIGN_NEW, 1, st);
   return hipGetLastError();
