@@ -12,11 +12,14 @@ mix: gets of half a batch of 2^20 record keys, then puts (upserts of new
 16-byte values) of the other half, over 10M prefilled records.
 
 Prints one JSON line. `value` is get+put keys per second; the line also
-carries effective HBM GB/s from algorithmic bytes, the roofline of the
-dominant kernel (per-launch durations from HIP events recorded by the
+carries the mean and median step time, get-only and put-only rates (events
+between the calls), effective HBM GB/s from algorithmic bytes, the roofline
+of the dominant kernel (per-launch durations from HIP events recorded by the
 library around every launch, beside the kernel's rocprofv3 duration from the
-committed profile when that was taken on the same kernel sources) and the
-CPU oracle timed on this host.
+committed profile when that was taken on the same kernel sources), a plain
+device copy timed as the achievable ceiling, a parity pass of the first steps
+against the CPU oracle (outside the timed region), and the oracle timed on
+this host.
 """
 from __future__ import annotations
 
@@ -95,37 +98,129 @@ def load_traffic(kernel, digest):
     return load_profile(kernel, digest, "hbm_bytes_per_launch")
 
 
-def cpu_baseline(wl, seconds, kv=False):
-    from oracle import oracle as O
+def row_scaled_err(a, b):
+    """|a - b| / max(|b|, max |b| over the row) element by element; non-finite
+    elements count 0 when both sides agree in kind (same infinity, or NaN)."""
+    a64, b64 = a.astype(np.float64), b.astype(np.float64)
+    nonfin = ~np.isfinite(a64) | ~np.isfinite(b64)
+    fb = np.where(np.isfinite(b64), np.abs(b64), 0.0)
+    scale = np.maximum(fb, fb.max(axis=-1, keepdims=True))
+    scale = np.where(scale == 0, 1.0, scale)
+    with np.errstate(invalid="ignore"):
+        err = np.where(nonfin, 0.0, np.abs(a64 - b64) / scale)
+    same = (np.isnan(a64) & np.isnan(b64)) | (a64 == b64)
+    return np.where(nonfin & ~same, np.inf, err)
 
-    t = O.OracleTable(wl.dim, wl.capacity)
+
+def max_ulp(a, b):
+    fin = np.isfinite(a) & np.isfinite(b)
+    ia = a[fin].astype(np.float32).view(np.int32).astype(np.int64)
+    ib = b[fin].astype(np.float32).view(np.int32).astype(np.int64)
+    ia = np.where(ia < 0, -(ia & 0x7FFFFFFF), ia)
+    ib = np.where(ib < 0, -(ib & 0x7FFFFFFF), ib)
+    return int(np.abs(ia - ib).max()) if ia.size else 0
+
+
+def parity_and_cpu_baseline(wl, args, kv, bounded, log):
+    """Runs the first parity_steps steps of the workload on a fresh GPU table
+    and on the CPU oracle, compares them (get outputs: bit-exact for rows no
+    put has changed, row-scaled error otherwise; then key -> row, rows and
+    accumulators of the last batch's keys), and keeps running the oracle alone
+    for about cpu_seconds of step time, which gives the CPU baseline. Returns
+    (parity record, cpu baseline record)."""
+    import torch
+    from oracle import oracle as O
+    from paper_2504_01506_amd import mlkv
+
+    D, n, h = wl.dim, wl.n, wl.n // 2
+    bound = args.staleness_bound
+    ora = O.OracleTable(D, wl.capacity, staleness_bound=bound)
     pre = wl.prefill_keys()
     if pre.size:
-        assert t.prefill_sorted(pre) == O.OK
-    steps, elapsed = 0, 0.0
-    while steps == 0 or elapsed < seconds:
+        assert ora.prefill_sorted(pre) == O.OK
+    P = 0 if args.no_parity else args.parity_steps
+    rec = None
+    if P:
+        gpu = mlkv.Table(D, wl.capacity, staleness_bound=bound)
+        gpu.reserve(n)
+        blocked = torch.empty(n, dtype=torch.uint8, device="cuda")
+        zero = torch.zeros((1 << 16, D), device="cuda") if bounded else None
+        for s0 in range(0, pre.size, 1 << 16):
+            kc = torch.from_numpy(pre[s0:s0 + (1 << 16)].view(np.int64)).cuda()
+            if bounded:
+                gpu.get_bounded(kc, None, blocked[:kc.numel()])
+                gpu.put_grad_sgd(kc, zero[:kc.numel()], 0.0)
+            else:
+                gpu.get(kc, None)
+        assert gpu.sync() == mlkv.MLKV_OK and gpu.size == ora.size
+        updated = np.zeros(wl.capacity, dtype=bool)
+        rec = {"steps": P, "max_row_scaled_err": 0.0, "max_ulp": 0, "get_rows_compared": 0,
+               "unupdated_rows_bit_exact": True}
+    cpu_s, steps = 0.0, 0
+    while steps < P or cpu_s < args.cpu_seconds:
         keys = wl.keys(steps)
-        if kv:
-            h = wl.n // 2
-            vals = wl.values(steps)
-            t0 = time.perf_counter()
-            rc, _ = t.get(keys[:h])
-            rc2 = t.put(keys[h:], vals)
+        kg = keys[:h] if kv else keys
+        kp = keys[h:] if kv else keys
+        src = wl.values(steps) if kv else wl.grads(steps)
+        t0 = time.perf_counter()
+        if bounded:
+            rc, want, _ = ora.get_bounded(kg)
         else:
-            grads = wl.grads(steps)
-            t0 = time.perf_counter()
-            rc, _ = t.get(keys)
-            rc2 = t.put_grad(keys, grads, wl.lr, wl.eps)
-        elapsed += time.perf_counter() - t0
+            rc, want = ora.get(kg)
+        rc2 = ora.put(kp, src) if kv else ora.put_grad(kp, src, wl.lr, wl.eps)
+        cpu_s += time.perf_counter() - t0
         assert rc == O.OK and rc2 == O.OK
+        if steps < P:
+            k_d = torch.from_numpy(kg.view(np.int64)).cuda()
+            out = torch.empty((kg.size, D), device="cuda")
+            if bounded:
+                gpu.get_bounded(k_d, out, blocked[:kg.size])
+            else:
+                gpu.get(k_d, out)
+            kp_d = torch.from_numpy(kp.view(np.int64)).cuda()
+            src_d = torch.from_numpy(src).cuda()
+            if kv:
+                gpu.put(kp_d, src_d)
+            else:
+                gpu.put_grad(kp_d, src_d, wl.lr, wl.eps)
+            assert gpu.sync() == mlkv.MLKV_OK
+            got = out.cpu().numpy()
+            rows_g = ora.lookup_rows(kg)
+            fresh = ~updated[rows_g]
+            if fresh.any() and not np.array_equal(got[fresh].view(np.uint32), want[fresh].view(np.uint32)):
+                rec["unupdated_rows_bit_exact"] = False
+            if (~fresh).any():
+                rec["max_row_scaled_err"] = max(rec["max_row_scaled_err"],
+                                                float(row_scaled_err(got[~fresh], want[~fresh]).max()))
+                rec["max_ulp"] = max(rec["max_ulp"], max_ulp(got[~fresh], want[~fresh]))
+            rec["get_rows_compared"] += int(kg.size)
+            rows_p = ora.lookup_rows(kp)
+            updated[rows_p] = True
+            if steps == P - 1:  # the last batch: key -> row, rows and accumulators
+                rows_d = gpu.lookup_rows(kp_d).cpu().numpy()
+                rec["key_to_row_bit_exact"] = bool(np.array_equal(rows_d, rows_p))
+                ur = np.unique(rows_p)
+                w_d, st_d = gpu.read_rows(torch.from_numpy(ur).cuda())
+                w_o, st_o = ora.read_rows(ur)
+                w_d, st_d = w_d.cpu().numpy(), st_d.cpu().numpy()
+                rec["rows_compared"] = int(ur.size)
+                rec["max_row_scaled_err"] = max(rec["max_row_scaled_err"], float(row_scaled_err(w_d, w_o).max()))
+                rec["max_ulp"] = max(rec["max_ulp"], max_ulp(w_d, w_o))
+                with np.errstate(invalid="ignore", divide="ignore"):
+                    st_err = np.where(st_d == st_o, 0.0, np.abs(st_d - st_o.astype(np.float64)) / np.abs(st_o))
+                rec["max_state_rel_err"] = float(np.nanmax(st_err)) if st_err.size else 0.0
+                rec["within_1e-5"] = bool(rec["max_row_scaled_err"] <= 1e-5 and rec["max_state_rel_err"] <= 1e-5)
+                gpu.close()
+                log(f"parity over {P} steps: {rec}")
         steps += 1
-    t.close()
+    ora.close()
     unit = "ops/s" if kv else "keys/s"
-    return {"value": wl.n * steps / elapsed, "unit": unit, "cores": 1, "kind": "oracle",
-            "sample": f"first {steps} steps of the same workload ({wl.n} keys each) after the "
-                      f"same prefill, single-threaded C++ oracle, {elapsed:.1f} s",
-            "host_cpus": os.cpu_count(), "host_affinity": len(os.sched_getaffinity(0)),
-            "cpu_model": host_cpu_model()}
+    cpu = {"value": wl.n * steps / cpu_s, "unit": unit, "cores": 1, "kind": "oracle",
+           "sample": f"the first {steps} steps of the same workload ({wl.n} keys each) after the "
+                     f"same prefill, single-threaded C++ oracle, {cpu_s:.1f} s of step time",
+           "host_cpus": os.cpu_count(), "host_affinity": len(os.sched_getaffinity(0)),
+           "cpu_model": host_cpu_model()}
+    return rec, cpu
 
 
 def host_cpu_model():
@@ -149,11 +244,15 @@ def main():
                     choices=["tiny", "dlrm", "kg", "gnn", "large", "kv-uniform", "kv-zipf"])
     ap.add_argument("--scale", type=float, default=1.0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the oracle leg (CPU baseline and parity pass)")
+    ap.add_argument("--no-parity", action="store_true", help="skip the parity pass against the oracle")
+    ap.add_argument("--parity-steps", type=int, default=3)
     ap.add_argument("--staleness-bound", type=int, default=None,
                     help="open the table with this staleness bound (gets then report blocked keys)")
-    ap.add_argument("--copy-mib", type=int, default=0,
-                    help="also run a plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--copy-mib", type=int, default=1024,
+                    help="size of the plain device copy timed as the achievable ceiling (and used to "
+                         "calibrate rocprofv3 counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -177,7 +276,7 @@ def main():
     D, n = wl.dim, wl.n
     kv = args.config.startswith("kv-")  # half gets, half puts of values
     h = n // 2
-    total_steps = args.warmup + 2 * args.steps
+    total_steps = args.warmup + args.steps  # the later passes reuse the timed batches
 
     # ---- inputs (host, seeded) -> HBM ------------------------------------
     t0 = time.perf_counter()
@@ -208,6 +307,7 @@ def main():
 
     bounded = args.staleness_bound is not None
     t = mlkv.Table(D, wl.capacity, staleness_bound=args.staleness_bound)
+    t.reserve(n)  # scratch for the batch: no allocation inside the steps
     blocked = torch.empty(n, dtype=torch.uint8, device="cuda")
     t0 = time.perf_counter()
     chunk = 1 << 16
@@ -223,27 +323,30 @@ def main():
     assert t.sync() == mlkv.MLKV_OK
     log(f"prefill {pre.size} keys in {time.perf_counter() - t0:.2f}s, size={t.size}")
 
-    def get(k, o):
+    def get(s):
+        k, o = (keys_d[s][:h], out[:h]) if kv else (keys_d[s], out)
         if bounded:
             t.get_bounded(k, o, blocked[:k.numel()])
         else:
             t.get(k, o)
 
-    def step(s):
+    def put(s):
         if kv:
-            get(keys_d[s][:h], out[:h])
             t.put(keys_d[s][h:], grads_d[s])
         else:
-            get(keys_d[s], out)
             t.put_grad(keys_d[s], grads_d[s], wl.lr, wl.eps)
 
+    def step(s):
+        get(s)
+        put(s)
+
+    Ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     # warm-up; the first step after the prefill is timed on its own (the cold
-    # step: first touch of the scratch, and the most inserts on a table that
-    # starts empty)
+    # step: the most inserts on a table that starts empty)
     first_ms = None
     for s in range(args.warmup):
         if s == 0:
-            e_a, e_b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e_a, e_b = Ev(), Ev()
             torch.cuda.synchronize()
             e_a.record()
             step(s)
@@ -255,18 +358,20 @@ def main():
     torch.cuda.synchronize()
     assert t.sync() == mlkv.MLKV_OK
 
-    # ---- timed region: K steps, nothing else on the stream ---------------
+    # ---- timed region: K steps, an event after each, nothing else on the stream
     first = args.warmup
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    timed = range(first, first + args.steps)
+    evs = [Ev() for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     w0 = time.perf_counter()
-    ev0.record()
-    for s in range(first, first + args.steps):
+    evs[0].record()
+    for i, s in enumerate(timed):
         step(s)
-    ev1.record()
+        evs[i + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
-    ms = ev0.elapsed_time(ev1)
+    ms = evs[0].elapsed_time(evs[-1])
+    per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
     assert t.sync() == mlkv.MLKV_OK
     if bounded:  # each step's put completes its get, so no get is ever blocked
         assert int(blocked.sum()) == 0, "a get was blocked"
@@ -277,17 +382,31 @@ def main():
         bytes_steps = [kernel_bytes_kv(h, Ur, n - h, Uw, D) for (Ur, Uw) in UM]
     else:
         bytes_steps = [kernel_bytes(n, U, M, D) for (U, M) in UM]
-    alg_bytes = sum(sum(b.values()) for b in bytes_steps[first:first + args.steps])
+    alg_bytes = sum(sum(bytes_steps[s].values()) for s in timed)
     gbps = alg_bytes / (ms * 1e-3) / 1e9
-    log(f"timed {args.steps} steps: {ms_step * 1e3:.2f} us/step (wall {wall * 1e3 / args.steps:.2f}), "
-        f"{keys_per_s / 1e9:.3f} G keys/s, {gbps:.0f} GB/s effective")
+    log(f"timed {args.steps} steps: {ms_step * 1e3:.2f} us/step (median {np.median(per_step) * 1e3:.2f}, "
+        f"wall {wall * 1e3 / args.steps:.2f}), {keys_per_s / 1e9:.3f} G keys/s, {gbps:.0f} GB/s effective")
 
-    # ---- per-kernel durations: the next K steps with events around every launch
-    second = first + args.steps
+    # ---- the same batches again, events between the get and the put calls
+    ev_g = [(Ev(), Ev(), Ev()) for _ in timed]
+    for (ea, eb, ec), s in zip(ev_g, timed):
+        ea.record()
+        get(s)
+        eb.record()
+        put(s)
+        ec.record()
+    torch.cuda.synchronize()
+    assert t.sync() == mlkv.MLKV_OK
+    t_get = float(np.median([ea.elapsed_time(eb) for ea, eb, _ in ev_g]))
+    t_put = float(np.median([eb.elapsed_time(ec) for _, eb, ec in ev_g]))
+    n_get, n_put = (h, n - h) if kv else (n, n)
+    log(f"get {t_get * 1e3:.2f} us, put {t_put * 1e3:.2f} us (medians)")
+
+    # ---- once more with events around every launch: per-kernel durations
     mlkv.mlkv_profile_enable(t.h, True)
-    ev2, ev3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev2, ev3 = Ev(), Ev()
     ev2.record()
-    for s in range(second, second + args.steps):
+    for s in timed:
         step(s)
     ev3.record()
     torch.cuda.synchronize()
@@ -298,7 +417,7 @@ def main():
     kinfo = {}
     for kname in KERNELS:
         tot_ms, cnt = prof[kname]
-        b = sum(bs[kname] for bs in bytes_steps[second:second + args.steps])
+        b = sum(bytes_steps[s][kname] for s in timed)
         if cnt == 0:
             continue
         avg_us = tot_ms * 1e3 / cnt
@@ -319,25 +438,35 @@ def main():
             "avg_launch_us": kinfo[dom]["avg_us"], "rocprofv3_avg_us": traced_us}
     log(f"kernels (events around every launch, {ms_prof * 1e3:.2f} us/step): {kinfo}")
 
-    if args.copy_mib:
-        a = torch.empty(args.copy_mib << 18, dtype=torch.float32, device="cuda").fill_(1.0)
-        b = torch.empty_like(a)
-        torch.cuda.synchronize()
-        b.copy_(a)
-        torch.cuda.synchronize()
-        log(f"copy of {args.copy_mib} MiB done")
-
     t.close()
     del keys_d, grads_d, out
     torch.cuda.empty_cache()
 
-    cpu = None
+    # ---- the achievable ceiling on this device: a plain 1 GiB device copy
+    copy_bytes = max(1, args.copy_mib) << 20
+    ca = torch.empty(copy_bytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    cb = torch.empty_like(ca)
+    best = None
+    for _ in range(3):
+        e_a, e_b = Ev(), Ev()
+        e_a.record()
+        cb.copy_(ca)
+        e_b.record()
+        torch.cuda.synchronize()
+        ms_c = e_a.elapsed_time(e_b)
+        best = ms_c if best is None else min(best, ms_c)
+    copy_gbps = 2 * copy_bytes / (best * 1e-3) / 1e9  # bytes read + written
+    del ca, cb
+    torch.cuda.empty_cache()
+    log(f"device copy of {copy_bytes >> 20} MiB: {copy_gbps:.0f} GB/s read+write")
+
+    parity, cpu = None, None
     if not args.no_cpu_baseline:
-        log("cpu baseline: oracle on the host")
-        cpu = cpu_baseline(wl, args.cpu_seconds, kv)
+        log("parity pass and cpu baseline: the oracle on the host")
+        parity, cpu = parity_and_cpu_baseline(wl, args, kv, bounded, log)
         log(f"cpu baseline: {cpu['value'] / 1e6:.3f} M {cpu['unit']}")
 
-    U_avg = float(np.mean([a + b if kv else a for a, b in UM[first:first + args.steps]]))
+    U_avg = float(np.mean([UM[s][0] + UM[s][1] if kv else UM[s][0] for s in timed]))
     if kv:
         workload = (f"{wl.name} key-value mix: {wl.capacity} records of dim {D} fp32 (16-byte values), "
                     f"{h} gets then {n - h} puts per step")
@@ -352,6 +481,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_step,
+        "ms_per_step_median": float(np.median(per_step)),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -366,10 +496,17 @@ def main():
         "gbps_effective": round(gbps, 1),
         "pct_of_peak_hbm": round(100.0 * gbps / PEAK_HBM_GBPS, 2),
         "alg_bytes_per_step": int(alg_bytes / args.steps),
+        "get_keys_per_s": n_get / (t_get * 1e-3),
+        "put_keys_per_s": n_put / (t_put * 1e-3),
+        "ms_get_median": t_get,
+        "ms_put_median": t_put,
         "ms_per_step_with_kernel_events": ms_prof,
         "ms_first_step": first_ms,
+        "copy_ceiling": {"gbps": round(copy_gbps, 1), "frac_of_peak": round(copy_gbps / PEAK_HBM_GBPS, 4),
+                         "what": f"device-to-device copy of {copy_bytes >> 20} MiB, read + write bytes, best of 3"},
         "roofline": roof,
         "kernels": kinfo,
+        "parity": parity,
         "cpu_baseline": cpu,
         "kernel_source_digest": digest,
     }
