@@ -358,20 +358,19 @@ def main():
     torch.cuda.synchronize()
     assert t.sync() == mlkv.MLKV_OK
 
-    # ---- timed region: K steps, an event after each, nothing else on the stream
+    # ---- timed region: K steps, nothing else on the stream
     first = args.warmup
     timed = range(first, first + args.steps)
-    evs = [Ev() for _ in range(args.steps + 1)]
+    ev0, ev1 = Ev(), Ev()
     torch.cuda.synchronize()
     w0 = time.perf_counter()
-    evs[0].record()
-    for i, s in enumerate(timed):
+    ev0.record()
+    for s in timed:
         step(s)
-        evs[i + 1].record()
+    ev1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
-    ms = evs[0].elapsed_time(evs[-1])
-    per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
+    ms = ev0.elapsed_time(ev1)
     assert t.sync() == mlkv.MLKV_OK
     if bounded:  # each step's put completes its get, so no get is ever blocked
         assert int(blocked.sum()) == 0, "a get was blocked"
@@ -384,10 +383,11 @@ def main():
         bytes_steps = [kernel_bytes(n, U, M, D) for (U, M) in UM]
     alg_bytes = sum(sum(bytes_steps[s].values()) for s in timed)
     gbps = alg_bytes / (ms * 1e-3) / 1e9
-    log(f"timed {args.steps} steps: {ms_step * 1e3:.2f} us/step (median {np.median(per_step) * 1e3:.2f}, "
-        f"wall {wall * 1e3 / args.steps:.2f}), {keys_per_s / 1e9:.3f} G keys/s, {gbps:.0f} GB/s effective")
+    log(f"timed {args.steps} steps: {ms_step * 1e3:.2f} us/step (wall {wall * 1e3 / args.steps:.2f}), "
+        f"{keys_per_s / 1e9:.3f} G keys/s, {gbps:.0f} GB/s effective")
 
     # ---- the same batches again, events between the get and the put calls
+    # (per-step times for the median, and the get and the put apart)
     ev_g = [(Ev(), Ev(), Ev()) for _ in timed]
     for (ea, eb, ec), s in zip(ev_g, timed):
         ea.record()
@@ -399,6 +399,7 @@ def main():
     assert t.sync() == mlkv.MLKV_OK
     t_get = float(np.median([ea.elapsed_time(eb) for ea, eb, _ in ev_g]))
     t_put = float(np.median([eb.elapsed_time(ec) for _, eb, ec in ev_g]))
+    per_step = [ea.elapsed_time(ec) for ea, _, ec in ev_g]
     n_get, n_put = (h, n - h) if kv else (n, n)
     log(f"get {t_get * 1e3:.2f} us, put {t_put * 1e3:.2f} us (medians)")
 

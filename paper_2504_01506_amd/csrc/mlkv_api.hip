@@ -29,8 +29,15 @@ struct mlkv_table {
   uint32_t nb_log2 = 0;
   uint64_t nb = 0;
   Bucket* idx = nullptr;
-  float* rows = nullptr;
+  float* rows = nullptr;   // all rows in HBM; for a tiered table the HBM row cache
   float* state = nullptr;
+  // tiered table: rows at home in pinned host memory, cache_rows of them in HBM
+  float* host_rows = nullptr;
+  uint32_t* slot_of_row = nullptr;  // [capacity] cache slot or kNoSlot
+  uint32_t* row_of_slot = nullptr;  // [cache_rows] row held or kNoSlot
+  uint8_t* dirty = nullptr;         // [cache_rows]
+  uint32_t* keep = nullptr;         // [cache_rows] lookahead call that asked for the slot's row
+  int64_t cache_rows = 0;
   Ctrl* ctrl = nullptr;
   // sequence number of calls that may change the table; starts at 1 because
   // the control block's epoch markers start at 0 ("no call")
@@ -202,6 +209,16 @@ int check_table(mlkv_table* t) {
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+RowStore store_of(const mlkv_table* t) {
+  RowStore s;
+  s.rows = t->rows;
+  s.host = t->host_rows;
+  s.slot = t->slot_of_row;
+  s.dirty = t->dirty;
+  s.D = t->dim;
+  return s;
+}
 
 hipEvent_t prof_event(mlkv_table* t) {
   if (!t->prof_pool.empty()) {
@@ -387,7 +404,7 @@ int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uin
   a.keys = d_keys;
   a.n = n;
   a.out = d_out;
-  a.rows = t->rows;
+  a.store = store_of(t);
   a.state = t->state;
   a.D = t->dim;
   a.seed = t->seed;
@@ -527,7 +544,7 @@ int put_call(mlkv_table* t, const uint64_t* d_keys, const float* src, int64_t n,
   a.keys = d_keys;
   a.grads = src;
   a.n = n;
-  a.rows = t->rows;
+  a.store = store_of(t);
   a.state = t->state;
   a.D = t->dim;
   a.seed = t->seed;
@@ -646,9 +663,7 @@ int mlkv_export(mlkv_table* t, int64_t nrows, float* d_rows_out, float* d_state_
   if (nrows < 0 || nrows > size) return fail(MLKV_EINVAL, "nrows must be in [0, size]");
   hipStream_t st = static_cast<hipStream_t>(hip_stream);
   hipError_t e = hipSuccess;
-  if (d_rows_out && nrows > 0)
-    e = hipMemcpyAsync(d_rows_out, t->rows, sizeof(float) * (size_t)nrows * (size_t)t->dim,
-                       hipMemcpyDeviceToDevice, st);
+  if (d_rows_out && nrows > 0) e = launch_export_rows(store_of(t), nrows, t->dim, d_rows_out, st);
   if (e == hipSuccess && d_state_out && nrows > 0)
     e = hipMemcpyAsync(d_state_out, t->state, sizeof(float) * (size_t)nrows, hipMemcpyDeviceToDevice, st);
   if (e == hipSuccess && (d_slot_keys_out || d_slot_rows_out))
@@ -664,7 +679,7 @@ int mlkv_read_rows(mlkv_table* t, const int64_t* d_rows, int64_t n, float* d_row
   if (n < 0 || n > 0x7FFFFFFFll) return fail(MLKV_EINVAL, "n must be in [0, 2^31 - 1]");
   if (n == 0) return MLKV_OK;
   if (d_rows == nullptr) return fail(MLKV_EINVAL, "rows is NULL");
-  hipError_t e = launch_read_rows(t->rows, t->state, t->dim, &t->ctrl->size[t->epoch & 1], d_rows, n,
+  hipError_t e = launch_read_rows(store_of(t), t->state, t->dim, &t->ctrl->size[t->epoch & 1], d_rows, n,
                                   d_rows_out, d_state_out, t->ctrl, static_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return hip_fail(e, "mlkv_read_rows launch");
   return MLKV_OK;

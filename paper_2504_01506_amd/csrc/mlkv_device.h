@@ -26,6 +26,39 @@ static_assert(sizeof(Bucket) == 128, "bucket must be one 128-byte line");
 constexpr int kClockBits = 24;
 constexpr unsigned long long kClockCount = (1ull << kClockBits) - 1;
 
+// Where the values of row r live. An ordinary table keeps every row in one HBM
+// array. A tiered table keeps every row in pinned host memory (its home) and
+// a fixed number of rows in an HBM cache: slot[r] is r's cache slot, or
+// kNoSlot when r is only at home. Writing a cached row marks its slot dirty
+// (written back to the home when the slot is reused).
+constexpr uint32_t kNoSlot = 0xFFFFFFFFu;
+struct RowStore {
+  float* rows;           // HBM: all rows [capacity][D], or the cache [cache rows][D]
+  float* host;           // tiered: pinned host rows [capacity][D]; else nullptr
+  const uint32_t* slot;  // tiered: [capacity] cache slot of each row; else nullptr
+  uint8_t* dirty;        // tiered: [cache rows] slot written since it was loaded
+  int D;
+  __device__ __forceinline__ const float* ptr(uint32_t r) const { return row_read(rows, host, slot, D, r); }
+  // the row about to be written (marks a cached row's slot dirty)
+  __device__ __forceinline__ float* wptr(uint32_t r) const { return row_write(rows, host, slot, dirty, D, r); }
+
+ private:
+  static __device__ __forceinline__ const float* row_read(float* rows, float* host, const uint32_t* slot, int D,
+                                                         uint32_t r) {
+    if (slot == nullptr) return rows + (size_t)r * (size_t)D;
+    const uint32_t s = slot[r];
+    return s != kNoSlot ? rows + (size_t)s * (size_t)D : host + (size_t)r * (size_t)D;
+  }
+  static __device__ __forceinline__ float* row_write(float* rows, float* host, const uint32_t* slot, uint8_t* dirty,
+                                                     int D, uint32_t r) {
+    if (slot == nullptr) return rows + (size_t)r * (size_t)D;
+    const uint32_t s = slot[r];
+    if (s == kNoSlot) return host + (size_t)r * (size_t)D;
+    dirty[s] = 1;
+    return rows + (size_t)s * (size_t)D;
+  }
+};
+
 // A key first inserted by the current call, owned by the lane that won its slot.
 struct NewKey {
   uint64_t key;

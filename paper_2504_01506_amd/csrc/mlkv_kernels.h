@@ -63,7 +63,7 @@ struct GetArgs {
   const uint64_t* keys;
   int64_t n;
   float* out;
-  float* rows;
+  RowStore store;
   float* state;
   int D;
   uint64_t seed;
@@ -95,7 +95,7 @@ struct PutArgs {
   const uint64_t* keys;
   const float* grads;
   int64_t n;
-  float* rows;
+  RowStore store;
   float* state;
   int D;
   uint64_t seed;
@@ -127,8 +127,9 @@ hipError_t launch_export_slots(const Bucket* idx, uint64_t nslots, uint64_t* key
                                uint32_t* rows_out, hipStream_t st);
 hipError_t launch_read_clock(const unsigned long long* clock, const unsigned long long* size_now,
                              const int64_t* ids, int64_t n, uint32_t* out, Ctrl* ctrl, hipStream_t st);
-hipError_t launch_read_rows(const float* rows, const float* state, int D, const unsigned long long* size_now,
+hipError_t launch_read_rows(const RowStore& store, const float* state, int D, const unsigned long long* size_now,
                             const int64_t* ids, int64_t n, float* w_out, float* st_out, Ctrl* ctrl,
                             hipStream_t st);
+hipError_t launch_export_rows(const RowStore& store, int64_t nrows, int D, float* out, hipStream_t st);
 
 }  // namespace mlkv

@@ -64,7 +64,7 @@ __device__ __forceinline__ typename VecT<VEC>::T init_vec(uint64_t s0, int col) 
 // kTrack: skipping stores costs registers, so tables without a staleness
 // bound use a variant without it).
 template <class M, bool kTrack>
-__device__ __forceinline__ void wave_emit_rows(float* __restrict__ out, const float* __restrict__ rows,
+__device__ __forceinline__ void wave_emit_rows(float* __restrict__ out, const RowStore& store,
                                                int D, int64_t wave_base, int64_t n, int how,
                                                uint32_t row, uint64_t s0, int lane) {
   constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, RPW = M::RPW;
@@ -90,7 +90,7 @@ __device__ __forceinline__ void wave_emit_rows(float* __restrict__ out, const fl
       const int64_t p = wave_base + r;
       if constexpr (kTrack) skip |= (hh == 2 ? 1u : 0u) << u;
       if (uu < UNITS && p < n && col < D) {
-        if (hh == 1) v[u] = load_vec<VEC>(rows + (size_t)rr * (size_t)D + col);
+        if (hh == 1) v[u] = load_vec<VEC>(store.ptr(rr) + col);
         else if (hh == 0) v[u] = init_vec<VEC>(ss, col);
       }
     }
@@ -111,7 +111,7 @@ __device__ __forceinline__ void wave_emit_rows(float* __restrict__ out, const fl
 template <class M, bool kTrack>
 __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
     Bucket* __restrict__ idx, uint32_t nb_log2, const uint64_t* __restrict__ keys, int64_t n,
-    float* __restrict__ out, const float* __restrict__ rows, int D, uint64_t seed,
+    float* __restrict__ out, const RowStore store, int D, uint64_t seed,
     NewKey* __restrict__ newlist, uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch,
     unsigned long long* __restrict__ clock, uint64_t cepoch, uint32_t bound, uint8_t* __restrict__ blocked,
     uint64_t* __restrict__ pc_key, uint32_t* __restrict__ pc_row, int tlen) {
@@ -175,7 +175,7 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
   }
   if (out != nullptr) {
     const uint64_t s0 = splitmix_mix(key ^ seed);
-    wave_emit_rows<M, kTrack>(out, rows, D, base + wave * 64, end, how, pr.row, s0, lane);
+    wave_emit_rows<M, kTrack>(out, store, D, base + wave * 64, end, how, pr.row, s0, lane);
   }
   __syncthreads();
   // the tile's list of new keys, in ascending key order (each at its rank)
@@ -389,7 +389,7 @@ __device__ __forceinline__ void rollback_clocks(unsigned long long* __restrict__
 constexpr int kInitRows = 4;
 template <int NT, class KP, class RP>
 __device__ __forceinline__ void write_init_rows(const KP ks, const RP rk, uint32_t m, uint64_t base,
-                                                float* __restrict__ rows, int D, uint64_t seed) {
+                                                const RowStore& store, int D, uint64_t seed) {
   constexpr uint32_t NW = NT / 64;
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   for (uint32_t j0 = wave; j0 < m; j0 += NW * kInitRows) {
@@ -401,7 +401,7 @@ __device__ __forceinline__ void write_init_rows(const KP ks, const RP rk, uint32
       w[r] = nullptr;
       s0[r] = 0;
       if (j < m) {
-        w[r] = rows + (base + rk[j]) * (uint64_t)D;
+        w[r] = store.wptr((uint32_t)(base + rk[j]));
         s0[r] = splitmix_mix(ks[j] ^ seed);
       }
     }
@@ -418,7 +418,7 @@ __device__ __forceinline__ void write_init_rows(const KP ks, const RP rk, uint32
 // initial rows (written along rows).
 template <int NT, class KP, class SP, class RP>
 __device__ __forceinline__ void write_new_rows(const KP ks, const SP sl, const RP rk, uint32_t m, uint64_t base,
-                                               Bucket* __restrict__ idx, float* __restrict__ rows,
+                                               Bucket* __restrict__ idx, const RowStore& store,
                                                float* __restrict__ state, int D, uint64_t seed,
                                                unsigned long long* __restrict__ clock, uint64_t cepoch) {
   for (uint32_t j = threadIdx.x; j < m; j += NT) {
@@ -428,12 +428,12 @@ __device__ __forceinline__ void write_new_rows(const KP ks, const SP sl, const R
     state[row] = 0.0f;
     if (clock != nullptr) clock[row] = new_row_clock(cepoch);
   }
-  write_init_rows<NT>(ks, rk, m, base, rows, D, seed);
+  write_init_rows<NT>(ks, rk, m, base, store, D, seed);
 }
 
 __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
     Bucket* __restrict__ idx, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
-    int ntiles, int tile_size, float* __restrict__ rows, float* __restrict__ state, int D,
+    int ntiles, int tile_size, const RowStore store, float* __restrict__ state, int D,
     uint64_t seed, int64_t capacity, Ctrl* ctrl, uint64_t epoch, uint64_t* __restrict__ xkey,
     uint32_t* __restrict__ xslot, unsigned long long* __restrict__ clock, uint64_t cepoch) {
   constexpr int NT = kAssignThreads;
@@ -621,7 +621,7 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
         if (j < c) s_sr[j] = rk[u];
       }
       __syncthreads();
-      write_init_rows<NT>(s_key, s_sr, c, base, rows, D, seed);
+      write_init_rows<NT>(s_key, s_sr, c, base, store, D, seed);
     } else {
       // more keys in the range than LDS holds: gather them in global scratch
       // at [below, below + c), which no other block's range overlaps, then
@@ -676,7 +676,7 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
           }
         }
         __syncthreads();
-        write_new_rows<NT>(s_mk, s_ms, s_mr, m, base, idx, rows, state, D, seed, clock, cepoch);
+        write_new_rows<NT>(s_mk, s_ms, s_mr, m, base, idx, store, state, D, seed, clock, cepoch);
         __syncthreads();
       }
     }
@@ -736,7 +736,7 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
     for (int b = 0; b < kAssignBatch; ++b) {
       const int t = tb + b * (int)gridDim.x;
       const uint32_t c = t < ntiles ? tile_cnt[t] : 0u;
-      write_init_rows<NT>(s_key + b * NT, s_rank + b * NT, c, size0, rows, D, seed);
+      write_init_rows<NT>(s_key + b * NT, s_rank + b * NT, c, size0, store, D, seed);
     }
     __syncthreads();
   }
@@ -1175,7 +1175,7 @@ struct SegmentOps {
   // Row-wise Adagrad step of one row, given its summed gradient g (fp32):
   // m = fp32(sum g^2 / D) over the group's lanes; G' = G + m;
   // den = sqrt(G') + eps; w -= lr * (g / den); writes w and G'.
-  static __device__ __forceinline__ void adagrad(const V (&g)[K], V (&w)[K], float G, float* __restrict__ rows,
+  static __device__ __forceinline__ void adagrad(const V (&g)[K], V (&w)[K], float G, float* __restrict__ wrow,
                                                  float* __restrict__ state, uint32_t row, int D, int q,
                                                  bool d_pow2, double inv_d, float lr, float eps) {
     double sq = 0.0;
@@ -1207,15 +1207,15 @@ struct SegmentOps {
           const float p = __fmul_rn(lr, qv);
           VecT<VEC>::set(w[k], x, __fsub_rn(VecT<VEC>::get(w[k], x), p));
         }
-        store_vec<VEC>(rows + (size_t)row * (size_t)D + col, w[k]);
+        store_vec<VEC>(wrow + col, w[k]);
       }
     }
     if (q == 0) state[row] = Gn;
   }
 
   // One SGD step: w -= lr * g (separate fp32 operations).
-  static __device__ __forceinline__ void sgd(const V (&g)[K], V (&w)[K], float* __restrict__ rows, uint32_t row,
-                                             int D, int q, float lr) {
+  static __device__ __forceinline__ void sgd(const V (&g)[K], V (&w)[K], float* __restrict__ wrow, int D, int q,
+                                             float lr) {
 #pragma unroll
     for (int k = 0; k < K; ++k) {
       const int col = (k * LPR + q) * VEC;
@@ -1223,30 +1223,29 @@ struct SegmentOps {
 #pragma unroll
         for (int x = 0; x < VEC; ++x)
           VecT<VEC>::set(w[k], x, __fsub_rn(VecT<VEC>::get(w[k], x), __fmul_rn(lr, VecT<VEC>::get(g[k], x))));
-        store_vec<VEC>(rows + (size_t)row * (size_t)D + col, w[k]);
+        store_vec<VEC>(wrow + col, w[k]);
       }
     }
   }
 
   // The row becomes g.
-  static __device__ __forceinline__ void assign(const V (&g)[K], float* __restrict__ rows, uint32_t row, int D,
-                                                int q) {
+  static __device__ __forceinline__ void assign(const V (&g)[K], float* __restrict__ wrow, int D, int q) {
 #pragma unroll
     for (int k = 0; k < K; ++k) {
       const int col = (k * LPR + q) * VEC;
-      if (col < D) store_vec<VEC>(rows + (size_t)row * (size_t)D + col, g[k]);
+      if (col < D) store_vec<VEC>(wrow + col, g[k]);
     }
   }
 
   // The update of op for one row; w and G are the row's current values
   // (not read for kOpAssign, G only for kOpAdagrad).
   static __device__ __forceinline__ void update(int op, const V (&g)[K], V (&w)[K], float G,
-                                                float* __restrict__ rows, float* __restrict__ state,
+                                                float* __restrict__ wrow, float* __restrict__ state,
                                                 uint32_t row, int D, int q, bool d_pow2, double inv_d, float lr,
                                                 float eps) {
-    if (op == kOpAdagrad) adagrad(g, w, G, rows, state, row, D, q, d_pow2, inv_d, lr, eps);
-    else if (op == kOpSgd) sgd(g, w, rows, row, D, q, lr);
-    else assign(g, rows, row, D, q);
+    if (op == kOpAdagrad) adagrad(g, w, G, wrow, state, row, D, q, d_pow2, inv_d, lr, eps);
+    else if (op == kOpSgd) sgd(g, w, wrow, D, q, lr);
+    else assign(g, wrow, D, q);
   }
 
   static __device__ __forceinline__ void zero(double (&acc)[K][VEC]) {
@@ -1279,7 +1278,7 @@ struct RedCtx {
   Bucket* idx;
   const float* grads;
   const double* partials;
-  float* rows;
+  RowStore store;
   float* state;
   int D;
   uint64_t seed;
@@ -1385,7 +1384,7 @@ __device__ __forceinline__ void resolve_new_rows(IP it, SP seg, uint32_t S, cons
       c.idx[slot / kSlots].row[slot % kSlots] = row;
       it[seg[s]] = make_item(true, row, item_low31(x));
       const uint64_t s0k = splitmix_mix(key ^ c.seed);
-      float* w = c.rows + (size_t)row * (size_t)c.D;
+      float* w = c.store.wptr(row);
       for (int col = 0; col < c.D; ++col) w[col] = init_elem(s0k, col);
       c.state[row] = 0.0f;
     }
@@ -1570,7 +1569,7 @@ __device__ __forceinline__ void update_segments(IP it, SP seg, uint32_t S, const
           const int col = (k * LPR + q) * VEC;
           if (col < D) {
             gf[u][k] = load_vec<VEC>(src + col);
-            w[u][k] = load_vec<VEC>(c.rows + (size_t)row[u] * (size_t)D + col);
+            w[u][k] = load_vec<VEC>(c.store.ptr(row[u]) + col);
           }
         }
         if (c.op == kOpAdagrad) G[u] = c.state[row[u]];
@@ -1579,7 +1578,8 @@ __device__ __forceinline__ void update_segments(IP it, SP seg, uint32_t S, const
 #pragma unroll
     for (int u = 0; u < BB; ++u) {
       if (s0 + u * NG < S) {
-        Ops::update(c.op, gf[u], w[u], G[u], c.rows, c.state, row[u], D, q, d_pow2, inv_d, c.lr, c.eps);
+        Ops::update(c.op, gf[u], w[u], G[u], c.store.wptr(row[u]), c.state, row[u], D, q, d_pow2, inv_d, c.lr,
+                    c.eps);
         if (c.clock != nullptr && q == 0) put_clock(c.clock, row[u]);
       }
     }
@@ -1877,14 +1877,17 @@ __device__ __forceinline__ void update_rows(const bool (&on)[N], const uint32_t 
   const int D = c.D;
   V w[N][K];
   float G[N];
+  float* wr[N];
 #pragma unroll
   for (int u = 0; u < N; ++u) {
     G[u] = 0.0f;
+    wr[u] = nullptr;
     if (on[u]) {
+      wr[u] = c.store.wptr(rw[u]);
 #pragma unroll
       for (int k = 0; k < K; ++k) {
         const int col = (k * LPR + q) * VEC;
-        if (col < D) w[u][k] = load_vec<VEC>(c.rows + (size_t)rw[u] * (size_t)D + col);
+        if (col < D) w[u][k] = load_vec<VEC>(wr[u] + col);
       }
       if (c.op == kOpAdagrad) G[u] = c.state[rw[u]];
     }
@@ -1892,7 +1895,7 @@ __device__ __forceinline__ void update_rows(const bool (&on)[N], const uint32_t 
 #pragma unroll
   for (int u = 0; u < N; ++u)
     if (on[u]) {
-      SegmentOps<M>::update(c.op, gq[u], w[u], G[u], c.rows, c.state, rw[u], D, q, d_pow2, inv_d, c.lr, c.eps);
+      SegmentOps<M>::update(c.op, gq[u], w[u], G[u], wr[u], c.state, rw[u], D, q, d_pow2, inv_d, c.lr, c.eps);
       if (c.clock != nullptr && q == 0) put_clock(c.clock, rw[u]);
     }
 }
@@ -1952,6 +1955,7 @@ __device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32
   V wc[K];
   float Gc = 0.0f;
   uint32_t rowc = 0;
+  float* wrc = nullptr;
   bool last_ends = true, last_owned = true;
   uint32_t last_end = 0;
   for (uint32_t j0 = lo; j0 < hi; j0 += B) {
@@ -1960,6 +1964,7 @@ __device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32
     RawRow<VEC> raw[B][K];
     V wl[B][K];
     float Gl[B];
+    float* wp[B];
 #pragma unroll
     for (int u = 0; u < B; ++u) {
       const uint32_t j = j0 + u;
@@ -1967,6 +1972,7 @@ __device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32
       fst[u] = 0;
       end[u] = 0;
       Gl[u] = 0.0f;
+      wp[u] = nullptr;
       if (j < hi) {
         x[u] = srt[j];
         const uint32_t s = sid[j];
@@ -1981,10 +1987,11 @@ __device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32
         }
         if (fst[u] == j && j >= lo) {  // an owned segment starts: its row (the first item carries it)
           const uint32_t r = item_tag(x[u]);
+          wp[u] = c.store.wptr(r);
 #pragma unroll
           for (int k = 0; k < K; ++k) {
             const int col = (k * LPR + q) * VEC;
-            if (col < D) wl[u][k] = load_vec<VEC>(c.rows + (size_t)r * (size_t)D + col);
+            if (col < D) wl[u][k] = load_vec<VEC>(wp[u] + col);
           }
           if (c.op == kOpAdagrad) Gl[u] = c.state[r];
         }
@@ -1996,6 +2003,7 @@ __device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32
       if (j < hi) {
         if (fst[u] == j) {  // (j >= lo here)
           rowc = item_tag(x[u]);
+          wrc = wp[u];
 #pragma unroll
           for (int k = 0; k < K; ++k) wc[k] = wl[u][k];
           Gc = Gl[u];
@@ -2013,7 +2021,7 @@ __device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32
           if (last_owned) {
             V g[K];
             to_f32(g, acc);
-            Ops::update(c.op, g, wc, Gc, c.rows, c.state, rowc, D, q, d_pow2, inv_d, c.lr, c.eps);
+            Ops::update(c.op, g, wc, Gc, wrc, c.state, rowc, D, q, d_pow2, inv_d, c.lr, c.eps);
             if (c.clock != nullptr && q == 0) put_clock(c.clock, rowc);
           } else {
             put_piece(acc);  // the end of a segment begun in an earlier share
@@ -2073,7 +2081,7 @@ __device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32
     }
     V g[K];
     to_f32(g, acc);  // the row and accumulator were loaded with the segment's first item
-    Ops::update(c.op, g, wc, Gc, c.rows, c.state, rowc, D, q, d_pow2, inv_d, c.lr, c.eps);
+    Ops::update(c.op, g, wc, Gc, wrc, c.state, rowc, D, q, d_pow2, inv_d, c.lr, c.eps);
     if (c.clock != nullptr && q == 0) put_clock(c.clock, rowc);
   }
 }
@@ -2111,7 +2119,7 @@ __device__ __forceinline__ void assign_segments(const uint64_t* srt, const uint3
 #pragma unroll
     for (int u = 0; u < BS; ++u) {
       if (s0 + u >= k1) continue;
-      SegmentOps<M>::assign(v[u], c.rows, rw[u], D, q);
+      SegmentOps<M>::assign(v[u], c.store.wptr(rw[u]), D, q);
       if (c.clock != nullptr && q == 0) put_clock(c.clock, rw[u]);
     }
   }
@@ -2167,7 +2175,7 @@ template <class M, int NT>
 __global__ __launch_bounds__(NT) void k_put_reduce(
     Bucket* __restrict__ idx, const uint64_t* __restrict__ items, const uint32_t* __restrict__ meta,
     int ntiles, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
-    const float* __restrict__ grads, double* __restrict__ partials, float* __restrict__ rows,
+    const float* __restrict__ grads, double* __restrict__ partials, const RowStore store,
     float* __restrict__ state, int D, uint64_t seed, float lr, float eps, int64_t capacity, Ctrl* ctrl,
     uint64_t epoch, uint64_t* __restrict__ spill, uint64_t spill_words, int op,
     unsigned long long* __restrict__ clock) {
@@ -2232,7 +2240,7 @@ __global__ __launch_bounds__(NT) void k_put_reduce(
     return;
   }
 
-  const RedCtx c{op, idx, grads, partials, rows, state, D, seed, lr, eps, size0, clock};
+  const RedCtx c{op, idx, grads, partials, store, state, D, seed, lr, eps, size0, clock};
   if (mp > (uint32_t)kRedCap) {
     reduce_partition_global<M, NT>(p, mp, items, meta, ntiles, c, newlist, tile_cnt, ctrl, spill, spill_words,
                                    s_piece, s_pref, s_w, s_w64, s_base);
@@ -2314,7 +2322,7 @@ __global__ __launch_bounds__(256) void k_export_slots(const Bucket* __restrict__
 
 // Copies rows and accumulators by row id; ids outside [0, size) give NaN
 // rows and latch MLKV_EINVAL (-1).
-__global__ __launch_bounds__(256) void k_read_rows(const float* __restrict__ rows, const float* __restrict__ state,
+__global__ __launch_bounds__(256) void k_read_rows(const RowStore store, const float* __restrict__ state,
                                                    int D, const unsigned long long* size_now,
                                                    const int64_t* __restrict__ ids, int64_t n,
                                                    float* __restrict__ w_out, float* __restrict__ st_out,
@@ -2327,7 +2335,7 @@ __global__ __launch_bounds__(256) void k_read_rows(const float* __restrict__ row
     const int64_t r = ids[i];
     const bool ok = r >= 0 && (uint64_t)r < size;
     if (!ok && c == 0) atomicCAS(&ctrl->latched, 0, -1);
-    if (w_out) w_out[e] = ok ? rows[(uint64_t)r * (uint64_t)D + c] : __builtin_nanf("");
+    if (w_out) w_out[e] = ok ? store.ptr((uint32_t)r)[c] : __builtin_nanf("");
     if (st_out && c == 0) st_out[i] = ok ? state[r] : __builtin_nanf("");
   }
 }
@@ -2357,7 +2365,7 @@ static hipError_t launch_get_t(const GetArgs& a, hipStream_t st, const LaunchHoo
   hook(K_GET_PROBE_GATHER, 0, st);
   auto kern = a.clock != nullptr ? k_get_probe_gather<M, true> : k_get_probe_gather<M, false>;
   hipLaunchKernelGGL(kern, dim3((unsigned)ntiles), dim3(kGetTile), 0, st, a.idx, a.nb_log2, a.keys, a.n,
-                     a.out, a.rows, a.D, a.seed, a.newlist, a.tile_cnt, a.ctrl, a.epoch, a.clock, a.cepoch,
+                     a.out, a.store, a.D, a.seed, a.newlist, a.tile_cnt, a.ctrl, a.epoch, a.clock, a.cepoch,
                      a.bound, a.blocked, a.pc_key, a.pc_row, tlen);
   hook(K_GET_PROBE_GATHER, 1, st);
   hipError_t e = hipGetLastError();
@@ -2365,7 +2373,7 @@ static hipError_t launch_get_t(const GetArgs& a, hipStream_t st, const LaunchHoo
   const int grid = (int)std::min<int64_t>(ntiles, 256);
   hook(K_ASSIGN_NEW, 0, st);
   hipLaunchKernelGGL(k_assign_new, dim3(grid), dim3(kAssignThreads), 0, st, a.idx, a.newlist,
-                     a.tile_cnt, (int)ntiles, tlen, a.rows, a.state, a.D, a.seed, a.capacity,
+                     a.tile_cnt, (int)ntiles, tlen, a.store, a.state, a.D, a.seed, a.capacity,
                      a.ctrl, a.epoch, a.xkey, a.xslot, a.clock, a.cepoch);
   hook(K_ASSIGN_NEW, 1, st);
   return hipGetLastError();
@@ -2409,7 +2417,7 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   if ((e = reduce_lds_attr<M>()) != hipSuccess) return e;
   hook(K_PUT_REDUCE, 0, st);
   hipLaunchKernelGGL((k_put_reduce<M, NT>), dim3((unsigned)np), dim3(NT), L::total, st, a.idx, a.items, a.meta,
-                     (int)ntiles, a.newlist, a.tile_cnt, a.grads, a.partials, a.rows, a.state, a.D, a.seed,
+                     (int)ntiles, a.newlist, a.tile_cnt, a.grads, a.partials, a.store, a.state, a.D, a.seed,
                      a.lr, a.eps, a.capacity, a.ctrl, a.epoch, a.spill, a.spill_words, a.op, a.clock);
   hook(K_PUT_REDUCE, 1, st);
   return hipGetLastError();
@@ -2459,13 +2467,31 @@ hipError_t launch_export_slots(const Bucket* idx, uint64_t nslots, uint64_t* key
   return hipGetLastError();
 }
 
-hipError_t launch_read_rows(const float* rows, const float* state, int D, const unsigned long long* size_now,
+hipError_t launch_read_rows(const RowStore& store, const float* state, int D, const unsigned long long* size_now,
                             const int64_t* ids, int64_t n, float* w_out, float* st_out, Ctrl* ctrl,
                             hipStream_t st) {
   const uint64_t total = (uint64_t)n * (uint64_t)D;
   const uint64_t grid = std::min<uint64_t>((total + 255) / 256, 65536);
-  hipLaunchKernelGGL(k_read_rows, dim3((unsigned)grid), dim3(256), 0, st, rows, state, D, size_now, ids, n,
+  hipLaunchKernelGGL(k_read_rows, dim3((unsigned)grid), dim3(256), 0, st, store, state, D, size_now, ids, n,
                      w_out, st_out, ctrl);
+  return hipGetLastError();
+}
+
+// Rows 0 .. nrows-1 in order, from wherever each lives.
+__global__ __launch_bounds__(256) void k_export_rows(const RowStore store, int64_t nrows, int D,
+                                                     float* __restrict__ out) {
+  const uint64_t total = (uint64_t)nrows * (uint64_t)D;
+  for (uint64_t e = (uint64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (uint64_t)gridDim.x * 256) {
+    const uint64_t r = e / (uint64_t)D;
+    out[e] = store.ptr((uint32_t)r)[e % (uint64_t)D];
+  }
+}
+
+hipError_t launch_export_rows(const RowStore& store, int64_t nrows, int D, float* out, hipStream_t st) {
+  const uint64_t total = (uint64_t)nrows * (uint64_t)D;
+  if (total == 0) return hipSuccess;
+  const uint64_t grid = std::min<uint64_t>((total + 255) / 256, 65536);
+  hipLaunchKernelGGL(k_export_rows, dim3((unsigned)grid), dim3(256), 0, st, store, nrows, D, out);
   return hipGetLastError();
 }
 
