@@ -74,7 +74,7 @@ def kernel_bytes_kv(nr, Ur, nw, Uw, D):
 
 def source_digest():
     h = hashlib.sha256()
-    for f in ("mlkv_device.h", "mlkv_kernels.h", "mlkv_kernels.hip"):
+    for f in ("mlkv_device.h", "mlkv_kernels.h", "mlkv_kernels.hip", "mlkv_tier.hip"):
         with open(os.path.join(ROOT, "paper_2504_01506_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -141,7 +141,8 @@ def parity_and_cpu_baseline(wl, args, kv, bounded, log):
     P = 0 if args.no_parity else args.parity_steps
     rec = None
     if P:
-        gpu = mlkv.Table(D, wl.capacity, staleness_bound=bound)
+        cache = max(1, int(wl.capacity * args.cache_frac)) if args.cache_frac else None
+        gpu = mlkv.Table(D, wl.capacity, staleness_bound=bound, cache_rows=cache)
         gpu.reserve(n)
         blocked = torch.empty(n, dtype=torch.uint8, device="cuda")
         zero = torch.zeros((1 << 16, D), device="cuda") if bounded else None
@@ -172,6 +173,8 @@ def parity_and_cpu_baseline(wl, args, kv, bounded, log):
         assert rc == O.OK and rc2 == O.OK
         if steps < P:
             k_d = torch.from_numpy(kg.view(np.int64)).cuda()
+            if args.cache_frac:
+                gpu.lookahead(k_d)
             out = torch.empty((kg.size, D), device="cuda")
             if bounded:
                 gpu.get_bounded(k_d, out, blocked[:kg.size])
@@ -250,6 +253,9 @@ def main():
     ap.add_argument("--parity-steps", type=int, default=3)
     ap.add_argument("--staleness-bound", type=int, default=None,
                     help="open the table with this staleness bound (gets then report blocked keys)")
+    ap.add_argument("--cache-frac", type=float, default=None,
+                    help="tiered table: rows in pinned host memory, this fraction of them cached in HBM; "
+                         "each step is lookahead(keys), get(keys), put_grad(keys)")
     ap.add_argument("--copy-mib", type=int, default=1024,
                     help="size of the plain device copy timed as the achievable ceiling (and used to "
                          "calibrate rocprofv3 counters)")
@@ -259,6 +265,11 @@ def main():
               "(the path is single-GPU by design)", file=sys.stderr)
         sys.exit(2)
 
+    if args.cache_frac is not None and (args.config.startswith("kv-") or args.staleness_bound is not None
+                                        or not 0.0 < args.cache_frac <= 1.0):
+        print("--cache-frac (0 < f <= 1) applies to the training-step workloads without a staleness bound",
+              file=sys.stderr)
+        sys.exit(2)
     if args.staleness_bound is not None and args.config.startswith("kv-"):
         print("--staleness-bound applies to the training-step workloads (get then put_grad of the same keys)",
               file=sys.stderr)
@@ -306,7 +317,9 @@ def main():
     log(f"inputs ready in {time.perf_counter() - t0:.1f}s: {total_steps} batches of {n} keys")
 
     bounded = args.staleness_bound is not None
-    t = mlkv.Table(D, wl.capacity, staleness_bound=args.staleness_bound)
+    tiered = args.cache_frac is not None
+    cache_rows = max(1, int(wl.capacity * args.cache_frac)) if tiered else None
+    t = mlkv.Table(D, wl.capacity, staleness_bound=args.staleness_bound, cache_rows=cache_rows)
     t.reserve(n)  # scratch for the batch: no allocation inside the steps
     blocked = torch.empty(n, dtype=torch.uint8, device="cuda")
     t0 = time.perf_counter()
@@ -322,6 +335,11 @@ def main():
             t.get(kc, None)
     assert t.sync() == mlkv.MLKV_OK
     log(f"prefill {pre.size} keys in {time.perf_counter() - t0:.2f}s, size={t.size}")
+    if tiered:  # warm the cache with a slice of the table
+        warm = np.random.default_rng(5).choice(pre, size=min(cache_rows, pre.size), replace=False)
+        t.lookahead(torch.from_numpy(warm.view(np.int64)).cuda())
+        assert t.sync() == mlkv.MLKV_OK
+        log(f"cache of {cache_rows} rows warmed: {t.cache_stats()}")
 
     def get(s):
         k, o = (keys_d[s][:h], out[:h]) if kv else (keys_d[s], out)
@@ -337,6 +355,8 @@ def main():
             t.put_grad(keys_d[s], grads_d[s], wl.lr, wl.eps)
 
     def step(s):
+        if tiered:
+            t.lookahead(keys_d[s])
         get(s)
         put(s)
 
@@ -404,6 +424,7 @@ def main():
     log(f"get {t_get * 1e3:.2f} us, put {t_put * 1e3:.2f} us (medians)")
 
     # ---- once more with events around every launch: per-kernel durations
+    tier0 = t.cache_stats() if tiered else None
     mlkv.mlkv_profile_enable(t.h, True)
     ev2, ev3 = Ev(), Ev()
     ev2.record()
@@ -416,6 +437,7 @@ def main():
     ms_prof = ev2.elapsed_time(ev3) / args.steps
     assert t.sync() == mlkv.MLKV_OK
     kinfo = {}
+    host_link = None
     for kname in KERNELS:
         tot_ms, cnt = prof[kname]
         b = sum(bytes_steps[s][kname] for s in timed)
@@ -425,7 +447,36 @@ def main():
         kinfo[kname] = {"avg_us": round(avg_us, 3), "launches": cnt,
                         "alg_bytes_per_launch": int(b / cnt),
                         "gbps": round(b / cnt / (avg_us * 1e-6) / 1e9, 1)}
-    dom = max(kinfo, key=lambda k: kinfo[k]["avg_us"] * kinfo[k]["launches"])
+    if tiered and prof["tier_copy"][1] > 0:
+        # the steps' lookahead copies: rows in over the host link, dirty rows back
+        tier1 = t.cache_stats()
+        for kname in ("tier_mark", "tier_plan", "tier_copy"):
+            tot_ms, cnt = prof[kname]
+            kinfo[kname] = {"avg_us": round(tot_ms * 1e3 / cnt, 3), "launches": cnt}
+        cnt = prof["tier_copy"][1]
+        kinfo["tier_copy"].update({"rows_in_per_launch": (tier1["loaded"] - tier0["loaded"]) / cnt,
+                                   "rows_back_per_launch": (tier1["written_back"] - tier0["written_back"]) / cnt})
+        # a bulk lookahead of rows mostly not cached: the copy is link-bound
+        bulk = np.random.default_rng(6).choice(pre, size=min(cache_rows, 1 << 20), replace=False)
+        bulk_d = torch.from_numpy(bulk.view(np.int64)).cuda()
+        torch.cuda.synchronize()
+        mlkv.mlkv_profile_enable(t.h, True)
+        t.lookahead(bulk_d)
+        torch.cuda.synchronize()
+        bprof = mlkv.mlkv_profile_read(t.h)
+        mlkv.mlkv_profile_enable(t.h, False)
+        assert t.sync() == mlkv.MLKV_OK
+        tier2 = t.cache_stats()
+        rows_in = tier2["loaded"] - tier1["loaded"]
+        rows_back = tier2["written_back"] - tier1["written_back"]
+        link_bytes = 4 * D * (rows_in + rows_back)
+        us = bprof["tier_copy"][0] * 1e3
+        host_link = {"kernel": "tier_copy", "what": f"lookahead of {bulk.size} random rows, {rows_in} of them "
+                                                    f"copied in and {rows_back} dirty ones written back",
+                     "achieved_gbps": round(link_bytes / (us * 1e-6) / 1e9, 2), "bytes": int(link_bytes),
+                     "launch_us": round(us, 2), "cache_rows": cache_rows, "counters": tier2}
+    dom = max((k for k in kinfo if "alg_bytes_per_launch" in kinfo[k]),
+              key=lambda k: kinfo[k]["avg_us"] * kinfo[k]["launches"])
     digest = source_digest()
     # the committed counters were taken on the full-size DLRM-shaped workload
     same_workload = args.config == "dlrm" and args.scale == 1.0 and not bounded
@@ -460,6 +511,27 @@ def main():
     del ca, cb
     torch.cuda.empty_cache()
     log(f"device copy of {copy_bytes >> 20} MiB: {copy_gbps:.0f} GB/s read+write")
+    if host_link is not None:
+        # the host link's ceiling: plain copies between pinned host memory and HBM
+        hb = 256 << 20
+        ph = torch.empty(hb // 4, dtype=torch.float32, pin_memory=True).fill_(1.0)
+        dd = torch.empty(hb // 4, dtype=torch.float32, device="cuda")
+        rates = {}
+        for name, (dst, src) in (("h2d", (dd, ph)), ("d2h", (ph, dd))):
+            best_l = None
+            for _ in range(3):
+                e_a, e_b = Ev(), Ev()
+                e_a.record()
+                dst.copy_(src, non_blocking=True)
+                e_b.record()
+                torch.cuda.synchronize()
+                ms_l = e_a.elapsed_time(e_b)
+                best_l = ms_l if best_l is None else min(best_l, ms_l)
+            rates[name] = round(hb / (best_l * 1e-3) / 1e9, 2)
+        del ph, dd
+        host_link["link_copy_gbps"] = rates
+        host_link["frac_of_h2d_copy"] = round(host_link["achieved_gbps"] / rates["h2d"], 4)
+        log(f"host link: lookahead copy {host_link['achieved_gbps']} GB/s, pinned copies {rates}")
 
     parity, cpu = None, None
     if not args.no_cpu_baseline:
@@ -493,6 +565,7 @@ def main():
             "rows": wl.capacity, "dim": D, "lookups_per_step": n, "prefill": int(pre.size),
             "unique_keys_per_step": round(U_avg, 1), "scale": args.scale,
             **({"staleness_bound": args.staleness_bound} if bounded else {}),
+            **({"tiered_cache_rows": cache_rows, "step": "lookahead + get + put_grad"} if tiered else {}),
         },
         "gbps_effective": round(gbps, 1),
         "pct_of_peak_hbm": round(100.0 * gbps / PEAK_HBM_GBPS, 2),
@@ -506,6 +579,7 @@ def main():
         "copy_ceiling": {"gbps": round(copy_gbps, 1), "frac_of_peak": round(copy_gbps / PEAK_HBM_GBPS, 4),
                          "what": f"device-to-device copy of {copy_bytes >> 20} MiB, read + write bytes, best of 3"},
         "roofline": roof,
+        **({"host_link": host_link} if host_link is not None else {}),
         "kernels": kinfo,
         "parity": parity,
         "cpu_baseline": cpu,

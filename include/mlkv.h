@@ -10,7 +10,8 @@
  *                                         modify function is "sum the gradients
  *                                         of duplicate keys, then one row-wise
  *                                         Adagrad step"
- * Tables live entirely in HBM. Calls on one table must be ordered on one HIP
+ * Tables live in HBM (a tiered table keeps its rows in host memory with an HBM
+ * cache, see mlkv_open_tiered). Calls on one table must be ordered on one HIP
  * stream. A table may carry a staleness bound (Sec. III-C1, see
  * mlkv_open_bounded); without one every get is served.
  *
@@ -116,14 +117,35 @@ int mlkv_get_noalloc(mlkv_table *t, const uint64_t *d_keys, int64_t n, float *d_
 int mlkv_get_bounded(mlkv_table *t, const uint64_t *d_keys, int64_t n, float *d_out, uint8_t *d_blocked,
                      void *hip_stream);
 
-/* Lookahead (Sec. III-A; look-ahead prefetching, Sec. III-C2) with the whole
- * table in HBM: makes d_keys resident ahead of the gets that will read them,
- * i.e. inserts the missing keys exactly as mlkv_get with d_out = NULL would
- * (rows in ascending key order, seeded initial rows), and returns nothing.
- * It never blocks and changes no staleness count (a new key starts at 0).
- * A table larger than HBM, which would make this a copy from host memory,
- * is not supported. 0 <= n <= 2^31 - 1; errors as for mlkv_get. */
+/* Opens a tiered table (for tables larger than HBM; the paper's buffer over a
+ * slower tier, Sec. III-C2): the rows live at home in pinned host memory
+ * (capacity * dim * 4 bytes, allocated with hipHostMalloc), cache_rows of them
+ * in an HBM cache; the index, the Adagrad accumulators and the staleness
+ * counts stay in HBM. Every call works on it as on an ordinary table with the
+ * same results: gets and puts read and write each row where it is (the cache
+ * slot, else its home over the host link; a cached row written by a put is
+ * written back when its slot is reused). mlkv_lookahead moves rows into the
+ * cache. 1 <= cache_rows <= capacity; otherwise as mlkv_open_ex. */
+mlkv_table *mlkv_open_tiered(int32_t dim, int64_t capacity, uint64_t seed, float max_load, int64_t cache_rows);
+
+/* Lookahead (Sec. III-A; look-ahead prefetching, Sec. III-C2): makes d_keys
+ * resident ahead of the gets that will read them. The missing keys are
+ * inserted exactly as mlkv_get with d_out = NULL would (rows in ascending key
+ * order, seeded initial rows); nothing is returned. On a tiered table the
+ * keys' rows are then brought into the HBM cache: rows already cached stay;
+ * each missing row takes the next cache slot, in FIFO order from a cursor,
+ * whose row this call does not ask for (that row is evicted, and written back
+ * home first if a put changed it); when the call asks for more rows than the
+ * cache can give it, the rest stay at home. It never blocks and changes no
+ * staleness count (a new key starts at 0). 0 <= n <= 2^31 - 1; errors as for
+ * mlkv_get. */
 int mlkv_lookahead(mlkv_table *t, const uint64_t *d_keys, int64_t n, void *hip_stream);
+
+/* Counters of a tiered table since it was opened (synchronizes the device):
+ * out[0] rows copied into the cache, out[1] rows evicted from it, out[2]
+ * evicted rows written back home, out[3] cache slots holding a row, out[4]
+ * cache slots. out: 5 int64 (host). MLKV_EINVAL on a table that is not tiered. */
+int mlkv_cache_stats(mlkv_table *t, int64_t *out);
 
 /* Rmw (Sec. III-B, step 8) with row-wise Adagrad as the modify function:
  * missing keys are inserted as in mlkv_get; then for every distinct key k of
@@ -212,12 +234,13 @@ int mlkv_read_staleness(mlkv_table *t, const int64_t *d_rows, int64_t n, uint32_
  * The library runs MLKV_NUM_KERNELS kernels: 0 get_probe_gather and
  * 1 assign_new for mlkv_get, mlkv_get_bounded and mlkv_lookahead;
  * 2 put_probe and 3 put_reduce for mlkv_put_grad, mlkv_put_grad_sgd and
- * mlkv_put. While enabled, HIP events are recorded on
+ * mlkv_put; 4 tier_mark, 5 tier_plan and 6 tier_copy for mlkv_lookahead on a
+ * tiered table. While enabled, HIP events are recorded on
  * the call's stream before and after every launch. mlkv_profile_read waits
  * for the recorded launches, writes per-kernel sums of their durations (ms)
  * and launch counts into the host arrays total_ms[MLKV_NUM_KERNELS] and
  * launches[MLKV_NUM_KERNELS], and forgets them. */
-#define MLKV_NUM_KERNELS 4
+#define MLKV_NUM_KERNELS 7
 int mlkv_profile_enable(mlkv_table *t, int enable);
 int mlkv_profile_read(mlkv_table *t, double *total_ms, int64_t *launches);
 /* Name of kernel `kernel` (0 <= kernel < MLKV_NUM_KERNELS), else NULL. */

@@ -8,7 +8,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = [os.path.join(CSRC, f) for f in ("mlkv_api.hip", "mlkv_kernels.hip")]
+SOURCES = [os.path.join(CSRC, f) for f in ("mlkv_api.hip", "mlkv_kernels.hip", "mlkv_tier.hip")]
 LIB = os.path.join(HERE, "libmlkv.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -38,6 +38,13 @@ struct mlkv_table {
   uint8_t* dirty = nullptr;         // [cache_rows]
   uint32_t* keep = nullptr;         // [cache_rows] lookahead call that asked for the slot's row
   int64_t cache_rows = 0;
+  void* host_alloc = nullptr;       // the pinned allocation behind host_rows
+  uint32_t tier_tag = 0;            // lookahead calls made (tags the rows each one keeps)
+  // lookahead scratch (tiered tables): misses and the copy plan, n entries each
+  uint32_t* miss = nullptr;
+  uint32_t* plan_slot = nullptr;
+  uint32_t* plan_old = nullptr;
+  uint32_t* plan_new = nullptr;
   Ctrl* ctrl = nullptr;
   // sequence number of calls that may change the table; starts at 1 because
   // the control block's epoch markers start at 0 ("no call")
@@ -102,11 +109,16 @@ void free_scratch_set(const ScratchSet& s) {
 
 ScratchSet current_set(mlkv_table* t) {
   ScratchSet s;
-  s.ptrs = {t->newlist, t->tile_cnt, t->items, t->meta, t->spill, t->partials, t->pc_key, t->pc_row};
+  s.ptrs = {t->newlist, t->tile_cnt, t->items, t->meta, t->spill, t->partials, t->pc_key, t->pc_row,
+            t->miss, t->plan_slot, t->plan_old, t->plan_new};
   return s;
 }
 
 void clear_workspace_ptrs(mlkv_table* t) {
+  t->miss = nullptr;
+  t->plan_slot = nullptr;
+  t->plan_old = nullptr;
+  t->plan_new = nullptr;
   t->pc_key = nullptr;
   t->pc_row = nullptr;
   t->partials = nullptr;
@@ -196,6 +208,14 @@ int ensure_workspace(mlkv_table* t, int64_t n, hipStream_t st) {
     free_workspace(t);
     return hip_fail(e, "scratch allocation");
   }
+  if (t->cache_rows > 0 &&
+      ((e = dev_alloc(&t->miss, sizeof(uint32_t) * (size_t)want)) != hipSuccess ||
+       (e = dev_alloc(&t->plan_slot, sizeof(uint32_t) * (size_t)want)) != hipSuccess ||
+       (e = dev_alloc(&t->plan_old, sizeof(uint32_t) * (size_t)want)) != hipSuccess ||
+       (e = dev_alloc(&t->plan_new, sizeof(uint32_t) * (size_t)want)) != hipSuccess)) {
+    free_workspace(t);
+    return hip_fail(e, "lookahead scratch allocation");
+  }
   t->ws_n = want;
   t->spill_words = spill_words;
   return MLKV_OK;
@@ -271,7 +291,13 @@ extern "C" {
 
 const char* mlkv_last_error(void) { return g_err.c_str(); }
 
-mlkv_table* mlkv_open_ex(int32_t dim, int64_t capacity, uint64_t seed, float max_load) {
+}  // extern "C"
+
+namespace {
+
+// Opens a table; cache_rows > 0 makes it tiered (rows at home in pinned host
+// memory, cache_rows of them in an HBM cache).
+mlkv_table* open_table(int32_t dim, int64_t capacity, uint64_t seed, float max_load, int64_t cache_rows) {
   if (dim < 1 || dim > 1024) {
     fail(MLKV_EINVAL, "dim must be in [1, 1024]");
     return nullptr;
@@ -307,13 +333,39 @@ mlkv_table* mlkv_open_ex(int32_t dim, int64_t capacity, uint64_t seed, float max
     return nullptr;
   }
   t->cus = std::max(1, t->cus);
+  t->cache_rows = cache_rows;
+  const int64_t hbm_rows = cache_rows > 0 ? cache_rows : capacity;
   if ((e = dev_alloc(&t->idx, sizeof(Bucket) * t->nb)) != hipSuccess ||
-      (e = dev_alloc(&t->rows, sizeof(float) * (size_t)capacity * (size_t)dim)) != hipSuccess ||
+      (e = dev_alloc(&t->rows, sizeof(float) * (size_t)hbm_rows * (size_t)dim)) != hipSuccess ||
       (e = dev_alloc(&t->state, sizeof(float) * (size_t)capacity)) != hipSuccess ||
       (e = dev_alloc(&t->ctrl, sizeof(Ctrl))) != hipSuccess) {
     hip_fail(e, "table allocation");
     mlkv_close(t);
     return nullptr;
+  }
+  if (cache_rows > 0) {
+    // the rows' home: pinned host memory the device reads and writes directly
+    void* h = nullptr;
+    e = hipHostMalloc(&h, sizeof(float) * (size_t)capacity * (size_t)dim, hipHostMallocMapped);
+    if (e == hipSuccess) {
+      t->host_alloc = h;
+      void* d = nullptr;
+      e = hipHostGetDevicePointer(&d, h, 0);
+      t->host_rows = static_cast<float*>(d);
+    }
+    if (e == hipSuccess) e = dev_alloc(&t->slot_of_row, sizeof(uint32_t) * (size_t)capacity);
+    if (e == hipSuccess) e = dev_alloc(&t->row_of_slot, sizeof(uint32_t) * (size_t)cache_rows);
+    if (e == hipSuccess) e = dev_alloc(&t->dirty, (size_t)cache_rows);
+    if (e == hipSuccess) e = dev_alloc(&t->keep, sizeof(uint32_t) * (size_t)cache_rows);
+    if (e == hipSuccess) e = hipMemset(t->slot_of_row, 0xFF, sizeof(uint32_t) * (size_t)capacity);  // no row cached
+    if (e == hipSuccess) e = hipMemset(t->row_of_slot, 0xFF, sizeof(uint32_t) * (size_t)cache_rows);
+    if (e == hipSuccess) e = hipMemset(t->dirty, 0, (size_t)cache_rows);
+    if (e == hipSuccess) e = hipMemset(t->keep, 0, sizeof(uint32_t) * (size_t)cache_rows);
+    if (e != hipSuccess) {
+      hip_fail(e, "tiered table allocation");
+      mlkv_close(t);
+      return nullptr;
+    }
   }
   // empty index: all key tags EMPTY (all ones) and all row ids pending (all ones)
   Ctrl c;
@@ -326,6 +378,22 @@ mlkv_table* mlkv_open_ex(int32_t dim, int64_t capacity, uint64_t seed, float max
     return nullptr;
   }
   return t;
+}
+
+}  // namespace
+
+extern "C" {
+
+mlkv_table* mlkv_open_ex(int32_t dim, int64_t capacity, uint64_t seed, float max_load) {
+  return open_table(dim, capacity, seed, max_load, 0);
+}
+
+mlkv_table* mlkv_open_tiered(int32_t dim, int64_t capacity, uint64_t seed, float max_load, int64_t cache_rows) {
+  if (cache_rows < 1 || cache_rows > capacity) {
+    fail(MLKV_EINVAL, "cache_rows must be in [1, capacity]");
+    return nullptr;
+  }
+  return open_table(dim, capacity, seed, max_load, cache_rows);
 }
 
 mlkv_table* mlkv_open(int32_t dim, int64_t capacity) {
@@ -364,6 +432,11 @@ void mlkv_close(mlkv_table* t) {
   (void)hipFree(t->state);
   (void)hipFree(t->ctrl);
   (void)hipFree(t->clock);
+  (void)hipFree(t->slot_of_row);
+  (void)hipFree(t->row_of_slot);
+  (void)hipFree(t->dirty);
+  (void)hipFree(t->keep);
+  if (t->host_alloc != nullptr) (void)hipHostFree(t->host_alloc);
   delete t;
 }
 
@@ -493,7 +566,53 @@ int mlkv_get_noalloc(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_
 }
 
 int mlkv_lookahead(mlkv_table* t, const uint64_t* d_keys, int64_t n, void* hip_stream) {
-  return get_call(t, d_keys, n, nullptr, nullptr, false, hip_stream);
+  int rc = get_call(t, d_keys, n, nullptr, nullptr, false, hip_stream);
+  if (rc != MLKV_OK || t->cache_rows == 0 || n == 0) return rc;
+  // tiered: the keys are resolved; now their rows come into the HBM cache
+  hipStream_t st = static_cast<hipStream_t>(hip_stream);
+  int64_t* rows_of_pos = reinterpret_cast<int64_t*>(t->items);  // put scratch, idle here
+  hipError_t e = launch_lookup(t->idx, t->nb_log2, d_keys, n, rows_of_pos, st);
+  if (e != hipSuccess) return hip_fail(e, "lookahead lookup launch");
+  if (++t->tier_tag == 0) ++t->tier_tag;  // 0 is the tag of no call
+  TierArgs a;
+  a.rows_of_pos = rows_of_pos;
+  a.n = n;
+  a.slot_of_row = t->slot_of_row;
+  a.row_of_slot = t->row_of_slot;
+  a.dirty = t->dirty;
+  a.keep = t->keep;
+  a.tag = t->tier_tag;
+  a.parity = t->tier_tag & 1u;
+  a.miss = t->miss;
+  a.plan_slot = t->plan_slot;
+  a.plan_old = t->plan_old;
+  a.plan_new = t->plan_new;
+  a.cache_rows = t->cache_rows;
+  a.cache = t->rows;
+  a.host = t->host_rows;
+  a.D = t->dim;
+  a.ctrl = t->ctrl;
+  e = launch_tier_lookahead(a, st, hook_of(t));
+  if (e != hipSuccess) return hip_fail(e, "lookahead copy launch");
+  return MLKV_OK;
+}
+
+int mlkv_cache_stats(mlkv_table* t, int64_t* out) {
+  int rc = check_table(t);
+  if (rc) return rc;
+  if (out == nullptr) return fail(MLKV_EINVAL, "out is NULL");
+  if (t->cache_rows == 0) return fail(MLKV_EINVAL, "the table is not tiered");
+  hipError_t e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+  Ctrl c;
+  e = hipMemcpy(&c, t->ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "read cache counters");
+  out[0] = (int64_t)c.tier_loaded;
+  out[1] = (int64_t)c.tier_evicted;
+  out[2] = (int64_t)c.tier_written;
+  out[3] = (int64_t)c.tier_filled;
+  out[4] = t->cache_rows;
+  return MLKV_OK;
 }
 
 int mlkv_get_bounded(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uint8_t* d_blocked,
@@ -715,7 +834,8 @@ int mlkv_profile_read(mlkv_table* t, double* total_ms, int64_t* launches) {
 }
 
 const char* mlkv_kernel_name(int kernel) {
-  static const char* names[K_COUNT] = {"get_probe_gather", "assign_new", "put_probe", "put_reduce"};
+  static const char* names[K_COUNT] = {"get_probe_gather", "assign_new", "put_probe", "put_reduce",
+                                       "tier_mark", "tier_plan", "tier_copy"};
   return (kernel >= 0 && kernel < K_COUNT) ? names[kernel] : nullptr;
 }
 

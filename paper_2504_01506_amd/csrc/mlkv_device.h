@@ -75,6 +75,16 @@ struct Ctrl {
   unsigned long long new_epoch;       // epoch of a call that inserted at least one key
   int latched;                        // first device-side error since mlkv_sync
   unsigned int pad[7];
+  // tiered tables: rows a lookahead call claimed as misses (ping-pong on the
+  // call count), the FIFO cursor over cache slots, the entries of the last
+  // copy plan, and running totals
+  unsigned long long tier_nmiss[2];
+  unsigned long long tier_cursor;
+  unsigned long long tier_nplan;
+  unsigned long long tier_loaded;   // rows copied from host memory into the cache
+  unsigned long long tier_evicted;  // rows whose slot was given to another row
+  unsigned long long tier_written;  // evicted rows written back (dirty)
+  unsigned long long tier_filled;   // slots holding a row
 };
 
 // ---------------------------------------------------------------------------

@@ -37,7 +37,10 @@ enum KernelId : int {
   K_ASSIGN_NEW = 1,
   K_PUT_PROBE = 2,
   K_PUT_REDUCE = 3,
-  K_COUNT = 4
+  K_TIER_MARK = 4,
+  K_TIER_PLAN = 5,
+  K_TIER_COPY = 6,
+  K_COUNT = 7
 };
 
 // Update a put call applies to each distinct key's row.
@@ -119,7 +122,30 @@ struct PutArgs {
   const uint32_t* pc_row;
 };
 
+// Lookahead of a tiered table, after its keys are resolved: rows_of_pos[n] the
+// row of each position (-1: absent).
+struct TierArgs {
+  const int64_t* rows_of_pos;
+  int64_t n;
+  uint32_t* slot_of_row;  // [capacity]
+  uint32_t* row_of_slot;  // [cache_rows]
+  uint8_t* dirty;         // [cache_rows]
+  uint32_t* keep;         // [cache_rows]
+  uint32_t tag;           // this lookahead call (never 0)
+  uint32_t parity;        // ping-pong index of the miss counter
+  uint32_t* miss;         // [n] scratch
+  uint32_t* plan_slot;    // [n] scratch
+  uint32_t* plan_old;
+  uint32_t* plan_new;
+  int64_t cache_rows;
+  float* cache;
+  float* host;
+  int D;
+  Ctrl* ctrl;
+};
+
 hipError_t launch_get(const GetArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook);
+hipError_t launch_tier_lookahead(const TierArgs& a, hipStream_t st, const LaunchHook& hook);
 hipError_t launch_put(const PutArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook);
 hipError_t launch_lookup(Bucket* idx, uint32_t nb_log2, const uint64_t* keys, int64_t n,
                          int64_t* rows_out, hipStream_t st);

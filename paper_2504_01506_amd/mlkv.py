@@ -18,7 +18,7 @@ MLKV_OK, MLKV_EINVAL, MLKV_EFULL, MLKV_ENOMEM, MLKV_EDEVICE = 0, -1, -2, -3, -4
 MLKV_DEFAULT_SEED = 0x4D4C4B56
 MLKV_RESERVED_KEY = 0xFFFFFFFFFFFFFFFF
 
-MLKV_NUM_KERNELS = 4
+MLKV_NUM_KERNELS = 7
 MLKV_NOALLOC_MAX_KEYS = 65536
 
 _lib = None
@@ -45,6 +45,8 @@ def load() -> ctypes.CDLL:
         "mlkv_open": (P, [I32, I64]),
         "mlkv_open_ex": (P, [I32, I64, U64, F32]),
         "mlkv_open_bounded": (P, [I32, I64, U64, F32, I64]),
+        "mlkv_open_tiered": (P, [I32, I64, U64, F32, I64]),
+        "mlkv_cache_stats": (INT, [P, P]),
         "mlkv_get": (INT, [P, P, I64, P, P]),
         "mlkv_get_bounded": (INT, [P, P, I64, P, P, P]),
         "mlkv_get_noalloc": (INT, [P, P, I64, P, P]),
@@ -129,6 +131,20 @@ def mlkv_open_bounded(dim: int, capacity: int, seed: int, max_load: float, stale
     if not h:
         raise MlkvError(MLKV_EINVAL, last_error())
     return h
+
+
+def mlkv_open_tiered(dim: int, capacity: int, seed: int, max_load: float, cache_rows: int) -> int:
+    h = load().mlkv_open_tiered(dim, capacity, seed, max_load, cache_rows)
+    if not h:
+        raise MlkvError(MLKV_EINVAL, last_error())
+    return h
+
+
+def mlkv_cache_stats(t: int) -> dict:
+    """{loaded, evicted, written_back, filled, cache_rows} of a tiered table."""
+    out = (ctypes.c_int64 * 5)()
+    _check(load().mlkv_cache_stats(t, out))
+    return dict(zip(("loaded", "evicted", "written_back", "filled", "cache_rows"), list(out)))
 
 
 def mlkv_get(t: int, keys, n: int, out, stream=None) -> int:
@@ -224,11 +240,16 @@ class Table:
     int64 tensor), rows fp32. Methods raise MlkvError on a non-zero code."""
 
     def __init__(self, dim: int, capacity: int, seed: int = MLKV_DEFAULT_SEED, max_load: float = 0.75,
-                 staleness_bound: int | None = None):
+                 staleness_bound: int | None = None, cache_rows: int | None = None):
         self.dim = int(dim)
         self.capacity = int(capacity)
         self.staleness_bound = staleness_bound
-        if staleness_bound is None:
+        self.cache_rows = cache_rows
+        if staleness_bound is not None and cache_rows is not None:
+            raise ValueError("a table is either bounded or tiered here")
+        if cache_rows is not None:
+            self.h = mlkv_open_tiered(self.dim, self.capacity, seed, max_load, int(cache_rows))
+        elif staleness_bound is None:
             self.h = mlkv_open_ex(self.dim, self.capacity, seed, max_load)
         else:
             self.h = mlkv_open_bounded(self.dim, self.capacity, seed, max_load, int(staleness_bound))
@@ -257,8 +278,12 @@ class Table:
         return blocked
 
     def lookahead(self, keys: torch.Tensor, stream=None):
-        """Insert the missing keys ahead of their gets (no output, no staleness count)."""
+        """Insert the missing keys ahead of their gets (no output, no staleness count);
+        on a tiered table, also bring their rows into the HBM cache."""
         _check(mlkv_lookahead(self.h, keys, keys.numel(), stream))
+
+    def cache_stats(self) -> dict:
+        return mlkv_cache_stats(self.h)
 
     def read_staleness(self, rows: torch.Tensor, stream=None) -> torch.Tensor:
         """Staleness counts (int32 view of uint32) of the given row ids (int64)."""
