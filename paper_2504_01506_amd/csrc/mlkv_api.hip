@@ -40,6 +40,7 @@ struct mlkv_table {
   int64_t cache_rows = 0;
   void* host_alloc = nullptr;       // the pinned allocation behind host_rows
   uint32_t tier_tag = 0;            // lookahead calls made (tags the rows each one keeps)
+  uint64_t tier_calls = 0;          // the same count without wrapping: its parity picks the miss counter
   // lookahead scratch (tiered tables): misses and the copy plan, n entries each
   uint32_t* miss = nullptr;
   uint32_t* plan_slot = nullptr;
@@ -582,7 +583,7 @@ int mlkv_lookahead(mlkv_table* t, const uint64_t* d_keys, int64_t n, void* hip_s
   a.dirty = t->dirty;
   a.keep = t->keep;
   a.tag = t->tier_tag;
-  a.parity = t->tier_tag & 1u;
+  a.parity = (uint32_t)(t->tier_calls++ & 1u);  // alternates on every call, also when the tag wraps
   a.miss = t->miss;
   a.plan_slot = t->plan_slot;
   a.plan_old = t->plan_old;
