@@ -39,13 +39,15 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBPS = 8000.0
 METRIC = "embedding get+put keys/sec and achieved HBM GB/s (% of peak), 1 MI355X"
 METRIC_KV = "key-value operations/sec, 50% get / 50% put, 1 MI355X"
-KERNELS = ("get_probe_gather", "assign_new", "put_probe", "put_reduce")
+KERNELS = ("get_probe_gather", "assign_new", "put_probe", "put_reduce", "rsort_count", "rsort_scatter",
+           "rsort_reduce")
 
 
-def kernel_bytes(n, U, M, D):
+def kernel_bytes(n, U, M, D, dedup="hash"):
     """Algorithmic bytes each kernel must move for one batch: n lookups, U
-    distinct keys of which M are new, rows of D fp32."""
-    return {
+    distinct keys of which M are new, rows of D fp32. With radix dedup the
+    reduce's bytes are rsort_reduce's; the sort passes move scratch only."""
+    b = {
         # keys in, one index entry (8 B tag + 4 B row) per distinct key,
         # distinct existing rows read, output rows written
         "get_probe_gather": 8 * n + 12 * U + 4 * D * (U - M) + 4 * D * n,
@@ -57,19 +59,25 @@ def kernel_bytes(n, U, M, D):
         # and written
         "put_reduce": 4 * D * n + 8 * D * U + 8 * U,
     }
+    return radix_bytes(b) if dedup == "radix" else b
 
 
-def kernel_bytes_kv(nr, Ur, nw, Uw, D):
+def radix_bytes(b):
+    return {**b, "rsort_count": 0, "rsort_scatter": 0, "rsort_reduce": b["put_reduce"], "put_reduce": 0}
+
+
+def kernel_bytes_kv(nr, Ur, nw, Uw, D, dedup="hash"):
     """The same for one step of the key-value mix: nr gets over Ur distinct
     existing keys, then a put of nw values over Uw distinct existing keys
     (the last value of each key is written)."""
-    return {
+    b = {
         "get_probe_gather": 8 * nr + 12 * Ur + 4 * D * Ur + 4 * D * nr,
         "assign_new": 0,
         "put_probe": 8 * nw + 12 * Uw,
         # the winning value of each key in, its row written
         "put_reduce": 8 * D * Uw,
     }
+    return radix_bytes(b) if dedup == "radix" else b
 
 
 def source_digest():
@@ -142,7 +150,7 @@ def parity_and_cpu_baseline(wl, args, kv, bounded, log):
     rec = None
     if P:
         cache = max(1, int(wl.capacity * args.cache_frac)) if args.cache_frac else None
-        gpu = mlkv.Table(D, wl.capacity, staleness_bound=bound, cache_rows=cache)
+        gpu = mlkv.Table(D, wl.capacity, staleness_bound=bound, cache_rows=cache, dedup=args.dedup)
         gpu.reserve(n)
         blocked = torch.empty(n, dtype=torch.uint8, device="cuda")
         zero = torch.zeros((1 << 16, D), device="cuda") if bounded else None
@@ -256,6 +264,9 @@ def main():
     ap.add_argument("--cache-frac", type=float, default=None,
                     help="tiered table: rows in pinned host memory, this fraction of them cached in HBM; "
                          "each step is lookahead(keys), get(keys), put_grad(keys)")
+    ap.add_argument("--dedup", choices=("hash", "radix"), default="hash",
+                    help="how puts find equal keys: hash partition + LDS grouping, or radix sort + run-length "
+                         "encoding (same results)")
     ap.add_argument("--copy-mib", type=int, default=1024,
                     help="size of the plain device copy timed as the achievable ceiling (and used to "
                          "calibrate rocprofv3 counters)")
@@ -319,7 +330,7 @@ def main():
     bounded = args.staleness_bound is not None
     tiered = args.cache_frac is not None
     cache_rows = max(1, int(wl.capacity * args.cache_frac)) if tiered else None
-    t = mlkv.Table(D, wl.capacity, staleness_bound=args.staleness_bound, cache_rows=cache_rows)
+    t = mlkv.Table(D, wl.capacity, staleness_bound=args.staleness_bound, cache_rows=cache_rows, dedup=args.dedup)
     t.reserve(n)  # scratch for the batch: no allocation inside the steps
     blocked = torch.empty(n, dtype=torch.uint8, device="cuda")
     t0 = time.perf_counter()
@@ -398,9 +409,9 @@ def main():
     ms_step = ms / args.steps
     keys_per_s = n * args.steps / (ms * 1e-3)
     if kv:
-        bytes_steps = [kernel_bytes_kv(h, Ur, n - h, Uw, D) for (Ur, Uw) in UM]
+        bytes_steps = [kernel_bytes_kv(h, Ur, n - h, Uw, D, args.dedup) for (Ur, Uw) in UM]
     else:
-        bytes_steps = [kernel_bytes(n, U, M, D) for (U, M) in UM]
+        bytes_steps = [kernel_bytes(n, U, M, D, args.dedup) for (U, M) in UM]
     alg_bytes = sum(sum(bytes_steps[s].values()) for s in timed)
     gbps = alg_bytes / (ms * 1e-3) / 1e9
     log(f"timed {args.steps} steps: {ms_step * 1e3:.2f} us/step (wall {wall * 1e3 / args.steps:.2f}), "
@@ -440,7 +451,7 @@ def main():
     host_link = None
     for kname in KERNELS:
         tot_ms, cnt = prof[kname]
-        b = sum(bytes_steps[s][kname] for s in timed)
+        b = sum(bytes_steps[s].get(kname, 0) for s in timed)
         if cnt == 0:
             continue
         avg_us = tot_ms * 1e3 / cnt
@@ -479,7 +490,7 @@ def main():
               key=lambda k: kinfo[k]["avg_us"] * kinfo[k]["launches"])
     digest = source_digest()
     # the committed counters were taken on the full-size DLRM-shaped workload
-    same_workload = args.config == "dlrm" and args.scale == 1.0 and not bounded
+    same_workload = args.config == "dlrm" and args.scale == 1.0 and not bounded and not tiered and args.dedup == "hash"
     traffic = load_traffic(dom, digest) if same_workload else None
     # the kernel's rocprofv3 duration, for comparison with the event-timed one
     # (an event pair around every launch adds about 2 us to each)
@@ -566,6 +577,7 @@ def main():
             "unique_keys_per_step": round(U_avg, 1), "scale": args.scale,
             **({"staleness_bound": args.staleness_bound} if bounded else {}),
             **({"tiered_cache_rows": cache_rows, "step": "lookahead + get + put_grad"} if tiered else {}),
+            **({"dedup": "radix sort + run-length encoding"} if args.dedup == "radix" else {}),
         },
         "gbps_effective": round(gbps, 1),
         "pct_of_peak_hbm": round(100.0 * gbps / PEAK_HBM_GBPS, 2),

@@ -176,6 +176,25 @@ int mlkv_put_grad_sgd(mlkv_table *t, const uint64_t *d_keys, const float *d_grad
  * is 0. d_values: n*dim floats, row-major. 0 <= n <= 2^30 - 1. */
 int mlkv_put(mlkv_table *t, const uint64_t *d_keys, const float *d_values, int64_t n, void *hip_stream);
 
+/* How the puts of a table (mlkv_put_grad, mlkv_put_grad_sgd, mlkv_put) find
+ * the equal keys of a batch before summing their gradients (Rmw, Sec. III-B;
+ * in-batch dedup of the sparse update):
+ *   MLKV_DEDUP_HASH  (the default) items of keys repeated within a tile of
+ *                    1024 positions are merged in LDS, then scattered by a
+ *                    hash digit of the key's row into partitions, and each
+ *                    partition is grouped by key with a hash table in LDS;
+ *   MLKV_DEDUP_RADIX the same in-tile merge, then a stable LSD radix sort of
+ *                    the items by the key's row (ceil(log2(capacity + index
+ *                    slots)) bits, passes of at most 9 bits), then runs of
+ *                    equal rows (run-length encoding) summed and applied.
+ * Results are identical either way. With MLKV_DEDUP_RADIX a put call takes at
+ * most 2^20 keys (MLKV_EINVAL above), and the table needs capacity + index
+ * slots < 2^32 (else this call fails with MLKV_EINVAL). Takes effect for the
+ * puts issued after it; returns MLKV_OK or MLKV_EINVAL. */
+#define MLKV_DEDUP_HASH 0
+#define MLKV_DEDUP_RADIX 1
+int mlkv_set_dedup(mlkv_table *t, int mode);
+
 /* Waits for all work on `hip_stream`, then returns and clears the first error
  * latched on the device since the previous mlkv_sync (MLKV_EFULL or
  * MLKV_EINVAL), or MLKV_OK. */
@@ -235,12 +254,14 @@ int mlkv_read_staleness(mlkv_table *t, const int64_t *d_rows, int64_t n, uint32_
  * 1 assign_new for mlkv_get, mlkv_get_bounded and mlkv_lookahead;
  * 2 put_probe and 3 put_reduce for mlkv_put_grad, mlkv_put_grad_sgd and
  * mlkv_put; 4 tier_mark, 5 tier_plan and 6 tier_copy for mlkv_lookahead on a
- * tiered table. While enabled, HIP events are recorded on
+ * tiered table; with radix dedup (mlkv_set_dedup) a put runs 2 put_probe,
+ * then 7 rsort_count and 8 rsort_scatter once per radix pass, then
+ * 9 rsort_reduce. While enabled, HIP events are recorded on
  * the call's stream before and after every launch. mlkv_profile_read waits
  * for the recorded launches, writes per-kernel sums of their durations (ms)
  * and launch counts into the host arrays total_ms[MLKV_NUM_KERNELS] and
  * launches[MLKV_NUM_KERNELS], and forgets them. */
-#define MLKV_NUM_KERNELS 7
+#define MLKV_NUM_KERNELS 10
 int mlkv_profile_enable(mlkv_table *t, int enable);
 int mlkv_profile_read(mlkv_table *t, double *total_ms, int64_t *launches);
 /* Name of kernel `kernel` (0 <= kernel < MLKV_NUM_KERNELS), else NULL. */

@@ -65,6 +65,9 @@ struct mlkv_table {
   uint32_t* meta = nullptr;
   uint64_t* spill = nullptr;
   uint64_t spill_words = 0;
+  uint32_t* rs_cnt = nullptr;  // radix dedup: per-tile digit counts and the item total
+  int dedup = kDedupHash;
+  int rs_bits = 0;             // radix dedup: bits of the sort key
   double* partials = nullptr;
   uint64_t* pc_key = nullptr;  // the last get's present keys and rows by position
   uint32_t* pc_row = nullptr;
@@ -111,7 +114,7 @@ void free_scratch_set(const ScratchSet& s) {
 ScratchSet current_set(mlkv_table* t) {
   ScratchSet s;
   s.ptrs = {t->newlist, t->tile_cnt, t->items, t->meta, t->spill, t->partials, t->pc_key, t->pc_row,
-            t->miss, t->plan_slot, t->plan_old, t->plan_new};
+            t->rs_cnt, t->miss, t->plan_slot, t->plan_old, t->plan_new};
   return s;
 }
 
@@ -128,6 +131,7 @@ void clear_workspace_ptrs(mlkv_table* t) {
   t->items = nullptr;
   t->meta = nullptr;
   t->spill = nullptr;
+  t->rs_cnt = nullptr;
   t->ws_n = 0;
   t->spill_words = 0;
 }
@@ -202,6 +206,9 @@ int ensure_workspace(mlkv_table* t, int64_t n, hipStream_t st) {
       (e = dev_alloc(&t->items, sizeof(uint64_t) * (size_t)slots)) != hipSuccess ||
       (e = dev_alloc(&t->meta, sizeof(uint32_t) * (size_t)kMaxParts * (size_t)put_tiles)) != hipSuccess ||
       (e = dev_alloc(&t->spill, sizeof(uint64_t) * (size_t)spill_words)) != hipSuccess ||
+      // radix counts: 2^kRsMaxBits digit rows of (radix tiles rounded up to 4), then the item total
+      (e = dev_alloc(&t->rs_cnt, sizeof(uint32_t) * (((size_t)(put_tiles + 3) / 4 + 4) * (1u << kRsMaxBits) + 64))) !=
+          hipSuccess ||
       (e = dev_alloc(&t->partials, sizeof(double) * (size_t)want * (size_t)t->dim)) != hipSuccess ||
       (e = dev_alloc(&t->pc_key, sizeof(uint64_t) * (size_t)slots)) != hipSuccess ||
       (e = dev_alloc(&t->pc_row, sizeof(uint32_t) * (size_t)slots)) != hipSuccess ||
@@ -652,6 +659,7 @@ int put_call(mlkv_table* t, const uint64_t* d_keys, const float* src, int64_t n,
     return fail(MLKV_EINVAL, "eps must be finite and >= 0");
   if (n == 0) return MLKV_OK;
   if (d_keys == nullptr || src == nullptr) return fail(MLKV_EINVAL, "keys or rows is NULL");
+  if (t->dedup == kDedupRadix && n > kRsMaxKeys) return fail(MLKV_EINVAL, "radix dedup takes at most 2^20 keys");
   if ((rc = ensure_workspace(t, n, static_cast<hipStream_t>(hip_stream))) != MLKV_OK) return rc;
   const uint32_t pb = call_part_bits(n, t->cus);
   // keys per put_probe tile: a multiple of 64, at most kPutTile, so that the
@@ -686,6 +694,11 @@ int put_call(mlkv_table* t, const uint64_t* d_keys, const float* src, int64_t n,
   a.clock = t->clock;
   a.pc_key = t->pc_key;
   a.pc_row = t->pc_row;
+  a.dedup = t->dedup;
+  a.cus = t->cus;
+  a.rs_bits = t->rs_bits;
+  a.rs_buf = t->spill;  // two n-item buffers (the spill area holds 4n words; radix puts never spill)
+  a.rs_cnt = t->rs_cnt;
   const bool vec4 = (t->dim % 4 == 0) && aligned16(src);
   hipError_t e = launch_put(a, vec4, static_cast<hipStream_t>(hip_stream), hook_of(t));
   if (e != hipSuccess) return hip_fail(e, "put launch");
@@ -705,6 +718,22 @@ int mlkv_put_grad(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, i
 int mlkv_put_grad_sgd(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, int64_t n, float lr,
                       void* hip_stream) {
   return put_call(t, d_keys, d_grads, n, kOpSgd, lr, 0.0f, hip_stream);
+}
+
+int mlkv_set_dedup(mlkv_table* t, int mode) {
+  int rc = check_table(t);
+  if (rc) return rc;
+  if (mode != kDedupHash && mode != kDedupRadix) return fail(MLKV_EINVAL, "unknown dedup mode");
+  if (mode == kDedupRadix) {
+    // sort keys: rows below capacity, a new key's index slot above it
+    const uint64_t top = (uint64_t)t->capacity + ((uint64_t)kSlots << t->nb_log2);
+    if (top > 0xFFFFFFFFull) return fail(MLKV_EINVAL, "radix dedup needs capacity + index slots < 2^32");
+    int b = 0;
+    while ((1ull << b) < top) ++b;
+    t->rs_bits = b;
+  }
+  t->dedup = mode;
+  return MLKV_OK;
 }
 
 int mlkv_put(mlkv_table* t, const uint64_t* d_keys, const float* d_values, int64_t n, void* hip_stream) {
@@ -836,7 +865,8 @@ int mlkv_profile_read(mlkv_table* t, double* total_ms, int64_t* launches) {
 
 const char* mlkv_kernel_name(int kernel) {
   static const char* names[K_COUNT] = {"get_probe_gather", "assign_new", "put_probe", "put_reduce",
-                                       "tier_mark", "tier_plan", "tier_copy"};
+                                       "tier_mark", "tier_plan", "tier_copy", "rsort_count",
+                                       "rsort_scatter", "rsort_reduce"};
   return (kernel >= 0 && kernel < K_COUNT) ? names[kernel] : nullptr;
 }
 

@@ -40,8 +40,21 @@ enum KernelId : int {
   K_TIER_MARK = 4,
   K_TIER_PLAN = 5,
   K_TIER_COPY = 6,
-  K_COUNT = 7
+  K_RSORT_COUNT = 7,
+  K_RSORT_SCATTER = 8,
+  K_RSORT_REDUCE = 9,
+  K_COUNT = 10
 };
+
+// How a put finds the equal keys of its batch.
+enum Dedup : int {
+  kDedupHash = 0,   // hash partition of the items, grouping in LDS per partition
+  kDedupRadix = 1   // stable LSD radix sort of the items by row, run-length encoding
+};
+constexpr int kRsTile = 4096;    // items per radix-sort block (four put tiles)
+constexpr int kRsMaxBits = 9;    // bits per radix pass at most
+constexpr int kRsChunk = 2048;   // sorted items per radix reduce block at most, before the cut moves to a run start
+constexpr int64_t kRsMaxKeys = 1 << 20;  // keys per put call with radix dedup
 
 // Update a put call applies to each distinct key's row.
 enum PutOp : int {
@@ -120,6 +133,11 @@ struct PutArgs {
   unsigned long long* clock;  // per-row staleness words, or nullptr when not tracked
   const uint64_t* pc_key;     // the last get's present keys and rows by position
   const uint32_t* pc_row;
+  int dedup;                  // Dedup
+  int cus;                    // compute units (radix reduce blocks at least)
+  int rs_bits;                // radix dedup: bits of the sort key (rows below capacity, new keys' slots above)
+  uint64_t* rs_buf;           // radix dedup: two n-item ping-pong buffers
+  uint32_t* rs_cnt;           // radix dedup: per-tile digit counts, then the item total
 };
 
 // Lookahead of a tiered table, after its keys are resolved: rows_of_pos[n] the

@@ -2294,6 +2294,315 @@ __global__ __launch_bounds__(NT) void k_put_reduce(
 }
 
 // ===========================================================================
+// Put with dedup by radix sort (Dedup kDedupRadix), the alternative to the
+// hash partition: put_probe with a single partition (its in-tile sums leave
+// each key at most one item per put tile), then a stable LSD radix sort of
+// all items by the key's row (rows below capacity, keys new in the call by
+// capacity + index slot), in passes of at most kRsMaxBits bits, each a count
+// kernel and a scatter kernel; then blocks that take even shares of the
+// sorted items, each cut moved forward to the start of a key's run,
+// run-length encode them in LDS and apply the updates as put_reduce does.
+// Stability keeps a key's items in put-tile order, which is position order.
+// ===========================================================================
+static_assert(kPresumMin == 2, "radix dedup: one item per key and put tile");
+static_assert(kRsTile == 4 * kPutTile, "a radix tile is four put tiles");
+constexpr int kRsThreads = 1024;
+constexpr int kRsPer = kRsTile / kRsThreads;
+constexpr int kRsDigits = 1 << kRsMaxBits;
+
+__device__ __forceinline__ uint32_t rs_key(uint64_t x, uint32_t cap) {
+  return item_fresh(x) ? cap + item_tag(x) : item_tag(x);
+}
+
+// The items a radix tile reads. First pass: put_probe's items, tile t being
+// put tiles 4t .. 4t+3, kPutTile slots each, the first (meta >> 16) of them
+// used. Later passes: the dense output of the previous pass.
+struct RsSrc {
+  const uint64_t* src;
+  const uint32_t* meta;   // first pass only
+  int ntiles;             // put tiles
+  const uint32_t* total;  // later passes: items in all
+};
+
+// Loads the tile's items: v[k] = item of element k * kRsThreads + tid, ok[k]
+// whether it exists.
+__device__ __forceinline__ void rs_load(const RsSrc& s, uint64_t (&v)[kRsPer], bool (&ok)[kRsPer]) {
+  const int64_t base = (int64_t)blockIdx.x * kRsTile;
+  const uint32_t T = s.meta == nullptr ? *s.total : 0u;
+#pragma unroll
+  for (int k = 0; k < kRsPer; ++k) {
+    const int64_t i = base + k * kRsThreads + threadIdx.x;
+    if (s.meta != nullptr) {
+      const int pt = (int)(i / kPutTile);
+      ok[k] = pt < s.ntiles && (uint32_t)(i % kPutTile) < (s.meta[pt] >> 16);
+    } else {
+      ok[k] = i < (int64_t)T;
+    }
+    v[k] = ok[k] ? s.src[i] : 0ull;
+  }
+}
+
+// Digit counts of one radix tile: cnt[d * stride + tile], digit-major, so that
+// a digit's counts over the tiles are contiguous (stride >= tiles, a multiple of 4).
+__global__ __launch_bounds__(kRsThreads) void k_rsort_count(RsSrc s, uint32_t cap, int shift, int bits,
+                                                            uint32_t* __restrict__ cnt, int stride) {
+  __shared__ uint32_t h[kRsDigits];
+  const int R = 1 << bits;
+  for (int d = threadIdx.x; d < R; d += kRsThreads) h[d] = 0;
+  uint64_t v[kRsPer];
+  bool ok[kRsPer];
+  rs_load(s, v, ok);
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kRsPer; ++k)
+    if (ok[k]) atomicAdd(&h[(rs_key(v[k], cap) >> shift) & (uint32_t)(R - 1)], 1u);
+  __syncthreads();
+  for (int d = threadIdx.x; d < R; d += kRsThreads) cnt[(size_t)d * stride + blockIdx.x] = h[d];
+}
+
+// Stable scatter of one radix tile by digit. An item goes to: items of smaller
+// digits in all tiles + items of its digit in earlier tiles + items of its
+// digit before it in this tile. The last term comes from a multisplit per
+// wave (lanes with the same digit found by one ballot per digit bit), waves
+// and batches taken in element order.
+__global__ __launch_bounds__(kRsThreads) void k_rsort_scatter(RsSrc s, uint32_t cap, int shift, int bits,
+                                                              const uint32_t* __restrict__ cnt, int rtiles,
+                                                              int stride, uint64_t* __restrict__ dst,
+                                                              uint32_t* __restrict__ total_out) {
+  constexpr int NT = kRsThreads, NW = NT / 64;
+  __shared__ uint32_t s_wc[NW * kRsDigits];  // per wave and digit: items, then where they start
+  __shared__ uint32_t s_run[kRsDigits];      // per digit: where the next batch's items start
+  __shared__ uint32_t s_w[NW];
+  const int R = 1 << bits;  // 16 .. kRsDigits
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int t = blockIdx.x;
+  uint64_t v[kRsPer];
+  bool ok[kRsPer];
+  rs_load(s, v, ok);
+  // the TPD threads of a digit (adjacent lanes) share the digit's counts
+  // over the tiles, four at a time (a digit's row is 16-byte aligned; the
+  // entries past the last tile are not counts)
+  {
+    const int TPD = NT / R;
+    const int d = tid / TPD, part = tid % TPD;
+    uint32_t all = 0, before = 0;
+    const uint4* row = reinterpret_cast<const uint4*>(cnt + (size_t)d * stride);
+    for (int u4 = part; u4 * 4 < rtiles; u4 += TPD) {
+      const uint4 c = row[u4];
+      const int u = u4 * 4;
+      const uint32_t c0 = c.x, c1 = u + 1 < rtiles ? c.y : 0u, c2 = u + 2 < rtiles ? c.z : 0u,
+                     c3 = u + 3 < rtiles ? c.w : 0u;
+      all += c0 + c1 + c2 + c3;
+      before += (u < t ? c0 : 0u) + (u + 1 < t ? c1 : 0u) + (u + 2 < t ? c2 : 0u) + (u + 3 < t ? c3 : 0u);
+    }
+    for (int o = 1; o < TPD; o <<= 1) {
+      all += __shfl_xor(all, o, 64);
+      before += __shfl_xor(before, o, 64);
+    }
+    uint32_t T;
+    const uint32_t ex = block_exclusive_scan<NT>(part == 0 ? all : 0u, s_w, &T);
+    if (part == 0) s_run[d] = ex + before;
+    if (total_out != nullptr && t == 0 && tid == 0) *total_out = T;
+  }
+  const uint64_t lt = (1ull << lane) - 1ull;
+#pragma unroll
+  for (int k = 0; k < kRsPer; ++k) {
+    for (int e = tid; e < NW * R; e += NT) s_wc[e] = 0u;
+    const uint32_t dg = ok[k] ? (rs_key(v[k], cap) >> shift) & (uint32_t)(R - 1) : 0u;
+    uint64_t m = __ballot(ok[k] ? 1 : 0);
+    for (int b = 0; b < bits; ++b) {
+      const bool on = (dg >> b) & 1u;
+      const uint64_t bb = __ballot(on ? 1 : 0);
+      m &= on ? bb : ~bb;
+    }
+    const uint32_t rank = (uint32_t)__popcll(m & lt);
+    __syncthreads();  // the table is cleared (and s_run written)
+    if (ok[k] && rank == 0) s_wc[wave * R + dg] = (uint32_t)__popcll(m);
+    __syncthreads();
+    if (tid < R) {
+      uint32_t run = s_run[tid];
+      for (int w = 0; w < NW; ++w) {
+        const uint32_t c = s_wc[w * R + tid];
+        s_wc[w * R + tid] = run;
+        run += c;
+      }
+      s_run[tid] = run;
+    }
+    __syncthreads();
+    if (ok[k]) dst[s_wc[wave * R + dg] + rank] = v[k];
+    __syncthreads();  // before the table is cleared again
+  }
+}
+
+// Cut point of the sorted items at or after p: the first position q >= p
+// where a key's run starts (q = T if none).
+template <int NT>
+__device__ __forceinline__ uint32_t rs_cut(const uint64_t* __restrict__ it, uint32_t T, uint32_t p,
+                                           uint32_t* s_min) {
+  if (p == 0 || p >= T) return min(p, T);
+  for (uint32_t q0 = p; q0 < T; q0 += NT) {
+    const uint32_t q = q0 + threadIdx.x;
+    if (threadIdx.x == 0) *s_min = T;
+    __syncthreads();
+    if (q < T && item_group(it[q]) != item_group(it[q - 1])) atomicMin(s_min, q);
+    __syncthreads();
+    const uint32_t f = *s_min;
+    __syncthreads();
+    if (f < T) return f;
+  }
+  return T;
+}
+
+// Run-length encoding of m sorted items it[0, m) (whole runs of equal keys)
+// into group_by_key's output: srt, seg, sid, info = {S, SA, MA, any key new
+// in the call}; segments that need a sum first (more than one item, or an
+// in-tile sum as the only item), their items [0, MA).
+template <int NT>
+__device__ __forceinline__ void encode_runs(const uint64_t* it, uint32_t m, uint64_t* srt, uint32_t* seg,
+                                            uint16_t* sid, uint32_t* r_start, uint32_t* r_dest, uint16_t* r_new,
+                                            uint16_t* r_of, uint32_t* s_w, uint32_t* info) {
+  constexpr int IPT = (kRedCap + NT - 1) / NT;
+  const int tid = threadIdx.x;
+  if (tid == 0) info[3] = 0u;
+  // 1. runs: the thread's IPT consecutive items
+  bool head[IPT];
+  uint32_t nh = 0;
+  bool fresh = false;
+#pragma unroll
+  for (int k = 0; k < IPT; ++k) {
+    const uint32_t j = (uint32_t)tid * IPT + k;
+    head[k] = j < m && (j == 0 || item_group(it[j]) != item_group(it[j - 1]));
+    nh += head[k] ? 1u : 0u;
+    fresh |= j < m && item_fresh(it[j]);
+  }
+  uint32_t S;
+  uint32_t r = block_exclusive_scan<NT>(nh, s_w, &S);
+  if (fresh) info[3] = 1u;
+#pragma unroll
+  for (int k = 0; k < IPT; ++k) {
+    const uint32_t j = (uint32_t)tid * IPT + k;
+    if (head[k]) r_start[r++] = j;
+    if (j < m) r_of[j] = (uint16_t)(r - 1);
+  }
+  if (tid == 0) r_start[S] = m;
+  __syncthreads();
+  // 2. new places: runs that need a sum first, in order, then the others
+  bool multi[IPT];
+  uint32_t len[IPT];
+  uint32_t packed = 0;  // runs that need a sum | their items << 16
+#pragma unroll
+  for (int k = 0; k < IPT; ++k) {
+    const uint32_t q = (uint32_t)tid * IPT + k;
+    multi[k] = false;
+    len[k] = 0;
+    if (q < S) {
+      len[k] = r_start[q + 1] - r_start[q];
+      multi[k] = len[k] > 1 || item_summed(it[r_start[q]]);
+      packed += multi[k] ? (1u | (len[k] << 16)) : 0u;
+    }
+  }
+  uint32_t tot;
+  const uint32_t pre = block_exclusive_scan<NT>(packed, s_w, &tot);
+  const uint32_t SA = tot & 0xFFFFu, MA = tot >> 16;
+  uint32_t na = pre & 0xFFFFu, ia = pre >> 16;
+#pragma unroll
+  for (int k = 0; k < IPT; ++k) {
+    const uint32_t q = (uint32_t)tid * IPT + k;
+    if (q < S) {
+      uint32_t ns, nd;
+      if (multi[k]) {
+        ns = na++;
+        nd = ia;
+        ia += len[k];
+      } else {
+        ns = SA + (q - na);  // the runs before q that need no sum, each one item
+        nd = MA + (q - na);
+      }
+      r_new[q] = (uint16_t)ns;
+      r_dest[q] = nd;
+      seg[ns] = nd;
+    }
+  }
+  if (tid == 0) {
+    seg[S] = m;
+    info[0] = S;
+    info[1] = SA;
+    info[2] = MA;
+  }
+  __syncthreads();
+  // 3. every item to its place
+  for (uint32_t j = tid; j < m; j += NT) {
+    const uint32_t q = r_of[j];
+    const uint32_t d = r_dest[q] + (j - r_start[q]);
+    srt[d] = it[j];
+    sid[d] = r_new[q];
+  }
+  __syncthreads();
+}
+
+template <class M, int NT>
+__global__ __launch_bounds__(NT) void k_rsort_reduce(
+    Bucket* __restrict__ idx, const uint64_t* __restrict__ sorted, const uint32_t* __restrict__ total,
+    int ntiles, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
+    const float* __restrict__ grads, double* __restrict__ partials, const RowStore store,
+    float* __restrict__ state, int D, uint64_t seed, float lr, float eps, int64_t capacity, Ctrl* ctrl,
+    uint64_t epoch, int op, unsigned long long* __restrict__ clock) {
+  using L = ReduceLds<NT>;
+  extern __shared__ __align__(16) unsigned char s_raw[];
+  uint64_t* s_it = reinterpret_cast<uint64_t*>(s_raw + L::it);
+  uint32_t* s_rstart = reinterpret_cast<uint32_t*>(s_raw + L::hidx);  // [kRedCap + 1]
+  uint32_t* s_rdest = reinterpret_cast<uint32_t*>(s_raw + L::hcnt);
+  uint16_t* s_rnew = reinterpret_cast<uint16_t*>(s_raw + L::inv);
+  uint16_t* s_rof = reinterpret_cast<uint16_t*>(s_raw + L::slot);
+  double* s_piece = reinterpret_cast<double*>(s_raw);      // reused region
+  uint64_t* s_chunk = reinterpret_cast<uint64_t*>(s_raw);  // reused region
+  uint64_t* s_srt = reinterpret_cast<uint64_t*>(s_raw + L::srt);
+  uint32_t* s_seg = reinterpret_cast<uint32_t*>(s_raw + L::seg);
+  uint16_t* s_sid = reinterpret_cast<uint16_t*>(s_raw + L::sid);
+  uint32_t* s_pref = reinterpret_cast<uint32_t*>(s_raw + L::pref);
+  uint32_t* s_w = reinterpret_cast<uint32_t*>(s_raw + L::w);
+  unsigned long long* s_w64 = reinterpret_cast<unsigned long long*>(s_raw + L::w64);
+  uint32_t* s_info = reinterpret_cast<uint32_t*>(s_raw + L::misc);
+  uint32_t* s_slo = reinterpret_cast<uint32_t*>(s_raw + L::slo);
+  static_assert(kRedHash >= kRedCap + 1, "run starts fit the hash region");
+
+  const uint64_t size0 = ctrl->size[epoch & 1];
+  const uint64_t new_e = ctrl->new_epoch, bad_e = ctrl->bad_epoch, ovf_e = ctrl->overflow_epoch;
+  const uint64_t Mnew = new_e == epoch ? count_new_keys<NT>(tile_cnt, ntiles, s_w64) : 0ull;
+  const int err = call_verdict(ctrl, epoch, size0, Mnew, capacity, bad_e, ovf_e);
+  const uint32_t T = *total;
+  const uint32_t nb = gridDim.x, b = blockIdx.x;
+  const uint32_t lo = rs_cut<NT>(sorted, T, (uint32_t)((uint64_t)T * b / nb), s_info + 4);
+  const uint32_t hi = rs_cut<NT>(sorted, T, (uint32_t)((uint64_t)T * (b + 1) / nb), s_info + 4);
+  const uint32_t m = hi - lo;
+  if (m == 0) return;
+  if (err) {
+    // undo the insertions of this call whose keys have their runs here
+    for (uint32_t j = threadIdx.x; j < m; j += NT) {
+      const uint64_t x = sorted[lo + j];
+      if (item_fresh(x)) {
+        const uint32_t slot = item_tag(x);
+        idx[slot / kSlots].key[slot % kSlots] = kEmptyKey;
+      }
+    }
+    return;
+  }
+  if (m > (uint32_t)kRedCap) {  // runs are at most one item per put tile; the host keeps this from happening
+    if (threadIdx.x == 0) atomicCAS(&ctrl->latched, 0, -4);
+    return;
+  }
+  for (uint32_t j = threadIdx.x; j < m; j += NT) s_it[j] = sorted[lo + j];
+  __syncthreads();
+  encode_runs<NT>(s_it, m, s_srt, s_seg, s_sid, s_rstart, s_rdest, s_rnew, s_rof, s_w, s_info);
+  const uint32_t S = s_info[0], SA = s_info[1], MA = s_info[2];
+  const RedCtx c{op, idx, grads, partials, store, state, D, seed, lr, eps, size0, clock};
+  if (s_info[3] != 0u)
+    resolve_new_rows<NT>(s_srt, s_seg, S, c, newlist, tile_cnt, ntiles, s_pref, s_w, s_w64, s_chunk);
+  if (op == kOpAssign) assign_segments<M, NT>(s_srt, s_seg, S, c);
+  else sum_and_update<M, NT>(s_srt, s_seg, s_sid, S, SA, MA, c, s_piece, s_slo);
+}
+
+// ===========================================================================
 // Inspection kernels
 // ===========================================================================
 __global__ __launch_bounds__(256) void k_lookup(Bucket* __restrict__ idx, uint32_t nb_log2,
@@ -2379,21 +2688,86 @@ static hipError_t launch_get_t(const GetArgs& a, hipStream_t st, const LaunchHoo
   return hipGetLastError();
 }
 
-// Whether the put_reduce instance of row map M may use its dynamic LDS on
-// each device (set once per device).
-template <class M>
-static hipError_t reduce_lds_attr() {
-  constexpr int kMaxDev = 64;
-  static bool done[kMaxDev] = {};
+// Lets kernel `f` (an instance of a reduce kernel) use `bytes` of dynamic
+// LDS on the current device; `done` remembers the devices where that is set.
+template <int kMaxDev>
+static hipError_t lds_attr(const void* f, int bytes, bool (&done)[kMaxDev]) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if (dev >= 0 && dev < kMaxDev && done[dev]) return hipSuccess;
-  constexpr int NT = ReduceCfg<M>::NT;
-  e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_put_reduce<M, NT>),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)ReduceLds<NT>::total);
+  e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
   if (e == hipSuccess && dev >= 0 && dev < kMaxDev) done[dev] = true;
   return e;
+}
+
+// Whether the put_reduce instance of row map M may use its dynamic LDS on
+// each device (set once per device).
+template <class M>
+static hipError_t reduce_lds_attr() {
+  static bool done[64] = {};
+  constexpr int NT = ReduceCfg<M>::NT;
+  return lds_attr(reinterpret_cast<const void*>(&k_put_reduce<M, NT>), (int)ReduceLds<NT>::total, done);
+}
+
+// The same for the radix reduce instance of row map M.
+template <class M>
+static hipError_t rsort_lds_attr() {
+  static bool done[64] = {};
+  constexpr int NT = ReduceCfg<M>::NT;
+  return lds_attr(reinterpret_cast<const void*>(&k_rsort_reduce<M, NT>), (int)ReduceLds<NT>::total, done);
+}
+
+// Put with radix dedup: put_probe (one partition), the radix passes, the
+// reduce over the sorted items.
+template <class M>
+static hipError_t launch_put_radix(const PutArgs& a, hipStream_t st, const LaunchHook& hook) {
+  constexpr int NT = ReduceCfg<M>::NT;
+  using L = ReduceLds<NT>;
+  const int64_t ntiles = (a.n + a.tlen - 1) / a.tlen;
+  hook(K_PUT_PROBE, 0, st);
+  hipLaunchKernelGGL(k_put_probe<M>, dim3((unsigned)ntiles), dim3(kPutThreads), 0, st, a.idx, a.nb_log2,
+                     a.keys, a.grads, a.n, a.tlen, a.D, a.op, 0, (int)ntiles, a.items, a.meta, a.partials,
+                     a.newlist, a.tile_cnt, a.ctrl, a.epoch, a.pc_key, a.pc_row);
+  hook(K_PUT_PROBE, 1, st);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // passes of at most kRsMaxBits bits (at least 4: a sort key spans at least 4 bits)
+  const int passes = (a.rs_bits + kRsMaxBits - 1) / kRsMaxBits;
+  const int bits = (a.rs_bits + passes - 1) / passes;
+  const int rtiles = (int)((ntiles + 3) / 4);
+  const int stride = (rtiles + 3) / 4 * 4;  // a digit's row of counts, padded to 16 bytes
+  uint32_t* cnt = a.rs_cnt;
+  uint32_t* total = a.rs_cnt + (size_t)stride * (1u << bits);
+  uint64_t* buf[2] = {a.rs_buf, a.rs_buf + a.n};
+  const uint32_t cap = (uint32_t)a.capacity;
+  for (int p = 0; p < passes; ++p) {
+    RsSrc src;
+    src.src = p == 0 ? a.items : buf[(p - 1) & 1];
+    src.meta = p == 0 ? a.meta : nullptr;
+    src.ntiles = (int)ntiles;
+    src.total = total;
+    hook(K_RSORT_COUNT, 0, st);
+    hipLaunchKernelGGL(k_rsort_count, dim3((unsigned)rtiles), dim3(kRsThreads), 0, st, src, cap, p * bits, bits,
+                       cnt, stride);
+    hook(K_RSORT_COUNT, 1, st);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hook(K_RSORT_SCATTER, 0, st);
+    hipLaunchKernelGGL(k_rsort_scatter, dim3((unsigned)rtiles), dim3(kRsThreads), 0, st, src, cap, p * bits, bits,
+                       (const uint32_t*)cnt, rtiles, stride, buf[p & 1], p == 0 ? total : (uint32_t*)nullptr);
+    hook(K_RSORT_SCATTER, 1, st);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  if ((e = rsort_lds_attr<M>()) != hipSuccess) return e;
+  // blocks: one per CU at least, at most kRsChunk sorted items each before the cuts move
+  const int64_t nb = std::max<int64_t>(a.cus, (a.n + kRsChunk - 1) / kRsChunk);
+  hook(K_RSORT_REDUCE, 0, st);
+  hipLaunchKernelGGL((k_rsort_reduce<M, NT>), dim3((unsigned)nb), dim3(NT), L::total, st, a.idx,
+                     (const uint64_t*)buf[(passes - 1) & 1], (const uint32_t*)total, (int)ntiles, a.newlist,
+                     a.tile_cnt, a.grads, a.partials, a.store, a.state, a.D, a.seed, a.lr, a.eps, a.capacity, a.ctrl,
+                     a.epoch, a.op, a.clock);
+  hook(K_RSORT_REDUCE, 1, st);
+  return hipGetLastError();
 }
 
 template <class M>
@@ -2405,6 +2779,7 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   static_assert((size_t)(kChunk + NT) * sizeof(uint64_t) + (size_t)(NT + 1) * sizeof(uint32_t) <= L::reuse,
                 "new-key chunk, sorted new keys and their counts must fit the reused LDS region");
   static_assert(L::total <= 160 * 1024, "LDS budget of a gfx950 workgroup");
+  if (a.dedup == kDedupRadix) return launch_put_radix<M>(a, st, hook);
   const int64_t ntiles = (a.n + a.tlen - 1) / a.tlen;
   const int np = 1 << a.pb;
   hook(K_PUT_PROBE, 0, st);

@@ -18,7 +18,9 @@ MLKV_OK, MLKV_EINVAL, MLKV_EFULL, MLKV_ENOMEM, MLKV_EDEVICE = 0, -1, -2, -3, -4
 MLKV_DEFAULT_SEED = 0x4D4C4B56
 MLKV_RESERVED_KEY = 0xFFFFFFFFFFFFFFFF
 
-MLKV_NUM_KERNELS = 7
+MLKV_NUM_KERNELS = 10
+MLKV_DEDUP_HASH, MLKV_DEDUP_RADIX = 0, 1
+DEDUP_MODES = {"hash": MLKV_DEDUP_HASH, "radix": MLKV_DEDUP_RADIX}
 MLKV_NOALLOC_MAX_KEYS = 65536
 
 _lib = None
@@ -59,6 +61,7 @@ def load() -> ctypes.CDLL:
         "mlkv_size": (I64, [P]),
         "mlkv_num_slots": (I64, [P]),
         "mlkv_reserve": (INT, [P, I64]),
+        "mlkv_set_dedup": (INT, [P, INT]),
         "mlkv_close": (None, [P]),
         "mlkv_last_error": (ctypes.c_char_p, []),
         "mlkv_lookup_rows": (INT, [P, P, I64, P, P]),
@@ -195,6 +198,10 @@ def mlkv_reserve(t: int, n: int) -> int:
     return load().mlkv_reserve(t, n)
 
 
+def mlkv_set_dedup(t: int, mode: int) -> int:
+    return load().mlkv_set_dedup(t, mode)
+
+
 def mlkv_close(t: int) -> None:
     load().mlkv_close(t)
 
@@ -240,7 +247,7 @@ class Table:
     int64 tensor), rows fp32. Methods raise MlkvError on a non-zero code."""
 
     def __init__(self, dim: int, capacity: int, seed: int = MLKV_DEFAULT_SEED, max_load: float = 0.75,
-                 staleness_bound: int | None = None, cache_rows: int | None = None):
+                 staleness_bound: int | None = None, cache_rows: int | None = None, dedup: str = "hash"):
         self.dim = int(dim)
         self.capacity = int(capacity)
         self.staleness_bound = staleness_bound
@@ -253,6 +260,13 @@ class Table:
             self.h = mlkv_open_ex(self.dim, self.capacity, seed, max_load)
         else:
             self.h = mlkv_open_bounded(self.dim, self.capacity, seed, max_load, int(staleness_bound))
+        if dedup != "hash":
+            self.set_dedup(dedup)
+
+    def set_dedup(self, mode: str):
+        """How puts find equal keys: "hash" (partition + LDS grouping) or "radix"
+        (radix sort by row + run-length encoding); results are the same."""
+        _check(mlkv_set_dedup(self.h, DEDUP_MODES[mode]))
 
     def close(self):
         if self.h:

@@ -87,10 +87,10 @@ class Pair:
     """A GPU table and an oracle table that receive exactly the same calls."""
 
     def __init__(self, dim, capacity, seed=mlkv.MLKV_DEFAULT_SEED, max_load=0.75, lazy_oracle=False,
-                 staleness_bound=None, cache_rows=None):
+                 staleness_bound=None, cache_rows=None, dedup="hash"):
         self.dim = dim
         self.gpu = mlkv.Table(dim, capacity, seed=seed, max_load=max_load, staleness_bound=staleness_bound,
-                              cache_rows=cache_rows)
+                              cache_rows=cache_rows, dedup=dedup)
         self.ora = O.OracleTable(dim, capacity, seed=seed, staleness_bound=staleness_bound)
         self.updated = np.zeros(capacity, dtype=bool)  # rows written by put_grad at least once
         self.stats = {"max_err": 0.0, "max_ulp": 0, "exact_mismatch": 0}
