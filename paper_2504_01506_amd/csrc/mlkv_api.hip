@@ -44,8 +44,6 @@ struct mlkv_table {
   // lookahead scratch (tiered tables): misses and the copy plan, n entries each
   uint32_t* miss = nullptr;
   uint32_t* plan_slot = nullptr;
-  uint32_t* plan_old = nullptr;
-  uint32_t* plan_new = nullptr;
   Ctrl* ctrl = nullptr;
   // sequence number of calls that may change the table; starts at 1 because
   // the control block's epoch markers start at 0 ("no call")
@@ -114,15 +112,13 @@ void free_scratch_set(const ScratchSet& s) {
 ScratchSet current_set(mlkv_table* t) {
   ScratchSet s;
   s.ptrs = {t->newlist, t->tile_cnt, t->items, t->meta, t->spill, t->partials, t->pc_key, t->pc_row,
-            t->rs_cnt, t->miss, t->plan_slot, t->plan_old, t->plan_new};
+            t->rs_cnt, t->miss, t->plan_slot};
   return s;
 }
 
 void clear_workspace_ptrs(mlkv_table* t) {
   t->miss = nullptr;
   t->plan_slot = nullptr;
-  t->plan_old = nullptr;
-  t->plan_new = nullptr;
   t->pc_key = nullptr;
   t->pc_row = nullptr;
   t->partials = nullptr;
@@ -218,9 +214,7 @@ int ensure_workspace(mlkv_table* t, int64_t n, hipStream_t st) {
   }
   if (t->cache_rows > 0 &&
       ((e = dev_alloc(&t->miss, sizeof(uint32_t) * (size_t)want)) != hipSuccess ||
-       (e = dev_alloc(&t->plan_slot, sizeof(uint32_t) * (size_t)want)) != hipSuccess ||
-       (e = dev_alloc(&t->plan_old, sizeof(uint32_t) * (size_t)want)) != hipSuccess ||
-       (e = dev_alloc(&t->plan_new, sizeof(uint32_t) * (size_t)want)) != hipSuccess)) {
+       (e = dev_alloc(&t->plan_slot, sizeof(uint32_t) * (size_t)want)) != hipSuccess)) {
     free_workspace(t);
     return hip_fail(e, "lookahead scratch allocation");
   }
@@ -578,12 +572,11 @@ int mlkv_lookahead(mlkv_table* t, const uint64_t* d_keys, int64_t n, void* hip_s
   if (rc != MLKV_OK || t->cache_rows == 0 || n == 0) return rc;
   // tiered: the keys are resolved; now their rows come into the HBM cache
   hipStream_t st = static_cast<hipStream_t>(hip_stream);
-  int64_t* rows_of_pos = reinterpret_cast<int64_t*>(t->items);  // put scratch, idle here
-  hipError_t e = launch_lookup(t->idx, t->nb_log2, d_keys, n, rows_of_pos, st);
-  if (e != hipSuccess) return hip_fail(e, "lookahead lookup launch");
   if (++t->tier_tag == 0) ++t->tier_tag;  // 0 is the tag of no call
   TierArgs a;
-  a.rows_of_pos = rows_of_pos;
+  a.idx = t->idx;
+  a.nb_log2 = t->nb_log2;
+  a.keys = d_keys;
   a.n = n;
   a.slot_of_row = t->slot_of_row;
   a.row_of_slot = t->row_of_slot;
@@ -593,14 +586,12 @@ int mlkv_lookahead(mlkv_table* t, const uint64_t* d_keys, int64_t n, void* hip_s
   a.parity = (uint32_t)(t->tier_calls++ & 1u);  // alternates on every call, also when the tag wraps
   a.miss = t->miss;
   a.plan_slot = t->plan_slot;
-  a.plan_old = t->plan_old;
-  a.plan_new = t->plan_new;
   a.cache_rows = t->cache_rows;
   a.cache = t->rows;
   a.host = t->host_rows;
   a.D = t->dim;
   a.ctrl = t->ctrl;
-  e = launch_tier_lookahead(a, st, hook_of(t));
+  hipError_t e = launch_tier_lookahead(a, st, hook_of(t));
   if (e != hipSuccess) return hip_fail(e, "lookahead copy launch");
   return MLKV_OK;
 }

@@ -140,10 +140,11 @@ struct PutArgs {
   uint32_t* rs_cnt;           // radix dedup: per-tile digit counts, then the item total
 };
 
-// Lookahead of a tiered table, after its keys are resolved: rows_of_pos[n] the
-// row of each position (-1: absent).
+// Lookahead of a tiered table, after the get kernels have resolved its n keys.
 struct TierArgs {
-  const int64_t* rows_of_pos;
+  Bucket* idx;
+  uint32_t nb_log2;
+  const uint64_t* keys;
   int64_t n;
   uint32_t* slot_of_row;  // [capacity]
   uint32_t* row_of_slot;  // [cache_rows]
@@ -153,8 +154,6 @@ struct TierArgs {
   uint32_t parity;        // ping-pong index of the miss counter
   uint32_t* miss;         // [n] scratch
   uint32_t* plan_slot;    // [n] scratch
-  uint32_t* plan_old;
-  uint32_t* plan_new;
   int64_t cache_rows;
   float* cache;
   float* host;

@@ -1,14 +1,19 @@
 // Tiered tables: rows at home in pinned host memory, a fixed number of them
 // cached in HBM. Lookahead (Sec. III-A, look-ahead prefetching of Sec. III-C2)
 // makes the rows of a batch resident in the cache ahead of their gets:
-//   mark    every position's row: a cached one is kept for this call, an
-//           uncached one is claimed (once per row) as a miss;
+//   mark    every position's key is looked up (the get kernels have just
+//           inserted the missing ones) and its row marked: a cached one is
+//           kept for this call, an uncached one is claimed (once per row) as
+//           a miss;
 //   plan    one block walks the cache slots from a FIFO cursor and gives the
-//           misses the first slots this call does not keep, evicting their
-//           rows (dirty ones are written back); misses beyond the slots that
-//           are free to take stay at home;
-//   copy    a wave per planned slot writes back the evicted row, then copies
-//           the missing row in, over the host link.
+//           misses the first slots this call does not keep;
+//   copy    a wave per four misses moves the directory entries (the slot's
+//           old row goes home, the missing row comes in; misses beyond the
+//           slots free to take stay at home), writes the evicted row back if
+//           it is dirty, then copies the missing row in, over the host link.
+// A taken slot is not kept by the call, so its old row is not one the call
+// asked for, and every miss is claimed once: the entries each miss changes
+// are its own, and the copy kernel changes them in parallel.
 // Gets and puts read and write rows wherever they are (RowStore), so the
 // cache never changes a result.
 #include "mlkv_kernels.h"
@@ -20,8 +25,10 @@ constexpr int kMarkThreads = 256;
 constexpr int kPlanThreads = 1024;
 constexpr int kCopyThreads = 256;
 constexpr int kCopyRows = 4;  // rows a wave copies at a time
+constexpr int kPlanPer = 16;  // cache slots a plan thread examines per pass
 
-__global__ __launch_bounds__(kMarkThreads) void k_tier_mark(const int64_t* __restrict__ rows_of_pos, int64_t n,
+__global__ __launch_bounds__(kMarkThreads) void k_tier_mark(Bucket* __restrict__ idx, uint32_t nb_log2,
+                                                            const uint64_t* __restrict__ keys, int64_t n,
                                                             uint32_t* __restrict__ slot_of_row,
                                                             uint32_t* __restrict__ keep, uint32_t tag,
                                                             uint32_t* __restrict__ miss, Ctrl* ctrl,
@@ -34,7 +41,11 @@ __global__ __launch_bounds__(kMarkThreads) void k_tier_mark(const int64_t* __res
   int64_t r = -1;
   uint32_t mine = 0xFFFFFFFFu;
   if (i < n) {
-    r = rows_of_pos[i];  // -1: key absent (a failed insert)
+    const uint64_t key = keys[i];
+    if (key != kEmptyKey) {
+      const Probe pr = probe_key(idx, nb_log2, key, false);
+      if (pr.status == P_HIT) r = pr.row;  // else absent (the call's insert failed)
+    }
     if (r >= 0) {
       const uint32_t s = slot_of_row[r];
       if (s < kClaimed) {
@@ -51,107 +62,126 @@ __global__ __launch_bounds__(kMarkThreads) void k_tier_mark(const int64_t* __res
   if (mine != 0xFFFFFFFFu) miss[s_base + mine] = (uint32_t)r;
 }
 
-__global__ __launch_bounds__(kPlanThreads) void k_tier_plan(uint32_t* __restrict__ slot_of_row,
-                                                            uint32_t* __restrict__ row_of_slot,
-                                                            uint8_t* __restrict__ dirty,
-                                                            const uint32_t* __restrict__ keep, uint32_t tag,
-                                                            const uint32_t* __restrict__ miss,
-                                                            uint32_t* __restrict__ plan_slot,
-                                                            uint32_t* __restrict__ plan_old,
-                                                            uint32_t* __restrict__ plan_new, uint64_t C, Ctrl* ctrl,
+__global__ __launch_bounds__(kPlanThreads) void k_tier_plan(const uint32_t* __restrict__ keep, uint32_t tag,
+                                                            uint32_t* __restrict__ plan_slot, uint64_t C, Ctrl* ctrl,
                                                             uint32_t parity) {
   constexpr int NT = kPlanThreads;
   __shared__ uint32_t s_w[NT / 64];
-  __shared__ unsigned long long s_w64[NT / 64];
   const uint64_t M = ctrl->tier_nmiss[parity];
   const uint64_t cur = ctrl->tier_cursor;
-  // the first M slots from the cursor on that this call does not keep
+  // the first M slots from the cursor on that this call does not keep; a
+  // thread examines kPlanPer consecutive slots per pass
   uint64_t found = 0;
-  for (uint64_t i0 = 0; i0 < C && found < M; i0 += NT) {
-    const uint64_t i = i0 + threadIdx.x;
-    const uint64_t s = (cur + i) % C;
-    const uint32_t cand = (i < C && keep[s] != tag) ? 1u : 0u;
+  for (uint64_t i0 = 0; i0 < C && found < M; i0 += (uint64_t)NT * kPlanPer) {
+    const uint64_t b = i0 + (uint64_t)threadIdx.x * kPlanPer;
+    // slot of position i from the cursor: cur + i < 2C, so one subtraction wraps it
+    auto slot_at = [&](uint64_t i) { const uint64_t x = cur + i; return x >= C ? x - C : x; };
+    uint32_t cand = 0;  // bit j: slot_at(b + j) is free to take
+#pragma unroll
+    for (int j = 0; j < kPlanPer; ++j) {
+      const uint64_t i = b + j;
+      if (i < C && keep[slot_at(i)] != tag) cand |= 1u << j;
+    }
     uint32_t tot;
-    const uint32_t pre = block_exclusive_scan<NT>(cand, s_w, &tot);
-    const uint64_t v = found + pre;
-    if (cand && v < M) plan_slot[v] = (uint32_t)s;
+    const uint32_t pre = block_exclusive_scan<NT>((uint32_t)__popc(cand), s_w, &tot);
+    uint64_t v = found + pre;
+    for (int j = 0; j < kPlanPer && v < M; ++j) {
+      if ((cand >> j) & 1u) {
+        const uint64_t sl = slot_at(b + j);
+        plan_slot[v] = (uint32_t)sl;
+        ++v;
+      }
+    }
     found += tot;
   }
   const uint64_t A = found < M ? found : M;
   __syncthreads();  // the plan's slots are written
-  // the taken slots change hands; misses without a slot stay at home
-  uint64_t ev = 0, wb = 0;
-  for (uint64_t v = threadIdx.x; v < M; v += NT) {
-    const uint32_t r = miss[v];
-    if (v >= A) {
-      slot_of_row[r] = kNoSlot;
-      continue;
-    }
-    const uint32_t s = plan_slot[v];
-    const uint32_t old = row_of_slot[s];
-    const bool write_back = old != kNoSlot && dirty[s] != 0;
-    if (old != kNoSlot) {
-      slot_of_row[old] = kNoSlot;
-      ++ev;
-    }
-    wb += write_back ? 1 : 0;
-    plan_old[v] = write_back ? old : kNoSlot;
-    plan_new[v] = r;
-    row_of_slot[s] = r;
-    slot_of_row[r] = s;
-    dirty[s] = 0;
-  }
-  ev = block_sum_u64<NT>(ev, s_w64);
-  wb = block_sum_u64<NT>(wb, s_w64);
-  // the cursor moves past the last slot taken
-  __shared__ unsigned long long s_last;
-  if (threadIdx.x == 0) s_last = cur;
-  __syncthreads();
-  if (A > 0 && threadIdx.x == 0) s_last = (plan_slot[A - 1] + 1) % C;
-  __syncthreads();
   if (threadIdx.x == 0) {
-    ctrl->tier_cursor = s_last;
+    ctrl->tier_cursor = A > 0 ? (plan_slot[A - 1] + 1 == C ? 0 : plan_slot[A - 1] + 1) : cur;  // past the last slot taken
     ctrl->tier_nplan = A;
-    ctrl->tier_loaded += A;
-    ctrl->tier_evicted += ev;
-    ctrl->tier_written += wb;
-    ctrl->tier_filled += A - ev;
   }
 }
 
-// A wave per planned slot (kCopyRows slots at a time): the evicted dirty row
-// goes back to its home, then the missing row comes in.
-__global__ __launch_bounds__(kCopyThreads) void k_tier_copy(const uint32_t* __restrict__ plan_slot,
-                                                            const uint32_t* __restrict__ plan_old,
-                                                            const uint32_t* __restrict__ plan_new,
-                                                            const Ctrl* ctrl, float* __restrict__ cache,
-                                                            float* __restrict__ host, int D) {
+// A wave per kCopyRows misses: a miss given a slot moves in (its slot's old
+// row goes home, written back first if dirty), a miss beyond the slots free
+// to take stays at home. Counters are added once per block.
+__global__ __launch_bounds__(kCopyThreads) void k_tier_copy(const uint32_t* __restrict__ miss,
+                                                            const uint32_t* __restrict__ plan_slot,
+                                                            uint32_t* __restrict__ slot_of_row,
+                                                            uint32_t* __restrict__ row_of_slot,
+                                                            uint8_t* __restrict__ dirty, Ctrl* ctrl, uint32_t parity,
+                                                            float* __restrict__ cache, float* __restrict__ host,
+                                                            int D) {
+  __shared__ unsigned long long s_ev, s_wb, s_in;
+  if (threadIdx.x == 0) s_ev = s_wb = s_in = 0;
+  __syncthreads();
+  const uint64_t M = ctrl->tier_nmiss[parity];
   const uint64_t A = ctrl->tier_nplan;
   const int lane = threadIdx.x & 63;
   const uint64_t waves = (uint64_t)gridDim.x * (kCopyThreads / 64);
   const uint64_t w0 = (uint64_t)blockIdx.x * (kCopyThreads / 64) + (threadIdx.x >> 6);
-  for (uint64_t e0 = w0 * kCopyRows; e0 < A; e0 += waves * kCopyRows) {
+  uint32_t ev = 0, wbn = 0, inn = 0;
+  for (uint64_t e0 = w0 * kCopyRows; e0 < M; e0 += waves * kCopyRows) {
     uint32_t s[kCopyRows], old[kCopyRows], nw[kCopyRows];
+    bool back[kCopyRows];
 #pragma unroll
     for (int u = 0; u < kCopyRows; ++u) {
       const uint64_t e = e0 + u;
-      s[u] = e < A ? plan_slot[e] : kNoSlot;
-      old[u] = e < A ? plan_old[e] : kNoSlot;
-      nw[u] = e < A ? plan_new[e] : kNoSlot;
+      s[u] = kNoSlot;
+      old[u] = kNoSlot;
+      nw[u] = kNoSlot;
+      back[u] = false;
+      if (e < M) {
+        const uint32_t r = miss[e];
+        if (e < A) {
+          s[u] = plan_slot[e];
+          old[u] = row_of_slot[s[u]];
+          back[u] = old[u] != kNoSlot && dirty[s[u]] != 0;
+          nw[u] = r;
+        } else if (lane == 0) {
+          slot_of_row[r] = kNoSlot;  // no slot for it: it stays at home
+        }
+      }
+    }
+    // the directory (one lane per entry; the copies below read no entry)
+    if (lane == 0) {
+#pragma unroll
+      for (int u = 0; u < kCopyRows; ++u) {
+        if (nw[u] == kNoSlot) continue;
+        if (old[u] != kNoSlot) slot_of_row[old[u]] = kNoSlot;
+        row_of_slot[s[u]] = nw[u];
+        slot_of_row[nw[u]] = s[u];
+        dirty[s[u]] = 0;
+        ev += old[u] != kNoSlot ? 1u : 0u;
+        wbn += back[u] ? 1u : 0u;
+        inn += 1u;
+      }
     }
     for (int col = lane; col < D; col += 64) {
       float wv[kCopyRows], nv[kCopyRows];
 #pragma unroll
       for (int u = 0; u < kCopyRows; ++u) {
-        if (old[u] != kNoSlot) wv[u] = cache[(size_t)s[u] * D + col];
+        if (back[u]) wv[u] = cache[(size_t)s[u] * D + col];
         if (nw[u] != kNoSlot) nv[u] = host[(size_t)nw[u] * D + col];
       }
 #pragma unroll
       for (int u = 0; u < kCopyRows; ++u) {
-        if (old[u] != kNoSlot) host[(size_t)old[u] * D + col] = wv[u];
+        if (back[u]) host[(size_t)old[u] * D + col] = wv[u];
         if (nw[u] != kNoSlot) cache[(size_t)s[u] * D + col] = nv[u];
       }
     }
+  }
+  if (lane == 0 && inn > 0) {
+    atomicAdd(&s_ev, (unsigned long long)ev);
+    atomicAdd(&s_wb, (unsigned long long)wbn);
+    atomicAdd(&s_in, (unsigned long long)inn);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0 && s_in > 0) {
+    atomicAdd(&ctrl->tier_loaded, s_in);
+    atomicAdd(&ctrl->tier_evicted, s_ev);
+    atomicAdd(&ctrl->tier_written, s_wb);
+    atomicAdd(&ctrl->tier_filled, s_in - s_ev);
   }
 }
 
@@ -159,22 +189,23 @@ hipError_t launch_tier_lookahead(const TierArgs& a, hipStream_t st, const Launch
   if (a.n == 0) return hipSuccess;
   hook(K_TIER_MARK, 0, st);
   const int64_t mb = (a.n + kMarkThreads - 1) / kMarkThreads;
-  hipLaunchKernelGGL(k_tier_mark, dim3((unsigned)mb), dim3(kMarkThreads), 0, st, a.rows_of_pos, a.n, a.slot_of_row,
+  hipLaunchKernelGGL(k_tier_mark, dim3((unsigned)mb), dim3(kMarkThreads), 0, st, a.idx, a.nb_log2, a.keys, a.n,
+                     a.slot_of_row,
                      a.keep, a.tag, a.miss, a.ctrl, a.parity);
   hook(K_TIER_MARK, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hook(K_TIER_PLAN, 0, st);
-  hipLaunchKernelGGL(k_tier_plan, dim3(1), dim3(kPlanThreads), 0, st, a.slot_of_row, a.row_of_slot, a.dirty, a.keep,
-                     a.tag, a.miss, a.plan_slot, a.plan_old, a.plan_new, (uint64_t)a.cache_rows, a.ctrl, a.parity);
+  hipLaunchKernelGGL(k_tier_plan, dim3(1), dim3(kPlanThreads), 0, st, a.keep, a.tag, a.plan_slot,
+                     (uint64_t)a.cache_rows, a.ctrl, a.parity);
   hook(K_TIER_PLAN, 1, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  const int64_t most = std::min<int64_t>(a.n, a.cache_rows);
+  // every miss (at most n) gets a lane group's turn
   const int64_t per_block = (kCopyThreads / 64) * kCopyRows;
-  const int64_t cb = std::max<int64_t>(1, std::min<int64_t>((most + per_block - 1) / per_block, 2048));
+  const int64_t cb = std::max<int64_t>(1, std::min<int64_t>((a.n + per_block - 1) / per_block, 2048));
   hook(K_TIER_COPY, 0, st);
-  hipLaunchKernelGGL(k_tier_copy, dim3((unsigned)cb), dim3(kCopyThreads), 0, st, a.plan_slot, a.plan_old,
-                     a.plan_new, a.ctrl, a.cache, a.host, a.D);
+  hipLaunchKernelGGL(k_tier_copy, dim3((unsigned)cb), dim3(kCopyThreads), 0, st, a.miss, a.plan_slot, a.slot_of_row,
+                     a.row_of_slot, a.dirty, a.ctrl, a.parity, a.cache, a.host, a.D);
   hook(K_TIER_COPY, 1, st);
   return hipGetLastError();
 }
