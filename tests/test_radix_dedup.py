@@ -9,6 +9,7 @@ the oracle, which has one dedup only: results must not depend on the mode.
   key's items in fp64 in position order, split between lane groups at
   different places; the rounded results agree on these inputs);
 * the full-size DLRM table for three steps, as the bench runs it;
+* staleness counts on a bounded table and a tiered table's cache;
 * the per-call limit (2^20 keys) and unknown modes are refused.
 """
 import numpy as np
@@ -151,3 +152,50 @@ def test_limits():
         t.put_grad(k, g, 0.01, 1e-8)
     t.set_dedup("hash")
     t.close()
+
+
+def test_bounded_staleness_counts_with_radix():
+    # gets two steps ahead of the puts (bound 1: some keys block); every put
+    # op lowers the counts of its distinct keys once, as with hash dedup
+    rng = np.random.default_rng(44)
+    dim = 16
+    pr = Pair(dim, 30_000, staleness_bound=1, dedup="radix")
+    batches, nblocked = [], 0
+    for s in range(9):
+        k = rng.integers(0, 7000, size=int(rng.integers(1000, 5000))).astype(np.uint64) * np.uint64(0x9E3779B1)
+        batches.append(k)
+        bl = pr.get_bounded(k)
+        nblocked += int(bl.sum())
+        if len(batches) > 2:
+            done = batches.pop(0)
+            g = rng.normal(0, 0.01, size=(done.size, dim)).astype(np.float32)
+            if s % 3 == 0:
+                pr.put(done, g, 0.01, 1e-8)
+            elif s % 3 == 1:
+                pr.put_sgd(done, g, 0.05)
+            else:
+                pr.upsert(done, g)
+            if bl.any():
+                pr.get_bounded(batches[-1][bl == 1])
+        pr.compare_staleness()
+    assert nblocked > 0
+    pr.compare_rows()
+    pr.check_index()
+    pr.close()
+
+
+def test_tiered_table_with_radix():
+    wl = W.make("dlrm", scale=0.02, steps=4)
+    cache = int(wl.capacity * 0.2)
+    pr = Pair(wl.dim, wl.capacity, cache_rows=cache, dedup="radix")
+    pr.prefill(wl.prefill_keys())
+    for s in range(4):
+        keys = wl.keys(s)
+        pr.lookahead(keys)
+        pr.get(keys)
+        pr.put(keys, wl.grads(s), wl.lr, wl.eps)
+    st = pr.gpu.cache_stats()
+    assert st["loaded"] > 0 and st["loaded"] == st["filled"] + st["evicted"] and st["filled"] <= cache
+    pr.compare_rows()
+    record("radix dedup tiered dlrm@0.02x4 cache=0.2", {**pr.stats, **st})
+    pr.close()
