@@ -1295,6 +1295,17 @@ __device__ __forceinline__ void put_clock(unsigned long long* __restrict__ clock
   if ((w & kClockCount) != 0) clock[row] = w - 1;
 }
 
+// The same from the low 32 bits of the word, loaded ahead with the row: they
+// hold the count (a nonzero count drops without borrowing from the epoch
+// bits above it, so only the low word is written).
+static_assert(kClockBits < 32, "the count fits the low word of a staleness word");
+__device__ __forceinline__ uint32_t clock_low(const unsigned long long* __restrict__ clock, uint32_t row) {
+  return reinterpret_cast<const uint32_t*>(clock + row)[0];  // little-endian: the low word comes first
+}
+__device__ __forceinline__ void put_clock_low(unsigned long long* __restrict__ clock, uint32_t row, uint32_t lo) {
+  if ((lo & (uint32_t)kClockCount) != 0u) reinterpret_cast<uint32_t*>(clock + row)[0] = lo - 1u;
+}
+
 // Run-length encodes items sorted by value: seg[s] = first item of segment s,
 // seg[S] = mp, sid[j] = segment of item j. Returns S (block-uniform).
 template <int NT, class IP, class SP, class DP>
@@ -1867,8 +1878,9 @@ __device__ __forceinline__ void add_raw(double* acc, const RawRow<VEC>& r, bool 
 
 // One update step (op of c) for the rows rw[u] with on[u], given their summed
 // gradients gq[u]: the rows (and accumulators) of the N keys are loaded
-// together, updated and written back; a bounded table's counts drop.
-template <class M, int N>
+// together, updated and written back; a bounded table's counts drop (kClk:
+// the table has staleness words).
+template <class M, int N, bool kClk>
 __device__ __forceinline__ void update_rows(const bool (&on)[N], const uint32_t (&rw)[N],
                                             const typename VecT<M::VEC>::T (&gq)[N][M::K], const RedCtx& c, int q,
                                             bool d_pow2, double inv_d) {
@@ -1878,10 +1890,13 @@ __device__ __forceinline__ void update_rows(const bool (&on)[N], const uint32_t 
   V w[N][K];
   float G[N];
   float* wr[N];
+  uint32_t cl[N];  // low words of the rows' staleness words (bounded tables)
+  const bool clk = kClk && q == 0;
 #pragma unroll
   for (int u = 0; u < N; ++u) {
     G[u] = 0.0f;
     wr[u] = nullptr;
+    cl[u] = 0u;
     if (on[u]) {
       wr[u] = c.store.wptr(rw[u]);
 #pragma unroll
@@ -1890,13 +1905,14 @@ __device__ __forceinline__ void update_rows(const bool (&on)[N], const uint32_t 
         if (col < D) w[u][k] = load_vec<VEC>(wr[u] + col);
       }
       if (c.op == kOpAdagrad) G[u] = c.state[rw[u]];
+      if (clk) cl[u] = clock_low(c.clock, rw[u]);
     }
   }
 #pragma unroll
   for (int u = 0; u < N; ++u)
     if (on[u]) {
       SegmentOps<M>::update(c.op, gq[u], w[u], G[u], wr[u], c.state, rw[u], D, q, d_pow2, inv_d, c.lr, c.eps);
-      if (c.clock != nullptr && q == 0) put_clock(c.clock, rw[u]);
+      if (clk) put_clock_low(c.clock, rw[u], cl[u]);
     }
 }
 
@@ -1910,7 +1926,7 @@ __device__ __forceinline__ void update_rows(const bool (&on)[N], const uint32_t 
 // cut between shares began adds the later parts in share order and updates
 // it. Each group also updates an even share of the keys seen once (g is their
 // gradient row).
-template <class M, int NT>
+template <class M, int NT, bool kClk>
 __device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32_t* seg, const uint16_t* sid,
                                                uint32_t S, uint32_t SA, uint32_t MA, const RedCtx& c,
                                                double* s_piece, uint32_t* s_slo) {
@@ -1954,6 +1970,8 @@ __device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32
   Ops::zero(acc);
   V wc[K];
   float Gc = 0.0f;
+  uint32_t Cc = 0u;  // low word of the open segment's staleness word (bounded tables)
+  const bool clk = kClk && q == 0;
   uint32_t rowc = 0;
   float* wrc = nullptr;
   bool last_ends = true, last_owned = true;
@@ -1964,6 +1982,7 @@ __device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32
     RawRow<VEC> raw[B][K];
     V wl[B][K];
     float Gl[B];
+    uint32_t Cl[B];
     float* wp[B];
 #pragma unroll
     for (int u = 0; u < B; ++u) {
@@ -1972,6 +1991,7 @@ __device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32
       fst[u] = 0;
       end[u] = 0;
       Gl[u] = 0.0f;
+      Cl[u] = 0u;
       wp[u] = nullptr;
       if (j < hi) {
         x[u] = srt[j];
@@ -1994,6 +2014,7 @@ __device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32
             if (col < D) wl[u][k] = load_vec<VEC>(wp[u] + col);
           }
           if (c.op == kOpAdagrad) Gl[u] = c.state[r];
+          if (clk) Cl[u] = clock_low(c.clock, r);
         }
       }
     }
@@ -2007,6 +2028,7 @@ __device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32
 #pragma unroll
           for (int k = 0; k < K; ++k) wc[k] = wl[u][k];
           Gc = Gl[u];
+          Cc = Cl[u];
         }
         const bool summ = item_summed(x[u]);
 #pragma unroll
@@ -2022,7 +2044,7 @@ __device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32
             V g[K];
             to_f32(g, acc);
             Ops::update(c.op, g, wc, Gc, wrc, c.state, rowc, D, q, d_pow2, inv_d, c.lr, c.eps);
-            if (c.clock != nullptr && q == 0) put_clock(c.clock, rowc);
+            if (clk) put_clock_low(c.clock, rowc, Cc);
           } else {
             put_piece(acc);  // the end of a segment begun in an earlier share
           }
@@ -2058,7 +2080,7 @@ __device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32
           }
         }
       }
-      update_rows<M, BS>(on, rw, gq, c, q, d_pow2, inv_d);
+      update_rows<M, BS, kClk>(on, rw, gq, c, q, d_pow2, inv_d);
     }
   }
 
@@ -2080,15 +2102,15 @@ __device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32
       }
     }
     V g[K];
-    to_f32(g, acc);  // the row and accumulator were loaded with the segment's first item
+    to_f32(g, acc);  // the row, accumulator and staleness word came with the segment's first item
     Ops::update(c.op, g, wc, Gc, wrc, c.state, rowc, D, q, d_pow2, inv_d, c.lr, c.eps);
-    if (c.clock != nullptr && q == 0) put_clock(c.clock, rowc);
+    if (clk) put_clock_low(c.clock, rowc, Cc);
   }
 }
 
 // Put with the assignment op: each key's row becomes the value row at its
 // last position. Lane groups take even shares of the segments.
-template <class M, int NT>
+template <class M, int NT, bool kClk>
 __device__ __forceinline__ void assign_segments(const uint64_t* srt, const uint32_t* seg, uint32_t S,
                                                 const RedCtx& c) {
   using Cfg = ReduceCfg<M>;
@@ -2101,11 +2123,13 @@ __device__ __forceinline__ void assign_segments(const uint64_t* srt, const uint3
   const uint32_t k0 = (uint32_t)((uint64_t)S * gid / NG), k1 = (uint32_t)((uint64_t)S * (gid + 1) / NG);
   for (uint32_t s0 = k0; s0 < k1; s0 += BS) {
     V v[BS][K];
-    uint32_t rw[BS];
+    uint32_t rw[BS], cl[BS];
+    const bool clk = kClk && q == 0;
 #pragma unroll
     for (int u = 0; u < BS; ++u) {
       const uint32_t s = s0 + u;
       rw[u] = 0;
+      cl[u] = 0u;
       if (s < k1) {
         rw[u] = item_tag(srt[seg[s]]);
         const float* src = c.grads + (size_t)item_pos(srt[seg[s + 1] - 1]) * (size_t)D;
@@ -2114,13 +2138,14 @@ __device__ __forceinline__ void assign_segments(const uint64_t* srt, const uint3
           const int col = (k * LPR + q) * VEC;
           if (col < D) v[u][k] = load_vec<VEC>(src + col);
         }
+        if (clk) cl[u] = clock_low(c.clock, rw[u]);
       }
     }
 #pragma unroll
     for (int u = 0; u < BS; ++u) {
       if (s0 + u >= k1) continue;
       SegmentOps<M>::assign(v[u], c.store.wptr(rw[u]), D, q);
-      if (c.clock != nullptr && q == 0) put_clock(c.clock, rw[u]);
+      if (clk) put_clock_low(c.clock, rw[u], cl[u]);
     }
   }
 }
@@ -2171,7 +2196,7 @@ __device__ __forceinline__ void reduce_partition_global(uint32_t p, uint32_t mp,
   update_segments<M, NT>(it, seg, S, c);
 }
 
-template <class M, int NT>
+template <class M, int NT, bool kClk>
 __global__ __launch_bounds__(NT) void k_put_reduce(
     Bucket* __restrict__ idx, const uint64_t* __restrict__ items, const uint32_t* __restrict__ meta,
     int ntiles, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
@@ -2289,8 +2314,8 @@ __global__ __launch_bounds__(NT) void k_put_reduce(
   const uint32_t S = s_info[0], SA = s_info[1], MA = s_info[2];
   if (s_info[3] != 0u)
     resolve_new_rows<NT>(s_srt, s_seg, S, c, newlist, tile_cnt, ntiles, s_pref, s_w, s_w64, s_chunk);
-  if (op == kOpAssign) assign_segments<M, NT>(s_srt, s_seg, S, c);
-  else sum_and_update<M, NT>(s_srt, s_seg, s_sid, S, SA, MA, c, s_piece, s_slo);
+  if (op == kOpAssign) assign_segments<M, NT, kClk>(s_srt, s_seg, S, c);
+  else sum_and_update<M, NT, kClk>(s_srt, s_seg, s_sid, S, SA, MA, c, s_piece, s_slo);
 }
 
 // ===========================================================================
@@ -2540,7 +2565,7 @@ __device__ __forceinline__ void encode_runs(const uint64_t* it, uint32_t m, uint
   __syncthreads();
 }
 
-template <class M, int NT>
+template <class M, int NT, bool kClk>
 __global__ __launch_bounds__(NT) void k_rsort_reduce(
     Bucket* __restrict__ idx, const uint64_t* __restrict__ sorted, const uint32_t* __restrict__ total,
     int ntiles, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
@@ -2598,8 +2623,8 @@ __global__ __launch_bounds__(NT) void k_rsort_reduce(
   const RedCtx c{op, idx, grads, partials, store, state, D, seed, lr, eps, size0, clock};
   if (s_info[3] != 0u)
     resolve_new_rows<NT>(s_srt, s_seg, S, c, newlist, tile_cnt, ntiles, s_pref, s_w, s_w64, s_chunk);
-  if (op == kOpAssign) assign_segments<M, NT>(s_srt, s_seg, S, c);
-  else sum_and_update<M, NT>(s_srt, s_seg, s_sid, S, SA, MA, c, s_piece, s_slo);
+  if (op == kOpAssign) assign_segments<M, NT, kClk>(s_srt, s_seg, S, c);
+  else sum_and_update<M, NT, kClk>(s_srt, s_seg, s_sid, S, SA, MA, c, s_piece, s_slo);
 }
 
 // ===========================================================================
@@ -2703,19 +2728,19 @@ static hipError_t lds_attr(const void* f, int bytes, bool (&done)[kMaxDev]) {
 
 // Whether the put_reduce instance of row map M may use its dynamic LDS on
 // each device (set once per device).
-template <class M>
+template <class M, bool kClk>
 static hipError_t reduce_lds_attr() {
   static bool done[64] = {};
   constexpr int NT = ReduceCfg<M>::NT;
-  return lds_attr(reinterpret_cast<const void*>(&k_put_reduce<M, NT>), (int)ReduceLds<NT>::total, done);
+  return lds_attr(reinterpret_cast<const void*>(&k_put_reduce<M, NT, kClk>), (int)ReduceLds<NT>::total, done);
 }
 
 // The same for the radix reduce instance of row map M.
-template <class M>
+template <class M, bool kClk>
 static hipError_t rsort_lds_attr() {
   static bool done[64] = {};
   constexpr int NT = ReduceCfg<M>::NT;
-  return lds_attr(reinterpret_cast<const void*>(&k_rsort_reduce<M, NT>), (int)ReduceLds<NT>::total, done);
+  return lds_attr(reinterpret_cast<const void*>(&k_rsort_reduce<M, NT, kClk>), (int)ReduceLds<NT>::total, done);
 }
 
 // Put with radix dedup: put_probe (one partition), the radix passes, the
@@ -2758,14 +2783,15 @@ static hipError_t launch_put_radix(const PutArgs& a, hipStream_t st, const Launc
     hook(K_RSORT_SCATTER, 1, st);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  if ((e = rsort_lds_attr<M>()) != hipSuccess) return e;
+  const bool clk = a.clock != nullptr;
+  if ((e = clk ? rsort_lds_attr<M, true>() : rsort_lds_attr<M, false>()) != hipSuccess) return e;
   // blocks: one per CU at least, at most kRsChunk sorted items each before the cuts move
   const int64_t nb = std::max<int64_t>(a.cus, (a.n + kRsChunk - 1) / kRsChunk);
+  auto rkern = clk ? k_rsort_reduce<M, NT, true> : k_rsort_reduce<M, NT, false>;
   hook(K_RSORT_REDUCE, 0, st);
-  hipLaunchKernelGGL((k_rsort_reduce<M, NT>), dim3((unsigned)nb), dim3(NT), L::total, st, a.idx,
-                     (const uint64_t*)buf[(passes - 1) & 1], (const uint32_t*)total, (int)ntiles, a.newlist,
-                     a.tile_cnt, a.grads, a.partials, a.store, a.state, a.D, a.seed, a.lr, a.eps, a.capacity, a.ctrl,
-                     a.epoch, a.op, a.clock);
+  hipLaunchKernelGGL(rkern, dim3((unsigned)nb), dim3(NT), L::total, st, a.idx, (const uint64_t*)buf[(passes - 1) & 1], (const uint32_t*)total,
+                     (int)ntiles, a.newlist, a.tile_cnt, a.grads, a.partials, a.store, a.state, a.D, a.seed, a.lr,
+                     a.eps, a.capacity, a.ctrl, a.epoch, a.op, a.clock);
   hook(K_RSORT_REDUCE, 1, st);
   return hipGetLastError();
 }
@@ -2789,11 +2815,14 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   hook(K_PUT_PROBE, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if ((e = reduce_lds_attr<M>()) != hipSuccess) return e;
+  const bool clk = a.clock != nullptr;  // a bounded table: puts lower the staleness counts
+  if ((e = clk ? reduce_lds_attr<M, true>() : reduce_lds_attr<M, false>()) != hipSuccess) return e;
+  auto kern = clk ? k_put_reduce<M, NT, true> : k_put_reduce<M, NT, false>;
   hook(K_PUT_REDUCE, 0, st);
-  hipLaunchKernelGGL((k_put_reduce<M, NT>), dim3((unsigned)np), dim3(NT), L::total, st, a.idx, a.items, a.meta,
-                     (int)ntiles, a.newlist, a.tile_cnt, a.grads, a.partials, a.store, a.state, a.D, a.seed,
-                     a.lr, a.eps, a.capacity, a.ctrl, a.epoch, a.spill, a.spill_words, a.op, a.clock);
+  hipLaunchKernelGGL(kern, dim3((unsigned)np), dim3(NT),
+                     L::total, st, a.idx, a.items, a.meta, (int)ntiles, a.newlist, a.tile_cnt, a.grads, a.partials,
+                     a.store, a.state, a.D, a.seed, a.lr, a.eps, a.capacity, a.ctrl, a.epoch, a.spill, a.spill_words,
+                     a.op, a.clock);
   hook(K_PUT_REDUCE, 1, st);
   return hipGetLastError();
 }
