@@ -21,3 +21,23 @@ def test_staleness_bound_is_refused_for_the_key_value_mix():
     r = _run("--config", "kv-uniform", "--staleness-bound", "0")
     assert r.returncode == 2
     assert "staleness-bound" in r.stderr
+
+
+def test_unknown_dedup_mode_is_refused():
+    r = _run("--dedup", "bucket")
+    assert r.returncode == 2
+    assert "--dedup" in r.stderr
+
+
+def test_radix_dedup_moves_the_reduce_bytes_to_its_reduce_kernel():
+    sys.path.insert(0, ROOT)
+    import bench
+    for n, U, M, D in ((212_992, 60_864, 0, 64), (4096, 1700, 1700, 16)):
+        h = bench.kernel_bytes(n, U, M, D)
+        r = bench.kernel_bytes(n, U, M, D, "radix")
+        assert sum(h.values()) == sum(r.values())
+        assert r["rsort_reduce"] == h["put_reduce"] and r["put_reduce"] == 0
+        assert r["rsort_count"] == r["rsort_scatter"] == 0
+    kv_h = bench.kernel_bytes_kv(1 << 19, 400_000, 1 << 19, 400_000, 4)
+    kv_r = bench.kernel_bytes_kv(1 << 19, 400_000, 1 << 19, 400_000, 4, "radix")
+    assert sum(kv_h.values()) == sum(kv_r.values()) and kv_r["rsort_reduce"] == kv_h["put_reduce"]
