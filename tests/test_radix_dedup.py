@@ -199,3 +199,18 @@ def test_tiered_table_with_radix():
     pr.compare_rows()
     record("radix dedup tiered dlrm@0.02x4 cache=0.2", {**pr.stats, **st})
     pr.close()
+
+
+def test_reserved_key_in_a_put_fails_the_whole_call():
+    rng = np.random.default_rng(45)
+    pr = Pair(8, 5000, dedup="radix")
+    keys = rng.choice(np.arange(1, 10**6, dtype=np.uint64), size=1500, replace=False)
+    pr.put(keys[:1000], rng.normal(0, 0.01, size=(1000, 8)).astype(np.float32), 0.01, 1e-8)
+    bad = keys.copy()
+    bad[700] = np.uint64(mlkv.MLKV_RESERVED_KEY)  # and 500 keys never seen
+    pr.gpu.put_grad(dev_keys(bad), dev(np.ones((bad.size, 8), np.float32)), 0.01, 1e-8)
+    assert pr.gpu.sync() == mlkv.MLKV_EINVAL
+    assert pr.gpu.size == 1000
+    pr.compare_rows()  # no row changed, nothing inserted
+    pr.check_index()
+    pr.close()
