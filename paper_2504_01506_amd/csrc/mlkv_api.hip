@@ -577,6 +577,8 @@ int mlkv_lookahead(mlkv_table* t, const uint64_t* d_keys, int64_t n, void* hip_s
   a.idx = t->idx;
   a.nb_log2 = t->nb_log2;
   a.keys = d_keys;
+  a.pc_key = t->pc_key;  // written by the get kernels of this lookahead
+  a.pc_row = t->pc_row;
   a.n = n;
   a.slot_of_row = t->slot_of_row;
   a.row_of_slot = t->row_of_slot;

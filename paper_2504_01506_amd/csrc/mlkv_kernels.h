@@ -145,6 +145,8 @@ struct TierArgs {
   Bucket* idx;
   uint32_t nb_log2;
   const uint64_t* keys;
+  const uint64_t* pc_key;  // the get's present keys and rows by position
+  const uint32_t* pc_row;
   int64_t n;
   uint32_t* slot_of_row;  // [capacity]
   uint32_t* row_of_slot;  // [cache_rows]

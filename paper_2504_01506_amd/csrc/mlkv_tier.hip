@@ -1,8 +1,8 @@
 // Tiered tables: rows at home in pinned host memory, a fixed number of them
 // cached in HBM. Lookahead (Sec. III-A, look-ahead prefetching of Sec. III-C2)
 // makes the rows of a batch resident in the cache ahead of their gets:
-//   mark    every position's key is looked up (the get kernels have just
-//           inserted the missing ones) and its row marked: a cached one is
+//   mark    every position's row (the row the lookahead's get found there,
+//           or, for a key it inserted, a lookup) is marked: a cached one is
 //           kept for this call, an uncached one is claimed (once per row) as
 //           a miss;
 //   plan    one block walks the cache slots from a FIFO cursor and gives the
@@ -28,7 +28,9 @@ constexpr int kCopyRows = 4;  // rows a wave copies at a time
 constexpr int kPlanPer = 16;  // cache slots a plan thread examines per pass
 
 __global__ __launch_bounds__(kMarkThreads) void k_tier_mark(Bucket* __restrict__ idx, uint32_t nb_log2,
-                                                            const uint64_t* __restrict__ keys, int64_t n,
+                                                            const uint64_t* __restrict__ keys,
+                                                            const uint64_t* __restrict__ pc_key,
+                                                            const uint32_t* __restrict__ pc_row, int64_t n,
                                                             uint32_t* __restrict__ slot_of_row,
                                                             uint32_t* __restrict__ keep, uint32_t tag,
                                                             uint32_t* __restrict__ miss, Ctrl* ctrl,
@@ -42,7 +44,9 @@ __global__ __launch_bounds__(kMarkThreads) void k_tier_mark(Bucket* __restrict__
   uint32_t mine = 0xFFFFFFFFu;
   if (i < n) {
     const uint64_t key = keys[i];
-    if (key != kEmptyKey) {
+    if (key != kEmptyKey && pc_key[i] == key) {
+      r = pc_row[i];  // present before the call: the get recorded its row here
+    } else if (key != kEmptyKey) {
       const Probe pr = probe_key(idx, nb_log2, key, false);
       if (pr.status == P_HIT) r = pr.row;  // else absent (the call's insert failed)
     }
@@ -189,8 +193,8 @@ hipError_t launch_tier_lookahead(const TierArgs& a, hipStream_t st, const Launch
   if (a.n == 0) return hipSuccess;
   hook(K_TIER_MARK, 0, st);
   const int64_t mb = (a.n + kMarkThreads - 1) / kMarkThreads;
-  hipLaunchKernelGGL(k_tier_mark, dim3((unsigned)mb), dim3(kMarkThreads), 0, st, a.idx, a.nb_log2, a.keys, a.n,
-                     a.slot_of_row,
+  hipLaunchKernelGGL(k_tier_mark, dim3((unsigned)mb), dim3(kMarkThreads), 0, st, a.idx, a.nb_log2, a.keys,
+                     a.pc_key, a.pc_row, a.n, a.slot_of_row,
                      a.keep, a.tag, a.miss, a.ctrl, a.parity);
   hook(K_TIER_MARK, 1, st);
   hipError_t e = hipGetLastError();
