@@ -1,7 +1,8 @@
 """mlkv_get_noalloc (the get that allocates nothing, its scratch in a fixed
 device array) against mlkv_get on a twin table: two calls in a row, the
 second smaller, then again after a put_grad on both tables; bit-exact
-output rows, key -> row and size. Larger batches are refused."""
+output rows, key -> row and size; the same on tiered twin tables, with rows
+cached, at home and evicted. Larger batches are refused."""
 import numpy as np
 import pytest
 import torch
@@ -39,6 +40,39 @@ def test_noalloc_get_matches_get_on_consecutive_calls(dim):
         assert t.sync() == mlkv.MLKV_OK
     get_both(a, b, second[::-1].copy(), dim)  # updated rows read back through both
     log(f"[noalloc] dim {dim}: size {a.size}")
+    a.close()
+    b.close()
+
+
+def test_noalloc_get_on_tiered_tables():
+    """Rows cached in HBM, at home in host memory, and evicted by a later
+    lookahead are read alike through both gets."""
+    dim, cap, cache = 32, 60_000, 3_000
+    rng = np.random.default_rng(11)
+    a = mlkv.Table(dim, cap, cache_rows=cache)
+    b = mlkv.Table(dim, cap, cache_rows=cache)
+    keys = rng.integers(0, 40_000, size=20_000).astype(np.uint64) * np.uint64(104729)
+    get_both(a, b, keys, dim)                      # inserts; rows at home
+    for t in (a, b):
+        t.lookahead(dev_keys(keys[:5_000]))        # part of the batch cached
+        assert t.sync() == mlkv.MLKV_OK
+    g = torch.from_numpy(rng.normal(0, 0.01, size=(keys.size, dim)).astype(np.float32)).cuda()
+    for t in (a, b):
+        t.put_grad(dev_keys(keys), g, 0.01, 1e-8)  # cached and home rows updated
+        assert t.sync() == mlkv.MLKV_OK
+    get_both(a, b, keys[::-1].copy(), dim)
+    for t in (a, b):
+        t.lookahead(dev_keys(keys[10_000:16_000]))  # evicts the first cached rows, writing them back
+        assert t.sync() == mlkv.MLKV_OK
+    get_both(a, b, keys[:12_000].copy(), dim)
+    # which rows stay at home when a lookahead asks for more than the free
+    # slots depends on the order the misses are listed in: the counters of the
+    # twins may differ, each table's must add up
+    for t in (a, b):
+        st = t.cache_stats()
+        log(f"[noalloc] tiered: {st}")
+        assert st["evicted"] > 0 and st["written_back"] > 0, "the second lookahead evicts dirty rows"
+        assert st["loaded"] == st["filled"] + st["evicted"] and st["filled"] == cache
     a.close()
     b.close()
 
