@@ -6,7 +6,8 @@
 //           kept for this call, an uncached one is claimed (once per row) as
 //           a miss;
 //   plan    one block walks the cache slots from a FIFO cursor and gives the
-//           misses the first slots this call does not keep;
+//           misses the first slots this call does not keep (row by row of
+//           contiguous slots, places counted by wave ballots and a scan);
 //   copy    a wave per four misses moves the directory entries (the slot's
 //           old row goes home, the missing row comes in; misses beyond the
 //           slots free to take stay at home), writes the evicted row back if
@@ -21,11 +22,11 @@
 namespace mlkv {
 
 constexpr uint32_t kClaimed = 0xFFFFFFFEu;  // slot_of_row of a miss claimed by the current call
-constexpr int kMarkThreads = 256;
+constexpr int kMarkThreads = 1024;  // one miss-counter addition per block, few blocks
 constexpr int kPlanThreads = 1024;
 constexpr int kCopyThreads = 256;
 constexpr int kCopyRows = 4;  // rows a wave copies at a time
-constexpr int kPlanPer = 16;  // cache slots a plan thread examines per pass
+constexpr int kPlanPer = 16;  // rows of kPlanThreads consecutive cache slots a plan pass examines
 
 __global__ __launch_bounds__(kMarkThreads) void k_tier_mark(Bucket* __restrict__ idx, uint32_t nb_log2,
                                                             const uint64_t* __restrict__ keys,
@@ -69,33 +70,49 @@ __global__ __launch_bounds__(kMarkThreads) void k_tier_mark(Bucket* __restrict__
 __global__ __launch_bounds__(kPlanThreads) void k_tier_plan(const uint32_t* __restrict__ keep, uint32_t tag,
                                                             uint32_t* __restrict__ plan_slot, uint64_t C, Ctrl* ctrl,
                                                             uint32_t parity) {
-  constexpr int NT = kPlanThreads;
-  __shared__ uint32_t s_w[NT / 64];
+  constexpr int NT = kPlanThreads, NW = NT / 64;
+  static_assert(kPlanPer * NW <= NT, "one scan entry per (row, wave)");
+  __shared__ uint32_t s_row[kPlanPer * NW];  // free slots per (row, wave), then the slots before them
+  __shared__ uint32_t s_w[NW];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
   const uint64_t M = ctrl->tier_nmiss[parity];
   const uint64_t cur = ctrl->tier_cursor;
-  // the first M slots from the cursor on that this call does not keep; a
-  // thread examines kPlanPer consecutive slots per pass
+  // the first M slots from the cursor on that this call does not keep. A pass
+  // examines kPlanPer rows of NT consecutive slots, thread t the t-th slot of
+  // each row, so that the loads of a row are contiguous; a slot's place among
+  // the free ones counts the free slots of earlier rows, of earlier waves in
+  // its row and of earlier lanes in its wave (a ballot)
   uint64_t found = 0;
   for (uint64_t i0 = 0; i0 < C && found < M; i0 += (uint64_t)NT * kPlanPer) {
-    const uint64_t b = i0 + (uint64_t)threadIdx.x * kPlanPer;
     // slot of position i from the cursor: cur + i < 2C, so one subtraction wraps it
     auto slot_at = [&](uint64_t i) { const uint64_t x = cur + i; return x >= C ? x - C : x; };
-    uint32_t cand = 0;  // bit j: slot_at(b + j) is free to take
+    uint32_t mine = 0;  // bit j: this thread's slot of row j is free to take
 #pragma unroll
     for (int j = 0; j < kPlanPer; ++j) {
-      const uint64_t i = b + j;
-      if (i < C && keep[slot_at(i)] != tag) cand |= 1u << j;
+      const uint64_t i = i0 + (uint64_t)j * NT + threadIdx.x;
+      if (i < C && keep[slot_at(i)] != tag) mine |= 1u << j;
     }
+    uint64_t bal[kPlanPer];
+#pragma unroll
+    for (int j = 0; j < kPlanPer; ++j) {
+      bal[j] = __ballot((mine >> j) & 1u);
+      if (lane == 0) s_row[j * NW + w] = (uint32_t)__popcll(bal[j]);
+    }
+    __syncthreads();
+    const uint32_t c = threadIdx.x < kPlanPer * NW ? s_row[threadIdx.x] : 0u;
     uint32_t tot;
-    const uint32_t pre = block_exclusive_scan<NT>((uint32_t)__popc(cand), s_w, &tot);
-    uint64_t v = found + pre;
-    for (int j = 0; j < kPlanPer && v < M; ++j) {
-      if ((cand >> j) & 1u) {
-        const uint64_t sl = slot_at(b + j);
-        plan_slot[v] = (uint32_t)sl;
-        ++v;
+    const uint32_t pre = block_exclusive_scan<NT>(c, s_w, &tot);  // its barriers: every count above is read
+    if (threadIdx.x < kPlanPer * NW) s_row[threadIdx.x] = pre;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kPlanPer; ++j) {
+      if ((mine >> j) & 1u) {
+        const uint64_t v = found + s_row[j * NW + w] + (uint64_t)__popcll(bal[j] & below);
+        if (v < M) plan_slot[v] = (uint32_t)slot_at(i0 + (uint64_t)j * NT + threadIdx.x);
       }
     }
+    __syncthreads();  // s_row is rewritten by the next pass
     found += tot;
   }
   const uint64_t A = found < M ? found : M;
@@ -204,9 +221,10 @@ hipError_t launch_tier_lookahead(const TierArgs& a, hipStream_t st, const Launch
                      (uint64_t)a.cache_rows, a.ctrl, a.parity);
   hook(K_TIER_PLAN, 1, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  // every miss (at most n) gets a lane group's turn
+  // every miss (at most n) gets a wave's turn; at most 256 blocks, which
+  // keep enough rows in flight for the host link and add the counters once each
   const int64_t per_block = (kCopyThreads / 64) * kCopyRows;
-  const int64_t cb = std::max<int64_t>(1, std::min<int64_t>((a.n + per_block - 1) / per_block, 2048));
+  const int64_t cb = std::max<int64_t>(1, std::min<int64_t>((a.n + per_block - 1) / per_block, 256));
   hook(K_TIER_COPY, 0, st);
   hipLaunchKernelGGL(k_tier_copy, dim3((unsigned)cb), dim3(kCopyThreads), 0, st, a.miss, a.plan_slot, a.slot_of_row,
                      a.row_of_slot, a.dirty, a.ctrl, a.parity, a.cache, a.host, a.D);
