@@ -136,7 +136,8 @@ mlkv_table *mlkv_open_tiered(int32_t dim, int64_t capacity, uint64_t seed, float
  * each missing row takes the next cache slot, in FIFO order from a cursor,
  * whose row this call does not ask for (that row is evicted, and written back
  * home first if a put changed it); when the call asks for more rows than the
- * cache can give it, the rest stay at home. It never blocks and changes no
+ * cache can give it, the rest stay at home (which ones may differ from run to
+ * run; no result depends on it). It never blocks and changes no
  * staleness count (a new key starts at 0). 0 <= n <= 2^31 - 1; errors as for
  * mlkv_get. */
 int mlkv_lookahead(mlkv_table *t, const uint64_t *d_keys, int64_t n, void *hip_stream);
