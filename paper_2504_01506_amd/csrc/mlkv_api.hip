@@ -69,6 +69,7 @@ struct mlkv_table {
   double* partials = nullptr;
   uint64_t* pc_key = nullptr;  // the last get's present keys and rows by position
   uint32_t* pc_row = nullptr;
+  bool pc_lookahead = false;   // they were last written by a lookahead (its gets usually follow)
   std::vector<ScratchSet> retired;  // replaced scratch, freed at sync / reserve / close
   int cus = 256;  // compute units of the device
 
@@ -498,10 +499,13 @@ int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uin
   a.blocked = d_blocked;
   a.pc_key = fixed ? nullptr : t->pc_key;
   a.pc_row = fixed ? nullptr : t->pc_row;
+  // after a lookahead, the positions of its keys skip the probe
+  a.pc_in = (!fixed && t->pc_lookahead) ? 1 : 0;
   a.cus = t->cus;
   const bool vec4 = (t->dim % 4 == 0) && (d_out == nullptr || aligned16(d_out));
   hipError_t e = launch_get(a, vec4, static_cast<hipStream_t>(hip_stream), fixed ? LaunchHook{} : hook_of(t));
   if (e != hipSuccess) return hip_fail(e, "mlkv_get launch");
+  if (!fixed) t->pc_lookahead = !count;  // a lookahead is the one get call that counts nothing
   t->epoch++;
   if (track) t->cepoch++;
   return MLKV_OK;

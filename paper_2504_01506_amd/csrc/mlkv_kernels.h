@@ -102,6 +102,9 @@ struct GetArgs {
   // nullptr: not recorded
   uint64_t* pc_key;
   uint32_t* pc_row;
+  // 1: a position whose key equals pc_key[i] takes pc_row[i] without probing
+  // (a present key's row never changes, so any recorded pair stays true)
+  int pc_in;
   int cus;  // compute units of the device
 };
 

@@ -114,7 +114,7 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
     float* __restrict__ out, const RowStore store, int D, uint64_t seed,
     NewKey* __restrict__ newlist, uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch,
     unsigned long long* __restrict__ clock, uint64_t cepoch, uint32_t bound, uint8_t* __restrict__ blocked,
-    uint64_t* __restrict__ pc_key, uint32_t* __restrict__ pc_row, int tlen) {
+    uint64_t* __restrict__ pc_key, uint32_t* __restrict__ pc_row, int pc_in, int tlen) {
   __shared__ uint32_t s_cnt;
   __shared__ uint64_t s_nkey[kGetTile];  // the tile's new keys and their slots
   __shared__ uint32_t s_nslot[kGetTile];
@@ -130,11 +130,17 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
   __syncthreads();
   uint64_t key = 0;
   Probe pr = {0, kPendingRow, P_NONE};
+  bool recorded = false;  // the key and its row came from the row cache
   if (i < end) {
     key = keys[i];
+    const uint64_t ck = pc_in ? pc_key[i] : kEmptyKey;
+    const uint32_t cr = pc_in ? pc_row[i] : kPendingRow;
     if (key == kEmptyKey) {
       pr.status = P_BAD;
       ctrl->bad_epoch = epoch;
+    } else if (ck == key) {
+      pr = {0u, cr, P_HIT};
+      recorded = true;
     } else {
       pr = probe_key(idx, nb_log2, key, true);
       if (pr.status == P_OVERFLOW) ctrl->overflow_epoch = epoch;
@@ -148,7 +154,7 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
   }
   // a key present before the call, with its row, for a put of the same
   // batch: a key's row never changes once assigned, so the pair stays valid
-  if (i < end && pc_key != nullptr) {
+  if (i < end && pc_key != nullptr && !recorded) {
     pc_key[i] = pr.status == P_HIT ? key : kEmptyKey;
     pc_row[i] = pr.row;
   }
@@ -2700,7 +2706,7 @@ static hipError_t launch_get_t(const GetArgs& a, hipStream_t st, const LaunchHoo
   auto kern = a.clock != nullptr ? k_get_probe_gather<M, true> : k_get_probe_gather<M, false>;
   hipLaunchKernelGGL(kern, dim3((unsigned)ntiles), dim3(kGetTile), 0, st, a.idx, a.nb_log2, a.keys, a.n,
                      a.out, a.store, a.D, a.seed, a.newlist, a.tile_cnt, a.ctrl, a.epoch, a.clock, a.cepoch,
-                     a.bound, a.blocked, a.pc_key, a.pc_row, tlen);
+                     a.bound, a.blocked, a.pc_key, a.pc_row, a.pc_in, tlen);
   hook(K_GET_PROBE_GATHER, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

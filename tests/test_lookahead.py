@@ -44,6 +44,45 @@ def test_lookahead_then_steps(bound, m, dim):
     pr.close()
 
 
+@pytest.mark.parametrize("kind", ["plain", "bounded", "tiered"])
+def test_get_after_lookahead_takes_recorded_rows(kind):
+    # a get right after a lookahead takes, at each position holding the key
+    # the lookahead found present there, the row it recorded, and probes the
+    # others: same keys at the same positions, other present keys, new keys,
+    # keys moved to other positions, a batch longer than the lookahead's
+    dim, m = 16, 40_000
+    rng = np.random.default_rng({"plain": 1, "bounded": 2, "tiered": 3}[kind])
+    pr = Pair(dim, 4 * m, staleness_bound=0 if kind == "bounded" else None,
+              cache_rows=m // 2 if kind == "tiered" else None)
+    keys = rng.choice(np.uint64(1) << np.uint64(40), size=2 * m, replace=False).astype(np.uint64)
+    present = keys[:m]
+
+    def get(k):
+        if kind == "bounded":
+            pr.get_bounded(k)
+        else:
+            pr.get(k)
+        grads = rng.normal(0, 0.01, size=(k.size, dim)).astype(np.float32)
+        pr.put(k, grads, 0.01, 1e-8)   # completes the get (bounded) and updates the rows
+
+    get(present)                                   # all new
+    a = present[rng.integers(0, m, size=30_000)]
+    pr.lookahead(a)                                # every key present: rows recorded by position
+    b = a.copy()
+    b[5_000:10_000] = present[rng.integers(0, m, size=5_000)]      # other present keys
+    b[10_000:12_000] = keys[m:m + 2_000]                            # new keys
+    rng.shuffle(b[20_000:25_000])                                   # same keys, other positions
+    get(b)
+    pr.lookahead(b[:7_000])
+    get(np.concatenate([b[:7_000], keys[m + 2_000:m + 3_000]]))     # longer batch than the lookahead
+    pr.compare_rows()
+    pr.check_index()
+    if kind == "bounded":
+        pr.compare_staleness()
+    log(f"[lookahead] get after lookahead ({kind}): size {pr.ora.size} stats={pr.stats}")
+    pr.close()
+
+
 def test_failed_lookahead_leaves_the_table_unchanged():
     pr = Pair(4, 100, staleness_bound=1)
     pr.get_bounded(np.arange(1, 51, dtype=np.uint64))
