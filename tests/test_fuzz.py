@@ -1,7 +1,7 @@
 """Random call sequences on the GPU and the CPU oracle side by side.
 
-Each sequence draws a row width, a capacity, optionally a staleness bound,
-and 30 calls, each one of: get (with or without an output), lookahead, put_grad,
+Each sequence draws a row width, a capacity, optionally a staleness bound
+or (tiered tables) an HBM cache of 2-20 % of the rows, and 30 calls, each one of: get (with or without an output), lookahead, put_grad,
 put_grad_sgd, put (upsert), a get whose new keys overflow the capacity, or a
 call holding the reserved key. Batch lengths cover the tile boundaries
 (1, 63..65, 255..257, 1023..1025) and random lengths; keys mix present keys,
@@ -45,19 +45,21 @@ def _ora_get(pr, keys):
     return pr.ora.get_bounded(keys)[0]
 
 
-@pytest.mark.parametrize("seed", range(24))
-def test_random_call_sequences(seed):
-    rng = np.random.default_rng(5000 + seed)
+def _sequence(seed, tiered):
+    rng = np.random.default_rng(5000 + seed + (1000 if tiered else 0))
     dim = int(rng.choice([1, 2, 4, 5, 8, 16, 31, 64, 128]))
     cap = int(rng.integers(3000, 40000))
-    bound = int(rng.integers(0, 3)) if seed % 3 == 2 else None
-    pr = Pair(dim, cap, staleness_bound=bound)
+    bound = int(rng.integers(0, 3)) if seed % 3 == 2 and not tiered else None
+    cache = max(1, int(cap * rng.uniform(0.02, 0.2))) if tiered else None
+    pr = Pair(dim, cap, staleness_bound=bound, cache_rows=cache)
     space = int(rng.choice([cap // 8, cap // 2, 4 * cap]))  # many repeats .. mostly new keys
     counts = {}
     for step in range(30):
         op = str(rng.choice(["get", "get", "get_null", "lookahead", "put_grad", "put_grad", "put_sgd", "put",
                              "over", "bad"]))
         n = int(rng.choice(LENGTHS)) if rng.random() < 0.6 else int(rng.integers(1, 20000))
+        if tiered and op == "lookahead":  # large enough to fill the cache and evict
+            n = int(rng.integers(max(1, cache // 2), min(20000, 3 * cache) + 1))
         size = pr.ora.size
         if op == "over":
             # more new keys than the table has room for (ids beyond the space)
@@ -111,6 +113,20 @@ def test_random_call_sequences(seed):
     pr.check_index()
     if bound is not None:
         pr.compare_staleness()
-    log(f"[fuzz] seed {seed}: dim {dim} cap {cap} bound {bound} space {space} size {pr.ora.size} "
-        f"calls {counts} stats={pr.stats}")
+    cs = pr.gpu.cache_stats() if tiered else None
+    if tiered:
+        assert cs["loaded"] == cs["filled"] + cs["evicted"] and cs["filled"] <= cache
+        assert cs["loaded"] > 0 or counts.get("lookahead", 0) == 0, "lookaheads bring rows into the cache"
+    log(f"[fuzz] seed {seed}: dim {dim} cap {cap} bound {bound} cache {cache} space {space} size {pr.ora.size} "
+        f"calls {counts} stats={pr.stats} cache_stats={cs}")
     pr.close()
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_call_sequences(seed):
+    _sequence(seed, tiered=False)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_call_sequences_on_tiered_tables(seed):
+    _sequence(seed, tiered=True)
