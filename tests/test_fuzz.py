@@ -1,7 +1,8 @@
 """Random call sequences on the GPU and the CPU oracle side by side.
 
 Each sequence draws a row width, a capacity, optionally a staleness bound
-or (tiered tables) an HBM cache of 2-20 % of the rows, and 30 calls, each one of: get (with or without an output), lookahead, put_grad,
+or (tiered tables) an HBM cache of 2-20 % of the rows, the dedup of its puts
+(hash partition, or radix sort), and 30 calls, each one of: get (with or without an output), lookahead, put_grad,
 put_grad_sgd, put (upsert), a get whose new keys overflow the capacity, or a
 call holding the reserved key. Batch lengths cover the tile boundaries
 (1, 63..65, 255..257, 1023..1025) and random lengths; keys mix present keys,
@@ -45,13 +46,13 @@ def _ora_get(pr, keys):
     return pr.ora.get_bounded(keys)[0]
 
 
-def _sequence(seed, tiered):
-    rng = np.random.default_rng(5000 + seed + (1000 if tiered else 0))
+def _sequence(seed, tiered, dedup="hash"):
+    rng = np.random.default_rng(5000 + seed + (1000 if tiered else 0) + (2000 if dedup != "hash" else 0))
     dim = int(rng.choice([1, 2, 4, 5, 8, 16, 31, 64, 128]))
     cap = int(rng.integers(3000, 40000))
     bound = int(rng.integers(0, 3)) if seed % 3 == 2 and not tiered else None
     cache = max(1, int(cap * rng.uniform(0.02, 0.2))) if tiered else None
-    pr = Pair(dim, cap, staleness_bound=bound, cache_rows=cache)
+    pr = Pair(dim, cap, staleness_bound=bound, cache_rows=cache, dedup=dedup)
     space = int(rng.choice([cap // 8, cap // 2, 4 * cap]))  # many repeats .. mostly new keys
     counts = {}
     for step in range(30):
@@ -117,7 +118,7 @@ def _sequence(seed, tiered):
     if tiered:
         assert cs["loaded"] == cs["filled"] + cs["evicted"] and cs["filled"] <= cache
         assert cs["loaded"] > 0 or counts.get("lookahead", 0) == 0, "lookaheads bring rows into the cache"
-    log(f"[fuzz] seed {seed}: dim {dim} cap {cap} bound {bound} cache {cache} space {space} size {pr.ora.size} "
+    log(f"[fuzz] seed {seed}: dim {dim} cap {cap} bound {bound} cache {cache} dedup {dedup} space {space} size {pr.ora.size} "
         f"calls {counts} stats={pr.stats} cache_stats={cs}")
     pr.close()
 
@@ -130,3 +131,8 @@ def test_random_call_sequences(seed):
 @pytest.mark.parametrize("seed", range(8))
 def test_random_call_sequences_on_tiered_tables(seed):
     _sequence(seed, tiered=True)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_call_sequences_with_radix_dedup(seed):
+    _sequence(seed, tiered=seed % 2 == 1, dedup="radix")
