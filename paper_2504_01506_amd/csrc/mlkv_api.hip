@@ -499,8 +499,9 @@ int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uin
   a.blocked = d_blocked;
   a.pc_key = fixed ? nullptr : t->pc_key;
   a.pc_row = fixed ? nullptr : t->pc_row;
-  // after a lookahead, the positions of its keys skip the probe
-  a.pc_in = (!fixed && t->pc_lookahead) ? 1 : 0;
+  // after a lookahead, the positions of its keys skip the probe (tables
+  // without a staleness bound)
+  a.pc_in = (!fixed && t->pc_lookahead && a.clock == nullptr) ? 1 : 0;
   a.cus = t->cus;
   const bool vec4 = (t->dim % 4 == 0) && (d_out == nullptr || aligned16(d_out));
   hipError_t e = launch_get(a, vec4, static_cast<hipStream_t>(hip_stream), fixed ? LaunchHook{} : hook_of(t));

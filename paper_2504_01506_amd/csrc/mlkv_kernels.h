@@ -103,7 +103,8 @@ struct GetArgs {
   uint64_t* pc_key;
   uint32_t* pc_row;
   // 1: a position whose key equals pc_key[i] takes pc_row[i] without probing
-  // (a present key's row never changes, so any recorded pair stays true)
+  // (a present key's row never changes, so any recorded pair stays true);
+  // not with a staleness clock
   int pc_in;
   int cus;  // compute units of the device
 };

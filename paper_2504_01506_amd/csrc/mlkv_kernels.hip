@@ -108,13 +108,15 @@ __device__ __forceinline__ void wave_emit_rows(float* __restrict__ out, const Ro
   }
 }
 
-template <class M, bool kTrack>
+// kPcIn: a position whose key equals pc_key[i] takes pc_row[i] without
+// probing (an instance of its own, so that other gets run unchanged)
+template <class M, bool kTrack, bool kPcIn>
 __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
     Bucket* __restrict__ idx, uint32_t nb_log2, const uint64_t* __restrict__ keys, int64_t n,
     float* __restrict__ out, const RowStore store, int D, uint64_t seed,
     NewKey* __restrict__ newlist, uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch,
     unsigned long long* __restrict__ clock, uint64_t cepoch, uint32_t bound, uint8_t* __restrict__ blocked,
-    uint64_t* __restrict__ pc_key, uint32_t* __restrict__ pc_row, int pc_in, int tlen) {
+    uint64_t* __restrict__ pc_key, uint32_t* __restrict__ pc_row, int tlen) {
   __shared__ uint32_t s_cnt;
   __shared__ uint64_t s_nkey[kGetTile];  // the tile's new keys and their slots
   __shared__ uint32_t s_nslot[kGetTile];
@@ -133,17 +135,22 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
   bool recorded = false;  // the key and its row came from the row cache
   if (i < end) {
     key = keys[i];
-    const uint64_t ck = pc_in ? pc_key[i] : kEmptyKey;
-    const uint32_t cr = pc_in ? pc_row[i] : kPendingRow;
     if (key == kEmptyKey) {
       pr.status = P_BAD;
       ctrl->bad_epoch = epoch;
-    } else if (ck == key) {
-      pr = {0u, cr, P_HIT};
-      recorded = true;
     } else {
-      pr = probe_key(idx, nb_log2, key, true);
-      if (pr.status == P_OVERFLOW) ctrl->overflow_epoch = epoch;
+      if constexpr (kPcIn) {
+        const uint64_t ck = pc_key[i];
+        const uint32_t cr = pc_row[i];
+        if (ck == key) {
+          pr = {0u, cr, P_HIT};
+          recorded = true;
+        }
+      }
+      if (!recorded) {
+        pr = probe_key(idx, nb_log2, key, true);
+        if (pr.status == P_OVERFLOW) ctrl->overflow_epoch = epoch;
+      }
     }
   }
   if (pr.status == P_NEW_MINE) {
@@ -2703,10 +2710,11 @@ static hipError_t launch_get_t(const GetArgs& a, hipStream_t st, const LaunchHoo
   const int tlen = get_tile_len(a.n, a.cus);
   const int64_t ntiles = (a.n + tlen - 1) / tlen;
   hook(K_GET_PROBE_GATHER, 0, st);
-  auto kern = a.clock != nullptr ? k_get_probe_gather<M, true> : k_get_probe_gather<M, false>;
+  auto kern = a.clock != nullptr ? k_get_probe_gather<M, true, false>
+                                  : a.pc_in ? k_get_probe_gather<M, false, true> : k_get_probe_gather<M, false, false>;
   hipLaunchKernelGGL(kern, dim3((unsigned)ntiles), dim3(kGetTile), 0, st, a.idx, a.nb_log2, a.keys, a.n,
                      a.out, a.store, a.D, a.seed, a.newlist, a.tile_cnt, a.ctrl, a.epoch, a.clock, a.cepoch,
-                     a.bound, a.blocked, a.pc_key, a.pc_row, a.pc_in, tlen);
+                     a.bound, a.blocked, a.pc_key, a.pc_row, tlen);
   hook(K_GET_PROBE_GATHER, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
