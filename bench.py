@@ -147,6 +147,8 @@ def parity_and_cpu_baseline(wl, args, kv, bounded, log):
     if pre.size:
         assert ora.prefill_sorted(pre) == O.OK
     P = 0 if args.no_parity else args.parity_steps
+    if P and args.pipelined:
+        P = max(P, 2)  # the first put comes with the second get
     rec = None
     if P:
         cache = max(1, int(wl.capacity * args.cache_frac)) if args.cache_frac else None
@@ -165,7 +167,11 @@ def parity_and_cpu_baseline(wl, args, kv, bounded, log):
         updated = np.zeros(wl.capacity, dtype=bool)
         rec = {"steps": P, "max_row_scaled_err": 0.0, "max_ulp": 0, "get_rows_compared": 0,
                "unupdated_rows_bit_exact": True}
+    # with --pipelined, step s is the get of batch s then the put of batch s - 1
+    # (on the GPU one mlkv_get_put_grad call), as in the timed steps
+    ov = args.pipelined
     cpu_s, steps = 0.0, 0
+    prev = None  # the previous step's put keys and gradients (pipelined steps)
     while steps < P or cpu_s < args.cpu_seconds:
         keys = wl.keys(steps)
         kg = keys[:h] if kv else keys
@@ -176,7 +182,10 @@ def parity_and_cpu_baseline(wl, args, kv, bounded, log):
             rc, want, _ = ora.get_bounded(kg)
         else:
             rc, want = ora.get(kg)
-        rc2 = ora.put(kp, src) if kv else ora.put_grad(kp, src, wl.lr, wl.eps)
+        if not ov:
+            rc2 = ora.put(kp, src) if kv else ora.put_grad(kp, src, wl.lr, wl.eps)
+        else:
+            rc2 = ora.put_grad(prev[0], prev[1], wl.lr, wl.eps) if prev is not None else O.OK
         cpu_s += time.perf_counter() - t0
         assert rc == O.OK and rc2 == O.OK
         if steps < P:
@@ -184,15 +193,18 @@ def parity_and_cpu_baseline(wl, args, kv, bounded, log):
             if args.cache_frac:
                 gpu.lookahead(k_d)
             out = torch.empty((kg.size, D), device="cuda")
-            if bounded:
+            kp_d = torch.from_numpy(kp.view(np.int64)).cuda()
+            src_d = torch.from_numpy(src).cuda()
+            if ov and prev is not None:
+                gpu.get_put_grad(k_d, out, prev[2], prev[3], wl.lr, wl.eps,
+                                 blocked=blocked[:kg.size] if bounded else None)
+            elif bounded:
                 gpu.get_bounded(k_d, out, blocked[:kg.size])
             else:
                 gpu.get(k_d, out)
-            kp_d = torch.from_numpy(kp.view(np.int64)).cuda()
-            src_d = torch.from_numpy(src).cuda()
             if kv:
                 gpu.put(kp_d, src_d)
-            else:
+            elif not ov:
                 gpu.put_grad(kp_d, src_d, wl.lr, wl.eps)
             assert gpu.sync() == mlkv.MLKV_OK
             got = out.cpu().numpy()
@@ -205,6 +217,8 @@ def parity_and_cpu_baseline(wl, args, kv, bounded, log):
                                                 float(row_scaled_err(got[~fresh], want[~fresh]).max()))
                 rec["max_ulp"] = max(rec["max_ulp"], max_ulp(got[~fresh], want[~fresh]))
             rec["get_rows_compared"] += int(kg.size)
+            if ov:  # this step's put is the previous batch's
+                kp, kp_d = (prev[0], prev[2]) if prev is not None else (kp[:0], kp_d[:0])
             rows_p = ora.lookup_rows(kp)
             updated[rows_p] = True
             if steps == P - 1:  # the last batch: key -> row, rows and accumulators
@@ -223,6 +237,9 @@ def parity_and_cpu_baseline(wl, args, kv, bounded, log):
                 rec["within_1e-5"] = bool(rec["max_row_scaled_err"] <= 1e-5 and rec["max_state_rel_err"] <= 1e-5)
                 gpu.close()
                 log(f"parity over {P} steps: {rec}")
+        if ov:
+            prev = (keys, src) + ((torch.from_numpy(keys.view(np.int64)).cuda(), torch.from_numpy(src).cuda())
+                                  if steps < P - 1 else (None, None))
         steps += 1
     ora.close()
     unit = "ops/s" if kv else "keys/s"
@@ -267,6 +284,9 @@ def main():
     ap.add_argument("--dedup", choices=("hash", "radix"), default="hash",
                     help="how puts find equal keys: hash partition + LDS grouping, or radix sort + run-length "
                          "encoding (same results)")
+    ap.add_argument("--pipelined", action="store_true",
+                    help="each step is one mlkv_get_put_grad call: the get of batch s, then the put_grad of "
+                         "batch s - 1 (asynchronous training; with a staleness bound, from bound 1)")
     ap.add_argument("--copy-mib", type=int, default=1024,
                     help="size of the plain device copy timed as the achievable ceiling (and used to "
                          "calibrate rocprofv3 counters)")
@@ -280,6 +300,10 @@ def main():
                                         or not 0.0 < args.cache_frac <= 1.0):
         print("--cache-frac (0 < f <= 1) applies to the training-step workloads without a staleness bound",
               file=sys.stderr)
+        sys.exit(2)
+    if args.pipelined and (args.config.startswith("kv-") or args.staleness_bound == 0):
+        print("--pipelined applies to the training-step workloads, without a staleness bound or with a bound of "
+              "at least 1 (at bound 0 the get blocks every key the pending put updates)", file=sys.stderr)
         sys.exit(2)
     if args.staleness_bound is not None and args.config.startswith("kv-"):
         print("--staleness-bound applies to the training-step workloads (get then put_grad of the same keys)",
@@ -365,11 +389,18 @@ def main():
         else:
             t.put_grad(keys_d[s], grads_d[s], wl.lr, wl.eps)
 
+    ov = args.pipelined
+
     def step(s):
         if tiered:
             t.lookahead(keys_d[s])
+        if ov and s > 0:  # the get of batch s, then the put of batch s - 1
+            t.get_put_grad(keys_d[s], out, keys_d[s - 1], grads_d[s - 1], wl.lr, wl.eps,
+                           blocked=blocked if bounded else None)
+            return
         get(s)
-        put(s)
+        if not ov:
+            put(s)
 
     Ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     # warm-up; the first step after the prefill is timed on its own (the cold
@@ -422,17 +453,22 @@ def main():
     ev_g = [(Ev(), Ev(), Ev()) for _ in timed]
     for (ea, eb, ec), s in zip(ev_g, timed):
         ea.record()
-        get(s)
+        if ov:  # one call per step: the get and the put are not apart
+            step(s)
+        else:
+            get(s)
         eb.record()
-        put(s)
+        if not ov:
+            put(s)
         ec.record()
     torch.cuda.synchronize()
     assert t.sync() == mlkv.MLKV_OK
-    t_get = float(np.median([ea.elapsed_time(eb) for ea, eb, _ in ev_g]))
-    t_put = float(np.median([eb.elapsed_time(ec) for _, eb, ec in ev_g]))
+    t_get = None if ov else float(np.median([ea.elapsed_time(eb) for ea, eb, _ in ev_g]))
+    t_put = None if ov else float(np.median([eb.elapsed_time(ec) for _, eb, ec in ev_g]))
     per_step = [ea.elapsed_time(ec) for ea, _, ec in ev_g]
     n_get, n_put = (h, n - h) if kv else (n, n)
-    log(f"get {t_get * 1e3:.2f} us, put {t_put * 1e3:.2f} us (medians)")
+    if not ov:
+        log(f"get {t_get * 1e3:.2f} us, put {t_put * 1e3:.2f} us (medians)")
 
     # ---- once more with events around every launch: per-kernel durations
     tier0 = t.cache_stats() if tiered else None
@@ -490,7 +526,8 @@ def main():
               key=lambda k: kinfo[k]["avg_us"] * kinfo[k]["launches"])
     digest = source_digest()
     # the committed counters were taken on the full-size DLRM-shaped workload
-    same_workload = args.config == "dlrm" and args.scale == 1.0 and not bounded and not tiered and args.dedup == "hash"
+    same_workload = (args.config == "dlrm" and args.scale == 1.0 and not bounded and not tiered
+                     and args.dedup == "hash" and not ov)
     traffic = load_traffic(dom, digest) if same_workload else None
     # the kernel's rocprofv3 duration, for comparison with the event-timed one
     # (an event pair around every launch adds about 2 us to each)
@@ -578,12 +615,13 @@ def main():
             **({"staleness_bound": args.staleness_bound} if bounded else {}),
             **({"tiered_cache_rows": cache_rows, "step": "lookahead + get + put_grad"} if tiered else {}),
             **({"dedup": "radix sort + run-length encoding"} if args.dedup == "radix" else {}),
+            **({"step": "get(batch s) then put_grad(batch s - 1), one mlkv_get_put_grad call"} if ov else {}),
         },
         "gbps_effective": round(gbps, 1),
         "pct_of_peak_hbm": round(100.0 * gbps / PEAK_HBM_GBPS, 2),
         "alg_bytes_per_step": int(alg_bytes / args.steps),
-        "get_keys_per_s": n_get / (t_get * 1e-3),
-        "put_keys_per_s": n_put / (t_put * 1e-3),
+        "get_keys_per_s": None if ov else n_get / (t_get * 1e-3),
+        "put_keys_per_s": None if ov else n_put / (t_put * 1e-3),
         "ms_get_median": t_get,
         "ms_put_median": t_put,
         "ms_per_step_with_kernel_events": ms_prof,

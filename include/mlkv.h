@@ -170,6 +170,35 @@ int mlkv_put_grad(mlkv_table *t, const uint64_t *d_keys, const float *d_grads, i
 int mlkv_put_grad_sgd(mlkv_table *t, const uint64_t *d_keys, const float *d_grads, int64_t n, float lr,
                       void *hip_stream);
 
+/* The Get of the next batch and the Rmw of the current one in the order of
+ * asynchronous training (Sec. II: an embedding read at step t + 1 may predate
+ * the update of step t, staleness s = t - k(t)), which a bounded table keeps
+ * within its bound (Sec. III-C1). Same results (output rows, blocked flags,
+ * key -> row, rows, accumulators, staleness counts, size, errors) as
+ *     mlkv_get_bounded(t, d_get_keys, n_get, d_out, d_blocked, s)  (mlkv_get
+ *                                                  on a table without a bound)
+ *     mlkv_put_grad(t, d_put_keys, d_grads, n_put, lr, eps, s)
+ * issued in that order, with one condition: every key of the put must be in
+ * the table before this call (in a training loop the previous get inserted
+ * it). A put key that is not, including one that this call's get inserts,
+ * makes the put part a no-op and is reported by the next mlkv_sync as
+ * MLKV_EINVAL; the get part is applied as if alone. Each part's other
+ * device-side errors make that part alone a no-op (the first is reported).
+ * The put's probe kernel runs first and takes the rows the last get recorded
+ * by position, then the get's kernels, then the put's row updates, all on
+ * hip_stream. get_done_event (a hipEvent_t, or NULL) is recorded on
+ * hip_stream once the get's rows are in d_out, before the row updates: work
+ * on another stream that waits for it (the model's step on the new batch)
+ * runs beside the updates. At s = 0 every key of the get that the put
+ * updates is blocked (its count is still 1); from s = 1 on, and on tables
+ * without a bound, none is. Arguments as for the two calls; d_blocked may be
+ * NULL on a table without a bound; d_out must not overlap d_get_keys,
+ * d_put_keys or d_grads. n_get = 0 or n_put = 0 makes it the other call
+ * alone (the event is then recorded after the get, or before the put). */
+int mlkv_get_put_grad(mlkv_table *t, const uint64_t *d_get_keys, int64_t n_get, float *d_out, uint8_t *d_blocked,
+                      const uint64_t *d_put_keys, const float *d_grads, int64_t n_put, float lr, float eps,
+                      void *get_done_event, void *hip_stream);
+
 /* Put (Sec. III-A), an upsert of a batch: for every distinct key of the batch
  * its row becomes d_values[i*dim ... i*dim + dim - 1] for the LAST position i
  * holding the key. Missing keys are inserted as in mlkv_get (rows in ascending

@@ -5,6 +5,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
+#include <utility>
 #include <string>
 #include <vector>
 
@@ -70,6 +71,10 @@ struct mlkv_table {
   uint64_t* pc_key = nullptr;  // the last get's present keys and rows by position
   uint32_t* pc_row = nullptr;
   bool pc_lookahead = false;   // they were last written by a lookahead (its gets usually follow)
+  // key-range lists of a get that runs between a put's probe and its reduce
+  // (mlkv_get_put_grad), apart from the put's items and metadata
+  uint64_t* mid_xkey = nullptr;
+  uint32_t* mid_xslot = nullptr;
   std::vector<ScratchSet> retired;  // replaced scratch, freed at sync / reserve / close
   int cus = 256;  // compute units of the device
 
@@ -113,7 +118,7 @@ void free_scratch_set(const ScratchSet& s) {
 ScratchSet current_set(mlkv_table* t) {
   ScratchSet s;
   s.ptrs = {t->newlist, t->tile_cnt, t->items, t->meta, t->spill, t->partials, t->pc_key, t->pc_row,
-            t->rs_cnt, t->miss, t->plan_slot};
+            t->rs_cnt, t->miss, t->plan_slot, t->mid_xkey, t->mid_xslot};
   return s;
 }
 
@@ -122,6 +127,8 @@ void clear_workspace_ptrs(mlkv_table* t) {
   t->plan_slot = nullptr;
   t->pc_key = nullptr;
   t->pc_row = nullptr;
+  t->mid_xkey = nullptr;
+  t->mid_xslot = nullptr;
   t->partials = nullptr;
   t->newlist = nullptr;
   t->tile_cnt = nullptr;
@@ -209,6 +216,8 @@ int ensure_workspace(mlkv_table* t, int64_t n, hipStream_t st) {
       (e = dev_alloc(&t->partials, sizeof(double) * (size_t)want * (size_t)t->dim)) != hipSuccess ||
       (e = dev_alloc(&t->pc_key, sizeof(uint64_t) * (size_t)slots)) != hipSuccess ||
       (e = dev_alloc(&t->pc_row, sizeof(uint32_t) * (size_t)slots)) != hipSuccess ||
+      (e = dev_alloc(&t->mid_xkey, sizeof(uint64_t) * (size_t)slots)) != hipSuccess ||
+      (e = dev_alloc(&t->mid_xslot, sizeof(uint32_t) * (size_t)slots)) != hipSuccess ||
       (e = hipMemsetAsync(t->pc_key, 0xFF, sizeof(uint64_t) * (size_t)slots, st)) != hipSuccess) {  // no key cached
     free_workspace(t);
     return hip_fail(e, "scratch allocation");
@@ -457,14 +466,8 @@ struct GetScratch {
   uint32_t* xslot;
 };
 
-// The get pipeline (probe + gather, then rows for new keys); d_blocked is
-// written when the table has a staleness bound and the call counts (a
-// lookahead does not). With `fixed`, the call uses that scratch, allocates
-// nothing and records no launch timings.
-int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uint8_t* d_blocked,
-             bool count, void* hip_stream, const GetScratch* fixed = nullptr) {
-  int rc = check_table(t);
-  if (rc) return rc;
+// Host-side checks of a get call's arguments (nothing is queued).
+int check_get(mlkv_table* t, const uint64_t* d_keys, int64_t n, uint8_t* d_blocked, bool count) {
   if (n < 0 || n > 0x7FFFFFFFll) return fail(MLKV_EINVAL, "n must be in [0, 2^31 - 1]");
   if (n == 0) return MLKV_OK;
   if (d_keys == nullptr) return fail(MLKV_EINVAL, "keys is NULL");
@@ -472,8 +475,15 @@ int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uin
   if (track && d_blocked == nullptr) return fail(MLKV_EINVAL, "blocked is NULL");
   if (track && t->cepoch >= (1ull << (64 - kClockBits)))
     return fail(MLKV_EINVAL, "the table has served 2^40 get calls, the most a bounded table counts");
-  if (fixed == nullptr && (rc = ensure_workspace(t, n, static_cast<hipStream_t>(hip_stream))) != MLKV_OK)
-    return rc;
+  return MLKV_OK;
+}
+
+// The launch arguments of a get of n > 0 keys with the table's epoch; the
+// row records and key-range lists are the table's (the put's items and
+// metadata, idle during a get), or `fixed`'s.
+GetArgs get_args(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uint8_t* d_blocked, bool count,
+                 const GetScratch* fixed) {
+  const bool track = count && t->clock != nullptr;
   GetArgs a;
   a.idx = t->idx;
   a.nb_log2 = t->nb_log2;
@@ -489,8 +499,6 @@ int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uin
   a.tile_cnt = fixed ? fixed->tile_cnt : t->tile_cnt;
   a.ctrl = t->ctrl;
   a.epoch = t->epoch;
-  // key-range overflow lists: the put pipeline's scratch (at least n entries
-  // each), idle during a get
   a.xkey = fixed ? fixed->xkey : t->items;
   a.xslot = fixed ? fixed->xslot : t->meta;
   a.clock = track ? t->clock : nullptr;
@@ -503,12 +511,36 @@ int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uin
   // without a staleness bound)
   a.pc_in = (!fixed && t->pc_lookahead && a.clock == nullptr) ? 1 : 0;
   a.cus = t->cus;
-  const bool vec4 = (t->dim % 4 == 0) && (d_out == nullptr || aligned16(d_out));
-  hipError_t e = launch_get(a, vec4, static_cast<hipStream_t>(hip_stream), fixed ? LaunchHook{} : hook_of(t));
-  if (e != hipSuccess) return hip_fail(e, "mlkv_get launch");
+  return a;
+}
+
+bool get_vec4(const mlkv_table* t, const float* d_out) {
+  return (t->dim % 4 == 0) && (d_out == nullptr || aligned16(d_out));
+}
+
+// The table's state after a get call was queued.
+void get_done(mlkv_table* t, bool count, bool fixed) {
   if (!fixed) t->pc_lookahead = !count;  // a lookahead is the one get call that counts nothing
   t->epoch++;
-  if (track) t->cepoch++;
+  if (count && t->clock != nullptr) t->cepoch++;
+}
+
+// The get pipeline (probe + gather, then rows for new keys); d_blocked is
+// written when the table has a staleness bound and the call counts (a
+// lookahead does not). With `fixed`, the call uses that scratch, allocates
+// nothing and records no launch timings.
+int get_call(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out, uint8_t* d_blocked,
+             bool count, void* hip_stream, const GetScratch* fixed = nullptr) {
+  int rc = check_table(t);
+  if (rc) return rc;
+  if ((rc = check_get(t, d_keys, n, d_blocked, count)) != MLKV_OK || n == 0) return rc;
+  if (fixed == nullptr && (rc = ensure_workspace(t, n, static_cast<hipStream_t>(hip_stream))) != MLKV_OK)
+    return rc;
+  const GetArgs a = get_args(t, d_keys, n, d_out, d_blocked, count, fixed);
+  hipError_t e = launch_get(a, get_vec4(t, d_out), static_cast<hipStream_t>(hip_stream),
+                            fixed ? LaunchHook{} : hook_of(t));
+  if (e != hipSuccess) return hip_fail(e, "mlkv_get launch");
+  get_done(t, count, fixed != nullptr);
   return MLKV_OK;
 }
 
@@ -645,12 +677,8 @@ int mlkv_read_staleness(mlkv_table* t, const int64_t* d_rows, int64_t n, uint32_
 
 namespace {
 
-// The put pipeline (probe, group, apply) with update `op` for every distinct
-// key; `src` holds n rows of gradients (or values for kOpAssign).
-int put_call(mlkv_table* t, const uint64_t* d_keys, const float* src, int64_t n, int op, float lr, float eps,
-             void* hip_stream) {
-  int rc = check_table(t);
-  if (rc) return rc;
+// Host-side checks of a put call's arguments (nothing is queued).
+int check_put(mlkv_table* t, const uint64_t* d_keys, const float* src, int64_t n, int op, float lr, float eps) {
   if (n < 0 || n > 0x3FFFFFFFll) return fail(MLKV_EINVAL, "n must be in [0, 2^30 - 1]");
   if (op != kOpAssign && !std::isfinite(lr)) return fail(MLKV_EINVAL, "lr must be finite");
   if (op == kOpAdagrad && (!std::isfinite(eps) || eps < 0.0f))
@@ -658,7 +686,11 @@ int put_call(mlkv_table* t, const uint64_t* d_keys, const float* src, int64_t n,
   if (n == 0) return MLKV_OK;
   if (d_keys == nullptr || src == nullptr) return fail(MLKV_EINVAL, "keys or rows is NULL");
   if (t->dedup == kDedupRadix && n > kRsMaxKeys) return fail(MLKV_EINVAL, "radix dedup takes at most 2^20 keys");
-  if ((rc = ensure_workspace(t, n, static_cast<hipStream_t>(hip_stream))) != MLKV_OK) return rc;
+  return MLKV_OK;
+}
+
+// The launch arguments of a put of n > 0 keys with the table's epoch.
+PutArgs put_args(mlkv_table* t, const uint64_t* d_keys, const float* src, int64_t n, int op, float lr, float eps) {
   const uint32_t pb = call_part_bits(n, t->cus);
   // keys per put_probe tile: a multiple of 64, at most kPutTile, so that the
   // tiles cover every CU when the batch is small
@@ -697,6 +729,18 @@ int put_call(mlkv_table* t, const uint64_t* d_keys, const float* src, int64_t n,
   a.rs_bits = t->rs_bits;
   a.rs_buf = t->spill;  // two n-item buffers (the spill area holds 4n words; radix puts never spill)
   a.rs_cnt = t->rs_cnt;
+  return a;
+}
+
+// The put pipeline (probe, group, apply) with update `op` for every distinct
+// key; `src` holds n rows of gradients (or values for kOpAssign).
+int put_call(mlkv_table* t, const uint64_t* d_keys, const float* src, int64_t n, int op, float lr, float eps,
+             void* hip_stream) {
+  int rc = check_table(t);
+  if (rc) return rc;
+  if ((rc = check_put(t, d_keys, src, n, op, lr, eps)) != MLKV_OK || n == 0) return rc;
+  if ((rc = ensure_workspace(t, n, static_cast<hipStream_t>(hip_stream))) != MLKV_OK) return rc;
+  const PutArgs a = put_args(t, d_keys, src, n, op, lr, eps);
   const bool vec4 = (t->dim % 4 == 0) && aligned16(src);
   hipError_t e = launch_put(a, vec4, static_cast<hipStream_t>(hip_stream), hook_of(t));
   if (e != hipSuccess) return hip_fail(e, "put launch");
@@ -716,6 +760,47 @@ int mlkv_put_grad(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, i
 int mlkv_put_grad_sgd(mlkv_table* t, const uint64_t* d_keys, const float* d_grads, int64_t n, float lr,
                       void* hip_stream) {
   return put_call(t, d_keys, d_grads, n, kOpSgd, lr, 0.0f, hip_stream);
+}
+
+int mlkv_get_put_grad(mlkv_table* t, const uint64_t* d_get_keys, int64_t n_get, float* d_out, uint8_t* d_blocked,
+                      const uint64_t* d_put_keys, const float* d_grads, int64_t n_put, float lr, float eps,
+                      void* get_done_event, void* hip_stream) {
+  int rc = check_table(t);
+  if (rc) return rc;
+  if ((rc = check_get(t, d_get_keys, n_get, d_blocked, true)) != MLKV_OK) return rc;
+  if ((rc = check_put(t, d_put_keys, d_grads, n_put, kOpAdagrad, lr, eps)) != MLKV_OK) return rc;
+  hipStream_t st = static_cast<hipStream_t>(hip_stream);
+  hipEvent_t done = static_cast<hipEvent_t>(get_done_event);
+  hipError_t e = hipSuccess;
+  if (n_put == 0) {
+    if ((rc = get_call(t, d_get_keys, n_get, d_out, d_blocked, true, hip_stream)) != MLKV_OK) return rc;
+    if (done != nullptr && (e = hipEventRecord(done, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    return MLKV_OK;
+  }
+  if (n_get == 0) {
+    if (done != nullptr && (e = hipEventRecord(done, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    return put_call(t, d_put_keys, d_grads, n_put, kOpAdagrad, lr, eps, hip_stream);
+  }
+  if ((rc = ensure_workspace(t, std::max(n_get, n_put), st)) != MLKV_OK) return rc;
+  // the get takes this epoch, the put the next; the put's probe kernel runs
+  // first (it reads the rows the last get recorded), then the get's kernels,
+  // then the put's row updates
+  PutArgs p = put_args(t, d_put_keys, d_grads, n_put, kOpAdagrad, lr, eps);
+  p.epoch = t->epoch + 1;
+  p.ahead = 1;
+  GetArgs g = get_args(t, d_get_keys, n_get, d_out, d_blocked, true, nullptr);
+  g.xkey = t->mid_xkey;
+  g.xslot = t->mid_xslot;
+  const bool pvec4 = (t->dim % 4 == 0) && aligned16(d_grads);
+  const LaunchHook hook = hook_of(t);
+  e = launch_put(p, pvec4, st, hook, kPutProbe);
+  if (e == hipSuccess) e = launch_get(g, get_vec4(t, d_out), st, hook);
+  if (e == hipSuccess && done != nullptr) e = hipEventRecord(done, st);
+  if (e == hipSuccess) e = launch_put(p, pvec4, st, hook, kPutAfterProbe);
+  if (e != hipSuccess) return hip_fail(e, "mlkv_get_put_grad launch");
+  get_done(t, true, false);
+  t->epoch++;  // the put
+  return MLKV_OK;
 }
 
 int mlkv_set_dedup(mlkv_table* t, int mode) {
@@ -751,6 +836,8 @@ int mlkv_sync(mlkv_table* t, void* hip_stream) {
     const int zero = 0;
     e = hipMemcpy(&t->ctrl->latched, &zero, sizeof(int), hipMemcpyHostToDevice);
     if (e != hipSuccess) return hip_fail(e, "clear error latch");
+    if (latched == kErrAbsent)
+      return fail(MLKV_EINVAL, "the put of mlkv_get_put_grad held a key absent from the table before the call");
     return fail(latched, latched == MLKV_EFULL ? "a call exceeded the table capacity"
                                                : "a call contained the reserved key");
   }

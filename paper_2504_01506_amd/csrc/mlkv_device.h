@@ -73,6 +73,12 @@ struct Ctrl {
   unsigned long long overflow_epoch;  // epoch of a call whose inserts overran the probe bound
   unsigned long long spill_next;      // bump allocator for partitions larger than LDS
   unsigned long long new_epoch;       // epoch of a call that inserted at least one key
+  // a put whose probe kernel runs ahead of a get's kernels (and its other
+  // kernels after them) marks its own errors here, so that the get does not
+  // overwrite them: the epoch of such a put that met the reserved key, and of
+  // one that met a key absent from the table before the pair of calls
+  unsigned long long apput_bad_epoch;
+  unsigned long long apput_absent_epoch;
   int latched;                        // first device-side error since mlkv_sync
   unsigned int pad[7];
   // tiered tables: rows a lookahead call claimed as misses (ping-pong on the

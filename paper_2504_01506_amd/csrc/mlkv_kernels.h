@@ -31,6 +31,10 @@ constexpr int kRedHash = 4096;   // LDS hash slots for that grouping (load <= 0.
 constexpr int kPartTarget = 1024; // put keys per partition the partition count aims for
 constexpr int kPresumMin = 2;    // a key repeated this often in a put_probe tile is summed there
 
+// Error code a kernel latches when a put whose probe ran ahead of a get met a
+// key that was not in the table before the two calls (reported as MLKV_EINVAL).
+constexpr int kErrAbsent = -5;
+
 // Kernels of the library, for per-launch timing.
 enum KernelId : int {
   K_GET_PROBE_GATHER = 0,
@@ -142,7 +146,17 @@ struct PutArgs {
   int rs_bits;                // radix dedup: bits of the sort key (rows below capacity, new keys' slots above)
   uint64_t* rs_buf;           // radix dedup: two n-item ping-pong buffers
   uint32_t* rs_cnt;           // radix dedup: per-tile digit counts, then the item total
+  // 1: the put's probe kernel runs ahead of the kernels of a get whose epoch
+  // is this one's less one, its other kernels after them (the probe inserts
+  // nothing: a key absent from the table before that get fails the put; it
+  // writes no new-key list or tile counts, which are the get's, and marks its
+  // errors in the control block's fields for such puts)
+  int ahead = 0;
 };
+
+// Which kernels of a put launch_put queues: all of them, only the probe
+// kernel, or the kernels after it.
+enum PutPhase : int { kPutAll = 0, kPutProbe = 1, kPutAfterProbe = 2 };
 
 // Lookahead of a tiered table, after the get kernels have resolved its n keys.
 struct TierArgs {
@@ -169,7 +183,7 @@ struct TierArgs {
 
 hipError_t launch_get(const GetArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook);
 hipError_t launch_tier_lookahead(const TierArgs& a, hipStream_t st, const LaunchHook& hook);
-hipError_t launch_put(const PutArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook);
+hipError_t launch_put(const PutArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook, int phase = kPutAll);
 hipError_t launch_lookup(Bucket* idx, uint32_t nb_log2, const uint64_t* keys, int64_t n,
                          int64_t* rows_out, hipStream_t st);
 hipError_t launch_export_slots(const Bucket* idx, uint64_t nslots, uint64_t* keys_out,

@@ -265,9 +265,11 @@ __device__ __forceinline__ uint64_t count_new_keys(const uint32_t* __restrict__ 
 
 // Decides whether the call fails, and publishes the size for the next call.
 __device__ __forceinline__ int call_verdict(Ctrl* ctrl, uint64_t epoch, uint64_t size0, uint64_t M,
-                                            int64_t capacity, uint64_t bad_epoch, uint64_t overflow_epoch) {
+                                            int64_t capacity, uint64_t bad_epoch, uint64_t overflow_epoch,
+                                            uint64_t absent_epoch = 0) {
   int err = 0;
   if (bad_epoch == epoch) err = -1;                                           // MLKV_EINVAL
+  else if (absent_epoch == epoch) err = kErrAbsent;                          // MLKV_EINVAL, its own message
   else if (overflow_epoch == epoch || size0 + M > (uint64_t)capacity) err = -2;  // MLKV_EFULL
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     ctrl->size[(epoch + 1) & 1] = err ? size0 : size0 + M;
@@ -792,7 +794,10 @@ __device__ __forceinline__ uint32_t group_partition(uint64_t group, int pb) {
 // ---------------------------------------------------------------------------
 constexpr int kTileHash = 2 * kPutTile;  // LDS hash slots per tile
 
-template <class M>
+// kAhead: the put's probe runs ahead of the kernels of the get whose epoch is
+// one less, its other kernels after them (PutArgs::ahead): it looks keys up
+// without inserting, and a key absent from the table fails the put.
+template <class M, bool kAhead>
 __global__ __launch_bounds__(kPutThreads) void k_put_probe(
     Bucket* __restrict__ idx, uint32_t nb_log2, const uint64_t* __restrict__ keys,
     const float* __restrict__ grads, int64_t n, int tlen, int D, int op, int pb, int ntiles,
@@ -1044,16 +1049,26 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
 
   // probe (and insert) each key now that its bucket has arrived
   Probe pr[KPT];
+  // ahead of a get: the size word that get starts from (it writes the other)
+  const uint64_t size_before = kAhead ? ctrl->size[(epoch + 1) & 1] : 0ull;
 #pragma unroll
   for (int kk = 0; kk < KPT; ++kk) {
     pr[kk] = {0, kPendingRow, inb[kk] ? P_BAD : P_NONE};
     if (cached[kk]) {
       pr[kk] = {0, crow[kk], P_HIT};
     } else if (key[kk] != kEmptyKey) {
-      pr[kk] = probe_with(idx, nb_log2, key[kk], true, hb[kk], bv[kk]);
-      if (pr[kk].status == P_OVERFLOW) ctrl->overflow_epoch = epoch;
+      pr[kk] = probe_with(idx, nb_log2, key[kk], !kAhead, hb[kk], bv[kk]);
+      if constexpr (kAhead) {
+        if (pr[kk].status != P_HIT || pr[kk].row >= size_before) {
+          pr[kk].status = P_ABSENT;
+          ctrl->apput_absent_epoch = epoch;
+        }
+      } else {
+        if (pr[kk].status == P_OVERFLOW) ctrl->overflow_epoch = epoch;
+      }
     } else if (pr[kk].status == P_BAD) {
-      ctrl->bad_epoch = epoch;
+      if constexpr (kAhead) ctrl->apput_bad_epoch = epoch;
+      else ctrl->bad_epoch = epoch;
     }
   }
   uint64_t x[KPT];
@@ -1126,7 +1141,7 @@ __global__ __launch_bounds__(kPutThreads) void k_put_probe(
       dst[0] = merged[kk] && op != kOpAssign ? (x[kk] | kItemSummed) : x[kk];
     }
   }
-  if (tid == 0) tile_cnt[tile] = s_cnt;
+  if (!kAhead && tid == 0) tile_cnt[tile] = s_cnt;  // ahead of a get, the counts are the get's
   // keys summed in chunks: add the chunks' partial sums in order
   if (op != kOpAssign && chunked) {
     __syncthreads();
@@ -2243,7 +2258,9 @@ __global__ __launch_bounds__(NT) void k_put_reduce(
   const uint32_t p = blockIdx.x;
   const int tid = threadIdx.x;
   const uint64_t size0 = ctrl->size[epoch & 1];
-  const uint64_t new_e = ctrl->new_epoch, bad_e = ctrl->bad_epoch, ovf_e = ctrl->overflow_epoch;
+  const uint64_t new_e = ctrl->new_epoch, ovf_e = ctrl->overflow_epoch;
+  const uint64_t bad_e = ctrl->apput_bad_epoch == epoch ? epoch : ctrl->bad_epoch;
+  const uint64_t abs_e = ctrl->apput_absent_epoch;
   const uint32_t* pm = meta + (size_t)p * ntiles;
   const bool one_chunk = ntiles <= NT;  // common case: one thread per tile
   const uint32_t mt0 = one_chunk && tid < ntiles ? pm[tid] : 0u;
@@ -2259,7 +2276,7 @@ __global__ __launch_bounds__(NT) void k_put_reduce(
   }
 
   const uint64_t Mnew = new_e == epoch ? count_new_keys<NT>(tile_cnt, ntiles, s_w64) : 0ull;
-  const int err = call_verdict(ctrl, epoch, size0, Mnew, capacity, bad_e, ovf_e);
+  const int err = call_verdict(ctrl, epoch, size0, Mnew, capacity, bad_e, ovf_e, abs_e);
   if (mp == 0) return;
   if (err) {
     if (Mnew == 0) return;
@@ -2605,9 +2622,10 @@ __global__ __launch_bounds__(NT) void k_rsort_reduce(
   static_assert(kRedHash >= kRedCap + 1, "run starts fit the hash region");
 
   const uint64_t size0 = ctrl->size[epoch & 1];
-  const uint64_t new_e = ctrl->new_epoch, bad_e = ctrl->bad_epoch, ovf_e = ctrl->overflow_epoch;
+  const uint64_t new_e = ctrl->new_epoch, ovf_e = ctrl->overflow_epoch;
+  const uint64_t bad_e = ctrl->apput_bad_epoch == epoch ? epoch : ctrl->bad_epoch;
   const uint64_t Mnew = new_e == epoch ? count_new_keys<NT>(tile_cnt, ntiles, s_w64) : 0ull;
-  const int err = call_verdict(ctrl, epoch, size0, Mnew, capacity, bad_e, ovf_e);
+  const int err = call_verdict(ctrl, epoch, size0, Mnew, capacity, bad_e, ovf_e, ctrl->apput_absent_epoch);
   const uint32_t T = *total;
   const uint32_t nb = gridDim.x, b = blockIdx.x;
   const uint32_t lo = rs_cut<NT>(sorted, T, (uint32_t)((uint64_t)T * b / nb), s_info + 4);
@@ -2759,18 +2777,27 @@ static hipError_t rsort_lds_attr() {
 
 // Put with radix dedup: put_probe (one partition), the radix passes, the
 // reduce over the sorted items.
+// The probe kernel of a put, with 2^pb partitions.
 template <class M>
-static hipError_t launch_put_radix(const PutArgs& a, hipStream_t st, const LaunchHook& hook) {
+static hipError_t launch_put_probe(const PutArgs& a, int pb, hipStream_t st, const LaunchHook& hook) {
+  const int64_t ntiles = (a.n + a.tlen - 1) / a.tlen;
+  auto kern = a.ahead ? k_put_probe<M, true> : k_put_probe<M, false>;
+  hook(K_PUT_PROBE, 0, st);
+  hipLaunchKernelGGL(kern, dim3((unsigned)ntiles), dim3(kPutThreads), 0, st, a.idx, a.nb_log2, a.keys, a.grads,
+                     a.n, a.tlen, a.D, a.op, pb, (int)ntiles, a.items, a.meta, a.partials, a.newlist, a.tile_cnt,
+                     a.ctrl, a.epoch, a.pc_key, a.pc_row);
+  hook(K_PUT_PROBE, 1, st);
+  return hipGetLastError();
+}
+
+template <class M>
+static hipError_t launch_put_radix(const PutArgs& a, hipStream_t st, const LaunchHook& hook, int phase) {
   constexpr int NT = ReduceCfg<M>::NT;
   using L = ReduceLds<NT>;
   const int64_t ntiles = (a.n + a.tlen - 1) / a.tlen;
-  hook(K_PUT_PROBE, 0, st);
-  hipLaunchKernelGGL(k_put_probe<M>, dim3((unsigned)ntiles), dim3(kPutThreads), 0, st, a.idx, a.nb_log2,
-                     a.keys, a.grads, a.n, a.tlen, a.D, a.op, 0, (int)ntiles, a.items, a.meta, a.partials,
-                     a.newlist, a.tile_cnt, a.ctrl, a.epoch, a.pc_key, a.pc_row);
-  hook(K_PUT_PROBE, 1, st);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  hipError_t e = hipSuccess;
+  if (phase != kPutAfterProbe && (e = launch_put_probe<M>(a, 0, st, hook)) != hipSuccess) return e;
+  if (phase == kPutProbe) return hipSuccess;
   // passes of at most kRsMaxBits bits (at least 4: a sort key spans at least 4 bits)
   const int passes = (a.rs_bits + kRsMaxBits - 1) / kRsMaxBits;
   const int bits = (a.rs_bits + passes - 1) / passes;
@@ -2811,7 +2838,7 @@ static hipError_t launch_put_radix(const PutArgs& a, hipStream_t st, const Launc
 }
 
 template <class M>
-static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHook& hook) {
+static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHook& hook, int phase) {
   constexpr int NT = ReduceCfg<M>::NT;
   using L = ReduceLds<NT>;
   static_assert((size_t)ReduceCfg<M>::NG * ReduceCfg<M>::DMAX * sizeof(double) <= L::reuse,
@@ -2819,16 +2846,12 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   static_assert((size_t)(kChunk + NT) * sizeof(uint64_t) + (size_t)(NT + 1) * sizeof(uint32_t) <= L::reuse,
                 "new-key chunk, sorted new keys and their counts must fit the reused LDS region");
   static_assert(L::total <= 160 * 1024, "LDS budget of a gfx950 workgroup");
-  if (a.dedup == kDedupRadix) return launch_put_radix<M>(a, st, hook);
+  if (a.dedup == kDedupRadix) return launch_put_radix<M>(a, st, hook, phase);
   const int64_t ntiles = (a.n + a.tlen - 1) / a.tlen;
   const int np = 1 << a.pb;
-  hook(K_PUT_PROBE, 0, st);
-  hipLaunchKernelGGL(k_put_probe<M>, dim3((unsigned)ntiles), dim3(kPutThreads), 0, st, a.idx, a.nb_log2,
-                     a.keys, a.grads, a.n, a.tlen, a.D, a.op, a.pb, (int)ntiles, a.items, a.meta, a.partials,
-                     a.newlist, a.tile_cnt, a.ctrl, a.epoch, a.pc_key, a.pc_row);
-  hook(K_PUT_PROBE, 1, st);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  hipError_t e = hipSuccess;
+  if (phase != kPutAfterProbe && (e = launch_put_probe<M>(a, a.pb, st, hook)) != hipSuccess) return e;
+  if (phase == kPutProbe) return hipSuccess;
   const bool clk = a.clock != nullptr;  // a bounded table: puts lower the staleness counts
   if ((e = clk ? reduce_lds_attr<M, true>() : reduce_lds_attr<M, false>()) != hipSuccess) return e;
   auto kern = clk ? k_put_reduce<M, NT, true> : k_put_reduce<M, NT, false>;
@@ -2867,8 +2890,8 @@ hipError_t launch_get(const GetArgs& a, bool vec4, hipStream_t st, const LaunchH
   return dispatch_map(a.D, vec4, [&](auto m) { return launch_get_t<decltype(m)>(a, st, hook); });
 }
 
-hipError_t launch_put(const PutArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook) {
-  return dispatch_map(a.D, vec4, [&](auto m) { return launch_put_t<decltype(m)>(a, st, hook); });
+hipError_t launch_put(const PutArgs& a, bool vec4, hipStream_t st, const LaunchHook& hook, int phase) {
+  return dispatch_map(a.D, vec4, [&](auto m) { return launch_put_t<decltype(m)>(a, st, hook, phase); });
 }
 
 hipError_t launch_lookup(Bucket* idx, uint32_t nb_log2, const uint64_t* keys, int64_t n, int64_t* rows_out,

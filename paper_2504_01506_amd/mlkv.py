@@ -56,6 +56,7 @@ def load() -> ctypes.CDLL:
         "mlkv_read_staleness": (INT, [P, P, I64, P, P]),
         "mlkv_put_grad": (INT, [P, P, P, I64, F32, F32, P]),
         "mlkv_put_grad_sgd": (INT, [P, P, P, I64, F32, P]),
+        "mlkv_get_put_grad": (INT, [P, P, I64, P, P, P, P, I64, F32, F32, P, P]),
         "mlkv_put": (INT, [P, P, P, I64, P]),
         "mlkv_sync": (INT, [P, P]),
         "mlkv_size": (I64, [P]),
@@ -172,6 +173,17 @@ def mlkv_read_staleness(t: int, rows, n: int, out, stream=None) -> int:
 
 def mlkv_put_grad(t: int, keys, grads, n: int, lr: float, eps: float, stream=None) -> int:
     return load().mlkv_put_grad(t, _ptr(keys), _ptr(grads), n, lr, eps, _stream(stream))
+
+
+def mlkv_get_put_grad(t: int, get_keys, n_get: int, out, blocked, put_keys, grads, n_put: int, lr: float,
+                      eps: float, get_done=None, stream=None) -> int:
+    ev = None
+    if get_done is not None:  # a torch.cuda.Event: its hipEvent_t exists once it has been recorded
+        if not get_done.cuda_event:
+            get_done.record()
+        ev = get_done.cuda_event
+    return load().mlkv_get_put_grad(t, _ptr(get_keys), n_get, _ptr(out), _ptr(blocked), _ptr(put_keys),
+                                    _ptr(grads), n_put, lr, eps, ev, _stream(stream))
 
 
 def mlkv_put_grad_sgd(t: int, keys, grads, n: int, lr: float, stream=None) -> int:
@@ -307,6 +319,19 @@ class Table:
 
     def put_grad(self, keys: torch.Tensor, grads: torch.Tensor, lr: float, eps: float, stream=None):
         _check(mlkv_put_grad(self.h, keys, grads, keys.numel(), lr, eps, stream))
+
+    def get_put_grad(self, get_keys: torch.Tensor, out: torch.Tensor | None, put_keys: torch.Tensor,
+                     grads: torch.Tensor, lr: float, eps: float, blocked: torch.Tensor | None = None,
+                     get_done: torch.cuda.Event | None = None, stream=None):
+        """The get of get_keys, then put_grad of put_keys, in one call (every put
+        key must be in the table before the call); get_done, if given, is
+        recorded once the rows are in `out`. Returns the blocked flags on a
+        table with a staleness bound, else None."""
+        if blocked is None and self.staleness_bound is not None:
+            blocked = torch.empty(get_keys.numel(), dtype=torch.uint8, device=get_keys.device)
+        _check(mlkv_get_put_grad(self.h, get_keys, get_keys.numel(), out, blocked, put_keys, grads,
+                                 put_keys.numel(), lr, eps, get_done, stream))
+        return blocked
 
     def put_grad_sgd(self, keys: torch.Tensor, grads: torch.Tensor, lr: float, stream=None):
         _check(mlkv_put_grad_sgd(self.h, keys, grads, keys.numel(), lr, stream))

@@ -190,6 +190,33 @@ class Pair:
         assert self.gpu.sync() == mlkv.MLKV_OK
         self.updated[self.ora.lookup_rows(keys)] = True
 
+    def get_put_grad(self, get_keys: np.ndarray, put_keys: np.ndarray, grads: np.ndarray, lr: float, eps: float):
+        """The get of get_keys overlapped with put_grad of put_keys on the GPU;
+        the oracle takes the get, then the put. Output rows and blocked flags
+        are compared as in get() / get_bounded(). Returns the blocked flags
+        (None on a table without a bound)."""
+        sentinel = np.float32(-7.25)
+        out = torch.full((get_keys.size, self.dim), float(sentinel), dtype=torch.float32, device="cuda")
+        bl_d = self.gpu.get_put_grad(dev_keys(get_keys), out, dev_keys(put_keys), dev(grads), lr, eps)
+        bounded = self.gpu.staleness_bound is not None
+        if bounded:
+            rc, want, bl = self.ora.get_bounded(get_keys)
+        else:
+            (rc, want), bl = self.ora.get(get_keys), np.zeros(get_keys.size, np.uint8)
+        assert rc == O.OK
+        assert self.ora.put_grad(put_keys, grads, lr, eps) == O.OK
+        assert self.gpu.sync() == mlkv.MLKV_OK
+        got = out.cpu().numpy()
+        if bounded:
+            got_bl = bl_d.cpu().numpy()
+            assert np.array_equal(got_bl, bl), f"blocked flags differ at {int(np.sum(got_bl != bl))} positions"
+        served = bl == 0
+        if served.any():
+            self.compare_get(get_keys[served], got[served], want[served])
+        assert np.all(got[~served] == sentinel), "a blocked position was written"
+        self.updated[self.ora.lookup_rows(put_keys)] = True
+        return bl if bounded else None
+
     def put_sgd(self, keys: np.ndarray, grads: np.ndarray, lr: float):
         self.gpu.put_grad_sgd(dev_keys(keys), dev(grads), lr)
         assert self.ora.put_grad_sgd(keys, grads, lr) == O.OK

@@ -41,3 +41,10 @@ def test_radix_dedup_moves_the_reduce_bytes_to_its_reduce_kernel():
     kv_h = bench.kernel_bytes_kv(1 << 19, 400_000, 1 << 19, 400_000, 4)
     kv_r = bench.kernel_bytes_kv(1 << 19, 400_000, 1 << 19, 400_000, 4, "radix")
     assert sum(kv_h.values()) == sum(kv_r.values()) and kv_r["rsort_reduce"] == kv_h["put_reduce"]
+
+
+def test_pipelined_steps_are_refused_at_bound_zero_and_for_the_key_value_mix():
+    for extra in (("--staleness-bound", "0"), ("--config", "kv-zipf")):
+        r = _run("--pipelined", *extra)
+        assert r.returncode == 2
+        assert "--pipelined" in r.stderr
