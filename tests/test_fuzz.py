@@ -4,7 +4,8 @@ Each sequence draws a row width, a capacity, optionally a staleness bound
 or (tiered tables) an HBM cache of 2-20 % of the rows, the dedup of its puts
 (hash partition, or radix sort), and 30 calls, each one of: get (with or without an output), lookahead, put_grad,
 put_grad_sgd, put (upsert), a get whose new keys overflow the capacity, or a
-call holding the reserved key. Batch lengths cover the tile boundaries
+call holding the reserved key; some sequences also draw mlkv_get_put_grad
+calls (a get with a put_grad of keys already in the table). Batch lengths cover the tile boundaries
 (1, 63..65, 255..257, 1023..1025) and random lengths; keys mix present keys,
 duplicates and new keys. After every call: the return codes agree (failures
 leave both tables unchanged), sizes agree, key -> row of the call's keys is
@@ -46,8 +47,9 @@ def _ora_get(pr, keys):
     return pr.ora.get_bounded(keys)[0]
 
 
-def _sequence(seed, tiered, dedup="hash"):
-    rng = np.random.default_rng(5000 + seed + (1000 if tiered else 0) + (2000 if dedup != "hash" else 0))
+def _sequence(seed, tiered, dedup="hash", pipe=False):
+    rng = np.random.default_rng(5000 + seed + (1000 if tiered else 0) + (2000 if dedup != "hash" else 0)
+                                + (3000 if pipe else 0))
     dim = int(rng.choice([1, 2, 4, 5, 8, 16, 31, 64, 128]))
     cap = int(rng.integers(3000, 40000))
     bound = int(rng.integers(0, 3)) if seed % 3 == 2 and not tiered else None
@@ -57,7 +59,7 @@ def _sequence(seed, tiered, dedup="hash"):
     counts = {}
     for step in range(30):
         op = str(rng.choice(["get", "get", "get_null", "lookahead", "put_grad", "put_grad", "put_sgd", "put",
-                             "over", "bad"]))
+                             "over", "bad"] + (["pipe", "pipe", "pipe"] if pipe else [])))
         n = int(rng.choice(LENGTHS)) if rng.random() < 0.6 else int(rng.integers(1, 20000))
         if tiered and op == "lookahead":  # large enough to fill the cache and evict
             n = int(rng.integers(max(1, cache // 2), min(20000, 3 * cache) + 1))
@@ -103,6 +105,13 @@ def _sequence(seed, tiered, dedup="hash"):
             assert pr.gpu.sync() == mlkv.MLKV_OK
         elif op == "put_grad":
             pr.put(keys, rng.normal(0, 0.01, size=(n, dim)).astype(np.float32), 0.01, 1e-8)
+        elif op == "pipe":
+            if size == 0:
+                continue
+            m = int(rng.choice(LENGTHS)) if rng.random() < 0.5 else int(rng.integers(1, 20000))
+            put_keys = pr.ora.row_keys(rng.integers(0, size, size=m).astype(np.int64))
+            pr.get_put_grad(keys, put_keys, rng.normal(0, 0.01, size=(m, dim)).astype(np.float32), 0.01, 1e-8)
+            pr.compare_rows(np.unique(pr.ora.lookup_rows(put_keys)))
         elif op == "put_sgd":
             pr.put_sgd(keys, rng.normal(0, 0.01, size=(n, dim)).astype(np.float32), 0.05)
         else:
@@ -136,3 +145,8 @@ def test_random_call_sequences_on_tiered_tables(seed):
 @pytest.mark.parametrize("seed", range(6))
 def test_random_call_sequences_with_radix_dedup(seed):
     _sequence(seed, tiered=seed % 2 == 1, dedup="radix")
+
+
+@pytest.mark.parametrize("seed", range(9))
+def test_random_call_sequences_with_pipelined_calls(seed):
+    _sequence(seed, tiered=seed % 3 == 1, pipe=True)
