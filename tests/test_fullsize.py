@@ -77,6 +77,34 @@ def test_full_size_dlrm_all_100_steps():
     pr.close()
 
 
+@pytest.mark.parametrize("bound", [None, 1])
+def test_full_size_dlrm_pipelined(bound):
+    """The DLRM-shaped workload in the calls `bench.py --pipelined` times: the
+    get of batch s and the put_grad of batch s - 1 in one mlkv_get_put_grad
+    call (the oracle takes the get, then the put), unbounded and at
+    staleness bound 1; every output and the rows each put updated compared."""
+    wl = W.make("dlrm", scale=1.0)
+    pr = Pair(wl.dim, wl.capacity, staleness_bound=bound)
+    pr.prefill(wl.prefill_keys())
+    rng = np.random.default_rng(101)
+    prev = wl.keys(0)
+    if bound is None:
+        pr.get(prev)
+    else:
+        assert not pr.get_bounded(prev).any()
+    for s in range(1, 4):
+        keys = wl.keys(s)
+        bl = pr.get_put_grad(keys, prev, wl.grads(s - 1), wl.lr, wl.eps)
+        assert bl is None or not bl.any()
+        check_step(pr, prev, rng, n_sample=5000)
+        log(f"[full] dlrm pipelined bound {bound} step {s}: ok, stats={pr.stats}")
+        prev = keys
+    if bound is not None:
+        pr.compare_staleness()
+    record(f"full-dlrm-pipelined-bound{bound}", pr.stats)
+    pr.close()
+
+
 def test_full_size_ragged_batch_and_repeat():
     """DLRM-sized table, a batch whose length is not a multiple of any tile,
     then the same keys again (all present)."""
