@@ -77,13 +77,13 @@ def test_full_size_dlrm_all_100_steps():
     pr.close()
 
 
-@pytest.mark.parametrize("bound", [None, 1])
-def test_full_size_dlrm_pipelined(bound):
-    """The DLRM-shaped workload in the calls `bench.py --pipelined` times: the
-    get of batch s and the put_grad of batch s - 1 in one mlkv_get_put_grad
-    call (the oracle takes the get, then the put), unbounded and at
-    staleness bound 1; every output and the rows each put updated compared."""
-    wl = W.make("dlrm", scale=1.0)
+@pytest.mark.parametrize("name,bound", [("dlrm", None), ("dlrm", 1), ("kg", None), ("gnn", None)])
+def test_full_size_pipelined(name, bound):
+    """A workload in the calls `bench.py --pipelined` times: the get of batch
+    s and the put_grad of batch s - 1 in one mlkv_get_put_grad call (the
+    oracle takes the get, then the put), unbounded and (DLRM) at staleness
+    bound 1; every output and the rows each put updated compared."""
+    wl = W.make(name, scale=1.0)
     pr = Pair(wl.dim, wl.capacity, staleness_bound=bound)
     pr.prefill(wl.prefill_keys())
     rng = np.random.default_rng(101)
@@ -92,16 +92,16 @@ def test_full_size_dlrm_pipelined(bound):
         pr.get(prev)
     else:
         assert not pr.get_bounded(prev).any()
-    for s in range(1, 4):
+    for s in range(1, STEPS[name] + 1):
         keys = wl.keys(s)
         bl = pr.get_put_grad(keys, prev, wl.grads(s - 1), wl.lr, wl.eps)
         assert bl is None or not bl.any()
         check_step(pr, prev, rng, n_sample=5000)
-        log(f"[full] dlrm pipelined bound {bound} step {s}: ok, stats={pr.stats}")
+        log(f"[full] {name} pipelined bound {bound} step {s}: ok, stats={pr.stats}")
         prev = keys
     if bound is not None:
         pr.compare_staleness()
-    record(f"full-dlrm-pipelined-bound{bound}", pr.stats)
+    record(f"full-{name}-pipelined-bound{bound}", pr.stats)
     pr.close()
 
 
