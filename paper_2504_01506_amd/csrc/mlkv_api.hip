@@ -75,6 +75,14 @@ struct mlkv_table {
   // (mlkv_get_put_grad), apart from the put's items and metadata
   uint64_t* mid_xkey = nullptr;
   uint32_t* mid_xslot = nullptr;
+  // new keys of a get filed by key range (RangeLists): the lists, the counts
+  // of two consecutive calls (ping-pong on rl_calls) then the number of
+  // ranges of the cut points, and the cut points
+  NewKey* rl_list = nullptr;
+  uint64_t rl_entries = 0;
+  uint32_t* rl_cnt = nullptr;
+  uint64_t* rl_cuts = nullptr;
+  uint64_t rl_calls = 0;
   std::vector<ScratchSet> retired;  // replaced scratch, freed at sync / reserve / close
   int cus = 256;  // compute units of the device
 
@@ -118,7 +126,7 @@ void free_scratch_set(const ScratchSet& s) {
 ScratchSet current_set(mlkv_table* t) {
   ScratchSet s;
   s.ptrs = {t->newlist, t->tile_cnt, t->items, t->meta, t->spill, t->partials, t->pc_key, t->pc_row,
-            t->rs_cnt, t->miss, t->plan_slot, t->mid_xkey, t->mid_xslot};
+            t->rs_cnt, t->miss, t->plan_slot, t->mid_xkey, t->mid_xslot, t->rl_list, t->rl_cnt, t->rl_cuts};
   return s;
 }
 
@@ -129,6 +137,10 @@ void clear_workspace_ptrs(mlkv_table* t) {
   t->pc_row = nullptr;
   t->mid_xkey = nullptr;
   t->mid_xslot = nullptr;
+  t->rl_list = nullptr;
+  t->rl_cnt = nullptr;
+  t->rl_cuts = nullptr;
+  t->rl_entries = 0;
   t->partials = nullptr;
   t->newlist = nullptr;
   t->tile_cnt = nullptr;
@@ -207,6 +219,7 @@ int ensure_workspace(mlkv_table* t, int64_t n, hipStream_t st) {
   const int64_t put_tiles = std::max<int64_t>(want / kPutTile, t->cus + 1);
   const int64_t slots = std::max<int64_t>(want, put_tiles * kPutTile);
   const uint64_t spill_words = 4ull * (uint64_t)want + 4096;
+  const uint64_t rl_entries = 2ull * (uint64_t)want + 64ull * kMaxRanges;
   if ((e = dev_alloc(&t->newlist, sizeof(NewKey) * ((size_t)slots + kGetTile))) != hipSuccess ||
       (e = dev_alloc(&t->tile_cnt, sizeof(uint32_t) * (size_t)get_tiles)) != hipSuccess ||
       (e = dev_alloc(&t->items, sizeof(uint64_t) * (size_t)slots)) != hipSuccess ||
@@ -220,6 +233,11 @@ int ensure_workspace(mlkv_table* t, int64_t n, hipStream_t st) {
       (e = dev_alloc(&t->pc_row, sizeof(uint32_t) * (size_t)slots)) != hipSuccess ||
       (e = dev_alloc(&t->mid_xkey, sizeof(uint64_t) * (size_t)slots)) != hipSuccess ||
       (e = dev_alloc(&t->mid_xslot, sizeof(uint32_t) * (size_t)slots)) != hipSuccess ||
+      // range lists: twice the keys in all, so that a range may hold twice its share
+      (e = dev_alloc(&t->rl_list, sizeof(NewKey) * rl_entries)) != hipSuccess ||
+      (e = dev_alloc(&t->rl_cnt, sizeof(uint32_t) * (2 * kMaxRanges + 1))) != hipSuccess ||
+      (e = dev_alloc(&t->rl_cuts, sizeof(uint64_t) * kMaxRanges)) != hipSuccess ||
+      (e = hipMemsetAsync(t->rl_cnt, 0, sizeof(uint32_t) * (2 * kMaxRanges + 1), st)) != hipSuccess ||
       (e = hipMemsetAsync(t->pc_key, 0xFF, sizeof(uint64_t) * (size_t)slots, st)) != hipSuccess) {  // no key cached
     free_workspace(t);
     return hip_fail(e, "scratch allocation");
@@ -232,6 +250,7 @@ int ensure_workspace(mlkv_table* t, int64_t n, hipStream_t st) {
   }
   t->ws_n = want;
   t->spill_words = spill_words;
+  t->rl_entries = rl_entries;
   return MLKV_OK;
 }
 
@@ -512,6 +531,15 @@ GetArgs get_args(mlkv_table* t, const uint64_t* d_keys, int64_t n, float* d_out,
   // after a lookahead, the positions of its keys skip the probe (tables
   // without a staleness bound)
   a.pc_in = (!fixed && t->pc_lookahead && a.clock == nullptr) ? 1 : 0;
+  if (!fixed) {
+    const uint32_t par = (uint32_t)(t->rl_calls & 1u);
+    a.rl.list = t->rl_list;
+    a.rl.entries = t->rl_entries;
+    a.rl.cnt = t->rl_cnt + par * kMaxRanges;
+    a.rl.cnt_next = t->rl_cnt + (par ^ 1u) * kMaxRanges;
+    a.rl.cuts = t->rl_cuts;
+    a.rl.cuts_g = t->rl_cnt + 2 * kMaxRanges;
+  }
   a.cus = t->cus;
   return a;
 }
@@ -522,7 +550,10 @@ bool get_vec4(const mlkv_table* t, const float* d_out) {
 
 // The table's state after a get call was queued.
 void get_done(mlkv_table* t, bool count, bool fixed) {
-  if (!fixed) t->pc_lookahead = !count;  // a lookahead is the one get call that counts nothing
+  if (!fixed) {
+    t->pc_lookahead = !count;  // a lookahead is the one get call that counts nothing
+    t->rl_calls++;             // the range counts it used are cleared for the call after next
+  }
   t->epoch++;
   if (count && t->clock != nullptr) t->cepoch++;
 }

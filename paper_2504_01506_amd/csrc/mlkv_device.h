@@ -79,6 +79,10 @@ struct Ctrl {
   // one that met a key absent from the table before the pair of calls
   unsigned long long apput_bad_epoch;
   unsigned long long apput_absent_epoch;
+  // a get whose probe kernel filed its new keys in range lists (see
+  // RangeLists), and one whose lists overflowed
+  unsigned long long rl_epoch;
+  unsigned long long rl_overflow_epoch;
   int latched;                        // first device-side error since mlkv_sync
   unsigned int pad[7];
   // tiered tables: rows a lookahead call claimed as misses (ping-pong on the

@@ -77,6 +77,24 @@ struct LaunchHook {
   }
 };
 
+// A get call's new keys filed by key range as the probe kernel inserts them,
+// with the cut points the last ranking by key ranges left (the keys of
+// global ranks floor(j M / G), j = 1 .. G - 1, of a call that inserted M keys
+// with G ranges): range q holds the keys in [cut q-1, cut q). Row assignment
+// then takes each range's keys from its list instead of searching every
+// tile's list. The cut points serve a call with the same G; any sorted set of
+// them is correct, the last call's keep the ranges about even.
+constexpr int kMaxRanges = 256;  // ranges of a get call at most (its row-assignment blocks)
+struct RangeLists {
+  NewKey* list = nullptr;      // [entries]: range q's keys from q * cap on; nullptr: no lists
+  uint64_t entries = 0;
+  uint32_t cap = 0;            // entries per range (set at launch: entries / ranges)
+  uint32_t* cnt = nullptr;     // [kMaxRanges] this call's counts per range (zero before it)
+  uint32_t* cnt_next = nullptr;  // [kMaxRanges] the next call's counts, cleared by this call
+  uint64_t* cuts = nullptr;    // [kMaxRanges - 1] the cut points
+  uint32_t* cuts_g = nullptr;  // the number of ranges the cut points are for (0: none)
+};
+
 struct GetArgs {
   Bucket* idx;
   uint32_t nb_log2;
@@ -110,6 +128,7 @@ struct GetArgs {
   // (a present key's row never changes, so any recorded pair stays true);
   // not with a staleness clock
   int pc_in;
+  RangeLists rl;
   int cus;  // compute units of the device
 };
 

@@ -116,10 +116,12 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
     float* __restrict__ out, const RowStore store, int D, uint64_t seed,
     NewKey* __restrict__ newlist, uint32_t* __restrict__ tile_cnt, Ctrl* ctrl, uint64_t epoch,
     unsigned long long* __restrict__ clock, uint64_t cepoch, uint32_t bound, uint8_t* __restrict__ blocked,
-    uint64_t* __restrict__ pc_key, uint32_t* __restrict__ pc_row, int tlen) {
+    uint64_t* __restrict__ pc_key, uint32_t* __restrict__ pc_row, int tlen, const RangeLists rl,
+    uint32_t nranges) {
   __shared__ uint32_t s_cnt;
   __shared__ uint64_t s_nkey[kGetTile];  // the tile's new keys and their slots
   __shared__ uint32_t s_nslot[kGetTile];
+  __shared__ uint64_t s_cuts[kMaxRanges - 1];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -200,6 +202,22 @@ __global__ __launch_bounds__(kGetTile) void k_get_probe_gather(
     newlist[base + r] = NewKey{k, s_nslot[tid], 0u};
   }
   if (tid == 0) tile_cnt[blockIdx.x] = c;
+  // the same keys filed by key range, when the cut points are for this
+  // call's number of ranges (block-uniform: c and the cut count)
+  if (rl.list != nullptr && c > 0 && *rl.cuts_g == nranges) {
+    for (uint32_t e = tid; e + 1 < nranges; e += kGetTile) s_cuts[e] = rl.cuts[e];
+    __syncthreads();
+    if ((uint32_t)tid < c) {
+      const uint64_t k = s_nkey[tid];
+      uint32_t q = 0;  // range q holds [cut q-1, cut q): q = cut points <= k
+      for (uint32_t step = kMaxRanges / 2; step >= 1; step >>= 1)
+        if (q + step < nranges && s_cuts[q + step - 1] <= k) q += step;
+      const uint32_t at = atomicAdd(&rl.cnt[q], 1u);
+      if (at < rl.cap) rl.list[(size_t)q * rl.cap + at] = NewKey{k, s_nslot[tid], 0u};
+      else ctrl->rl_overflow_epoch = epoch;
+    }
+    if (tid == 0) ctrl->rl_epoch = epoch;
+  }
 }
 
 // ===========================================================================
@@ -283,6 +301,7 @@ __device__ __forceinline__ int call_verdict(Ctrl* ctrl, uint64_t epoch, uint64_t
 // write their initial rows and zero accumulators; or roll the call back.
 // ===========================================================================
 constexpr int kAssignThreads = 256;
+static_assert(kMaxRanges <= kAssignThreads, "a block reads every range count with one thread each");
 constexpr int kAssignBatch = 8;
 constexpr int kAssignMine = kAssignBatch * kAssignThreads;
 // With few new keys each block ranks its tiles' keys against all of them,
@@ -450,7 +469,7 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
     Bucket* __restrict__ idx, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
     int ntiles, int tile_size, const RowStore store, float* __restrict__ state, int D,
     uint64_t seed, int64_t capacity, Ctrl* ctrl, uint64_t epoch, uint64_t* __restrict__ xkey,
-    uint32_t* __restrict__ xslot, unsigned long long* __restrict__ clock, uint64_t cepoch) {
+    uint32_t* __restrict__ xslot, unsigned long long* __restrict__ clock, uint64_t cepoch, const RangeLists rl) {
   constexpr int NT = kAssignThreads;
   __shared__ unsigned long long s_w64[NT / 64];
   __shared__ uint32_t s_w[NT / 64];
@@ -462,6 +481,9 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
   static_assert(kRangeCap * 14 <= (int)sizeof(s_buf) && kRangeSamples * 12 <= (int)sizeof(s_buf), "LDS");
   static_assert(kRangeSamples == NT * kSortPT && kRangeCap <= 65536, "sample and range sizes");
 
+  // the next call's range counts start at zero (this call's are read below)
+  if (rl.list != nullptr && blockIdx.x == 0)
+    for (int e = threadIdx.x; e < kMaxRanges; e += NT) rl.cnt_next[e] = 0u;
   const uint64_t size0 = ctrl->size[epoch & 1];
   const bool any_new = ctrl->new_epoch == epoch;
   const uint64_t M = any_new ? count_new_keys<NT>(tile_cnt, ntiles, s_w64) : 0ull;
@@ -481,75 +503,103 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
   }
 
   if (M * (uint64_t)((ntiles + NT - 1) / NT) > kAssignDirectWork) {
-    // ---- many new keys: key ranges. Every block takes the same sample of the
-    // new keys (sample k is the new key at position floor(k M / S) of the
-    // tiles' lists laid end to end) and the same cut points from it, which
-    // give block g the keys in [lo, hi). A binary search of both bounds in
-    // every tile's sorted list of new keys counts the keys below lo, the
-    // block's first rank, and finds the block's own, which are then ranked
-    // among themselves. No block waits for another.
-    constexpr uint32_t S = kRangeSamples;
-    uint32_t* s_sat = reinterpret_cast<uint32_t*>(s_buf + S);     // [S] offsets of the samples in the lists
-    {
-      const int tpt = (ntiles + NT - 1) / NT;  // consecutive tiles per thread
-      const int tb = min(ntiles, (int)threadIdx.x * tpt), te = min(ntiles, tb + tpt);
-      uint32_t mine = 0;
-      for (int t = tb; t < te; ++t) mine += tile_cnt[t];
-      uint32_t tot;
-      uint64_t pre = block_exclusive_scan<NT>(mine, s_w, &tot);
-      uint64_t k = (pre * S + M - 1) / M;  // first sample at or after pre
-      for (int t = tb; t < te && k < S; ++t) {
-        const uint32_t c = tile_cnt[t];
-        for (; k < S; ++k) {
-          const uint64_t gk = k * M / S;
-          if (gk >= pre + c) break;
-          s_sat[k] = (uint32_t)t * (uint32_t)tile_size + (uint32_t)(gk - pre);
-        }
-        pre += c;
-      }
-    }
-    __syncthreads();
-    uint64_t v[kSortPT];
-#pragma unroll
-    for (uint32_t u = 0; u < kSortPT; ++u) v[u] = newlist[s_sat[threadIdx.x + u * NT]].key;
-    // the cut points: the samples of rank g S / G and (g + 1) S / G of the
-    // sorted sample (with fewer new keys than samples a key is sampled more
-    // than once, and equal cut points give an empty range); eight sample
-    // gaps per range keep the largest range near twice the mean
+    // ---- many new keys: key ranges. Block g ranks the new keys of the g-th
+    // key range among themselves, after the count of new keys below the
+    // range. The probe kernel has filed the keys by range when cut points for
+    // this many ranges were left (RangeLists): the range's keys are its list,
+    // the keys below it the lists before. Otherwise every block takes the
+    // same sample of the new keys (sample k is the new key at position
+    // floor(k M / S) of the tiles' lists laid end to end) and the same cut
+    // points from it, which give block g the keys in [lo, hi); a binary
+    // search of both bounds in every tile's sorted list of new keys counts
+    // the keys below lo and finds the block's own. No block waits for another.
     const uint32_t g = blockIdx.x, G = gridDim.x;
-    sort_keys_8pt<NT>(v, s_buf, s_buf + S);
-    {
-      const uint32_t r1 = (uint32_t)((uint64_t)g * S / G), r2 = (uint32_t)((uint64_t)(g + 1) * S / G);
-#pragma unroll
-      for (uint32_t u = 0; u < kSortPT; ++u) {
-        if (threadIdx.x * kSortPT + u == r1) s_cut[0] = v[u];
-        if (threadIdx.x * kSortPT + u == r2) s_cut[1] = v[u];
-      }
-      if (threadIdx.x == 0) s_nc = 0;
-    }
-    __syncthreads();
-    const uint64_t lo = g == 0 ? 0ull : s_cut[0];
-    const uint64_t hi = g + 1 == G ? kEmptyKey : s_cut[1];
-    // keys in [lo, hi) first go to LDS: key, slot (later the rank), and
-    // their order by local sub-range
     uint64_t* s_key = s_buf;                                                 // [kRangeCap]
     uint32_t* s_sr = reinterpret_cast<uint32_t*>(s_buf + kRangeCap);        // [kRangeCap]
     uint16_t* s_ord = reinterpret_cast<uint16_t*>(s_sr + kRangeCap);        // [kRangeCap]
-    uint64_t below = search_tile_lists<NT>(newlist, tile_cnt, ntiles, tile_size, lo, hi,
-                                           [&](uint32_t off, uint32_t cnt) {
-                                             const uint32_t at = atomicAdd(&s_nc, cnt);
-                                             for (uint32_t e = 0; e < cnt && at + e < (uint32_t)kRangeCap; ++e) {
-                                               s_key[at + e] = newlist[off + e].key;
-                                               s_sr[at + e] = off + e;  // slot and position are read later
-                                             }
-                                           });
-    below = block_sum_u64<NT>(below, s_w64);  // its barriers also publish s_nc and the gathered keys
-    const uint32_t c = s_nc;
-    const uint64_t base = size0 + below;
-    if (c <= (uint32_t)kRangeCap) {
-      // the slot of each gathered key, from its list entry
-      for (uint32_t j = threadIdx.x; j < c; j += NT) s_sr[j] = newlist[s_sr[j]].slot;
+    const bool listed = rl.list != nullptr && ctrl->rl_epoch == epoch && ctrl->rl_overflow_epoch != epoch;
+    const NewKey* my_list = listed ? rl.list + (size_t)g * rl.cap : nullptr;
+    uint64_t below = 0, lo = 0, hi = kEmptyKey;
+    uint32_t c = 0;
+    if (listed) {
+      below = block_sum_u64<NT>(threadIdx.x < g ? rl.cnt[threadIdx.x] : 0u, s_w64);
+      c = rl.cnt[g];
+      if (c <= (uint32_t)kRangeCap)
+        for (uint32_t j = threadIdx.x; j < c; j += NT) {
+          const NewKey nk = my_list[j];
+          s_key[j] = nk.key;
+          s_sr[j] = nk.slot;
+        }
       __syncthreads();
+    } else {
+      constexpr uint32_t S = kRangeSamples;
+      uint32_t* s_sat = reinterpret_cast<uint32_t*>(s_buf + S);     // [S] offsets of the samples in the lists
+      {
+        const int tpt = (ntiles + NT - 1) / NT;  // consecutive tiles per thread
+        const int tb = min(ntiles, (int)threadIdx.x * tpt), te = min(ntiles, tb + tpt);
+        uint32_t mine = 0;
+        for (int t = tb; t < te; ++t) mine += tile_cnt[t];
+        uint32_t tot;
+        uint64_t pre = block_exclusive_scan<NT>(mine, s_w, &tot);
+        uint64_t k = (pre * S + M - 1) / M;  // first sample at or after pre
+        for (int t = tb; t < te && k < S; ++t) {
+          const uint32_t c = tile_cnt[t];
+          for (; k < S; ++k) {
+            const uint64_t gk = k * M / S;
+            if (gk >= pre + c) break;
+            s_sat[k] = (uint32_t)t * (uint32_t)tile_size + (uint32_t)(gk - pre);
+          }
+          pre += c;
+        }
+      }
+      __syncthreads();
+      uint64_t v[kSortPT];
+  #pragma unroll
+      for (uint32_t u = 0; u < kSortPT; ++u) v[u] = newlist[s_sat[threadIdx.x + u * NT]].key;
+      // the cut points: the samples of rank g S / G and (g + 1) S / G of the
+      // sorted sample (with fewer new keys than samples a key is sampled more
+      // than once, and equal cut points give an empty range); eight sample
+      // gaps per range keep the largest range near twice the mean
+      sort_keys_8pt<NT>(v, s_buf, s_buf + S);
+      {
+        const uint32_t r1 = (uint32_t)((uint64_t)g * S / G), r2 = (uint32_t)((uint64_t)(g + 1) * S / G);
+  #pragma unroll
+        for (uint32_t u = 0; u < kSortPT; ++u) {
+          if (threadIdx.x * kSortPT + u == r1) s_cut[0] = v[u];
+          if (threadIdx.x * kSortPT + u == r2) s_cut[1] = v[u];
+        }
+        if (threadIdx.x == 0) s_nc = 0;
+      }
+      __syncthreads();
+      lo = g == 0 ? 0ull : s_cut[0];
+      hi = g + 1 == G ? kEmptyKey : s_cut[1];
+      // keys in [lo, hi) first go to LDS: key, slot (later the rank), and
+      // their order by local sub-range
+      below = search_tile_lists<NT>(newlist, tile_cnt, ntiles, tile_size, lo, hi, [&](uint32_t off, uint32_t cnt) {
+        const uint32_t at = atomicAdd(&s_nc, cnt);
+        for (uint32_t e = 0; e < cnt && at + e < (uint32_t)kRangeCap; ++e) {
+          s_key[at + e] = newlist[off + e].key;
+          s_sr[at + e] = off + e;  // slot and position are read later
+        }
+      });
+      below = block_sum_u64<NT>(below, s_w64);  // its barriers also publish s_nc and the gathered keys
+      c = s_nc;
+      if (c <= (uint32_t)kRangeCap) {
+        // the slot of each gathered key, from its list entry
+        for (uint32_t j = threadIdx.x; j < c; j += NT) s_sr[j] = newlist[s_sr[j]].slot;
+      }
+      __syncthreads();
+    }
+    const uint64_t base = size0 + below;
+    // cut points for the next call: cut j is the key of global rank
+    // floor(j M / G), so the keys of rank R give cuts j in [ceil(R G / M),
+    // ceil((R + 1) G / M))
+    auto leave_cuts = [&](uint64_t key, uint64_t R) {
+      if (rl.list == nullptr) return;
+      const uint64_t jb = (R * G + M - 1) / M, je = ((R + 1) * G + M - 1) / M;
+      for (uint64_t j = jb < 1 ? 1 : jb; j < je && j < G; ++j) rl.cuts[j - 1] = key;
+    };
+    if (c <= (uint32_t)kRangeCap) {
       // rank among the range's keys, through kSub local sub-ranges cut at a
       // sample of the gathered keys: sub-range counts and their prefix, the
       // keys listed by sub-range, then each key ranked inside its sub-range
@@ -627,6 +677,7 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
           idx[slot / kSlots].row[slot % kSlots] = (uint32_t)(base + r);
           state[base + r] = 0.0f;
           if (clock != nullptr) clock[base + r] = new_row_clock(cepoch);
+          leave_cuts(key, below + r);
         }
       }
       __syncthreads();
@@ -644,14 +695,22 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
       __syncthreads();
       if (threadIdx.x == 0) s_nc = 0;
       __syncthreads();
-      search_tile_lists<NT>(newlist, tile_cnt, ntiles, tile_size, lo, hi, [&](uint32_t off, uint32_t cnt) {
-        const uint32_t at = atomicAdd(&s_nc, cnt);
-        for (uint32_t e = 0; e < cnt; ++e) {
-          const NewKey nk = newlist[off + e];
-          xkey[below + at + e] = nk.key;
-          xslot[below + at + e] = nk.slot;
+      if (listed) {
+        for (uint32_t j = threadIdx.x; j < c; j += NT) {
+          const NewKey nk = my_list[j];
+          xkey[below + j] = nk.key;
+          xslot[below + j] = nk.slot;
         }
-      });
+      } else {
+        search_tile_lists<NT>(newlist, tile_cnt, ntiles, tile_size, lo, hi, [&](uint32_t off, uint32_t cnt) {
+          const uint32_t at = atomicAdd(&s_nc, cnt);
+          for (uint32_t e = 0; e < cnt; ++e) {
+            const NewKey nk = newlist[off + e];
+            xkey[below + at + e] = nk.key;
+            xslot[below + at + e] = nk.slot;
+          }
+        });
+      }
       __syncthreads();
       const uint64_t* rk_key = xkey + below;
       const uint32_t* rk_slot = xslot + below;
@@ -688,6 +747,7 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
             s_mk[j] = mk[u];
             s_ms[j] = rk_slot[j0 + j];
             s_mr[j] = r[u];
+            leave_cuts(mk[u], below + r[u]);
           }
         }
         __syncthreads();
@@ -695,6 +755,7 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
         __syncthreads();
       }
     }
+    if (rl.list != nullptr && g == 0 && threadIdx.x == 0) *rl.cuts_g = G;
     return;
   }
 
@@ -2727,20 +2788,22 @@ template <class M>
 static hipError_t launch_get_t(const GetArgs& a, hipStream_t st, const LaunchHook& hook) {
   const int tlen = get_tile_len(a.n, a.cus);
   const int64_t ntiles = (a.n + tlen - 1) / tlen;
+  const int grid = (int)std::min<int64_t>(ntiles, kMaxRanges);  // row assignment: one block per key range
+  RangeLists rl = a.rl;
+  if (rl.list != nullptr) rl.cap = (uint32_t)std::min<uint64_t>(rl.entries / (uint64_t)grid, 0xFFFFFFFFull);
   hook(K_GET_PROBE_GATHER, 0, st);
   auto kern = a.clock != nullptr ? k_get_probe_gather<M, true, false>
                                   : a.pc_in ? k_get_probe_gather<M, false, true> : k_get_probe_gather<M, false, false>;
   hipLaunchKernelGGL(kern, dim3((unsigned)ntiles), dim3(kGetTile), 0, st, a.idx, a.nb_log2, a.keys, a.n,
                      a.out, a.store, a.D, a.seed, a.newlist, a.tile_cnt, a.ctrl, a.epoch, a.clock, a.cepoch,
-                     a.bound, a.blocked, a.pc_key, a.pc_row, tlen);
+                     a.bound, a.blocked, a.pc_key, a.pc_row, tlen, rl, (uint32_t)grid);
   hook(K_GET_PROBE_GATHER, 1, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int grid = (int)std::min<int64_t>(ntiles, 256);
   hook(K_ASSIGN_NEW, 0, st);
   hipLaunchKernelGGL(k_assign_new, dim3(grid), dim3(kAssignThreads), 0, st, a.idx, a.newlist,
                      a.tile_cnt, (int)ntiles, tlen, a.store, a.state, a.D, a.seed, a.capacity,
-                     a.ctrl, a.epoch, a.xkey, a.xslot, a.clock, a.cepoch);
+                     a.ctrl, a.epoch, a.xkey, a.xslot, a.clock, a.cepoch, rl);
   hook(K_ASSIGN_NEW, 1, st);
   return hipGetLastError();
 }
@@ -2775,8 +2838,6 @@ static hipError_t rsort_lds_attr() {
   return lds_attr(reinterpret_cast<const void*>(&k_rsort_reduce<M, NT, kClk>), (int)ReduceLds<NT>::total, done);
 }
 
-// Put with radix dedup: put_probe (one partition), the radix passes, the
-// reduce over the sorted items.
 // The probe kernel of a put, with 2^pb partitions.
 template <class M>
 static hipError_t launch_put_probe(const PutArgs& a, int pb, hipStream_t st, const LaunchHook& hook) {
@@ -2790,6 +2851,8 @@ static hipError_t launch_put_probe(const PutArgs& a, int pb, hipStream_t st, con
   return hipGetLastError();
 }
 
+// Put with radix dedup: put_probe (one partition), the radix passes, the
+// reduce over the sorted items.
 template <class M>
 static hipError_t launch_put_radix(const PutArgs& a, hipStream_t st, const LaunchHook& hook, int phase) {
   constexpr int NT = ReduceCfg<M>::NT;
