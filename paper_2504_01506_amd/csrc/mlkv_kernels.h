@@ -84,7 +84,7 @@ struct LaunchHook {
 // then takes each range's keys from its list instead of searching every
 // tile's list. The cut points serve a call with the same G; any sorted set of
 // them is correct, the last call's keep the ranges about even.
-constexpr int kMaxRanges = 256;  // ranges of a get call at most (its row-assignment blocks)
+constexpr int kMaxRanges = 512;  // ranges of a get call at most (its row-assignment blocks, two per CU)
 struct RangeLists {
   NewKey* list = nullptr;      // [entries]: range q's keys from q * cap on; nullptr: no lists
   uint64_t entries = 0;

@@ -301,7 +301,6 @@ __device__ __forceinline__ int call_verdict(Ctrl* ctrl, uint64_t epoch, uint64_t
 // write their initial rows and zero accumulators; or roll the call back.
 // ===========================================================================
 constexpr int kAssignThreads = 256;
-static_assert(kMaxRanges <= kAssignThreads, "a block reads every range count with one thread each");
 constexpr int kAssignBatch = 8;
 constexpr int kAssignMine = kAssignBatch * kAssignThreads;
 // With few new keys each block ranks its tiles' keys against all of them,
@@ -522,7 +521,9 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
     uint64_t below = 0, lo = 0, hi = kEmptyKey;
     uint32_t c = 0;
     if (listed) {
-      below = block_sum_u64<NT>(threadIdx.x < g ? rl.cnt[threadIdx.x] : 0u, s_w64);
+      uint64_t mine = 0;
+      for (uint32_t r = threadIdx.x; r < g; r += NT) mine += rl.cnt[r];
+      below = block_sum_u64<NT>(mine, s_w64);
       c = rl.cnt[g];
       if (c <= (uint32_t)kRangeCap)
         for (uint32_t j = threadIdx.x; j < c; j += NT) {
