@@ -307,7 +307,9 @@ constexpr int kAssignMine = kAssignBatch * kAssignThreads;
 // streamed through LDS once per NT tiles of the call: about 13 us plus 44 ns
 // per (new key x NT tiles) on MI355X (55 us at 256 new keys of a 213k-key,
 // 832-tile batch; 1.4 ms at 8192), while key ranges take 44-50 us from a few
-// hundred keys up. The direct ranking is used up to kAssignDirectWork new
+// hundred keys up when each block must search every tile's list for its
+// range, and far less with range lists (those calls always take them). The
+// direct ranking is otherwise used up to kAssignDirectWork new
 // keys x tile chunks.
 constexpr uint64_t kAssignDirectWork = 768;
 constexpr int kRangeSamples = 2048;  // sample of the new keys that splits the key space among the blocks
@@ -501,7 +503,10 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
     return;
   }
 
-  if (M * (uint64_t)((ntiles + NT - 1) / NT) > kAssignDirectWork) {
+  // the probe kernel filed the new keys by range (RangeLists): ranking them
+  // by range then costs little for any number of them
+  const bool listed = rl.list != nullptr && ctrl->rl_epoch == epoch && ctrl->rl_overflow_epoch != epoch;
+  if (listed || M * (uint64_t)((ntiles + NT - 1) / NT) > kAssignDirectWork) {
     // ---- many new keys: key ranges. Block g ranks the new keys of the g-th
     // key range among themselves, after the count of new keys below the
     // range. The probe kernel has filed the keys by range when cut points for
@@ -516,7 +521,6 @@ __global__ __launch_bounds__(kAssignThreads) void k_assign_new(
     uint64_t* s_key = s_buf;                                                 // [kRangeCap]
     uint32_t* s_sr = reinterpret_cast<uint32_t*>(s_buf + kRangeCap);        // [kRangeCap]
     uint16_t* s_ord = reinterpret_cast<uint16_t*>(s_sr + kRangeCap);        // [kRangeCap]
-    const bool listed = rl.list != nullptr && ctrl->rl_epoch == epoch && ctrl->rl_overflow_epoch != epoch;
     const NewKey* my_list = listed ? rl.list + (size_t)g * rl.cap : nullptr;
     uint64_t below = 0, lo = 0, hi = kEmptyKey;
     uint32_t c = 0;
