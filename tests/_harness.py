@@ -191,7 +191,7 @@ class Pair:
         self.updated[self.ora.lookup_rows(keys)] = True
 
     def get_put_grad(self, get_keys: np.ndarray, put_keys: np.ndarray, grads: np.ndarray, lr: float, eps: float):
-        """The get of get_keys overlapped with put_grad of put_keys on the GPU;
+        """The get of get_keys, then put_grad of put_keys, in one GPU call;
         the oracle takes the get, then the put. Output rows and blocked flags
         are compared as in get() / get_bounded(). Returns the blocked flags
         (None on a table without a bound)."""
