@@ -67,6 +67,7 @@ def test_host_side_validation_without_a_gpu(lib):
     assert lib.mlkv_get_bounded(None, None, 10, None, None, None) == mlkv.MLKV_EINVAL
     assert lib.mlkv_read_staleness(None, None, 10, None, None) == mlkv.MLKV_EINVAL
     assert lib.mlkv_lookahead(None, None, 10, None) == mlkv.MLKV_EINVAL
+    assert lib.mlkv_get_put_grad(None, None, 10, None, None, None, None, 10, 0.1, 0.0, None, None) == mlkv.MLKV_EINVAL
     lib.mlkv_close(None)  # no-op
 
 

@@ -246,3 +246,34 @@ def test_work_waiting_for_the_get_done_event_sees_the_rows():
         cur = nxt
     pr.compare_rows()
     pr.close()
+
+
+def test_argument_checks_leave_the_table_alone():
+    # each refused call returns MLKV_EINVAL before queuing anything: the table
+    # answers the next call as if the refused ones had not been made
+    rng = np.random.default_rng(59)
+    dim = 16
+    pr = Pair(dim, 20_000, staleness_bound=1)
+    k = _keys(rng, 2000, 8000)
+    pr.get_bounded(k)
+    h = pr.gpu.h
+    kd, gd = dev_keys(k), dev(rng.normal(0, 0.01, size=(k.size, dim)).astype(np.float32))
+    out = torch.empty((k.size, dim), dtype=torch.float32, device="cuda")
+    bl = torch.empty(k.size, dtype=torch.uint8, device="cuda")
+    call = mlkv.mlkv_get_put_grad
+    assert call(h, kd, k.size, out, None, kd, gd, k.size, 0.01, 1e-8) == mlkv.MLKV_EINVAL  # no blocked flags
+    assert "blocked" in mlkv.mlkv_last_error()
+    assert call(h, kd, -1, out, bl, kd, gd, k.size, 0.01, 1e-8) == mlkv.MLKV_EINVAL
+    assert call(h, kd, k.size, out, bl, kd, gd, -1, 0.01, 1e-8) == mlkv.MLKV_EINVAL
+    assert call(h, kd, k.size, out, bl, kd, gd, k.size, float("nan"), 1e-8) == mlkv.MLKV_EINVAL
+    assert call(h, kd, k.size, out, bl, kd, gd, k.size, 0.01, -1.0) == mlkv.MLKV_EINVAL
+    assert call(h, kd, k.size, out, bl, kd, None, k.size, 0.01, 1e-8) == mlkv.MLKV_EINVAL
+    assert call(h, None, k.size, out, bl, kd, gd, k.size, 0.01, 1e-8) == mlkv.MLKV_EINVAL
+    assert pr.gpu.sync() == mlkv.MLKV_OK
+    # the same table goes on as the oracle does
+    nxt = _keys(rng, 1500, 8000)
+    bl2 = pr.get_put_grad(nxt, k, rng.normal(0, 0.01, size=(k.size, dim)).astype(np.float32), 0.01, 1e-8)
+    assert bl2 is not None
+    pr.compare_staleness()
+    pr.compare_rows()
+    pr.close()
