@@ -2204,6 +2204,83 @@ __device__ __forceinline__ void sum_and_update(const uint64_t* srt, const uint32
 
 // Put with the assignment op: each key's row becomes the value row at its
 // last position. Lane groups take even shares of the segments.
+// An upsert whose keys were all present before the call: each key's row
+// takes the value at the key's last position, so the partition needs no
+// grouping, only the largest position per row (an LDS hash table from row to
+// position + 1), then one write per row, lane groups taking equal shares of
+// the rows in slot order.
+constexpr uint32_t kNoRowKey = 0xFFFFFFFFu;  // an empty slot (no row has this id)
+template <class M, int NT, bool kClk>
+__device__ __forceinline__ void upsert_last(const uint64_t* __restrict__ it, uint32_t mp, const RedCtx& c,
+                                            uint32_t* s_row, uint32_t* s_last, uint16_t* s_list, uint32_t* s_w) {
+  static_assert(kRedHash == 4096 && kRedHash % NT == 0, "12-bit slot hash, whole slots per thread");
+  for (uint32_t h = threadIdx.x; h < (uint32_t)kRedHash; h += NT) {
+    s_row[h] = kNoRowKey;
+    s_last[h] = 0u;
+  }
+  __syncthreads();
+  for (uint32_t j = threadIdx.x; j < mp; j += NT) {
+    const uint64_t x = it[j];
+    const uint32_t row = item_tag(x);
+    uint32_t h = (row * 0x9E3779B1u) >> 20;
+    while (true) {
+      const uint32_t old = atomicCAS(&s_row[h], kNoRowKey, row);
+      if (old == kNoRowKey || old == row) break;
+      h = (h + 1) & (kRedHash - 1);
+    }
+    atomicMax(&s_last[h], item_pos(x) + 1u);
+  }
+  __syncthreads();
+  constexpr int PER = kRedHash / NT;
+  uint32_t occ = 0;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) occ += s_row[threadIdx.x * PER + e] != kNoRowKey ? 1u : 0u;
+  uint32_t S;
+  uint32_t at = block_exclusive_scan<NT>(occ, s_w, &S);
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const uint32_t h = threadIdx.x * PER + e;
+    if (s_row[h] != kNoRowKey) s_list[at++] = (uint16_t)h;
+  }
+  __syncthreads();
+  using Cfg = ReduceCfg<M>;
+  constexpr int VEC = M::VEC, LPR = M::LPR, K = M::K, NG = Cfg::NG, BS = Cfg::BS;
+  using V = typename VecT<VEC>::T;
+  const int lane = threadIdx.x & 63;
+  const int q = lane % LPR;
+  const int gid = (threadIdx.x >> 6) * M::RPW + lane / LPR;
+  const int D = c.D;
+  const uint32_t k0 = (uint32_t)((uint64_t)S * gid / NG), k1 = (uint32_t)((uint64_t)S * (gid + 1) / NG);
+  for (uint32_t s0 = k0; s0 < k1; s0 += BS) {
+    V v[BS][K];
+    uint32_t rw[BS], cl[BS];
+    const bool clk = kClk && q == 0;
+#pragma unroll
+    for (int u = 0; u < BS; ++u) {
+      const uint32_t sl = s0 + u;
+      rw[u] = 0;
+      cl[u] = 0u;
+      if (sl < k1) {
+        const uint32_t h = s_list[sl];
+        rw[u] = s_row[h];
+        const float* src = c.grads + (size_t)(s_last[h] - 1u) * (size_t)D;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const int col = (k * LPR + q) * VEC;
+          if (col < D) v[u][k] = load_vec<VEC>(src + col);
+        }
+        if (clk) cl[u] = clock_low(c.clock, rw[u]);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < BS; ++u) {
+      if (s0 + u >= k1) continue;
+      SegmentOps<M>::assign(v[u], c.store.wptr(rw[u]), D, q);
+      if (clk) put_clock_low(c.clock, rw[u], cl[u]);
+    }
+  }
+}
+
 template <class M, int NT, bool kClk>
 __device__ __forceinline__ void assign_segments(const uint64_t* srt, const uint32_t* seg, uint32_t S,
                                                 const RedCtx& c) {
@@ -2290,7 +2367,10 @@ __device__ __forceinline__ void reduce_partition_global(uint32_t p, uint32_t mp,
   update_segments<M, NT>(it, seg, S, c);
 }
 
-template <class M, int NT, bool kClk>
+// kUpsert: the instance for upserts (PutOp kOpAssign), whose partitions
+// without keys new in the call take the value at each key's last position
+// without grouping (upsert_last).
+template <class M, int NT, bool kClk, bool kUpsert>
 __global__ __launch_bounds__(NT) void k_put_reduce(
     Bucket* __restrict__ idx, const uint64_t* __restrict__ items, const uint32_t* __restrict__ meta,
     int ntiles, const NewKey* __restrict__ newlist, const uint32_t* __restrict__ tile_cnt,
@@ -2406,6 +2486,14 @@ __global__ __launch_bounds__(NT) void k_put_reduce(
     }
   }
 
+  if constexpr (kUpsert) {
+    uint32_t fresh = 0;
+    for (uint32_t j = tid; j < mp; j += NT) fresh |= item_fresh(s_it[j]) ? 1u : 0u;
+    if (__syncthreads_or((int)fresh) == 0) {
+      upsert_last<M, NT, kClk>(s_it, mp, c, s_hidx, s_hcnt, s_slot, s_w);
+      return;
+    }
+  }
   group_by_key<NT>(s_it, mp, s_srt, s_seg, s_sid, s_hidx, s_hcnt, s_inv, s_slot, s_ord, s_lid, s_mask, s_w64, s_info);
   const uint32_t S = s_info[0], SA = s_info[1], MA = s_info[2];
   if (s_info[3] != 0u)
@@ -2828,11 +2916,12 @@ static hipError_t lds_attr(const void* f, int bytes, bool (&done)[kMaxDev]) {
 
 // Whether the put_reduce instance of row map M may use its dynamic LDS on
 // each device (set once per device).
-template <class M, bool kClk>
+template <class M, bool kClk, bool kUpsert>
 static hipError_t reduce_lds_attr() {
   static bool done[64] = {};
   constexpr int NT = ReduceCfg<M>::NT;
-  return lds_attr(reinterpret_cast<const void*>(&k_put_reduce<M, NT, kClk>), (int)ReduceLds<NT>::total, done);
+  return lds_attr(reinterpret_cast<const void*>(&k_put_reduce<M, NT, kClk, kUpsert>), (int)ReduceLds<NT>::total,
+                  done);
 }
 
 // The same for the radix reduce instance of row map M.
@@ -2921,8 +3010,12 @@ static hipError_t launch_put_t(const PutArgs& a, hipStream_t st, const LaunchHoo
   if (phase != kPutAfterProbe && (e = launch_put_probe<M>(a, a.pb, st, hook)) != hipSuccess) return e;
   if (phase == kPutProbe) return hipSuccess;
   const bool clk = a.clock != nullptr;  // a bounded table: puts lower the staleness counts
-  if ((e = clk ? reduce_lds_attr<M, true>() : reduce_lds_attr<M, false>()) != hipSuccess) return e;
-  auto kern = clk ? k_put_reduce<M, NT, true> : k_put_reduce<M, NT, false>;
+  const bool ups = a.op == kOpAssign;
+  if ((e = clk ? (ups ? reduce_lds_attr<M, true, true>() : reduce_lds_attr<M, true, false>())
+               : (ups ? reduce_lds_attr<M, false, true>() : reduce_lds_attr<M, false, false>())) != hipSuccess)
+    return e;
+  auto kern = clk ? (ups ? k_put_reduce<M, NT, true, true> : k_put_reduce<M, NT, true, false>)
+                  : (ups ? k_put_reduce<M, NT, false, true> : k_put_reduce<M, NT, false, false>);
   hook(K_PUT_REDUCE, 0, st);
   hipLaunchKernelGGL(kern, dim3((unsigned)np), dim3(NT),
                      L::total, st, a.idx, a.items, a.meta, (int)ntiles, a.newlist, a.tile_cnt, a.grads, a.partials,

@@ -78,3 +78,31 @@ def test_full_size_dlrm_sgd_and_put():
     pr.get(keys)
     log(f"[full] dlrm sgd+put stats={pr.stats}")
     pr.close()
+
+
+@pytest.mark.parametrize("dim,bound", [(4, None), (64, None), (130, None), (16, 1)])
+def test_upsert_of_present_keys_takes_the_last_position_across_tiles(dim, bound):
+    # a put whose partitions hold no key new in the call writes each row from
+    # its key's last position without grouping; a call with a few new keys
+    # mixes such partitions with grouped ones. Zipf repeats put one key in
+    # many tiles, so the last position is found across tiles.
+    rng = np.random.default_rng(dim + 7)
+    nkeys, n = 40_000, 300_000
+    pr = Pair(dim, 60_000, staleness_bound=bound)
+    universe = np.arange(1, nkeys + 1, dtype=np.uint64) * np.uint64(0x9E3779B97F4A7C15)
+    pr.prefill(np.sort(universe))
+    ranks = np.minimum(rng.zipf(1.1, size=n), nkeys) - 1
+    keys = universe[ranks]
+    if bound is not None:
+        pr.get_bounded(keys)
+        assert pr.compare_staleness().any()
+    pr.upsert(keys, rng.normal(0, 1, size=(n, dim)).astype(np.float32))
+    if bound is not None:
+        assert not pr.compare_staleness().any()  # the put lowered the counts the get raised
+    keys = keys.copy()
+    keys[rng.choice(n, size=64, replace=False)] = np.arange(10**6, 10**6 + 64, dtype=np.uint64)
+    pr.upsert(keys, rng.normal(0, 1, size=(n, dim)).astype(np.float32))
+    pr.compare_rows()
+    pr.check_index()
+    log(f"[upsert] dim {dim} bound {bound} size {pr.ora.size}")
+    pr.close()
